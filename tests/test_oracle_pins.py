@@ -1,0 +1,437 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Each test checks an oracle function against something other than itself:
+library routines (torch conv2d / max_pool2d / bf16 cast), exact integer or
+rational arithmetic, brute-force loops, the telescoping identity of Eq. 2,
+the frozen output of an all-off gate (Eq. 3), and the closed-form response of
+an impulse residual. They are chosen so that a dropped term, a wrong sign, a
+wrong tap index or a transposed operand fails at least one of them.
+"""
+from fractions import Fraction
+import math
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+from oracle import skipconv_oracle as O
+
+pytestmark = pytest.mark.filterwarnings("ignore::RuntimeWarning")
+
+
+def _rng(seed):
+    return np.random.Generator(np.random.PCG64(seed))
+
+
+def torch_conv(x_nhwc, w, stride, pad, groups):
+    """Library cross-check of Eq. 1 (cross-correlation, as CNN frameworks define w * x)."""
+    x = torch.from_numpy(np.ascontiguousarray(x_nhwc, dtype=np.float64)).permute(0, 3, 1, 2)
+    wt = torch.from_numpy(np.asarray(w, dtype=np.float64))
+    z = F.conv2d(x, wt, stride=stride, padding=pad, groups=groups)
+    return z.permute(0, 2, 3, 1).numpy()
+
+
+def brute_update(rho, w, stride, pad, groups, sites):
+    """Seven nested loops: the convolution at the listed sites, term by term."""
+    n_, h, wd, c_in = rho.shape
+    c_out, cg, k, _ = w.shape
+    og = c_out // groups
+    out = np.zeros((len(sites), c_out))
+    for si, (n, i, j) in enumerate(sites):
+        for co in range(c_out):
+            gi = co // og
+            acc = 0.0
+            for kh in range(k):
+                for kw in range(k):
+                    y, x = i * stride - pad + kh, j * stride - pad + kw
+                    if 0 <= y < h and 0 <= x < wd:
+                        for cl in range(cg):
+                            acc += float(w[co, cl, kh, kw]) * float(rho[n, y, x, gi * cg + cl])
+            out[si, co] = acc
+    return out
+
+
+# ----------------------------------------------------------------------------
+# bf16 rounding
+# ----------------------------------------------------------------------------
+
+def test_bf16_rne_matches_torch_cast():
+    rng = _rng(1)
+    vals = [rng.normal(0, 1, 20000), rng.normal(0, 1e-38, 2000), rng.normal(0, 1e30, 2000)]
+    v = np.concatenate(vals).astype(np.float32)
+    # exact ties: low 16 bits = 0x8000 with an even and an odd kept bit
+    ties = np.array([0x3F808000, 0x3F818000, 0xBF808000, 0x00008000, 0x7F7F8000, 0x7F7FFFFF],
+                    dtype=np.uint32).view(np.float32)
+    special = np.array([0.0, -0.0, np.inf, -np.inf, 3.0e38, -3.4e38, 1e-45], dtype=np.float32)
+    v = np.concatenate([v, ties, special])
+    ours = O.f32_to_bf16_rne(v)
+    ref = torch.from_numpy(v).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(ours, ref)
+    nan = np.array([np.nan, -np.nan], dtype=np.float32)
+    assert np.isnan(O.bf16_bits_to_f32(O.f32_to_bf16_rne(nan))).all()
+
+
+def test_bf16_widen_exact():
+    bits = np.arange(0, 65536, dtype=np.uint32).astype(np.uint16)
+    f = O.bf16_bits_to_f32(bits)
+    ref = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(torch.float32).numpy()
+    fin = np.isfinite(ref)
+    assert np.array_equal(f[fin].view(np.uint32), ref[fin].view(np.uint32))
+    assert np.array_equal(np.isnan(f), np.isnan(ref))
+
+
+# ----------------------------------------------------------------------------
+# Gate statistic (Eq. 5)
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("p", [1, 2])
+def test_pixel_stat_integer_exact(p):
+    rng = _rng(2)
+    r = rng.integers(-9, 10, size=(2, 5, 6, 13)).astype(np.float32)
+    a = O.pixel_stat(r, p)
+    ri = r.astype(np.int64)
+    ref = (ri * ri).sum(-1) if p == 2 else np.abs(ri).sum(-1)
+    assert np.array_equal(a.astype(np.int64), ref)
+
+
+@pytest.mark.parametrize("k,stride", [(1, 1), (3, 1), (3, 2), (5, 1), (5, 2)])
+def test_support_stat_is_box_filter(k, stride):
+    """Integer-valued a: the support sum equals a library box filter with zero padding."""
+    rng = _rng(3)
+    a = rng.integers(0, 50, size=(2, 9, 11)).astype(np.float32)
+    pad = (k - 1) // 2
+    ho, wo = O.out_size(9, k, stride, pad), O.out_size(11, k, stride, pad)
+    s = O.support_stat(a, k, stride, pad, ho, wo, "rf")
+    box = F.conv2d(torch.from_numpy(a.astype(np.float64))[:, None], torch.ones(1, 1, k, k, dtype=torch.float64),
+                   stride=stride, padding=pad)[:, 0].numpy()
+    assert s.shape == box.shape
+    assert np.array_equal(s.astype(np.float64), box)
+
+
+def test_support_stat_centre_and_1x1():
+    rng = _rng(4)
+    a = rng.random((1, 8, 7), dtype=np.float32)
+    s1 = O.support_stat(a, 1, 1, 0, 8, 7, "rf")
+    assert np.array_equal(s1, a)
+    sc = O.support_stat(a, 3, 2, 1, 4, 4, "centre")
+    assert np.array_equal(sc, a[:, ::2, ::2])
+
+
+def test_statistic_within_rounding_bound_of_exact_rational():
+    """fp32 canonical statistic vs the exact rational sum of squares over the support."""
+    rng = _rng(5)
+    c, k = 6, 3
+    x1 = rng.random((1, 6, 6, c), dtype=np.float32)
+    x0 = (x1 + rng.normal(0, 0.05, x1.shape).astype(np.float32)).astype(np.float32)
+    r = O.residual(x1, x0)
+    s = O.support_stat(O.pixel_stat(r, 2), k, 1, 1, 6, 6)
+    u = 2.0 ** -24
+    nterms = c * k * k
+    gamma = (nterms + 2) * u / (1 - (nterms + 2) * u)
+    flips = 0
+    for i in range(6):
+        for j in range(6):
+            ex = Fraction(0)
+            for kh in range(k):
+                for kw in range(k):
+                    y, xx = i - 1 + kh, j - 1 + kw
+                    if 0 <= y < 6 and 0 <= xx < 6:
+                        for ch in range(c):
+                            v = Fraction(float(r[0, y, xx, ch]))
+                            ex += v * v
+            err = abs(Fraction(float(s[0, i, j])) - ex)
+            assert err <= Fraction(gamma) * ex
+            # the gate decision agrees with the exact one unless the threshold lies within the bound
+            for eps2 in (float(ex) * 0.999, float(ex) * 1.001, float(ex)):
+                eps = float(np.float32(math.sqrt(eps2)))
+                thr = Fraction(eps) * Fraction(eps)
+                g = O.gate(s[:, i:i + 1, j:j + 1], eps, 2, False)[0, 0, 0]
+                if abs(ex - thr) > Fraction(gamma) * ex:
+                    assert bool(g) == (ex > thr)
+                else:
+                    flips += 0 if bool(g) == (ex > thr) else 1
+    assert flips <= 36  # counted, only possible within one rounding bound of eps
+
+
+def test_residual_is_ieee_subtraction():
+    rng = _rng(6)
+    a = rng.random(1000, dtype=np.float32)
+    b = rng.random(1000, dtype=np.float32)
+    r = O.residual(a, b)
+    ref = (torch.from_numpy(a) - torch.from_numpy(b)).numpy()
+    assert np.array_equal(r.view(np.uint32), ref.view(np.uint32))
+
+
+# ----------------------------------------------------------------------------
+# Gate (Eq. 5) and blocks (structured sparsity)
+# ----------------------------------------------------------------------------
+
+def _nonzero_patch(r, k, stride, pad, ho, wo):
+    n, h, w, _ = r.shape
+    out = np.zeros((n, ho, wo), bool)
+    for b in range(n):
+        for i in range(ho):
+            for j in range(wo):
+                for kh in range(k):
+                    for kw in range(k):
+                        y, x = i * stride - pad + kh, j * stride - pad + kw
+                        if 0 <= y < h and 0 <= x < w and np.any(r[b, y, x] != 0):
+                            out[b, i, j] = True
+    return out
+
+
+@pytest.mark.parametrize("stride", [1, 2])
+def test_eps0_gate_is_nonzero_patch_indicator(stride):
+    rng = _rng(7)
+    r = rng.normal(0, 1, size=(2, 9, 8, 3)).astype(np.float32)
+    r[rng.random((2, 9, 8)) < 0.8] = 0.0
+    ho, wo = O.out_size(9, 3, stride, 1), O.out_size(8, 3, stride, 1)
+    for p in (1, 2):
+        s = O.support_stat(O.pixel_stat(r, p), 3, stride, 1, ho, wo)
+        g = O.gate(s, 0.0, p, False)
+        assert np.array_equal(g, _nonzero_patch(r, 3, stride, 1, ho, wo))
+
+
+def test_gate_eps_inf_empty_monotone_nan_and_reference():
+    rng = _rng(8)
+    s = (rng.random((2, 6, 6)) * 4).astype(np.float32)
+    s[0, 2, 3] = np.nan
+    off = O.gate(s, np.float32(np.inf), 2, False)
+    assert off.sum() == 1 and off[0, 2, 3]  # only the NaN site
+    prev = None
+    for eps in (0.0, 0.3, 0.7, 1.0, 1.5, 2.5):
+        g = O.gate(s, eps, 2, False)
+        if prev is not None:
+            assert not np.any(g & ~prev)
+        prev = g
+    assert O.gate(s, np.float32(np.inf), 2, True).all()
+    # strict comparison: a statistic equal to the threshold is off (round(sigmoid(0)) = 0)
+    t = np.array([[[0.25]]], dtype=np.float32)
+    assert not O.gate(t, 0.5, 2, False)[0, 0, 0]
+    assert not O.gate(t, 0.25, 1, False)[0, 0, 0]
+
+
+@pytest.mark.parametrize("b", [1, 2, 3, 4, 8])
+def test_block_pool_is_ceil_maxpool(b):
+    rng = _rng(9 + b)
+    g = rng.random((3, 13, 10)) < 0.1
+    m = O.block_pool(g, b)
+    ref = F.max_pool2d(torch.from_numpy(g.astype(np.float32))[:, None], b, b, ceil_mode=True)[:, 0]
+    assert np.array_equal(m, ref.numpy() > 0)
+    up = O.block_upsample(m, b, 13, 10)
+    assert not np.any(g & ~up)  # the block mask covers every gated site
+    lst = O.active_list(m)
+    brute = [n * m.shape[1] * m.shape[2] + i * m.shape[2] + j
+             for n in range(m.shape[0]) for i in range(m.shape[1]) for j in range(m.shape[2]) if m[n, i, j]]
+    assert lst.tolist() == brute
+
+
+# ----------------------------------------------------------------------------
+# Sparse update (Eq. 3)
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("k,stride,groups", [(1, 1, 1), (3, 1, 1), (3, 2, 1), (3, 1, 4), (1, 2, 2), (5, 1, 1)])
+def test_update_at_sites_bruteforce(k, stride, groups):
+    rng = _rng(10 + k * 7 + stride + groups)
+    c_in, c_out = 4, 8
+    rho = rng.normal(0, 1, (2, 7, 6, c_in))
+    w = rng.normal(0, 1, (c_out, c_in // groups, k, k))
+    pad = (k - 1) // 2
+    ho, wo = O.out_size(7, k, stride, pad), O.out_size(6, k, stride, pad)
+    sel = rng.random((2, ho, wo)) < 0.4
+    sn, si, sj = np.nonzero(sel)
+    u = O.conv_at_sites(rho, w, stride, pad, groups, sn, si, sj, chunk=5)
+    ref = brute_update(rho, w, stride, pad, groups, list(zip(sn, si, sj)))
+    np.testing.assert_allclose(u, ref, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("k,stride,groups", [(3, 1, 1), (3, 2, 1), (1, 1, 1), (3, 1, 6)])
+def test_reference_step_is_dense_conv(k, stride, groups):
+    rng = _rng(20 + k + stride + groups)
+    c = 6
+    x = rng.random((2, 10, 9, c), dtype=np.float32)
+    w = rng.normal(0, 1, (c, c // groups, k, k)).astype(np.float32)
+    lay = O.SkipConvOracle(w, n=2, h=10, w=9, stride=stride, groups=groups, eps=10.0, block=2)
+    out = lay.step(x)
+    ref = torch_conv(x, w, stride, (k - 1) // 2, groups)
+    np.testing.assert_allclose(out["z"], ref, rtol=1e-12, atol=1e-12)
+    assert out["count"] == out["block_mask"].size and out["reference"]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("block", [1, 3])
+def test_eps0_telescopes_to_dense_conv_integer_exact(dtype, block):
+    """Eq. 2 telescoping: with eps = 0 the accumulated output is w * x_T, bit for bit on integers."""
+    rng = _rng(30)
+    c = 5
+    w = rng.integers(-2, 3, (7, c, 3, 3)).astype(np.float32)
+    lay = O.SkipConvOracle(w, n=1, h=11, w=12, eps=0.0, block=block, dtype=dtype)
+    x = rng.integers(0, 8, (1, 11, 12, c)).astype(np.float32)
+    for t in range(6):
+        x = x.copy()
+        sel = rng.random((1, 11, 12)) < 0.15
+        x[sel] = rng.integers(0, 8, (int(sel.sum()), c))
+        xs = x if dtype == "f32" else O.f32_to_bf16_rne(x)
+        out = lay.step(xs)
+        assert np.array_equal(out["z"], torch_conv(x, w, 1, 1, 1))
+
+
+def test_eps0_telescopes_exact_residual_mode():
+    rng = _rng(31)
+    c = 4
+    w = rng.normal(0, 1, (6, c, 3, 3)).astype(np.float32)
+    lay = O.SkipConvOracle(w, n=1, h=9, w=10, stride=2, eps=0.0, exact_residual=True)
+    for t in range(5):
+        x = rng.random((1, 9, 10, c), dtype=np.float32)
+        x[:, :4] = 0.5  # part of the frame static
+        out = lay.step(x)
+    ref = torch_conv(x, w, 2, 1, 1)
+    assert np.max(np.abs(out["z"] - ref)) <= 1e-12 * max(1.0, np.max(np.abs(ref)))
+
+
+def test_all_gates_off_freezes_output_and_prev_advances():
+    rng = _rng(32)
+    c = 3
+    w = rng.normal(0, 1, (4, c, 3, 3)).astype(np.float32)
+    lay = O.SkipConvOracle(w, n=1, h=8, w=8, eps=np.float32(np.inf))
+    xs = [rng.random((1, 8, 8, c), dtype=np.float32) for _ in range(4)]
+    z1 = lay.step(xs[0])["z"]
+    for t in (1, 2):
+        out = lay.step(xs[t])
+        assert out["count"] == 0 and len(out["active"]) == 0
+        assert np.array_equal(out["z"], z1)
+    lay.eps = 0.0
+    out = lay.step(xs[3])
+    ref = z1 + torch_conv(xs[3].astype(np.float64) - xs[2].astype(np.float64), w, 1, 1, 1)
+    np.testing.assert_allclose(out["z"], ref, rtol=1e-6, atol=1e-6)
+
+
+def test_reset_mid_stream_gives_dense_frame():
+    rng = _rng(33)
+    c = 4
+    w = rng.normal(0, 1, (4, c, 3, 3)).astype(np.float32)
+    lay = O.SkipConvOracle(w, n=1, h=8, w=9, eps=0.5, block=2)
+    for _ in range(3):
+        lay.step(rng.random((1, 8, 9, c), dtype=np.float32))
+    lay.reset()
+    x = rng.random((1, 8, 9, c), dtype=np.float32)
+    out = lay.step(x)
+    assert out["reference"] and out["count"] == out["block_mask"].size
+    np.testing.assert_allclose(out["z"], torch_conv(x, w, 1, 1, 1), rtol=1e-12, atol=1e-12)
+
+
+def _load_golden(name):
+    import os
+    path = os.path.join(os.path.dirname(__file__), "golden", name)
+    rows = [ln for ln in open(path) if ln.strip() and not ln.startswith("#")]
+    return np.array([[float(v) for v in ln.split()] for ln in rows])
+
+
+def test_impulse_response_golden():
+    """One changed pixel: Eq. 3 updates exactly the outputs whose support holds it,
+    by the kernel read backwards (hand-derived fixture)."""
+    w = np.arange(1, 10, dtype=np.float32).reshape(1, 1, 3, 3)
+    lay = O.SkipConvOracle(w, n=1, h=5, w=5, eps=0.0)
+    x0 = np.zeros((1, 5, 5, 1), np.float32)
+    lay.step(x0)
+    x1 = x0.copy()
+    x1[0, 2, 2, 0] = 1.0
+    out = lay.step(x1)
+    expect = _load_golden("impulse_3x3_5x5.txt")
+    assert np.array_equal(out["z"][0, :, :, 0], expect)
+    assert np.array_equal(out["site_mask"][0], expect != 0)
+
+
+@pytest.mark.parametrize("k,stride,b", [(3, 1, 1), (3, 1, 2), (3, 2, 1), (5, 1, 3), (1, 1, 2)])
+def test_impulse_active_set_closed_form(k, stride, b):
+    rng = _rng(40 + k + stride + b)
+    h, w, c = 11, 10, 3
+    pad = (k - 1) // 2
+    wt = rng.normal(0, 1, (2, c, k, k)).astype(np.float32)
+    lay = O.SkipConvOracle(wt, n=1, h=h, w=w, stride=stride, eps=0.0, block=b)
+    x0 = rng.random((1, h, w, c), dtype=np.float32)
+    lay.step(x0)
+    qy, qx = 4, 7
+    x1 = x0.copy()
+    x1[0, qy, qx, 1] += np.float32(0.75)
+    out = lay.step(x1)
+    ho, wo = lay.h_out, lay.w_out
+    exp = np.zeros((1, ho, wo), bool)
+    for i in range(ho):
+        for j in range(wo):
+            if i * stride - pad <= qy <= i * stride - pad + k - 1 and j * stride - pad <= qx <= j * stride - pad + k - 1:
+                exp[0, i, j] = True
+    assert np.array_equal(out["site_mask"], exp)
+    blocks = {(i // b, j // b) for i, j in zip(*np.nonzero(exp[0]))}
+    hb = -(-ho // b)
+    wb = -(-wo // b)
+    assert sorted(out["active"].tolist()) == sorted(bi * wb + bj for bi, bj in blocks)
+    assert out["block_mask"].shape == (1, hb, wb)
+
+
+def test_nan_frame_gates_on_then_reset_recovers():
+    rng = _rng(50)
+    c = 3
+    w = rng.normal(0, 1, (4, c, 3, 3)).astype(np.float32)
+    lay = O.SkipConvOracle(w, n=1, h=8, w=8, eps=np.float32(1e6))
+    x = rng.random((1, 8, 8, c), dtype=np.float32)
+    lay.step(x)
+    xn = x.copy()
+    xn[0, 3, 5, 2] = np.nan
+    out = lay.step(xn)
+    exp = np.zeros((8, 8), bool)
+    exp[2:5, 4:7] = True
+    assert np.array_equal(out["site_mask"][0], exp)
+    assert np.array_equal(np.isnan(out["z"][0]).any(-1), exp)
+    lay.reset()
+    x3 = rng.random((1, 8, 8, c), dtype=np.float32)
+    out = lay.step(x3)
+    assert np.isfinite(out["z"]).all()
+    np.testing.assert_allclose(out["z"], torch_conv(x3, w, 1, 1, 1), rtol=1e-12, atol=1e-12)
+
+
+def test_stack_residual_zero_outside_upstream_active_set():
+    """Chained layers (Sec. 3.1): the next layer's input changes only where this layer updated."""
+    rng = _rng(60)
+    w1 = rng.normal(0, 0.5, (6, 3, 3, 3)).astype(np.float32)
+    l1 = O.SkipConvOracle(w1, n=1, h=16, w=16, eps=0.3, dtype="bf16")
+    y_prev = None
+    x = rng.random((1, 16, 16, 3), dtype=np.float32)
+    for t in range(5):
+        x = x.copy()
+        x[0, 3 + t:7 + t, 4:8] = rng.random((4, 4, 3), dtype=np.float32)
+        out = l1.step(O.f32_to_bf16_rne(x))
+        y = O.activation_to_storage(out["z"], "relu", "bf16")
+        if y_prev is not None:
+            changed = np.any(y != y_prev, axis=-1)
+            assert not np.any(changed & ~out["mask"])
+        y_prev = y
+
+
+def test_bf16_operand_rounding_applied():
+    """bf16 layers convolve bf16(r): an update equals the fp64 conv of the rounded residual."""
+    rng = _rng(61)
+    w = O.f32_to_bf16_rne(rng.normal(0, 1, (3, 2, 3, 3)).astype(np.float32))
+    lay = O.SkipConvOracle(w, n=1, h=6, w=6, eps=0.0, dtype="bf16")
+    x0 = O.f32_to_bf16_rne(rng.random((1, 6, 6, 2), dtype=np.float32))
+    x1 = O.f32_to_bf16_rne(rng.random((1, 6, 6, 2), dtype=np.float32) * 3)
+    z0 = lay.step(x0)["z"]
+    z1 = lay.step(x1)["z"]
+    r = O.bf16_bits_to_f32(x1) - O.bf16_bits_to_f32(x0)
+    rho = torch.from_numpy(r).to(torch.bfloat16).to(torch.float64).numpy()
+    wf = O.bf16_bits_to_f32(w)
+    np.testing.assert_allclose(z1 - z0, torch_conv(rho, wf, 1, 1, 1), rtol=1e-12, atol=1e-12)
+
+
+def test_mac_accounting():
+    rng = _rng(62)
+    w = rng.normal(0, 1, (8, 4, 3, 3)).astype(np.float32)
+    lay = O.SkipConvOracle(w, n=1, h=10, w=10, eps=0.5, block=2)
+    lay.step(rng.random((1, 10, 10, 4), dtype=np.float32))
+    x = rng.random((1, 10, 10, 4), dtype=np.float32)
+    out = lay.step(x)
+    assert out["active_macs"] == int(out["mask"].sum()) * 8 * 4 * 9
+    assert lay.dense_macs() == 100 * 8 * 4 * 9
+    d = O.mac_weighted_density([out["active_macs"], 0], [lay.dense_macs(), lay.dense_macs()])
+    assert d == pytest.approx(out["mask"].mean() / 2)
