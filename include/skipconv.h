@@ -1,0 +1,192 @@
+/*
+ * skipconv.h -- C ABI of the MI355X (gfx950) streaming Skip-Convolution layer.
+ *
+ * The layer follows Habibian et al., "Skip-Convolutions for Efficient Video
+ * Processing" (CVPR 2021):
+ *   Eq. 2  r_t = x_t - x_{t-1}; by linearity z_t = z_{t-1} + w * r_t.
+ *   Eq. 3  z~_t = z~_{t-1} + g(r_t) (.) (w * r_t): the convolution runs only at
+ *          output locations where the gate is on; elsewhere z~_{t-1} is kept.
+ *   Eq. 5  Input-Norm gate g = round(sigmoid(||r_t|| - eps)), the norm taken
+ *          over the kernel support (all input channels x k x k) of each output.
+ *   Sec. 3.2.2 structured gates: max-pool the gate with kernel = stride = b,
+ *          then nearest upsample, so the mask is constant on b x b blocks.
+ *   Sec. 3.1 the first frame (and each reference frame after a reset, the
+ *          reset period of Table 4) is computed over the whole frame.
+ *
+ * Conventions shared by every call:
+ *   - Tensors are NHWC, densely packed. Inputs x are in the layer dtype (fp32,
+ *     or bf16 as raw 16-bit patterns). The output state z is fp32.
+ *   - Weights are OIHW: c_out x (c_in/groups) x k x k, in the layer dtype.
+ *   - "device pointer" means memory of the current HIP device; "host pointer"
+ *     means ordinary host memory. The library never takes ownership of a
+ *     caller pointer.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *     Work is enqueued on it without host synchronisation unless a call says
+ *     otherwise.
+ *   - Every call returns SKIPCONV_OK (0) or a negative skipconv_status. No C++
+ *     exception crosses this boundary. A failed call leaves the handle as it
+ *     was, except after SKIPCONV_E_HIP from enqueued work, after which the
+ *     state is undefined until skipconv_reset.
+ *   - A handle is not thread-safe; distinct handles are independent.
+ */
+#ifndef SKIPCONV_H
+#define SKIPCONV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum skipconv_status {
+  SKIPCONV_OK = 0,
+  SKIPCONV_E_INVALID_ARG = -1,  /* bad descriptor field, NULL pointer, bad size */
+  SKIPCONV_E_UNSUPPORTED = -2,  /* valid but not implemented (e.g. 1 < groups < c_in) */
+  SKIPCONV_E_OOM = -3,          /* device allocation failed */
+  SKIPCONV_E_HIP = -4,          /* a HIP runtime call or kernel launch failed */
+  SKIPCONV_E_STATE = -5,        /* call not allowed in the handle's current state */
+  SKIPCONV_E_SMALL_BUFFER = -6  /* caller buffer smaller than required */
+} skipconv_status;
+
+enum { SKIPCONV_F32 = 0, SKIPCONV_BF16 = 1 };
+
+/* Gate support (Eq. 5): RF = norm over each output's whole kernel support
+ * (c_in x k x k, zero padding contributes nothing); CENTRE = norm over the
+ * single input pixel under the output (o * stride). */
+enum { SKIPCONV_SUPPORT_RF = 0, SKIPCONV_SUPPORT_CENTRE = 1 };
+
+/* Optional activation output kept beside z, for chaining layers: NONE = no
+ * buffer; IDENTITY = dtype(z); RELU = dtype(max(z, 0)). It changes only at
+ * updated sites, like z (z is pre-activation, Eq. 1). */
+enum { SKIPCONV_ACT_NONE = 0, SKIPCONV_ACT_IDENTITY = 1, SKIPCONV_ACT_RELU = 2 };
+
+/* KEEP_STATS: also store each frame's per-site gate statistic (fp32) and
+ * per-site gate bit (before block pooling), for skipconv_copy_stat /
+ * skipconv_copy_site_mask. FORCE_DENSE: every block is active on every frame
+ * (the same kernels, run dense; used as the dense baseline). */
+enum { SKIPCONV_FLAG_KEEP_STATS = 1u, SKIPCONV_FLAG_FORCE_DENSE = 2u };
+
+typedef struct skipconv_desc {
+  int32_t n;        /* independent streams (batch), >= 1 */
+  int32_t h, w;     /* input frame height, width, >= 1 */
+  int32_t c_in;     /* input channels, >= 1 */
+  int32_t c_out;    /* output channels, 1..256 (dense) or == c_in (depthwise) */
+  int32_t kernel;   /* k: odd, 1..7 */
+  int32_t stride;   /* s: 1..4 */
+  int32_t pad;      /* zero padding, 0..k-1; -1 selects (k-1)/2 */
+  int32_t groups;   /* 1 (dense) or c_in == c_out (depthwise) */
+  int32_t block;    /* b: gate block side, 1..64 (1 = per-site gate) */
+  int32_t norm_p;   /* 1: sum |r| > eps;  2: sum r^2 > eps^2 */
+  int32_t support;  /* SKIPCONV_SUPPORT_* */
+  int32_t dtype;    /* SKIPCONV_F32 or SKIPCONV_BF16 (inputs, weights, activation out) */
+  int32_t act_out;  /* SKIPCONV_ACT_* */
+  uint32_t flags;   /* SKIPCONV_FLAG_* */
+  float eps;        /* threshold, >= 0 or +inf; NaN is rejected */
+} skipconv_desc;
+
+typedef struct skipconv_layer* skipconv_t;
+
+/* Fill *d with defaults: n = h = w = c_in = c_out = 1, kernel 3, stride 1,
+ * pad -1, groups 1, block 1, norm_p 2, RF support, fp32, no activation
+ * output, no flags, eps 0. Host only. */
+int skipconv_desc_init(skipconv_desc* d);
+
+/* Check a descriptor without touching the GPU. Returns OK, E_INVALID_ARG or
+ * E_UNSUPPORTED. Host only. */
+int skipconv_validate(const skipconv_desc* d);
+
+/* Output and block-grid extents: h_out = (h + 2 pad - k) / stride + 1 (same
+ * for w); hb = ceil(h_out / block), wb = ceil(w_out / block). Host only;
+ * any output pointer may be NULL. */
+int skipconv_out_shape(const skipconv_desc* d, int32_t* h_out, int32_t* w_out,
+                       int32_t* hb, int32_t* wb);
+
+/* Device bytes one layer needs (packed weights, two x_{t-1} slots, z, the
+ * optional activation buffer, gate masks, active list, counters). Host only. */
+int skipconv_workspace_size(const skipconv_desc* d, size_t* bytes);
+
+/* Create a layer.
+ *   weights:   device pointer, OIHW in d->dtype; copied and repacked on
+ *              `stream` (the caller may free it once that work completes).
+ *   workspace: device pointer of at least skipconv_workspace_size bytes,
+ *              256-byte aligned, owned by the caller and kept alive until
+ *              skipconv_destroy; or NULL to let the library allocate it.
+ *   *out:      the new handle, or NULL on failure.
+ * The first step after create is a reference frame. */
+int skipconv_create(const skipconv_desc* d, const void* weights, void* workspace,
+                    size_t workspace_bytes, void* stream, skipconv_t* out);
+
+/* Process one frame (Eq. 3).
+ *   x_t: device pointer, 16-byte aligned, N x H x W x C_in in the layer
+ *        dtype; read by work enqueued on `stream`, so it must stay valid
+ *        until that work is done.
+ *   *z_t: (may be NULL) set to the device pointer of the persistent state,
+ *        N x H_out x W_out x C_out fp32, valid until the next step, reset or
+ *        destroy on this handle. Copy it to keep it.
+ * Enqueues the gate kernel (residual, support statistic, threshold, block
+ * pooling, ordered compaction, x_{t-1} update) and the sparse convolution
+ * kernel (gather of residual patches, MFMA product over active sites only,
+ * accumulate into z) on `stream`; no host synchronisation. */
+int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t);
+
+/* Make the next step a reference frame: x_{t-1} taken as zero, every site
+ * active, z assigned instead of accumulated (Sec. 3.1, Table 4). */
+int skipconv_reset(skipconv_t h);
+
+/* Change eps for later steps (same rules as the descriptor field). */
+int skipconv_set_eps(skipconv_t h, float eps);
+
+/* Release the handle and memory the library allocated. NULL is a no-op.
+ * Work still enqueued on the handle's streams must be complete. */
+int skipconv_destroy(skipconv_t h);
+
+/* Device pointer of the activation output (N x H_out x W_out x C_out in the
+ * layer dtype), or E_STATE when act_out is NONE. Valid like z. */
+int skipconv_activation(skipconv_t h, const void** y);
+
+/* Descriptor the handle was created with (eps as last set). Host only. */
+int skipconv_get_desc(skipconv_t h, skipconv_desc* d);
+
+/* ---- introspection (tests and benchmarks; each synchronises `stream`) ---- */
+
+/* Active blocks and active output sites of the last step. */
+int skipconv_active_count(skipconv_t h, void* stream, int64_t* blocks, int64_t* sites);
+
+/* Host copy of the last step's block mask, N x HB x WB bytes (0/1). */
+int skipconv_copy_block_mask(skipconv_t h, void* stream, uint8_t* host, size_t bytes);
+
+/* Host copy of the last step's active list: ascending block indices
+ * n*HB*WB + bi*WB + bj. capacity in entries; *count receives the length. */
+int skipconv_copy_active_list(skipconv_t h, void* stream, uint32_t* host, size_t capacity,
+                              int64_t* count);
+
+/* Host copies of the last step's per-site gate bit (N x H_out x W_out bytes)
+ * and gate statistic (fp32, same shape). E_STATE without KEEP_STATS. */
+int skipconv_copy_site_mask(skipconv_t h, void* stream, uint8_t* host, size_t bytes);
+int skipconv_copy_stat(skipconv_t h, void* stream, float* host, size_t bytes);
+
+/* Dense-equivalent and active MACs of the last step (the per-layer cost the
+ * gate loss of Eq. 9 weighs). */
+int skipconv_frame_macs(skipconv_t h, void* stream, uint64_t* dense, uint64_t* active);
+
+/* Static text for a status code. Host only. */
+const char* skipconv_status_string(int status);
+
+/* Last error message recorded on this handle (or the last failed create on
+ * this thread when h is NULL); never NULL. Host only. */
+const char* skipconv_last_error(skipconv_t h);
+
+/* ---- kernel timing (benchmarks) ----
+ * Time the next `frames` steps kernel by kernel with HIP events recorded on
+ * the step's stream: on skipconv_timing_read, ms[0] receives the summed
+ * milliseconds of the gate kernel and ms[1] of the convolution kernel, over
+ * the steps since skipconv_timing_begin (synchronises the stream). */
+int skipconv_timing_begin(skipconv_t h, int frames);
+int skipconv_timing_read(skipconv_t h, void* stream, double* ms, int* frames_timed);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SKIPCONV_H */

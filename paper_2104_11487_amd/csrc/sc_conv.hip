@@ -1,0 +1,419 @@
+// Sparse convolution of the Skip-Conv layer over the active sites (Eq. 3):
+//   z[o] += sum_{kh,kw,ci} w[co, ci, kh, kw] * rho[o*s - pad + (kh, kw), ci]
+// for every output site o inside an active block; untouched sites keep
+// z_{t-1}. rho is the residual x_t - x_{t-1} in fp32 (fp32 layers) or rounded
+// to bf16 (bf16 layers); on a reference frame x_{t-1} = 0 and z is assigned.
+//
+// The work is the im2col matrix product restricted to the active columns
+// (Sec. 4.2): rows = active sites, K = (kh, kw, ci), N = C_out. Rows are
+// enumerated block by block from the ordered active list (row g belongs to
+// list entry g / b^2, site g % b^2 of that block in row-major order), in
+// tiles of 64 rows; a persistent grid walks the tiles, reading the active
+// count from device memory, with each XCD taking one contiguous range of
+// tiles so that neighbouring sites (shared halo pixels) stay in one L2.
+//
+// Dense layers: each wave owns 16 rows and all output channels. For every
+// k-step a lane gathers its A fragment straight from the two frames
+// (x_t - x_{t-1}, rounded to bf16), and reads its B fragments from the
+// weights repacked at create time into the MFMA operand layout; products
+// accumulate in fp32 (v_mfma_f32_16x16x32_bf16, or v_mfma_f32_16x16x4_f32 for
+// fp32 layers). The epilogue adds the tile into z (each site belongs to
+// exactly one row, so there are no atomics) and refreshes the activation
+// output at the same sites.
+//
+// Depthwise layers (groups = C): no contraction to speak of, so no MFMA; one
+// thread per (site, 8 channels) sums the k x k taps with fp32 FMAs.
+#include "sc_device.h"
+#include "sc_kernels.h"
+
+namespace sc {
+
+namespace {
+
+constexpr int kConvThreads = 256;
+constexpr int kRowsPerTile = 64;
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+struct Site {
+  int n, oy, ox;
+  bool ok;
+};
+
+__device__ __forceinline__ Site site_of_row(const ConvParams& p, long g, long total_rows,
+                                            int bb) {
+  Site st{0, 0, 0, false};
+  if (g < total_rows) {
+    const int j = (int)(g / bb);
+    const int within = (int)(g - (long)j * bb);
+    const uint32_t blk = p.list[j];
+    const int per_img = p.hb * p.wb;
+    st.n = (int)(blk / per_img);
+    const int rem = (int)(blk - (uint32_t)st.n * per_img);
+    const int bi = rem / p.wb, bj = rem - bi * p.wb;
+    const int wy = within / p.block;
+    st.oy = bi * p.block + wy;
+    st.ox = bj * p.block + (within - wy * p.block);
+    st.ok = st.oy < p.h_out && st.ox < p.w_out;
+  }
+  return st;
+}
+
+// Tile walk of a persistent grid: XCD x = blockIdx % 8 takes a contiguous
+// range of tiles (workgroups are dispatched to the 8 XCDs round-robin).
+struct TileWalk {
+  int t, end, step;
+  __device__ TileWalk(int ntiles) {
+    const int g = gridDim.x, b = blockIdx.x;
+    if ((g & 7) == 0) {
+      const int xcd = b & 7, idx = b >> 3, per = g >> 3;
+      const int chunk = (ntiles + 7) >> 3;
+      const int t0 = xcd * chunk;
+      t = t0 + idx;
+      end = min(ntiles, t0 + chunk);
+      step = per;
+    } else {
+      t = b;
+      end = ntiles;
+      step = g;
+    }
+  }
+};
+
+__device__ __forceinline__ float activate(float v, int act) { return act == 2 ? fmaxf(v, 0.0f) : v; }
+
+template <typename T>
+__device__ __forceinline__ void store_y(void* y, size_t i, float v) {
+  Elem<T>::store1(static_cast<T*>(y), i, v);
+}
+
+// ---------------------------------------------------------------- bf16 ----
+
+template <bool FAST>
+__device__ __forceinline__ bf16x8 gather_a_bf16(const ConvParams& p, const uint16_t* xt,
+                                                const uint16_t* xp, const Site& st, int iy, int ix,
+                                                int ks, int kq) {
+  float v[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = 0.0f;
+  if (FAST) {
+    const int cpt = p.c >> 5;  // k-steps per tap
+    const int tap = ks / cpt;
+    const int c0 = (ks - tap * cpt) * 32 + kq * 8;
+    const int kh = tap / p.k, kw = tap - kh * p.k;
+    const int y = iy + kh, x = ix + kw;
+    if (st.ok && y >= 0 && y < p.h && x >= 0 && x < p.w) {
+      const size_t off = ((size_t)(st.n * p.h + y) * p.w + x) * p.c + c0;
+      float a[8], b[8];
+      Elem<uint16_t>::load8(xt, off, a);
+      if (!p.reference) {
+        Elem<uint16_t>::load8(xp, off, b);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = __fsub_rn(a[e], b[e]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = a[e];
+      }
+    }
+  } else {
+    const int kk = p.k * p.k * p.c;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int kidx = ks * 32 + kq * 8 + e;
+      if (kidx < kk && st.ok) {
+        const int tap = kidx / p.c, ci = kidx - tap * p.c;
+        const int kh = tap / p.k, kw = tap - kh * p.k;
+        const int y = iy + kh, x = ix + kw;
+        if (y >= 0 && y < p.h && x >= 0 && x < p.w) {
+          const size_t off = ((size_t)(st.n * p.h + y) * p.w + x) * p.c + ci;
+          const float a = bf16_to_f32(xt[off]);
+          const float b = p.reference ? 0.0f : bf16_to_f32(xp[off]);
+          v[e] = __fsub_rn(a, b);
+        }
+      }
+    }
+  }
+  u32x4 u;
+  u.x = f32_to_bf16(v[0]) | (f32_to_bf16(v[1]) << 16);
+  u.y = f32_to_bf16(v[2]) | (f32_to_bf16(v[3]) << 16);
+  u.z = f32_to_bf16(v[4]) | (f32_to_bf16(v[5]) << 16);
+  u.w = f32_to_bf16(v[6]) | (f32_to_bf16(v[7]) << 16);
+  return __builtin_bit_cast(bf16x8, u);
+}
+
+template <bool FAST, int NTN>
+__global__ void __launch_bounds__(kConvThreads) conv_bf16_kernel(ConvParams p) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, kq = lane >> 4;
+  const int bb = p.block * p.block;
+  const long total_rows = (long)p.counters[kCtrCount] * bb;
+  const int ntiles = (int)((total_rows + kRowsPerTile - 1) / kRowsPerTile);
+  const uint16_t* xt = static_cast<const uint16_t*>(p.x_t);
+  const uint16_t* xp = static_cast<const uint16_t*>(p.x_prev);
+  const bf16x8* wp = static_cast<const bf16x8*>(p.wpack);
+
+  for (TileWalk tw(ntiles); tw.t < tw.end; tw.t += tw.step) {
+    const long g = (long)tw.t * kRowsPerTile + wave * 16 + r16;
+    const Site st = site_of_row(p, g, total_rows, bb);
+    const int iy = st.oy * p.stride - p.pad, ix = st.ox * p.stride - p.pad;
+    floatx4 acc[NTN];
+#pragma unroll
+    for (int i = 0; i < NTN; ++i) acc[i] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+
+    for (int ks = 0; ks < p.ksteps; ++ks) {
+      const bf16x8 a = gather_a_bf16<FAST>(p, xt, xp, st, iy, ix, ks, kq);
+      const bf16x8* wk = wp + (size_t)ks * NTN * 64 + lane;
+#pragma unroll
+      for (int i = 0; i < NTN; ++i)
+        acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, wk[i * 64], acc[i], 0, 0, 0);
+    }
+
+    // epilogue: lane holds D[4*(lane/16) + v][lane % 16] of each 16x16 tile
+    const int zrow_mine = st.ok ? (st.n * p.h_out + st.oy) * p.w_out + st.ox : -1;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int zrow = __shfl(zrow_mine, kq * 4 + v, 64);
+      if (zrow < 0) continue;
+#pragma unroll
+      for (int i = 0; i < NTN; ++i) {
+        const int col = i * 16 + r16;
+        if (col >= p.c_out) continue;
+        const size_t idx = (size_t)zrow * p.c_out + col;
+        const float nv = p.reference ? acc[i][v] : p.z[idx] + acc[i][v];
+        p.z[idx] = nv;
+        if (p.act) store_y<uint16_t>(p.y, idx, activate(nv, p.act));
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------- fp32 ----
+
+template <int NTN>
+__global__ void __launch_bounds__(kConvThreads) conv_f32_kernel(ConvParams p) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, kq = lane >> 4;
+  const int bb = p.block * p.block;
+  const long total_rows = (long)p.counters[kCtrCount] * bb;
+  const int ntiles = (int)((total_rows + kRowsPerTile - 1) / kRowsPerTile);
+  const float* xt = static_cast<const float*>(p.x_t);
+  const float* xp = static_cast<const float*>(p.x_prev);
+  const float* wp = static_cast<const float*>(p.wpack);
+  const int kk = p.k * p.k * p.c;
+
+  for (TileWalk tw(ntiles); tw.t < tw.end; tw.t += tw.step) {
+    const long g = (long)tw.t * kRowsPerTile + wave * 16 + r16;
+    const Site st = site_of_row(p, g, total_rows, bb);
+    const int iy = st.oy * p.stride - p.pad, ix = st.ox * p.stride - p.pad;
+    floatx4 acc[NTN];
+#pragma unroll
+    for (int i = 0; i < NTN; ++i) acc[i] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+
+    for (int ks = 0; ks < p.ksteps; ++ks) {
+      const int kidx = ks * 4 + kq;
+      float a = 0.0f;
+      if (st.ok && kidx < kk) {
+        const int tap = kidx / p.c, ci = kidx - tap * p.c;
+        const int kh = tap / p.k, kw = tap - kh * p.k;
+        const int y = iy + kh, x = ix + kw;
+        if (y >= 0 && y < p.h && x >= 0 && x < p.w) {
+          const size_t off = ((size_t)(st.n * p.h + y) * p.w + x) * p.c + ci;
+          a = p.reference ? xt[off] : __fsub_rn(xt[off], xp[off]);
+        }
+      }
+      const float* wk = wp + (size_t)ks * NTN * 64 + lane;
+#pragma unroll
+      for (int i = 0; i < NTN; ++i)
+        acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, wk[i * 64], acc[i], 0, 0, 0);
+    }
+
+    const int zrow_mine = st.ok ? (st.n * p.h_out + st.oy) * p.w_out + st.ox : -1;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int zrow = __shfl(zrow_mine, kq * 4 + v, 64);
+      if (zrow < 0) continue;
+#pragma unroll
+      for (int i = 0; i < NTN; ++i) {
+        const int col = i * 16 + r16;
+        if (col >= p.c_out) continue;
+        const size_t idx = (size_t)zrow * p.c_out + col;
+        const float nv = p.reference ? acc[i][v] : p.z[idx] + acc[i][v];
+        p.z[idx] = nv;
+        if (p.act) store_y<float>(p.y, idx, activate(nv, p.act));
+      }
+    }
+  }
+}
+
+// ----------------------------------------------------------- depthwise ----
+
+template <typename T, int VEC>
+__global__ void __launch_bounds__(kConvThreads) depthwise_kernel(ConvParams p) {
+  const int bb = p.block * p.block;
+  const long total_rows = (long)p.counters[kCtrCount] * bb;
+  const int ntiles = (int)((total_rows + kRowsPerTile - 1) / kRowsPerTile);
+  const T* xt = static_cast<const T*>(p.x_t);
+  const T* xp = static_cast<const T*>(p.x_prev);
+  const float* wp = static_cast<const float*>(p.wpack);  // [tap][c] fp32
+  const int nchunk = p.c / VEC;
+  const bool bf16 = sizeof(T) == 2;
+
+  for (TileWalk tw(ntiles); tw.t < tw.end; tw.t += tw.step) {
+    for (int item = threadIdx.x; item < kRowsPerTile * nchunk; item += kConvThreads) {
+      const int row = item / nchunk;
+      const int c0 = (item - row * nchunk) * VEC;
+      const Site st = site_of_row(p, (long)tw.t * kRowsPerTile + row, total_rows, bb);
+      if (!st.ok) continue;
+      const int iy = st.oy * p.stride - p.pad, ix = st.ox * p.stride - p.pad;
+      float acc[VEC];
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) acc[j] = 0.0f;
+      for (int kh = 0; kh < p.k; ++kh) {
+        const int y = iy + kh;
+        if (y < 0 || y >= p.h) continue;
+        for (int kw = 0; kw < p.k; ++kw) {
+          const int x = ix + kw;
+          if (x < 0 || x >= p.w) continue;
+          const size_t off = ((size_t)(st.n * p.h + y) * p.w + x) * p.c + c0;
+          float a[VEC], b[VEC];
+          if (VEC == 8) {
+            Elem<T>::load8(xt, off, a);
+            if (!p.reference) Elem<T>::load8(xp, off, b);
+          } else if (VEC == 4) {
+            Elem<T>::load4(xt, off, a);
+            if (!p.reference) Elem<T>::load4(xp, off, b);
+          } else {
+            a[0] = Elem<T>::load1(xt, off);
+            if (!p.reference) b[0] = Elem<T>::load1(xp, off);
+          }
+          const float* wt = wp + (kh * p.k + kw) * p.c + c0;
+#pragma unroll
+          for (int j = 0; j < VEC; ++j) {
+            float r = p.reference ? a[j] : __fsub_rn(a[j], b[j]);
+            if (bf16) r = bf16_to_f32(f32_to_bf16(r));
+            acc[j] = __builtin_fmaf(wt[j], r, acc[j]);
+          }
+        }
+      }
+      const size_t zb = ((size_t)(st.n * p.h_out + st.oy) * p.w_out + st.ox) * p.c_out + c0;
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) {
+        const float nv = p.reference ? acc[j] : p.z[zb + j] + acc[j];
+        p.z[zb + j] = nv;
+        if (p.act) store_y<T>(p.y, zb + j, activate(nv, p.act));
+      }
+    }
+  }
+}
+
+// -------------------------------------------------------------- repack ----
+
+// B fragment layout of v_mfma_f32_16x16x32_bf16: for k-step ks and output tile
+// nt, lane l holds B[k = ks*32 + 8*(l/16) + e][n = nt*16 + l%16], e = 0..7,
+// with K ordered (kh, kw, ci). For v_mfma_f32_16x16x4_f32 lane l holds
+// B[k = ks*4 + l/16][n = nt*16 + l%16]. Entries beyond K or C_out are zero.
+__global__ void pack_mfma_kernel(const void* w, void* out, int dtype, int c_out, int c_in, int k,
+                                 int ksteps, int ntn) {
+  const int per_lane = dtype == 1 ? 8 : 1;
+  const int kstep = dtype == 1 ? 32 : 4;
+  const long total = (long)ksteps * ntn * 64 * per_lane;
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= total) return;
+  const int e = (int)(i % per_lane);
+  const long q = i / per_lane;
+  const int lane = (int)(q % 64);
+  const long q2 = q / 64;
+  const int nt = (int)(q2 % ntn);
+  const int ks = (int)(q2 / ntn);
+  const int kidx = ks * kstep + (lane >> 4) * per_lane + e;
+  const int co = nt * 16 + (lane & 15);
+  const int kk = k * k * c_in;
+  float v = 0.0f;
+  if (kidx < kk && co < c_out) {
+    const int tap = kidx / c_in, ci = kidx - tap * c_in;
+    const int kh = tap / k, kw = tap - kh * k;
+    const size_t src = (((size_t)co * c_in + ci) * k + kh) * k + kw;
+    v = dtype == 1 ? bf16_to_f32(static_cast<const uint16_t*>(w)[src]) : static_cast<const float*>(w)[src];
+  }
+  if (dtype == 1)
+    static_cast<uint16_t*>(out)[i] = (uint16_t)f32_to_bf16(v);  // exact: v is a bf16 value
+  else
+    static_cast<float*>(out)[i] = v;
+}
+
+// Depthwise weights (C x 1 x k x k) to [tap][c] fp32.
+__global__ void pack_depthwise_kernel(const void* w, float* out, int dtype, int c, int k) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= c * k * k) return;
+  const int tap = i / c, ch = i - tap * c;
+  const size_t src = (size_t)ch * k * k + tap;
+  out[i] = dtype == 1 ? bf16_to_f32(static_cast<const uint16_t*>(w)[src]) : static_cast<const float*>(w)[src];
+}
+
+template <bool FAST>
+hipError_t launch_conv_bf16(const ConvParams& p, int grid, hipStream_t st) {
+  switch (p.ntiles_n) {
+    case 1: hipLaunchKernelGGL((conv_bf16_kernel<FAST, 1>), dim3(grid), dim3(kConvThreads), 0, st, p); break;
+    case 2: hipLaunchKernelGGL((conv_bf16_kernel<FAST, 2>), dim3(grid), dim3(kConvThreads), 0, st, p); break;
+    case 4: hipLaunchKernelGGL((conv_bf16_kernel<FAST, 4>), dim3(grid), dim3(kConvThreads), 0, st, p); break;
+    case 8: hipLaunchKernelGGL((conv_bf16_kernel<FAST, 8>), dim3(grid), dim3(kConvThreads), 0, st, p); break;
+    case 12: hipLaunchKernelGGL((conv_bf16_kernel<FAST, 12>), dim3(grid), dim3(kConvThreads), 0, st, p); break;
+    case 16: hipLaunchKernelGGL((conv_bf16_kernel<FAST, 16>), dim3(grid), dim3(kConvThreads), 0, st, p); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_conv_f32(const ConvParams& p, int grid, hipStream_t st) {
+  switch (p.ntiles_n) {
+    case 1: hipLaunchKernelGGL((conv_f32_kernel<1>), dim3(grid), dim3(kConvThreads), 0, st, p); break;
+    case 2: hipLaunchKernelGGL((conv_f32_kernel<2>), dim3(grid), dim3(kConvThreads), 0, st, p); break;
+    case 4: hipLaunchKernelGGL((conv_f32_kernel<4>), dim3(grid), dim3(kConvThreads), 0, st, p); break;
+    case 8: hipLaunchKernelGGL((conv_f32_kernel<8>), dim3(grid), dim3(kConvThreads), 0, st, p); break;
+    case 12: hipLaunchKernelGGL((conv_f32_kernel<12>), dim3(grid), dim3(kConvThreads), 0, st, p); break;
+    case 16: hipLaunchKernelGGL((conv_f32_kernel<16>), dim3(grid), dim3(kConvThreads), 0, st, p); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_conv(const ConvParams& p, int dtype, bool fast, int grid, hipStream_t st) {
+  if (dtype == 0) return launch_conv_f32(p, grid, st);
+  return fast ? launch_conv_bf16<true>(p, grid, st) : launch_conv_bf16<false>(p, grid, st);
+}
+
+hipError_t launch_depthwise(const ConvParams& p, int dtype, int grid, hipStream_t st) {
+  if (dtype == 0) {
+    if (p.c % 4 == 0)
+      hipLaunchKernelGGL((depthwise_kernel<float, 4>), dim3(grid), dim3(kConvThreads), 0, st, p);
+    else
+      hipLaunchKernelGGL((depthwise_kernel<float, 1>), dim3(grid), dim3(kConvThreads), 0, st, p);
+  } else {
+    if (p.c % 8 == 0)
+      hipLaunchKernelGGL((depthwise_kernel<uint16_t, 8>), dim3(grid), dim3(kConvThreads), 0, st, p);
+    else
+      hipLaunchKernelGGL((depthwise_kernel<uint16_t, 1>), dim3(grid), dim3(kConvThreads), 0, st, p);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_mfma(const void* w, void* out, int dtype, int c_out, int c_in, int k,
+                            int ksteps, int ntiles_n, hipStream_t st) {
+  const long total = (long)ksteps * ntiles_n * 64 * (dtype == 1 ? 8 : 1);
+  const int grid = (int)((total + 255) / 256);
+  hipLaunchKernelGGL(pack_mfma_kernel, dim3(grid), dim3(256), 0, st, w, out, dtype, c_out, c_in, k,
+                     ksteps, ntiles_n);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_depthwise(const void* w, float* out, int dtype, int c, int k,
+                                 hipStream_t st) {
+  const int total = c * k * k;
+  hipLaunchKernelGGL(pack_depthwise_kernel, dim3((total + 255) / 256), dim3(256), 0, st, w, out,
+                     dtype, c, k);
+  return hipGetLastError();
+}
+
+}  // namespace sc

@@ -1,0 +1,65 @@
+// Kernel parameter blocks and launchers of the Skip-Conv layer (host + device).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sc {
+
+// counters[] slots in the workspace
+constexpr int kCtrCount = 0;  // active blocks of the last gate pass
+constexpr int kCtrDone = 1;   // gate workgroups finished (returned to 0 by the last one)
+constexpr int kNumCounters = 16;
+
+constexpr int kMaxTileBlocks = 256;  // blocks per gate tile: (ts / b)^2 <= 256
+
+// Gate: residual, support statistic, threshold, block pooling, compaction.
+struct GateParams {
+  const void* x_t;      // N x H x W x C, layer dtype
+  const void* x_prev;   // x_{t-1} slot being read (unused on reference frames)
+  void* x_keep;         // spare slot receiving x_t
+  int n, h, w, c;
+  int h_out, w_out, k, stride, pad, block, hb, wb;
+  int ts, tiles_y, tiles_x;     // tile side (sites) and tile grid per image
+  int halo_floats;              // LDS floats reserved for the a[] halo
+  int stage_stride;             // LDS floats per staged pixel (>= c, odd)
+  int rows_per_batch;           // halo rows staged at once
+  int copy_in_halo;             // 1: every owned input pixel lies in its tile's halo
+  int norm_p, support, reference, force_dense, keep_stats;
+  double thr;                   // eps^2 (p = 2) or eps (p = 1), exact in fp64
+  uint8_t* block_mask;          // N x HB x WB
+  uint32_t* list;               // N x HB x WB (first count entries valid)
+  uint32_t* counters;
+  float* stat;                  // N x H_out x W_out (keep_stats)
+  uint8_t* site_mask;           // N x H_out x W_out (keep_stats)
+};
+
+// Sparse convolution over the active sites (dense groups = 1).
+struct ConvParams {
+  const void* x_t;
+  const void* x_prev;
+  const void* wpack;            // packed MFMA B fragments
+  float* z;                     // N x H_out x W_out x C_out fp32
+  void* y;                      // optional activation output (layer dtype)
+  const uint32_t* list;
+  const uint32_t* counters;
+  int n, h, w, c, c_out;
+  int h_out, w_out, k, stride, pad, block, hb, wb;
+  int ksteps;                   // K padded to the MFMA k-step, in steps
+  int ntiles_n;                 // ceil(C_out / 16)
+  int reference;                // assign z instead of accumulating; x_{t-1} = 0
+  int act;                      // 0 none, 1 identity, 2 relu
+};
+
+hipError_t launch_gate(const GateParams& p, int dtype, int vec, int grid, size_t lds_bytes,
+                       hipStream_t st);
+hipError_t launch_conv(const ConvParams& p, int dtype, bool fast, int grid, hipStream_t st);
+hipError_t launch_depthwise(const ConvParams& p, int dtype, int grid, hipStream_t st);
+
+// One-time weight repacks (create time).
+hipError_t launch_pack_mfma(const void* w, void* out, int dtype, int c_out, int c_in, int k,
+                            int ksteps, int ntiles_n, hipStream_t st);
+hipError_t launch_pack_depthwise(const void* w, float* out, int dtype, int c, int k,
+                                 hipStream_t st);
+
+}  // namespace sc

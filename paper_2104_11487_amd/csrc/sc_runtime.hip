@@ -1,0 +1,576 @@
+// Host runtime of the Skip-Conv layer: descriptor validation, workspace
+// layout, weight repack, ping-pong x_{t-1} slots, the per-frame launch
+// sequence, introspection and kernel timing. Implements include/skipconv.h.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "../../include/skipconv.h"
+#include "sc_kernels.h"
+
+namespace {
+
+thread_local char g_create_error[256] = "";
+
+constexpr size_t kAlign = 256;
+constexpr size_t kLdsLimit = 60 * 1024;  // dynamic; the gate kernel adds 2 KB static
+constexpr size_t kStageBudget = 48 * 1024;
+constexpr int kMaxCout = 256;
+
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+struct Geometry {
+  int pad, h_out, w_out, hb, wb, nb;
+  int ts, tiles_y, tiles_x, gate_grid;
+  int hh_max, hw_max, halo_floats, stage_stride, rows_per_batch;
+  size_t gate_lds;
+  int copy_in_halo;
+  bool depthwise;
+  int kk, ksteps, ntn;  // dense: K, k-steps, 16-wide output tiles (padded to an instantiated count)
+  bool fast;
+  int vec;              // gate load width (elements)
+  size_t elem;
+  size_t off_wpack, off_slot0, off_slot1, off_z, off_y, off_bmask, off_list, off_ctr, off_stat,
+      off_smask, total;
+  size_t wpack_bytes, x_bytes, z_bytes;
+  int conv_max_tiles;
+};
+
+int fail(char* buf, int code, const char* msg) {
+  if (buf) snprintf(buf, 256, "%s", msg);
+  return code;
+}
+
+int ntn_for(int c_out) {
+  const int t = (c_out + 15) / 16;
+  static const int opts[] = {1, 2, 4, 8, 12, 16};
+  for (int o : opts)
+    if (t <= o) return o;
+  return -1;
+}
+
+// Validates the descriptor and derives every size. Host only.
+int derive(const skipconv_desc* d, Geometry* g, char* err) {
+  if (!d) return fail(err, SKIPCONV_E_INVALID_ARG, "descriptor is NULL");
+  if (d->n < 1 || d->h < 1 || d->w < 1 || d->c_in < 1 || d->c_out < 1)
+    return fail(err, SKIPCONV_E_INVALID_ARG, "n, h, w, c_in and c_out must be >= 1");
+  if (d->kernel < 1 || d->kernel % 2 == 0 || d->kernel > 7)
+    return fail(err, SKIPCONV_E_INVALID_ARG, "kernel must be odd, 1..7");
+  if (d->stride < 1 || d->stride > 4) return fail(err, SKIPCONV_E_INVALID_ARG, "stride must be 1..4");
+  const int pad = d->pad == -1 ? (d->kernel - 1) / 2 : d->pad;
+  if (pad < 0 || pad > d->kernel - 1)
+    return fail(err, SKIPCONV_E_INVALID_ARG, "pad must be -1 or 0..kernel-1");
+  if (d->groups < 1 || d->c_in % d->groups || d->c_out % d->groups)
+    return fail(err, SKIPCONV_E_INVALID_ARG, "groups must divide c_in and c_out");
+  const bool depthwise = d->groups > 1;
+  if (depthwise && !(d->groups == d->c_in && d->c_out == d->c_in))
+    return fail(err, SKIPCONV_E_UNSUPPORTED, "only groups == 1 or groups == c_in == c_out");
+  if (d->block < 1 || d->block > 64) return fail(err, SKIPCONV_E_INVALID_ARG, "block must be 1..64");
+  if (d->norm_p != 1 && d->norm_p != 2) return fail(err, SKIPCONV_E_INVALID_ARG, "norm_p must be 1 or 2");
+  if (d->support != SKIPCONV_SUPPORT_RF && d->support != SKIPCONV_SUPPORT_CENTRE)
+    return fail(err, SKIPCONV_E_INVALID_ARG, "unknown support");
+  if (d->dtype != SKIPCONV_F32 && d->dtype != SKIPCONV_BF16)
+    return fail(err, SKIPCONV_E_INVALID_ARG, "unknown dtype");
+  if (d->act_out < SKIPCONV_ACT_NONE || d->act_out > SKIPCONV_ACT_RELU)
+    return fail(err, SKIPCONV_E_INVALID_ARG, "unknown act_out");
+  if (d->flags & ~(uint32_t)(SKIPCONV_FLAG_KEEP_STATS | SKIPCONV_FLAG_FORCE_DENSE))
+    return fail(err, SKIPCONV_E_INVALID_ARG, "unknown flag bits");
+  if (std::isnan(d->eps) || d->eps < 0.0f) return fail(err, SKIPCONV_E_INVALID_ARG, "eps must be >= 0");
+  if (!depthwise && d->c_out > kMaxCout) return fail(err, SKIPCONV_E_UNSUPPORTED, "c_out > 256");
+
+  Geometry& G = *g;
+  G = Geometry{};
+  G.pad = pad;
+  const int k = d->kernel, s = d->stride;
+  G.h_out = (d->h + 2 * pad - k) / s + 1;
+  G.w_out = (d->w + 2 * pad - k) / s + 1;
+  if (d->h + 2 * pad < k || d->w + 2 * pad < k || G.h_out < 1 || G.w_out < 1)
+    return fail(err, SKIPCONV_E_INVALID_ARG, "frame smaller than the kernel");
+  const int b = d->block;
+  G.hb = (G.h_out + b - 1) / b;
+  G.wb = (G.w_out + b - 1) / b;
+  const long nb = (long)d->n * G.hb * G.wb;
+  const long sites = (long)d->n * G.h_out * G.w_out;
+  const long xel = (long)d->n * d->h * d->w * d->c_in;
+  if (nb > (1L << 30) || sites * d->c_out > (1L << 40) || xel > (1L << 40) ||
+      (long)d->n * d->h * d->w > (1L << 31) - 1 || sites > (1L << 31) - 1)
+    return fail(err, SKIPCONV_E_UNSUPPORTED, "tensor too large");
+  G.nb = (int)nb;
+  G.depthwise = depthwise;
+  G.elem = d->dtype == SKIPCONV_BF16 ? 2 : 4;
+
+  // gate tiling: ts x ts output sites, whole blocks, about 16 x 16 sites
+  G.ts = b <= 16 ? b * (16 / b) : b;
+  G.tiles_y = (G.h_out + G.ts - 1) / G.ts;
+  G.tiles_x = (G.w_out + G.ts - 1) / G.ts;
+  G.gate_grid = d->n * G.tiles_y * G.tiles_x;
+  G.hh_max = (G.ts - 1) * s + k;
+  G.hw_max = G.hh_max;
+  G.halo_floats = G.hh_max * G.hw_max;
+  G.stage_stride = d->c_in | 1;
+  const size_t row_bytes = (size_t)G.hw_max * G.stage_stride * 4;
+  G.rows_per_batch = (int)std::max<size_t>(1, std::min<size_t>(kStageBudget / row_bytes, G.hh_max));
+  G.gate_lds = ((size_t)G.halo_floats + (size_t)G.rows_per_batch * G.hw_max * G.stage_stride) * 4;
+  if (G.gate_lds > kLdsLimit)
+    return fail(err, SKIPCONV_E_UNSUPPORTED, "gate tile does not fit in LDS (too many channels)");
+  if (d->dtype == SKIPCONV_BF16)
+    G.vec = (d->c_in % 8 == 0) ? 8 : 1;
+  else
+    G.vec = (d->c_in % 4 == 0) ? 4 : 1;
+
+  // does every tile's halo cover the input pixels it owns?
+  G.copy_in_halo = 1;
+  for (int ty = 0; ty < G.tiles_y && G.copy_in_halo; ++ty) {
+    const int oy0 = ty * G.ts, oh = std::min(G.ts, G.h_out - oy0);
+    const int lo = oy0 * s - pad, hi = (oy0 + oh - 1) * s - pad + k - 1;
+    const int own1 = ty == G.tiles_y - 1 ? d->h : std::min(d->h, (oy0 + G.ts) * s);
+    if (oy0 * s < lo || own1 - 1 > hi) G.copy_in_halo = 0;
+  }
+  for (int tx = 0; tx < G.tiles_x && G.copy_in_halo; ++tx) {
+    const int ox0 = tx * G.ts, ow = std::min(G.ts, G.w_out - ox0);
+    const int lo = ox0 * s - pad, hi = (ox0 + ow - 1) * s - pad + k - 1;
+    const int own1 = tx == G.tiles_x - 1 ? d->w : std::min(d->w, (ox0 + G.ts) * s);
+    if (ox0 * s < lo || own1 - 1 > hi) G.copy_in_halo = 0;
+  }
+
+  // convolution geometry
+  G.kk = k * k * (d->c_in / d->groups);
+  if (!depthwise) {
+    const int kstep = d->dtype == SKIPCONV_BF16 ? 32 : 4;
+    G.ksteps = (G.kk + kstep - 1) / kstep;
+    G.ntn = ntn_for(d->c_out);
+    G.fast = d->dtype == SKIPCONV_BF16 && d->c_in % 32 == 0;
+    G.wpack_bytes = (size_t)G.ksteps * G.ntn * 64 * (d->dtype == SKIPCONV_BF16 ? 16 : 4);
+  } else {
+    G.wpack_bytes = (size_t)k * k * d->c_in * 4;
+  }
+  G.conv_max_tiles = (int)(((long)G.nb * b * b + 63) / 64);
+
+  G.x_bytes = (size_t)xel * G.elem;
+  G.z_bytes = (size_t)sites * d->c_out * 4;
+  size_t off = 0;
+  G.off_wpack = off; off = align_up(off + G.wpack_bytes);
+  G.off_slot0 = off; off = align_up(off + G.x_bytes);
+  G.off_slot1 = off; off = align_up(off + G.x_bytes);
+  G.off_z = off; off = align_up(off + G.z_bytes);
+  G.off_y = off;
+  if (d->act_out != SKIPCONV_ACT_NONE) off = align_up(off + (size_t)sites * d->c_out * G.elem);
+  G.off_bmask = off; off = align_up(off + (size_t)nb);
+  G.off_list = off; off = align_up(off + (size_t)nb * 4);
+  G.off_ctr = off; off = align_up(off + sc::kNumCounters * 4);
+  G.off_stat = off;
+  G.off_smask = off;
+  if (d->flags & SKIPCONV_FLAG_KEEP_STATS) {
+    off = align_up(off + (size_t)sites * 4);
+    G.off_smask = off;
+    off = align_up(off + (size_t)sites);
+  }
+  G.total = off;
+  return SKIPCONV_OK;
+}
+
+}  // namespace
+
+struct skipconv_layer {
+  skipconv_desc d;
+  Geometry g;
+  int device = 0;
+  int num_cu = 256;
+  char* ws = nullptr;
+  bool owns_ws = false;
+  int cur = 0;               // slot holding x_{t-1}
+  bool ref_pending = true;
+  long long frames = 0;
+  char last_error[256] = "";
+  // timing
+  std::vector<hipEvent_t> ev;
+  int timing_frames = 0, timing_done = 0;
+
+  void* wpack() { return ws + g.off_wpack; }
+  void* slot(int i) { return ws + (i ? g.off_slot1 : g.off_slot0); }
+  float* z() { return reinterpret_cast<float*>(ws + g.off_z); }
+  void* y() { return d.act_out ? (void*)(ws + g.off_y) : nullptr; }
+  uint8_t* bmask() { return reinterpret_cast<uint8_t*>(ws + g.off_bmask); }
+  uint32_t* list() { return reinterpret_cast<uint32_t*>(ws + g.off_list); }
+  uint32_t* ctr() { return reinterpret_cast<uint32_t*>(ws + g.off_ctr); }
+  float* stat() { return reinterpret_cast<float*>(ws + g.off_stat); }
+  uint8_t* smask() { return reinterpret_cast<uint8_t*>(ws + g.off_smask); }
+};
+
+namespace {
+
+int hip_fail(skipconv_t h, hipError_t e, const char* what) {
+  if (h) snprintf(h->last_error, sizeof(h->last_error), "%s: %s", what, hipGetErrorString(e));
+  return SKIPCONV_E_HIP;
+}
+
+double threshold(const skipconv_desc& d) {
+  const double e = (double)d.eps;  // fp32 -> fp64 is exact; e * e is exact in fp64
+  return d.norm_p == 2 ? e * e : e;
+}
+
+int conv_grid(const skipconv_layer* h) {
+  int grid = std::min(h->g.conv_max_tiles, h->num_cu * 4);
+  if (grid >= 8) grid = (grid + 7) / 8 * 8;
+  return std::max(grid, 1);
+}
+
+void destroy_events(skipconv_layer* h) {
+  for (hipEvent_t e : h->ev) (void)hipEventDestroy(e);
+  h->ev.clear();
+  h->timing_frames = h->timing_done = 0;
+}
+
+}  // namespace
+
+extern "C" {
+
+int skipconv_desc_init(skipconv_desc* d) {
+  if (!d) return SKIPCONV_E_INVALID_ARG;
+  std::memset(d, 0, sizeof(*d));
+  d->n = d->h = d->w = d->c_in = d->c_out = 1;
+  d->kernel = 3;
+  d->stride = 1;
+  d->pad = -1;
+  d->groups = 1;
+  d->block = 1;
+  d->norm_p = 2;
+  d->support = SKIPCONV_SUPPORT_RF;
+  d->dtype = SKIPCONV_F32;
+  d->act_out = SKIPCONV_ACT_NONE;
+  d->flags = 0;
+  d->eps = 0.0f;
+  return SKIPCONV_OK;
+}
+
+int skipconv_validate(const skipconv_desc* d) {
+  Geometry g;
+  return derive(d, &g, g_create_error);
+}
+
+int skipconv_out_shape(const skipconv_desc* d, int32_t* h_out, int32_t* w_out, int32_t* hb,
+                       int32_t* wb) {
+  Geometry g;
+  const int rc = derive(d, &g, g_create_error);
+  if (rc) return rc;
+  if (h_out) *h_out = g.h_out;
+  if (w_out) *w_out = g.w_out;
+  if (hb) *hb = g.hb;
+  if (wb) *wb = g.wb;
+  return SKIPCONV_OK;
+}
+
+int skipconv_workspace_size(const skipconv_desc* d, size_t* bytes) {
+  if (!bytes) return SKIPCONV_E_INVALID_ARG;
+  Geometry g;
+  const int rc = derive(d, &g, g_create_error);
+  if (rc) return rc;
+  *bytes = g.total;
+  return SKIPCONV_OK;
+}
+
+int skipconv_create(const skipconv_desc* d, const void* weights, void* workspace,
+                    size_t workspace_bytes, void* stream, skipconv_t* out) {
+  if (!out) return fail(g_create_error, SKIPCONV_E_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  Geometry g;
+  int rc = derive(d, &g, g_create_error);
+  if (rc) return rc;
+  if (!weights) return fail(g_create_error, SKIPCONV_E_INVALID_ARG, "weights is NULL");
+  if (workspace && workspace_bytes < g.total)
+    return fail(g_create_error, SKIPCONV_E_SMALL_BUFFER, "workspace smaller than skipconv_workspace_size");
+  if (workspace && (reinterpret_cast<uintptr_t>(workspace) % kAlign))
+    return fail(g_create_error, SKIPCONV_E_INVALID_ARG, "workspace must be 256-byte aligned");
+
+  skipconv_layer* h = new (std::nothrow) skipconv_layer();
+  if (!h) return fail(g_create_error, SKIPCONV_E_OOM, "host allocation failed");
+  h->d = *d;
+  h->d.pad = g.pad;
+  h->g = g;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = hipGetDevice(&h->device);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&h->num_cu, hipDeviceAttributeMultiprocessorCount, h->device);
+  if (e != hipSuccess) {
+    snprintf(g_create_error, sizeof(g_create_error), "no HIP device: %s", hipGetErrorString(e));
+    delete h;
+    return SKIPCONV_E_HIP;
+  }
+  if (workspace) {
+    h->ws = static_cast<char*>(workspace);
+  } else {
+    void* p = nullptr;
+    e = hipMalloc(&p, g.total);
+    if (e != hipSuccess) {
+      snprintf(g_create_error, sizeof(g_create_error), "hipMalloc(%zu): %s", g.total, hipGetErrorString(e));
+      delete h;
+      return SKIPCONV_E_OOM;
+    }
+    h->ws = static_cast<char*>(p);
+    h->owns_ws = true;
+  }
+  e = hipMemsetAsync(h->ctr(), 0, sc::kNumCounters * 4, st);
+  if (e == hipSuccess) e = hipMemsetAsync(h->bmask(), 0, g.nb, st);
+  if (e == hipSuccess) e = hipMemsetAsync(h->list(), 0, (size_t)g.nb * 4, st);
+  if (e == hipSuccess) {
+    if (g.depthwise)
+      e = sc::launch_pack_depthwise(weights, static_cast<float*>(h->wpack()), d->dtype, d->c_in,
+                                    d->kernel, st);
+    else
+      e = sc::launch_pack_mfma(weights, h->wpack(), d->dtype, d->c_out, d->c_in, d->kernel,
+                               g.ksteps, g.ntn, st);
+  }
+  if (e != hipSuccess) {
+    snprintf(g_create_error, sizeof(g_create_error), "create: %s", hipGetErrorString(e));
+    if (h->owns_ws) (void)hipFree(h->ws);
+    delete h;
+    return SKIPCONV_E_HIP;
+  }
+  *out = h;
+  return SKIPCONV_OK;
+}
+
+int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t) {
+  if (!h) return SKIPCONV_E_STATE;
+  if (!x_t) return fail(h->last_error, SKIPCONV_E_INVALID_ARG, "x_t is NULL");
+  if (reinterpret_cast<uintptr_t>(x_t) % 16)
+    return fail(h->last_error, SKIPCONV_E_INVALID_ARG, "x_t must be 16-byte aligned");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const skipconv_desc& d = h->d;
+  const Geometry& g = h->g;
+  const bool ref = h->ref_pending;
+
+  sc::GateParams gp{};
+  gp.x_t = x_t;
+  gp.x_prev = h->slot(h->cur);
+  gp.x_keep = h->slot(h->cur ^ 1);
+  gp.n = d.n; gp.h = d.h; gp.w = d.w; gp.c = d.c_in;
+  gp.h_out = g.h_out; gp.w_out = g.w_out; gp.k = d.kernel; gp.stride = d.stride; gp.pad = g.pad;
+  gp.block = d.block; gp.hb = g.hb; gp.wb = g.wb;
+  gp.ts = g.ts; gp.tiles_y = g.tiles_y; gp.tiles_x = g.tiles_x;
+  gp.halo_floats = g.halo_floats; gp.stage_stride = g.stage_stride;
+  gp.rows_per_batch = g.rows_per_batch; gp.copy_in_halo = g.copy_in_halo;
+  gp.norm_p = d.norm_p; gp.support = d.support; gp.reference = ref ? 1 : 0;
+  gp.force_dense = (d.flags & SKIPCONV_FLAG_FORCE_DENSE) ? 1 : 0;
+  gp.keep_stats = (d.flags & SKIPCONV_FLAG_KEEP_STATS) ? 1 : 0;
+  gp.thr = threshold(d);
+  gp.block_mask = h->bmask(); gp.list = h->list(); gp.counters = h->ctr();
+  gp.stat = h->stat(); gp.site_mask = h->smask();
+
+  sc::ConvParams cp{};
+  cp.x_t = x_t;
+  cp.x_prev = h->slot(h->cur);
+  cp.wpack = h->wpack();
+  cp.z = h->z();
+  cp.y = h->y();
+  cp.list = h->list();
+  cp.counters = h->ctr();
+  cp.n = d.n; cp.h = d.h; cp.w = d.w; cp.c = d.c_in; cp.c_out = d.c_out;
+  cp.h_out = g.h_out; cp.w_out = g.w_out; cp.k = d.kernel; cp.stride = d.stride; cp.pad = g.pad;
+  cp.block = d.block; cp.hb = g.hb; cp.wb = g.wb;
+  cp.ksteps = g.ksteps; cp.ntiles_n = g.ntn;
+  cp.reference = ref ? 1 : 0;
+  cp.act = d.act_out;
+
+  const bool timing = h->timing_done < h->timing_frames;
+  hipError_t e = hipSuccess;
+  if (timing) e = hipEventRecord(h->ev[3 * h->timing_done], st);
+  if (e == hipSuccess) e = sc::launch_gate(gp, d.dtype, g.vec, g.gate_grid, g.gate_lds, st);
+  if (e != hipSuccess) return hip_fail(h, e, "gate launch");
+  if (timing) e = hipEventRecord(h->ev[3 * h->timing_done + 1], st);
+  if (e == hipSuccess) {
+    if (g.depthwise)
+      e = sc::launch_depthwise(cp, d.dtype, conv_grid(h), st);
+    else
+      e = sc::launch_conv(cp, d.dtype, g.fast, conv_grid(h), st);
+  }
+  if (e != hipSuccess) return hip_fail(h, e, "conv launch");
+  if (timing) {
+    e = hipEventRecord(h->ev[3 * h->timing_done + 2], st);
+    if (e != hipSuccess) return hip_fail(h, e, "event record");
+    ++h->timing_done;
+  }
+  h->cur ^= 1;
+  h->ref_pending = false;
+  ++h->frames;
+  if (z_t) *z_t = h->z();
+  return SKIPCONV_OK;
+}
+
+int skipconv_reset(skipconv_t h) {
+  if (!h) return SKIPCONV_E_STATE;
+  h->ref_pending = true;
+  return SKIPCONV_OK;
+}
+
+int skipconv_set_eps(skipconv_t h, float eps) {
+  if (!h) return SKIPCONV_E_STATE;
+  if (std::isnan(eps) || eps < 0.0f) return fail(h->last_error, SKIPCONV_E_INVALID_ARG, "eps must be >= 0");
+  h->d.eps = eps;
+  return SKIPCONV_OK;
+}
+
+int skipconv_destroy(skipconv_t h) {
+  if (!h) return SKIPCONV_OK;
+  destroy_events(h);
+  if (h->owns_ws) (void)hipFree(h->ws);
+  delete h;
+  return SKIPCONV_OK;
+}
+
+int skipconv_activation(skipconv_t h, const void** y) {
+  if (!h) return SKIPCONV_E_STATE;
+  if (!y) return SKIPCONV_E_INVALID_ARG;
+  if (h->d.act_out == SKIPCONV_ACT_NONE) return fail(h->last_error, SKIPCONV_E_STATE, "no activation output");
+  *y = h->y();
+  return SKIPCONV_OK;
+}
+
+int skipconv_get_desc(skipconv_t h, skipconv_desc* d) {
+  if (!h) return SKIPCONV_E_STATE;
+  if (!d) return SKIPCONV_E_INVALID_ARG;
+  *d = h->d;
+  return SKIPCONV_OK;
+}
+
+static int copy_back(skipconv_t h, void* stream, void* host, const void* dev, size_t bytes) {
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = hipMemcpyAsync(host, dev, bytes, hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return hip_fail(h, e, "copy to host");
+  return SKIPCONV_OK;
+}
+
+int skipconv_active_count(skipconv_t h, void* stream, int64_t* blocks, int64_t* sites) {
+  if (!h) return SKIPCONV_E_STATE;
+  if (h->frames == 0) return fail(h->last_error, SKIPCONV_E_STATE, "no step yet");
+  uint32_t cnt = 0;
+  int rc = copy_back(h, stream, &cnt, h->ctr() + sc::kCtrCount, 4);
+  if (rc) return rc;
+  if (blocks) *blocks = cnt;
+  if (sites) {
+    std::vector<uint8_t> m(h->g.nb);
+    rc = copy_back(h, stream, m.data(), h->bmask(), m.size());
+    if (rc) return rc;
+    const int b = h->d.block;
+    int64_t tot = 0;
+    for (int i = 0; i < h->g.nb; ++i) {
+      if (!m[i]) continue;
+      const int rem = i % (h->g.hb * h->g.wb);
+      const int bi = rem / h->g.wb, bj = rem % h->g.wb;
+      const int ny = std::min(b, h->g.h_out - bi * b), nx = std::min(b, h->g.w_out - bj * b);
+      tot += (int64_t)ny * nx;
+    }
+    *sites = tot;
+  }
+  return SKIPCONV_OK;
+}
+
+int skipconv_copy_block_mask(skipconv_t h, void* stream, uint8_t* host, size_t bytes) {
+  if (!h) return SKIPCONV_E_STATE;
+  if (!host) return SKIPCONV_E_INVALID_ARG;
+  if (bytes < (size_t)h->g.nb) return fail(h->last_error, SKIPCONV_E_SMALL_BUFFER, "block mask buffer too small");
+  return copy_back(h, stream, host, h->bmask(), h->g.nb);
+}
+
+int skipconv_copy_active_list(skipconv_t h, void* stream, uint32_t* host, size_t capacity,
+                              int64_t* count) {
+  if (!h) return SKIPCONV_E_STATE;
+  if (!host || !count) return SKIPCONV_E_INVALID_ARG;
+  uint32_t cnt = 0;
+  int rc = copy_back(h, stream, &cnt, h->ctr() + sc::kCtrCount, 4);
+  if (rc) return rc;
+  *count = cnt;
+  if (capacity < cnt) return fail(h->last_error, SKIPCONV_E_SMALL_BUFFER, "list buffer too small");
+  if (cnt == 0) return SKIPCONV_OK;
+  return copy_back(h, stream, host, h->list(), (size_t)cnt * 4);
+}
+
+int skipconv_copy_site_mask(skipconv_t h, void* stream, uint8_t* host, size_t bytes) {
+  if (!h) return SKIPCONV_E_STATE;
+  if (!(h->d.flags & SKIPCONV_FLAG_KEEP_STATS)) return fail(h->last_error, SKIPCONV_E_STATE, "KEEP_STATS not set");
+  const size_t need = (size_t)h->d.n * h->g.h_out * h->g.w_out;
+  if (!host) return SKIPCONV_E_INVALID_ARG;
+  if (bytes < need) return fail(h->last_error, SKIPCONV_E_SMALL_BUFFER, "site mask buffer too small");
+  return copy_back(h, stream, host, h->smask(), need);
+}
+
+int skipconv_copy_stat(skipconv_t h, void* stream, float* host, size_t bytes) {
+  if (!h) return SKIPCONV_E_STATE;
+  if (!(h->d.flags & SKIPCONV_FLAG_KEEP_STATS)) return fail(h->last_error, SKIPCONV_E_STATE, "KEEP_STATS not set");
+  const size_t need = (size_t)h->d.n * h->g.h_out * h->g.w_out * 4;
+  if (!host) return SKIPCONV_E_INVALID_ARG;
+  if (bytes < need) return fail(h->last_error, SKIPCONV_E_SMALL_BUFFER, "stat buffer too small");
+  return copy_back(h, stream, host, h->stat(), need);
+}
+
+int skipconv_frame_macs(skipconv_t h, void* stream, uint64_t* dense, uint64_t* active) {
+  if (!h) return SKIPCONV_E_STATE;
+  const uint64_t per_site = (uint64_t)h->d.c_out * (h->d.c_in / h->d.groups) * h->d.kernel * h->d.kernel;
+  const uint64_t sites = (uint64_t)h->d.n * h->g.h_out * h->g.w_out;
+  if (dense) *dense = sites * per_site;
+  if (active) {
+    int64_t s = 0;
+    const int rc = skipconv_active_count(h, stream, nullptr, &s);
+    if (rc) return rc;
+    *active = (uint64_t)s * per_site;
+  }
+  return SKIPCONV_OK;
+}
+
+const char* skipconv_status_string(int status) {
+  switch (status) {
+    case SKIPCONV_OK: return "ok";
+    case SKIPCONV_E_INVALID_ARG: return "invalid argument";
+    case SKIPCONV_E_UNSUPPORTED: return "unsupported";
+    case SKIPCONV_E_OOM: return "out of device memory";
+    case SKIPCONV_E_HIP: return "HIP error";
+    case SKIPCONV_E_STATE: return "invalid state";
+    case SKIPCONV_E_SMALL_BUFFER: return "buffer too small";
+    default: return "unknown status";
+  }
+}
+
+const char* skipconv_last_error(skipconv_t h) { return h ? h->last_error : g_create_error; }
+
+int skipconv_timing_begin(skipconv_t h, int frames) {
+  if (!h) return SKIPCONV_E_STATE;
+  if (frames < 0 || frames > (1 << 20)) return SKIPCONV_E_INVALID_ARG;
+  destroy_events(h);
+  h->ev.resize((size_t)frames * 3, nullptr);
+  for (auto& e : h->ev) {
+    const hipError_t r = hipEventCreate(&e);
+    if (r != hipSuccess) {
+      destroy_events(h);
+      return hip_fail(h, r, "hipEventCreate");
+    }
+  }
+  h->timing_frames = frames;
+  h->timing_done = 0;
+  return SKIPCONV_OK;
+}
+
+int skipconv_timing_read(skipconv_t h, void* stream, double* ms, int* frames_timed) {
+  if (!h) return SKIPCONV_E_STATE;
+  if (!ms) return SKIPCONV_E_INVALID_ARG;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return hip_fail(h, e, "sync");
+  ms[0] = ms[1] = 0.0;
+  for (int i = 0; i < h->timing_done; ++i) {
+    float a = 0.f, b = 0.f;
+    e = hipEventElapsedTime(&a, h->ev[3 * i], h->ev[3 * i + 1]);
+    if (e == hipSuccess) e = hipEventElapsedTime(&b, h->ev[3 * i + 1], h->ev[3 * i + 2]);
+    if (e != hipSuccess) return hip_fail(h, e, "hipEventElapsedTime");
+    ms[0] += a;
+    ms[1] += b;
+  }
+  if (frames_timed) *frames_timed = h->timing_done;
+  return SKIPCONV_OK;
+}
+
+}  // extern "C"

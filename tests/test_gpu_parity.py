@@ -1,0 +1,333 @@
+"""GPU parity: the HIP Skip-Conv layer against the CPU oracle, frame by frame.
+
+Gate statistic, site mask, block mask and active list must match bit for bit;
+z must agree within 1e-4 (fp32 layers) or 2e-2 (bf16 layers) normwise after
+every frame, and bit for bit on integer-valued data. Calls go through the C
+ABI (ctypes binding); torch only supplies device memory and the stream.
+"""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import skipconv_oracle as O  # noqa: E402
+from paper_2104_11487_amd import skipconv as S  # noqa: E402
+from paper_2104_11487_amd import synthetic as syn  # noqa: E402
+from parity_util import (compare_frame, eps_for_density, say, to_device,  # noqa: E402
+                         to_host_storage, weight_storage, rel_err, TOL)
+
+pytestmark = pytest.mark.gpu
+
+
+def _layer_pair(w_f32, *, n, h, w, dtype, eps, block, stride=1, pad=-1, groups=1, norm_p=2,
+                support="rf", keep_stats=True, act_out="none", force_dense=False):
+    ws = weight_storage(w_f32, dtype)
+    layer = S.SkipConv(to_device(ws, dtype), n=n, h=h, w=w, stride=stride, pad=pad, groups=groups,
+                       eps=eps, block=block, norm_p=norm_p, support=support, keep_stats=keep_stats,
+                       act_out=act_out, force_dense=force_dense)
+    orc = O.SkipConvOracle(ws, n=n, h=h, w=w, stride=stride, pad=None if pad == -1 else pad,
+                           groups=groups, eps=eps, block=block, norm_p=norm_p, support=support,
+                           dtype=dtype)
+    return layer, orc
+
+
+def run_single(frames, w_f32, *, dtype, eps, block, tag, resets=(), exact_z=False,
+               keep_stats=True, **kw):
+    n, h, w, _ = frames[0].shape
+    layer, orc = _layer_pair(w_f32, n=n, h=h, w=w, dtype=dtype, eps=eps, block=block,
+                             keep_stats=keep_stats, **kw)
+    worst, dens = 0.0, []
+    for t, f in enumerate(frames):
+        if t in resets:
+            layer.reset()
+            orc.reset()
+        xs = syn.to_storage(f, dtype)
+        say(f"[{tag}] frame {t} shape={f.shape} eps={eps:.4g} b={block}")
+        layer.step(to_device(xs, dtype))
+        ref = orc.step(xs)
+        worst = max(worst, compare_frame(layer, ref, dtype, t=t, tag=tag, keep_stats=keep_stats,
+                                         exact_z=exact_z))
+        dens.append(ref["count"] / ref["block_mask"].size)
+    layer.close()
+    return worst, dens
+
+
+def oracle_stats(frames, w_shape, *, dtype, stride=1, pad=None):
+    """Per-frame gate statistics of frames 2.. from the oracle (for eps calibration)."""
+    k = w_shape[2]
+    p = (k - 1) // 2 if pad is None else pad
+    out, prev = [], None
+    for f in frames:
+        x = O.storage_to_f32(syn.to_storage(f, dtype), dtype)
+        if prev is not None:
+            r = O.residual(x, prev)
+            a = O.pixel_stat(r, 2)
+            ho, wo = O.out_size(x.shape[1], k, stride, p), O.out_size(x.shape[2], k, stride, p)
+            out.append(O.support_stat(a, k, stride, p, ho, wo))
+        prev = x
+    return out
+
+
+# ---------------------------------------------------------------- 3x3 fp32 --
+
+@pytest.mark.parametrize("eps", [0.05, 0.0, float("inf")])
+def test_square16_fp32(eps):
+    wl = syn.workloads()["square16"]
+    frames = list(wl.video())
+    worst, dens = run_single(frames, wl.weights()[0], dtype="f32", eps=eps, block=1,
+                             tag=f"square16 eps={eps}")
+    if eps == float("inf"):
+        assert dens[1:] == [0.0] * (len(frames) - 1)
+    if eps == 0.05:
+        assert 0.0 < np.mean(dens[1:]) < 0.5
+
+
+def test_square16_fp32_bench_config():
+    """Same layer with the statistics buffers off, as the benchmark runs it."""
+    wl = syn.workloads()["square16"]
+    frames = list(wl.video())
+    run_single(frames, wl.weights()[0], dtype="f32", eps=0.05, block=1, keep_stats=False,
+               tag="square16 nostats", resets=(5,))
+
+
+# ------------------------------------------------------------ 3x3 64 bf16 --
+
+@pytest.fixture(scope="module")
+def rect64():
+    wl = syn.workloads()["rect64"]
+    frames = list(wl.video(16))
+    stats = oracle_stats(frames, (64, 64, 3, 3), dtype="bf16")
+    return wl, frames, stats
+
+
+@pytest.mark.parametrize("block", [1, 4, 8])
+@pytest.mark.parametrize("density", [0.1, 0.25, 0.5])
+def test_rect64_bf16_density_sweep(rect64, block, density):
+    wl, frames, stats = rect64
+    eps = eps_for_density(stats, block, 128, 96, density)
+    worst, dens = run_single(frames, wl.weights()[0], dtype="bf16", eps=eps, block=block,
+                             tag=f"rect64 b={block} d={density}", keep_stats=(block != 8))
+    assert abs(np.mean(dens[1:]) - density) < 0.1
+
+
+def test_rect64_full_sequence_with_reset(rect64):
+    wl, _, stats = rect64
+    frames = list(wl.video(32))
+    eps = eps_for_density(stats, 8, 128, 96, 0.25)
+    run_single(frames, wl.weights()[0], dtype="bf16", eps=eps, block=8, keep_stats=False,
+               tag="rect64 32 frames", resets=(16,))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("block", [1, 8])
+def test_integer_video_bit_exact(dtype, block):
+    """Integer-valued frames and weights: every product and sum is exact, so z is bit-exact."""
+    rng = np.random.Generator(np.random.PCG64(77))
+    c = 64
+    w = syn.integer_weights(64, c, 3, seed=78)
+    x = rng.integers(0, 8, (1, 128, 96, c)).astype(np.float32)
+    frames = []
+    for t in range(8):
+        x = x.copy()
+        y0 = 10 + 7 * t
+        x[0, y0:y0 + 20, 30:60] = rng.integers(0, 8, (20, 30, c))
+        frames.append(x)
+    run_single(frames, w, dtype=dtype, eps=3.0, block=block, exact_z=True,
+               tag=f"integer {dtype} b={block}")
+
+
+def test_determinism(rect64):
+    wl, frames, stats = rect64
+    eps = eps_for_density(stats, 4, 128, 96, 0.25)
+    outs = []
+    for rep in range(2):
+        ws = weight_storage(wl.weights()[0], "bf16")
+        layer = S.SkipConv(to_device(ws, "bf16"), n=1, h=128, w=96, eps=eps, block=4, keep_stats=True)
+        rec = []
+        for t, f in enumerate(frames[:8]):
+            say(f"[determinism] rep {rep} frame {t}")
+            z = layer.step(to_device(syn.to_storage(f, "bf16"), "bf16"))
+            torch.cuda.synchronize()
+            rec.append((z.cpu().numpy().copy(), layer.active_list(), layer.stat()))
+        outs.append(rec)
+        layer.close()
+    for (za, la, sa), (zb, lb, sb) in zip(*outs):
+        assert np.array_equal(za.view(np.uint32), zb.view(np.uint32))
+        assert np.array_equal(la, lb) and np.array_equal(sa.view(np.uint32), sb.view(np.uint32))
+
+
+def test_nan_frame_and_reset():
+    rng = np.random.Generator(np.random.PCG64(90))
+    c = 32
+    w = syn.he_weights(32, c, 3, seed=91)
+    x0 = rng.random((1, 24, 20, c), dtype=np.float32)
+    x1 = x0.copy()
+    x1[0, 5, 7, 3] = np.nan
+    x2 = rng.random((1, 24, 20, c), dtype=np.float32)
+    for dtype in ("f32", "bf16"):
+        run_single([x0, x1, x2, x2], w, dtype=dtype, eps=1e4, block=1, resets=(2,),
+                   tag=f"nan {dtype}")
+
+
+# ------------------------------------------------- chained layers (teacher) --
+
+def run_chain(frames, weights, specs, *, dtype, act, epss, block, tag, keep_stats=True):
+    """Each layer is compared with an oracle layer fed the GPU's own input for that layer."""
+    n, h, w, _ = frames[0].shape
+    layers, orcs = [], []
+    hh, ww = h, w
+    for i, (wt, sp) in enumerate(zip(weights, specs)):
+        last = i == len(weights) - 1
+        lay, orc = _layer_pair(wt, n=n, h=hh, w=ww, dtype=dtype, eps=epss[i], block=block,
+                               stride=sp.stride, groups=sp.groups, keep_stats=keep_stats,
+                               act_out="none" if last else act)
+        layers.append(lay)
+        orcs.append(orc)
+        hh, ww = lay.h_out, lay.w_out
+    worst = [0.0] * len(layers)
+    for t, f in enumerate(frames):
+        x_dev = to_device(syn.to_storage(f, dtype), dtype)
+        x_host = syn.to_storage(f, dtype)
+        for i, (lay, orc) in enumerate(zip(layers, orcs)):
+            say(f"[{tag}] frame {t} layer {i}")
+            lay.step(x_dev)
+            ref = orc.step(x_host)
+            worst[i] = max(worst[i], compare_frame(lay, ref, dtype, t=t, tag=f"{tag} L{i}",
+                                                   keep_stats=keep_stats))
+            if i + 1 < len(layers):
+                x_dev = lay.activation()
+                torch.cuda.synchronize()
+                x_host = to_host_storage(x_dev, dtype)
+                # the activation output is dtype(act(z)) of the GPU's own z
+                zg = lay._z.cpu().numpy()
+                exp = O.activation_to_storage(zg.astype(np.float64), act, dtype)
+                assert np.array_equal(x_host, exp), f"{tag} L{i}: activation output"
+    for lay in layers:
+        lay.close()
+    return worst
+
+
+def test_mbconv192_pointwise_then_depthwise():
+    wl = syn.workloads()["mbconv192"]
+    frames = list(wl.video(12))
+    ws = wl.weights()
+    run_chain(frames, ws, wl.layers, dtype="bf16", act="identity", epss=[2.0, 1.5], block=8,
+              tag="mbconv192")
+
+
+def test_stack6_relu_strided():
+    wl = syn.workloads()["stack6"]
+    frames = list(wl.video(5))
+    sched = syn.eps_schedule(6) * 0.5
+    run_chain(frames, wl.weights(), wl.layers, dtype="bf16", act="relu", epss=list(sched), block=1,
+              tag="stack6")
+
+
+# --------------------------------------------------- full size, sampled z --
+
+def test_blob128_full_size_sampled():
+    """4 x 512 x 512 x 128 bf16, 16 x 16 blocks: gate outputs in full, z at sampled sites."""
+    wl = syn.workloads()["blob128"]
+    nfr = 3
+    frames = list(wl.video(nfr))
+    w32 = wl.weights()[0]
+    wbits = weight_storage(w32, "bf16")
+    wf = O.bf16_bits_to_f32(wbits).astype(np.float64)
+    stats = oracle_stats(frames[:2], (128, 128, 3, 3), dtype="bf16")
+    eps = eps_for_density(stats, 16, 512, 512, 0.25)
+    layer = S.SkipConv(to_device(wbits, "bf16"), n=4, h=512, w=512, eps=eps, block=16)
+    rng = np.random.Generator(np.random.PCG64(5))
+    ns = 3000
+    sn, si, sj = rng.integers(0, 4, ns), rng.integers(0, 512, ns), rng.integers(0, 512, ns)
+    si[:8] = [0, 0, 511, 511, 255, 256, 0, 511]
+    sj[:8] = [0, 511, 0, 511, 256, 255, 300, 17]
+    z_ref = np.zeros((ns, 128))
+    prev = None
+    for t, f in enumerate(frames):
+        xs = syn.to_storage(f, "bf16")
+        say(f"[blob128] frame {t} eps={eps:.4g}")
+        z = layer.step(to_device(xs, "bf16"))
+        x32 = O.bf16_bits_to_f32(xs)
+        ref = prev is None
+        r = O.residual(x32, np.zeros_like(x32) if ref else prev)
+        s = O.support_stat(O.pixel_stat(r, 2), 3, 1, 1, 512, 512)
+        g = O.gate(s, eps, 2, ref)
+        m_blk = O.block_pool(g, 16)
+        torch.cuda.synchronize()
+        assert np.array_equal(layer.block_mask().astype(bool), m_blk), f"blob128 t={t}: block mask"
+        assert np.array_equal(layer.active_list(), O.active_list(m_blk)), f"blob128 t={t}: list"
+        m = O.block_upsample(m_blk, 16, 512, 512)[sn, si, sj]
+        rp = np.pad(r, ((0, 0), (1, 1), (1, 1), (0, 0)))
+        patches = np.stack([rp[sn, si + kh, sj + kw] for kh in range(3) for kw in range(3)], 1)
+        patches = patches.reshape(ns, 3, 3, 128)
+        u = O.conv_at_sites(O.operand(patches, "bf16"), wf, 1, 0, 1, np.arange(ns),
+                            np.zeros(ns, int), np.zeros(ns, int))
+        if ref:
+            z_ref = u
+        else:
+            z_ref = np.where(m[:, None], z_ref + u, z_ref)
+        zg = z[sn, si, sj].cpu().numpy()
+        e = rel_err(zg, z_ref)
+        say(f"[blob128] frame {t} density={m_blk.mean():.3f} sampled rel err {e:.2e}")
+        assert e <= TOL["bf16"]
+        prev = x32
+    layer.close()
+
+
+# ------------------------------------------------------------- edge cases --
+
+EDGE = [
+    # n, h, w, c_in, c_out, k, stride, pad, groups, block, dtype, norm_p, support
+    (2, 13, 11, 8, 24, 3, 1, -1, 1, 3, "bf16", 2, "rf"),
+    (1, 9, 7, 3, 16, 3, 2, -1, 1, 1, "bf16", 2, "rf"),
+    (1, 10, 10, 32, 32, 5, 1, -1, 1, 4, "bf16", 2, "rf"),
+    (1, 17, 5, 16, 8, 1, 2, -1, 1, 2, "f32", 2, "rf"),
+    (1, 6, 6, 4, 4, 3, 1, 0, 1, 2, "f32", 2, "rf"),
+    (1, 40, 40, 16, 16, 3, 1, -1, 1, 32, "f32", 2, "rf"),
+    (1, 12, 12, 12, 12, 3, 1, -1, 12, 2, "f32", 2, "rf"),
+    (1, 15, 11, 24, 24, 5, 2, -1, 24, 1, "bf16", 2, "rf"),
+    (1, 16, 16, 32, 32, 3, 1, -1, 1, 1, "bf16", 1, "rf"),
+    (1, 16, 16, 32, 32, 3, 2, -1, 1, 2, "bf16", 2, "centre"),
+    (1, 8, 8, 64, 256, 3, 1, -1, 1, 1, "bf16", 2, "rf"),
+    (1, 8, 8, 32, 200, 1, 1, -1, 1, 1, "bf16", 2, "rf"),
+    (1, 1, 1, 8, 16, 1, 1, -1, 1, 1, "f32", 2, "rf"),
+    (3, 20, 36, 40, 48, 3, 1, -1, 1, 5, "bf16", 2, "rf"),
+    (1, 33, 31, 7, 5, 7, 3, -1, 1, 2, "f32", 1, "rf"),
+]
+
+
+@pytest.mark.parametrize("case", EDGE, ids=[f"edge{i}" for i in range(len(EDGE))])
+def test_edge_geometries(case):
+    n, h, w, ci, co, k, s, pad, g, b, dtype, p, sup = case
+    rng = np.random.Generator(np.random.PCG64(1000 + sum(case[:10])))
+    wt = rng.normal(0, (2.0 / (k * k * ci / g)) ** 0.5, (co, ci // g, k, k)).astype(np.float32)
+    x = rng.random((n, h, w, ci), dtype=np.float32)
+    frames = [x]
+    for t in range(4):
+        x = x.copy()
+        y0, x0 = (2 * t) % max(1, h - 2), (3 * t) % max(1, w - 2)
+        x[:, y0:y0 + 3, x0:x0 + 3] = rng.random((n, min(3, h - y0), min(3, w - x0), ci), dtype=np.float32)
+        x += rng.normal(0, 0.003, x.shape).astype(np.float32)
+        frames.append(x)
+    eps = 0.5 if p == 2 else 2.0
+    run_single(frames, wt, dtype=dtype, eps=eps, block=b, stride=s, pad=pad, groups=g, norm_p=p,
+               support=sup, tag=f"edge {case}", resets=(3,))
+
+
+def test_force_dense_equals_eps0_on_changing_frames():
+    """FORCE_DENSE runs every block; on frames that change everywhere that is the eps = 0 layer."""
+    rng = np.random.Generator(np.random.PCG64(2024))
+    w = syn.he_weights(32, 32, 3, seed=7)
+    frames = [rng.random((1, 20, 20, 32), dtype=np.float32) for _ in range(4)]
+    ws = weight_storage(w, "bf16")
+    layer = S.SkipConv(to_device(ws, "bf16"), n=1, h=20, w=20, eps=1e9, block=4, keep_stats=True,
+                       force_dense=True)
+    orc = O.SkipConvOracle(ws, n=1, h=20, w=20, eps=0.0, block=4, dtype="bf16")
+    for t, f in enumerate(frames):
+        xs = syn.to_storage(f, "bf16")
+        say(f"[force_dense] frame {t}")
+        layer.step(to_device(xs, "bf16"))
+        ref = orc.step(xs)
+        assert ref["count"] == ref["block_mask"].size
+        compare_frame(layer, ref, "bf16", t=t, tag="force_dense", keep_stats=True)
+    layer.close()
