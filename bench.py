@@ -1,0 +1,486 @@
+"""Benchmark of the streaming Skip-Conv layer on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload rect64|blob128|square16]
+
+One step = one call of skipconv_step on one batch (the whole hot path: gate
+kernel + sparse convolution kernel) over a frame of the synthetic clip; the
+clip repeats with a reset (dense reference frame) at its first frame. Inputs
+are resident in HBM before the timed region. Prints one JSON line.
+
+Default workload (rect64): 3x3 conv 64 -> 64, bf16 operands with fp32
+accumulation, 128 x 96 frames, batch 1, a 32-frame clip of four moving
+textured rectangles over a static noise background; gate eps calibrated on
+the GPU's own gate statistics to ~25 % block density with 8 x 8 blocks.
+The sweep covers blocks {1, 4, 8} x densities {10, 25, 50 %} plus the same
+kernels forced dense and torch's conv2d (MIOpen) on the same shape.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "Skip-Conv frames/s and active-site TFLOP/s (% MFMA/HBM peak) vs gate density"
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_F32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+
+
+def log(msg: str) -> None:
+    print(msg, file=sys.stderr, flush=True)
+
+
+# --------------------------------------------------------------- workloads --
+
+def load_workload(name: str, frames: int | None):
+    from paper_2104_11487_amd import synthetic as syn
+
+    wl = syn.workloads()[name]
+    nfr = frames or wl.frames
+    t0 = time.time()
+    clip = [syn.to_storage(f, wl.dtype) for f in wl.video(nfr)]
+    log(f"[bench] generated {len(clip)} frames of {wl.name} in {time.time() - t0:.1f}s")
+    return wl, clip
+
+
+def upload(clip, dtype):
+    import torch
+
+    out = []
+    for x in clip:
+        if dtype == "bf16":
+            out.append(torch.from_numpy(x.view(np.int16)).cuda().view(torch.bfloat16))
+        else:
+            out.append(torch.from_numpy(x).cuda())
+    return out
+
+
+def weight_tensor(w32, dtype):
+    import torch
+
+    t = torch.from_numpy(w32).cuda()
+    return t.to(torch.bfloat16) if dtype == "bf16" else t
+
+
+# ------------------------------------------------------------- calibration --
+
+def gpu_stats(layer_kw, wt, frames_dev):
+    """Per-frame gate statistics of frames 2.. from the GPU layer itself (KEEP_STATS)."""
+    from paper_2104_11487_amd.skipconv import SkipConv
+    import torch
+
+    lay = SkipConv(wt, eps=0.0, block=1, keep_stats=True, **layer_kw)
+    stats = []
+    for t, x in enumerate(frames_dev):
+        lay.step(x)
+        if t > 0:
+            torch.cuda.synchronize()
+            stats.append(lay.stat())
+    lay.close()
+    return stats
+
+
+def eps_for_density(stats, block, h_out, w_out, target):
+    vals = []
+    for s in stats:
+        n = s.shape[0]
+        hb, wb = -(-h_out // block), -(-w_out // block)
+        pad = np.full((n, hb * block, wb * block), -np.inf, np.float32)
+        pad[:, :h_out, :w_out] = np.nan_to_num(s, nan=np.inf)
+        vals.append(pad.reshape(n, hb, block, wb, block).max(axis=(2, 4)).reshape(-1))
+    v = np.concatenate(vals).astype(np.float64)
+    return float(np.sqrt(max(float(np.quantile(v, 1.0 - target)), 0.0)))
+
+
+# ------------------------------------------------------------------ timing --
+
+def run_steps(layer, frames_dev, steps, start, *, every=0):
+    """Run `steps` steps from clip position `start` (reset at each clip start).
+
+    With every > 0, HIP events bracket both kernels of every `every`-th step.
+    Returns (wall seconds, gate ms, conv ms, clip positions of the timed steps, next position).
+    """
+    import torch
+    from paper_2104_11487_amd import skipconv as S
+
+    nfr = len(frames_dev)
+    ntimed = (steps + every - 1) // every if every else 0
+    if every:
+        S.skipconv_timing_begin(layer.handle, ntimed, every)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    pos = start
+    for _ in range(steps):
+        if pos % nfr == 0:
+            layer.reset()
+        layer.step(frames_dev[pos % nfr])
+        pos += 1
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gate_ms = conv_ms = 0.0
+    timed_pos = np.zeros(0, np.int64)
+    if every:
+        gate_ms, conv_ms, n, idx = S.skipconv_timing_read(layer.handle, layer._stream(), ntimed)
+        assert n == ntimed, (n, ntimed)
+        timed_pos = (start + idx.astype(np.int64)) % nfr
+        S.skipconv_timing_begin(layer.handle, 0, 1)
+    return wall, gate_ms, conv_ms, timed_pos, pos
+
+
+def clip_active(layer, frames_dev):
+    """Active sites and blocks of every clip position (one pass, reset at frame 0)."""
+    sites, blocks = [], []
+    layer.reset()
+    for x in frames_dev:
+        layer.step(x)
+        b, s = layer.active_count()
+        sites.append(s)
+        blocks.append(b)
+    return np.array(sites, np.int64), np.array(blocks, np.int64)
+
+
+def event_period(nfr: int) -> int:
+    """Sampling period of the per-kernel events, coprime with the clip length."""
+    for e in (5, 7, 11, 13):
+        if np.gcd(e, nfr) == 1:
+            return e
+    return 1
+
+
+def measure_point(make_layer, frames_dev, steps, warmup, geom, *, label, events=True):
+    """Warm up, then time exactly `steps` steps; per-kernel times from HIP events on sampled steps."""
+    layer = make_layer()
+    sites, blocks = clip_active(layer, frames_dev)
+    nfr = len(frames_dev)
+    pos = nfr
+    if warmup:
+        _, _, _, _, pos = run_steps(layer, frames_dev, warmup, pos)
+    pos = (pos + nfr - 1) // nfr * nfr  # timed steps start at a clip boundary
+    every = event_period(nfr) if events else 0
+    wall, gate_ms, conv_ms, tpos, _ = run_steps(layer, frames_dev, steps, pos, every=every)
+    layer.close()
+    idx = np.arange(steps) % nfr
+    act_sites = sites[idx].astype(np.float64)
+    macs_per_site = geom["c_out"] * geom["kk"]
+    flops_active = 2.0 * act_sites.sum() * macs_per_site
+    flops_dense = 2.0 * geom["sites"] * macs_per_site * steps
+    nt = max(len(tpos), 1)
+    # algorithmic work of the timed launches
+    conv_flop = 2.0 * sites[tpos].sum() * macs_per_site / nt
+    xb, nb = geom["x_bytes"], geom["nb"]
+    ref = (tpos == 0)
+    gate_bytes = (np.where(ref, 2 * xb, 3 * xb) + 2 * nb + 4 * blocks[tpos]).sum() / nt
+    gate_us = 1e3 * gate_ms / nt if len(tpos) else None
+    conv_us = 1e3 * conv_ms / nt if len(tpos) else None
+    res = {
+        "label": label,
+        "ms_per_step": 1e3 * wall / steps,
+        "frames_per_s": steps * geom["n"] / wall,
+        "density": float(act_sites.sum() / (geom["sites"] * steps)),
+        "density_steady": float(sites[1:].sum() / (geom["sites"] * (nfr - 1))),
+        "active_tflops": flops_active / wall / 1e12,
+        "dense_equiv_tflops": flops_dense / wall / 1e12,
+        "gate_us": gate_us,
+        "conv_us": conv_us,
+        "timed_launches": int(len(tpos)),
+        "event_period": every,
+        "conv_flop_per_launch": conv_flop,
+        "gate_bytes_per_launch": float(gate_bytes),
+        "conv_active_tflops": conv_flop / (conv_us * 1e-6) / 1e12 if conv_us else None,
+        "gate_gbs": gate_bytes / (gate_us * 1e-6) / 1e9 if gate_us else None,
+    }
+    log(f"[bench] {label}: {res['frames_per_s']:.0f} frames/s, {res['ms_per_step'] * 1e3:.1f} us/step, "
+        f"density {res['density']:.3f}, gate {gate_us or 0:.1f} us, conv {conv_us or 0:.1f} us")
+    return res
+
+
+def torch_dense_us(wt, shape, stride, steps=200):
+    """torch conv2d (MIOpen) of the same shape, channels-last, for context only."""
+    import torch
+    import torch.nn.functional as F
+
+    n, h, w, c = shape
+    x = torch.randn(n, c, h, w, device="cuda", dtype=wt.dtype).contiguous(memory_format=torch.channels_last)
+    k = wt.shape[2]
+    wcl = wt.contiguous(memory_format=torch.channels_last)
+    for _ in range(10):
+        F.conv2d(x, wcl, stride=stride, padding=(k - 1) // 2)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        F.conv2d(x, wcl, stride=stride, padding=(k - 1) // 2)
+    torch.cuda.synchronize()
+    return 1e6 * (time.perf_counter() - t0) / steps
+
+
+# ------------------------------------------------------------ CPU baseline --
+
+def cpu_baseline(wl, clip, w32, eps, block, budget_s=12.0):
+    """The CPU oracle as it stands, single-threaded BLAS, over a bounded sample of the clip."""
+    from threadpoolctl import threadpool_limits
+    from oracle import skipconv_oracle as O
+
+    lay_spec = wl.layers[0]
+    wbits = w32 if wl.dtype == "f32" else O.f32_to_bf16_rne(w32)
+    done, t0 = 0, time.perf_counter()
+    with threadpool_limits(limits=1):
+        orc = O.SkipConvOracle(wbits, n=wl.n, h=wl.h, w=wl.w, stride=lay_spec.stride, eps=eps,
+                               block=block, dtype=wl.dtype)
+        while True:
+            pos = done % len(clip)
+            if pos == 0:
+                orc.reset()
+            orc.step(clip[pos])
+            done += 1
+            el = time.perf_counter() - t0
+            if el >= budget_s and done >= min(len(clip), 4):
+                break
+            if el >= 3 * budget_s:
+                break
+    el = time.perf_counter() - t0
+    return {"value": done * wl.n / el, "unit": "frames/s", "cores": 1, "kind": "oracle",
+            "sample": f"{done} consecutive steps of the same clip ({wl.name}, eps={eps:.4g}, b={block}, "
+                      f"reset every {len(clip)} frames), {el:.1f}s, numpy fp64 with BLAS limited to 1 thread"}
+
+
+# ---------------------------------------------------------------- traffic --
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(os.path.join(ROOT, "paper_2104_11487_amd", "csrc"))):
+        with open(os.path.join(ROOT, "paper_2104_11487_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def profiled_traffic(workload: str, kernel: str):
+    """HBM bytes per launch from a committed rocprofv3 counter summary, if it is current."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_hash") != kernel_source_hash():
+        return None
+    k = rec.get("kernels", {}).get(kernel)
+    return None if k is None else k.get("bytes_per_launch")
+
+
+def summarize_pmc(fetch_db: str, write_db: str, out_json: str, *, workload: str, copy_mib: int):
+    """Average FETCH_SIZE / WRITE_SIZE (KiB per dispatch) per kernel, scaled by a plain copy.
+
+    Inputs are the SQLite databases rocprofv3 writes for one --pmc FETCH_SIZE
+    run and one --pmc WRITE_SIZE run of the same command. The largest
+    device-to-device copy in the run (the --copy-probe of `copy_mib` MiB, which
+    reads and writes exactly that many bytes) gives the bytes per counter unit.
+    """
+    import sqlite3
+
+    def rows(db, counter):
+        con = sqlite3.connect(db)
+        out = con.execute("select kernel_name, value from counters_collection where counter_name = ?",
+                          (counter,)).fetchall()
+        con.close()
+        return out
+
+    fetch, write = rows(fetch_db, "FETCH_SIZE"), rows(write_db, "WRITE_SIZE")
+    copy_bytes = float(copy_mib << 20)
+    is_copy = lambda k: "copyBuffer" in k or ("copy" in k.lower() and "sc::" not in k)
+    cf = max((v for k, v in fetch if is_copy(k)), default=0.0)
+    cw = max((v for k, v in write if is_copy(k)), default=0.0)
+    f_scale = copy_bytes / cf if cf > 0 else None
+    w_scale = copy_bytes / cw if cw > 0 else None
+    kernels = {}
+    for label, pred in (("gate", lambda k: "gate_kernel" in k), ("compact", lambda k: "compact_kernel" in k),
+                        ("conv", lambda k: "conv_" in k and "_kernel" in k),
+                        ("depthwise", lambda k: "depthwise_kernel" in k)):
+        vf = [v for k, v in fetch if pred(k)]
+        vw = [v for k, v in write if pred(k)]
+        names = sorted({k for k, _ in fetch if pred(k)})
+        if not vf or not vw or f_scale is None or w_scale is None:
+            continue
+        af, aw = sum(vf) / len(vf), sum(vw) / len(vw)
+        kernels[label] = {"kernel": names[0] if len(names) == 1 else names, "dispatches": len(vf),
+                          "fetch_kib": af, "write_kib": aw, "fetch_bytes": af * f_scale,
+                          "write_bytes": aw * w_scale, "bytes_per_launch": af * f_scale + aw * w_scale}
+    rec = {"workload": workload, "source_hash": kernel_source_hash(), "copy_mib": copy_mib,
+           "copy_fetch_kib": cf, "copy_write_kib": cw, "fetch_bytes_per_unit": f_scale,
+           "write_bytes_per_unit": w_scale, "kernels": kernels}
+    with open(out_json, "w") as fh:
+        json.dump(rec, fh, indent=1)
+    print(json.dumps(rec, indent=1))
+
+
+def summarize_trace(db: str, out_md: str, command: str) -> None:
+    """Markdown table of per-kernel dispatch counts and durations from a rocprofv3 --kernel-trace database."""
+    import sqlite3
+
+    con = sqlite3.connect(db)
+    rows = con.execute("select name, count(*), sum(duration), avg(duration), min(duration), max(duration) "
+                       "from kernels group by name order by sum(duration) desc").fetchall()
+    con.close()
+    total = sum(r[2] for r in rows) or 1.0
+    lines = [f"# rocprofv3 kernel trace: {os.path.basename(db)}", "", "Command:", "", "```", command, "```", "",
+             "| kernel | calls | total us | avg us | min us | max us | share |",
+             "|---|---:|---:|---:|---:|---:|---:|"]
+    for name, n, tot, avg, mn, mx in rows:
+        short = name.replace("(anonymous namespace)::", "").split("(sc::")[0].split("(unsigned")[0]
+        lines.append(f"| `{short[:90]}` | {n} | {tot / 1e3:.1f} | {avg / 1e3:.2f} | {mn / 1e3:.2f} | "
+                     f"{mx / 1e3:.2f} | {100 * tot / total:.1f}% |")
+    with open(out_md, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+# -------------------------------------------------------------------- main --
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=640)
+    ap.add_argument("--warmup", type=int, default=64)
+    ap.add_argument("--workload", default="rect64", choices=["rect64", "blob128", "square16"])
+    ap.add_argument("--block", type=int, default=None)
+    ap.add_argument("--density", type=float, default=0.25)
+    ap.add_argument("--frames", type=int, default=None)
+    ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-events", action="store_true", help="time without per-kernel events")
+    ap.add_argument("--eps", type=float, default=None,
+                    help="fixed gate threshold (skips calibration; used for counter runs)")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="also run one device-to-device copy of MIB MiB (counter calibration)")
+    ap.add_argument("--summarize-trace", nargs=3, metavar=("TRACE_DB", "OUT_MD", "COMMAND"),
+                    help="write a markdown summary of a rocprofv3 --kernel-trace database")
+    ap.add_argument("--summarize-pmc", nargs=3, metavar=("FETCH_DB", "WRITE_DB", "OUT_JSON"),
+                    help="turn the databases of two rocprofv3 --pmc runs into a traffic summary")
+    args = ap.parse_args()
+    if args.summarize_trace:
+        summarize_trace(*args.summarize_trace)
+        return
+    if args.summarize_pmc:
+        summarize_pmc(*args.summarize_pmc, workload=args.workload, copy_mib=args.copy_probe)
+        return
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the layer runs on a single "
+              "MI355X; independent streams would shard across GPUs with no communication.",
+              file=sys.stderr, flush=True)
+        sys.exit(2)
+
+    import torch
+    from paper_2104_11487_amd import skipconv as S
+    from paper_2104_11487_amd.skipconv import SkipConv
+
+    S.lib()  # fail loudly if the HIP library is missing
+    torch.cuda.set_device(0)
+    wl, clip = load_workload(args.workload, args.frames)
+    frames_dev = upload(clip, wl.dtype)
+    w32 = wl.weights()[0]
+    wt = weight_tensor(w32, wl.dtype)
+    spec = wl.layers[0]
+    block = args.block or wl.block
+    layer_kw = dict(n=wl.n, h=wl.h, w=wl.w, stride=spec.stride, groups=spec.groups)
+    probe = SkipConv(wt, eps=0.0, block=block, **layer_kw)
+    h_out, w_out = probe.h_out, probe.w_out
+    probe.close()
+    kk = spec.k * spec.k * spec.c_in // spec.groups
+    x_bytes = wl.n * wl.h * wl.w * wl.c * (2 if wl.dtype == "bf16" else 4)
+    geom = {"n": wl.n, "sites": wl.n * h_out * w_out, "c_out": spec.c_out, "kk": kk, "x_bytes": x_bytes,
+            "nb": wl.n * (-(-h_out // block)) * (-(-w_out // block))}
+
+    if args.copy_probe:
+        src = torch.empty(args.copy_probe << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+    stats = None if args.eps is not None else gpu_stats(layer_kw, wt, frames_dev)
+
+    def mk(b, eps, dense=False):
+        return lambda: SkipConv(wt, eps=eps, block=b, force_dense=dense, **layer_kw)
+
+    eps_head = args.eps if args.eps is not None else eps_for_density(stats, block, h_out, w_out, args.density)
+    head = measure_point(mk(block, eps_head), frames_dev, args.steps, args.warmup, geom,
+                         label=f"b={block} d={args.density}", events=not args.no_events)
+
+    sweep = []
+    if not args.no_sweep and stats is not None:
+        sweep_steps = max(len(clip) * 2, min(args.steps, 256))
+        for b in ([1, 4, 8] if args.workload != "blob128" else [16]):
+            for d in (0.1, 0.25, 0.5):
+                e = eps_for_density(stats, b, h_out, w_out, d)
+                g2 = dict(geom, nb=wl.n * (-(-h_out // b)) * (-(-w_out // b)))
+                r = measure_point(mk(b, e), frames_dev, sweep_steps, len(clip), g2, label=f"b={b} d={d}")
+                r.update({"block": b, "target_density": d, "eps": e})
+                sweep.append(r)
+        r = measure_point(mk(block, 0.0, dense=True), frames_dev, sweep_steps, len(clip), geom,
+                          label=f"forced dense b={block}")
+        r.update({"block": block, "target_density": 1.0, "forced_dense": True})
+        sweep.append(r)
+        tus = torch_dense_us(wt, (wl.n, wl.h, wl.w, wl.c), spec.stride)
+        sweep.append({"label": "torch conv2d (MIOpen), dense, same shape", "us_per_frame_batch": tus,
+                      "dense_tflops": 2.0 * geom["sites"] * spec.c_out * kk / (tus * 1e-6) / 1e12})
+        log(f"[bench] torch conv2d dense: {tus:.1f} us")
+
+    # roofline of the dominant kernel, from the events of the timed region
+    peak_mfma = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
+    roof = None
+    if head["conv_us"] is not None:
+        if head["conv_us"] >= head["gate_us"]:
+            a = head["conv_active_tflops"]
+            roof = {"kernel": "conv (sparse gather-MFMA)", "bound": "mfma", "achieved": a,
+                    "peak": peak_mfma, "unit": "TFLOP/s", "frac": a / peak_mfma,
+                    "traffic": profiled_traffic(args.workload, "conv"),
+                    "flop_per_launch": head["conv_flop_per_launch"], "us_per_launch": head["conv_us"]}
+        else:
+            a = head["gate_gbs"]
+            roof = {"kernel": "gate (residual, statistic, compaction)", "bound": "hbm", "achieved": a,
+                    "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": a / PEAK_HBM_GBS,
+                    "traffic": profiled_traffic(args.workload, "gate"),
+                    "bytes_per_launch": head["gate_bytes_per_launch"], "us_per_launch": head["gate_us"]}
+
+    cpu = None
+    if not args.no_cpu:
+        cpu = cpu_baseline(wl, clip, w32, eps_head, block)
+        log(f"[bench] cpu oracle: {cpu['value']:.2f} frames/s")
+
+    out = {
+        "metric": METRIC,
+        "value": head["frames_per_s"],
+        "unit": "frames/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": head["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": f"{wl.name}: {spec.k}x{spec.k} conv {spec.c_in}->{spec.c_out} stride {spec.stride}, "
+                        f"{wl.h}x{wl.w} frames, batch {wl.n}, {len(clip)}-frame clip (reset at frame 1), "
+                        f"gate block {block}, eps for ~{args.density:.0%} density",
+            "eps": eps_head, "block": block, "density": head["density"],
+            "density_steady": head["density_steady"],
+            "active_tflops": head["active_tflops"], "dense_equiv_tflops": head["dense_equiv_tflops"],
+            "gate_us": head["gate_us"], "conv_us": head["conv_us"],
+        },
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "sweep": sweep,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -178,12 +178,16 @@ const char* skipconv_status_string(int status);
 const char* skipconv_last_error(skipconv_t h);
 
 /* ---- kernel timing (benchmarks) ----
- * Time the next `frames` steps kernel by kernel with HIP events recorded on
- * the step's stream: on skipconv_timing_read, ms[0] receives the summed
- * milliseconds of the gate kernel and ms[1] of the convolution kernel, over
- * the steps since skipconv_timing_begin (synchronises the stream). */
-int skipconv_timing_begin(skipconv_t h, int frames);
-int skipconv_timing_read(skipconv_t h, void* stream, double* ms, int* frames_timed);
+ * Time kernel by kernel, with HIP events recorded on the step's stream, every
+ * `every`-th step (every >= 1) of the following steps, for up to `frames`
+ * timed steps. skipconv_timing_read (synchronises `stream`) returns in ms[0]
+ * the summed milliseconds of the gate kernel and in ms[1] of the convolution
+ * kernel over the timed steps, and their count; `mask` (may be NULL) receives
+ * for each of them its index among the steps since skipconv_timing_begin.
+ * frames = 0 stops timing. */
+int skipconv_timing_begin(skipconv_t h, int frames, int every);
+int skipconv_timing_read(skipconv_t h, void* stream, double* ms, int* frames_timed,
+                         int32_t* step_index, int capacity);
 
 #ifdef __cplusplus
 }

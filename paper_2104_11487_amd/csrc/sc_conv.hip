@@ -187,6 +187,145 @@ __global__ void __launch_bounds__(kConvThreads) conv_bf16_kernel(ConvParams p) {
   }
 }
 
+// ------------------------------------------------------- bf16, halo ----
+//
+// Block tiles (b in {4, 8, 16, 32, 64}, C_in % 32 == 0): a tile is `tr` output
+// rows x b columns of one active block. Its input halo ((tr-1)s+k rows x
+// (b-1)s+k columns x C_in) is loaded once with 16-byte loads, turned into
+// rho = bf16(x_t - x_{t-1}) and stored in LDS with a pixel stride of
+// 2*C_in + 16 bytes (16 consecutive pixels read 16 bytes each on distinct
+// banks). MFMA A fragments are then read straight from the halo: row m of the
+// tile at tap (kh, kw) is halo pixel (ly*s + kh, lx*s + kw), so no im2col copy
+// is made. Waves are laid out WAVES_M x WAVES_N; each owns WM x WN 16x16
+// output tiles and reads its B fragments from the packed weights (L1/L2).
+
+template <int WAVES_M, int WAVES_N, int WM, int WN>
+__global__ void __launch_bounds__(64 * WAVES_M * WAVES_N) conv_halo_kernel(ConvParams p, HaloParams hp) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t halo[];
+  constexpr int kThreads = 64 * WAVES_M * WAVES_N;
+  constexpr int kUnroll = 4;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave % WAVES_M, wn = wave / WAVES_M;
+  const int r16 = lane & 15, kq = lane >> 4;
+  const int b = p.block, s = p.stride, k = p.k, c = p.c;
+  const int tpb = hp.tiles_per_block;
+  const int ntiles = (int)p.counters[kCtrCount] * tpb;
+  const uint16_t* xt = static_cast<const uint16_t*>(p.x_t);
+  const uint16_t* xp = static_cast<const uint16_t*>(p.x_prev);
+  const bf16x8* wp = static_cast<const bf16x8*>(p.wpack);
+  const int chunks_per_px = c >> 3;
+  const int csteps = c >> 5;  // k-steps per tap
+
+  // halo pixel of this lane's row in each of its M-tiles, before the tap offset
+  int pix_base[WM];
+#pragma unroll
+  for (int i = 0; i < WM; ++i) {
+    const int m = (wm * WM + i) * 16 + r16;
+    const int ly = m / b, lx = m - ly * b;
+    pix_base[i] = ly * s * hp.hw + lx * s;
+  }
+
+  for (TileWalk tw(ntiles); tw.t < tw.end; tw.t += tw.step) {
+    const int j = tw.t / tpb, band = tw.t - j * tpb;
+    const uint32_t blk = p.list[j];
+    const int per_img = p.hb * p.wb;
+    const int n = (int)(blk / per_img);
+    const int rem = (int)(blk - (uint32_t)n * per_img);
+    const int bi = rem / p.wb, bj = rem - bi * p.wb;
+    const int oy0 = bi * b + band * hp.tr, ox0 = bj * b;
+    const int rows_ok = min(hp.tr, p.h_out - oy0), cols_ok = min(b, p.w_out - ox0);
+    const int iy0 = oy0 * s - p.pad, ix0 = ox0 * s - p.pad;
+
+    // ---- halo: rho = bf16(x_t - x_{t-1}), zero outside the frame ----
+    const int total = hp.hh * hp.hw * chunks_per_px;
+    for (int base = 0; base < total; base += kThreads * kUnroll) {
+      float va[kUnroll][8], vb[kUnroll][8];
+      int dst[kUnroll];
+      bool in[kUnroll];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int idx = base + u * kThreads + threadIdx.x;
+        const int px = idx / chunks_per_px, ch = idx - px * chunks_per_px;
+        const int hy = px / hp.hw, hx = px - hy * hp.hw;
+        const int y = iy0 + hy, x = ix0 + hx;
+        in[u] = idx < total && y >= 0 && y < p.h && x >= 0 && x < p.w;
+        dst[u] = idx < total ? px * hp.pstride + ch * 16 : -1;
+        if (in[u]) {
+          const size_t off = ((size_t)(n * p.h + y) * p.w + x) * c + ch * 8;
+          Elem<uint16_t>::load8(xt, off, va[u]);
+          if (!p.reference) Elem<uint16_t>::load8(xp, off, vb[u]);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        if (dst[u] < 0) continue;
+        u32x4 q = {0u, 0u, 0u, 0u};
+        if (in[u]) {
+          float r[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) r[e] = p.reference ? va[u][e] : __fsub_rn(va[u][e], vb[u][e]);
+          q.x = f32_to_bf16(r[0]) | (f32_to_bf16(r[1]) << 16);
+          q.y = f32_to_bf16(r[2]) | (f32_to_bf16(r[3]) << 16);
+          q.z = f32_to_bf16(r[4]) | (f32_to_bf16(r[5]) << 16);
+          q.w = f32_to_bf16(r[6]) | (f32_to_bf16(r[7]) << 16);
+        }
+        *reinterpret_cast<u32x4*>(halo + dst[u]) = q;
+      }
+    }
+    __syncthreads();
+
+    // ---- MFMA over K = (kh, kw, ci) ----
+    floatx4 acc[WM][WN];
+#pragma unroll
+    for (int i = 0; i < WM; ++i)
+#pragma unroll
+      for (int jn = 0; jn < WN; ++jn) acc[i][jn] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+
+    int ks = 0;
+    for (int kh = 0; kh < k; ++kh) {
+      for (int kw = 0; kw < k; ++kw) {
+        const int tap_off = kh * hp.hw + kw;
+        for (int cc = 0; cc < csteps; ++cc, ++ks) {
+          const bf16x8* wk = wp + ((size_t)ks * p.ntiles_n + wn * WN) * 64 + lane;
+          bf16x8 bfr[WN];
+#pragma unroll
+          for (int jn = 0; jn < WN; ++jn) bfr[jn] = wk[jn * 64];
+          const int coff = (cc * 32 + kq * 8) * 2;
+#pragma unroll
+          for (int i = 0; i < WM; ++i) {
+            const bf16x8 a =
+                *reinterpret_cast<const bf16x8*>(halo + (pix_base[i] + tap_off) * hp.pstride + coff);
+#pragma unroll
+            for (int jn = 0; jn < WN; ++jn)
+              acc[i][jn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bfr[jn], acc[i][jn], 0, 0, 0);
+          }
+        }
+      }
+    }
+
+    // ---- epilogue: z (+)= acc at the tile's sites inside the output grid ----
+#pragma unroll
+    for (int i = 0; i < WM; ++i) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int m = (wm * WM + i) * 16 + kq * 4 + v;
+        const int ly = m / b, lx = m - ly * b;
+        if (ly >= rows_ok || lx >= cols_ok) continue;
+        const size_t zrow = ((size_t)(n * p.h_out + oy0 + ly) * p.w_out + ox0 + lx) * p.c_out;
+#pragma unroll
+        for (int jn = 0; jn < WN; ++jn) {
+          const int col = (wn * WN + jn) * 16 + r16;
+          if (col >= p.c_out) continue;
+          const float nv = p.reference ? acc[i][jn][v] : p.z[zrow + col] + acc[i][jn][v];
+          p.z[zrow + col] = nv;
+          if (p.act) store_y<uint16_t>(p.y, zrow + col, activate(nv, p.act));
+        }
+      }
+    }
+    __syncthreads();  // the next tile overwrites the halo
+  }
+}
+
 // ---------------------------------------------------------------- fp32 ----
 
 template <int NTN>
@@ -377,11 +516,90 @@ hipError_t launch_conv_f32(const ConvParams& p, int grid, hipStream_t st) {
   return hipGetLastError();
 }
 
+template <int WAVES_M, int WAVES_N, int WM, int WN>
+hipError_t launch_halo_t(const ConvParams& p, const HaloParams& hp, int grid, hipStream_t st) {
+  auto fn = conv_halo_kernel<WAVES_M, WAVES_N, WM, WN>;
+  if (hp.lds_bytes > 64 * 1024) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, hp.lds_bytes);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(fn, dim3(grid), dim3(64 * WAVES_M * WAVES_N), hp.lds_bytes, st, p, hp);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_conv(const ConvParams& p, int dtype, bool fast, int grid, hipStream_t st) {
   if (dtype == 0) return launch_conv_f32(p, grid, st);
   return fast ? launch_conv_bf16<true>(p, grid, st) : launch_conv_bf16<false>(p, grid, st);
+}
+
+namespace {
+template <int WAVES_M, int WAVES_N, int WM, int WN>
+int halo_occ_t(const HaloParams& hp) {
+  auto fn = conv_halo_kernel<WAVES_M, WAVES_N, WM, WN>;
+  if (hp.lds_bytes > 64 * 1024 &&
+      hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
+                          hp.lds_bytes) != hipSuccess)
+    return 0;
+  int blocks = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, fn, 64 * WAVES_M * WAVES_N, hp.lds_bytes) !=
+      hipSuccess)
+    return 0;
+  return blocks;
+}
+}  // namespace
+
+int conv_halo_occupancy(const HaloParams& hp) {
+  switch (hp.config) {
+    case 0: return halo_occ_t<2, 1, 4, 1>(hp);
+    case 1: return halo_occ_t<2, 1, 4, 2>(hp);
+    case 2: return halo_occ_t<2, 1, 4, 4>(hp);
+    case 3: return halo_occ_t<2, 1, 4, 8>(hp);
+    case 4: return halo_occ_t<4, 1, 2, 12>(hp);
+    case 5: return halo_occ_t<4, 1, 2, 16>(hp);
+    case 10: return halo_occ_t<4, 1, 1, 1>(hp);
+    case 11: return halo_occ_t<4, 1, 1, 2>(hp);
+    case 12: return halo_occ_t<4, 1, 1, 4>(hp);
+    case 13: return halo_occ_t<4, 1, 1, 8>(hp);
+    case 14: return halo_occ_t<4, 1, 1, 12>(hp);
+    case 15: return halo_occ_t<4, 1, 1, 16>(hp);
+    case 20: return halo_occ_t<1, 1, 1, 1>(hp);
+    case 21: return halo_occ_t<1, 2, 1, 1>(hp);
+    case 22: return halo_occ_t<1, 4, 1, 1>(hp);
+    case 23: return halo_occ_t<1, 4, 1, 2>(hp);
+    case 24: return halo_occ_t<1, 4, 1, 3>(hp);
+    case 25: return halo_occ_t<1, 4, 1, 4>(hp);
+    default: return 0;
+  }
+}
+
+hipError_t launch_conv_halo(const ConvParams& p, const HaloParams& hp, int grid, hipStream_t st) {
+  switch (hp.config) {
+    // 2 x 1 waves, 4 x WN tiles each: 128-site tiles (b >= 16)
+    case 0: return launch_halo_t<2, 1, 4, 1>(p, hp, grid, st);
+    case 1: return launch_halo_t<2, 1, 4, 2>(p, hp, grid, st);
+    case 2: return launch_halo_t<2, 1, 4, 4>(p, hp, grid, st);
+    case 3: return launch_halo_t<2, 1, 4, 8>(p, hp, grid, st);
+    case 4: return launch_halo_t<4, 1, 2, 12>(p, hp, grid, st);
+    case 5: return launch_halo_t<4, 1, 2, 16>(p, hp, grid, st);
+    // 4 x 1 waves, 1 x WN tiles each: 64-site tiles (b = 8)
+    case 10: return launch_halo_t<4, 1, 1, 1>(p, hp, grid, st);
+    case 11: return launch_halo_t<4, 1, 1, 2>(p, hp, grid, st);
+    case 12: return launch_halo_t<4, 1, 1, 4>(p, hp, grid, st);
+    case 13: return launch_halo_t<4, 1, 1, 8>(p, hp, grid, st);
+    case 14: return launch_halo_t<4, 1, 1, 12>(p, hp, grid, st);
+    case 15: return launch_halo_t<4, 1, 1, 16>(p, hp, grid, st);
+    // 1 x WAVES_N waves: 16-site tiles (b = 4)
+    case 20: return launch_halo_t<1, 1, 1, 1>(p, hp, grid, st);
+    case 21: return launch_halo_t<1, 2, 1, 1>(p, hp, grid, st);
+    case 22: return launch_halo_t<1, 4, 1, 1>(p, hp, grid, st);
+    case 23: return launch_halo_t<1, 4, 1, 2>(p, hp, grid, st);
+    case 24: return launch_halo_t<1, 4, 1, 3>(p, hp, grid, st);
+    case 25: return launch_halo_t<1, 4, 1, 4>(p, hp, grid, st);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_depthwise(const ConvParams& p, int dtype, int grid, hipStream_t st) {

@@ -14,14 +14,15 @@
 // (kh, kw) in row-major order, in fp32; the threshold comparison in fp64.
 //
 // One workgroup owns a TS x TS tile of output sites (whole blocks). It loads
-// the input halo of its tile row by row with coalesced 16-byte loads,
-// squares the residual into an LDS staging area laid out [pixel][channel],
-// and then one thread per halo pixel sums its channels in order. Input pixels
+// the input halo of its tile in batches of rows with coalesced 16-byte loads
+// (several in flight per thread), squares the residual into an LDS staging
+// area laid out [pixel][channel] with 16-byte aligned pixel rows, and then one
+// thread per halo pixel sums its channels in order, four per LDS read. Input pixels
 // the tile owns are copied into the spare x_{t-1} slot on the way (ping-pong:
 // the slot being read is never written in the same step). Every workgroup
-// then writes its block flags; the last workgroup to finish (device-scope
-// counter) scans all block flags in index order and writes the active list
-// and its length. That counter is returned to zero by the same workgroup.
+// then writes its block flags. A second, one-workgroup kernel scans all
+// block flags in index order and writes the active list and its length (a
+// kernel boundary, rather than a device-wide counter, orders the two).
 #include "sc_device.h"
 #include "sc_kernels.h"
 
@@ -32,18 +33,57 @@ namespace sc {
 namespace {
 
 constexpr int kGateThreads = 256;
-
-// Sum of the staged per-channel terms of one pixel, ascending channel order.
-__device__ __forceinline__ float sum_channels(const float* row, int c) {
-  float acc = 0.0f;
-  for (int i = 0; i < c; ++i) acc = add_rn(acc, row[i]);
-  return acc;
-}
+constexpr int kUnroll = 4;  // staging chunks whose loads are issued together
 
 __device__ __forceinline__ float term(float r, int norm_p) {
   return norm_p == 2 ? mul_rn(r, r) : fabsf(r);
 }
 
+// Sum of the staged per-channel terms of one pixel, ascending channel order.
+// Rows are 16-byte aligned when c % 4 == 0, so four terms come per LDS read;
+// the additions stay strictly sequential.
+__device__ __forceinline__ float sum_channels(const float* row, int c) {
+  float acc = 0.0f;
+  if ((c & 3) == 0) {
+    const float4* r4 = reinterpret_cast<const float4*>(row);
+    for (int i = 0; i < (c >> 2); ++i) {
+      const float4 v = r4[i];
+      acc = add_rn(acc, v.x);
+      acc = add_rn(acc, v.y);
+      acc = add_rn(acc, v.z);
+      acc = add_rn(acc, v.w);
+    }
+  } else {
+    for (int i = 0; i < c; ++i) acc = add_rn(acc, row[i]);
+  }
+  return acc;
+}
+
+template <typename T, int VEC>
+__device__ __forceinline__ void load_vec(const T* p, size_t off, float* v) {
+  if (VEC == 8) {
+    Elem<T>::load8(p, off, v);
+  } else if (VEC == 4) {
+    Elem<T>::load4(p, off, v);
+  } else {
+    v[0] = Elem<T>::load1(p, off);
+  }
+}
+
+template <typename T, int VEC>
+__device__ __forceinline__ void copy_vec(T* dst, const T* src, size_t off) {
+  if (VEC * sizeof(T) == 16) {
+    *reinterpret_cast<uint4*>(dst + off) = *reinterpret_cast<const uint4*>(src + off);
+  } else if (VEC * sizeof(T) == 8) {
+    *reinterpret_cast<uint2*>(dst + off) = *reinterpret_cast<const uint2*>(src + off);
+  } else {
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) dst[off + j] = src[off + j];
+  }
+}
+
+// Stage the per-channel terms of `rows` halo rows into LDS ([pixel][channel],
+// cs floats per pixel). Loads of kUnroll chunks are issued before any is used.
 template <typename T, int VEC>
 __device__ void stage_rows(const GateParams& p, int n, int hb0, int rows, int iy0, int ix0, int hw,
                            int xs, int xe, int own_y0, int own_y1, int own_x0, int own_x1,
@@ -54,61 +94,72 @@ __device__ void stage_rows(const GateParams& p, int n, int hb0, int rows, int iy
   const int c = p.c;
   const int nchunk = (xe - xs) * c / VEC;
   const int total = rows * nchunk;
-  for (int idx = threadIdx.x; idx < total; idx += kGateThreads) {
-    const int row = idx / nchunk;
-    const int ch = idx - row * nchunk;
-    const int y = iy0 + hb0 + row;
-    if (y < 0 || y >= p.h) continue;
-    const int e = ch * VEC;
-    const int px = e / c;
-    const int ci = e - px * c;
-    const int x = xs + px;
-    const size_t off = ((size_t)(n * p.h + y) * p.w + x) * c + ci;
-    float vt[VEC], vp[VEC];
-    if (VEC == 8) {
-      Elem<T>::load8(xt, off, vt);
-    } else if (VEC == 4) {
-      Elem<T>::load4(xt, off, vt);
-    } else {
-      vt[0] = Elem<T>::load1(xt, off);
-    }
-    if (p.reference) {
+  for (int base = 0; base < total; base += kGateThreads * kUnroll) {
+    float vt[kUnroll][VEC], vp[kUnroll][VEC];
+    size_t off[kUnroll];
+    int dst[kUnroll];
+    bool valid[kUnroll], own[kUnroll];
 #pragma unroll
-      for (int j = 0; j < VEC; ++j) vp[j] = 0.0f;
-    } else if (VEC == 8) {
-      Elem<T>::load8(xp, off, vp);
-    } else if (VEC == 4) {
-      Elem<T>::load4(xp, off, vp);
-    } else {
-      vp[0] = Elem<T>::load1(xp, off);
-    }
-    float* dst = stage + (size_t)(row * hw + (x - ix0)) * cs + ci;
+    for (int u = 0; u < kUnroll; ++u) {
+      const int idx = base + u * kGateThreads + threadIdx.x;
+      const int row = idx / nchunk;
+      const int ch = idx - row * nchunk;
+      const int y = iy0 + hb0 + row;
+      valid[u] = idx < total && y >= 0 && y < p.h;
+      const int e = ch * VEC;
+      const int px = e / c;
+      const int ci = e - px * c;
+      const int x = xs + px;
+      off[u] = valid[u] ? ((size_t)(n * p.h + y) * p.w + x) * c + ci : 0;
+      dst[u] = (row * hw + (x - ix0)) * cs + ci;
+      own[u] = copy_in_halo && y >= own_y0 && y < own_y1 && x >= own_x0 && x < own_x1;
+      if (valid[u]) {
+        load_vec<T, VEC>(xt, off[u], vt[u]);
+        if (p.reference) {
 #pragma unroll
-    for (int j = 0; j < VEC; ++j) dst[j] = term(__fsub_rn(vt[j], vp[j]), p.norm_p);
-    if (copy_in_halo && y >= own_y0 && y < own_y1 && x >= own_x0 && x < own_x1) {
-      // copy the raw elements of x_t into the spare slot
-      if (VEC * sizeof(T) == 16) {
-        *reinterpret_cast<uint4*>(keep + off) = *reinterpret_cast<const uint4*>(xt + off);
-      } else if (VEC * sizeof(T) == 8) {
-        *reinterpret_cast<uint2*>(keep + off) = *reinterpret_cast<const uint2*>(xt + off);
-      } else {
-#pragma unroll
-        for (int j = 0; j < VEC; ++j) keep[off + j] = xt[off + j];
+          for (int j = 0; j < VEC; ++j) vp[u][j] = 0.0f;
+        } else {
+          load_vec<T, VEC>(xp, off[u], vp[u]);
+        }
       }
     }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      if (!valid[u]) continue;
+      float tv[VEC];
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) tv[j] = term(__fsub_rn(vt[u][j], vp[u][j]), p.norm_p);
+      float* d = stage + dst[u];
+      if (VEC % 4 == 0) {
+#pragma unroll
+        for (int j = 0; j < VEC; j += 4)
+          *reinterpret_cast<float4*>(d + j) = make_float4(tv[j], tv[j + 1], tv[j + 2], tv[j + 3]);
+      } else {
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) d[j] = tv[j];
+      }
+      if (own[u]) copy_vec<T, VEC>(keep, xt, off[u]);
+    }
   }
+}
+
+// Workgroup b runs tile remap(b): XCD b % 8 (workgroups go to the XCDs
+// round-robin) receives a contiguous range of tiles, so neighbouring tiles
+// share their halo rows through one L2.
+__device__ __forceinline__ int xcd_tile(int b, int g) {
+  const int per = g >> 3, rem = g & 7, x = b & 7;
+  return x * per + min(x, rem) + (b >> 3);
 }
 
 template <typename T, int VEC>
 __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
   extern __shared__ float lds[];
   __shared__ uint32_t blk_flag[kMaxTileBlocks];
-  __shared__ uint32_t scan_buf[kGateThreads];
-  __shared__ int is_last;
 
+  const int tile = xcd_tile(blockIdx.x, gridDim.x);
   const int tiles_per_img = p.tiles_y * p.tiles_x;
-  const int n = blockIdx.x / tiles_per_img;
-  const int trem = blockIdx.x - n * tiles_per_img;
+  const int n = tile / tiles_per_img;
+  const int trem = tile - n * tiles_per_img;
   const int ty = trem / p.tiles_x;
   const int tx = trem - ty * p.tiles_x;
   const int oy0 = ty * p.ts, ox0 = tx * p.ts;
@@ -122,8 +173,8 @@ __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
   const int own_y1 = (ty == p.tiles_y - 1) ? p.h : min(p.h, (oy0 + p.ts) * s);
   const int own_x1 = (tx == p.tiles_x - 1) ? p.w : min(p.w, (ox0 + p.ts) * s);
 
-  float* a_halo = lds;                       // hh * hw
-  float* stage = lds + p.halo_floats;        // rows_per_batch * hw * cs
+  float* a_halo = lds;                 // hh * hw
+  float* stage = lds + p.halo_floats;  // rows_per_batch * hw * cs (16-byte aligned)
   const int cs = p.stage_stride;
 
   const int tb_w = p.ts / p.block;
@@ -187,38 +238,58 @@ __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
     p.block_mask[((size_t)n * p.hb + bi0 + by) * p.wb + bj0 + bx] = (uint8_t)blk_flag[by * tb_w + bx];
   }
 
-  // completion: the last workgroup compacts the block mask in index order
-  __threadfence();
+}
+
+// Ordered compaction (one workgroup of kScanThreads): each thread takes a
+// contiguous run of 16-byte words of block flags (bytes 0/1, the buffer is
+// zero-padded to whole words), counts them, the workgroup scans the counts,
+// and every thread writes the indices of its active blocks in ascending order.
+constexpr int kScanThreads = 1024;
+
+__global__ void __launch_bounds__(kScanThreads) compact_kernel(const uint8_t* block_mask, int nb,
+                                                               uint32_t* list, uint32_t* counters) {
+  __shared__ uint32_t wave_sum[kScanThreads / 64];
+  const int nwords = (nb + 15) >> 4;
+  const int per = (nwords + kScanThreads - 1) / kScanThreads;
+  const int w0 = min(nwords, (int)threadIdx.x * per), w1 = min(nwords, w0 + per);
+  const uint4* bm4 = reinterpret_cast<const uint4*>(block_mask);
+  uint32_t cnt = 0;
+  for (int i = w0; i < w1; ++i) {
+    const uint4 v = bm4[i];
+    cnt += __popc(v.x) + __popc(v.y) + __popc(v.z) + __popc(v.w);
+  }
+  // inclusive scan: within the wave by shuffles, then over the wave totals
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  uint32_t incl = cnt;
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t v = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += v;
+  }
+  if (lane == 63) wave_sum[wave] = incl;
   __syncthreads();
   if (threadIdx.x == 0) {
-    const uint32_t prev = atomicAdd(&p.counters[kCtrDone], 1u);
-    is_last = (prev == gridDim.x - 1) ? 1 : 0;
+    uint32_t run = 0;
+    for (int i = 0; i < kScanThreads / 64; ++i) {
+      const uint32_t v = wave_sum[i];
+      wave_sum[i] = run;
+      run += v;
+    }
+    counters[kCtrCount] = run;
   }
   __syncthreads();
-  if (!is_last) return;
-  __threadfence();
-
-  const int nb = p.n * p.hb * p.wb;
-  const int per = (nb + kGateThreads - 1) / kGateThreads;
-  const int b0 = min(nb, (int)threadIdx.x * per), b1 = min(nb, b0 + per);
-  const volatile uint8_t* bm = p.block_mask;
-  uint32_t cnt = 0;
-  for (int i = b0; i < b1; ++i) cnt += bm[i] ? 1u : 0u;
-  scan_buf[threadIdx.x] = cnt;
-  __syncthreads();
-  // inclusive scan over the 256 per-thread counts (Hillis-Steele)
-  for (int off = 1; off < kGateThreads; off <<= 1) {
-    uint32_t v = (threadIdx.x >= (unsigned)off) ? scan_buf[threadIdx.x - off] : 0u;
-    __syncthreads();
-    scan_buf[threadIdx.x] += v;
-    __syncthreads();
-  }
-  uint32_t pos = scan_buf[threadIdx.x] - cnt;
-  for (int i = b0; i < b1; ++i)
-    if (bm[i]) p.list[pos++] = (uint32_t)i;
-  if (threadIdx.x == kGateThreads - 1) {
-    p.counters[kCtrCount] = scan_buf[kGateThreads - 1];
-    p.counters[kCtrDone] = 0u;
+  uint32_t pos = wave_sum[wave] + incl - cnt;
+  for (int i = w0; i < w1; ++i) {
+    const uint4 v = bm4[i];
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      uint32_t bits = w[q];
+      while (bits) {
+        const int bit = __ffs(bits) - 1;  // flags are 0/1: set bits sit at 0, 8, 16, 24
+        list[pos++] = (uint32_t)(i * 16 + q * 4 + (bit >> 3));
+        bits &= bits - 1;
+      }
+    }
   }
 }
 
@@ -227,6 +298,12 @@ __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
 template <typename T, int VEC>
 static hipError_t launch_gate_t(const GateParams& p, int grid, size_t lds_bytes, hipStream_t st) {
   hipLaunchKernelGGL((gate_kernel<T, VEC>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_compact(const uint8_t* block_mask, int nb, uint32_t* list, uint32_t* counters,
+                          hipStream_t st) {
+  hipLaunchKernelGGL(compact_kernel, dim3(1), dim3(kScanThreads), 0, st, block_mask, nb, list, counters);
   return hipGetLastError();
 }
 

@@ -8,7 +8,7 @@ namespace sc {
 
 // counters[] slots in the workspace
 constexpr int kCtrCount = 0;  // active blocks of the last gate pass
-constexpr int kCtrDone = 1;   // gate workgroups finished (returned to 0 by the last one)
+constexpr int kCtrSpare = 1;
 constexpr int kNumCounters = 16;
 
 constexpr int kMaxTileBlocks = 256;  // blocks per gate tile: (ts / b)^2 <= 256
@@ -51,9 +51,25 @@ struct ConvParams {
   int act;                      // 0 none, 1 identity, 2 relu
 };
 
+// Block-halo variant of the dense bf16 convolution (see sc_conv.hip).
+struct HaloParams {
+  int config;            // wave layout / tile shape instantiation
+  int tr;                // output rows per tile (tile = tr x block sites)
+  int tiles_per_block;   // block / tr
+  int hh, hw;            // halo rows and columns: (tr-1)*s+k, (block-1)*s+k
+  int pstride;           // LDS bytes per halo pixel: 2*c_in + 16
+  int lds_bytes;         // hh * hw * pstride
+  int threads;           // workgroup size
+};
+
 hipError_t launch_gate(const GateParams& p, int dtype, int vec, int grid, size_t lds_bytes,
                        hipStream_t st);
+// Ordered compaction of the block flags into the active list and its count.
+hipError_t launch_compact(const uint8_t* block_mask, int nb, uint32_t* list, uint32_t* counters,
+                          hipStream_t st);
 hipError_t launch_conv(const ConvParams& p, int dtype, bool fast, int grid, hipStream_t st);
+hipError_t launch_conv_halo(const ConvParams& p, const HaloParams& hp, int grid, hipStream_t st);
+int conv_halo_occupancy(const HaloParams& hp);  // resident workgroups per CU (0 on error)
 hipError_t launch_depthwise(const ConvParams& p, int dtype, int grid, hipStream_t st);
 
 // One-time weight repacks (create time).

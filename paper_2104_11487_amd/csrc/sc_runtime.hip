@@ -19,8 +19,9 @@ thread_local char g_create_error[256] = "";
 
 constexpr size_t kAlign = 256;
 constexpr size_t kLdsLimit = 60 * 1024;  // dynamic; the gate kernel adds 2 KB static
-constexpr size_t kStageBudget = 48 * 1024;
+constexpr size_t kStageBudget = 36 * 1024;
 constexpr int kMaxCout = 256;
+constexpr long kHaloLdsLimit = 160 * 1024;  // LDS of one gfx950 CU
 
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
@@ -33,6 +34,8 @@ struct Geometry {
   bool depthwise;
   int kk, ksteps, ntn;  // dense: K, k-steps, 16-wide output tiles (padded to an instantiated count)
   bool fast;
+  bool halo;            // dense bf16 block-halo kernel (else the gather kernel)
+  sc::HaloParams hp;
   int vec;              // gate load width (elements)
   size_t elem;
   size_t off_wpack, off_slot0, off_slot1, off_z, off_y, off_bmask, off_list, off_ctr, off_stat,
@@ -104,17 +107,25 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
   G.depthwise = depthwise;
   G.elem = d->dtype == SKIPCONV_BF16 ? 2 : 4;
 
-  // gate tiling: ts x ts output sites, whole blocks, about 16 x 16 sites
-  G.ts = b <= 16 ? b * (16 / b) : b;
+  // gate tiling: ts x ts output sites made of whole blocks, about 16 x 16
+  // sites, or 8 x 8 when 16 x 16 tiles would not give every CU two tiles
+  {
+    const int t16 = b <= 16 ? b * (16 / b) : b;
+    const long n16 = (long)d->n * ((G.h_out + t16 - 1) / t16) * ((G.w_out + t16 - 1) / t16);
+    G.ts = (n16 < 512 && b <= 8) ? b * (8 / b) : t16;
+  }
   G.tiles_y = (G.h_out + G.ts - 1) / G.ts;
   G.tiles_x = (G.w_out + G.ts - 1) / G.ts;
   G.gate_grid = d->n * G.tiles_y * G.tiles_x;
   G.hh_max = (G.ts - 1) * s + k;
   G.hw_max = G.hh_max;
   G.halo_floats = G.hh_max * G.hw_max;
-  G.stage_stride = d->c_in | 1;
+  // staged pixel rows: 16-byte aligned (+4 floats keeps 16 lanes' float4 reads
+  // on distinct banks) when c_in % 4 == 0, else an odd stride
+  G.stage_stride = (d->c_in % 4 == 0) ? d->c_in + 4 : (d->c_in | 1);
   const size_t row_bytes = (size_t)G.hw_max * G.stage_stride * 4;
   G.rows_per_batch = (int)std::max<size_t>(1, std::min<size_t>(kStageBudget / row_bytes, G.hh_max));
+  G.halo_floats = (G.halo_floats + 3) / 4 * 4;  // staging area starts 16-byte aligned
   G.gate_lds = ((size_t)G.halo_floats + (size_t)G.rows_per_batch * G.hw_max * G.stage_stride) * 4;
   if (G.gate_lds > kLdsLimit)
     return fail(err, SKIPCONV_E_UNSUPPORTED, "gate tile does not fit in LDS (too many channels)");
@@ -151,6 +162,39 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
   }
   G.conv_max_tiles = (int)(((long)G.nb * b * b + 63) / 64);
 
+  // block-halo kernel: tile = tr rows x b columns of a block, chosen per wave layout
+  G.halo = false;
+  if (!depthwise && d->dtype == SKIPCONV_BF16 && d->c_in % 32 == 0 &&
+      (b == 4 || b == 8 || b == 16 || b == 32 || b == 64)) {
+    static const int ntns[] = {1, 2, 4, 8, 12, 16};
+    int ni = 0;
+    while (ntns[ni] != G.ntn) ++ni;
+    sc::HaloParams& H = G.hp;
+    if (b >= 16) {
+      H.tr = 128 / b;
+      H.config = ni;                 // 0..5
+      H.threads = G.ntn <= 8 ? 128 : 256;
+    } else if (b == 8) {
+      H.tr = 8;
+      H.config = 10 + ni;
+      H.threads = 256;
+    } else {
+      H.tr = 4;
+      H.config = 20 + ni;
+      H.threads = G.ntn == 1 ? 64 : (G.ntn == 2 ? 128 : 256);
+    }
+    H.tiles_per_block = b / H.tr;
+    H.hh = (H.tr - 1) * s + k;
+    H.hw = (b - 1) * s + k;
+    H.pstride = 2 * d->c_in + 16;
+    const long lds = (long)H.hh * H.hw * H.pstride;
+    if (lds <= kHaloLdsLimit) {
+      H.lds_bytes = (int)lds;
+      G.halo = true;
+      G.conv_max_tiles = G.nb * H.tiles_per_block;
+    }
+  }
+
   G.x_bytes = (size_t)xel * G.elem;
   G.z_bytes = (size_t)sites * d->c_out * 4;
   size_t off = 0;
@@ -160,7 +204,7 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
   G.off_z = off; off = align_up(off + G.z_bytes);
   G.off_y = off;
   if (d->act_out != SKIPCONV_ACT_NONE) off = align_up(off + (size_t)sites * d->c_out * G.elem);
-  G.off_bmask = off; off = align_up(off + (size_t)nb);
+  G.off_bmask = off; off = align_up(off + (size_t)nb + 16);  // zero padding to whole 16-byte words
   G.off_list = off; off = align_up(off + (size_t)nb * 4);
   G.off_ctr = off; off = align_up(off + sc::kNumCounters * 4);
   G.off_stat = off;
@@ -181,6 +225,7 @@ struct skipconv_layer {
   Geometry g;
   int device = 0;
   int num_cu = 256;
+  int conv_occ = 4;          // resident conv workgroups per CU
   char* ws = nullptr;
   bool owns_ws = false;
   int cur = 0;               // slot holding x_{t-1}
@@ -189,7 +234,8 @@ struct skipconv_layer {
   char last_error[256] = "";
   // timing
   std::vector<hipEvent_t> ev;
-  int timing_frames = 0, timing_done = 0;
+  std::vector<int32_t> ev_step;
+  int timing_frames = 0, timing_done = 0, timing_every = 1, timing_seen = 0;
 
   void* wpack() { return ws + g.off_wpack; }
   void* slot(int i) { return ws + (i ? g.off_slot1 : g.off_slot0); }
@@ -215,7 +261,7 @@ double threshold(const skipconv_desc& d) {
 }
 
 int conv_grid(const skipconv_layer* h) {
-  int grid = std::min(h->g.conv_max_tiles, h->num_cu * 4);
+  int grid = std::min(h->g.conv_max_tiles, h->num_cu * h->conv_occ);
   if (grid >= 8) grid = (grid + 7) / 8 * 8;
   return std::max(grid, 1);
 }
@@ -223,7 +269,9 @@ int conv_grid(const skipconv_layer* h) {
 void destroy_events(skipconv_layer* h) {
   for (hipEvent_t e : h->ev) (void)hipEventDestroy(e);
   h->ev.clear();
-  h->timing_frames = h->timing_done = 0;
+  h->ev_step.clear();
+  h->timing_frames = h->timing_done = h->timing_seen = 0;
+  h->timing_every = 1;
 }
 
 }  // namespace
@@ -300,6 +348,16 @@ int skipconv_create(const skipconv_desc* d, const void* weights, void* workspace
     delete h;
     return SKIPCONV_E_HIP;
   }
+  if (g.halo) {
+    int max_lds = 0;
+    if (hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, h->device) != hipSuccess ||
+        max_lds < g.hp.lds_bytes) {
+      h->g.halo = false;  // this device cannot hold the halo: gather kernel
+      h->g.conv_max_tiles = (int)(((long)g.nb * d->block * d->block + 63) / 64);
+    } else {
+      h->conv_occ = std::max(1, std::min(8, sc::conv_halo_occupancy(g.hp)));
+    }
+  }
   if (workspace) {
     h->ws = static_cast<char*>(workspace);
   } else {
@@ -314,7 +372,7 @@ int skipconv_create(const skipconv_desc* d, const void* weights, void* workspace
     h->owns_ws = true;
   }
   e = hipMemsetAsync(h->ctr(), 0, sc::kNumCounters * 4, st);
-  if (e == hipSuccess) e = hipMemsetAsync(h->bmask(), 0, g.nb, st);
+  if (e == hipSuccess) e = hipMemsetAsync(h->bmask(), 0, g.off_list - g.off_bmask, st);
   if (e == hipSuccess) e = hipMemsetAsync(h->list(), 0, (size_t)g.nb * 4, st);
   if (e == hipSuccess) {
     if (g.depthwise)
@@ -376,15 +434,20 @@ int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t
   cp.reference = ref ? 1 : 0;
   cp.act = d.act_out;
 
-  const bool timing = h->timing_done < h->timing_frames;
+  const bool timing = h->timing_done < h->timing_frames && h->timing_seen % h->timing_every == 0;
+  if (h->timing_frames) ++h->timing_seen;
+  if (timing) h->ev_step[h->timing_done] = h->timing_seen - 1;
   hipError_t e = hipSuccess;
   if (timing) e = hipEventRecord(h->ev[3 * h->timing_done], st);
   if (e == hipSuccess) e = sc::launch_gate(gp, d.dtype, g.vec, g.gate_grid, g.gate_lds, st);
+  if (e == hipSuccess) e = sc::launch_compact(h->bmask(), g.nb, h->list(), h->ctr(), st);
   if (e != hipSuccess) return hip_fail(h, e, "gate launch");
   if (timing) e = hipEventRecord(h->ev[3 * h->timing_done + 1], st);
   if (e == hipSuccess) {
     if (g.depthwise)
       e = sc::launch_depthwise(cp, d.dtype, conv_grid(h), st);
+    else if (g.halo)
+      e = sc::launch_conv_halo(cp, g.hp, conv_grid(h), st);
     else
       e = sc::launch_conv(cp, d.dtype, g.fast, conv_grid(h), st);
   }
@@ -537,11 +600,12 @@ const char* skipconv_status_string(int status) {
 
 const char* skipconv_last_error(skipconv_t h) { return h ? h->last_error : g_create_error; }
 
-int skipconv_timing_begin(skipconv_t h, int frames) {
+int skipconv_timing_begin(skipconv_t h, int frames, int every) {
   if (!h) return SKIPCONV_E_STATE;
-  if (frames < 0 || frames > (1 << 20)) return SKIPCONV_E_INVALID_ARG;
+  if (frames < 0 || frames > (1 << 20) || every < 1) return SKIPCONV_E_INVALID_ARG;
   destroy_events(h);
   h->ev.resize((size_t)frames * 3, nullptr);
+  h->ev_step.assign((size_t)frames, -1);
   for (auto& e : h->ev) {
     const hipError_t r = hipEventCreate(&e);
     if (r != hipSuccess) {
@@ -550,13 +614,16 @@ int skipconv_timing_begin(skipconv_t h, int frames) {
     }
   }
   h->timing_frames = frames;
-  h->timing_done = 0;
+  h->timing_every = every;
   return SKIPCONV_OK;
 }
 
-int skipconv_timing_read(skipconv_t h, void* stream, double* ms, int* frames_timed) {
+int skipconv_timing_read(skipconv_t h, void* stream, double* ms, int* frames_timed,
+                         int32_t* step_index, int capacity) {
   if (!h) return SKIPCONV_E_STATE;
   if (!ms) return SKIPCONV_E_INVALID_ARG;
+  if (step_index && capacity < h->timing_done)
+    return fail(h->last_error, SKIPCONV_E_SMALL_BUFFER, "step_index buffer too small");
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = hipStreamSynchronize(st);
   if (e != hipSuccess) return hip_fail(h, e, "sync");
@@ -568,6 +635,7 @@ int skipconv_timing_read(skipconv_t h, void* stream, double* ms, int* frames_tim
     if (e != hipSuccess) return hip_fail(h, e, "hipEventElapsedTime");
     ms[0] += a;
     ms[1] += b;
+    if (step_index) step_index[i] = h->ev_step[i];
   }
   if (frames_timed) *frames_timed = h->timing_done;
   return SKIPCONV_OK;

@@ -71,9 +71,9 @@ _SIGS = {
                                            ctypes.POINTER(ctypes.c_uint64)]),
     "skipconv_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "skipconv_last_error": (ctypes.c_char_p, [_P]),
-    "skipconv_timing_begin": (ctypes.c_int, [_P, ctypes.c_int]),
+    "skipconv_timing_begin": (ctypes.c_int, [_P, ctypes.c_int, ctypes.c_int]),
     "skipconv_timing_read": (ctypes.c_int, [_P, _P, ctypes.POINTER(ctypes.c_double),
-                                            ctypes.POINTER(ctypes.c_int)]),
+                                            ctypes.POINTER(ctypes.c_int), _P, ctypes.c_int]),
 }
 
 
@@ -213,15 +213,20 @@ def skipconv_last_error(h: Optional[int] = None) -> str:
     return lib().skipconv_last_error(h).decode()
 
 
-def skipconv_timing_begin(h: int, frames: int) -> None:
-    _check(lib().skipconv_timing_begin(h, frames), h)
+def skipconv_timing_begin(h: int, frames: int, every: int = 1) -> None:
+    _check(lib().skipconv_timing_begin(h, frames, every), h)
 
 
-def skipconv_timing_read(h: int, stream: int) -> Tuple[float, float, int]:
+def skipconv_timing_read(h: int, stream: int, capacity: int = 0):
+    """(gate ms, conv ms, timed steps, their indices since timing_begin)."""
+    import numpy as np
     ms = (ctypes.c_double * 2)()
     n = ctypes.c_int()
-    _check(lib().skipconv_timing_read(h, stream, ms, ctypes.byref(n)), h)
-    return ms[0], ms[1], n.value
+    idx = np.zeros(max(capacity, 1), np.int32)
+    _check(lib().skipconv_timing_read(h, stream, ms, ctypes.byref(n),
+                                      idx.ctypes.data_as(ctypes.c_void_p) if capacity else None,
+                                      capacity), h)
+    return ms[0], ms[1], n.value, idx[:n.value].copy() if capacity else None
 
 
 # ----------------------------------------------------------- torch layer ----

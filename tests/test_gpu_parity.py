@@ -293,6 +293,14 @@ EDGE = [
     (1, 1, 1, 8, 16, 1, 1, -1, 1, 1, "f32", 2, "rf"),
     (3, 20, 36, 40, 48, 3, 1, -1, 1, 5, "bf16", 2, "rf"),
     (1, 33, 31, 7, 5, 7, 3, -1, 1, 2, "f32", 1, "rf"),
+    # block-halo kernel: ragged ceil-mode blocks, strides, every wave layout family
+    (1, 37, 29, 32, 64, 3, 1, -1, 1, 8, "bf16", 2, "rf"),
+    (2, 40, 50, 64, 192, 3, 2, -1, 1, 4, "bf16", 2, "rf"),
+    (1, 70, 40, 32, 256, 3, 1, -1, 1, 16, "bf16", 2, "rf"),
+    (1, 66, 66, 32, 48, 1, 1, -1, 1, 32, "bf16", 2, "rf"),
+    (1, 64, 70, 32, 16, 3, 1, -1, 1, 64, "bf16", 2, "rf"),
+    (1, 20, 20, 64, 200, 5, 2, -1, 1, 8, "bf16", 1, "rf"),
+    (1, 24, 24, 32, 32, 3, 1, 0, 1, 4, "bf16", 2, "centre"),
 ]
 
 
@@ -330,4 +338,32 @@ def test_force_dense_equals_eps0_on_changing_frames():
         ref = orc.step(xs)
         assert ref["count"] == ref["block_mask"].size
         compare_frame(layer, ref, "bf16", t=t, tag="force_dense", keep_stats=True)
+    layer.close()
+
+
+@pytest.mark.parametrize("block,groups,k", [(1, 1, 1), (8, 1, 1), (4, 1, 3), (1, 32, 1), (2, 32, 3)])
+def test_operand_rounding_bit_exact(block, groups, k):
+    """bf16 layers convolve bf16_rne(x_t - x_{t-1}): with a one-hot (identity) kernel and
+    z_{t-1} = 0, the update of frame 3 must equal the oracle's rounded residual bit for bit."""
+    rng = np.random.Generator(np.random.PCG64(4242 + block + groups + k))
+    c = 32
+    w = np.zeros((c, c // groups, k, k), np.float32)
+    for co in range(c):
+        w[co, 0 if groups > 1 else co, k // 2, k // 2] = 1.0
+    ws = weight_storage(w, "bf16")
+    zero = np.zeros((1, 16, 16, c), np.float32)
+    u = syn.to_storage(rng.normal(0, 1, (1, 16, 16, c)).astype(np.float32), "bf16")
+    v = syn.to_storage(rng.normal(0, 1, (1, 16, 16, c)).astype(np.float32) * 3, "bf16")
+    layer = S.SkipConv(to_device(ws, "bf16"), n=1, h=16, w=16, groups=groups, eps=float("inf"),
+                       block=block)
+    say(f"[operand rounding] b={block} g={groups} k={k}")
+    layer.step(to_device(syn.to_storage(zero, "bf16"), "bf16"))   # reference frame: z = 0
+    layer.step(to_device(u, "bf16"))                                # gated off; x_{t-1} <- u
+    layer.set_eps(0.0)
+    z = layer.step(to_device(v, "bf16"))                            # z = bf16(v - u)
+    torch.cuda.synchronize()
+    r = O.residual(O.bf16_bits_to_f32(v), O.bf16_bits_to_f32(u))
+    exp = O.bf16_bits_to_f32(O.f32_to_bf16_rne(r))
+    got = z.cpu().numpy()
+    assert np.array_equal(got.view(np.uint32), exp.view(np.uint32))
     layer.close()
