@@ -158,6 +158,7 @@ def event_period(nfr: int) -> int:
 def measure_point(make_layer, frames_dev, steps, warmup, geom, *, label, events=True):
     """Warm up, then time exactly `steps` steps; per-kernel times from HIP events on sampled steps."""
     layer = make_layer()
+    fused = layer.fused
     sites, blocks = clip_active(layer, frames_dev)
     nfr = len(frames_dev)
     pos = nfr
@@ -178,10 +179,16 @@ def measure_point(make_layer, frames_dev, steps, warmup, geom, *, label, events=
     xb, nb = geom["x_bytes"], geom["nb"]
     ref = (tpos == 0)
     gate_bytes = (np.where(ref, 2 * xb, 3 * xb) + 2 * nb + 4 * blocks[tpos]).sum() / nt
+    # fused kernel: x_t, x_{t-1} read once, x_t copied, z read-modify-written at
+    # active sites (written only on a reference frame), weights, block flags
+    zb = 4.0 * geom["c_out"] * sites[tpos]
+    fused_bytes = (np.where(ref, 2 * xb, 3 * xb) + np.where(ref, zb, 2 * zb) + nb
+                   + geom["w_bytes"]).sum() / nt
     gate_us = 1e3 * gate_ms / nt if len(tpos) else None
     conv_us = 1e3 * conv_ms / nt if len(tpos) else None
     res = {
         "label": label,
+        "pipeline": "fused" if fused else "split",
         "ms_per_step": 1e3 * wall / steps,
         "frames_per_s": steps * geom["n"] / wall,
         "density": float(act_sites.sum() / (geom["sites"] * steps)),
@@ -196,9 +203,14 @@ def measure_point(make_layer, frames_dev, steps, warmup, geom, *, label, events=
         "gate_bytes_per_launch": float(gate_bytes),
         "conv_active_tflops": conv_flop / (conv_us * 1e-6) / 1e12 if conv_us else None,
         "gate_gbs": gate_bytes / (gate_us * 1e-6) / 1e9 if gate_us else None,
+        "fused_bytes_per_launch": float(fused_bytes) if fused else None,
     }
-    log(f"[bench] {label}: {res['frames_per_s']:.0f} frames/s, {res['ms_per_step'] * 1e3:.1f} us/step, "
-        f"density {res['density']:.3f}, gate {gate_us or 0:.1f} us, conv {conv_us or 0:.1f} us")
+    if fused:
+        log(f"[bench] {label}: {res['frames_per_s']:.0f} frames/s, {res['ms_per_step'] * 1e3:.1f} us/step, "
+            f"density {res['density']:.3f}, fused kernel {gate_us or 0:.1f} us")
+    else:
+        log(f"[bench] {label}: {res['frames_per_s']:.0f} frames/s, {res['ms_per_step'] * 1e3:.1f} us/step, "
+            f"density {res['density']:.3f}, gate {gate_us or 0:.1f} us, conv {conv_us or 0:.1f} us")
     return res
 
 
@@ -302,6 +314,7 @@ def summarize_pmc(fetch_db: str, write_db: str, out_json: str, *, workload: str,
     w_scale = copy_bytes / cw if cw > 0 else None
     kernels = {}
     for label, pred in (("gate", lambda k: "gate_kernel" in k), ("compact", lambda k: "compact_kernel" in k),
+                        ("fused", lambda k: "fused_kernel" in k),
                         ("conv", lambda k: "conv_" in k and "_kernel" in k),
                         ("depthwise", lambda k: "depthwise_kernel" in k)):
         vf = [v for k, v in fetch if pred(k)]
@@ -356,6 +369,8 @@ def main():
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-events", action="store_true", help="time without per-kernel events")
+    ap.add_argument("--split", action="store_true",
+                    help="force the gate + compaction + conv pipeline instead of the fused kernel")
     ap.add_argument("--eps", type=float, default=None,
                     help="fixed gate threshold (skips calibration; used for counter runs)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -396,7 +411,8 @@ def main():
     kk = spec.k * spec.k * spec.c_in // spec.groups
     x_bytes = wl.n * wl.h * wl.w * wl.c * (2 if wl.dtype == "bf16" else 4)
     geom = {"n": wl.n, "sites": wl.n * h_out * w_out, "c_out": spec.c_out, "kk": kk, "x_bytes": x_bytes,
-            "nb": wl.n * (-(-h_out // block)) * (-(-w_out // block))}
+            "nb": wl.n * (-(-h_out // block)) * (-(-w_out // block)),
+            "w_bytes": kk * spec.c_out * (2 if wl.dtype == "bf16" else 4)}
 
     if args.copy_probe:
         src = torch.empty(args.copy_probe << 20, dtype=torch.uint8, device="cuda")
@@ -405,8 +421,8 @@ def main():
         torch.cuda.synchronize()
     stats = None if args.eps is not None else gpu_stats(layer_kw, wt, frames_dev)
 
-    def mk(b, eps, dense=False):
-        return lambda: SkipConv(wt, eps=eps, block=b, force_dense=dense, **layer_kw)
+    def mk(b, eps, dense=False, split=args.split):
+        return lambda: SkipConv(wt, eps=eps, block=b, force_dense=dense, split=split, **layer_kw)
 
     eps_head = args.eps if args.eps is not None else eps_for_density(stats, block, h_out, w_out, args.density)
     head = measure_point(mk(block, eps_head), frames_dev, args.steps, args.warmup, geom,
@@ -426,6 +442,10 @@ def main():
                           label=f"forced dense b={block}")
         r.update({"block": block, "target_density": 1.0, "forced_dense": True})
         sweep.append(r)
+        r = measure_point(mk(block, eps_head, split=not args.split), frames_dev, sweep_steps, len(clip), geom,
+                          label=f"b={block} d={args.density} other pipeline")
+        r.update({"block": block, "target_density": args.density})
+        sweep.append(r)
         tus = torch_dense_us(wt, (wl.n, wl.h, wl.w, wl.c), spec.stride)
         sweep.append({"label": "torch conv2d (MIOpen), dense, same shape", "us_per_frame_batch": tus,
                       "dense_tflops": 2.0 * geom["sites"] * spec.c_out * kk / (tus * 1e-6) / 1e12})
@@ -434,7 +454,22 @@ def main():
     # roofline of the dominant kernel, from the events of the timed region
     peak_mfma = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
     roof = None
-    if head["conv_us"] is not None:
+    if head["gate_us"] is not None and head["pipeline"] == "fused":
+        fb, ff, fus = head["fused_bytes_per_launch"], head["conv_flop_per_launch"], head["gate_us"]
+        hbm_bound = fb / (PEAK_HBM_GBS * 1e9) >= ff / (peak_mfma * 1e12)
+        if hbm_bound:
+            a = fb / (fus * 1e-6) / 1e9
+            roof = {"kernel": "fused (residual, gate, local compaction, MFMA conv, z update)", "bound": "hbm",
+                    "achieved": a, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": a / PEAK_HBM_GBS,
+                    "traffic": profiled_traffic(args.workload, "fused"), "bytes_per_launch": fb,
+                    "flop_per_launch": ff, "us_per_launch": fus}
+        else:
+            a = ff / (fus * 1e-6) / 1e12
+            roof = {"kernel": "fused (residual, gate, local compaction, MFMA conv, z update)", "bound": "mfma",
+                    "achieved": a, "peak": peak_mfma, "unit": "TFLOP/s", "frac": a / peak_mfma,
+                    "traffic": profiled_traffic(args.workload, "fused"), "bytes_per_launch": fb,
+                    "flop_per_launch": ff, "us_per_launch": fus}
+    elif head["conv_us"] is not None:
         if head["conv_us"] >= head["gate_us"]:
             a = head["conv_active_tflops"]
             roof = {"kernel": "conv (sparse gather-MFMA)", "bound": "mfma", "achieved": a,
@@ -473,7 +508,10 @@ def main():
             "eps": eps_head, "block": block, "density": head["density"],
             "density_steady": head["density_steady"],
             "active_tflops": head["active_tflops"], "dense_equiv_tflops": head["dense_equiv_tflops"],
-            "gate_us": head["gate_us"], "conv_us": head["conv_us"],
+            "pipeline": head["pipeline"],
+            "kernel_us": head["gate_us"] if head["pipeline"] == "fused" else None,
+            "gate_us": head["gate_us"] if head["pipeline"] == "split" else None,
+            "conv_us": head["conv_us"] if head["pipeline"] == "split" else None,
         },
         "roofline": roof,
         "cpu_baseline": cpu,

@@ -64,8 +64,14 @@ enum { SKIPCONV_ACT_NONE = 0, SKIPCONV_ACT_IDENTITY = 1, SKIPCONV_ACT_RELU = 2 }
 /* KEEP_STATS: also store each frame's per-site gate statistic (fp32) and
  * per-site gate bit (before block pooling), for skipconv_copy_stat /
  * skipconv_copy_site_mask. FORCE_DENSE: every block is active on every frame
- * (the same kernels, run dense; used as the dense baseline). */
-enum { SKIPCONV_FLAG_KEEP_STATS = 1u, SKIPCONV_FLAG_FORCE_DENSE = 2u };
+ * (the same kernels, run dense; used as the dense baseline). SPLIT_PIPELINE:
+ * never use the fused single-pass kernel; run the gate, compaction and
+ * convolution kernels separately (the choice is otherwise made at create). */
+enum {
+  SKIPCONV_FLAG_KEEP_STATS = 1u,
+  SKIPCONV_FLAG_FORCE_DENSE = 2u,
+  SKIPCONV_FLAG_SPLIT_PIPELINE = 4u
+};
 
 typedef struct skipconv_desc {
   int32_t n;        /* independent streams (batch), >= 1 */
@@ -148,6 +154,11 @@ int skipconv_activation(skipconv_t h, const void** y);
 /* Descriptor the handle was created with (eps as last set). Host only. */
 int skipconv_get_desc(skipconv_t h, skipconv_desc* d);
 
+/* Kernels one step launches: *fused = 1 for the single-pass kernel (gate,
+ * local compaction and MFMA product in one launch), 0 for the gate +
+ * compaction + convolution pipeline. Host only. */
+int skipconv_pipeline(skipconv_t h, int32_t* fused);
+
 /* ---- introspection (tests and benchmarks; each synchronises `stream`) ---- */
 
 /* Active blocks and active output sites of the last step. */
@@ -181,8 +192,9 @@ const char* skipconv_last_error(skipconv_t h);
  * Time kernel by kernel, with HIP events recorded on the step's stream, every
  * `every`-th step (every >= 1) of the following steps, for up to `frames`
  * timed steps. skipconv_timing_read (synchronises `stream`) returns in ms[0]
- * the summed milliseconds of the gate kernel and in ms[1] of the convolution
- * kernel over the timed steps, and their count; `mask` (may be NULL) receives
+ * the summed milliseconds of the gate and compaction kernels (of the fused
+ * kernel in the single-pass pipeline) and in ms[1] of the convolution kernel
+ * (0 in the single-pass pipeline) over the timed steps, and their count; `mask` (may be NULL) receives
  * for each of them its index among the steps since skipconv_timing_begin.
  * frames = 0 stops timing. */
 int skipconv_timing_begin(skipconv_t h, int frames, int every);

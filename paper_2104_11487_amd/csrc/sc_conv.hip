@@ -518,13 +518,8 @@ hipError_t launch_conv_f32(const ConvParams& p, int grid, hipStream_t st) {
 
 template <int WAVES_M, int WAVES_N, int WM, int WN>
 hipError_t launch_halo_t(const ConvParams& p, const HaloParams& hp, int grid, hipStream_t st) {
-  auto fn = conv_halo_kernel<WAVES_M, WAVES_N, WM, WN>;
-  if (hp.lds_bytes > 64 * 1024) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, hp.lds_bytes);
-    if (e != hipSuccess) return e;
-  }
-  hipLaunchKernelGGL(fn, dim3(grid), dim3(64 * WAVES_M * WAVES_N), hp.lds_bytes, st, p, hp);
+  hipLaunchKernelGGL((conv_halo_kernel<WAVES_M, WAVES_N, WM, WN>), dim3(grid), dim3(64 * WAVES_M * WAVES_N),
+                     hp.lds_bytes, st, p, hp);
   return hipGetLastError();
 }
 
@@ -539,8 +534,7 @@ namespace {
 template <int WAVES_M, int WAVES_N, int WM, int WN>
 int halo_occ_t(const HaloParams& hp) {
   auto fn = conv_halo_kernel<WAVES_M, WAVES_N, WM, WN>;
-  if (hp.lds_bytes > 64 * 1024 &&
-      hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
+  if (hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
                           hp.lds_bytes) != hipSuccess)
     return 0;
   int blocks = 0;

@@ -1,0 +1,391 @@
+// Fused single-pass Skip-Conv step for dense bf16 layers (groups = 1,
+// C_in % 32 == 0): one workgroup per TS x TS tile of output sites made of
+// whole gate blocks, doing every step of Eq. 3 for its tile in one launch:
+//
+//   1. weights: chunks of the packed weights are copied into LDS with
+//      asynchronous global_load_lds by the waves that hold no halo pixel, so
+//      the copy overlaps the gate work;
+//   2. halo: one thread per input pixel of the tile's halo loads its channels
+//      of x_t and x_{t-1} (16-byte loads, all in flight together), forms
+//      r = x_t - x_{t-1} in fp32 (Eq. 2), sums the statistic terms over the
+//      channels in ascending order in registers (canonical arithmetic, one
+//      rounding per multiply and per add), writes rho = bf16_rne(r) to an LDS
+//      halo kept for the product, and copies owned pixels of x_t into the
+//      spare x_{t-1} slot;
+//   3. gate (Eq. 5): support sums over taps in row-major order, exact fp64
+//      threshold, block OR (Sec. 3.2.2); block flags go to global memory;
+//   4. local compaction: the active sites of the tile, in row-major order
+//      (wave ballot + workgroup prefix), become the rows of the product;
+//   5. MFMA product over the active rows only (Sec. 4.2: im2col restricted to
+//      the non-sparse columns, never materialised: A fragments are read from
+//      the LDS halo at each row's pixel + tap offset; rows past the active
+//      count read a zero pixel), fragments read one k-step ahead; the old z of
+//      the lane's outputs is fetched before the product starts;
+//   6. epilogue: z (+)= U at the active sites, activation output refreshed.
+//
+// Inactive tiles stop after step 4, so the hardware dispatcher balances the
+// work. The ordered global active list is not needed by this pipeline; it is
+// produced on demand for introspection by the compaction kernel.
+#include "sc_device.h"
+#include "sc_kernels.h"
+#include "sc_stream.h"
+
+#pragma clang fp contract(off)
+
+namespace sc {
+
+namespace {
+
+constexpr int kThreads = 512;
+constexpr int kWaves = kThreads / 64;
+constexpr int kGroupM = 4;  // waves along M; kWaves / kGroupM along N
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float floatx2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// bf16 round-to-nearest-even of two floats, packed (v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2{a, b}, bf16x2));
+}
+
+// Issue chunk `chunk` of the packed weights (k-steps [chunk*kc, ...), all
+// 16-column tiles) into LDS buffer chunk % nbuf, using waves [w0, kWaves). In
+// the packed order a chunk is contiguous: unit u = one 1 KB B fragment set.
+template <int NTN>
+__device__ __forceinline__ void issue_b(const FusedParams& p, uint8_t* ldsb, int chunk, int wave,
+                                        int lane, int w0) {
+  const int ks0 = chunk * p.kc;
+  const int nks = min(p.kc, p.ksteps - ks0);
+  const int units = nks * NTN;
+  uint8_t* dst = ldsb + (size_t)(chunk % p.nbuf) * p.kc * NTN * 1024;
+  const bf16x8* src = static_cast<const bf16x8*>(p.wpack) + (size_t)ks0 * NTN * 64 + lane;
+  for (int u = wave - w0; u < units; u += kWaves - w0)
+    __builtin_amdgcn_global_load_lds(src + (size_t)u * 64, dst + u * 1024, 16, 0, 0);
+}
+
+template <int WM, int WN>
+__global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
+  constexpr int NTN = WN * (kWaves / kGroupM);
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  __shared__ uint32_t blk_flag[kMaxTileBlocks];
+  __shared__ int rows_pix[kMaxTileBlocks];
+  __shared__ int rows_site[kMaxTileBlocks];
+  __shared__ uint32_t wave_cnt[kWaves];
+
+  const GateParams& g = p.g;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, kq = lane >> 4;
+  const int tile = xcd_tile(blockIdx.x, gridDim.x);
+  const int tiles_per_img = g.tiles_y * g.tiles_x;
+  const int n = tile / tiles_per_img;
+  const int trem = tile - n * tiles_per_img;
+  const int ty = trem / g.tiles_x;
+  const int tx = trem - ty * g.tiles_x;
+  const int oy0 = ty * g.ts, ox0 = tx * g.ts;
+  const int oh = min(g.ts, g.h_out - oy0), ow = min(g.ts, g.w_out - ox0);
+  const int s = g.stride, k = g.k, c = g.c;
+  const int iy0 = oy0 * s - g.pad, ix0 = ox0 * s - g.pad;
+  const int hh = (oh - 1) * s + k, hw = (ow - 1) * s + k;
+  const int own_y0 = oy0 * s, own_x0 = ox0 * s;
+  const int own_y1 = (ty == g.tiles_y - 1) ? g.h : min(g.h, (oy0 + g.ts) * s);
+  const int own_x1 = (tx == g.tiles_x - 1) ? g.w : min(g.w, (ox0 + g.ts) * s);
+
+  uint8_t* ldsb = lds + p.off_b;
+  uint8_t* halo = lds + p.off_halo;
+  float* a_halo = reinterpret_cast<float*>(lds + p.off_a);
+  const int tb_w = g.ts / g.block;
+  const int npix = hh * hw;
+
+  // 1. weights: waves past the ones holding halo pixels issue the first chunk
+  const int bw0 = min(kWaves - 1, (npix + 63) >> 6);
+  if (wave >= bw0) issue_b<NTN>(p, ldsb, 0, wave, lane, bw0);
+  for (int i = threadIdx.x; i < kMaxTileBlocks; i += kThreads) blk_flag[i] = 0u;
+  // the zero pixel read by MFMA rows past the active count
+  for (int i = threadIdx.x; i < (p.pstride >> 4); i += kThreads)
+    *reinterpret_cast<u32x4*>(halo + (size_t)p.zero_pix * p.pstride + i * 16) = u32x4{0u, 0u, 0u, 0u};
+
+  // 2. halo: one thread per pixel, channels in registers, statistic summed in order
+  const uint16_t* xt = static_cast<const uint16_t*>(g.x_t);
+  const uint16_t* xp = static_cast<const uint16_t*>(g.x_prev);
+  uint16_t* keep = static_cast<uint16_t*>(g.x_keep);
+  const int cpp = c >> 3;  // 16-byte chunks per pixel
+  for (int q = threadIdx.x; q < npix; q += kThreads) {
+    const int hy = q / hw, hx = q - hy * hw;
+    const int y = iy0 + hy, x = ix0 + hx;
+    const bool in = y >= 0 && y < g.h && x >= 0 && x < g.w;
+    const bool own = in && g.copy_in_halo && y >= own_y0 && y < own_y1 && x >= own_x0 && x < own_x1;
+    const size_t base = in ? ((size_t)(n * g.h + y) * g.w + x) * c : 0;
+    uint8_t* hrow = halo + (size_t)q * p.pstride;
+    float acc = 0.0f;
+    for (int c0 = 0; c0 < cpp; c0 += 8) {
+      const int nch = min(8, cpp - c0);
+      uint4 vt[8], vp[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        vt[j] = uint4{0u, 0u, 0u, 0u};
+        vp[j] = uint4{0u, 0u, 0u, 0u};
+        if (j < nch && in) {
+          vt[j] = *reinterpret_cast<const uint4*>(xt + base + (c0 + j) * 8);
+          if (!g.reference) vp[j] = *reinterpret_cast<const uint4*>(xp + base + (c0 + j) * 8);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        if (j >= nch) break;
+        u32x4 rq = {0u, 0u, 0u, 0u};
+        if (in) {
+          const uint32_t wt[4] = {vt[j].x, vt[j].y, vt[j].z, vt[j].w};
+          const uint32_t wpv[4] = {vp[j].x, vp[j].y, vp[j].z, vp[j].w};
+          uint32_t outw[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            // channels 2e (low half) and 2e + 1 (high half), in ascending order
+            const float r0 = __fsub_rn(__uint_as_float(wt[e] << 16), __uint_as_float(wpv[e] << 16));
+            const float r1 =
+                __fsub_rn(__uint_as_float(wt[e] & 0xffff0000u), __uint_as_float(wpv[e] & 0xffff0000u));
+            acc = add_rn(acc, term(r0, g.norm_p));
+            acc = add_rn(acc, term(r1, g.norm_p));
+            outw[e] = pack_bf16(r0, r1);
+          }
+          rq = u32x4{outw[0], outw[1], outw[2], outw[3]};
+          if (own) *reinterpret_cast<uint4*>(keep + base + (c0 + j) * 8) = vt[j];
+        }
+        *reinterpret_cast<u32x4*>(hrow + (c0 + j) * 16) = rq;
+      }
+    }
+    a_halo[q] = in ? acc : 0.0f;
+  }
+
+  if (!g.copy_in_halo) {
+    const int ny = own_y1 - own_y0, nx = own_x1 - own_x0;
+    const int per_row = nx * c;
+    for (int i = threadIdx.x; i < ny * per_row; i += kThreads) {
+      const int yy = i / per_row, e = i - yy * per_row;
+      const size_t o = ((size_t)(n * g.h + own_y0 + yy) * g.w + own_x0) * c + e;
+      keep[o] = xt[o];
+    }
+  }
+  __syncthreads();
+
+  // 3. gate
+  for (int q = threadIdx.x; q < oh * ow; q += kThreads) {
+    const int ly = q / ow, lx = q - ly * ow;
+    float sv;
+    if (g.support == 0) {
+      sv = 0.0f;
+      const float* base = a_halo + (ly * s) * hw + lx * s;
+      for (int kh = 0; kh < k; ++kh)
+        for (int kw = 0; kw < k; ++kw) sv = add_rn(sv, base[kh * hw + kw]);
+    } else {
+      sv = a_halo[(ly * s + g.pad) * hw + lx * s + g.pad];
+    }
+    const bool on = g.reference || g.force_dense || ((double)sv > g.thr) || (sv != sv);
+    if (g.keep_stats) {
+      const size_t o = ((size_t)n * g.h_out + oy0 + ly) * g.w_out + ox0 + lx;
+      g.stat[o] = sv;
+      g.site_mask[o] = on ? 1 : 0;
+    }
+    if (on) blk_flag[(ly / g.block) * tb_w + lx / g.block] = 1u;
+  }
+  __syncthreads();
+  {
+    const int nby = (oh + g.block - 1) / g.block, nbx = (ow + g.block - 1) / g.block;
+    const int bi0 = oy0 / g.block, bj0 = ox0 / g.block;
+    for (int i = threadIdx.x; i < nby * nbx; i += kThreads) {
+      const int by = i / nbx, bx = i - by * nbx;
+      g.block_mask[((size_t)n * g.hb + bi0 + by) * g.wb + bj0 + bx] = (uint8_t)blk_flag[by * tb_w + bx];
+    }
+  }
+
+  // 4. local compaction: one site per thread (<= 256 sites), row-major order
+  {
+    const int q = threadIdx.x;
+    const int ly = q / ow, lx = q - (q / ow) * ow;
+    const bool act = q < oh * ow && blk_flag[(ly / g.block) * tb_w + lx / g.block] != 0u;
+    const unsigned long long m = __ballot(act);
+    const uint32_t rank = __popcll(m & ((1ull << lane) - 1ull));
+    if (lane == 0) wave_cnt[wave] = (uint32_t)__popcll(m);
+    __syncthreads();
+    uint32_t off = 0;
+    for (int w = 0; w < wave; ++w) off += wave_cnt[w];
+    if (act) {
+      rows_pix[off + rank] = (ly * s) * hw + lx * s;
+      rows_site[off + rank] = (n * g.h_out + oy0 + ly) * g.w_out + ox0 + lx;
+    }
+  }
+  __syncthreads();
+  int nrows = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) nrows += (int)wave_cnt[w];
+  if (nrows == 0) return;  // every barrier above waited for the weight loads
+
+  // 5. MFMA over the active rows: wave (wm, wn) owns M-tiles wm*WM.. and N-tiles wn*WN..
+  const int wm = wave % kGroupM, wn = wave / kGroupM;
+  floatx4 acc[WM][WN];
+#pragma unroll
+  for (int i = 0; i < WM; ++i)
+#pragma unroll
+    for (int j = 0; j < WN; ++j) acc[i][j] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+  int abase[WM], tapmul[WM];
+#pragma unroll
+  for (int i = 0; i < WM; ++i) {
+    const int row = (wm * WM + i) * 16 + r16;
+    const bool ok = row < nrows;
+    abase[i] = (ok ? rows_pix[row] : p.zero_pix) * p.pstride + kq * 16;
+    tapmul[i] = ok ? p.pstride : 0;  // the zero pixel ignores the tap offset
+  }
+  const bool busy = wm * WM * 16 < nrows;
+  // old z of this lane's outputs, fetched now so the load overlaps the product
+  floatx4 zold[WM][WN];
+#pragma unroll
+  for (int i = 0; i < WM; ++i)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int row = (wm * WM + i) * 16 + kq * 4 + v;
+      const bool rok = busy && row < nrows && !g.reference;
+      const size_t zrow = rok ? (size_t)rows_site[row] * p.c_out : 0;
+#pragma unroll
+      for (int j = 0; j < WN; ++j) {
+        const int col = (wn * WN + j) * 16 + r16;
+        zold[i][j][v] = (rok && col < p.c_out) ? p.z[zrow + col] : 0.0f;
+      }
+    }
+  const int csteps = p.csteps;
+  for (int chunk = 0; chunk < p.nchunks; ++chunk) {
+    if (chunk + 1 < p.nchunks) issue_b<NTN>(p, ldsb, chunk + 1, wave, lane, 0);
+    if (busy) {
+      const int ks0 = chunk * p.kc;
+      const int nks = min(p.kc, p.ksteps - ks0);
+      const uint8_t* bbuf =
+          ldsb + (size_t)(chunk % p.nbuf) * p.kc * NTN * 1024 + (wn * WN) * 1024 + lane * 16;
+      int tap = ks0 / csteps, cc = ks0 - tap * csteps;
+      bf16x8 acur[WM], bcur[WN];
+      {
+        const int kh = tap / k, kw = tap - kh * k;
+        const int toff = kh * hw + kw, coff = cc * 64;
+#pragma unroll
+        for (int j = 0; j < WN; ++j) bcur[j] = *reinterpret_cast<const bf16x8*>(bbuf + j * 1024);
+#pragma unroll
+        for (int i = 0; i < WM; ++i)
+          acur[i] = *reinterpret_cast<const bf16x8*>(halo + abase[i] + toff * tapmul[i] + coff);
+      }
+      for (int kk = 0; kk < nks; ++kk) {
+        // fragments of the next k-step (the last step re-reads its own)
+        const bool more = kk + 1 < nks;
+        if (more && ++cc == csteps) {
+          cc = 0;
+          ++tap;
+        }
+        const int kn = more ? kk + 1 : kk;
+        const int kh = tap / k, kw = tap - kh * k;
+        const int toff = kh * hw + kw, coff = cc * 64;
+        bf16x8 anxt[WM], bnxt[WN];
+#pragma unroll
+        for (int j = 0; j < WN; ++j) bnxt[j] = *reinterpret_cast<const bf16x8*>(bbuf + (kn * NTN + j) * 1024);
+#pragma unroll
+        for (int i = 0; i < WM; ++i)
+          anxt[i] = *reinterpret_cast<const bf16x8*>(halo + abase[i] + toff * tapmul[i] + coff);
+#pragma unroll
+        for (int i = 0; i < WM; ++i)
+#pragma unroll
+          for (int j = 0; j < WN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(acur[i], bcur[j], acc[i][j], 0, 0, 0);
+#pragma unroll
+        for (int j = 0; j < WN; ++j) bcur[j] = bnxt[j];
+#pragma unroll
+        for (int i = 0; i < WM; ++i) acur[i] = anxt[i];
+      }
+    }
+    if (chunk + 1 < p.nchunks) __syncthreads();  // next chunk landed; this buffer free
+  }
+
+  // 6. epilogue
+  if (!busy) return;
+#pragma unroll
+  for (int i = 0; i < WM; ++i) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int row = (wm * WM + i) * 16 + kq * 4 + v;
+      if (row >= nrows) continue;
+      const size_t zrow = (size_t)rows_site[row] * p.c_out;
+#pragma unroll
+      for (int j = 0; j < WN; ++j) {
+        const int col = (wn * WN + j) * 16 + r16;
+        if (col >= p.c_out) continue;
+        const float nv = g.reference ? acc[i][j][v] : zold[i][j][v] + acc[i][j][v];
+        p.z[zrow + col] = nv;
+        if (p.act) Elem<uint16_t>::store1(static_cast<uint16_t*>(p.y), zrow + col,
+                                          p.act == 2 ? fmaxf(nv, 0.0f) : nv);
+      }
+    }
+  }
+}
+
+template <int WM, int WN>
+hipError_t launch_fused_t(const FusedParams& p, int grid, hipStream_t st) {
+  hipLaunchKernelGGL((fused_kernel<WM, WN>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p);
+  return hipGetLastError();
+}
+
+// Allow the kernel its dynamic LDS (above the 64 KB default) and report how
+// many workgroups fit on one CU; done once, at create time.
+template <int WM, int WN>
+int prepare_fused_t(const FusedParams& p) {
+  const void* fn = reinterpret_cast<const void*>(fused_kernel<WM, WN>);
+  if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, p.lds_bytes) != hipSuccess) return 0;
+  int blocks = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, fused_kernel<WM, WN>, kThreads, p.lds_bytes) !=
+      hipSuccess)
+    return 0;
+  return blocks;
+}
+
+}  // namespace
+
+// Instantiations: WM = M-tiles per wave (1 for 8x8 tiles, 4 for 16x16 tiles),
+// WN = N-tiles per wave = ntiles_n / 2 (two waves share the N dimension).
+int prepare_fused(const FusedParams& p) {
+  if (p.mw == 1) {
+    switch (p.ntiles_n) {
+      case 2: return prepare_fused_t<1, 1>(p);
+      case 4: return prepare_fused_t<1, 2>(p);
+      case 8: return prepare_fused_t<1, 4>(p);
+      case 12: return prepare_fused_t<1, 6>(p);
+      case 16: return prepare_fused_t<1, 8>(p);
+      default: return 0;
+    }
+  }
+  if (p.mw == 4) {
+    switch (p.ntiles_n) {
+      case 2: return prepare_fused_t<4, 1>(p);
+      case 4: return prepare_fused_t<4, 2>(p);
+      case 8: return prepare_fused_t<4, 4>(p);
+      default: return 0;
+    }
+  }
+  return 0;
+}
+
+hipError_t launch_fused(const FusedParams& p, int grid, hipStream_t st) {
+  if (p.mw == 1) {
+    switch (p.ntiles_n) {
+      case 2: return launch_fused_t<1, 1>(p, grid, st);
+      case 4: return launch_fused_t<1, 2>(p, grid, st);
+      case 8: return launch_fused_t<1, 4>(p, grid, st);
+      case 12: return launch_fused_t<1, 6>(p, grid, st);
+      case 16: return launch_fused_t<1, 8>(p, grid, st);
+      default: return hipErrorInvalidValue;
+    }
+  }
+  if (p.mw == 4) {
+    switch (p.ntiles_n) {
+      case 2: return launch_fused_t<4, 1>(p, grid, st);
+      case 4: return launch_fused_t<4, 2>(p, grid, st);
+      case 8: return launch_fused_t<4, 4>(p, grid, st);
+      default: return hipErrorInvalidValue;
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace sc

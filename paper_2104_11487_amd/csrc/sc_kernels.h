@@ -62,6 +62,24 @@ struct HaloParams {
   int threads;           // workgroup size
 };
 
+// Fused single-pass step for dense bf16 layers (see sc_fused.hip). `g` carries
+// the gate geometry of the fused tiling (ts, tiles, staging rows).
+struct FusedParams {
+  GateParams g;
+  const void* wpack;
+  float* z;
+  void* y;
+  int c_out, ntiles_n, ksteps, csteps, act;
+  int kc, nchunks, nbuf;   // weight chunks: k-steps per chunk, chunk count, LDS buffers
+  int mw;                  // 16-row MFMA tiles per wave (1 for 8x8 tiles, 4 for 16x16)
+  int pstride;             // LDS bytes per rho halo pixel: 2*c_in + 16
+  int zero_pix;            // index of the all-zero pixel just past the halo
+  int off_b, off_halo, off_a, lds_bytes;
+};
+
+hipError_t launch_fused(const FusedParams& p, int grid, hipStream_t st);
+int prepare_fused(const FusedParams& p);  // create time: LDS attribute; workgroups per CU (0 on error)
+
 hipError_t launch_gate(const GateParams& p, int dtype, int vec, int grid, size_t lds_bytes,
                        hipStream_t st);
 // Ordered compaction of the block flags into the active list and its count.

@@ -10,7 +10,7 @@
 #include <new>
 #include <vector>
 
-#include "../../include/skipconv.h"
+#include "skipconv.h"
 #include "sc_kernels.h"
 
 namespace {
@@ -22,6 +22,18 @@ constexpr size_t kLdsLimit = 60 * 1024;  // dynamic; the gate kernel adds 2 KB s
 constexpr size_t kStageBudget = 36 * 1024;
 constexpr int kMaxCout = 256;
 constexpr long kHaloLdsLimit = 160 * 1024;  // LDS of one gfx950 CU
+constexpr long kFusedLdsLimit = 156 * 1024; // dynamic LDS of the fused kernel (+ ~3 KB static)
+
+// Does every tile's halo contain the input pixels the tile owns?
+int halo_covers_owned(int n_in, int n_out, int ts, int tiles, int s, int pad, int k) {
+  for (int t = 0; t < tiles; ++t) {
+    const int o0 = t * ts, on = std::min(ts, n_out - o0);
+    const int hi = (o0 + on - 1) * s - pad + k - 1;
+    const int own1 = t == tiles - 1 ? n_in : std::min(n_in, (o0 + ts) * s);
+    if (own1 - 1 > hi) return 0;
+  }
+  return 1;
+}
 
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
@@ -36,6 +48,9 @@ struct Geometry {
   bool fast;
   bool halo;            // dense bf16 block-halo kernel (else the gather kernel)
   sc::HaloParams hp;
+  bool fused;           // single-pass kernel instead of gate + compaction + conv
+  int f_ts, f_tiles_y, f_tiles_x, f_grid, f_copy_in_halo;
+  int f_kc, f_nchunks, f_nbuf, f_mw, f_pstride, f_zero_pix, f_off_b, f_off_halo, f_off_a, f_lds;
   int vec;              // gate load width (elements)
   size_t elem;
   size_t off_wpack, off_slot0, off_slot1, off_z, off_y, off_bmask, off_list, off_ctr, off_stat,
@@ -81,7 +96,7 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
     return fail(err, SKIPCONV_E_INVALID_ARG, "unknown dtype");
   if (d->act_out < SKIPCONV_ACT_NONE || d->act_out > SKIPCONV_ACT_RELU)
     return fail(err, SKIPCONV_E_INVALID_ARG, "unknown act_out");
-  if (d->flags & ~(uint32_t)(SKIPCONV_FLAG_KEEP_STATS | SKIPCONV_FLAG_FORCE_DENSE))
+  if (d->flags & ~(uint32_t)(SKIPCONV_FLAG_KEEP_STATS | SKIPCONV_FLAG_FORCE_DENSE | SKIPCONV_FLAG_SPLIT_PIPELINE))
     return fail(err, SKIPCONV_E_INVALID_ARG, "unknown flag bits");
   if (std::isnan(d->eps) || d->eps < 0.0f) return fail(err, SKIPCONV_E_INVALID_ARG, "eps must be >= 0");
   if (!depthwise && d->c_out > kMaxCout) return fail(err, SKIPCONV_E_UNSUPPORTED, "c_out > 256");
@@ -195,6 +210,48 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
     }
   }
 
+  // fused single-pass kernel: dense bf16, C_in % 32 == 0, tiles of <= 16 x 16
+  // sites, output tiles split over two wave groups (ntn >= 2)
+  G.fused = false;
+  if (!depthwise && d->dtype == SKIPCONV_BF16 && d->c_in % 32 == 0 && b <= 16 && G.ntn >= 2 &&
+      !(d->flags & SKIPCONV_FLAG_SPLIT_PIPELINE)) {
+    const int ts = b <= 8 ? b * (8 / b) : b;
+    const int mw = ts <= 8 ? 1 : 4;
+    if (!(mw == 4 && G.ntn > 8)) {
+      const int hh = (ts - 1) * s + k;
+      const long pstride = 2L * d->c_in + 16;
+      const long halo_b = ((long)hh * hh + 1) * pstride;  // + the zero pixel
+      const long a_b = ((long)hh * hh * 4 + 15) / 16 * 16;
+      const long whole = (long)G.ksteps * G.ntn * 1024;
+      long b_bytes = whole;
+      int kc = G.ksteps, nbuf = 1;
+      if (whole + halo_b + a_b > kFusedLdsLimit) {
+        kc = std::max(1, 16 / G.ntn);
+        nbuf = 2;
+        b_bytes = (long)nbuf * kc * G.ntn * 1024;
+      }
+      if (b_bytes + halo_b + a_b <= kFusedLdsLimit) {
+        G.fused = true;
+        G.f_ts = ts;
+        G.f_mw = mw;
+        G.f_kc = kc;
+        G.f_nbuf = nbuf;
+        G.f_nchunks = (G.ksteps + kc - 1) / kc;
+        G.f_pstride = (int)pstride;
+        G.f_zero_pix = hh * hh;
+        G.f_off_b = 0;
+        G.f_off_halo = (int)b_bytes;
+        G.f_off_a = (int)(b_bytes + halo_b);
+        G.f_lds = (int)(b_bytes + halo_b + a_b);
+        G.f_tiles_y = (G.h_out + ts - 1) / ts;
+        G.f_tiles_x = (G.w_out + ts - 1) / ts;
+        G.f_grid = d->n * G.f_tiles_y * G.f_tiles_x;
+        G.f_copy_in_halo = halo_covers_owned(d->h, G.h_out, ts, G.f_tiles_y, s, pad, k) &&
+                           halo_covers_owned(d->w, G.w_out, ts, G.f_tiles_x, s, pad, k);
+      }
+    }
+  }
+
   G.x_bytes = (size_t)xel * G.elem;
   G.z_bytes = (size_t)sites * d->c_out * 4;
   size_t off = 0;
@@ -226,6 +283,7 @@ struct skipconv_layer {
   int device = 0;
   int num_cu = 256;
   int conv_occ = 4;          // resident conv workgroups per CU
+  bool list_valid = false;   // active list/count match the last step (fused steps skip them)
   char* ws = nullptr;
   bool owns_ws = false;
   int cur = 0;               // slot holding x_{t-1}
@@ -250,6 +308,39 @@ struct skipconv_layer {
 
 namespace {
 
+sc::GateParams gate_params(skipconv_layer* h, const void* x_t, bool ref);
+
+// Kernel parameters of the fused single-pass kernel (x_t / reference set per step).
+sc::FusedParams fused_params(skipconv_layer* h, const void* x_t, bool ref) {
+  const skipconv_desc& d = h->d;
+  const Geometry& g = h->g;
+  sc::FusedParams fp{};
+  fp.g = gate_params(h, x_t, ref);
+  fp.g.ts = g.f_ts;
+  fp.g.tiles_y = g.f_tiles_y;
+  fp.g.tiles_x = g.f_tiles_x;
+  fp.g.copy_in_halo = g.f_copy_in_halo;
+  fp.wpack = h->wpack();
+  fp.z = h->z();
+  fp.y = h->y();
+  fp.c_out = d.c_out;
+  fp.ntiles_n = g.ntn;
+  fp.ksteps = g.ksteps;
+  fp.csteps = d.c_in / 32;
+  fp.act = d.act_out;
+  fp.kc = g.f_kc;
+  fp.nchunks = g.f_nchunks;
+  fp.nbuf = g.f_nbuf;
+  fp.mw = g.f_mw;
+  fp.pstride = g.f_pstride;
+  fp.zero_pix = g.f_zero_pix;
+  fp.off_b = g.f_off_b;
+  fp.off_halo = g.f_off_halo;
+  fp.off_a = g.f_off_a;
+  fp.lds_bytes = g.f_lds;
+  return fp;
+}
+
 int hip_fail(skipconv_t h, hipError_t e, const char* what) {
   if (h) snprintf(h->last_error, sizeof(h->last_error), "%s: %s", what, hipGetErrorString(e));
   return SKIPCONV_E_HIP;
@@ -258,6 +349,29 @@ int hip_fail(skipconv_t h, hipError_t e, const char* what) {
 double threshold(const skipconv_desc& d) {
   const double e = (double)d.eps;  // fp32 -> fp64 is exact; e * e is exact in fp64
   return d.norm_p == 2 ? e * e : e;
+}
+
+sc::GateParams gate_params(skipconv_layer* h, const void* x_t, bool ref) {
+  const skipconv_desc& d = h->d;
+  const Geometry& g = h->g;
+  sc::GateParams gp{};
+  gp.x_t = x_t;
+  gp.x_prev = h->slot(h->cur);
+  gp.x_keep = h->slot(h->cur ^ 1);
+  gp.n = d.n; gp.h = d.h; gp.w = d.w; gp.c = d.c_in;
+  gp.h_out = g.h_out; gp.w_out = g.w_out; gp.k = d.kernel; gp.stride = d.stride; gp.pad = g.pad;
+  gp.block = d.block; gp.hb = g.hb; gp.wb = g.wb;
+  gp.ts = g.ts; gp.tiles_y = g.tiles_y; gp.tiles_x = g.tiles_x;
+  gp.halo_floats = g.halo_floats; gp.stage_stride = g.stage_stride;
+  gp.rows_per_batch = g.rows_per_batch; gp.copy_in_halo = g.copy_in_halo;
+  gp.norm_p = d.norm_p; gp.support = d.support; gp.reference = ref ? 1 : 0;
+  gp.force_dense = (d.flags & SKIPCONV_FLAG_FORCE_DENSE) ? 1 : 0;
+  gp.keep_stats = (d.flags & SKIPCONV_FLAG_KEEP_STATS) ? 1 : 0;
+  gp.thr = threshold(d);
+  gp.block_mask = h->bmask(); gp.list = h->list(); gp.counters = h->ctr();
+  gp.stat = h->stat(); gp.site_mask = h->smask();
+
+  return gp;
 }
 
 int conv_grid(const skipconv_layer* h) {
@@ -348,6 +462,12 @@ int skipconv_create(const skipconv_desc* d, const void* weights, void* workspace
     delete h;
     return SKIPCONV_E_HIP;
   }
+  // The single-pass kernel serialises load, gate and product inside each
+  // workgroup; it wins while the frame has few tiles (latency regime) and the
+  // split pipeline wins on large frames, where each kernel streams at its own
+  // roofline. Threshold: four tiles per CU.
+  if (h->g.fused && (h->g.f_grid > 4 * h->num_cu || sc::prepare_fused(fused_params(h, nullptr, true)) < 1))
+    h->g.fused = false;
   if (g.halo) {
     int max_lds = 0;
     if (hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, h->device) != hipSuccess ||
@@ -402,22 +522,7 @@ int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t
   const Geometry& g = h->g;
   const bool ref = h->ref_pending;
 
-  sc::GateParams gp{};
-  gp.x_t = x_t;
-  gp.x_prev = h->slot(h->cur);
-  gp.x_keep = h->slot(h->cur ^ 1);
-  gp.n = d.n; gp.h = d.h; gp.w = d.w; gp.c = d.c_in;
-  gp.h_out = g.h_out; gp.w_out = g.w_out; gp.k = d.kernel; gp.stride = d.stride; gp.pad = g.pad;
-  gp.block = d.block; gp.hb = g.hb; gp.wb = g.wb;
-  gp.ts = g.ts; gp.tiles_y = g.tiles_y; gp.tiles_x = g.tiles_x;
-  gp.halo_floats = g.halo_floats; gp.stage_stride = g.stage_stride;
-  gp.rows_per_batch = g.rows_per_batch; gp.copy_in_halo = g.copy_in_halo;
-  gp.norm_p = d.norm_p; gp.support = d.support; gp.reference = ref ? 1 : 0;
-  gp.force_dense = (d.flags & SKIPCONV_FLAG_FORCE_DENSE) ? 1 : 0;
-  gp.keep_stats = (d.flags & SKIPCONV_FLAG_KEEP_STATS) ? 1 : 0;
-  gp.thr = threshold(d);
-  gp.block_mask = h->bmask(); gp.list = h->list(); gp.counters = h->ctr();
-  gp.stat = h->stat(); gp.site_mask = h->smask();
+  const sc::GateParams gp = gate_params(h, x_t, ref);
 
   sc::ConvParams cp{};
   cp.x_t = x_t;
@@ -437,21 +542,31 @@ int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t
   const bool timing = h->timing_done < h->timing_frames && h->timing_seen % h->timing_every == 0;
   if (h->timing_frames) ++h->timing_seen;
   if (timing) h->ev_step[h->timing_done] = h->timing_seen - 1;
+
   hipError_t e = hipSuccess;
   if (timing) e = hipEventRecord(h->ev[3 * h->timing_done], st);
-  if (e == hipSuccess) e = sc::launch_gate(gp, d.dtype, g.vec, g.gate_grid, g.gate_lds, st);
-  if (e == hipSuccess) e = sc::launch_compact(h->bmask(), g.nb, h->list(), h->ctr(), st);
-  if (e != hipSuccess) return hip_fail(h, e, "gate launch");
-  if (timing) e = hipEventRecord(h->ev[3 * h->timing_done + 1], st);
-  if (e == hipSuccess) {
-    if (g.depthwise)
-      e = sc::launch_depthwise(cp, d.dtype, conv_grid(h), st);
-    else if (g.halo)
-      e = sc::launch_conv_halo(cp, g.hp, conv_grid(h), st);
-    else
-      e = sc::launch_conv(cp, d.dtype, g.fast, conv_grid(h), st);
+  if (g.fused) {
+    const sc::FusedParams fp = fused_params(h, x_t, ref);
+    if (e == hipSuccess) e = sc::launch_fused(fp, g.f_grid, st);
+    if (e != hipSuccess) return hip_fail(h, e, "fused launch");
+    if (timing) e = hipEventRecord(h->ev[3 * h->timing_done + 1], st);
+    h->list_valid = false;
+  } else {
+    if (e == hipSuccess) e = sc::launch_gate(gp, d.dtype, g.vec, g.gate_grid, g.gate_lds, st);
+    if (e == hipSuccess) e = sc::launch_compact(h->bmask(), g.nb, h->list(), h->ctr(), st);
+    if (e != hipSuccess) return hip_fail(h, e, "gate launch");
+    if (timing) e = hipEventRecord(h->ev[3 * h->timing_done + 1], st);
+    if (e == hipSuccess) {
+      if (g.depthwise)
+        e = sc::launch_depthwise(cp, d.dtype, conv_grid(h), st);
+      else if (g.halo)
+        e = sc::launch_conv_halo(cp, g.hp, conv_grid(h), st);
+      else
+        e = sc::launch_conv(cp, d.dtype, g.fast, conv_grid(h), st);
+    }
+    if (e != hipSuccess) return hip_fail(h, e, "conv launch");
+    h->list_valid = true;
   }
-  if (e != hipSuccess) return hip_fail(h, e, "conv launch");
   if (timing) {
     e = hipEventRecord(h->ev[3 * h->timing_done + 2], st);
     if (e != hipSuccess) return hip_fail(h, e, "event record");
@@ -493,6 +608,13 @@ int skipconv_activation(skipconv_t h, const void** y) {
   return SKIPCONV_OK;
 }
 
+int skipconv_pipeline(skipconv_t h, int32_t* fused) {
+  if (!h) return SKIPCONV_E_STATE;
+  if (!fused) return SKIPCONV_E_INVALID_ARG;
+  *fused = h->g.fused ? 1 : 0;
+  return SKIPCONV_OK;
+}
+
 int skipconv_get_desc(skipconv_t h, skipconv_desc* d) {
   if (!h) return SKIPCONV_E_STATE;
   if (!d) return SKIPCONV_E_INVALID_ARG;
@@ -508,9 +630,20 @@ static int copy_back(skipconv_t h, void* stream, void* host, const void* dev, si
   return SKIPCONV_OK;
 }
 
+// The fused pipeline does not build the ordered list; build it on demand.
+static int ensure_list(skipconv_t h, void* stream) {
+  if (h->list_valid) return SKIPCONV_OK;
+  const hipError_t e = sc::launch_compact(h->bmask(), h->g.nb, h->list(), h->ctr(), static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(h, e, "compaction launch");
+  h->list_valid = true;
+  return SKIPCONV_OK;
+}
+
 int skipconv_active_count(skipconv_t h, void* stream, int64_t* blocks, int64_t* sites) {
   if (!h) return SKIPCONV_E_STATE;
   if (h->frames == 0) return fail(h->last_error, SKIPCONV_E_STATE, "no step yet");
+  int rc0 = ensure_list(h, stream);
+  if (rc0) return rc0;
   uint32_t cnt = 0;
   int rc = copy_back(h, stream, &cnt, h->ctr() + sc::kCtrCount, 4);
   if (rc) return rc;
@@ -544,8 +677,10 @@ int skipconv_copy_active_list(skipconv_t h, void* stream, uint32_t* host, size_t
                               int64_t* count) {
   if (!h) return SKIPCONV_E_STATE;
   if (!host || !count) return SKIPCONV_E_INVALID_ARG;
+  int rc = ensure_list(h, stream);
+  if (rc) return rc;
   uint32_t cnt = 0;
-  int rc = copy_back(h, stream, &cnt, h->ctr() + sc::kCtrCount, 4);
+  rc = copy_back(h, stream, &cnt, h->ctr() + sc::kCtrCount, 4);
   if (rc) return rc;
   *count = cnt;
   if (capacity < cnt) return fail(h->last_error, SKIPCONV_E_SMALL_BUFFER, "list buffer too small");

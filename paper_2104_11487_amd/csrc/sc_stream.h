@@ -1,0 +1,69 @@
+// Streaming helpers shared by the gate kernel and the fused gate+conv kernel:
+// canonical per-pixel statistic, vector loads/copies, XCD-aware tile order.
+#pragma once
+
+#include "sc_device.h"
+
+#pragma clang fp contract(off)
+
+namespace sc {
+
+constexpr int kUnroll = 4;  // staging chunks whose loads are issued together
+
+__device__ __forceinline__ float term(float r, int norm_p) {
+  return norm_p == 2 ? mul_rn(r, r) : fabsf(r);
+}
+
+// Sum of the staged per-channel terms of one pixel, ascending channel order.
+// Rows are 16-byte aligned when c % 4 == 0, so four terms come per LDS read;
+// the additions stay strictly sequential.
+__device__ __forceinline__ float sum_channels(const float* row, int c) {
+  float acc = 0.0f;
+  if ((c & 3) == 0) {
+    const float4* r4 = reinterpret_cast<const float4*>(row);
+#pragma unroll 4
+    for (int i = 0; i < (c >> 2); ++i) {
+      const float4 v = r4[i];
+      acc = add_rn(acc, v.x);
+      acc = add_rn(acc, v.y);
+      acc = add_rn(acc, v.z);
+      acc = add_rn(acc, v.w);
+    }
+  } else {
+    for (int i = 0; i < c; ++i) acc = add_rn(acc, row[i]);
+  }
+  return acc;
+}
+
+template <typename T, int VEC>
+__device__ __forceinline__ void load_vec(const T* p, size_t off, float* v) {
+  if (VEC == 8) {
+    Elem<T>::load8(p, off, v);
+  } else if (VEC == 4) {
+    Elem<T>::load4(p, off, v);
+  } else {
+    v[0] = Elem<T>::load1(p, off);
+  }
+}
+
+template <typename T, int VEC>
+__device__ __forceinline__ void copy_vec(T* dst, const T* src, size_t off) {
+  if (VEC * sizeof(T) == 16) {
+    *reinterpret_cast<uint4*>(dst + off) = *reinterpret_cast<const uint4*>(src + off);
+  } else if (VEC * sizeof(T) == 8) {
+    *reinterpret_cast<uint2*>(dst + off) = *reinterpret_cast<const uint2*>(src + off);
+  } else {
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) dst[off + j] = src[off + j];
+  }
+}
+
+// Workgroup b runs tile remap(b): XCD b % 8 (workgroups go to the XCDs
+// round-robin) receives a contiguous range of tiles, so neighbouring tiles
+// share their halo rows through one L2.
+__device__ __forceinline__ int xcd_tile(int b, int g) {
+  const int per = g >> 3, rem = g & 7, x = b & 7;
+  return x * per + min(x, rem) + (b >> 3);
+}
+
+}  // namespace sc

@@ -27,7 +27,7 @@ SKIPCONV_E_SMALL_BUFFER = -6
 SKIPCONV_F32, SKIPCONV_BF16 = 0, 1
 SKIPCONV_SUPPORT_RF, SKIPCONV_SUPPORT_CENTRE = 0, 1
 SKIPCONV_ACT_NONE, SKIPCONV_ACT_IDENTITY, SKIPCONV_ACT_RELU = 0, 1, 2
-SKIPCONV_FLAG_KEEP_STATS, SKIPCONV_FLAG_FORCE_DENSE = 1, 2
+SKIPCONV_FLAG_KEEP_STATS, SKIPCONV_FLAG_FORCE_DENSE, SKIPCONV_FLAG_SPLIT_PIPELINE = 1, 2, 4
 
 
 class skipconv_desc(ctypes.Structure):
@@ -60,6 +60,7 @@ _SIGS = {
     "skipconv_destroy": (ctypes.c_int, [_P]),
     "skipconv_activation": (ctypes.c_int, [_P, ctypes.POINTER(_P)]),
     "skipconv_get_desc": (ctypes.c_int, [_P, _D]),
+    "skipconv_pipeline": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_int32)]),
     "skipconv_active_count": (ctypes.c_int, [_P, _P, ctypes.POINTER(ctypes.c_int64),
                                              ctypes.POINTER(ctypes.c_int64)]),
     "skipconv_copy_block_mask": (ctypes.c_int, [_P, _P, _P, ctypes.c_size_t]),
@@ -167,6 +168,12 @@ def skipconv_get_desc(h: int) -> skipconv_desc:
     return d
 
 
+def skipconv_pipeline(h: int) -> int:
+    f = ctypes.c_int32()
+    _check(lib().skipconv_pipeline(h, ctypes.byref(f)), h)
+    return f.value
+
+
 def skipconv_active_count(h: int, stream: int) -> Tuple[int, int]:
     b, s = ctypes.c_int64(), ctypes.c_int64()
     _check(lib().skipconv_active_count(h, stream, ctypes.byref(b), ctypes.byref(s)), h)
@@ -237,14 +244,15 @@ _ACT = {"none": SKIPCONV_ACT_NONE, "identity": SKIPCONV_ACT_IDENTITY, "relu": SK
 
 def make_desc(*, n, h, w, c_in, c_out, kernel, stride=1, pad=-1, groups=1, block=1, norm_p=2,
               support="rf", dtype="f32", act_out="none", eps=0.0, keep_stats=False,
-              force_dense=False) -> skipconv_desc:
+              force_dense=False, split=False) -> skipconv_desc:
     d = skipconv_desc_init()
     d.n, d.h, d.w, d.c_in, d.c_out = n, h, w, c_in, c_out
     d.kernel, d.stride, d.pad, d.groups, d.block = kernel, stride, pad, groups, block
     d.norm_p, d.support = norm_p, _SUPPORT[support]
     d.dtype = SKIPCONV_BF16 if dtype == "bf16" else SKIPCONV_F32
     d.act_out = _ACT[act_out]
-    d.flags = (SKIPCONV_FLAG_KEEP_STATS if keep_stats else 0) | (SKIPCONV_FLAG_FORCE_DENSE if force_dense else 0)
+    d.flags = ((SKIPCONV_FLAG_KEEP_STATS if keep_stats else 0) | (SKIPCONV_FLAG_FORCE_DENSE if force_dense else 0)
+               | (SKIPCONV_FLAG_SPLIT_PIPELINE if split else 0))
     d.eps = eps
     return d
 
@@ -261,7 +269,7 @@ class SkipConv:
     def __init__(self, weight, *, n: int, h: int, w: int, stride: int = 1, pad: int = -1,
                  groups: int = 1, eps: float = 0.0, block: int = 1, norm_p: int = 2,
                  support: str = "rf", act_out: str = "none", keep_stats: bool = False,
-                 force_dense: bool = False, stream=None):
+                 force_dense: bool = False, split: bool = False, stream=None):
         import torch
 
         if not weight.is_cuda:
@@ -275,7 +283,7 @@ class SkipConv:
         self.desc = make_desc(n=n, h=h, w=w, c_in=cg * groups, c_out=c_out, kernel=k, stride=stride,
                               pad=pad, groups=groups, block=block, norm_p=norm_p, support=support,
                               dtype=self.dtype, act_out=act_out, eps=eps, keep_stats=keep_stats,
-                              force_dense=force_dense)
+                              force_dense=force_dense, split=split)
         self.h_out, self.w_out, self.hb, self.wb = skipconv_out_shape(self.desc)
         nbytes = skipconv_workspace_size(self.desc)
         self.device = weight.device
@@ -320,6 +328,10 @@ class SkipConv:
 
     def reset(self):
         skipconv_reset(self.handle)
+
+    @property
+    def fused(self) -> bool:
+        return bool(skipconv_pipeline(self.handle))
 
     def set_eps(self, eps: float):
         skipconv_set_eps(self.handle, eps)

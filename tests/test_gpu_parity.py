@@ -20,11 +20,11 @@ pytestmark = pytest.mark.gpu
 
 
 def _layer_pair(w_f32, *, n, h, w, dtype, eps, block, stride=1, pad=-1, groups=1, norm_p=2,
-                support="rf", keep_stats=True, act_out="none", force_dense=False):
+                support="rf", keep_stats=True, act_out="none", force_dense=False, split=False):
     ws = weight_storage(w_f32, dtype)
     layer = S.SkipConv(to_device(ws, dtype), n=n, h=h, w=w, stride=stride, pad=pad, groups=groups,
                        eps=eps, block=block, norm_p=norm_p, support=support, keep_stats=keep_stats,
-                       act_out=act_out, force_dense=force_dense)
+                       act_out=act_out, force_dense=force_dense, split=split)
     orc = O.SkipConvOracle(ws, n=n, h=h, w=w, stride=stride, pad=None if pad == -1 else pad,
                            groups=groups, eps=eps, block=block, norm_p=norm_p, support=support,
                            dtype=dtype)
@@ -42,7 +42,7 @@ def run_single(frames, w_f32, *, dtype, eps, block, tag, resets=(), exact_z=Fals
             layer.reset()
             orc.reset()
         xs = syn.to_storage(f, dtype)
-        say(f"[{tag}] frame {t} shape={f.shape} eps={eps:.4g} b={block}")
+        say(f"[{tag}] frame {t} shape={f.shape} eps={eps:.4g} b={block} fused={layer.fused}")
         layer.step(to_device(xs, dtype))
         ref = orc.step(xs)
         worst = max(worst, compare_frame(layer, ref, dtype, t=t, tag=tag, keep_stats=keep_stats,
@@ -100,27 +100,34 @@ def rect64():
     return wl, frames, stats
 
 
+PIPE = pytest.mark.parametrize("split", [False, True], ids=["fused", "split"])
+
+
+@PIPE
 @pytest.mark.parametrize("block", [1, 4, 8])
 @pytest.mark.parametrize("density", [0.1, 0.25, 0.5])
-def test_rect64_bf16_density_sweep(rect64, block, density):
+def test_rect64_bf16_density_sweep(rect64, block, density, split):
     wl, frames, stats = rect64
     eps = eps_for_density(stats, block, 128, 96, density)
     worst, dens = run_single(frames, wl.weights()[0], dtype="bf16", eps=eps, block=block,
-                             tag=f"rect64 b={block} d={density}", keep_stats=(block != 8))
+                             tag=f"rect64 b={block} d={density} split={split}", keep_stats=(block != 8),
+                             split=split)
     assert abs(np.mean(dens[1:]) - density) < 0.1
 
 
-def test_rect64_full_sequence_with_reset(rect64):
+@PIPE
+def test_rect64_full_sequence_with_reset(rect64, split):
     wl, _, stats = rect64
     frames = list(wl.video(32))
     eps = eps_for_density(stats, 8, 128, 96, 0.25)
     run_single(frames, wl.weights()[0], dtype="bf16", eps=eps, block=8, keep_stats=False,
-               tag="rect64 32 frames", resets=(16,))
+               tag="rect64 32 frames", resets=(16,), split=split)
 
 
+@PIPE
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
-@pytest.mark.parametrize("block", [1, 8])
-def test_integer_video_bit_exact(dtype, block):
+@pytest.mark.parametrize("block", [1, 8, 16])
+def test_integer_video_bit_exact(dtype, block, split):
     """Integer-valued frames and weights: every product and sum is exact, so z is bit-exact."""
     rng = np.random.Generator(np.random.PCG64(77))
     c = 64
@@ -133,16 +140,18 @@ def test_integer_video_bit_exact(dtype, block):
         x[0, y0:y0 + 20, 30:60] = rng.integers(0, 8, (20, 30, c))
         frames.append(x)
     run_single(frames, w, dtype=dtype, eps=3.0, block=block, exact_z=True,
-               tag=f"integer {dtype} b={block}")
+               tag=f"integer {dtype} b={block}", split=split)
 
 
-def test_determinism(rect64):
+@PIPE
+def test_determinism(rect64, split):
     wl, frames, stats = rect64
     eps = eps_for_density(stats, 4, 128, 96, 0.25)
     outs = []
     for rep in range(2):
         ws = weight_storage(wl.weights()[0], "bf16")
-        layer = S.SkipConv(to_device(ws, "bf16"), n=1, h=128, w=96, eps=eps, block=4, keep_stats=True)
+        layer = S.SkipConv(to_device(ws, "bf16"), n=1, h=128, w=96, eps=eps, block=4, keep_stats=True,
+                           split=split)
         rec = []
         for t, f in enumerate(frames[:8]):
             say(f"[determinism] rep {rep} frame {t}")
@@ -156,7 +165,8 @@ def test_determinism(rect64):
         assert np.array_equal(la, lb) and np.array_equal(sa.view(np.uint32), sb.view(np.uint32))
 
 
-def test_nan_frame_and_reset():
+@PIPE
+def test_nan_frame_and_reset(split):
     rng = np.random.Generator(np.random.PCG64(90))
     c = 32
     w = syn.he_weights(32, c, 3, seed=91)
@@ -166,12 +176,12 @@ def test_nan_frame_and_reset():
     x2 = rng.random((1, 24, 20, c), dtype=np.float32)
     for dtype in ("f32", "bf16"):
         run_single([x0, x1, x2, x2], w, dtype=dtype, eps=1e4, block=1, resets=(2,),
-                   tag=f"nan {dtype}")
+                   tag=f"nan {dtype}", split=split)
 
 
 # ------------------------------------------------- chained layers (teacher) --
 
-def run_chain(frames, weights, specs, *, dtype, act, epss, block, tag, keep_stats=True):
+def run_chain(frames, weights, specs, *, dtype, act, epss, block, tag, keep_stats=True, split=False):
     """Each layer is compared with an oracle layer fed the GPU's own input for that layer."""
     n, h, w, _ = frames[0].shape
     layers, orcs = [], []
@@ -180,7 +190,7 @@ def run_chain(frames, weights, specs, *, dtype, act, epss, block, tag, keep_stat
         last = i == len(weights) - 1
         lay, orc = _layer_pair(wt, n=n, h=hh, w=ww, dtype=dtype, eps=epss[i], block=block,
                                stride=sp.stride, groups=sp.groups, keep_stats=keep_stats,
-                               act_out="none" if last else act)
+                               act_out="none" if last else act, split=split)
         layers.append(lay)
         orcs.append(orc)
         hh, ww = lay.h_out, lay.w_out
@@ -207,25 +217,28 @@ def run_chain(frames, weights, specs, *, dtype, act, epss, block, tag, keep_stat
     return worst
 
 
-def test_mbconv192_pointwise_then_depthwise():
+@PIPE
+def test_mbconv192_pointwise_then_depthwise(split):
     wl = syn.workloads()["mbconv192"]
     frames = list(wl.video(12))
     ws = wl.weights()
     run_chain(frames, ws, wl.layers, dtype="bf16", act="identity", epss=[2.0, 1.5], block=8,
-              tag="mbconv192")
+              tag="mbconv192", split=split)
 
 
-def test_stack6_relu_strided():
+@PIPE
+def test_stack6_relu_strided(split):
     wl = syn.workloads()["stack6"]
     frames = list(wl.video(5))
     sched = syn.eps_schedule(6) * 0.5
     run_chain(frames, wl.weights(), wl.layers, dtype="bf16", act="relu", epss=list(sched), block=1,
-              tag="stack6")
+              tag="stack6", split=split)
 
 
 # --------------------------------------------------- full size, sampled z --
 
-def test_blob128_full_size_sampled():
+@PIPE
+def test_blob128_full_size_sampled(split):
     """4 x 512 x 512 x 128 bf16, 16 x 16 blocks: gate outputs in full, z at sampled sites."""
     wl = syn.workloads()["blob128"]
     nfr = 3
@@ -235,7 +248,7 @@ def test_blob128_full_size_sampled():
     wf = O.bf16_bits_to_f32(wbits).astype(np.float64)
     stats = oracle_stats(frames[:2], (128, 128, 3, 3), dtype="bf16")
     eps = eps_for_density(stats, 16, 512, 512, 0.25)
-    layer = S.SkipConv(to_device(wbits, "bf16"), n=4, h=512, w=512, eps=eps, block=16)
+    layer = S.SkipConv(to_device(wbits, "bf16"), n=4, h=512, w=512, eps=eps, block=16, split=split)
     rng = np.random.Generator(np.random.PCG64(5))
     ns = 3000
     sn, si, sj = rng.integers(0, 4, ns), rng.integers(0, 512, ns), rng.integers(0, 512, ns)
@@ -245,7 +258,7 @@ def test_blob128_full_size_sampled():
     prev = None
     for t, f in enumerate(frames):
         xs = syn.to_storage(f, "bf16")
-        say(f"[blob128] frame {t} eps={eps:.4g}")
+        say(f"[blob128] frame {t} eps={eps:.4g} fused={layer.fused}")
         z = layer.step(to_device(xs, "bf16"))
         x32 = O.bf16_bits_to_f32(xs)
         ref = prev is None
@@ -304,8 +317,9 @@ EDGE = [
 ]
 
 
+@PIPE
 @pytest.mark.parametrize("case", EDGE, ids=[f"edge{i}" for i in range(len(EDGE))])
-def test_edge_geometries(case):
+def test_edge_geometries(case, split):
     n, h, w, ci, co, k, s, pad, g, b, dtype, p, sup = case
     rng = np.random.Generator(np.random.PCG64(1000 + sum(case[:10])))
     wt = rng.normal(0, (2.0 / (k * k * ci / g)) ** 0.5, (co, ci // g, k, k)).astype(np.float32)
@@ -319,17 +333,18 @@ def test_edge_geometries(case):
         frames.append(x)
     eps = 0.5 if p == 2 else 2.0
     run_single(frames, wt, dtype=dtype, eps=eps, block=b, stride=s, pad=pad, groups=g, norm_p=p,
-               support=sup, tag=f"edge {case}", resets=(3,))
+               support=sup, tag=f"edge {case}", resets=(3,), split=split)
 
 
-def test_force_dense_equals_eps0_on_changing_frames():
+@PIPE
+def test_force_dense_equals_eps0_on_changing_frames(split):
     """FORCE_DENSE runs every block; on frames that change everywhere that is the eps = 0 layer."""
     rng = np.random.Generator(np.random.PCG64(2024))
     w = syn.he_weights(32, 32, 3, seed=7)
     frames = [rng.random((1, 20, 20, 32), dtype=np.float32) for _ in range(4)]
     ws = weight_storage(w, "bf16")
     layer = S.SkipConv(to_device(ws, "bf16"), n=1, h=20, w=20, eps=1e9, block=4, keep_stats=True,
-                       force_dense=True)
+                       force_dense=True, split=split)
     orc = O.SkipConvOracle(ws, n=1, h=20, w=20, eps=0.0, block=4, dtype="bf16")
     for t, f in enumerate(frames):
         xs = syn.to_storage(f, "bf16")
@@ -341,8 +356,9 @@ def test_force_dense_equals_eps0_on_changing_frames():
     layer.close()
 
 
+@PIPE
 @pytest.mark.parametrize("block,groups,k", [(1, 1, 1), (8, 1, 1), (4, 1, 3), (1, 32, 1), (2, 32, 3)])
-def test_operand_rounding_bit_exact(block, groups, k):
+def test_operand_rounding_bit_exact(block, groups, k, split):
     """bf16 layers convolve bf16_rne(x_t - x_{t-1}): with a one-hot (identity) kernel and
     z_{t-1} = 0, the update of frame 3 must equal the oracle's rounded residual bit for bit."""
     rng = np.random.Generator(np.random.PCG64(4242 + block + groups + k))
@@ -352,10 +368,16 @@ def test_operand_rounding_bit_exact(block, groups, k):
         w[co, 0 if groups > 1 else co, k // 2, k // 2] = 1.0
     ws = weight_storage(w, "bf16")
     zero = np.zeros((1, 16, 16, c), np.float32)
-    u = syn.to_storage(rng.normal(0, 1, (1, 16, 16, c)).astype(np.float32), "bf16")
-    v = syn.to_storage(rng.normal(0, 1, (1, 16, 16, c)).astype(np.float32) * 3, "bf16")
+    u32 = rng.normal(0, 1, (1, 16, 16, c)).astype(np.float32)
+    v32 = rng.normal(0, 1, (1, 16, 16, c)).astype(np.float32) * 3
+    # exact round-half cases: 1 - (256 + 4m) = -(255 + 4m) lies halfway between bf16 neighbours
+    u32[0, :4] = 1.0
+    v32[0, :4] = (256.0 + 4.0 * rng.integers(0, 60, (4, 16, c))).astype(np.float32)
+    v32[0, 4, :, :8] = -v32[0, 0, :, :8]
+    u = syn.to_storage(u32, "bf16")
+    v = syn.to_storage(v32, "bf16")
     layer = S.SkipConv(to_device(ws, "bf16"), n=1, h=16, w=16, groups=groups, eps=float("inf"),
-                       block=block)
+                       block=block, split=split)
     say(f"[operand rounding] b={block} g={groups} k={k}")
     layer.step(to_device(syn.to_storage(zero, "bf16"), "bf16"))   # reference frame: z = 0
     layer.step(to_device(u, "bf16"))                                # gated off; x_{t-1} <- u
@@ -367,3 +389,17 @@ def test_operand_rounding_bit_exact(block, groups, k):
     got = z.cpu().numpy()
     assert np.array_equal(got.view(np.uint32), exp.view(np.uint32))
     layer.close()
+
+
+def test_pipeline_selection():
+    """The fused single-pass kernel is chosen for dense bf16 layers with C_in % 32 == 0,
+    blocks <= 16 and at most four tiles per CU; SPLIT_PIPELINE forces the three-kernel pipeline."""
+    w = to_device(weight_storage(syn.he_weights(64, 64, 3, seed=1), "bf16"), "bf16")
+    assert S.SkipConv(w, n=1, h=32, w=32, block=8).fused
+    assert not S.SkipConv(w, n=1, h=32, w=32, block=8, split=True).fused
+    assert not S.SkipConv(w, n=1, h=64, w=64, block=32).fused
+    assert not S.SkipConv(w, n=4, h=512, w=512, block=16).fused
+    w16 = to_device(weight_storage(syn.he_weights(16, 64, 3, seed=1), "bf16"), "bf16")
+    assert not S.SkipConv(w16, n=1, h=32, w=32, block=8).fused
+    w3 = to_device(weight_storage(syn.he_weights(64, 3, 3, seed=1), "bf16"), "bf16")
+    assert not S.SkipConv(w3, n=1, h=32, w=32, block=1).fused
