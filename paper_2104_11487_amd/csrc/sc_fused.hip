@@ -19,8 +19,8 @@
 //   5. MFMA product over the active rows only (Sec. 4.2: im2col restricted to
 //      the non-sparse columns, never materialised: A fragments are read from
 //      the LDS halo at each row's pixel + tap offset; rows past the active
-//      count read a zero pixel), fragments read one k-step ahead; the old z of
-//      the lane's outputs is fetched before the product starts;
+//      count read a zero pixel); the old z of the lane's outputs is fetched
+//      before the product starts;
 //   6. epilogue: z (+)= U at the active sites, activation output refreshed.
 //
 // Inactive tiles stop after step 4, so the hardware dispatcher balances the
@@ -258,42 +258,62 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
       const int nks = min(p.kc, p.ksteps - ks0);
       const uint8_t* bbuf =
           ldsb + (size_t)(chunk % p.nbuf) * p.kc * NTN * 1024 + (wn * WN) * 1024 + lane * 16;
-      int tap = ks0 / csteps, cc = ks0 - tap * csteps;
-      bf16x8 acur[WM], bcur[WN];
-      {
-        const int kh = tap / k, kw = tap - kh * k;
-        const int toff = kh * hw + kw, coff = cc * 64;
+      // walk the k-steps (kh, kw, cc) incrementally, kU at a time: the fragment
+      // reads of a group are all issued before its MFMAs, so LDS latency is
+      // paid once per group rather than once per k-step
+      constexpr int kU = 4;
+      const int tap0 = ks0 / csteps;
+      int cc = ks0 - tap0 * csteps, kh = tap0 / k, kw = tap0 - (tap0 / k) * k;
+      const uint8_t* bptr = bbuf;
+      int kk = 0;
+      for (; kk + kU <= nks; kk += kU) {
+        bf16x8 a[kU][WM], bfr[kU][WN];
 #pragma unroll
-        for (int j = 0; j < WN; ++j) bcur[j] = *reinterpret_cast<const bf16x8*>(bbuf + j * 1024);
+        for (int u = 0; u < kU; ++u) {
+          const int off = (kh * hw + kw), coff = cc * 64;
 #pragma unroll
-        for (int i = 0; i < WM; ++i)
-          acur[i] = *reinterpret_cast<const bf16x8*>(halo + abase[i] + toff * tapmul[i] + coff);
-      }
-      for (int kk = 0; kk < nks; ++kk) {
-        // fragments of the next k-step (the last step re-reads its own)
-        const bool more = kk + 1 < nks;
-        if (more && ++cc == csteps) {
-          cc = 0;
-          ++tap;
+          for (int j = 0; j < WN; ++j) bfr[u][j] = *reinterpret_cast<const bf16x8*>(bptr + (u * NTN + j) * 1024);
+#pragma unroll
+          for (int i = 0; i < WM; ++i)
+            a[u][i] = *reinterpret_cast<const bf16x8*>(halo + abase[i] + off * tapmul[i] + coff);
+          if (++cc == csteps) {
+            cc = 0;
+            if (++kw == k) {
+              kw = 0;
+              ++kh;
+            }
+          }
         }
-        const int kn = more ? kk + 1 : kk;
-        const int kh = tap / k, kw = tap - kh * k;
-        const int toff = kh * hw + kw, coff = cc * 64;
-        bf16x8 anxt[WM], bnxt[WN];
 #pragma unroll
-        for (int j = 0; j < WN; ++j) bnxt[j] = *reinterpret_cast<const bf16x8*>(bbuf + (kn * NTN + j) * 1024);
+        for (int u = 0; u < kU; ++u)
+#pragma unroll
+          for (int i = 0; i < WM; ++i)
+#pragma unroll
+            for (int j = 0; j < WN; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[u][i], bfr[u][j], acc[i][j], 0, 0, 0);
+        bptr += kU * NTN * 1024;
+      }
+      for (; kk < nks; ++kk) {
+        const int off = (kh * hw + kw), coff = cc * 64;
+        bf16x8 a[WM], bfr[WN];
+#pragma unroll
+        for (int j = 0; j < WN; ++j) bfr[j] = *reinterpret_cast<const bf16x8*>(bptr + j * 1024);
 #pragma unroll
         for (int i = 0; i < WM; ++i)
-          anxt[i] = *reinterpret_cast<const bf16x8*>(halo + abase[i] + toff * tapmul[i] + coff);
+          a[i] = *reinterpret_cast<const bf16x8*>(halo + abase[i] + off * tapmul[i] + coff);
 #pragma unroll
         for (int i = 0; i < WM; ++i)
 #pragma unroll
           for (int j = 0; j < WN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(acur[i], bcur[j], acc[i][j], 0, 0, 0);
-#pragma unroll
-        for (int j = 0; j < WN; ++j) bcur[j] = bnxt[j];
-#pragma unroll
-        for (int i = 0; i < WM; ++i) acur[i] = anxt[i];
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], bfr[j], acc[i][j], 0, 0, 0);
+        bptr += NTN * 1024;
+        if (++cc == csteps) {
+          cc = 0;
+          if (++kw == k) {
+            kw = 0;
+            ++kh;
+          }
+        }
       }
     }
     if (chunk + 1 < p.nchunks) __syncthreads();  // next chunk landed; this buffer free
