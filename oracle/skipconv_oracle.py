@@ -29,11 +29,13 @@ rest of the design notes):
 * norm order p is a parameter: p = 2 compares sum(r^2) over the support with
   eps^2; p = 1 (the paper's default) compares sum(|r|) with eps.
 * canonical statistic arithmetic, so that gate masks are reproducible bit for
-  bit: residual r = fl32(x_t - x_prev); per-pixel sum over channels in
-  ascending channel order, in float32, one rounding per multiply and per add
-  (no fused multiply-add); then the support sum over taps (kh, kw) in row-major
-  order, in float32, out-of-frame taps contributing nothing; the comparison is
-  done exactly in float64 (eps is a float32, so eps*eps is exact in float64).
+  bit: residual r = fl32(x_t - x_prev); per pixel, the channel terms are
+  summed in chunks of 8 consecutive channels (ascending within a chunk), and
+  the chunk sums added in ascending chunk order, all in float32 with one
+  rounding per multiply and per add (no fused multiply-add); then the support
+  sum over taps (kh, kw) in row-major order, in float32, out-of-frame taps
+  contributing nothing; the comparison is done exactly in float64 (eps is a
+  float32, so eps*eps is exact in float64).
 * a NaN statistic turns the gate on, so a NaN input reaches z instead of being
   silently skipped.
 * blocks are anchored at output (0, 0); partial edge blocks pool the sites they
@@ -60,6 +62,7 @@ import numpy as np
 
 F32 = np.float32
 F64 = np.float64
+CHUNK = 8  # channels per chunk in the canonical order of the gate statistic
 
 # ----------------------------------------------------------------------------
 # Storage dtypes. bf16 values travel as their raw 16-bit patterns (uint16).
@@ -123,19 +126,27 @@ def residual(x_t: np.ndarray, x_prev: np.ndarray) -> np.ndarray:
 
 
 def pixel_stat(r: np.ndarray, norm_p: int) -> np.ndarray:
-    """Per-pixel part of the support norm (Eq. 5): sum over channels, in order.
+    """Per-pixel part of the support norm (Eq. 5): sum over channels in the canonical order.
 
-    r: (N, H, W, C) float32. Returns (N, H, W) float32 holding
-    sum_c r^2 (p = 2) or sum_c |r| (p = 1), accumulated from c = 0 upward in
-    float32 with the multiply and the add rounded separately.
+    r: (N, H, W, C) float32. Returns (N, H, W) float32 holding sum_c r^2
+    (p = 2) or sum_c |r| (p = 1). Canonical order: the channels are taken in
+    chunks of CHUNK consecutive channels (the last chunk may be shorter);
+    within a chunk the terms are added in ascending channel order starting
+    from +0, and the chunk sums are then added in ascending chunk order
+    starting from +0. Every multiply and every add is rounded to float32
+    separately (no fused multiply-add).
     """
     if norm_p not in (1, 2):
         raise ValueError("norm_p must be 1 or 2")
     acc = np.zeros(r.shape[:3], dtype=np.float32)
-    for c in range(r.shape[3]):
-        v = r[..., c]
-        term = np.multiply(v, v, dtype=np.float32) if norm_p == 2 else np.abs(v)
-        acc = np.add(acc, term, dtype=np.float32)
+    nc = r.shape[3]
+    for c0 in range(0, nc, CHUNK):
+        part = np.zeros(r.shape[:3], dtype=np.float32)
+        for c in range(c0, min(c0 + CHUNK, nc)):
+            v = r[..., c]
+            term = np.multiply(v, v, dtype=np.float32) if norm_p == 2 else np.abs(v)
+            part = np.add(part, term, dtype=np.float32)
+        acc = np.add(acc, part, dtype=np.float32)
     return acc
 
 

@@ -85,6 +85,22 @@ def test_bf16_widen_exact():
 # Gate statistic (Eq. 5)
 # ----------------------------------------------------------------------------
 
+def test_pixel_stat_canonical_order():
+    """The canonical order (chunks of 8 channels, ascending within and across chunks) is
+    observable in fp32: a value that cancels inside one chunk order differs from another order."""
+    r = np.zeros((1, 1, 1, 16), np.float32)
+    r[..., 0] = 1.0
+    r[..., 1:8] = 2.0 ** -13   # each square 2^-26: lost against 1.0 one at a time
+    r[..., 8:16] = 2.0 ** -13  # next chunk: 8 * 2^-26 = 2^-23 survives as a chunk sum
+    a = O.pixel_stat(r, 2)[0, 0, 0]
+    assert a == np.float32(1.0) + np.float32(2.0 ** -23)
+    seq = np.float32(0.0)
+    for v in r[0, 0, 0]:
+        seq = np.float32(seq + np.float32(v * v))
+    assert seq == np.float32(1.0)  # plain left-to-right order loses every small term
+    assert O.CHUNK == 8
+
+
 @pytest.mark.parametrize("p", [1, 2])
 def test_pixel_stat_integer_exact(p):
     rng = _rng(2)
