@@ -7,9 +7,9 @@
 //      the copy overlaps the gate work;
 //   2. halo: one thread per input pixel of the tile's halo loads its channels
 //      of x_t and x_{t-1} (16-byte loads, all in flight together), forms
-//      r = x_t - x_{t-1} in fp32 (Eq. 2), sums the statistic terms over the
-//      channels in ascending order in registers (canonical arithmetic, one
-//      rounding per multiply and per add), writes rho = bf16_rne(r) to an LDS
+//      r = x_t - x_{t-1} in fp32 (Eq. 2), sums the statistic terms in the
+//      canonical order in registers (8-channel chunk sums in ascending order,
+//      one rounding per multiply and per add), writes rho = bf16_rne(r) to an LDS
 //      halo kept for the product, and copies owned pixels of x_t into the
 //      spare x_{t-1} slot;
 //   3. gate (Eq. 5): support sums over taps in row-major order, exact fp64
@@ -104,7 +104,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
   for (int i = threadIdx.x; i < (p.pstride >> 4); i += kThreads)
     *reinterpret_cast<u32x4*>(halo + (size_t)p.zero_pix * p.pstride + i * 16) = u32x4{0u, 0u, 0u, 0u};
 
-  // 2. halo: one thread per pixel, channels in registers, statistic summed in order
+  // 2. halo: one thread per pixel, channels in registers, statistic in canonical order
   const uint16_t* xt = static_cast<const uint16_t*>(g.x_t);
   const uint16_t* xp = static_cast<const uint16_t*>(g.x_prev);
   uint16_t* keep = static_cast<uint16_t*>(g.x_keep);
@@ -137,16 +137,18 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
           const uint32_t wt[4] = {vt[j].x, vt[j].y, vt[j].z, vt[j].w};
           const uint32_t wpv[4] = {vp[j].x, vp[j].y, vp[j].z, vp[j].w};
           uint32_t outw[4];
+          float part = 0.0f;  // chunk sum: this chunk's 8 channels in ascending order
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            // channels 2e (low half) and 2e + 1 (high half), in ascending order
+            // channels 2e (low half) and 2e + 1 (high half)
             const float r0 = __fsub_rn(__uint_as_float(wt[e] << 16), __uint_as_float(wpv[e] << 16));
             const float r1 =
                 __fsub_rn(__uint_as_float(wt[e] & 0xffff0000u), __uint_as_float(wpv[e] & 0xffff0000u));
-            acc = add_rn(acc, term(r0, g.norm_p));
-            acc = add_rn(acc, term(r1, g.norm_p));
+            part = add_rn(part, term(r0, g.norm_p));
+            part = add_rn(part, term(r1, g.norm_p));
             outw[e] = pack_bf16(r0, r1);
           }
+          acc = add_rn(acc, part);  // chunk sums in ascending chunk order
           rq = u32x4{outw[0], outw[1], outw[2], outw[3]};
           if (own) *reinterpret_cast<uint4*>(keep + base + (c0 + j) * 8) = vt[j];
         }

@@ -9,15 +9,16 @@
 //             "non-sparse columns" of the im2col product)
 //
 // Statistic arithmetic is canonical so that masks are reproducible bit for
-// bit: fp32 r; per pixel a[q] = sum over channels in ascending order (one
-// rounding per multiply and per add, no FMA); s[o] = sum of a over the taps
+// bit: fp32 r; per pixel a[q] = chunk sums of 8 consecutive channels (terms
+// added in ascending order), then the chunk sums added in ascending order,
+// one rounding per multiply and per add, no FMA; s[o] = sum of a over the taps
 // (kh, kw) in row-major order, in fp32; the threshold comparison in fp64.
 //
-// One workgroup owns a TS x TS tile of output sites (whole blocks). It loads
-// the input halo of its tile in batches of rows with coalesced 16-byte loads
-// (several in flight per thread), squares the residual into an LDS staging
-// area laid out [pixel][channel] with 16-byte aligned pixel rows, and then one
-// thread per halo pixel sums its channels in order, four per LDS read. Input pixels
+// One workgroup owns a TS x TS tile of output sites (whole blocks). One
+// thread takes one 8-channel chunk of one halo pixel at a time (a 16-byte
+// load of each frame for bf16; consecutive threads read consecutive chunks,
+// eight chunks in flight per thread), forms the chunk sum and parks it in LDS;
+// then one thread per halo pixel adds its chunk sums in order. Input pixels
 // the tile owns are copied into the spare x_{t-1} slot on the way (ping-pong:
 // the slot being read is never written in the same step). Every workgroup
 // then writes its block flags. A second, one-workgroup kernel scans all
@@ -34,63 +35,93 @@ namespace sc {
 namespace {
 
 constexpr int kGateThreads = 256;
-// Stage the per-channel terms of `rows` halo rows into LDS ([pixel][channel],
-// cs floats per pixel). Loads of kUnroll chunks are issued before any is used.
+// Per-chunk partial sums of the tile's halo: one item = one chunk of kChunk
+// channels of one halo pixel (consecutive items = consecutive chunks, so the
+// loads of a wave are contiguous). kItems items per thread have their loads in
+// flight together. VEC = kChunk (vector path, c % kChunk == 0) or 1 (scalar).
 template <typename T, int VEC>
-__device__ void stage_rows(const GateParams& p, int n, int hb0, int rows, int iy0, int ix0, int hw,
-                           int xs, int xe, int own_y0, int own_y1, int own_x0, int own_x1,
-                           float* stage, int cs, bool copy_in_halo) {
+__device__ void halo_partials(const GateParams& p, int n, int iy0, int ix0, int hh, int hw, int own_y0,
+                              int own_y1, int own_x0, int own_x1, float* part) {
+  // bf16 chunks stay packed (one uint4 per frame) until they are consumed
+  constexpr bool kPacked = sizeof(T) == 2 && VEC == kChunk;
+  constexpr int kItems = kPacked ? 8 : 4;
   const T* xt = static_cast<const T*>(p.x_t);
   const T* xp = static_cast<const T*>(p.x_prev);
   T* keep = static_cast<T*>(p.x_keep);
   const int c = p.c;
-  const int nchunk = (xe - xs) * c / VEC;
-  const int total = rows * nchunk;
-  for (int base = 0; base < total; base += kGateThreads * kUnroll) {
-    float vt[kUnroll][VEC], vp[kUnroll][VEC];
-    size_t off[kUnroll];
-    int dst[kUnroll];
-    bool valid[kUnroll], own[kUnroll];
+  const int nchk = (c + kChunk - 1) / kChunk;
+  const int total = hh * hw * nchk;
+  for (int base = 0; base < total; base += kGateThreads * kItems) {
+    uint4 raw_t[kPacked ? kItems : 1], raw_p[kPacked ? kItems : 1];
+    float vt[kPacked ? 1 : kItems][kChunk], vp[kPacked ? 1 : kItems][kChunk];
+    size_t off[kItems];
+    int slot[kItems], nel[kItems];
+    bool in[kItems], own[kItems];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
+    for (int u = 0; u < kItems; ++u) {
       const int idx = base + u * kGateThreads + threadIdx.x;
-      const int row = idx / nchunk;
-      const int ch = idx - row * nchunk;
-      const int y = iy0 + hb0 + row;
-      valid[u] = idx < total && y >= 0 && y < p.h;
-      const int e = ch * VEC;
-      const int px = e / c;
-      const int ci = e - px * c;
-      const int x = xs + px;
-      off[u] = valid[u] ? ((size_t)(n * p.h + y) * p.w + x) * c + ci : 0;
-      dst[u] = (row * hw + (x - ix0)) * cs + ci;
-      own[u] = copy_in_halo && y >= own_y0 && y < own_y1 && x >= own_x0 && x < own_x1;
-      if (valid[u]) {
-        load_vec<T, VEC>(xt, off[u], vt[u]);
-        if (p.reference) {
-#pragma unroll
-          for (int j = 0; j < VEC; ++j) vp[u][j] = 0.0f;
+      const int px = idx / nchk, ch = idx - px * nchk;
+      const int hy = px / hw, hx = px - hy * hw;
+      const int y = iy0 + hy, x = ix0 + hx;
+      in[u] = idx < total && y >= 0 && y < p.h && x >= 0 && x < p.w;
+      slot[u] = idx < total ? px * p.stage_stride + ch : -1;
+      nel[u] = min(kChunk, c - ch * kChunk);
+      off[u] = in[u] ? ((size_t)(n * p.h + y) * p.w + x) * c + ch * kChunk : 0;
+      own[u] = in[u] && p.copy_in_halo && y >= own_y0 && y < own_y1 && x >= own_x0 && x < own_x1;
+      if (kPacked) {
+        raw_t[kPacked ? u : 0] = uint4{0u, 0u, 0u, 0u};
+        raw_p[kPacked ? u : 0] = uint4{0u, 0u, 0u, 0u};
+        if (in[u]) {
+          raw_t[kPacked ? u : 0] = *reinterpret_cast<const uint4*>(xt + off[u]);
+          if (!p.reference) raw_p[kPacked ? u : 0] = *reinterpret_cast<const uint4*>(xp + off[u]);
+        }
+      } else if (in[u]) {
+        const int uu = kPacked ? 0 : u;
+        if (VEC == kChunk) {
+          load_vec<T, kChunk>(xt, off[u], vt[uu]);
+          if (!p.reference) load_vec<T, kChunk>(xp, off[u], vp[uu]);
+          else
+            for (int j = 0; j < kChunk; ++j) vp[uu][j] = 0.0f;
         } else {
-          load_vec<T, VEC>(xp, off[u], vp[u]);
+#pragma unroll
+          for (int j = 0; j < kChunk; ++j) {
+            vt[uu][j] = j < nel[u] ? Elem<T>::load1(xt, off[u] + j) : 0.0f;
+            vp[uu][j] = (j < nel[u] && !p.reference) ? Elem<T>::load1(xp, off[u] + j) : 0.0f;
+          }
         }
       }
     }
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      if (!valid[u]) continue;
-      float tv[VEC];
+    for (int u = 0; u < kItems; ++u) {
+      if (slot[u] < 0) continue;
+      float part_u = 0.0f;
+      if (in[u]) {
+        float r[kChunk];
+        if (kPacked) {
+          const uint4 a = raw_t[kPacked ? u : 0], b = raw_p[kPacked ? u : 0];
+          const uint32_t wa[4] = {a.x, a.y, a.z, a.w}, wb[4] = {b.x, b.y, b.z, b.w};
 #pragma unroll
-      for (int j = 0; j < VEC; ++j) tv[j] = term(__fsub_rn(vt[u][j], vp[u][j]), p.norm_p);
-      float* d = stage + dst[u];
-      if (VEC % 4 == 0) {
+          for (int e = 0; e < 4; ++e) {
+            r[2 * e] = __fsub_rn(__uint_as_float(wa[e] << 16), __uint_as_float(wb[e] << 16));
+            r[2 * e + 1] = __fsub_rn(__uint_as_float(wa[e] & 0xffff0000u), __uint_as_float(wb[e] & 0xffff0000u));
+          }
+        } else {
+          const int uu = kPacked ? 0 : u;
 #pragma unroll
-        for (int j = 0; j < VEC; j += 4)
-          *reinterpret_cast<float4*>(d + j) = make_float4(tv[j], tv[j + 1], tv[j + 2], tv[j + 3]);
-      } else {
+          for (int j = 0; j < kChunk; ++j) r[j] = p.reference ? vt[uu][j] : __fsub_rn(vt[uu][j], vp[uu][j]);
+        }
+        if (VEC == kChunk) {
+          part_u = chunk_sum<kChunk>(r, p.norm_p);
+          if (own[u]) copy_vec<T, kChunk>(keep, xt, off[u]);
+        } else {
 #pragma unroll
-        for (int j = 0; j < VEC; ++j) d[j] = tv[j];
+          for (int j = 0; j < kChunk; ++j)
+            if (j < nel[u]) part_u = add_rn(part_u, term(r[j], p.norm_p));
+          if (own[u])
+            for (int j = 0; j < nel[u]; ++j) keep[off[u] + j] = xt[off[u] + j];
+        }
       }
-      if (own[u]) copy_vec<T, VEC>(keep, xt, off[u]);
+      part[slot[u]] = part_u;
     }
   }
 }
@@ -111,34 +142,30 @@ __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
   const int s = p.stride, k = p.k;
   const int iy0 = oy0 * s - p.pad, ix0 = ox0 * s - p.pad;
   const int hh = (oh - 1) * s + k, hw = (ow - 1) * s + k;
-  const int xs = max(ix0, 0), xe = min(ix0 + hw, p.w);
   // input pixels this tile owns (copied to the spare x_{t-1} slot)
   const int own_y0 = oy0 * s, own_x0 = ox0 * s;
   const int own_y1 = (ty == p.tiles_y - 1) ? p.h : min(p.h, (oy0 + p.ts) * s);
   const int own_x1 = (tx == p.tiles_x - 1) ? p.w : min(p.w, (ox0 + p.ts) * s);
 
   float* a_halo = lds;                 // hh * hw
-  float* stage = lds + p.halo_floats;  // rows_per_batch * hw * cs (16-byte aligned)
-  const int cs = p.stage_stride;
+  float* part = lds + p.halo_floats;   // hh * hw * stage_stride chunk sums
+  const int nchk = (p.c + kChunk - 1) / kChunk;
 
   const int tb_w = p.ts / p.block;
   const int nblk_y = (oh + p.block - 1) / p.block, nblk_x = (ow + p.block - 1) / p.block;
   for (int i = threadIdx.x; i < kMaxTileBlocks; i += kGateThreads) blk_flag[i] = 0u;
 
-  for (int hb0 = 0; hb0 < hh; hb0 += p.rows_per_batch) {
-    const int rows = min(p.rows_per_batch, hh - hb0);
-    if (xe > xs)
-      stage_rows<T, VEC>(p, n, hb0, rows, iy0, ix0, hw, xs, xe, own_y0, own_y1, own_x0, own_x1, stage,
-                         cs, p.copy_in_halo != 0);
-    __syncthreads();
-    for (int q = threadIdx.x; q < rows * hw; q += kGateThreads) {
-      const int row = q / hw, col = q - row * hw;
-      const int y = iy0 + hb0 + row, x = ix0 + col;
-      float a = 0.0f;
-      if (y >= 0 && y < p.h && x >= 0 && x < p.w) a = sum_channels(stage + (size_t)q * cs, p.c);
-      a_halo[(hb0 + row) * hw + col] = a;
+  halo_partials<T, VEC>(p, n, iy0, ix0, hh, hw, own_y0, own_y1, own_x0, own_x1, part);
+  __syncthreads();
+  for (int q = threadIdx.x; q < hh * hw; q += kGateThreads) {
+    const int hy = q / hw, hx = q - hy * hw;
+    const int y = iy0 + hy, x = ix0 + hx;
+    float a = 0.0f;
+    if (y >= 0 && y < p.h && x >= 0 && x < p.w) {
+      const float* pp = part + q * p.stage_stride;
+      for (int ch = 0; ch < nchk; ++ch) a = add_rn(a, pp[ch]);
     }
-    __syncthreads();
+    a_halo[q] = a;
   }
 
   if (!p.copy_in_halo) {
@@ -153,6 +180,7 @@ __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
       keep[off] = xt[off];
     }
   }
+  __syncthreads();
 
   // support statistic, threshold, block flags
   for (int q = threadIdx.x; q < oh * ow; q += kGateThreads) {
@@ -176,12 +204,16 @@ __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
   }
   __syncthreads();
 
+  if (p.split_blocks) {
+    // the tile is part of one block: one flag per tile, OR-ed per block by the compaction
+    if (threadIdx.x == 0) p.tile_flags[tile] = (uint8_t)(blk_flag[0] != 0u);
+    return;
+  }
   const int bi0 = oy0 / p.block, bj0 = ox0 / p.block;
   for (int i = threadIdx.x; i < nblk_y * nblk_x; i += kGateThreads) {
     const int by = i / nblk_x, bx = i - by * nblk_x;
     p.block_mask[((size_t)n * p.hb + bi0 + by) * p.wb + bj0 + bx] = (uint8_t)blk_flag[by * tb_w + bx];
   }
-
 }
 
 // Ordered compaction (one workgroup of kScanThreads): each thread takes a
@@ -190,9 +222,30 @@ __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
 // and every thread writes the indices of its active blocks in ascending order.
 constexpr int kScanThreads = 1024;
 
-__global__ void __launch_bounds__(kScanThreads) compact_kernel(const uint8_t* block_mask, int nb,
-                                                               uint32_t* list, uint32_t* counters) {
+__global__ void __launch_bounds__(kScanThreads) compact_kernel(uint8_t* block_mask, int nb,
+                                                               uint32_t* list, uint32_t* counters,
+                                                               const uint8_t* tile_flags, int n_img, int hb,
+                                                               int wb, int bt, int tiles_y, int tiles_x) {
   __shared__ uint32_t wave_sum[kScanThreads / 64];
+  if (tile_flags) {
+    // blocks larger than the gate tiles: block flag = OR of its bt x bt tiles
+    for (int blk = threadIdx.x; blk < nb; blk += kScanThreads) {
+      const int img = blk / (hb * wb), rem = blk - img * hb * wb;
+      const int bi = rem / wb, bj = rem - bi * wb;
+      uint8_t f = 0;
+      for (int dy = 0; dy < bt; ++dy) {
+        const int ty = bi * bt + dy;
+        if (ty >= tiles_y) break;
+        for (int dx = 0; dx < bt; ++dx) {
+          const int tx = bj * bt + dx;
+          if (tx >= tiles_x) break;
+          f |= tile_flags[((size_t)img * tiles_y + ty) * tiles_x + tx];
+        }
+      }
+      block_mask[blk] = f ? 1 : 0;
+    }
+    __syncthreads();
+  }
   const int nwords = (nb + 15) >> 4;
   const int per = (nwords + kScanThreads - 1) / kScanThreads;
   const int w0 = min(nwords, (int)threadIdx.x * per), w1 = min(nwords, w0 + per);
@@ -245,19 +298,21 @@ static hipError_t launch_gate_t(const GateParams& p, int grid, size_t lds_bytes,
   return hipGetLastError();
 }
 
-hipError_t launch_compact(const uint8_t* block_mask, int nb, uint32_t* list, uint32_t* counters,
-                          hipStream_t st) {
-  hipLaunchKernelGGL(compact_kernel, dim3(1), dim3(kScanThreads), 0, st, block_mask, nb, list, counters);
+hipError_t launch_compact(uint8_t* block_mask, int nb, uint32_t* list, uint32_t* counters,
+                          const uint8_t* tile_flags, int n, int hb, int wb, int bt, int tiles_y,
+                          int tiles_x, hipStream_t st) {
+  hipLaunchKernelGGL(compact_kernel, dim3(1), dim3(kScanThreads), 0, st, block_mask, nb, list, counters,
+                     tile_flags, n, hb, wb, bt, tiles_y, tiles_x);
   return hipGetLastError();
 }
 
 hipError_t launch_gate(const GateParams& p, int dtype, int vec, int grid, size_t lds_bytes,
                        hipStream_t st) {
   if (dtype == 0) {
-    if (vec == 4) return launch_gate_t<float, 4>(p, grid, lds_bytes, st);
+    if (vec == kChunk) return launch_gate_t<float, kChunk>(p, grid, lds_bytes, st);
     return launch_gate_t<float, 1>(p, grid, lds_bytes, st);
   }
-  if (vec == 8) return launch_gate_t<uint16_t, 8>(p, grid, lds_bytes, st);
+  if (vec == kChunk) return launch_gate_t<uint16_t, kChunk>(p, grid, lds_bytes, st);
   return launch_gate_t<uint16_t, 1>(p, grid, lds_bytes, st);
 }
 

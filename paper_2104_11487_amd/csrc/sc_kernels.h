@@ -22,12 +22,14 @@ struct GateParams {
   int h_out, w_out, k, stride, pad, block, hb, wb;
   int ts, tiles_y, tiles_x;     // tile side (sites) and tile grid per image
   int halo_floats;              // LDS floats reserved for the a[] halo
-  int stage_stride;             // LDS floats per staged pixel (>= c, odd)
-  int rows_per_batch;           // halo rows staged at once
+  int stage_stride;             // LDS floats of chunk sums per halo pixel (>= ceil(c/8), odd)
+  int rows_per_batch;           // unused (whole halo staged at once)
   int copy_in_halo;             // 1: every owned input pixel lies in its tile's halo
   int norm_p, support, reference, force_dense, keep_stats;
   double thr;                   // eps^2 (p = 2) or eps (p = 1), exact in fp64
   uint8_t* block_mask;          // N x HB x WB
+  uint8_t* tile_flags;          // N x tiles_y x tiles_x when blocks are larger than tiles
+  int split_blocks;             // 1: ts < block (b % ts == 0): flags per tile, OR-ed by the compaction
   uint32_t* list;               // N x HB x WB (first count entries valid)
   uint32_t* counters;
   float* stat;                  // N x H_out x W_out (keep_stats)
@@ -83,8 +85,11 @@ int prepare_fused(const FusedParams& p);  // create time: LDS attribute; workgro
 hipError_t launch_gate(const GateParams& p, int dtype, int vec, int grid, size_t lds_bytes,
                        hipStream_t st);
 // Ordered compaction of the block flags into the active list and its count.
-hipError_t launch_compact(const uint8_t* block_mask, int nb, uint32_t* list, uint32_t* counters,
-                          hipStream_t st);
+// When tile_flags is non-NULL, block flags are first formed as the OR of the
+// (block / ts)^2 tile flags of each block (tiles_y x tiles_x tiles per image).
+hipError_t launch_compact(uint8_t* block_mask, int nb, uint32_t* list, uint32_t* counters,
+                          const uint8_t* tile_flags, int n, int hb, int wb, int bt, int tiles_y,
+                          int tiles_x, hipStream_t st);
 hipError_t launch_conv(const ConvParams& p, int dtype, bool fast, int grid, hipStream_t st);
 hipError_t launch_conv_halo(const ConvParams& p, const HaloParams& hp, int grid, hipStream_t st);
 int conv_halo_occupancy(const HaloParams& hp);  // resident workgroups per CU (0 on error)

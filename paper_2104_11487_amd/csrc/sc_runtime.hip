@@ -19,7 +19,6 @@ thread_local char g_create_error[256] = "";
 
 constexpr size_t kAlign = 256;
 constexpr size_t kLdsLimit = 60 * 1024;  // dynamic; the gate kernel adds 2 KB static
-constexpr size_t kStageBudget = 36 * 1024;
 constexpr int kMaxCout = 256;
 constexpr long kHaloLdsLimit = 160 * 1024;  // LDS of one gfx950 CU
 constexpr long kFusedLdsLimit = 156 * 1024; // dynamic LDS of the fused kernel (+ ~3 KB static)
@@ -39,7 +38,7 @@ size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
 struct Geometry {
   int pad, h_out, w_out, hb, wb, nb;
-  int ts, tiles_y, tiles_x, gate_grid;
+  int ts, tiles_y, tiles_x, gate_grid, split_blocks;
   int hh_max, hw_max, halo_floats, stage_stride, rows_per_batch;
   size_t gate_lds;
   int copy_in_halo;
@@ -53,8 +52,8 @@ struct Geometry {
   int f_kc, f_nchunks, f_nbuf, f_mw, f_pstride, f_zero_pix, f_off_b, f_off_halo, f_off_a, f_lds;
   int vec;              // gate load width (elements)
   size_t elem;
-  size_t off_wpack, off_slot0, off_slot1, off_z, off_y, off_bmask, off_list, off_ctr, off_stat,
-      off_smask, total;
+  size_t off_wpack, off_slot0, off_slot1, off_z, off_y, off_bmask, off_tflag, off_list, off_ctr,
+      off_stat, off_smask, total;
   size_t wpack_bytes, x_bytes, z_bytes;
   int conv_max_tiles;
 };
@@ -123,31 +122,49 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
   G.elem = d->dtype == SKIPCONV_BF16 ? 2 : 4;
 
   // gate tiling: ts x ts output sites made of whole blocks, about 16 x 16
-  // sites, or 8 x 8 when 16 x 16 tiles would not give every CU two tiles
+  // sites, or 8 x 8 when 16 x 16 tiles would not give every CU two tiles or
+  // their chunk sums would not fit in LDS. LDS: the a[] halo plus one fp32
+  // chunk sum per (halo pixel, 8-channel chunk), odd row stride.
+  const int nchk = (d->c_in + 7) / 8;
+  G.stage_stride = nchk | 1;
+  auto gate_lds_for = [&](int ts) {
+    const long eh = (long)(std::min(ts, G.h_out) - 1) * s + k;  // largest halo actually used
+    const long ew = (long)(std::min(ts, G.w_out) - 1) * s + k;
+    const long halo = (eh * ew + 3) / 4 * 4;
+    return (halo + eh * ew * G.stage_stride) * 4;
+  };
   {
     const int t16 = b <= 16 ? b * (16 / b) : b;
+    const int t8 = b <= 8 ? b * (8 / b) : b;
     const long n16 = (long)d->n * ((G.h_out + t16 - 1) / t16) * ((G.w_out + t16 - 1) / t16);
-    G.ts = (n16 < 512 && b <= 8) ? b * (8 / b) : t16;
+    G.ts = (n16 < 512 && b <= 8) ? t8 : t16;
+    if (gate_lds_for(G.ts) > (long)kLdsLimit && b <= 8) G.ts = t8;
+    // blocks larger than a tile that fits: 16 x 16 (or 8 x 8) tiles, one flag
+    // per tile, OR-ed per block by the compaction kernel
+    G.split_blocks = 0;
+    if (gate_lds_for(G.ts) > (long)kLdsLimit && b > 16) {
+      for (int t : {16, 8})
+        if (b % t == 0 && gate_lds_for(t) <= (long)kLdsLimit) {
+          G.ts = t;
+          G.split_blocks = 1;
+          break;
+        }
+    }
   }
   G.tiles_y = (G.h_out + G.ts - 1) / G.ts;
   G.tiles_x = (G.w_out + G.ts - 1) / G.ts;
   G.gate_grid = d->n * G.tiles_y * G.tiles_x;
-  G.hh_max = (G.ts - 1) * s + k;
-  G.hw_max = G.hh_max;
-  G.halo_floats = G.hh_max * G.hw_max;
-  // staged pixel rows: 16-byte aligned (+4 floats keeps 16 lanes' float4 reads
-  // on distinct banks) when c_in % 4 == 0, else an odd stride
-  G.stage_stride = (d->c_in % 4 == 0) ? d->c_in + 4 : (d->c_in | 1);
-  const size_t row_bytes = (size_t)G.hw_max * G.stage_stride * 4;
-  G.rows_per_batch = (int)std::max<size_t>(1, std::min<size_t>(kStageBudget / row_bytes, G.hh_max));
-  G.halo_floats = (G.halo_floats + 3) / 4 * 4;  // staging area starts 16-byte aligned
-  G.gate_lds = ((size_t)G.halo_floats + (size_t)G.rows_per_batch * G.hw_max * G.stage_stride) * 4;
+  G.hh_max = (std::min(G.ts, G.h_out) - 1) * s + k;
+  G.hw_max = (std::min(G.ts, G.w_out) - 1) * s + k;
+  G.halo_floats = (G.hh_max * G.hw_max + 3) / 4 * 4;
+  G.rows_per_batch = G.hh_max;
+  G.gate_lds = gate_lds_for(G.ts);
   if (G.gate_lds > kLdsLimit)
     return fail(err, SKIPCONV_E_UNSUPPORTED, "gate tile does not fit in LDS (too many channels)");
   if (d->dtype == SKIPCONV_BF16)
     G.vec = (d->c_in % 8 == 0) ? 8 : 1;
   else
-    G.vec = (d->c_in % 4 == 0) ? 4 : 1;
+    G.vec = (d->c_in % 8 == 0) ? 8 : 1;
 
   // does every tile's halo cover the input pixels it owns?
   G.copy_in_halo = 1;
@@ -262,6 +279,7 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
   G.off_y = off;
   if (d->act_out != SKIPCONV_ACT_NONE) off = align_up(off + (size_t)sites * d->c_out * G.elem);
   G.off_bmask = off; off = align_up(off + (size_t)nb + 16);  // zero padding to whole 16-byte words
+  G.off_tflag = off; off = align_up(off + (size_t)G.gate_grid);
   G.off_list = off; off = align_up(off + (size_t)nb * 4);
   G.off_ctr = off; off = align_up(off + sc::kNumCounters * 4);
   G.off_stat = off;
@@ -300,6 +318,7 @@ struct skipconv_layer {
   float* z() { return reinterpret_cast<float*>(ws + g.off_z); }
   void* y() { return d.act_out ? (void*)(ws + g.off_y) : nullptr; }
   uint8_t* bmask() { return reinterpret_cast<uint8_t*>(ws + g.off_bmask); }
+  uint8_t* tflags() { return reinterpret_cast<uint8_t*>(ws + g.off_tflag); }
   uint32_t* list() { return reinterpret_cast<uint32_t*>(ws + g.off_list); }
   uint32_t* ctr() { return reinterpret_cast<uint32_t*>(ws + g.off_ctr); }
   float* stat() { return reinterpret_cast<float*>(ws + g.off_stat); }
@@ -369,9 +388,17 @@ sc::GateParams gate_params(skipconv_layer* h, const void* x_t, bool ref) {
   gp.keep_stats = (d.flags & SKIPCONV_FLAG_KEEP_STATS) ? 1 : 0;
   gp.thr = threshold(d);
   gp.block_mask = h->bmask(); gp.list = h->list(); gp.counters = h->ctr();
+  gp.tile_flags = h->tflags(); gp.split_blocks = g.split_blocks;
   gp.stat = h->stat(); gp.site_mask = h->smask();
 
   return gp;
+}
+
+hipError_t launch_compaction(skipconv_layer* h, hipStream_t st) {
+  const Geometry& g = h->g;
+  return sc::launch_compact(h->bmask(), g.nb, h->list(), h->ctr(), g.split_blocks ? h->tflags() : nullptr,
+                            h->d.n, g.hb, g.wb, g.split_blocks ? h->d.block / g.ts : 0, g.tiles_y, g.tiles_x,
+                            st);
 }
 
 int conv_grid(const skipconv_layer* h) {
@@ -553,7 +580,7 @@ int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t
     h->list_valid = false;
   } else {
     if (e == hipSuccess) e = sc::launch_gate(gp, d.dtype, g.vec, g.gate_grid, g.gate_lds, st);
-    if (e == hipSuccess) e = sc::launch_compact(h->bmask(), g.nb, h->list(), h->ctr(), st);
+    if (e == hipSuccess) e = launch_compaction(h, st);
     if (e != hipSuccess) return hip_fail(h, e, "gate launch");
     if (timing) e = hipEventRecord(h->ev[3 * h->timing_done + 1], st);
     if (e == hipSuccess) {
@@ -633,7 +660,8 @@ static int copy_back(skipconv_t h, void* stream, void* host, const void* dev, si
 // The fused pipeline does not build the ordered list; build it on demand.
 static int ensure_list(skipconv_t h, void* stream) {
   if (h->list_valid) return SKIPCONV_OK;
-  const hipError_t e = sc::launch_compact(h->bmask(), h->g.nb, h->list(), h->ctr(), static_cast<hipStream_t>(stream));
+  const hipError_t e = sc::launch_compact(h->bmask(), h->g.nb, h->list(), h->ctr(), nullptr, 0, 0, 0, 0, 0, 0,
+                                          static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(h, e, "compaction launch");
   h->list_valid = true;
   return SKIPCONV_OK;

@@ -14,25 +14,18 @@ __device__ __forceinline__ float term(float r, int norm_p) {
   return norm_p == 2 ? mul_rn(r, r) : fabsf(r);
 }
 
-// Sum of the staged per-channel terms of one pixel, ascending channel order.
-// Rows are 16-byte aligned when c % 4 == 0, so four terms come per LDS read;
-// the additions stay strictly sequential.
-__device__ __forceinline__ float sum_channels(const float* row, int c) {
-  float acc = 0.0f;
-  if ((c & 3) == 0) {
-    const float4* r4 = reinterpret_cast<const float4*>(row);
-#pragma unroll 4
-    for (int i = 0; i < (c >> 2); ++i) {
-      const float4 v = r4[i];
-      acc = add_rn(acc, v.x);
-      acc = add_rn(acc, v.y);
-      acc = add_rn(acc, v.z);
-      acc = add_rn(acc, v.w);
-    }
-  } else {
-    for (int i = 0; i < c; ++i) acc = add_rn(acc, row[i]);
-  }
-  return acc;
+// Canonical order of the per-pixel statistic: channels in chunks of kChunk
+// consecutive channels; within a chunk the terms are added in ascending
+// order from +0; the chunk sums are then added in ascending chunk order.
+constexpr int kChunk = 8;
+
+// Ordered sum of the terms of up to kChunk consecutive channels (one chunk).
+template <int N>
+__device__ __forceinline__ float chunk_sum(const float* r, int norm_p) {
+  float part = 0.0f;
+#pragma unroll
+  for (int i = 0; i < N; ++i) part = add_rn(part, term(r[i], norm_p));
+  return part;
 }
 
 template <typename T, int VEC>
