@@ -34,6 +34,13 @@ constexpr int kConvThreads = 256;
 constexpr int kRowsPerTile = 64;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float floatx2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// bf16 round-to-nearest-even of two floats, packed (v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2{a, b}, bf16x2));
+}
 
 struct Site {
   int n, oy, ox;
@@ -190,44 +197,60 @@ __global__ void __launch_bounds__(kConvThreads) conv_bf16_kernel(ConvParams p) {
 // ------------------------------------------------------- bf16, halo ----
 //
 // Block tiles (b in {4, 8, 16, 32, 64}, C_in % 32 == 0): a tile is `tr` output
-// rows x b columns of one active block. Its input halo ((tr-1)s+k rows x
-// (b-1)s+k columns x C_in) is loaded once with 16-byte loads, turned into
-// rho = bf16(x_t - x_{t-1}) and stored in LDS with a pixel stride of
-// 2*C_in + 16 bytes (16 consecutive pixels read 16 bytes each on distinct
-// banks). MFMA A fragments are then read straight from the halo: row m of the
-// tile at tap (kh, kw) is halo pixel (ly*s + kh, lx*s + kw), so no im2col copy
-// is made. Waves are laid out WAVES_M x WAVES_N; each owns WM x WN 16x16
-// output tiles and reads its B fragments from the packed weights (L1/L2).
+// rows x b columns of one active block. Per tile:
+//   1. the accumulators start from z_{t-1} of the tile's sites (0 on a
+//      reference frame), loaded straight into the MFMA output layout, so the
+//      read half of the z update overlaps the halo load;
+//   2. the input halo ((tr-1)s+k rows x (b-1)s+k columns x C_in) is loaded with
+//      16-byte loads, eight per thread in flight, turned into
+//      rho = bf16(x_t - x_{t-1}) and stored in LDS with a pixel stride of
+//      2*C_in + 16 bytes (16 consecutive pixels read 16 bytes each on distinct
+//      banks);
+//   3. MFMA A fragments are read straight from the halo (row m of the tile at
+//      tap (kh, kw) is halo pixel (ly*s + kh, lx*s + kw): no im2col copy); B
+//      fragments come from the packed weights (L1/L2) one k-step ahead of use;
+//   4. the accumulators are stored back to z (and the activation output).
+// Waves are laid out WAVES_M x WAVES_N; each owns WM x WN 16x16 output tiles.
 
 template <int WAVES_M, int WAVES_N, int WM, int WN>
-__global__ void __launch_bounds__(64 * WAVES_M * WAVES_N) conv_halo_kernel(ConvParams p, HaloParams hp) {
+__global__ void __launch_bounds__(64 * WAVES_M * WAVES_N) __attribute__((amdgpu_waves_per_eu(2)))
+conv_halo_kernel(ConvParams p, HaloParams hp) {
   extern __shared__ __attribute__((aligned(16))) uint8_t halo[];
   constexpr int kThreads = 64 * WAVES_M * WAVES_N;
-  constexpr int kUnroll = 4;
+  constexpr int kUnroll = WM >= 8 ? 4 : 8;         // halo loads in flight per thread
+  constexpr int kR = WN <= 2 ? 8 : (WN == 3 ? 6 : 4);  // B register ring (kR - 1 k-steps of lookahead), even
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave % WAVES_M, wn = wave / WAVES_M;
   const int r16 = lane & 15, kq = lane >> 4;
   const int b = p.block, s = p.stride, k = p.k, c = p.c;
+  const int lb = __ffs(b) - 1;
   const int tpb = hp.tiles_per_block;
   const int ntiles = (int)p.counters[kCtrCount] * tpb;
   const uint16_t* xt = static_cast<const uint16_t*>(p.x_t);
   const uint16_t* xp = static_cast<const uint16_t*>(p.x_prev);
-  const bf16x8* wp = static_cast<const bf16x8*>(p.wpack);
+  // packed weights through a buffer resource: lane offset in a VGPR, the
+  // (k-step, column tile) offset in an SGPR
+  const __amdgpu_buffer_rsrc_t wrs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p.wpack), 0, p.ksteps * p.ntiles_n * 1024, 0x00020000);
+  const int boff = lane * 16;
+  const int wn0 = __builtin_amdgcn_readfirstlane(wn) * WN;  // first 16-channel output tile
   const int chunks_per_px = c >> 3;
   const int csteps = c >> 5;  // k-steps per tap
+  const int ksteps = p.ksteps;
+  const int ntn = p.ntiles_n;
 
-  // halo pixel of this lane's row in each of its M-tiles, before the tap offset
-  int pix_base[WM];
+  // halo byte offset of this lane's A row in each of its M-tiles, before the tap
+  int abase[WM];
 #pragma unroll
   for (int i = 0; i < WM; ++i) {
     const int m = (wm * WM + i) * 16 + r16;
-    const int ly = m / b, lx = m - ly * b;
-    pix_base[i] = ly * s * hp.hw + lx * s;
+    const int ly = m >> lb, lx = m & (b - 1);
+    abase[i] = (ly * s * hp.hw + lx * s) * hp.pstride + kq * 16;
   }
 
   for (TileWalk tw(ntiles); tw.t < tw.end; tw.t += tw.step) {
-    const int j = tw.t / tpb, band = tw.t - j * tpb;
-    const uint32_t blk = p.list[j];
+    const int j0 = tw.t / tpb, band = tw.t - j0 * tpb;
+    const uint32_t blk = p.list[j0];
     const int per_img = p.hb * p.wb;
     const int n = (int)(blk / per_img);
     const int rem = (int)(blk - (uint32_t)n * per_img);
@@ -236,10 +259,32 @@ __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N) conv_halo_kernel(ConvP
     const int rows_ok = min(hp.tr, p.h_out - oy0), cols_ok = min(b, p.w_out - ox0);
     const int iy0 = oy0 * s - p.pad, ix0 = ox0 * s - p.pad;
 
-    // ---- halo: rho = bf16(x_t - x_{t-1}), zero outside the frame ----
+    // ---- 1. accumulators = z_{t-1} at the tile's sites ----
+    // The product is computed transposed (weights as the MFMA A operand), so
+    // a lane's accumulator holds 4 consecutive output channels of one site:
+    // z moves in 16-byte pieces.
+    auto site = [&](int i) {  // output site of this lane in M-tile i, -1 outside the frame
+      const int m = (wm * WM + i) * 16 + r16;
+      const int ly = m >> lb, lx = m & (b - 1);
+      return (ly < rows_ok && lx < cols_ok) ? (n * p.h_out + oy0 + ly) * p.w_out + ox0 + lx : -1;
+    };
+    floatx4 acc[WM][WN];
+#pragma unroll
+    for (int i = 0; i < WM; ++i) {
+      const int st = site(i);
+#pragma unroll
+      for (int jn = 0; jn < WN; ++jn) {
+        const int col = (wn0 + jn) * 16 + kq * 4;
+        acc[i][jn] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+        if (st >= 0 && !p.reference && col < p.c_out)
+          acc[i][jn] = *reinterpret_cast<const floatx4*>(p.z + (size_t)st * p.c_out + col);
+      }
+    }
+
+    // ---- 2. halo: rho = bf16(x_t - x_{t-1}), zero outside the frame ----
     const int total = hp.hh * hp.hw * chunks_per_px;
     for (int base = 0; base < total; base += kThreads * kUnroll) {
-      float va[kUnroll][8], vb[kUnroll][8];
+      uint4 ra[kUnroll], rb[kUnroll];
       int dst[kUnroll];
       bool in[kUnroll];
 #pragma unroll
@@ -250,79 +295,113 @@ __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N) conv_halo_kernel(ConvP
         const int y = iy0 + hy, x = ix0 + hx;
         in[u] = idx < total && y >= 0 && y < p.h && x >= 0 && x < p.w;
         dst[u] = idx < total ? px * hp.pstride + ch * 16 : -1;
+        ra[u] = uint4{0u, 0u, 0u, 0u};
+        rb[u] = uint4{0u, 0u, 0u, 0u};
         if (in[u]) {
           const size_t off = ((size_t)(n * p.h + y) * p.w + x) * c + ch * 8;
-          Elem<uint16_t>::load8(xt, off, va[u]);
-          if (!p.reference) Elem<uint16_t>::load8(xp, off, vb[u]);
+          ra[u] = *reinterpret_cast<const uint4*>(xt + off);
+          if (!p.reference) rb[u] = *reinterpret_cast<const uint4*>(xp + off);
         }
       }
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
         if (dst[u] < 0) continue;
-        u32x4 q = {0u, 0u, 0u, 0u};
-        if (in[u]) {
-          float r[8];
+        const uint32_t wa[4] = {ra[u].x, ra[u].y, ra[u].z, ra[u].w};
+        const uint32_t wb[4] = {rb[u].x, rb[u].y, rb[u].z, rb[u].w};
+        uint32_t q[4];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) r[e] = p.reference ? va[u][e] : __fsub_rn(va[u][e], vb[u][e]);
-          q.x = f32_to_bf16(r[0]) | (f32_to_bf16(r[1]) << 16);
-          q.y = f32_to_bf16(r[2]) | (f32_to_bf16(r[3]) << 16);
-          q.z = f32_to_bf16(r[4]) | (f32_to_bf16(r[5]) << 16);
-          q.w = f32_to_bf16(r[6]) | (f32_to_bf16(r[7]) << 16);
+        for (int e = 0; e < 4; ++e) {
+          const float r0 = __fsub_rn(__uint_as_float(wa[e] << 16), __uint_as_float(wb[e] << 16));
+          const float r1 = __fsub_rn(__uint_as_float(wa[e] & 0xffff0000u), __uint_as_float(wb[e] & 0xffff0000u));
+          q[e] = pack_bf16(r0, r1);
         }
-        *reinterpret_cast<u32x4*>(halo + dst[u]) = q;
+        *reinterpret_cast<u32x4*>(halo + dst[u]) = u32x4{q[0], q[1], q[2], q[3]};
       }
     }
     __syncthreads();
 
-    // ---- MFMA over K = (kh, kw, ci) ----
-    floatx4 acc[WM][WN];
+    // ---- 3. MFMA over K = (kh, kw, ci) ----
+    // B fragments are loaded kR - 1 k-steps ahead into a ring of registers; the
+    // A fragments of step s + 1 are read from LDS before the MFMAs of step s
+    // (two register sets). The main loop has no data-dependent branches, so the
+    // waits count outstanding loads instead of draining them, and scheduling
+    // barriers keep the compiler from sinking the reads back to their use.
+    bf16x8 bq[kR][WN];
+    bf16x8 aq[2][WM];
+    auto load_b = [&](bf16x8* dst, int ks) {
 #pragma unroll
-    for (int i = 0; i < WM; ++i)
+      for (int jn = 0; jn < WN; ++jn)
+        dst[jn] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(
+                                                 wrs, boff, (ks * ntn + wn0 + jn) * 1024, 0));
+    };
+    int aoff = 0, cc = 0, kw = 0, snext = 0;  // halo offset of the next A step (kh, kw, cc)
+    auto read_a = [&](bf16x8* dst) {
 #pragma unroll
-      for (int jn = 0; jn < WN; ++jn) acc[i][jn] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
-
+      for (int i = 0; i < WM; ++i) dst[i] = *reinterpret_cast<const bf16x8*>(halo + abase[i] + aoff);
+      // advance to the following step without branches; stays on the last step
+      const bool more = ++snext < ksteps;
+      const int c1 = cc + 1;
+      const bool wrap = c1 == csteps;
+      const int kw1 = kw + (wrap ? 1 : 0);
+      const bool wrap2 = kw1 == k;
+      int a1 = aoff + 64;
+      a1 += wrap ? hp.pstride - csteps * 64 : 0;
+      a1 += wrap2 ? (hp.hw - k) * hp.pstride : 0;
+      cc = more ? (wrap ? 0 : c1) : cc;
+      kw = more ? (wrap2 ? 0 : kw1) : kw;
+      aoff = more ? a1 : aoff;
+    };
+    auto mfmas = [&](const bf16x8* a, const bf16x8* bf) {
+#pragma unroll
+      for (int i = 0; i < WM; ++i)
+#pragma unroll
+        for (int jn = 0; jn < WN; ++jn)
+          acc[i][jn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bf[jn], a[i], acc[i][jn], 0, 0, 0);
+    };
+#pragma unroll
+    for (int r = 0; r < kR - 1; ++r) load_b(bq[r], min(r, ksteps - 1));
+    read_a(aq[0]);
     int ks = 0;
-    for (int kh = 0; kh < k; ++kh) {
-      for (int kw = 0; kw < k; ++kw) {
-        const int tap_off = kh * hp.hw + kw;
-        for (int cc = 0; cc < csteps; ++cc, ++ks) {
-          const bf16x8* wk = wp + ((size_t)ks * p.ntiles_n + wn * WN) * 64 + lane;
-          bf16x8 bfr[WN];
+    for (; ks + kR <= ksteps; ks += kR) {
 #pragma unroll
-          for (int jn = 0; jn < WN; ++jn) bfr[jn] = wk[jn * 64];
-          const int coff = (cc * 32 + kq * 8) * 2;
-#pragma unroll
-          for (int i = 0; i < WM; ++i) {
-            const bf16x8 a =
-                *reinterpret_cast<const bf16x8*>(halo + (pix_base[i] + tap_off) * hp.pstride + coff);
-#pragma unroll
-            for (int jn = 0; jn < WN; ++jn)
-              acc[i][jn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bfr[jn], acc[i][jn], 0, 0, 0);
-          }
-        }
+      for (int r = 0; r < kR; ++r) {
+        load_b(bq[(r + kR - 1) % kR], min(ks + r + kR - 1, ksteps - 1));
+        read_a(aq[(r + 1) & 1]);
+        __builtin_amdgcn_sched_barrier(0);
+        mfmas(aq[r & 1], bq[r]);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
+#pragma unroll
+    for (int r = 0; r < kR - 1; ++r)
+      if (r < ksteps - ks) {
+        read_a(aq[(r + 1) & 1]);
+        mfmas(aq[r & 1], bq[r]);
+      }
+    // all waves are done with the halo: the next tile may overwrite it (no
+    // stores are outstanding here, so this barrier waits on nothing in memory)
+    __syncthreads();
 
-    // ---- epilogue: z (+)= acc at the tile's sites inside the output grid ----
+    // ---- 4. store z (+ activation output) ----
 #pragma unroll
     for (int i = 0; i < WM; ++i) {
+      const int st = site(i);
+      if (st < 0) continue;
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int m = (wm * WM + i) * 16 + kq * 4 + v;
-        const int ly = m / b, lx = m - ly * b;
-        if (ly >= rows_ok || lx >= cols_ok) continue;
-        const size_t zrow = ((size_t)(n * p.h_out + oy0 + ly) * p.w_out + ox0 + lx) * p.c_out;
-#pragma unroll
-        for (int jn = 0; jn < WN; ++jn) {
-          const int col = (wn * WN + jn) * 16 + r16;
-          if (col >= p.c_out) continue;
-          const float nv = p.reference ? acc[i][jn][v] : p.z[zrow + col] + acc[i][jn][v];
-          p.z[zrow + col] = nv;
-          if (p.act) store_y<uint16_t>(p.y, zrow + col, activate(nv, p.act));
+      for (int jn = 0; jn < WN; ++jn) {
+        const int col = (wn0 + jn) * 16 + kq * 4;
+        if (col >= p.c_out) continue;
+        const size_t o = (size_t)st * p.c_out + col;
+        *reinterpret_cast<floatx4*>(p.z + o) = acc[i][jn];
+        if (p.act) {
+          const uint32_t lo = f32_to_bf16(activate(acc[i][jn][0], p.act)) |
+                              (f32_to_bf16(activate(acc[i][jn][1], p.act)) << 16);
+          const uint32_t hi = f32_to_bf16(activate(acc[i][jn][2], p.act)) |
+                              (f32_to_bf16(activate(acc[i][jn][3], p.act)) << 16);
+          *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.y) + o) = uint2{lo, hi};
         }
       }
     }
-    __syncthreads();  // the next tile overwrites the halo
   }
 }
 
@@ -545,53 +624,31 @@ int halo_occ_t(const HaloParams& hp) {
 }
 }  // namespace
 
+#define SC_HALO_CONFIGS(X)                                                              \
+  X(0, 1, 1, 8, 1) X(1, 1, 2, 8, 1) X(2, 1, 4, 8, 1) X(3, 1, 4, 8, 2)                    \
+  X(10, 1, 1, 4, 1) X(11, 1, 2, 4, 1) X(12, 1, 4, 4, 1) X(13, 1, 4, 4, 2) X(14, 1, 4, 4, 3) \
+  X(15, 1, 4, 4, 4)                                                                      \
+  X(20, 1, 1, 1, 1) X(21, 1, 2, 1, 1) X(22, 1, 4, 1, 1) X(23, 1, 4, 1, 2) X(24, 1, 4, 1, 3) \
+  X(25, 1, 4, 1, 4)
+
 int conv_halo_occupancy(const HaloParams& hp) {
   switch (hp.config) {
-    case 0: return halo_occ_t<2, 1, 4, 1>(hp);
-    case 1: return halo_occ_t<2, 1, 4, 2>(hp);
-    case 2: return halo_occ_t<2, 1, 4, 4>(hp);
-    case 3: return halo_occ_t<2, 1, 4, 8>(hp);
-    case 4: return halo_occ_t<4, 1, 2, 12>(hp);
-    case 5: return halo_occ_t<4, 1, 2, 16>(hp);
-    case 10: return halo_occ_t<4, 1, 1, 1>(hp);
-    case 11: return halo_occ_t<4, 1, 1, 2>(hp);
-    case 12: return halo_occ_t<4, 1, 1, 4>(hp);
-    case 13: return halo_occ_t<4, 1, 1, 8>(hp);
-    case 14: return halo_occ_t<4, 1, 1, 12>(hp);
-    case 15: return halo_occ_t<4, 1, 1, 16>(hp);
-    case 20: return halo_occ_t<1, 1, 1, 1>(hp);
-    case 21: return halo_occ_t<1, 2, 1, 1>(hp);
-    case 22: return halo_occ_t<1, 4, 1, 1>(hp);
-    case 23: return halo_occ_t<1, 4, 1, 2>(hp);
-    case 24: return halo_occ_t<1, 4, 1, 3>(hp);
-    case 25: return halo_occ_t<1, 4, 1, 4>(hp);
+#define SC_X(id, a, b, c, d) \
+  case id:                   \
+    return halo_occ_t<a, b, c, d>(hp);
+    SC_HALO_CONFIGS(SC_X)
+#undef SC_X
     default: return 0;
   }
 }
 
 hipError_t launch_conv_halo(const ConvParams& p, const HaloParams& hp, int grid, hipStream_t st) {
   switch (hp.config) {
-    // 2 x 1 waves, 4 x WN tiles each: 128-site tiles (b >= 16)
-    case 0: return launch_halo_t<2, 1, 4, 1>(p, hp, grid, st);
-    case 1: return launch_halo_t<2, 1, 4, 2>(p, hp, grid, st);
-    case 2: return launch_halo_t<2, 1, 4, 4>(p, hp, grid, st);
-    case 3: return launch_halo_t<2, 1, 4, 8>(p, hp, grid, st);
-    case 4: return launch_halo_t<4, 1, 2, 12>(p, hp, grid, st);
-    case 5: return launch_halo_t<4, 1, 2, 16>(p, hp, grid, st);
-    // 4 x 1 waves, 1 x WN tiles each: 64-site tiles (b = 8)
-    case 10: return launch_halo_t<4, 1, 1, 1>(p, hp, grid, st);
-    case 11: return launch_halo_t<4, 1, 1, 2>(p, hp, grid, st);
-    case 12: return launch_halo_t<4, 1, 1, 4>(p, hp, grid, st);
-    case 13: return launch_halo_t<4, 1, 1, 8>(p, hp, grid, st);
-    case 14: return launch_halo_t<4, 1, 1, 12>(p, hp, grid, st);
-    case 15: return launch_halo_t<4, 1, 1, 16>(p, hp, grid, st);
-    // 1 x WAVES_N waves: 16-site tiles (b = 4)
-    case 20: return launch_halo_t<1, 1, 1, 1>(p, hp, grid, st);
-    case 21: return launch_halo_t<1, 2, 1, 1>(p, hp, grid, st);
-    case 22: return launch_halo_t<1, 4, 1, 1>(p, hp, grid, st);
-    case 23: return launch_halo_t<1, 4, 1, 2>(p, hp, grid, st);
-    case 24: return launch_halo_t<1, 4, 1, 3>(p, hp, grid, st);
-    case 25: return launch_halo_t<1, 4, 1, 4>(p, hp, grid, st);
+#define SC_X(id, a, b, c, d) \
+  case id:                   \
+    return launch_halo_t<a, b, c, d>(p, hp, grid, st);
+    SC_HALO_CONFIGS(SC_X)
+#undef SC_X
     default: return hipErrorInvalidValue;
   }
 }

@@ -197,24 +197,28 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
   // block-halo kernel: tile = tr rows x b columns of a block, chosen per wave layout
   G.halo = false;
   if (!depthwise && d->dtype == SKIPCONV_BF16 && d->c_in % 32 == 0 &&
-      (b == 4 || b == 8 || b == 16 || b == 32 || b == 64)) {
+      d->c_out % 4 == 0 && (b == 4 || b == 8 || b == 16 || b == 32 || b == 64)) {
     static const int ntns[] = {1, 2, 4, 8, 12, 16};
     int ni = 0;
     while (ntns[ni] != G.ntn) ++ni;
     sc::HaloParams& H = G.hp;
+    // waves: 1 along M x WAVES_N along N; each wave owns all rows of the tile
     if (b >= 16) {
-      H.tr = 128 / b;
-      H.config = ni;                 // 0..5
-      H.threads = G.ntn <= 8 ? 128 : 256;
-    } else if (b == 8) {
+      if (G.ntn <= 8) {  // 128-site tiles, WM = 8
+        H.tr = 128 / b;
+        H.config = G.ntn == 1 ? 0 : (G.ntn == 2 ? 1 : (G.ntn == 4 ? 2 : 3));
+      } else {           // 64-site tiles, WM = 4
+        H.tr = 64 / b;
+        H.config = G.ntn == 12 ? 14 : 15;
+      }
+    } else if (b == 8) {  // the whole block: 64 sites, WM = 4
       H.tr = 8;
       H.config = 10 + ni;
-      H.threads = 256;
-    } else {
+    } else {              // b = 4: 16 sites, WM = 1
       H.tr = 4;
       H.config = 20 + ni;
-      H.threads = G.ntn == 1 ? 64 : (G.ntn == 2 ? 128 : 256);
     }
+    H.threads = 64 * (G.ntn == 1 ? 1 : (G.ntn == 2 ? 2 : 4));
     H.tiles_per_block = b / H.tr;
     H.hh = (H.tr - 1) * s + k;
     H.hw = (b - 1) * s + k;
