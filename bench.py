@@ -102,11 +102,16 @@ def eps_for_density(stats, block, h_out, w_out, target):
 
 # ------------------------------------------------------------------ timing --
 
-def run_steps(layer, frames_dev, steps, start, *, every=0):
+def run_steps(layer, frames_dev, steps, start, *, every=0, block=None):
     """Run `steps` steps from clip position `start` (reset at each clip start).
 
-    With every > 0, HIP events bracket both kernels of every `every`-th step.
-    Returns (wall seconds, gate ms, conv ms, clip positions of the timed steps, next position).
+    With every > 0, HIP events (recorded by the library on the launch stream)
+    bracket both kernels of every `every`-th step. With block = (period, length),
+    a HIP event pair on the launch stream brackets `length` consecutive steps
+    once every `period` steps, and the kernel time is the bracketed time over the
+    launches inside (for a one-kernel step: duration plus the dispatch gap).
+    Returns (wall seconds, gate ms, conv ms, clip positions of the timed launches,
+    next position).
     """
     import torch
     from paper_2104_11487_amd import skipconv as S
@@ -115,13 +120,24 @@ def run_steps(layer, frames_dev, steps, start, *, every=0):
     ntimed = (steps + every - 1) // every if every else 0
     if every:
         S.skipconv_timing_begin(layer.handle, ntimed, every)
+    pairs, timed = [], []
+    stream = layer.stream if layer.stream is not None else torch.cuda.current_stream()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     pos = start
-    for _ in range(steps):
+    for j in range(steps):
         if pos % nfr == 0:
             layer.reset()
+        opened = block is not None and j % block[0] == 0 and j + block[1] <= steps
+        if opened:
+            ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            ev[0].record(stream)
         layer.step(frames_dev[pos % nfr])
+        if block is not None and j % block[0] < block[1] and j - j % block[0] + block[1] <= steps:
+            timed.append(pos % nfr)
+            if j % block[0] == block[1] - 1:
+                ev[1].record(stream)
+                pairs.append(ev)
         pos += 1
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -132,6 +148,9 @@ def run_steps(layer, frames_dev, steps, start, *, every=0):
         assert n == ntimed, (n, ntimed)
         timed_pos = (start + idx.astype(np.int64)) % nfr
         S.skipconv_timing_begin(layer.handle, 0, 1)
+    elif pairs:
+        gate_ms = float(sum(a.elapsed_time(b) for a, b in pairs))
+        timed_pos = np.array(timed, np.int64)
     return wall, gate_ms, conv_ms, timed_pos, pos
 
 
@@ -148,11 +167,25 @@ def clip_active(layer, frames_dev):
 
 
 def event_period(nfr: int) -> int:
-    """Sampling period of the per-kernel events, coprime with the clip length."""
-    for e in (5, 7, 11, 13):
+    """Sampling period of the per-kernel events of the multi-kernel pipeline.
+
+    Coprime with the clip length, so the sampled steps walk through every clip
+    position, and long enough (>= 17 steps) that the event records, each a
+    marker packet on the stream, add little to the timed wall clock.
+    """
+    for e in (17, 19, 23, 29, 31, 37):
         if np.gcd(e, nfr) == 1:
             return e
     return 1
+
+
+def event_blocks(nfr: int, length: int = 16):
+    """(period, length) of the bracketed runs of the one-kernel pipeline.
+
+    Consecutive runs start length/2 clip positions apart, so together they
+    cover the clip; one event pair per run keeps the marker cost per step small.
+    """
+    return 2 * nfr + length // 2, length
 
 
 def measure_point(make_layer, frames_dev, steps, warmup, geom, *, label, events=True):
@@ -165,8 +198,9 @@ def measure_point(make_layer, frames_dev, steps, warmup, geom, *, label, events=
     if warmup:
         _, _, _, _, pos = run_steps(layer, frames_dev, warmup, pos)
     pos = (pos + nfr - 1) // nfr * nfr  # timed steps start at a clip boundary
-    every = event_period(nfr) if events else 0
-    wall, gate_ms, conv_ms, tpos, _ = run_steps(layer, frames_dev, steps, pos, every=every)
+    every = event_period(nfr) if events and not fused else 0
+    blk = event_blocks(nfr) if events and fused else None
+    wall, gate_ms, conv_ms, tpos, _ = run_steps(layer, frames_dev, steps, pos, every=every, block=blk)
     layer.close()
     idx = np.arange(steps) % nfr
     act_sites = sites[idx].astype(np.float64)
@@ -198,7 +232,8 @@ def measure_point(make_layer, frames_dev, steps, warmup, geom, *, label, events=
         "gate_us": gate_us,
         "conv_us": conv_us,
         "timed_launches": int(len(tpos)),
-        "event_period": every,
+        "event_period": every if every else None,
+        "event_blocks": list(blk) if blk else None,
         "conv_flop_per_launch": conv_flop,
         "gate_bytes_per_launch": float(gate_bytes),
         "conv_active_tflops": conv_flop / (conv_us * 1e-6) / 1e12 if conv_us else None,

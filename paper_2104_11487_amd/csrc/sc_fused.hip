@@ -3,27 +3,32 @@
 // whole gate blocks, doing every step of Eq. 3 for its tile in one launch:
 //
 //   1. weights: chunks of the packed weights are copied into LDS with
-//      asynchronous global_load_lds by the waves that hold no halo pixel, so
-//      the copy overlaps the gate work;
-//   2. halo: one thread per input pixel of the tile's halo loads its channels
-//      of x_t and x_{t-1} (16-byte loads, all in flight together), forms
-//      r = x_t - x_{t-1} in fp32 (Eq. 2), sums the statistic terms in the
-//      canonical order in registers (8-channel chunk sums in ascending order,
-//      one rounding per multiply and per add), writes rho = bf16_rne(r) to an LDS
-//      halo kept for the product, and copies owned pixels of x_t into the
-//      spare x_{t-1} slot;
+//      asynchronous global_load_lds at kernel start, so the copy overlaps the
+//      halo and gate work (whose barriers wait on LDS traffic only);
+//   2. halo: every thread takes 8-channel chunks of the tile's halo pixels
+//      (16-byte loads of x_t and x_{t-1}, several in flight), forms
+//      r = x_t - x_{t-1} in fp32 (Eq. 2) and the chunk's statistic sum in the
+//      canonical order (channels ascending, one rounding per multiply and per
+//      add), parks the sum in LDS, writes rho = bf16_rne(r) to an LDS halo kept
+//      for the product, and copies owned pixels of x_t into the spare x_{t-1}
+//      slot; then one thread per pixel adds its chunk sums in ascending order;
 //   3. gate (Eq. 5): support sums over taps in row-major order, exact fp64
 //      threshold, block OR (Sec. 3.2.2); block flags go to global memory;
-//   4. local compaction: the active sites of the tile, in row-major order
-//      (wave ballot + workgroup prefix), become the rows of the product;
-//   5. MFMA product over the active rows only (Sec. 4.2: im2col restricted to
-//      the non-sparse columns, never materialised: A fragments are read from
-//      the LDS halo at each row's pixel + tap offset; rows past the active
-//      count read a zero pixel); the old z of the lane's outputs is fetched
-//      before the product starts;
-//   6. epilogue: z (+)= U at the active sites, activation output refreshed.
+//   4. product rows: for tiles of up to 8 x 8 sites the rows are all sites
+//      of the tile (one 16-row MFMA tile per wave) and the gate only decides
+//      which rows are stored; for larger tiles the active sites are compacted
+//      in row-major order (wave ballot + workgroup prefix) and become the
+//      rows; the old z of the stored rows is fetched before the product so
+//      its latency overlaps it;
+//   5. MFMA product over the rows (Sec. 4.2: im2col restricted to the
+//      non-sparse columns, never materialised: A fragments are read from the
+//      LDS halo at each row's pixel + tap offset; rows past the last one read
+//      a zero pixel);
+//   6. epilogue: z (+)= U at the active sites, activation output refreshed
+//      (the product is formed transposed, weights as the MFMA A operand, so a
+//      lane holds 4 consecutive output channels and z moves in 16-byte pieces).
 //
-// Inactive tiles stop after step 4, so the hardware dispatcher balances the
+// Inactive tiles stop after step 3, so the hardware dispatcher balances the
 // work. The ordered global active list is not needed by this pipeline; it is
 // produced on demand for introspection by the compaction kernel.
 #include "sc_device.h"
@@ -38,7 +43,6 @@ namespace {
 
 constexpr int kThreads = 512;
 constexpr int kWaves = kThreads / 64;
-constexpr int kGroupM = 4;  // waves along M; kWaves / kGroupM along N
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float floatx2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -63,14 +67,25 @@ __device__ __forceinline__ void issue_b(const FusedParams& p, uint8_t* ldsb, int
     __builtin_amdgcn_global_load_lds(src + (size_t)u * 64, dst + u * 1024, 16, 0, 0);
 }
 
-template <int WM, int WN>
+// Workgroup barrier that orders LDS accesses only: outstanding global loads
+// and stores (the weight copy, the z prefetch, the x_t copy) stay in flight.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Wave layout of the product: GM waves along M (WM 16-row tiles each) by 2
+// along N (WN 16-column tiles each); waves past the first 2 * GM do no MFMA.
+template <int WM, int WN, int GM>
 __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
-  constexpr int NTN = WN * (kWaves / kGroupM);
+  constexpr int NTN = WN * 2;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   __shared__ uint32_t blk_flag[kMaxTileBlocks];
   __shared__ int rows_pix[kMaxTileBlocks];
   __shared__ int rows_site[kMaxTileBlocks];
   __shared__ uint32_t wave_cnt[kWaves];
+  __shared__ uint32_t tile_on;
 
   const GateParams& g = p.g;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -96,68 +111,98 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
   const int tb_w = g.ts / g.block;
   const int npix = hh * hw;
 
-  // 1. weights: waves past the ones holding halo pixels issue the first chunk
-  const int bw0 = min(kWaves - 1, (npix + 63) >> 6);
+  // 1. weights: the waves past the first few issue the first chunk; the
+  // barriers up to the product wait on LDS traffic only
+  const int bw0 = min(kWaves - 1, 2);
   if (wave >= bw0) issue_b<NTN>(p, ldsb, 0, wave, lane, bw0);
   for (int i = threadIdx.x; i < kMaxTileBlocks; i += kThreads) blk_flag[i] = 0u;
+  if (threadIdx.x == 0) tile_on = 0u;
   // the zero pixel read by MFMA rows past the active count
   for (int i = threadIdx.x; i < (p.pstride >> 4); i += kThreads)
     *reinterpret_cast<u32x4*>(halo + (size_t)p.zero_pix * p.pstride + i * 16) = u32x4{0u, 0u, 0u, 0u};
 
-  // 2. halo: one thread per pixel, channels in registers, statistic in canonical order
+  // Product rows. With one M-tile per wave (tiles of <= 8 x 8 sites) the rows
+  // are all sites of the tile in row-major order, fixed before the gate, which
+  // only decides which rows are stored. With larger tiles the rows are the
+  // active sites, compacted after the gate (step 4).
+  // The product is computed transposed (weights as the MFMA A operand): a
+  // lane's accumulator holds 4 consecutive output channels of one row, so z
+  // moves in 16-byte pieces.
+  constexpr bool kStatic = GM * WM * 16 == 64;
+  const int wm = wave % GM, wn = wave / GM;
+  int abase[WM], tapmul[WM], zsite[WM];
+  uint32_t blk_of[WM];
+  floatx4 zold[WM][WN];
+  if (kStatic) {
+#pragma unroll
+    for (int i = 0; i < WM; ++i) {
+      const int row = (wm * WM + i) * 16 + r16;
+      const int ly = row / g.ts, lx = row - (row / g.ts) * g.ts;
+      const bool ok = wn < 2 && ly < oh && lx < ow;
+      abase[i] = (ok ? (ly * s) * hw + lx * s : p.zero_pix) * p.pstride + kq * 16;
+      tapmul[i] = ok ? p.pstride : 0;  // the zero pixel ignores the tap offset
+      zsite[i] = ok ? (n * g.h_out + oy0 + ly) * g.w_out + ox0 + lx : -1;
+      blk_of[i] = ok ? (ly / g.block) * tb_w + lx / g.block : 0u;
+    }
+  }
+
+  // 2. halo: one item = one 8-channel chunk of one halo pixel (consecutive
+  // items are consecutive chunks, so a wave's loads are contiguous); kItems
+  // items per thread have their loads in flight together. Each item forms r
+  // in fp32, its chunk sum in canonical order (channels ascending, one
+  // rounding per multiply and per add) and rho = bf16_rne(r) for the product.
   const uint16_t* xt = static_cast<const uint16_t*>(g.x_t);
   const uint16_t* xp = static_cast<const uint16_t*>(g.x_prev);
   uint16_t* keep = static_cast<uint16_t*>(g.x_keep);
-  const int cpp = c >> 3;  // 16-byte chunks per pixel
-  for (int q = threadIdx.x; q < npix; q += kThreads) {
-    const int hy = q / hw, hx = q - hy * hw;
-    const int y = iy0 + hy, x = ix0 + hx;
-    const bool in = y >= 0 && y < g.h && x >= 0 && x < g.w;
-    const bool own = in && g.copy_in_halo && y >= own_y0 && y < own_y1 && x >= own_x0 && x < own_x1;
-    const size_t base = in ? ((size_t)(n * g.h + y) * g.w + x) * c : 0;
-    uint8_t* hrow = halo + (size_t)q * p.pstride;
-    float acc = 0.0f;
-    for (int c0 = 0; c0 < cpp; c0 += 8) {
-      const int nch = min(8, cpp - c0);
-      uint4 vt[8], vp[8];
+  float* part = reinterpret_cast<float*>(lds + p.off_part);
+  const int nchk = c >> 3;  // 16-byte chunks per pixel
+  const int total = npix * nchk;
+  constexpr int kItems = 4;
+  for (int base = 0; base < total; base += kThreads * kItems) {
+    uint4 vt[kItems], vp[kItems];
+    size_t off[kItems];
+    int px[kItems], ch[kItems];
+    bool in[kItems], own[kItems];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        vt[j] = uint4{0u, 0u, 0u, 0u};
-        vp[j] = uint4{0u, 0u, 0u, 0u};
-        if (j < nch && in) {
-          vt[j] = *reinterpret_cast<const uint4*>(xt + base + (c0 + j) * 8);
-          if (!g.reference) vp[j] = *reinterpret_cast<const uint4*>(xp + base + (c0 + j) * 8);
-        }
-      }
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        if (j >= nch) break;
-        u32x4 rq = {0u, 0u, 0u, 0u};
-        if (in) {
-          const uint32_t wt[4] = {vt[j].x, vt[j].y, vt[j].z, vt[j].w};
-          const uint32_t wpv[4] = {vp[j].x, vp[j].y, vp[j].z, vp[j].w};
-          uint32_t outw[4];
-          float part = 0.0f;  // chunk sum: this chunk's 8 channels in ascending order
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            // channels 2e (low half) and 2e + 1 (high half)
-            const float r0 = __fsub_rn(__uint_as_float(wt[e] << 16), __uint_as_float(wpv[e] << 16));
-            const float r1 =
-                __fsub_rn(__uint_as_float(wt[e] & 0xffff0000u), __uint_as_float(wpv[e] & 0xffff0000u));
-            part = add_rn(part, term(r0, g.norm_p));
-            part = add_rn(part, term(r1, g.norm_p));
-            outw[e] = pack_bf16(r0, r1);
-          }
-          acc = add_rn(acc, part);  // chunk sums in ascending chunk order
-          rq = u32x4{outw[0], outw[1], outw[2], outw[3]};
-          if (own) *reinterpret_cast<uint4*>(keep + base + (c0 + j) * 8) = vt[j];
-        }
-        *reinterpret_cast<u32x4*>(hrow + (c0 + j) * 16) = rq;
+    for (int u = 0; u < kItems; ++u) {
+      const int idx = base + u * kThreads + threadIdx.x;
+      px[u] = idx < total ? idx / nchk : -1;
+      ch[u] = idx - px[u] * nchk;
+      const int hy = px[u] / hw, hx = px[u] - hy * hw;
+      const int y = iy0 + hy, x = ix0 + hx;
+      in[u] = px[u] >= 0 && y >= 0 && y < g.h && x >= 0 && x < g.w;
+      own[u] = in[u] && g.copy_in_halo && y >= own_y0 && y < own_y1 && x >= own_x0 && x < own_x1;
+      off[u] = in[u] ? ((size_t)(n * g.h + y) * g.w + x) * c + ch[u] * 8 : 0;
+      vt[u] = uint4{0u, 0u, 0u, 0u};
+      vp[u] = uint4{0u, 0u, 0u, 0u};
+      if (in[u]) {
+        vt[u] = *reinterpret_cast<const uint4*>(xt + off[u]);
+        if (!g.reference) vp[u] = *reinterpret_cast<const uint4*>(xp + off[u]);
       }
     }
-    a_halo[q] = in ? acc : 0.0f;
+#pragma unroll
+    for (int u = 0; u < kItems; ++u) {
+      if (px[u] < 0) continue;
+      const uint32_t wt[4] = {vt[u].x, vt[u].y, vt[u].z, vt[u].w};
+      const uint32_t wpv[4] = {vp[u].x, vp[u].y, vp[u].z, vp[u].w};
+      uint32_t outw[4];
+      float sum = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        // channels 2e (low half) and 2e + 1 (high half)
+        const float r0 = __fsub_rn(__uint_as_float(wt[e] << 16), __uint_as_float(wpv[e] << 16));
+        const float r1 = __fsub_rn(__uint_as_float(wt[e] & 0xffff0000u), __uint_as_float(wpv[e] & 0xffff0000u));
+        sum = add_rn(sum, term(r0, g.norm_p));
+        sum = add_rn(sum, term(r1, g.norm_p));
+        outw[e] = pack_bf16(r0, r1);
+      }
+      // out-of-frame pixels: zero operand and zero statistic (outw, sum are 0)
+      *reinterpret_cast<u32x4*>(halo + (size_t)px[u] * p.pstride + ch[u] * 16) =
+          u32x4{outw[0], outw[1], outw[2], outw[3]};
+      part[px[u] * p.pstage + ch[u]] = sum;
+      if (own[u]) *reinterpret_cast<uint4*>(keep + off[u]) = vt[u];
+    }
   }
-
   if (!g.copy_in_halo) {
     const int ny = own_y1 - own_y0, nx = own_x1 - own_x0;
     const int per_row = nx * c;
@@ -167,7 +212,14 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
       keep[o] = xt[o];
     }
   }
-  __syncthreads();
+  lds_barrier();
+  // pixel statistic: the chunk sums of each pixel added in ascending chunk order
+  for (int q = threadIdx.x; q < npix; q += kThreads) {
+    float acc = 0.0f;
+    for (int j = 0; j < nchk; ++j) acc = add_rn(acc, part[q * p.pstage + j]);
+    a_halo[q] = acc;
+  }
+  lds_barrier();
 
   // 3. gate
   for (int q = threadIdx.x; q < oh * ow; q += kThreads) {
@@ -187,9 +239,12 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
       g.stat[o] = sv;
       g.site_mask[o] = on ? 1 : 0;
     }
-    if (on) blk_flag[(ly / g.block) * tb_w + lx / g.block] = 1u;
+    if (on) {
+      blk_flag[(ly / g.block) * tb_w + lx / g.block] = 1u;
+      tile_on = 1u;
+    }
   }
-  __syncthreads();
+  lds_barrier();
   {
     const int nby = (oh + g.block - 1) / g.block, nbx = (ow + g.block - 1) / g.block;
     const int bi0 = oy0 / g.block, bj0 = ox0 / g.block;
@@ -199,59 +254,76 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
     }
   }
 
-  // 4. local compaction: one site per thread (<= 256 sites), row-major order
-  {
-    const int q = threadIdx.x;
-    const int ly = q / ow, lx = q - (q / ow) * ow;
-    const bool act = q < oh * ow && blk_flag[(ly / g.block) * tb_w + lx / g.block] != 0u;
-    const unsigned long long m = __ballot(act);
-    const uint32_t rank = __popcll(m & ((1ull << lane) - 1ull));
-    if (lane == 0) wave_cnt[wave] = (uint32_t)__popcll(m);
-    __syncthreads();
-    uint32_t off = 0;
-    for (int w = 0; w < wave; ++w) off += wave_cnt[w];
-    if (act) {
-      rows_pix[off + rank] = (ly * s) * hw + lx * s;
-      rows_site[off + rank] = (n * g.h_out + oy0 + ly) * g.w_out + ox0 + lx;
+  if (!tile_on) {
+    __builtin_amdgcn_s_waitcnt(0);  // no weight copy may still target this workgroup's LDS
+    return;
+  }
+  __syncthreads();  // the first weight chunk has landed in LDS
+
+  // 4. local compaction (tiles of more than 64 sites): one site per thread
+  // (<= 256 sites), row-major order
+  int nrows = 0;
+  if (!kStatic) {
+    {
+      const int q = threadIdx.x;
+      const int ly = q / ow, lx = q - (q / ow) * ow;
+      const bool act = q < oh * ow && blk_flag[(ly / g.block) * tb_w + lx / g.block] != 0u;
+      const unsigned long long m = __ballot(act);
+      const uint32_t rank = __popcll(m & ((1ull << lane) - 1ull));
+      if (lane == 0) wave_cnt[wave] = (uint32_t)__popcll(m);
+      lds_barrier();
+      uint32_t off = 0;
+      for (int w = 0; w < wave; ++w) off += wave_cnt[w];
+      if (act) {
+        rows_pix[off + rank] = (ly * s) * hw + lx * s;
+        rows_site[off + rank] = (n * g.h_out + oy0 + ly) * g.w_out + ox0 + lx;
+      }
+    }
+    lds_barrier();
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) nrows += (int)wave_cnt[w];
+#pragma unroll
+    for (int i = 0; i < WM; ++i) {
+      const int row = (wm * WM + i) * 16 + r16;
+      const bool ok = row < nrows;
+      abase[i] = (ok ? rows_pix[row] : p.zero_pix) * p.pstride + kq * 16;
+      tapmul[i] = ok ? p.pstride : 0;
+      zsite[i] = ok ? rows_site[row] : -1;
+      blk_of[i] = 0u;
+    }
+    // old z of the active rows, fetched now so that the load overlaps the product
+#pragma unroll
+    for (int i = 0; i < WM; ++i)
+#pragma unroll
+      for (int j = 0; j < WN; ++j) {
+        const int col = (wn * WN + j) * 16 + kq * 4;
+        zold[i][j] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+        if (zsite[i] >= 0 && !g.reference && col < p.c_out)
+          zold[i][j] = *reinterpret_cast<const floatx4*>(p.z + (size_t)zsite[i] * p.c_out + col);
+      }
+  } else {
+    // rows of blocks the gate left off are computed but not stored; the old z
+    // of the stored rows is fetched now so that the load overlaps the product
+#pragma unroll
+    for (int i = 0; i < WM; ++i) {
+      if (zsite[i] >= 0 && blk_flag[blk_of[i]] == 0u) zsite[i] = -1;
+#pragma unroll
+      for (int j = 0; j < WN; ++j) {
+        const int col = (wn * WN + j) * 16 + kq * 4;
+        zold[i][j] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+        if (zsite[i] >= 0 && !g.reference && col < p.c_out)
+          zold[i][j] = *reinterpret_cast<const floatx4*>(p.z + (size_t)zsite[i] * p.c_out + col);
+      }
     }
   }
-  __syncthreads();
-  int nrows = 0;
-#pragma unroll
-  for (int w = 0; w < kWaves; ++w) nrows += (int)wave_cnt[w];
-  if (nrows == 0) return;  // every barrier above waited for the weight loads
+  const bool busy = wn < 2 && (kStatic ? wm * WM * 16 < g.ts * g.ts : wm * WM * 16 < nrows);
 
-  // 5. MFMA over the active rows: wave (wm, wn) owns M-tiles wm*WM.. and N-tiles wn*WN..
-  const int wm = wave % kGroupM, wn = wave / kGroupM;
+  // 5. MFMA over the rows: wave (wm, wn) owns M-tiles wm*WM.. and N-tiles wn*WN..
   floatx4 acc[WM][WN];
 #pragma unroll
   for (int i = 0; i < WM; ++i)
 #pragma unroll
     for (int j = 0; j < WN; ++j) acc[i][j] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
-  int abase[WM], tapmul[WM];
-#pragma unroll
-  for (int i = 0; i < WM; ++i) {
-    const int row = (wm * WM + i) * 16 + r16;
-    const bool ok = row < nrows;
-    abase[i] = (ok ? rows_pix[row] : p.zero_pix) * p.pstride + kq * 16;
-    tapmul[i] = ok ? p.pstride : 0;  // the zero pixel ignores the tap offset
-  }
-  const bool busy = wm * WM * 16 < nrows;
-  // old z of this lane's outputs, fetched now so the load overlaps the product
-  floatx4 zold[WM][WN];
-#pragma unroll
-  for (int i = 0; i < WM; ++i)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int row = (wm * WM + i) * 16 + kq * 4 + v;
-      const bool rok = busy && row < nrows && !g.reference;
-      const size_t zrow = rok ? (size_t)rows_site[row] * p.c_out : 0;
-#pragma unroll
-      for (int j = 0; j < WN; ++j) {
-        const int col = (wn * WN + j) * 16 + r16;
-        zold[i][j][v] = (rok && col < p.c_out) ? p.z[zrow + col] : 0.0f;
-      }
-    }
   const int csteps = p.csteps;
   for (int chunk = 0; chunk < p.nchunks; ++chunk) {
     if (chunk + 1 < p.nchunks) issue_b<NTN>(p, ldsb, chunk + 1, wave, lane, 0);
@@ -292,7 +364,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
           for (int i = 0; i < WM; ++i)
 #pragma unroll
             for (int j = 0; j < WN; ++j)
-              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[u][i], bfr[u][j], acc[i][j], 0, 0, 0);
+              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[u][j], a[u][i], acc[i][j], 0, 0, 0);
         bptr += kU * NTN * 1024;
       }
       for (; kk < nks; ++kk) {
@@ -307,7 +379,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
         for (int i = 0; i < WM; ++i)
 #pragma unroll
           for (int j = 0; j < WN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], bfr[j], acc[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[j], a[i], acc[i][j], 0, 0, 0);
         bptr += NTN * 1024;
         if (++cc == csteps) {
           cc = 0;
@@ -321,42 +393,45 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
     if (chunk + 1 < p.nchunks) __syncthreads();  // next chunk landed; this buffer free
   }
 
-  // 6. epilogue
+  // 6. epilogue: z = z_{t-1} + U (assigned on a reference frame), activation output
   if (!busy) return;
 #pragma unroll
   for (int i = 0; i < WM; ++i) {
+    if (zsite[i] < 0) continue;
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int row = (wm * WM + i) * 16 + kq * 4 + v;
-      if (row >= nrows) continue;
-      const size_t zrow = (size_t)rows_site[row] * p.c_out;
+    for (int j = 0; j < WN; ++j) {
+      const int col = (wn * WN + j) * 16 + kq * 4;
+      if (col >= p.c_out) continue;
+      floatx4 nv;
 #pragma unroll
-      for (int j = 0; j < WN; ++j) {
-        const int col = (wn * WN + j) * 16 + r16;
-        if (col >= p.c_out) continue;
-        const float nv = g.reference ? acc[i][j][v] : zold[i][j][v] + acc[i][j][v];
-        p.z[zrow + col] = nv;
-        if (p.act) Elem<uint16_t>::store1(static_cast<uint16_t*>(p.y), zrow + col,
-                                          p.act == 2 ? fmaxf(nv, 0.0f) : nv);
+      for (int v = 0; v < 4; ++v) nv[v] = g.reference ? acc[i][j][v] : zold[i][j][v] + acc[i][j][v];
+      const size_t o = (size_t)zsite[i] * p.c_out + col;
+      *reinterpret_cast<floatx4*>(p.z + o) = nv;
+      if (p.act) {
+        float av[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) av[v] = p.act == 2 ? fmaxf(nv[v], 0.0f) : nv[v];
+        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.y) + o) =
+            uint2{f32_to_bf16(av[0]) | (f32_to_bf16(av[1]) << 16), f32_to_bf16(av[2]) | (f32_to_bf16(av[3]) << 16)};
       }
     }
   }
 }
 
-template <int WM, int WN>
+template <int WM, int WN, int GM>
 hipError_t launch_fused_t(const FusedParams& p, int grid, hipStream_t st) {
-  hipLaunchKernelGGL((fused_kernel<WM, WN>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p);
+  hipLaunchKernelGGL((fused_kernel<WM, WN, GM>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p);
   return hipGetLastError();
 }
 
 // Allow the kernel its dynamic LDS (above the 64 KB default) and report how
 // many workgroups fit on one CU; done once, at create time.
-template <int WM, int WN>
+template <int WM, int WN, int GM>
 int prepare_fused_t(const FusedParams& p) {
-  const void* fn = reinterpret_cast<const void*>(fused_kernel<WM, WN>);
+  const void* fn = reinterpret_cast<const void*>(fused_kernel<WM, WN, GM>);
   if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, p.lds_bytes) != hipSuccess) return 0;
   int blocks = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, fused_kernel<WM, WN>, kThreads, p.lds_bytes) !=
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, fused_kernel<WM, WN, GM>, kThreads, p.lds_bytes) !=
       hipSuccess)
     return 0;
   return blocks;
@@ -364,24 +439,26 @@ int prepare_fused_t(const FusedParams& p) {
 
 }  // namespace
 
-// Instantiations: WM = M-tiles per wave (1 for 8x8 tiles, 4 for 16x16 tiles),
-// WN = N-tiles per wave = ntiles_n / 2 (two waves share the N dimension).
+// Instantiations: tiles of <= 8 x 8 sites use 4 x 2 waves of one M-tile
+// each (a 2 x 2 layout of 2 M-tiles per wave reads less LDS but measured
+// slower); 16 x 16 tiles use 4 x 2 waves of 4 M-tiles each. WN = N-tiles per
+// wave = ntiles_n / 2.
 int prepare_fused(const FusedParams& p) {
   if (p.mw == 1) {
     switch (p.ntiles_n) {
-      case 2: return prepare_fused_t<1, 1>(p);
-      case 4: return prepare_fused_t<1, 2>(p);
-      case 8: return prepare_fused_t<1, 4>(p);
-      case 12: return prepare_fused_t<1, 6>(p);
-      case 16: return prepare_fused_t<1, 8>(p);
+      case 2: return prepare_fused_t<1, 1, 4>(p);
+      case 4: return prepare_fused_t<1, 2, 4>(p);
+      case 8: return prepare_fused_t<1, 4, 4>(p);
+      case 12: return prepare_fused_t<1, 6, 4>(p);
+      case 16: return prepare_fused_t<1, 8, 4>(p);
       default: return 0;
     }
   }
   if (p.mw == 4) {
     switch (p.ntiles_n) {
-      case 2: return prepare_fused_t<4, 1>(p);
-      case 4: return prepare_fused_t<4, 2>(p);
-      case 8: return prepare_fused_t<4, 4>(p);
+      case 2: return prepare_fused_t<4, 1, 4>(p);
+      case 4: return prepare_fused_t<4, 2, 4>(p);
+      case 8: return prepare_fused_t<4, 4, 4>(p);
       default: return 0;
     }
   }
@@ -391,19 +468,19 @@ int prepare_fused(const FusedParams& p) {
 hipError_t launch_fused(const FusedParams& p, int grid, hipStream_t st) {
   if (p.mw == 1) {
     switch (p.ntiles_n) {
-      case 2: return launch_fused_t<1, 1>(p, grid, st);
-      case 4: return launch_fused_t<1, 2>(p, grid, st);
-      case 8: return launch_fused_t<1, 4>(p, grid, st);
-      case 12: return launch_fused_t<1, 6>(p, grid, st);
-      case 16: return launch_fused_t<1, 8>(p, grid, st);
+      case 2: return launch_fused_t<1, 1, 4>(p, grid, st);
+      case 4: return launch_fused_t<1, 2, 4>(p, grid, st);
+      case 8: return launch_fused_t<1, 4, 4>(p, grid, st);
+      case 12: return launch_fused_t<1, 6, 4>(p, grid, st);
+      case 16: return launch_fused_t<1, 8, 4>(p, grid, st);
       default: return hipErrorInvalidValue;
     }
   }
   if (p.mw == 4) {
     switch (p.ntiles_n) {
-      case 2: return launch_fused_t<4, 1>(p, grid, st);
-      case 4: return launch_fused_t<4, 2>(p, grid, st);
-      case 8: return launch_fused_t<4, 4>(p, grid, st);
+      case 2: return launch_fused_t<4, 1, 4>(p, grid, st);
+      case 4: return launch_fused_t<4, 2, 4>(p, grid, st);
+      case 8: return launch_fused_t<4, 4, 4>(p, grid, st);
       default: return hipErrorInvalidValue;
     }
   }

@@ -76,7 +76,8 @@ struct FusedParams {
   int mw;                  // 16-row MFMA tiles per wave (1 for 8x8 tiles, 4 for 16x16)
   int pstride;             // LDS bytes per rho halo pixel: 2*c_in + 16
   int zero_pix;            // index of the all-zero pixel just past the halo
-  int off_b, off_halo, off_a, lds_bytes;
+  int pstage;              // LDS floats per halo pixel of chunk sums: (c_in / 8) | 1
+  int off_b, off_halo, off_a, off_part, lds_bytes;
 };
 
 hipError_t launch_fused(const FusedParams& p, int grid, hipStream_t st);

@@ -50,6 +50,7 @@ struct Geometry {
   bool fused;           // single-pass kernel instead of gate + compaction + conv
   int f_ts, f_tiles_y, f_tiles_x, f_grid, f_copy_in_halo;
   int f_kc, f_nchunks, f_nbuf, f_mw, f_pstride, f_zero_pix, f_off_b, f_off_halo, f_off_a, f_lds;
+  int f_pstage, f_off_part;
   int vec;              // gate load width (elements)
   size_t elem;
   size_t off_wpack, off_slot0, off_slot1, off_z, off_y, off_bmask, off_tflag, off_list, off_ctr,
@@ -234,8 +235,8 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
   // fused single-pass kernel: dense bf16, C_in % 32 == 0, tiles of <= 16 x 16
   // sites, output tiles split over two wave groups (ntn >= 2)
   G.fused = false;
-  if (!depthwise && d->dtype == SKIPCONV_BF16 && d->c_in % 32 == 0 && b <= 16 && G.ntn >= 2 &&
-      !(d->flags & SKIPCONV_FLAG_SPLIT_PIPELINE)) {
+  if (!depthwise && d->dtype == SKIPCONV_BF16 && d->c_in % 32 == 0 && d->c_out % 4 == 0 && b <= 16 &&
+      G.ntn >= 2 && !(d->flags & SKIPCONV_FLAG_SPLIT_PIPELINE)) {
     const int ts = b <= 8 ? b * (8 / b) : b;
     const int mw = ts <= 8 ? 1 : 4;
     if (!(mw == 4 && G.ntn > 8)) {
@@ -243,15 +244,17 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
       const long pstride = 2L * d->c_in + 16;
       const long halo_b = ((long)hh * hh + 1) * pstride;  // + the zero pixel
       const long a_b = ((long)hh * hh * 4 + 15) / 16 * 16;
+      const int pstage = (d->c_in / 8) | 1;
+      const long part_b = ((long)hh * hh * pstage * 4 + 15) / 16 * 16;
       const long whole = (long)G.ksteps * G.ntn * 1024;
       long b_bytes = whole;
       int kc = G.ksteps, nbuf = 1;
-      if (whole + halo_b + a_b > kFusedLdsLimit) {
+      if (whole + halo_b + a_b + part_b > kFusedLdsLimit) {
         kc = std::max(1, 16 / G.ntn);
         nbuf = 2;
         b_bytes = (long)nbuf * kc * G.ntn * 1024;
       }
-      if (b_bytes + halo_b + a_b <= kFusedLdsLimit) {
+      if (b_bytes + halo_b + a_b + part_b <= kFusedLdsLimit) {
         G.fused = true;
         G.f_ts = ts;
         G.f_mw = mw;
@@ -263,7 +266,9 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
         G.f_off_b = 0;
         G.f_off_halo = (int)b_bytes;
         G.f_off_a = (int)(b_bytes + halo_b);
-        G.f_lds = (int)(b_bytes + halo_b + a_b);
+        G.f_off_part = (int)(b_bytes + halo_b + a_b);
+        G.f_pstage = pstage;
+        G.f_lds = (int)(b_bytes + halo_b + a_b + part_b);
         G.f_tiles_y = (G.h_out + ts - 1) / ts;
         G.f_tiles_x = (G.w_out + ts - 1) / ts;
         G.f_grid = d->n * G.f_tiles_y * G.f_tiles_x;
@@ -360,6 +365,8 @@ sc::FusedParams fused_params(skipconv_layer* h, const void* x_t, bool ref) {
   fp.off_b = g.f_off_b;
   fp.off_halo = g.f_off_halo;
   fp.off_a = g.f_off_a;
+  fp.off_part = g.f_off_part;
+  fp.pstage = g.f_pstage;
   fp.lds_bytes = g.f_lds;
   return fp;
 }
