@@ -18,6 +18,10 @@ Processing", CVPR 2021):
   the norm taken over the kernel support of each output (all input channels
   times k_h x k_w). round(sigmoid(y)) is 1 exactly when y > 0 (a tie at y = 0
   rounds half-to-even to 0), so the gate is the comparison "norm > eps".
+* Sec. 3.2.1, Eq. 6-7 (Output-Norm gate): the residual norm is multiplied by the
+  norm of the whole weight tensor (all four dimensions) before the comparison
+  with eps. By Young's inequality (Eq. 6) that product bounds the norm of the
+  skipped update at the site, so a skipped site's update has norm <= eps.
 * Sec. 3.2.2, "Structured Sparsity": max-pool the gate with kernel = stride = b,
   then nearest-neighbour upsample by b, giving b x b constant masks.
 * Sec. 4.2, "Runtime speed up": the sparse convolution is an im2col matrix
@@ -38,6 +42,11 @@ rest of the design notes):
   float32, so eps*eps is exact in float64).
 * a NaN statistic turns the gate on, so a NaN input reaches z instead of being
   silently skipped.
+* Output-Norm gate: the weight norm is kept in the same power as the residual
+  statistic (sum |w| for p = 1, sum w^2 for p = 2), summed in float64 over the
+  weights in ascending flat OIHW order (|w| and w^2 of float32 or bf16 values
+  are exact in float64); the gate compares statistic * weight norm with the
+  threshold, the product rounded once in float64.
 * blocks are anchored at output (0, 0); partial edge blocks pool the sites they
   hold (ceil mode). The active list is the ascending row-major list of active
   block indices n*HB*WB + bi*WB + bj.
@@ -180,19 +189,34 @@ def support_stat(a: np.ndarray, k: int, stride: int, pad: int, h_out: int, w_out
     return s
 
 
-def gate(s: np.ndarray, eps: float, norm_p: int, reference: bool) -> np.ndarray:
-    """g = round(sigmoid(norm - eps)) (Eq. 5) as an exact comparison.
+def weight_norm(weight: np.ndarray, norm_p: int) -> float:
+    """Norm of the whole weight tensor for the Output-Norm gate (Eq. 7).
+
+    Returned in the power the gate compares: sum |w| for p = 1, sum w^2 (the
+    squared 2-norm) for p = 2. The terms are taken in ascending flat OIHW order
+    and added one at a time in float64 (a Python float).
+    """
+    acc = 0.0
+    for v in np.asarray(weight, dtype=np.float64).reshape(-1).tolist():
+        acc += abs(v) if norm_p == 1 else v * v
+    return acc
+
+
+def gate(s: np.ndarray, eps: float, norm_p: int, reference: bool, wnorm: float = 1.0) -> np.ndarray:
+    """g = round(sigmoid(norm - eps)) (Eq. 5, or Eq. 7 with wnorm) as an exact comparison.
 
     On a reference frame every site is on (Sec. 3.1). Otherwise the site is on
-    when the statistic exceeds the threshold (eps^2 for p = 2, eps for p = 1),
-    compared exactly in float64, or when the statistic is NaN.
+    when statistic * wnorm exceeds the threshold (eps^2 for p = 2, eps for
+    p = 1), computed in float64, or when the statistic is NaN. wnorm is 1 for
+    the Input-Norm gate (the product is then exact) and weight_norm(w, p) for
+    the Output-Norm gate.
     """
     if reference:
         return np.ones(s.shape, dtype=bool)
     e = float(np.float32(eps))
     thr = e * e if norm_p == 2 else e
     sd = s.astype(np.float64)
-    return (sd > thr) | np.isnan(sd)
+    return (sd * wnorm > thr) | np.isnan(sd)
 
 
 def block_pool(g: np.ndarray, b: int) -> np.ndarray:
@@ -273,12 +297,14 @@ class SkipConvOracle:
     weight: OIHW (C_out, C_in/groups, k, k). For dtype 'bf16' the weights are
     given either as bf16 bit patterns (uint16) or as float values, which are
     then rounded to bf16 exactly as a bf16 layer stores them.
+    gate: 'input' (Input-Norm gate, Eq. 5) or 'output' (Output-Norm gate, Eq. 7;
+    the norm of the stored weights).
     """
 
     def __init__(self, weight: np.ndarray, *, n: int, h: int, w: int, stride: int = 1,
                  pad: Optional[int] = None, groups: int = 1, eps: float = 0.0, block: int = 1,
                  norm_p: int = 2, support: str = "rf", dtype: str = "f32",
-                 exact_residual: bool = False):
+                 exact_residual: bool = False, gate: str = "input"):
         weight = np.asarray(weight)
         if dtype == "bf16":
             bits = weight if weight.dtype == np.uint16 else f32_to_bf16_rne(weight.astype(np.float32))
@@ -299,6 +325,9 @@ class SkipConvOracle:
         self.support = support
         self.dtype = dtype
         self.exact_residual = exact_residual
+        assert gate in ("input", "output"), gate
+        self.gate_kind = gate
+        self.wnorm = weight_norm(self.weight, norm_p) if gate == "output" else 1.0
         self.z = np.zeros((n, self.h_out, self.w_out, self.c_out), dtype=np.float64)
         self.x_prev = None
         self.reference_pending = True
@@ -319,7 +348,7 @@ class SkipConvOracle:
         r = residual(x32, prev)
         a = pixel_stat(r, self.norm_p)
         s = support_stat(a, self.k, self.stride, self.pad, self.h_out, self.w_out, self.support)
-        g = gate(s, self.eps, self.norm_p, ref)
+        g = gate(s, self.eps, self.norm_p, ref, self.wnorm)
         m_blk = block_pool(g, self.block)
         m = block_upsample(m_blk, self.block, self.h_out, self.w_out)
         lst = active_list(m_blk)

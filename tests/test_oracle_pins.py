@@ -451,3 +451,91 @@ def test_mac_accounting():
     assert lay.dense_macs() == 100 * 8 * 4 * 9
     d = O.mac_weighted_density([out["active_macs"], 0], [lay.dense_macs(), lay.dense_macs()])
     assert d == pytest.approx(out["mask"].mean() / 2)
+
+
+# ----------------------------------------------------------------------------
+# Output-Norm gate (Sec. 3.2.1, Eq. 6-7)
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("p", [1, 2])
+def test_weight_norm_is_the_whole_tensor_norm(p):
+    # integer weights: the float64 sum is exact, so it must equal the integer norm
+    rng = _rng(60)
+    w = rng.integers(-7, 8, (5, 3, 3, 3)).astype(np.float64)
+    exact = int(np.abs(w).sum()) if p == 1 else int((w.astype(np.int64) ** 2).sum())
+    assert O.weight_norm(w, p) == float(exact)
+    # random weights: within the sequential-summation bound of the correctly rounded sum
+    w = rng.normal(0, 0.1, (16, 8, 3, 3)).astype(np.float32)
+    terms = [abs(float(v)) if p == 1 else float(v) * float(v) for v in w.reshape(-1)]
+    ref = math.fsum(terms)
+    assert abs(O.weight_norm(w, p) - ref) <= len(terms) * 2.0 ** -52 * ref
+    # a per-output-channel norm or a max would differ from the whole-tensor norm
+    assert O.weight_norm(w, p) > max(O.weight_norm(w[c], p) for c in range(w.shape[0]))
+
+
+@pytest.mark.parametrize("p", [1, 2])
+def test_output_norm_gate_bounds_skipped_updates(p):
+    """Young's inequality (Eq. 6): at a skipped site, ||w * r||_p <= ||w||_p ||r||_p <= eps."""
+    rng = _rng(61 + p)
+    n, h, wd, c, co, k = 1, 12, 10, 8, 6, 3
+    w = rng.normal(0, 0.3, (co, c, k, k)).astype(np.float32)
+    x0 = rng.random((n, h, wd, c), dtype=np.float32)
+    x1 = x0 + rng.normal(0, 0.05, x0.shape).astype(np.float32) * (rng.random(x0.shape) < 0.3)
+    x1 = x1.astype(np.float32)
+    wn = O.weight_norm(w, p)
+    r = O.residual(x1, x0)
+    s = O.support_stat(O.pixel_stat(r, p), k, 1, 1, h, wd, "rf")
+    # eps at the median of the gated quantity, so both outcomes occur
+    q = s.astype(np.float64) * wn
+    eps = float(np.float32(np.median(q) if p == 1 else math.sqrt(float(np.median(q)))))
+    lay = O.SkipConvOracle(w, n=n, h=h, w=wd, eps=eps, norm_p=p, gate="output")
+    lay.step(x0)
+    out = lay.step(x1)
+    off = ~out["site_mask"]
+    assert 0 < off.sum() < off.size
+    sn, si, sj = np.nonzero(off)
+    u = brute_update(r.astype(np.float64), w.astype(np.float64), 1, 1, 1, list(zip(sn, si, sj)))
+    un = np.abs(u).sum(axis=1) if p == 1 else np.sqrt((u * u).sum(axis=1))
+    # the statistic is a float32 sum: allow its rounding (relative K * 2^-24)
+    assert np.all(un <= eps * (1.0 + 1e-4)), (un.max(), eps)
+    # a tight case: one non-zero weight (the centre tap of channel 0) and isolated
+    # impulses in channel 0, so ||w * r|| = ||w|| ||r|| at the impulse sites; the
+    # gate must then skip exactly the impulses whose update norm is <= eps (a
+    # smaller weight norm, e.g. one output channel's, would skip larger ones)
+    w = np.zeros((2, c, k, k), np.float32)
+    w[0, 0, 1, 1] = 1.5
+    x0 = np.zeros((n, h, wd, c), np.float32)
+    x1 = x0.copy()
+    amps = np.array([0.25, 0.5, 1.0, 2.0, 4.0, 8.0], np.float32)
+    pos = [(1, 1), (1, 6), (5, 2), (5, 7), (9, 1), (9, 6)]
+    for (y, x), a in zip(pos, amps):
+        x1[0, y, x, 0] = a
+    eps = 1.4 if p == 1 else 1.4  # between 1.5 * 0.5 and 1.5 * 1.0
+    lay = O.SkipConvOracle(w, n=n, h=h, w=wd, eps=eps, norm_p=p, gate="output")
+    lay.step(x0)
+    out = lay.step(x1)
+    for (y, x), a in zip(pos, amps):
+        assert bool(out["site_mask"][0, y, x]) == (1.5 * float(a) > eps), (y, x, a)
+
+
+@pytest.mark.parametrize("p", [1, 2])
+def test_output_norm_gate_equals_input_norm_at_scaled_eps(p):
+    """With ||w||_p a power of two the Output-Norm gate is the Input-Norm gate at eps / ||w||_p."""
+    rng = _rng(70 + p)
+    n, h, wd, c, k = 2, 9, 11, 8, 3
+    w = np.zeros((4, c, k, k), np.float32)
+    # four entries +-0.5: sum |w| = 2, sum w^2 = 1; scaled by 4: 8 and 16
+    idx = rng.choice(w.size, 4, replace=False)
+    w.reshape(-1)[idx] = np.array([0.5, -0.5, 0.5, -0.5], np.float32) * 4
+    wn = O.weight_norm(w, p)
+    assert wn == (8.0 if p == 1 else 16.0)
+    scale = 8.0 if p == 1 else 4.0  # ||w||_p itself (the 2-norm is sqrt(16))
+    frames = [rng.random((n, h, wd, c), dtype=np.float32) for _ in range(4)]
+    frames = [f * (rng.random(f.shape) < 0.5) for f in frames]
+    eps = 0.75
+    a = O.SkipConvOracle(w, n=n, h=h, w=wd, eps=eps, norm_p=p, gate="output")
+    b = O.SkipConvOracle(w, n=n, h=h, w=wd, eps=eps / scale, norm_p=p, gate="input")
+    for f in frames:
+        ra, rb = a.step(f.astype(np.float32)), b.step(f.astype(np.float32))
+        assert np.array_equal(ra["site_mask"], rb["site_mask"])
+        assert np.array_equal(ra["z"], rb["z"])
