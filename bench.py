@@ -456,8 +456,8 @@ def main():
         torch.cuda.synchronize()
     stats = None if args.eps is not None else gpu_stats(layer_kw, wt, frames_dev)
 
-    def mk(b, eps, dense=False, split=args.split):
-        return lambda: SkipConv(wt, eps=eps, block=b, force_dense=dense, split=split, **layer_kw)
+    def mk(b, eps, dense=False, split=args.split, gate="input"):
+        return lambda: SkipConv(wt, eps=eps, block=b, force_dense=dense, split=split, gate=gate, **layer_kw)
 
     eps_head = args.eps if args.eps is not None else eps_for_density(stats, block, h_out, w_out, args.density)
     head = measure_point(mk(block, eps_head), frames_dev, args.steps, args.warmup, geom,
@@ -480,6 +480,14 @@ def main():
         r = measure_point(mk(block, eps_head, split=not args.split), frames_dev, sweep_steps, len(clip), geom,
                           label=f"b={block} d={args.density} other pipeline")
         r.update({"block": block, "target_density": args.density})
+        sweep.append(r)
+        # Output-Norm gate (Eq. 7) at the same density: with p = 2 it compares
+        # s * sum(w^2) with eps^2, so eps scales by the weight 2-norm
+        wq = wt.float().cpu().numpy().astype(np.float64)
+        e_out = eps_head * float(np.sqrt(np.sum(wq * wq)))
+        r = measure_point(mk(block, e_out, gate="output"), frames_dev, sweep_steps, len(clip), geom,
+                          label=f"output-norm gate b={block} d={args.density}")
+        r.update({"block": block, "target_density": args.density, "gate": "output-norm", "eps": e_out})
         sweep.append(r)
         tus = torch_dense_us(wt, (wl.n, wl.h, wl.w, wl.c), spec.stride)
         sweep.append({"label": "torch conv2d (MIOpen), dense, same shape", "us_per_frame_batch": tus,

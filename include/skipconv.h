@@ -8,6 +8,9 @@
  *          output locations where the gate is on; elsewhere z~_{t-1} is kept.
  *   Eq. 5  Input-Norm gate g = round(sigmoid(||r_t|| - eps)), the norm taken
  *          over the kernel support (all input channels x k x k) of each output.
+ *   Eq. 7  Output-Norm gate g = round(sigmoid(||w|| ||r_t|| - eps)), ||w|| the
+ *          norm of the whole weight tensor (Young's inequality, Eq. 6, makes
+ *          the product a bound on the norm of the skipped update).
  *   Sec. 3.2.2 structured gates: max-pool the gate with kernel = stride = b,
  *          then nearest upsample, so the mask is constant on b x b blocks.
  *   Sec. 3.1 the first frame (and each reference frame after a reset, the
@@ -56,6 +59,16 @@ enum { SKIPCONV_F32 = 0, SKIPCONV_BF16 = 1 };
  * single input pixel under the output (o * stride). */
 enum { SKIPCONV_SUPPORT_RF = 0, SKIPCONV_SUPPORT_CENTRE = 1 };
 
+/* Gate function (Sec. 3.2.1). Both compare in the power of the statistic:
+ *   INPUT_NORM   (Eq. 5): s > eps (p = 1) or s > eps^2 (p = 2), s the support
+ *                statistic of the residual;
+ *   OUTPUT_NORM  (Eq. 7): s * W > eps (p = 1) or s * W > eps^2 (p = 2), with
+ *                W = sum |w| (p = 1) or sum w^2 (p = 2) over the whole weight
+ *                tensor, summed in fp64 in ascending OIHW order at create; the
+ *                product is rounded once in fp64.
+ * A NaN statistic turns the gate on in both; a reference frame is dense. */
+enum { SKIPCONV_GATE_INPUT_NORM = 0, SKIPCONV_GATE_OUTPUT_NORM = 1 };
+
 /* Optional activation output kept beside z, for chaining layers: NONE = no
  * buffer; IDENTITY = dtype(z); RELU = dtype(max(z, 0)). It changes only at
  * updated sites, like z (z is pre-activation, Eq. 1). */
@@ -89,13 +102,14 @@ typedef struct skipconv_desc {
   int32_t act_out;  /* SKIPCONV_ACT_* */
   uint32_t flags;   /* SKIPCONV_FLAG_* */
   float eps;        /* threshold, >= 0 or +inf; NaN is rejected */
+  int32_t gate;     /* SKIPCONV_GATE_* */
 } skipconv_desc;
 
 typedef struct skipconv_layer* skipconv_t;
 
 /* Fill *d with defaults: n = h = w = c_in = c_out = 1, kernel 3, stride 1,
  * pad -1, groups 1, block 1, norm_p 2, RF support, fp32, no activation
- * output, no flags, eps 0. Host only. */
+ * output, no flags, eps 0, Input-Norm gate. Host only. */
 int skipconv_desc_init(skipconv_desc* d);
 
 /* Check a descriptor without touching the GPU. Returns OK, E_INVALID_ARG or

@@ -233,7 +233,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
     } else {
       sv = a_halo[(ly * s + g.pad) * hw + lx * s + g.pad];
     }
-    const bool on = g.reference || g.force_dense || ((double)sv > g.thr) || (sv != sv);
+    const bool on = g.reference || g.force_dense || ((double)sv * g.wnorm > g.thr) || (sv != sv);
     if (g.keep_stats) {
       const size_t o = ((size_t)n * g.h_out + oy0 + ly) * g.w_out + ox0 + lx;
       g.stat[o] = sv;

@@ -194,7 +194,7 @@ __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
     } else {
       sv = a_halo[(ly * s + p.pad) * hw + lx * s + p.pad];
     }
-    const bool on = p.reference || p.force_dense || ((double)sv > p.thr) || (sv != sv);
+    const bool on = p.reference || p.force_dense || ((double)sv * p.wnorm > p.thr) || (sv != sv);
     if (p.keep_stats) {
       const size_t o = ((size_t)n * p.h_out + oy0 + ly) * p.w_out + ox0 + lx;
       p.stat[o] = sv;

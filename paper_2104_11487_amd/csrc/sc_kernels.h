@@ -27,6 +27,7 @@ struct GateParams {
   int copy_in_halo;             // 1: every owned input pixel lies in its tile's halo
   int norm_p, support, reference, force_dense, keep_stats;
   double thr;                   // eps^2 (p = 2) or eps (p = 1), exact in fp64
+  double wnorm;                 // statistic factor: 1 (Input-Norm gate) or the weight norm (Output-Norm)
   uint8_t* block_mask;          // N x HB x WB
   uint8_t* tile_flags;          // N x tiles_y x tiles_x when blocks are larger than tiles
   int split_blocks;             // 1: ts < block (b % ts == 0): flags per tile, OR-ed by the compaction

@@ -90,6 +90,8 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
     return fail(err, SKIPCONV_E_UNSUPPORTED, "only groups == 1 or groups == c_in == c_out");
   if (d->block < 1 || d->block > 64) return fail(err, SKIPCONV_E_INVALID_ARG, "block must be 1..64");
   if (d->norm_p != 1 && d->norm_p != 2) return fail(err, SKIPCONV_E_INVALID_ARG, "norm_p must be 1 or 2");
+  if (d->gate != SKIPCONV_GATE_INPUT_NORM && d->gate != SKIPCONV_GATE_OUTPUT_NORM)
+    return fail(err, SKIPCONV_E_INVALID_ARG, "gate must be a SKIPCONV_GATE_* value");
   if (d->support != SKIPCONV_SUPPORT_RF && d->support != SKIPCONV_SUPPORT_CENTRE)
     return fail(err, SKIPCONV_E_INVALID_ARG, "unknown support");
   if (d->dtype != SKIPCONV_F32 && d->dtype != SKIPCONV_BF16)
@@ -310,6 +312,7 @@ struct skipconv_layer {
   int device = 0;
   int num_cu = 256;
   int conv_occ = 4;          // resident conv workgroups per CU
+  double wnorm = 1.0;        // gate weight factor: 1 (Input-Norm) or the weight norm (Output-Norm)
   bool list_valid = false;   // active list/count match the last step (fused steps skip them)
   char* ws = nullptr;
   bool owns_ws = false;
@@ -371,6 +374,38 @@ sc::FusedParams fused_params(skipconv_layer* h, const void* x_t, bool ref) {
   return fp;
 }
 
+// Output-Norm gate (Eq. 7): the norm of the whole weight tensor, in the power
+// of the statistic (sum |w| for p = 1, sum w^2 for p = 2), summed in fp64 in
+// ascending OIHW order. |w| and w^2 of fp32 / bf16 values are exact in fp64,
+// so the only roundings are the additions, in that order. The weights are
+// read back once, at create (a host synchronisation on `st`).
+hipError_t weight_norm(skipconv_layer* h, const void* weights, hipStream_t st) {
+  const skipconv_desc& d = h->d;
+  const size_t numel = (size_t)d.c_out * (d.c_in / d.groups) * d.kernel * d.kernel;
+  const size_t esz = d.dtype == SKIPCONV_BF16 ? 2 : 4;
+  std::vector<uint8_t> host(numel * esz);
+  hipError_t e = hipMemcpyAsync(host.data(), weights, host.size(), hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return e;
+  double acc = 0.0;
+  for (size_t i = 0; i < numel; ++i) {
+    float f;
+    if (esz == 2) {
+      uint16_t b;
+      std::memcpy(&b, host.data() + 2 * i, 2);
+      const uint32_t u = (uint32_t)b << 16;
+      std::memcpy(&f, &u, 4);
+    } else {
+      std::memcpy(&f, host.data() + 4 * i, 4);
+    }
+    const double v = (double)f;
+    const double term = d.norm_p == 1 ? std::fabs(v) : v * v;
+    acc = acc + term;
+  }
+  h->wnorm = acc;
+  return hipSuccess;
+}
+
 int hip_fail(skipconv_t h, hipError_t e, const char* what) {
   if (h) snprintf(h->last_error, sizeof(h->last_error), "%s: %s", what, hipGetErrorString(e));
   return SKIPCONV_E_HIP;
@@ -398,6 +433,7 @@ sc::GateParams gate_params(skipconv_layer* h, const void* x_t, bool ref) {
   gp.force_dense = (d.flags & SKIPCONV_FLAG_FORCE_DENSE) ? 1 : 0;
   gp.keep_stats = (d.flags & SKIPCONV_FLAG_KEEP_STATS) ? 1 : 0;
   gp.thr = threshold(d);
+  gp.wnorm = h->wnorm;
   gp.block_mask = h->bmask(); gp.list = h->list(); gp.counters = h->ctr();
   gp.tile_flags = h->tflags(); gp.split_blocks = g.split_blocks;
   gp.stat = h->stat(); gp.site_mask = h->smask();
@@ -445,6 +481,7 @@ int skipconv_desc_init(skipconv_desc* d) {
   d->act_out = SKIPCONV_ACT_NONE;
   d->flags = 0;
   d->eps = 0.0f;
+  d->gate = SKIPCONV_GATE_INPUT_NORM;
   return SKIPCONV_OK;
 }
 
@@ -540,6 +577,7 @@ int skipconv_create(const skipconv_desc* d, const void* weights, void* workspace
       e = sc::launch_pack_mfma(weights, h->wpack(), d->dtype, d->c_out, d->c_in, d->kernel,
                                g.ksteps, g.ntn, st);
   }
+  if (e == hipSuccess && d->gate == SKIPCONV_GATE_OUTPUT_NORM) e = weight_norm(h, weights, st);
   if (e != hipSuccess) {
     snprintf(g_create_error, sizeof(g_create_error), "create: %s", hipGetErrorString(e));
     if (h->owns_ws) (void)hipFree(h->ws);

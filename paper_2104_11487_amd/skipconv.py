@@ -26,6 +26,7 @@ SKIPCONV_E_SMALL_BUFFER = -6
 
 SKIPCONV_F32, SKIPCONV_BF16 = 0, 1
 SKIPCONV_SUPPORT_RF, SKIPCONV_SUPPORT_CENTRE = 0, 1
+SKIPCONV_GATE_INPUT_NORM, SKIPCONV_GATE_OUTPUT_NORM = 0, 1
 SKIPCONV_ACT_NONE, SKIPCONV_ACT_IDENTITY, SKIPCONV_ACT_RELU = 0, 1, 2
 SKIPCONV_FLAG_KEEP_STATS, SKIPCONV_FLAG_FORCE_DENSE, SKIPCONV_FLAG_SPLIT_PIPELINE = 1, 2, 4
 
@@ -36,7 +37,7 @@ class skipconv_desc(ctypes.Structure):
                 ("stride", ctypes.c_int32), ("pad", ctypes.c_int32), ("groups", ctypes.c_int32),
                 ("block", ctypes.c_int32), ("norm_p", ctypes.c_int32), ("support", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("act_out", ctypes.c_int32), ("flags", ctypes.c_uint32),
-                ("eps", ctypes.c_float)]
+                ("eps", ctypes.c_float), ("gate", ctypes.c_int32)]
 
 
 class SkipConvError(RuntimeError):
@@ -240,11 +241,12 @@ def skipconv_timing_read(h: int, stream: int, capacity: int = 0):
 
 _SUPPORT = {"rf": SKIPCONV_SUPPORT_RF, "centre": SKIPCONV_SUPPORT_CENTRE}
 _ACT = {"none": SKIPCONV_ACT_NONE, "identity": SKIPCONV_ACT_IDENTITY, "relu": SKIPCONV_ACT_RELU}
+_GATE = {"input": SKIPCONV_GATE_INPUT_NORM, "output": SKIPCONV_GATE_OUTPUT_NORM}
 
 
 def make_desc(*, n, h, w, c_in, c_out, kernel, stride=1, pad=-1, groups=1, block=1, norm_p=2,
               support="rf", dtype="f32", act_out="none", eps=0.0, keep_stats=False,
-              force_dense=False, split=False) -> skipconv_desc:
+              force_dense=False, split=False, gate="input") -> skipconv_desc:
     d = skipconv_desc_init()
     d.n, d.h, d.w, d.c_in, d.c_out = n, h, w, c_in, c_out
     d.kernel, d.stride, d.pad, d.groups, d.block = kernel, stride, pad, groups, block
@@ -254,6 +256,7 @@ def make_desc(*, n, h, w, c_in, c_out, kernel, stride=1, pad=-1, groups=1, block
     d.flags = ((SKIPCONV_FLAG_KEEP_STATS if keep_stats else 0) | (SKIPCONV_FLAG_FORCE_DENSE if force_dense else 0)
                | (SKIPCONV_FLAG_SPLIT_PIPELINE if split else 0))
     d.eps = eps
+    d.gate = _GATE[gate]
     return d
 
 
@@ -269,7 +272,7 @@ class SkipConv:
     def __init__(self, weight, *, n: int, h: int, w: int, stride: int = 1, pad: int = -1,
                  groups: int = 1, eps: float = 0.0, block: int = 1, norm_p: int = 2,
                  support: str = "rf", act_out: str = "none", keep_stats: bool = False,
-                 force_dense: bool = False, split: bool = False, stream=None):
+                 force_dense: bool = False, split: bool = False, gate: str = "input", stream=None):
         import torch
 
         if not weight.is_cuda:
@@ -282,7 +285,7 @@ class SkipConv:
         c_out, cg, k, _ = weight.shape
         self.desc = make_desc(n=n, h=h, w=w, c_in=cg * groups, c_out=c_out, kernel=k, stride=stride,
                               pad=pad, groups=groups, block=block, norm_p=norm_p, support=support,
-                              dtype=self.dtype, act_out=act_out, eps=eps, keep_stats=keep_stats,
+                              dtype=self.dtype, act_out=act_out, eps=eps, keep_stats=keep_stats, gate=gate,
                               force_dense=force_dense, split=split)
         self.h_out, self.w_out, self.hb, self.wb = skipconv_out_shape(self.desc)
         nbytes = skipconv_workspace_size(self.desc)

@@ -24,7 +24,7 @@ def test_desc_defaults(lib):
     d = S.skipconv_desc_init()
     assert (d.n, d.h, d.w, d.c_in, d.c_out) == (1, 1, 1, 1, 1)
     assert (d.kernel, d.stride, d.pad, d.groups, d.block, d.norm_p) == (3, 1, -1, 1, 1, 2)
-    assert d.eps == 0.0 and d.flags == 0
+    assert d.eps == 0.0 and d.flags == 0 and d.gate == S.SKIPCONV_GATE_INPUT_NORM
     assert S.skipconv_validate(d) == S.SKIPCONV_OK
 
 
@@ -45,6 +45,7 @@ def good(**kw):
     ("dtype", 2, S.SKIPCONV_E_INVALID_ARG), ("act_out", 3, S.SKIPCONV_E_INVALID_ARG),
     ("flags", 8, S.SKIPCONV_E_INVALID_ARG), ("eps", -1.0, S.SKIPCONV_E_INVALID_ARG),
     ("eps", float("nan"), S.SKIPCONV_E_INVALID_ARG), ("c_out", 272, S.SKIPCONV_E_UNSUPPORTED),
+    ("gate", 7, S.SKIPCONV_E_INVALID_ARG), ("gate", -1, S.SKIPCONV_E_INVALID_ARG),
 ])
 def test_validation_codes(lib, field, value, code):
     d = good()
@@ -61,6 +62,8 @@ def test_valid_variants(lib):
     assert S.skipconv_validate(good(stride=2, pad=0)) == 0
     assert S.skipconv_validate(good(block=64, h=20, w=20)) == 0
     assert S.skipconv_validate(good(support="centre", norm_p=1)) == 0
+    assert S.skipconv_validate(good(gate="output")) == 0
+    assert S.skipconv_validate(good(gate="output", norm_p=1, dtype="f32")) == 0
 
 
 @pytest.mark.parametrize("h,w,k,s,pad,b,exp", [

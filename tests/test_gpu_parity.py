@@ -20,14 +20,15 @@ pytestmark = pytest.mark.gpu
 
 
 def _layer_pair(w_f32, *, n, h, w, dtype, eps, block, stride=1, pad=-1, groups=1, norm_p=2,
-                support="rf", keep_stats=True, act_out="none", force_dense=False, split=False):
+                support="rf", keep_stats=True, act_out="none", force_dense=False, split=False,
+                gate="input"):
     ws = weight_storage(w_f32, dtype)
     layer = S.SkipConv(to_device(ws, dtype), n=n, h=h, w=w, stride=stride, pad=pad, groups=groups,
                        eps=eps, block=block, norm_p=norm_p, support=support, keep_stats=keep_stats,
-                       act_out=act_out, force_dense=force_dense, split=split)
+                       act_out=act_out, force_dense=force_dense, split=split, gate=gate)
     orc = O.SkipConvOracle(ws, n=n, h=h, w=w, stride=stride, pad=None if pad == -1 else pad,
                            groups=groups, eps=eps, block=block, norm_p=norm_p, support=support,
-                           dtype=dtype)
+                           dtype=dtype, gate=gate)
     return layer, orc
 
 
@@ -403,3 +404,62 @@ def test_pipeline_selection():
     assert not S.SkipConv(w16, n=1, h=32, w=32, block=8).fused
     w3 = to_device(weight_storage(syn.he_weights(64, 3, 3, seed=1), "bf16"), "bf16")
     assert not S.SkipConv(w3, n=1, h=32, w=32, block=1).fused
+
+
+# ------------------------------------------------------ Output-Norm gate --
+
+def _output_norm_eps(frames, ws, dtype, p, site_density):
+    """eps giving about `site_density` of sites on for the Output-Norm gate (oracle statistics)."""
+    w64 = O.bf16_bits_to_f32(ws) if dtype == "bf16" else ws
+    wn = O.weight_norm(w64, p)
+    k = ws.shape[2]
+    vals, prev = [], None
+    for f in frames:
+        x = O.storage_to_f32(syn.to_storage(f, dtype), dtype)
+        if prev is not None:
+            a = O.pixel_stat(O.residual(x, prev), p)
+            vals.append(O.support_stat(a, k, 1, (k - 1) // 2, x.shape[1], x.shape[2]).reshape(-1))
+        prev = x
+    q = float(np.quantile(np.concatenate(vals).astype(np.float64) * wn, 1.0 - site_density))
+    return q if p == 1 else float(np.sqrt(q))
+
+
+@PIPE
+@pytest.mark.parametrize("p", [1, 2])
+@pytest.mark.parametrize("block", [1, 8])
+def test_output_norm_gate_rect64(p, block, split):
+    wl = syn.workloads()["rect64"]
+    frames = list(wl.video(10))
+    w = wl.weights()[0]
+    eps = _output_norm_eps(frames, weight_storage(w, "bf16"), "bf16", p, 0.25)
+    worst, dens = run_single(frames, w, dtype="bf16", eps=eps, block=block, norm_p=p, gate="output",
+                             tag=f"rect64 output-norm p={p} b={block} split={split}", split=split,
+                             resets=(6,))
+    assert 0.0 < np.mean(dens[1:]) < 1.0
+
+
+@pytest.mark.parametrize("p", [1, 2])
+def test_output_norm_gate_square16_fp32(p):
+    wl = syn.workloads()["square16"]
+    frames = list(wl.video())
+    w = wl.weights()[0]
+    eps = _output_norm_eps(frames, weight_storage(w, "f32"), "f32", p, 0.1)
+    worst, dens = run_single(frames, w, dtype="f32", eps=eps, block=1, norm_p=p, gate="output",
+                             tag=f"square16 output-norm p={p}")
+    assert 0.0 < np.mean(dens[1:]) < 0.5
+
+
+@PIPE
+def test_output_norm_gate_depthwise_and_stride(split):
+    """Output-Norm gate on a depthwise bf16 layer and a strided dense layer (split-only shapes too)."""
+    rng = np.random.Generator(np.random.PCG64(91))
+    for (c_in, c_out, groups, stride, dtype) in ((32, 32, 32, 1, "bf16"), (32, 64, 1, 2, "bf16")):
+        w = rng.normal(0, 0.2, (c_out, c_in // groups, 3, 3)).astype(np.float32)
+        x = rng.random((1, 24, 20, c_in), dtype=np.float32)
+        frames = [x]
+        for t in range(3):
+            x = x.copy()
+            x[:, 3 * t:3 * t + 5, 2 * t:2 * t + 6] += 0.3
+            frames.append(x)
+        run_single(frames, w, dtype=dtype, eps=2.0, block=2, norm_p=1, gate="output", groups=groups,
+                   stride=stride, tag=f"output-norm c={c_in}->{c_out} g={groups} s={stride}", split=split)
