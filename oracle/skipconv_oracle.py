@@ -22,6 +22,10 @@ Processing", CVPR 2021):
   norm of the whole weight tensor (all four dimensions) before the comparison
   with eps. By Young's inequality (Eq. 6) that product bounds the norm of the
   skipped update at the site, so a skipped site's update has norm <= eps.
+* Sec. 3.2.1, Eq. 8 (Gumbel gate at inference): a light convolution f(r; phi)
+  with one output channel and the layer's kernel size, stride and padding
+  scores every output location; the gate rounds sigmoid(f), i.e. it is on
+  exactly when f > 0. phi is a given parameter here (training is out of scope).
 * Sec. 3.2.2, "Structured Sparsity": max-pool the gate with kernel = stride = b,
   then nearest-neighbour upsample by b, giving b x b constant masks.
 * Sec. 4.2, "Runtime speed up": the sparse convolution is an im2col matrix
@@ -42,6 +46,12 @@ rest of the design notes):
   float32, so eps*eps is exact in float64).
 * a NaN statistic turns the gate on, so a NaN input reaches z instead of being
   silently skipped.
+* Gumbel gate score, canonical order: for every input pixel q and tap (kh, kw),
+  a[q, kh, kw] = sum over channels of phi[c, kh, kw] * r[q, c] in chunks of 8
+  (ascending within a chunk from +0, chunk sums ascending from +0); then
+  f[o] = sum of a over the in-frame taps of o in row-major order, plus the
+  gate bias, all in float32 with one rounding per operation. The threshold
+  eps is not used by this gate.
 * Output-Norm gate: the weight norm is kept in the same power as the residual
   statistic (sum |w| for p = 1, sum w^2 for p = 2), summed in float64 over the
   weights in ascending flat OIHW order (|w| and w^2 of float32 or bf16 values
@@ -219,6 +229,54 @@ def gate(s: np.ndarray, eps: float, norm_p: int, reference: bool, wnorm: float =
     return (sd * wnorm > thr) | np.isnan(sd)
 
 
+def learned_pixel_taps(r: np.ndarray, phi: np.ndarray) -> np.ndarray:
+    """Per-pixel, per-tap terms of the gate convolution f(r; phi) (Eq. 8, inference).
+
+    r: (N, H, W, C) float32; phi: (C, k, k), the gate's single output channel.
+    Returns (N, H, W, k, k) float32 with a[q, kh, kw] = sum_c phi[c, kh, kw] * r[q, c]
+    in the canonical chunked order, every multiply and add rounded to float32.
+    """
+    phi = np.asarray(phi, dtype=np.float32)
+    nc, k, _ = phi.shape
+    assert r.shape[3] == nc
+    acc = np.zeros(r.shape[:3] + (k, k), dtype=np.float32)
+    for c0 in range(0, nc, CHUNK):
+        part = np.zeros_like(acc)
+        for c in range(c0, min(c0 + CHUNK, nc)):
+            term = np.multiply(r[..., c][..., None, None], phi[c][None, None, None], dtype=np.float32)
+            part = np.add(part, term, dtype=np.float32)
+        acc = np.add(acc, part, dtype=np.float32)
+    return acc
+
+
+def learned_score(a: np.ndarray, bias: float, stride: int, pad: int, h_out: int, w_out: int) -> np.ndarray:
+    """f(r; phi)[o] = sum over in-frame taps (row-major) of a[o*stride - pad + tap, tap], + bias.
+
+    Float32, one rounding per add; the bias is added last.
+    """
+    n, h, w, k, _ = a.shape
+    s = np.zeros((n, h_out, w_out), dtype=np.float32)
+    oi, oj = np.arange(h_out), np.arange(w_out)
+    for kh in range(k):
+        rows = oi * stride - pad + kh
+        rv = (rows >= 0) & (rows < h)
+        for kw in range(k):
+            cols = oj * stride - pad + kw
+            cv = (cols >= 0) & (cols < w)
+            blk = np.zeros((n, h_out, w_out), dtype=np.float32)
+            blk[:, np.ix_(rv, cv)[0], np.ix_(rv, cv)[1]] = \
+                a[:, rows[rv]][:, :, cols[cv]][..., kh, kw]
+            s = np.add(s, blk, dtype=np.float32)
+    return np.add(s, np.float32(bias), dtype=np.float32)
+
+
+def learned_gate(y: np.ndarray, reference: bool) -> np.ndarray:
+    """round(sigmoid(f)) at inference (Eq. 8): on exactly when f > 0, or f is NaN, or a reference frame."""
+    if reference:
+        return np.ones(y.shape, dtype=bool)
+    return (y > 0) | np.isnan(y)
+
+
 def block_pool(g: np.ndarray, b: int) -> np.ndarray:
     """Max-pool of the site gate with kernel = stride = b, ceil mode (Sec. 3.2.2)."""
     n, ho, wo = g.shape
@@ -297,14 +355,17 @@ class SkipConvOracle:
     weight: OIHW (C_out, C_in/groups, k, k). For dtype 'bf16' the weights are
     given either as bf16 bit patterns (uint16) or as float values, which are
     then rounded to bf16 exactly as a bf16 layer stores them.
-    gate: 'input' (Input-Norm gate, Eq. 5) or 'output' (Output-Norm gate, Eq. 7;
-    the norm of the stored weights).
+    gate: 'input' (Input-Norm gate, Eq. 5), 'output' (Output-Norm gate, Eq. 7;
+    the norm of the stored weights) or 'learned' (Gumbel gate at inference,
+    Eq. 8: gate_weight (C_in, k, k) float32 and gate_bias score each output; the
+    step's 'stat' is then the score f).
     """
 
     def __init__(self, weight: np.ndarray, *, n: int, h: int, w: int, stride: int = 1,
                  pad: Optional[int] = None, groups: int = 1, eps: float = 0.0, block: int = 1,
                  norm_p: int = 2, support: str = "rf", dtype: str = "f32",
-                 exact_residual: bool = False, gate: str = "input"):
+                 exact_residual: bool = False, gate: str = "input",
+                 gate_weight: Optional[np.ndarray] = None, gate_bias: float = 0.0):
         weight = np.asarray(weight)
         if dtype == "bf16":
             bits = weight if weight.dtype == np.uint16 else f32_to_bf16_rne(weight.astype(np.float32))
@@ -325,9 +386,12 @@ class SkipConvOracle:
         self.support = support
         self.dtype = dtype
         self.exact_residual = exact_residual
-        assert gate in ("input", "output"), gate
+        assert gate in ("input", "output", "learned"), gate
         self.gate_kind = gate
         self.wnorm = weight_norm(self.weight, norm_p) if gate == "output" else 1.0
+        if gate == "learned":
+            self.phi = np.asarray(gate_weight, dtype=np.float32).reshape(self.c_in, self.k, self.k)
+            self.gate_bias = float(np.float32(gate_bias))
         self.z = np.zeros((n, self.h_out, self.w_out, self.c_out), dtype=np.float64)
         self.x_prev = None
         self.reference_pending = True
@@ -346,9 +410,14 @@ class SkipConvOracle:
         ref = self.reference_pending
         prev = np.zeros_like(x32) if (ref or self.x_prev is None) else self.x_prev
         r = residual(x32, prev)
-        a = pixel_stat(r, self.norm_p)
-        s = support_stat(a, self.k, self.stride, self.pad, self.h_out, self.w_out, self.support)
-        g = gate(s, self.eps, self.norm_p, ref, self.wnorm)
+        if self.gate_kind == "learned":
+            a = learned_pixel_taps(r, self.phi)
+            s = learned_score(a, self.gate_bias, self.stride, self.pad, self.h_out, self.w_out)
+            g = learned_gate(s, ref)
+        else:
+            a = pixel_stat(r, self.norm_p)
+            s = support_stat(a, self.k, self.stride, self.pad, self.h_out, self.w_out, self.support)
+            g = gate(s, self.eps, self.norm_p, ref, self.wnorm)
         m_blk = block_pool(g, self.block)
         m = block_upsample(m_blk, self.block, self.h_out, self.w_out)
         lst = active_list(m_blk)

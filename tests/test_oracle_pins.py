@@ -539,3 +539,70 @@ def test_output_norm_gate_equals_input_norm_at_scaled_eps(p):
         ra, rb = a.step(f.astype(np.float32)), b.step(f.astype(np.float32))
         assert np.array_equal(ra["site_mask"], rb["site_mask"])
         assert np.array_equal(ra["z"], rb["z"])
+
+
+# ----------------------------------------------------------------------------
+# Gumbel gate at inference (Sec. 3.2.1, Eq. 8)
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("k,stride", [(1, 1), (3, 1), (3, 2), (5, 1)])
+def test_learned_score_is_single_channel_conv2d(k, stride):
+    rng = _rng(80 + k + stride)
+    n, h, wd, c = 2, 11, 9, 19
+    r = rng.normal(0, 1, (n, h, wd, c)).astype(np.float32)
+    phi = rng.normal(0, 0.5, (c, k, k)).astype(np.float32)
+    pad = (k - 1) // 2
+    ho, wo = O.out_size(h, k, stride, pad), O.out_size(wd, k, stride, pad)
+    y = O.learned_score(O.learned_pixel_taps(r, phi), -0.125, stride, pad, ho, wo)
+    ref = torch_conv(r.astype(np.float64), phi[None].astype(np.float64), stride, pad, 1)[..., 0] - 0.125
+    mag = torch_conv(np.abs(r).astype(np.float64), np.abs(phi)[None].astype(np.float64), stride, pad, 1)[..., 0]
+    # float32 recursive summation: |error| <= (terms) * 2^-24 * sum |phi r| (+ the bias add)
+    bound = (c * k * k + 2) * 2.0 ** -24 * (mag + 0.125)
+    assert np.all(np.abs(y - ref) <= bound)
+
+
+def test_learned_score_single_tap_is_exact_shift():
+    """phi non-zero at one tap only, integer data: f[o] is exactly the channel sum at that tap's pixel."""
+    rng = _rng(85)
+    n, h, wd, c = 1, 7, 8, 12
+    r = rng.integers(-4, 5, (n, h, wd, c)).astype(np.float32)
+    phi = np.zeros((c, 3, 3), np.float32)
+    phi[:, 0, 2] = rng.integers(-3, 4, c).astype(np.float32)
+    y = O.learned_score(O.learned_pixel_taps(r, phi), 0.0, 1, 1, h, wd)
+    exp = np.zeros((n, h, wd), np.float64)
+    for i in range(h):
+        for j in range(wd):
+            yy, xx = i - 1 + 0, j - 1 + 2
+            if 0 <= yy < h and 0 <= xx < wd:
+                exp[0, i, j] = float((r[0, yy, xx].astype(np.float64) * phi[:, 0, 2]).sum())
+    assert np.array_equal(y.astype(np.float64), exp)
+
+
+def test_learned_gate_with_unit_phi_is_input_norm_p1_on_growing_frames():
+    """phi = 1, bias = -eps and non-negative residuals: f = s - eps, so f > 0 iff s > eps (Eq. 5, p = 1)."""
+    rng = _rng(86)
+    n, h, wd, c, co, k = 1, 10, 12, 16, 8, 3
+    w = rng.normal(0, 0.3, (co, c, k, k)).astype(np.float32)
+    x = rng.random((n, h, wd, c), dtype=np.float32)
+    frames = [x]
+    for t in range(4):
+        grow = (rng.random(x.shape[:3]) < 0.04)[..., None]
+        x = (x + rng.random(x.shape, dtype=np.float32) * 0.1 * grow).astype(np.float32)
+        frames.append(x)
+    eps = 0.3
+    a = O.SkipConvOracle(w, n=n, h=h, w=wd, eps=0.0, norm_p=2, gate="learned",
+                         gate_weight=np.ones((c, k, k), np.float32), gate_bias=-eps)
+    b = O.SkipConvOracle(w, n=n, h=h, w=wd, eps=eps, norm_p=1, gate="input")
+    partial = 0
+    for f in frames:
+        ra, rb = a.step(f), b.step(f)
+        assert np.array_equal(ra["site_mask"], rb["site_mask"])
+        assert np.array_equal(ra["z"], rb["z"])
+        partial += 0 < int(ra["site_mask"].sum()) < ra["site_mask"].size
+    assert partial >= 3  # the non-reference masks are neither all on nor all off
+
+
+def test_learned_gate_nan_reference_and_strictness():
+    y = np.array([[[0.0, -0.0, 1e-30, -1e-30, np.nan]]], np.float32)
+    assert O.learned_gate(y, False).tolist() == [[[False, False, True, False, True]]]
+    assert O.learned_gate(y, True).all()
