@@ -88,7 +88,8 @@ def gpu_stats(layer_kw, wt, frames_dev):
     return stats
 
 
-def eps_for_density(stats, block, h_out, w_out, target):
+def block_quantile(stats, block, h_out, w_out, target):
+    """Value v such that about `target` of the blocks have a site statistic above v."""
     vals = []
     for s in stats:
         n = s.shape[0]
@@ -97,7 +98,12 @@ def eps_for_density(stats, block, h_out, w_out, target):
         pad[:, :h_out, :w_out] = np.nan_to_num(s, nan=np.inf)
         vals.append(pad.reshape(n, hb, block, wb, block).max(axis=(2, 4)).reshape(-1))
     v = np.concatenate(vals).astype(np.float64)
-    return float(np.sqrt(max(float(np.quantile(v, 1.0 - target)), 0.0)))
+    return float(np.quantile(v, 1.0 - target))
+
+
+def eps_for_density(stats, block, h_out, w_out, target):
+    """Input-Norm eps (p = 2: the statistic is compared with eps^2) for about `target` block density."""
+    return float(np.sqrt(max(block_quantile(stats, block, h_out, w_out, target), 0.0)))
 
 
 # ------------------------------------------------------------------ timing --
@@ -488,6 +494,29 @@ def main():
         r = measure_point(mk(block, e_out, gate="output"), frames_dev, sweep_steps, len(clip), geom,
                           label=f"output-norm gate b={block} d={args.density}")
         r.update({"block": block, "target_density": args.density, "gate": "output-norm", "eps": e_out})
+        sweep.append(r)
+        # learned gate (Eq. 8 at inference; split pipeline): seeded random phi,
+        # bias from the GPU's own scores for the same block density
+        import torch
+        rng = np.random.Generator(np.random.PCG64(7))
+        phi = torch.from_numpy(rng.normal(0, 0.05, (spec.c_in, spec.k, spec.k)).astype(np.float32)).cuda()
+        probe = SkipConv(wt, eps=0.0, block=1, keep_stats=True, gate="learned", **layer_kw)
+        probe.set_gate_weights(phi, 0.0)
+        scores = []
+        for t, x in enumerate(frames_dev):
+            probe.step(x)
+            if t > 0:
+                torch.cuda.synchronize()
+                scores.append(probe.stat())
+        probe.close()
+        bias = -block_quantile(scores, block, h_out, w_out, args.density)
+        def mk_learned():
+            lay = SkipConv(wt, eps=0.0, block=block, gate="learned", **layer_kw)
+            lay.set_gate_weights(phi, bias)
+            return lay
+        r = measure_point(mk_learned, frames_dev, sweep_steps, len(clip), geom,
+                          label=f"learned gate b={block} d={args.density}")
+        r.update({"block": block, "target_density": args.density, "gate": "learned", "bias": bias})
         sweep.append(r)
         tus = torch_dense_us(wt, (wl.n, wl.h, wl.w, wl.c), spec.stride)
         sweep.append({"label": "torch conv2d (MIOpen), dense, same shape", "us_per_frame_batch": tus,

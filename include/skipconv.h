@@ -11,6 +11,8 @@
  *   Eq. 7  Output-Norm gate g = round(sigmoid(||w|| ||r_t|| - eps)), ||w|| the
  *          norm of the whole weight tensor (Young's inequality, Eq. 6, makes
  *          the product a bound on the norm of the skipped update).
+ *   Eq. 8  Gumbel gate at inference g = round(sigmoid(f(r_t; phi))), f a
+ *          convolution with one output channel and the layer's geometry.
  *   Sec. 3.2.2 structured gates: max-pool the gate with kernel = stride = b,
  *          then nearest upsample, so the mask is constant on b x b blocks.
  *   Sec. 3.1 the first frame (and each reference frame after a reset, the
@@ -66,8 +68,14 @@ enum { SKIPCONV_SUPPORT_RF = 0, SKIPCONV_SUPPORT_CENTRE = 1 };
  *                W = sum |w| (p = 1) or sum w^2 (p = 2) over the whole weight
  *                tensor, summed in fp64 in ascending OIHW order at create; the
  *                product is rounded once in fp64.
- * A NaN statistic turns the gate on in both; a reference frame is dense. */
-enum { SKIPCONV_GATE_INPUT_NORM = 0, SKIPCONV_GATE_OUTPUT_NORM = 1 };
+ *   LEARNED      (Eq. 8, inference): f > 0, f(r; phi) = bias + sum over the
+ *                in-frame taps (row-major) of a[q, tap], a[q, tap] = sum_c
+ *                phi[c, tap] * r[q, c] over chunks of 8 channels (ascending
+ *                within a chunk, chunk sums ascending), all fp32 without FMA;
+ *                phi and bias come from skipconv_set_gate_weights; eps and
+ *                norm_p are not used. Split pipeline only.
+ * A NaN statistic turns the gate on in all three; a reference frame is dense. */
+enum { SKIPCONV_GATE_INPUT_NORM = 0, SKIPCONV_GATE_OUTPUT_NORM = 1, SKIPCONV_GATE_LEARNED = 2 };
 
 /* Optional activation output kept beside z, for chaining layers: NONE = no
  * buffer; IDENTITY = dtype(z); RELU = dtype(max(z, 0)). It changes only at
@@ -156,6 +164,15 @@ int skipconv_reset(skipconv_t h);
 
 /* Change eps for later steps (same rules as the descriptor field). */
 int skipconv_set_eps(skipconv_t h, float eps);
+
+/* Parameters of a SKIPCONV_GATE_LEARNED layer's gate convolution (Eq. 8).
+ *   phi:  device pointer, fp32, c_in x k x k (a one-output-channel OIHW
+ *         tensor); copied and repacked on `stream`, so it may be freed once
+ *         that work completes.
+ *   bias: the gate convolution's bias (not NaN).
+ * Required before the first step of such a layer (E_STATE otherwise); may be
+ * called again between steps. E_STATE for layers with another gate. */
+int skipconv_set_gate_weights(skipconv_t h, const float* phi, float bias, void* stream);
 
 /* Release the handle and memory the library allocated. NULL is a no-op.
  * Work still enqueued on the handle's streams must be complete. */

@@ -126,7 +126,51 @@ __device__ void halo_partials(const GateParams& p, int n, int iy0, int ix0, int 
   }
 }
 
-template <typename T, int VEC>
+// Learned gate (Eq. 8 at inference): one thread per halo pixel forms, for
+// every tap (kh, kw), a[q, tap] = sum_c phi[tap][c] * r[q, c] in the canonical
+// chunked order (8 channels ascending within a chunk from +0, chunk sums
+// ascending from +0, one rounding per multiply and per add), and copies the
+// pixel into the spare x_{t-1} slot if the tile owns it. phi is staged in LDS.
+template <typename T, int KL>
+__device__ void learned_halo(const GateParams& p, int n, int iy0, int ix0, int hh, int hw, int own_y0,
+                             int own_y1, int own_x0, int own_x1, float* a2, const float* phi) {
+  constexpr int K2 = KL * KL;
+  const T* xt = static_cast<const T*>(p.x_t);
+  const T* xp = static_cast<const T*>(p.x_prev);
+  T* keep = static_cast<T*>(p.x_keep);
+  const int c = p.c;
+  for (int q = threadIdx.x; q < hh * hw; q += kGateThreads) {
+    const int hy = q / hw, hx = q - hy * hw;
+    const int y = iy0 + hy, x = ix0 + hx;
+    const bool in = y >= 0 && y < p.h && x >= 0 && x < p.w;
+    const bool own = in && p.copy_in_halo && y >= own_y0 && y < own_y1 && x >= own_x0 && x < own_x1;
+    float acc[K2];
+#pragma unroll
+    for (int t = 0; t < K2; ++t) acc[t] = 0.0f;
+    if (in) {
+      const size_t base = ((size_t)(n * p.h + y) * p.w + x) * c;
+      for (int c0 = 0; c0 < c; c0 += kChunk) {
+        const int nel = min(kChunk, c - c0);
+        float part[K2];
+#pragma unroll
+        for (int t = 0; t < K2; ++t) part[t] = 0.0f;
+        for (int j = 0; j < nel; ++j) {
+          const float vt = Elem<T>::load1(xt, base + c0 + j);
+          const float r = p.reference ? vt : __fsub_rn(vt, Elem<T>::load1(xp, base + c0 + j));
+          if (own) keep[base + c0 + j] = xt[base + c0 + j];
+#pragma unroll
+          for (int t = 0; t < K2; ++t) part[t] = add_rn(part[t], mul_rn(phi[t * c + c0 + j], r));
+        }
+#pragma unroll
+        for (int t = 0; t < K2; ++t) acc[t] = add_rn(acc[t], part[t]);
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < K2; ++t) a2[q * K2 + t] = acc[t];
+  }
+}
+
+template <typename T, int VEC, int KL>
 __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
   extern __shared__ float lds[];
   __shared__ uint32_t blk_flag[kMaxTileBlocks];
@@ -155,17 +199,29 @@ __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
   const int nblk_y = (oh + p.block - 1) / p.block, nblk_x = (ow + p.block - 1) / p.block;
   for (int i = threadIdx.x; i < kMaxTileBlocks; i += kGateThreads) blk_flag[i] = 0u;
 
-  halo_partials<T, VEC>(p, n, iy0, ix0, hh, hw, own_y0, own_y1, own_x0, own_x1, part);
-  __syncthreads();
-  for (int q = threadIdx.x; q < hh * hw; q += kGateThreads) {
-    const int hy = q / hw, hx = q - hy * hw;
-    const int y = iy0 + hy, x = ix0 + hx;
-    float a = 0.0f;
-    if (y >= 0 && y < p.h && x >= 0 && x < p.w) {
-      const float* pp = part + q * p.stage_stride;
-      for (int ch = 0; ch < nchk; ++ch) a = add_rn(a, pp[ch]);
+  if constexpr (KL == 0) {
+    halo_partials<T, VEC>(p, n, iy0, ix0, hh, hw, own_y0, own_y1, own_x0, own_x1, part);
+    __syncthreads();
+    for (int q = threadIdx.x; q < hh * hw; q += kGateThreads) {
+      const int hy = q / hw, hx = q - hy * hw;
+      const int y = iy0 + hy, x = ix0 + hx;
+      float a = 0.0f;
+      if (y >= 0 && y < p.h && x >= 0 && x < p.w) {
+        const float* pp = part + q * p.stage_stride;
+        for (int ch = 0; ch < nchk; ++ch) a = add_rn(a, pp[ch]);
+      }
+      a_halo[q] = a;
     }
-    a_halo[q] = a;
+  } else {
+    // stage phi ([tap][c]) in LDS when it fits, then the per-pixel, per-tap gate terms
+    const float* phi = p.phi;
+    if (p.phi_off >= 0) {
+      float* staged = lds + p.phi_off;
+      for (int i = threadIdx.x; i < KL * KL * p.c; i += kGateThreads) staged[i] = p.phi[i];
+      __syncthreads();
+      phi = staged;
+    }
+    learned_halo<T, KL>(p, n, iy0, ix0, hh, hw, own_y0, own_y1, own_x0, own_x1, lds, phi);
   }
 
   if (!p.copy_in_halo) {
@@ -186,6 +242,28 @@ __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
   for (int q = threadIdx.x; q < oh * ow; q += kGateThreads) {
     const int ly = q / ow, lx = q - ly * ow;
     float sv;
+    if constexpr (KL > 0) {
+      // gate score: in-frame taps in row-major order, then the bias; on when > 0
+      sv = 0.0f;
+      for (int kh = 0; kh < KL; ++kh) {
+        const int hy = ly * s + kh, y = iy0 + hy;
+        if (y < 0 || y >= p.h) continue;
+        for (int kw = 0; kw < KL; ++kw) {
+          const int hx = lx * s + kw, x = ix0 + hx;
+          if (x < 0 || x >= p.w) continue;
+          sv = add_rn(sv, lds[(hy * hw + hx) * (KL * KL) + kh * KL + kw]);
+        }
+      }
+      sv = add_rn(sv, p.gate_bias);
+      const bool on = p.reference || p.force_dense || sv > 0.0f || (sv != sv);
+      if (p.keep_stats) {
+        const size_t o = ((size_t)n * p.h_out + oy0 + ly) * p.w_out + ox0 + lx;
+        p.stat[o] = sv;
+        p.site_mask[o] = on ? 1 : 0;
+      }
+      if (on) blk_flag[(ly / p.block) * tb_w + lx / p.block] = 1u;
+      continue;
+    }
     if (p.support == 0) {
       sv = 0.0f;
       const float* base = a_halo + (ly * s) * hw + lx * s;
@@ -294,7 +372,30 @@ __global__ void __launch_bounds__(kScanThreads) compact_kernel(uint8_t* block_ma
 
 template <typename T, int VEC>
 static hipError_t launch_gate_t(const GateParams& p, int grid, size_t lds_bytes, hipStream_t st) {
-  hipLaunchKernelGGL((gate_kernel<T, VEC>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p);
+  switch (p.learned) {
+    case 0: hipLaunchKernelGGL((gate_kernel<T, VEC, 0>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p); break;
+    case 1: hipLaunchKernelGGL((gate_kernel<T, VEC, 1>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p); break;
+    case 3: hipLaunchKernelGGL((gate_kernel<T, VEC, 3>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p); break;
+    case 5: hipLaunchKernelGGL((gate_kernel<T, VEC, 5>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p); break;
+    case 7: hipLaunchKernelGGL((gate_kernel<T, VEC, 7>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+// Pack the learned gate's weights from [c][kh][kw] (a one-output-channel OIHW
+// tensor) to [tap][c].
+__global__ void pack_phi_kernel(const float* src, float* dst, int c, int k2) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < c * k2) {
+    const int ch = i / k2, t = i - ch * k2;
+    dst[t * c + ch] = src[i];
+  }
+}
+
+hipError_t launch_pack_phi(const float* src, float* dst, int c, int k, hipStream_t st) {
+  const int total = c * k * k;
+  hipLaunchKernelGGL(pack_phi_kernel, dim3((total + 255) / 256), dim3(256), 0, st, src, dst, c, k * k);
   return hipGetLastError();
 }
 

@@ -35,6 +35,11 @@ struct GateParams {
   uint32_t* counters;
   float* stat;                  // N x H_out x W_out (keep_stats)
   uint8_t* site_mask;           // N x H_out x W_out (keep_stats)
+  // learned gate (Eq. 8 at inference): phi [tap][c] fp32, bias; 0 = norm gates
+  int learned;
+  const float* phi;
+  float gate_bias;
+  int phi_off;                  // LDS float offset of the staged phi, or -1: read phi from memory
 };
 
 // Sparse convolution over the active sites (dense groups = 1).
@@ -86,6 +91,7 @@ int prepare_fused(const FusedParams& p);  // create time: LDS attribute; workgro
 
 hipError_t launch_gate(const GateParams& p, int dtype, int vec, int grid, size_t lds_bytes,
                        hipStream_t st);
+hipError_t launch_pack_phi(const float* src, float* dst, int c, int k, hipStream_t st);
 // Ordered compaction of the block flags into the active list and its count.
 // When tile_flags is non-NULL, block flags are first formed as the OR of the
 // (block / ts)^2 tile flags of each block (tiles_y x tiles_x tiles per image).

@@ -54,7 +54,10 @@ struct Geometry {
   int vec;              // gate load width (elements)
   size_t elem;
   size_t off_wpack, off_slot0, off_slot1, off_z, off_y, off_bmask, off_tflag, off_list, off_ctr,
-      off_stat, off_smask, total;
+      off_stat, off_smask, off_phi, total;
+  int learned;          // learned gate: its kernel size (the layer's k), else 0
+  bool phi_in_lds;      // learned gate: phi staged in LDS (else read through the caches)
+  int phi_off;          // learned gate: LDS float offset of the staged phi
   size_t wpack_bytes, x_bytes, z_bytes;
   int conv_max_tiles;
 };
@@ -90,7 +93,8 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
     return fail(err, SKIPCONV_E_UNSUPPORTED, "only groups == 1 or groups == c_in == c_out");
   if (d->block < 1 || d->block > 64) return fail(err, SKIPCONV_E_INVALID_ARG, "block must be 1..64");
   if (d->norm_p != 1 && d->norm_p != 2) return fail(err, SKIPCONV_E_INVALID_ARG, "norm_p must be 1 or 2");
-  if (d->gate != SKIPCONV_GATE_INPUT_NORM && d->gate != SKIPCONV_GATE_OUTPUT_NORM)
+  if (d->gate != SKIPCONV_GATE_INPUT_NORM && d->gate != SKIPCONV_GATE_OUTPUT_NORM &&
+      d->gate != SKIPCONV_GATE_LEARNED)
     return fail(err, SKIPCONV_E_INVALID_ARG, "gate must be a SKIPCONV_GATE_* value");
   if (d->support != SKIPCONV_SUPPORT_RF && d->support != SKIPCONV_SUPPORT_CENTRE)
     return fail(err, SKIPCONV_E_INVALID_ARG, "unknown support");
@@ -130,9 +134,15 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
   // chunk sum per (halo pixel, 8-channel chunk), odd row stride.
   const int nchk = (d->c_in + 7) / 8;
   G.stage_stride = nchk | 1;
+  G.learned = d->gate == SKIPCONV_GATE_LEARNED ? k : 0;
+  // learned gate: phi is staged in LDS unless that alone would not fit
+  const long phi_floats = (long)k * k * d->c_in;
+  G.phi_in_lds = G.learned && phi_floats * 4 <= (long)kLdsLimit / 2;
   auto gate_lds_for = [&](int ts) {
     const long eh = (long)(std::min(ts, G.h_out) - 1) * s + k;  // largest halo actually used
     const long ew = (long)(std::min(ts, G.w_out) - 1) * s + k;
+    if (G.learned)  // per-pixel, per-tap gate terms (+ the staged phi)
+      return ((eh * ew * k * k + 3) / 4 * 4 + (G.phi_in_lds ? phi_floats : 0)) * 4;
     const long halo = (eh * ew + 3) / 4 * 4;
     return (halo + eh * ew * G.stage_stride) * 4;
   };
@@ -160,6 +170,7 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
   G.hh_max = (std::min(G.ts, G.h_out) - 1) * s + k;
   G.hw_max = (std::min(G.ts, G.w_out) - 1) * s + k;
   G.halo_floats = (G.hh_max * G.hw_max + 3) / 4 * 4;
+  G.phi_off = (G.hh_max * G.hw_max * k * k + 3) / 4 * 4;
   G.rows_per_batch = G.hh_max;
   G.gate_lds = gate_lds_for(G.ts);
   if (G.gate_lds > kLdsLimit)
@@ -238,7 +249,7 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
   // sites, output tiles split over two wave groups (ntn >= 2)
   G.fused = false;
   if (!depthwise && d->dtype == SKIPCONV_BF16 && d->c_in % 32 == 0 && d->c_out % 4 == 0 && b <= 16 &&
-      G.ntn >= 2 && !(d->flags & SKIPCONV_FLAG_SPLIT_PIPELINE)) {
+      G.ntn >= 2 && !G.learned && !(d->flags & SKIPCONV_FLAG_SPLIT_PIPELINE)) {
     const int ts = b <= 8 ? b * (8 / b) : b;
     const int mw = ts <= 8 ? 1 : 4;
     if (!(mw == 4 && G.ntn > 8)) {
@@ -300,6 +311,8 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
     G.off_smask = off;
     off = align_up(off + (size_t)sites);
   }
+  G.off_phi = off;
+  if (G.learned) off = align_up(off + (size_t)k * k * d->c_in * 4);
   G.total = off;
   return SKIPCONV_OK;
 }
@@ -335,6 +348,9 @@ struct skipconv_layer {
   uint32_t* ctr() { return reinterpret_cast<uint32_t*>(ws + g.off_ctr); }
   float* stat() { return reinterpret_cast<float*>(ws + g.off_stat); }
   uint8_t* smask() { return reinterpret_cast<uint8_t*>(ws + g.off_smask); }
+  float* phi() { return reinterpret_cast<float*>(ws + g.off_phi); }
+  bool phi_set = false;      // learned gate: skipconv_set_gate_weights was called
+  float gate_bias = 0.0f;
 };
 
 namespace {
@@ -434,6 +450,10 @@ sc::GateParams gate_params(skipconv_layer* h, const void* x_t, bool ref) {
   gp.keep_stats = (d.flags & SKIPCONV_FLAG_KEEP_STATS) ? 1 : 0;
   gp.thr = threshold(d);
   gp.wnorm = h->wnorm;
+  gp.learned = g.learned;
+  gp.phi = h->phi();
+  gp.gate_bias = h->gate_bias;
+  gp.phi_off = g.phi_in_lds ? g.phi_off : -1;
   gp.block_mask = h->bmask(); gp.list = h->list(); gp.counters = h->ctr();
   gp.tile_flags = h->tflags(); gp.split_blocks = g.split_blocks;
   gp.stat = h->stat(); gp.site_mask = h->smask();
@@ -593,6 +613,8 @@ int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t
   if (!x_t) return fail(h->last_error, SKIPCONV_E_INVALID_ARG, "x_t is NULL");
   if (reinterpret_cast<uintptr_t>(x_t) % 16)
     return fail(h->last_error, SKIPCONV_E_INVALID_ARG, "x_t must be 16-byte aligned");
+  if (h->g.learned && !h->phi_set)
+    return fail(h->last_error, SKIPCONV_E_STATE, "learned gate: call skipconv_set_gate_weights first");
   hipStream_t st = static_cast<hipStream_t>(stream);
   const skipconv_desc& d = h->d;
   const Geometry& g = h->g;
@@ -665,6 +687,18 @@ int skipconv_set_eps(skipconv_t h, float eps) {
   if (!h) return SKIPCONV_E_STATE;
   if (std::isnan(eps) || eps < 0.0f) return fail(h->last_error, SKIPCONV_E_INVALID_ARG, "eps must be >= 0");
   h->d.eps = eps;
+  return SKIPCONV_OK;
+}
+
+int skipconv_set_gate_weights(skipconv_t h, const float* phi, float bias, void* stream) {
+  if (!h) return SKIPCONV_E_STATE;
+  if (!h->g.learned) return fail(h->last_error, SKIPCONV_E_STATE, "the layer's gate is not SKIPCONV_GATE_LEARNED");
+  if (!phi) return fail(h->last_error, SKIPCONV_E_INVALID_ARG, "phi is NULL");
+  if (std::isnan(bias)) return fail(h->last_error, SKIPCONV_E_INVALID_ARG, "bias is NaN");
+  const hipError_t e = sc::launch_pack_phi(phi, h->phi(), h->d.c_in, h->d.kernel, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(h, e, "set_gate_weights");
+  h->gate_bias = bias;
+  h->phi_set = true;
   return SKIPCONV_OK;
 }
 

@@ -26,7 +26,7 @@ SKIPCONV_E_SMALL_BUFFER = -6
 
 SKIPCONV_F32, SKIPCONV_BF16 = 0, 1
 SKIPCONV_SUPPORT_RF, SKIPCONV_SUPPORT_CENTRE = 0, 1
-SKIPCONV_GATE_INPUT_NORM, SKIPCONV_GATE_OUTPUT_NORM = 0, 1
+SKIPCONV_GATE_INPUT_NORM, SKIPCONV_GATE_OUTPUT_NORM, SKIPCONV_GATE_LEARNED = 0, 1, 2
 SKIPCONV_ACT_NONE, SKIPCONV_ACT_IDENTITY, SKIPCONV_ACT_RELU = 0, 1, 2
 SKIPCONV_FLAG_KEEP_STATS, SKIPCONV_FLAG_FORCE_DENSE, SKIPCONV_FLAG_SPLIT_PIPELINE = 1, 2, 4
 
@@ -58,6 +58,7 @@ _SIGS = {
     "skipconv_step": (ctypes.c_int, [_P, _P, _P, ctypes.POINTER(_P)]),
     "skipconv_reset": (ctypes.c_int, [_P]),
     "skipconv_set_eps": (ctypes.c_int, [_P, ctypes.c_float]),
+    "skipconv_set_gate_weights": (ctypes.c_int, [_P, _P, ctypes.c_float, _P]),
     "skipconv_destroy": (ctypes.c_int, [_P]),
     "skipconv_activation": (ctypes.c_int, [_P, ctypes.POINTER(_P)]),
     "skipconv_get_desc": (ctypes.c_int, [_P, _D]),
@@ -153,6 +154,10 @@ def skipconv_set_eps(h: int, eps: float) -> None:
     _check(lib().skipconv_set_eps(h, eps), h)
 
 
+def skipconv_set_gate_weights(h: int, phi_ptr: int, bias: float, stream: int) -> None:
+    _check(lib().skipconv_set_gate_weights(h, phi_ptr, bias, stream), h)
+
+
 def skipconv_destroy(h: int) -> None:
     _check(lib().skipconv_destroy(h))
 
@@ -241,7 +246,8 @@ def skipconv_timing_read(h: int, stream: int, capacity: int = 0):
 
 _SUPPORT = {"rf": SKIPCONV_SUPPORT_RF, "centre": SKIPCONV_SUPPORT_CENTRE}
 _ACT = {"none": SKIPCONV_ACT_NONE, "identity": SKIPCONV_ACT_IDENTITY, "relu": SKIPCONV_ACT_RELU}
-_GATE = {"input": SKIPCONV_GATE_INPUT_NORM, "output": SKIPCONV_GATE_OUTPUT_NORM}
+_GATE = {"input": SKIPCONV_GATE_INPUT_NORM, "output": SKIPCONV_GATE_OUTPUT_NORM,
+         "learned": SKIPCONV_GATE_LEARNED}
 
 
 def make_desc(*, n, h, w, c_in, c_out, kernel, stride=1, pad=-1, groups=1, block=1, norm_p=2,
@@ -339,6 +345,15 @@ class SkipConv:
     def set_eps(self, eps: float):
         skipconv_set_eps(self.handle, eps)
         self.desc.eps = eps
+
+    def set_gate_weights(self, phi, bias: float = 0.0):
+        """Learned gate (Eq. 8): phi is a float32 GPU tensor of C_in x k x k (or 1 x C_in x k x k)."""
+        t = self.torch
+        if not phi.is_cuda or phi.dtype != t.float32 or phi.numel() != self.desc.c_in * self.desc.kernel ** 2:
+            raise ValueError("phi must be a float32 GPU tensor of c_in x k x k elements")
+        phi = phi.contiguous()
+        skipconv_set_gate_weights(self.handle, phi.data_ptr(), bias, self._stream())
+        self._phi = phi  # keep the source alive until the repack has run
 
     def active_count(self) -> Tuple[int, int]:
         return skipconv_active_count(self.handle, self._stream())

@@ -46,6 +46,7 @@ def good(**kw):
     ("flags", 8, S.SKIPCONV_E_INVALID_ARG), ("eps", -1.0, S.SKIPCONV_E_INVALID_ARG),
     ("eps", float("nan"), S.SKIPCONV_E_INVALID_ARG), ("c_out", 272, S.SKIPCONV_E_UNSUPPORTED),
     ("gate", 7, S.SKIPCONV_E_INVALID_ARG), ("gate", -1, S.SKIPCONV_E_INVALID_ARG),
+    ("gate", 3, S.SKIPCONV_E_INVALID_ARG),
 ])
 def test_validation_codes(lib, field, value, code):
     d = good()
@@ -64,6 +65,8 @@ def test_valid_variants(lib):
     assert S.skipconv_validate(good(support="centre", norm_p=1)) == 0
     assert S.skipconv_validate(good(gate="output")) == 0
     assert S.skipconv_validate(good(gate="output", norm_p=1, dtype="f32")) == 0
+    assert S.skipconv_validate(good(gate="learned")) == 0
+    assert S.skipconv_validate(good(gate="learned", kernel=7, dtype="f32", c_in=256)) == 0
 
 
 @pytest.mark.parametrize("h,w,k,s,pad,b,exp", [

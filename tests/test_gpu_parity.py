@@ -21,14 +21,16 @@ pytestmark = pytest.mark.gpu
 
 def _layer_pair(w_f32, *, n, h, w, dtype, eps, block, stride=1, pad=-1, groups=1, norm_p=2,
                 support="rf", keep_stats=True, act_out="none", force_dense=False, split=False,
-                gate="input"):
+                gate="input", phi=None, gate_bias=0.0):
     ws = weight_storage(w_f32, dtype)
     layer = S.SkipConv(to_device(ws, dtype), n=n, h=h, w=w, stride=stride, pad=pad, groups=groups,
                        eps=eps, block=block, norm_p=norm_p, support=support, keep_stats=keep_stats,
                        act_out=act_out, force_dense=force_dense, split=split, gate=gate)
+    if gate == "learned":
+        layer.set_gate_weights(torch.from_numpy(np.ascontiguousarray(phi, np.float32)).cuda(), gate_bias)
     orc = O.SkipConvOracle(ws, n=n, h=h, w=w, stride=stride, pad=None if pad == -1 else pad,
                            groups=groups, eps=eps, block=block, norm_p=norm_p, support=support,
-                           dtype=dtype, gate=gate)
+                           dtype=dtype, gate=gate, gate_weight=phi, gate_bias=gate_bias)
     return layer, orc
 
 
@@ -463,3 +465,83 @@ def test_output_norm_gate_depthwise_and_stride(split):
             frames.append(x)
         run_single(frames, w, dtype=dtype, eps=2.0, block=2, norm_p=1, gate="output", groups=groups,
                    stride=stride, tag=f"output-norm c={c_in}->{c_out} g={groups} s={stride}", split=split)
+
+
+# --------------------------------------------------- learned gate (Eq. 8) --
+
+def _learned_bias(frames, phi, dtype, k, stride, site_density):
+    """Gate bias giving about `site_density` of sites on (oracle scores without bias)."""
+    pad = (k - 1) // 2
+    vals, prev = [], None
+    for f in frames:
+        x = O.storage_to_f32(syn.to_storage(f, dtype), dtype)
+        if prev is not None:
+            a = O.learned_pixel_taps(O.residual(x, prev), phi)
+            ho, wo = O.out_size(x.shape[1], k, stride, pad), O.out_size(x.shape[2], k, stride, pad)
+            vals.append(O.learned_score(a, 0.0, stride, pad, ho, wo).reshape(-1))
+        prev = x
+    return float(np.float32(-np.quantile(np.concatenate(vals), 1.0 - site_density)))
+
+
+@pytest.mark.parametrize("block", [1, 8])
+def test_learned_gate_rect64(block):
+    wl = syn.workloads()["rect64"]
+    frames = list(wl.video(10))
+    rng = np.random.Generator(np.random.PCG64(95))
+    phi = rng.normal(0, 0.05, (64, 3, 3)).astype(np.float32)
+    # per-site score quantile; with 8 x 8 blocks a much smaller site fraction leaves blocks off
+    bias = _learned_bias(frames, phi, "bf16", 3, 1, 0.25 if block == 1 else 0.003)
+    worst, dens = run_single(frames, wl.weights()[0], dtype="bf16", eps=0.0, block=block, gate="learned",
+                             phi=phi, gate_bias=bias, tag=f"rect64 learned gate b={block}", resets=(6,))
+    assert 0.0 < np.mean(dens[1:]) < 1.0
+
+
+@pytest.mark.parametrize("case", [
+    # c_in, c_out, k, stride, dtype, block, groups
+    (16, 16, 3, 1, "f32", 1, 1),
+    (12, 24, 5, 2, "f32", 2, 1),
+    (32, 64, 1, 1, "bf16", 4, 1),
+    (8, 16, 7, 1, "bf16", 1, 1),
+    (24, 24, 3, 1, "bf16", 1, 24),
+    (64, 64, 3, 1, "bf16", 8, 1),
+    (256, 16, 7, 1, "f32", 1, 1),   # phi (50 KB) read through the caches, not staged in LDS
+], ids=["f32k3", "f32k5s2", "bf16k1", "bf16k7", "bf16dw", "bf16halo", "f32k7c256"])
+def test_learned_gate_geometries(case):
+    c_in, c_out, k, stride, dtype, block, groups = case
+    rng = np.random.Generator(np.random.PCG64(96 + k + c_in))
+    w = rng.normal(0, 0.2, (c_out, c_in // groups, k, k)).astype(np.float32)
+    phi = rng.normal(0, 0.3, (c_in, k, k)).astype(np.float32)
+    x = rng.random((2, 21, 17, c_in), dtype=np.float32)
+    frames = [x]
+    for t in range(4):
+        x = x.copy()
+        x[:, 2 + 3 * t:6 + 3 * t, 1 + 2 * t:7 + 2 * t] += rng.normal(0, 0.5, (2, 4, 6, c_in)).astype(np.float32)
+        frames.append(x)
+    bias = _learned_bias(frames, phi, dtype, k, stride, 0.3)
+    run_single(frames, w, dtype=dtype, eps=0.0, block=block, stride=stride, groups=groups, gate="learned",
+               phi=phi, gate_bias=bias, tag=f"learned {case}", resets=(3,))
+
+
+def test_learned_gate_requires_weights_and_nan_turns_on():
+    wl = syn.workloads()["square16"]
+    w = wl.weights()[0]
+    ws = weight_storage(w, "f32")
+    layer = S.SkipConv(to_device(ws, "f32"), n=1, h=32, w=32, gate="learned", block=1, keep_stats=True)
+    x = to_device(syn.to_storage(next(iter(wl.video())), "f32"), "f32")
+    with pytest.raises(S.SkipConvError) as ei:
+        layer.step(x)
+    assert ei.value.code == S.SKIPCONV_E_STATE
+    # an input-norm layer refuses gate weights
+    other = S.SkipConv(to_device(ws, "f32"), n=1, h=32, w=32, block=1)
+    with pytest.raises(S.SkipConvError):
+        other.set_gate_weights(torch.zeros(16 * 9, device="cuda"), 0.0)
+    other.close()
+    layer.close()
+    # NaN residual: score NaN, gate on, z NaN there (and everywhere the NaN reaches)
+    frames = list(wl.video())[:3]
+    f2 = frames[2].copy()
+    f2[0, 5, 7, 3] = np.nan
+    frames[2] = f2
+    phi = np.full((16, 3, 3), -1.0, np.float32)  # strongly negative scores: off unless NaN
+    run_single(frames, w, dtype="f32", eps=0.0, block=1, gate="learned", phi=phi, gate_bias=-1.0,
+               tag="learned NaN")
