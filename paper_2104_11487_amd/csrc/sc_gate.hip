@@ -130,8 +130,10 @@ __device__ void halo_partials(const GateParams& p, int n, int iy0, int ix0, int 
 // every tap (kh, kw), a[q, tap] = sum_c phi[tap][c] * r[q, c] in the canonical
 // chunked order (8 channels ascending within a chunk from +0, chunk sums
 // ascending from +0, one rounding per multiply and per add), and copies the
-// pixel into the spare x_{t-1} slot if the tile owns it. phi is staged in LDS.
-template <typename T, int KL>
+// pixel into the spare x_{t-1} slot if the tile owns it. phi is [tap][c]
+// (staged in LDS when it fits). VEC = 8: channel chunks move as 16-byte
+// vectors (c % 8 == 0).
+template <typename T, int VEC, int KL>
 __device__ void learned_halo(const GateParams& p, int n, int iy0, int ix0, int hh, int hw, int own_y0,
                              int own_y1, int own_x0, int own_x1, float* a2, const float* phi) {
   constexpr int K2 = KL * KL;
@@ -151,18 +153,38 @@ __device__ void learned_halo(const GateParams& p, int n, int iy0, int ix0, int h
       const size_t base = ((size_t)(n * p.h + y) * p.w + x) * c;
       for (int c0 = 0; c0 < c; c0 += kChunk) {
         const int nel = min(kChunk, c - c0);
-        float part[K2];
+        float r[kChunk];
+        if (VEC == kChunk) {
+          float vt[kChunk], vp[kChunk];
+          load_vec<T, kChunk>(xt, base + c0, vt);
+          if (!p.reference) load_vec<T, kChunk>(xp, base + c0, vp);
 #pragma unroll
-        for (int t = 0; t < K2; ++t) part[t] = 0.0f;
-        for (int j = 0; j < nel; ++j) {
-          const float vt = Elem<T>::load1(xt, base + c0 + j);
-          const float r = p.reference ? vt : __fsub_rn(vt, Elem<T>::load1(xp, base + c0 + j));
-          if (own) keep[base + c0 + j] = xt[base + c0 + j];
+          for (int j = 0; j < kChunk; ++j) r[j] = p.reference ? vt[j] : __fsub_rn(vt[j], vp[j]);
+          if (own) copy_vec<T, kChunk>(keep, xt, base + c0);
+        } else {
 #pragma unroll
-          for (int t = 0; t < K2; ++t) part[t] = add_rn(part[t], mul_rn(phi[t * c + c0 + j], r));
+          for (int j = 0; j < kChunk; ++j) {
+            const float vt = j < nel ? Elem<T>::load1(xt, base + c0 + j) : 0.0f;
+            const float vp = (j < nel && !p.reference) ? Elem<T>::load1(xp, base + c0 + j) : 0.0f;
+            r[j] = __fsub_rn(vt, vp);
+            if (own && j < nel) keep[base + c0 + j] = xt[base + c0 + j];
+          }
         }
 #pragma unroll
-        for (int t = 0; t < K2; ++t) acc[t] = add_rn(acc[t], part[t]);
+        for (int t = 0; t < K2; ++t) {
+          const float* ph = phi + t * c + c0;
+          float part = 0.0f;
+          if (VEC == kChunk) {
+            const float4 f0 = *reinterpret_cast<const float4*>(ph);
+            const float4 f1 = *reinterpret_cast<const float4*>(ph + 4);
+            const float f[kChunk] = {f0.x, f0.y, f0.z, f0.w, f1.x, f1.y, f1.z, f1.w};
+#pragma unroll
+            for (int j = 0; j < kChunk; ++j) part = add_rn(part, mul_rn(f[j], r[j]));
+          } else {
+            for (int j = 0; j < nel; ++j) part = add_rn(part, mul_rn(ph[j], r[j]));
+          }
+          acc[t] = add_rn(acc[t], part);
+        }
       }
     }
 #pragma unroll
@@ -221,7 +243,7 @@ __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
       __syncthreads();
       phi = staged;
     }
-    learned_halo<T, KL>(p, n, iy0, ix0, hh, hw, own_y0, own_y1, own_x0, own_x1, lds, phi);
+    learned_halo<T, VEC, KL>(p, n, iy0, ix0, hh, hw, own_y0, own_y1, own_x0, own_x1, lds, phi);
   }
 
   if (!p.copy_in_halo) {

@@ -151,6 +151,7 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
     const int t8 = b <= 8 ? b * (8 / b) : b;
     const long n16 = (long)d->n * ((G.h_out + t16 - 1) / t16) * ((G.w_out + t16 - 1) / t16);
     G.ts = (n16 < 512 && b <= 8) ? t8 : t16;
+    if (G.learned && b <= 8) G.ts = t8;  // the per-tap learned gate is VALU-heavy: more, smaller tiles
     if (gate_lds_for(G.ts) > (long)kLdsLimit && b <= 8) G.ts = t8;
     // blocks larger than a tile that fits: 16 x 16 (or 8 x 8) tiles, one flag
     // per tile, OR-ed per block by the compaction kernel
