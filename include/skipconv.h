@@ -87,11 +87,16 @@ enum { SKIPCONV_ACT_NONE = 0, SKIPCONV_ACT_IDENTITY = 1, SKIPCONV_ACT_RELU = 2 }
  * skipconv_copy_site_mask. FORCE_DENSE: every block is active on every frame
  * (the same kernels, run dense; used as the dense baseline). SPLIT_PIPELINE:
  * never use the fused single-pass kernel; run the gate, compaction and
- * convolution kernels separately (the choice is otherwise made at create). */
+ * convolution kernels separately (the choice is otherwise made at create).
+ * EMIT_RESIDUAL (needs an activation output): after every step, also hand a
+ * chained successor its residual: r = fl32(y_new - y_old) at the blocks this
+ * step updated (fp32, plus its bf16 rounding for bf16 layers) and r = 0 at
+ * the blocks only the previous step updated; see skipconv_step_chained. */
 enum {
   SKIPCONV_FLAG_KEEP_STATS = 1u,
   SKIPCONV_FLAG_FORCE_DENSE = 2u,
-  SKIPCONV_FLAG_SPLIT_PIPELINE = 4u
+  SKIPCONV_FLAG_SPLIT_PIPELINE = 4u,
+  SKIPCONV_FLAG_EMIT_RESIDUAL = 8u
 };
 
 typedef struct skipconv_desc {
@@ -157,6 +162,23 @@ int skipconv_create(const skipconv_desc* d, const void* weights, void* workspace
  * kernel (gather of residual patches, MFMA product over active sites only,
  * accumulate into z) on `stream`; no host synchronisation. */
 int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t);
+
+/* Process one frame of a layer whose input is the activation output of the
+ * layer `up` (sparse residual propagation between stacked layers, Sec. 3.1:
+ * the successor's input changes only where `up` updated z). `up` must have
+ * been created with SKIPCONV_FLAG_EMIT_RESIDUAL, its output must match this
+ * layer's input (n, h_out = h, w_out = w, c_out = c_in, same dtype), and it
+ * must have stepped the same frame already on `stream` (stream order).
+ * Instead of reading x_t and x_{t-1} over the whole frame, the gate reads
+ * `up`'s residual, and gate tiles whose input region holds no active block of
+ * `up` skip their loads (norm gates); the convolution reads the residual
+ * operand. Masks, counts and z are exactly those that skipconv_step with
+ * x_t = dtype(act(z_up)) would give. A reference frame of this layer reads
+ * `up`'s activation output in full. This layer's own x_{t-1} slots are not
+ * maintained: step it with skipconv_step only after a reset.
+ * Errors: E_INVALID_ARG (NULL or mismatched `up`), E_STATE (`up` does not emit
+ * its residual or has not stepped), E_HIP. */
+int skipconv_step_chained(skipconv_t h, skipconv_t up, void* stream, const float** z_t);
 
 /* Make the next step a reference frame: x_{t-1} taken as zero, every site
  * active, z assigned instead of accumulated (Sec. 3.1, Table 4). */

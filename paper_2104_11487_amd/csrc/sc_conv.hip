@@ -113,7 +113,7 @@ __device__ __forceinline__ bf16x8 gather_a_bf16(const ConvParams& p, const uint1
       const size_t off = ((size_t)(st.n * p.h + y) * p.w + x) * p.c + c0;
       float a[8], b[8];
       Elem<uint16_t>::load8(xt, off, a);
-      if (!p.reference) {
+      if (!p.no_prev) {
         Elem<uint16_t>::load8(xp, off, b);
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[e] = __fsub_rn(a[e], b[e]);
@@ -134,7 +134,7 @@ __device__ __forceinline__ bf16x8 gather_a_bf16(const ConvParams& p, const uint1
         if (y >= 0 && y < p.h && x >= 0 && x < p.w) {
           const size_t off = ((size_t)(st.n * p.h + y) * p.w + x) * p.c + ci;
           const float a = bf16_to_f32(xt[off]);
-          const float b = p.reference ? 0.0f : bf16_to_f32(xp[off]);
+          const float b = p.no_prev ? 0.0f : bf16_to_f32(xp[off]);
           v[e] = __fsub_rn(a, b);
         }
       }
@@ -300,7 +300,7 @@ conv_halo_kernel(ConvParams p, HaloParams hp) {
         if (in[u]) {
           const size_t off = ((size_t)(n * p.h + y) * p.w + x) * c + ch * 8;
           ra[u] = *reinterpret_cast<const uint4*>(xt + off);
-          if (!p.reference) rb[u] = *reinterpret_cast<const uint4*>(xp + off);
+          if (!p.no_prev) rb[u] = *reinterpret_cast<const uint4*>(xp + off);
         }
       }
 #pragma unroll
@@ -436,7 +436,7 @@ __global__ void __launch_bounds__(kConvThreads) conv_f32_kernel(ConvParams p) {
         const int y = iy + kh, x = ix + kw;
         if (y >= 0 && y < p.h && x >= 0 && x < p.w) {
           const size_t off = ((size_t)(st.n * p.h + y) * p.w + x) * p.c + ci;
-          a = p.reference ? xt[off] : __fsub_rn(xt[off], xp[off]);
+          a = p.no_prev ? xt[off] : __fsub_rn(xt[off], xp[off]);
         }
       }
       const float* wk = wp + (size_t)ks * NTN * 64 + lane;
@@ -496,18 +496,18 @@ __global__ void __launch_bounds__(kConvThreads) depthwise_kernel(ConvParams p) {
           float a[VEC], b[VEC];
           if (VEC == 8) {
             Elem<T>::load8(xt, off, a);
-            if (!p.reference) Elem<T>::load8(xp, off, b);
+            if (!p.no_prev) Elem<T>::load8(xp, off, b);
           } else if (VEC == 4) {
             Elem<T>::load4(xt, off, a);
-            if (!p.reference) Elem<T>::load4(xp, off, b);
+            if (!p.no_prev) Elem<T>::load4(xp, off, b);
           } else {
             a[0] = Elem<T>::load1(xt, off);
-            if (!p.reference) b[0] = Elem<T>::load1(xp, off);
+            if (!p.no_prev) b[0] = Elem<T>::load1(xp, off);
           }
           const float* wt = wp + (kh * p.k + kw) * p.c + c0;
 #pragma unroll
           for (int j = 0; j < VEC; ++j) {
-            float r = p.reference ? a[j] : __fsub_rn(a[j], b[j]);
+            float r = p.no_prev ? a[j] : __fsub_rn(a[j], b[j]);
             if (bf16) r = bf16_to_f32(f32_to_bf16(r));
             acc[j] = __builtin_fmaf(wt[j], r, acc[j]);
           }

@@ -67,26 +67,26 @@ __device__ void halo_partials(const GateParams& p, int n, int iy0, int ix0, int 
       slot[u] = idx < total ? px * p.stage_stride + ch : -1;
       nel[u] = min(kChunk, c - ch * kChunk);
       off[u] = in[u] ? ((size_t)(n * p.h + y) * p.w + x) * c + ch * kChunk : 0;
-      own[u] = in[u] && p.copy_in_halo && y >= own_y0 && y < own_y1 && x >= own_x0 && x < own_x1;
+      own[u] = in[u] && keep && p.copy_in_halo && y >= own_y0 && y < own_y1 && x >= own_x0 && x < own_x1;
       if (kPacked) {
         raw_t[kPacked ? u : 0] = uint4{0u, 0u, 0u, 0u};
         raw_p[kPacked ? u : 0] = uint4{0u, 0u, 0u, 0u};
         if (in[u]) {
           raw_t[kPacked ? u : 0] = *reinterpret_cast<const uint4*>(xt + off[u]);
-          if (!p.reference) raw_p[kPacked ? u : 0] = *reinterpret_cast<const uint4*>(xp + off[u]);
+          if (!p.no_prev) raw_p[kPacked ? u : 0] = *reinterpret_cast<const uint4*>(xp + off[u]);
         }
       } else if (in[u]) {
         const int uu = kPacked ? 0 : u;
         if (VEC == kChunk) {
           load_vec<T, kChunk>(xt, off[u], vt[uu]);
-          if (!p.reference) load_vec<T, kChunk>(xp, off[u], vp[uu]);
+          if (!p.no_prev) load_vec<T, kChunk>(xp, off[u], vp[uu]);
           else
             for (int j = 0; j < kChunk; ++j) vp[uu][j] = 0.0f;
         } else {
 #pragma unroll
           for (int j = 0; j < kChunk; ++j) {
             vt[uu][j] = j < nel[u] ? Elem<T>::load1(xt, off[u] + j) : 0.0f;
-            vp[uu][j] = (j < nel[u] && !p.reference) ? Elem<T>::load1(xp, off[u] + j) : 0.0f;
+            vp[uu][j] = (j < nel[u] && !p.no_prev) ? Elem<T>::load1(xp, off[u] + j) : 0.0f;
           }
         }
       }
@@ -108,7 +108,7 @@ __device__ void halo_partials(const GateParams& p, int n, int iy0, int ix0, int 
         } else {
           const int uu = kPacked ? 0 : u;
 #pragma unroll
-          for (int j = 0; j < kChunk; ++j) r[j] = p.reference ? vt[uu][j] : __fsub_rn(vt[uu][j], vp[uu][j]);
+          for (int j = 0; j < kChunk; ++j) r[j] = p.no_prev ? vt[uu][j] : __fsub_rn(vt[uu][j], vp[uu][j]);
         }
         if (VEC == kChunk) {
           part_u = chunk_sum<kChunk>(r, p.norm_p);
@@ -145,7 +145,7 @@ __device__ void learned_halo(const GateParams& p, int n, int iy0, int ix0, int h
     const int hy = q / hw, hx = q - hy * hw;
     const int y = iy0 + hy, x = ix0 + hx;
     const bool in = y >= 0 && y < p.h && x >= 0 && x < p.w;
-    const bool own = in && p.copy_in_halo && y >= own_y0 && y < own_y1 && x >= own_x0 && x < own_x1;
+    const bool own = in && keep && p.copy_in_halo && y >= own_y0 && y < own_y1 && x >= own_x0 && x < own_x1;
     float acc[K2];
 #pragma unroll
     for (int t = 0; t < K2; ++t) acc[t] = 0.0f;
@@ -157,15 +157,15 @@ __device__ void learned_halo(const GateParams& p, int n, int iy0, int ix0, int h
         if (VEC == kChunk) {
           float vt[kChunk], vp[kChunk];
           load_vec<T, kChunk>(xt, base + c0, vt);
-          if (!p.reference) load_vec<T, kChunk>(xp, base + c0, vp);
+          if (!p.no_prev) load_vec<T, kChunk>(xp, base + c0, vp);
 #pragma unroll
-          for (int j = 0; j < kChunk; ++j) r[j] = p.reference ? vt[j] : __fsub_rn(vt[j], vp[j]);
+          for (int j = 0; j < kChunk; ++j) r[j] = p.no_prev ? vt[j] : __fsub_rn(vt[j], vp[j]);
           if (own) copy_vec<T, kChunk>(keep, xt, base + c0);
         } else {
 #pragma unroll
           for (int j = 0; j < kChunk; ++j) {
             const float vt = j < nel ? Elem<T>::load1(xt, base + c0 + j) : 0.0f;
-            const float vp = (j < nel && !p.reference) ? Elem<T>::load1(xp, base + c0 + j) : 0.0f;
+            const float vp = (j < nel && !p.no_prev) ? Elem<T>::load1(xp, base + c0 + j) : 0.0f;
             r[j] = __fsub_rn(vt, vp);
             if (own && j < nel) keep[base + c0 + j] = xt[base + c0 + j];
           }
@@ -221,6 +221,40 @@ __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
   const int nblk_y = (oh + p.block - 1) / p.block, nblk_x = (ow + p.block - 1) / p.block;
   for (int i = threadIdx.x; i < kMaxTileBlocks; i += kGateThreads) blk_flag[i] = 0u;
 
+  if (p.up_mask) {
+    // chained input: the residual is zero outside the upstream layer's active
+    // blocks; a tile whose input region meets none of them has a zero statistic
+    // at every site (gate off) and skips its loads
+    const int y0 = max(iy0, 0), y1 = min(iy0 + hh, p.h), x0 = max(ix0, 0), x1 = min(ix0 + hw, p.w);
+    const int by0 = y0 / p.up_block, by1 = (y1 - 1) / p.up_block;
+    const int bx0 = x0 / p.up_block, bx1 = (x1 - 1) / p.up_block;
+    const int nbx = bx1 - bx0 + 1, cnt = (by1 - by0 + 1) * nbx;
+    int any = 0;
+    for (int i = threadIdx.x; i < cnt; i += kGateThreads) {
+      const int by = by0 + i / nbx, bx = bx0 + i % nbx;
+      any |= p.up_mask[((size_t)n * p.up_hb + by) * p.up_wb + bx] != 0;
+    }
+    if (!__syncthreads_or(any)) {
+      if (p.keep_stats)
+        for (int q = threadIdx.x; q < oh * ow; q += kGateThreads) {
+          const int ly = q / ow, lx = q - ly * ow;
+          const size_t o = ((size_t)n * p.h_out + oy0 + ly) * p.w_out + ox0 + lx;
+          p.stat[o] = 0.0f;
+          p.site_mask[o] = 0;
+        }
+      if (p.split_blocks) {
+        if (threadIdx.x == 0) p.tile_flags[tile] = 0;
+        return;
+      }
+      const int bi0 = oy0 / p.block, bj0 = ox0 / p.block;
+      for (int i = threadIdx.x; i < nblk_y * nblk_x; i += kGateThreads) {
+        const int by = i / nblk_x, bx = i - by * nblk_x;
+        p.block_mask[((size_t)n * p.hb + bi0 + by) * p.wb + bj0 + bx] = 0;
+      }
+      return;
+    }
+  }
+
   if constexpr (KL == 0) {
     halo_partials<T, VEC>(p, n, iy0, ix0, hh, hw, own_y0, own_y1, own_x0, own_x1, part);
     __syncthreads();
@@ -246,7 +280,7 @@ __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
     learned_halo<T, VEC, KL>(p, n, iy0, ix0, hh, hw, own_y0, own_y1, own_x0, own_x1, lds, phi);
   }
 
-  if (!p.copy_in_halo) {
+  if (!p.copy_in_halo && p.x_keep) {
     // x_{t-1} update for owned pixels no output support reaches
     const T* xt = static_cast<const T*>(p.x_t);
     T* keep = static_cast<T*>(p.x_keep);

@@ -26,6 +26,7 @@ struct GateParams {
   int rows_per_batch;           // unused (whole halo staged at once)
   int copy_in_halo;             // 1: every owned input pixel lies in its tile's halo
   int norm_p, support, reference, force_dense, keep_stats;
+  int no_prev;                  // x_{t-1} taken as 0 (reference frames; residual inputs)
   double thr;                   // eps^2 (p = 2) or eps (p = 1), exact in fp64
   double wnorm;                 // statistic factor: 1 (Input-Norm gate) or the weight norm (Output-Norm)
   uint8_t* block_mask;          // N x HB x WB
@@ -40,6 +41,10 @@ struct GateParams {
   const float* phi;
   float gate_bias;
   int phi_off;                  // LDS float offset of the staged phi, or -1: read phi from memory
+  // chained input (x_t is the upstream layer's residual): tiles whose input
+  // region holds no upstream active block skip their loads; NULL = no skip
+  const uint8_t* up_mask;
+  int up_block, up_hb, up_wb;
 };
 
 // Sparse convolution over the active sites (dense groups = 1).
@@ -55,7 +60,8 @@ struct ConvParams {
   int h_out, w_out, k, stride, pad, block, hb, wb;
   int ksteps;                   // K padded to the MFMA k-step, in steps
   int ntiles_n;                 // ceil(C_out / 16)
-  int reference;                // assign z instead of accumulating; x_{t-1} = 0
+  int reference;                // assign z instead of accumulating
+  int no_prev;                  // x_{t-1} taken as 0 (reference frames; residual inputs)
   int act;                      // 0 none, 1 identity, 2 relu
 };
 
@@ -102,6 +108,13 @@ hipError_t launch_conv(const ConvParams& p, int dtype, bool fast, int grid, hipS
 hipError_t launch_conv_halo(const ConvParams& p, const HaloParams& hp, int grid, hipStream_t st);
 int conv_halo_occupancy(const HaloParams& hp);  // resident workgroups per CU (0 on error)
 hipError_t launch_depthwise(const ConvParams& p, int dtype, int grid, hipStream_t st);
+
+// Residual emission of a layer that feeds a chained layer: at the blocks the
+// step updated, y = dtype(act(z)) and r = y_new - y_old (fp32, and its bf16
+// rounding for bf16 layers); at blocks updated by the previous step only, r = 0.
+hipError_t launch_emit(const uint8_t* block_mask, uint8_t* prev_mask, int nb, const float* z, void* y,
+                       float* r32, uint16_t* rb, int n, int hb, int wb, int block, int h_out, int w_out,
+                       int c_out, int act, int dtype, hipStream_t st);
 
 // One-time weight repacks (create time).
 hipError_t launch_pack_mfma(const void* w, void* out, int dtype, int c_out, int c_in, int k,

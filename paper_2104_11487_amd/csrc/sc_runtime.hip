@@ -54,7 +54,7 @@ struct Geometry {
   int vec;              // gate load width (elements)
   size_t elem;
   size_t off_wpack, off_slot0, off_slot1, off_z, off_y, off_bmask, off_tflag, off_list, off_ctr,
-      off_stat, off_smask, off_phi, total;
+      off_stat, off_smask, off_phi, off_r32, off_rb, off_prev, total;
   int learned;          // learned gate: its kernel size (the layer's k), else 0
   bool phi_in_lds;      // learned gate: phi staged in LDS (else read through the caches)
   int phi_off;          // learned gate: LDS float offset of the staged phi
@@ -102,7 +102,10 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
     return fail(err, SKIPCONV_E_INVALID_ARG, "unknown dtype");
   if (d->act_out < SKIPCONV_ACT_NONE || d->act_out > SKIPCONV_ACT_RELU)
     return fail(err, SKIPCONV_E_INVALID_ARG, "unknown act_out");
-  if (d->flags & ~(uint32_t)(SKIPCONV_FLAG_KEEP_STATS | SKIPCONV_FLAG_FORCE_DENSE | SKIPCONV_FLAG_SPLIT_PIPELINE))
+  if ((d->flags & SKIPCONV_FLAG_EMIT_RESIDUAL) && d->act_out == SKIPCONV_ACT_NONE)
+    return fail(err, SKIPCONV_E_INVALID_ARG, "EMIT_RESIDUAL needs an activation output");
+  if (d->flags & ~(uint32_t)(SKIPCONV_FLAG_KEEP_STATS | SKIPCONV_FLAG_FORCE_DENSE | SKIPCONV_FLAG_SPLIT_PIPELINE |
+                             SKIPCONV_FLAG_EMIT_RESIDUAL))
     return fail(err, SKIPCONV_E_INVALID_ARG, "unknown flag bits");
   if (std::isnan(d->eps) || d->eps < 0.0f) return fail(err, SKIPCONV_E_INVALID_ARG, "eps must be >= 0");
   if (!depthwise && d->c_out > kMaxCout) return fail(err, SKIPCONV_E_UNSUPPORTED, "c_out > 256");
@@ -314,6 +317,14 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
   }
   G.off_phi = off;
   if (G.learned) off = align_up(off + (size_t)k * k * d->c_in * 4);
+  G.off_r32 = G.off_rb = G.off_prev = off;
+  if (d->flags & SKIPCONV_FLAG_EMIT_RESIDUAL) {  // residual handed to a chained successor
+    off = align_up(off + (size_t)sites * d->c_out * 4);
+    G.off_rb = off;
+    if (d->dtype == SKIPCONV_BF16) off = align_up(off + (size_t)sites * d->c_out * 2);
+    G.off_prev = off;
+    off = align_up(off + (size_t)nb + 16);
+  }
   G.total = off;
   return SKIPCONV_OK;
 }
@@ -350,6 +361,10 @@ struct skipconv_layer {
   float* stat() { return reinterpret_cast<float*>(ws + g.off_stat); }
   uint8_t* smask() { return reinterpret_cast<uint8_t*>(ws + g.off_smask); }
   float* phi() { return reinterpret_cast<float*>(ws + g.off_phi); }
+  bool emits() const { return (d.flags & SKIPCONV_FLAG_EMIT_RESIDUAL) != 0; }
+  float* r32() { return reinterpret_cast<float*>(ws + g.off_r32); }
+  uint16_t* rb() { return reinterpret_cast<uint16_t*>(ws + g.off_rb); }
+  uint8_t* prev_mask() { return reinterpret_cast<uint8_t*>(ws + g.off_prev); }
   bool phi_set = false;      // learned gate: skipconv_set_gate_weights was called
   float gate_bias = 0.0f;
 };
@@ -375,7 +390,7 @@ sc::FusedParams fused_params(skipconv_layer* h, const void* x_t, bool ref) {
   fp.ntiles_n = g.ntn;
   fp.ksteps = g.ksteps;
   fp.csteps = d.c_in / 32;
-  fp.act = d.act_out;
+  fp.act = h->emits() ? 0 : d.act_out;  // an emitting layer writes y in the emit pass
   fp.kc = g.f_kc;
   fp.nchunks = g.f_nchunks;
   fp.nbuf = g.f_nbuf;
@@ -423,6 +438,13 @@ hipError_t weight_norm(skipconv_layer* h, const void* weights, hipStream_t st) {
   return hipSuccess;
 }
 
+hipError_t launch_emit(skipconv_layer* h, hipStream_t st) {
+  const Geometry& g = h->g;
+  return sc::launch_emit(h->bmask(), h->prev_mask(), g.nb, h->z(), h->y(), h->r32(), h->rb(), h->d.n, g.hb,
+                         g.wb, h->d.block, g.h_out, g.w_out, h->d.c_out, h->d.act_out,
+                         h->d.dtype == SKIPCONV_BF16 ? 1 : 0, st);
+}
+
 int hip_fail(skipconv_t h, hipError_t e, const char* what) {
   if (h) snprintf(h->last_error, sizeof(h->last_error), "%s: %s", what, hipGetErrorString(e));
   return SKIPCONV_E_HIP;
@@ -446,7 +468,7 @@ sc::GateParams gate_params(skipconv_layer* h, const void* x_t, bool ref) {
   gp.ts = g.ts; gp.tiles_y = g.tiles_y; gp.tiles_x = g.tiles_x;
   gp.halo_floats = g.halo_floats; gp.stage_stride = g.stage_stride;
   gp.rows_per_batch = g.rows_per_batch; gp.copy_in_halo = g.copy_in_halo;
-  gp.norm_p = d.norm_p; gp.support = d.support; gp.reference = ref ? 1 : 0;
+  gp.norm_p = d.norm_p; gp.support = d.support; gp.reference = ref ? 1 : 0; gp.no_prev = ref ? 1 : 0;
   gp.force_dense = (d.flags & SKIPCONV_FLAG_FORCE_DENSE) ? 1 : 0;
   gp.keep_stats = (d.flags & SKIPCONV_FLAG_KEEP_STATS) ? 1 : 0;
   gp.thr = threshold(d);
@@ -590,6 +612,9 @@ int skipconv_create(const skipconv_desc* d, const void* weights, void* workspace
   e = hipMemsetAsync(h->ctr(), 0, sc::kNumCounters * 4, st);
   if (e == hipSuccess) e = hipMemsetAsync(h->bmask(), 0, g.off_list - g.off_bmask, st);
   if (e == hipSuccess) e = hipMemsetAsync(h->list(), 0, (size_t)g.nb * 4, st);
+  if (e == hipSuccess && d->act_out != SKIPCONV_ACT_NONE)
+    e = hipMemsetAsync(h->y(), 0, (size_t)d->n * g.h_out * g.w_out * d->c_out * g.elem, st);
+  if (e == hipSuccess && h->emits()) e = hipMemsetAsync(h->r32(), 0, g.total - g.off_r32, st);
   if (e == hipSuccess) {
     if (g.depthwise)
       e = sc::launch_pack_depthwise(weights, static_cast<float*>(h->wpack()), d->dtype, d->c_in,
@@ -636,7 +661,8 @@ int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t
   cp.block = d.block; cp.hb = g.hb; cp.wb = g.wb;
   cp.ksteps = g.ksteps; cp.ntiles_n = g.ntn;
   cp.reference = ref ? 1 : 0;
-  cp.act = d.act_out;
+  cp.no_prev = ref ? 1 : 0;
+  cp.act = h->emits() ? 0 : d.act_out;
 
   const bool timing = h->timing_done < h->timing_frames && h->timing_seen % h->timing_every == 0;
   if (h->timing_frames) ++h->timing_seen;
@@ -666,12 +692,81 @@ int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t
     if (e != hipSuccess) return hip_fail(h, e, "conv launch");
     h->list_valid = true;
   }
+  if (h->emits()) {
+    e = launch_emit(h, st);
+    if (e != hipSuccess) return hip_fail(h, e, "emit launch");
+  }
   if (timing) {
     e = hipEventRecord(h->ev[3 * h->timing_done + 2], st);
     if (e != hipSuccess) return hip_fail(h, e, "event record");
     ++h->timing_done;
   }
   h->cur ^= 1;
+  h->ref_pending = false;
+  ++h->frames;
+  if (z_t) *z_t = h->z();
+  return SKIPCONV_OK;
+}
+
+int skipconv_step_chained(skipconv_t h, skipconv_t up, void* stream, const float** z_t) {
+  if (!h) return SKIPCONV_E_STATE;
+  if (!up || up == h) return fail(h->last_error, SKIPCONV_E_INVALID_ARG, "upstream handle is NULL or the layer itself");
+  if (!up->emits()) return fail(h->last_error, SKIPCONV_E_STATE, "the upstream layer does not emit its residual");
+  if (up->d.n != h->d.n || up->g.h_out != h->d.h || up->g.w_out != h->d.w || up->d.c_out != h->d.c_in ||
+      up->d.dtype != h->d.dtype)
+    return fail(h->last_error, SKIPCONV_E_INVALID_ARG, "upstream output does not match this layer's input");
+  if (up->frames == 0) return fail(h->last_error, SKIPCONV_E_STATE, "the upstream layer has not stepped yet");
+  if (h->g.learned && !h->phi_set)
+    return fail(h->last_error, SKIPCONV_E_STATE, "learned gate: call skipconv_set_gate_weights first");
+  // a reference frame reads the whole input: the upstream activation buffer
+  if (h->ref_pending) return skipconv_step(h, up->y(), stream, z_t);
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const skipconv_desc& d = h->d;
+  const Geometry& g = h->g;
+  const bool bf16 = d.dtype == SKIPCONV_BF16;
+  // gate on the upstream residual (fp32); no x_{t-1} slot is read or written
+  sc::GateParams gp = gate_params(h, up->r32(), false);
+  gp.x_prev = nullptr;
+  gp.x_keep = nullptr;
+  gp.no_prev = 1;
+  if (!g.learned) {  // a zero residual leaves a norm gate off: tiles without upstream blocks skip
+    gp.up_mask = up->bmask();
+    gp.up_block = up->d.block;
+    gp.up_hb = up->g.hb;
+    gp.up_wb = up->g.wb;
+  }
+  hipError_t e = sc::launch_gate(gp, SKIPCONV_F32, d.c_in % 8 == 0 ? 8 : 1, g.gate_grid, g.gate_lds, st);
+  if (e == hipSuccess) e = launch_compaction(h, st);
+  if (e != hipSuccess) return hip_fail(h, e, "chained gate launch");
+  // convolution of the residual operand (bf16-rounded for bf16 layers), accumulated into z
+  sc::ConvParams cp{};
+  cp.x_t = bf16 ? (const void*)up->rb() : (const void*)up->r32();
+  cp.x_prev = nullptr;
+  cp.wpack = h->wpack();
+  cp.z = h->z();
+  cp.y = h->y();
+  cp.list = h->list();
+  cp.counters = h->ctr();
+  cp.n = d.n; cp.h = d.h; cp.w = d.w; cp.c = d.c_in; cp.c_out = d.c_out;
+  cp.h_out = g.h_out; cp.w_out = g.w_out; cp.k = d.kernel; cp.stride = d.stride; cp.pad = g.pad;
+  cp.block = d.block; cp.hb = g.hb; cp.wb = g.wb;
+  cp.ksteps = g.ksteps; cp.ntiles_n = g.ntn;
+  cp.reference = 0;
+  cp.no_prev = 1;
+  cp.act = h->emits() ? 0 : d.act_out;
+  if (g.depthwise)
+    e = sc::launch_depthwise(cp, d.dtype, conv_grid(h), st);
+  else if (g.halo)
+    e = sc::launch_conv_halo(cp, g.hp, conv_grid(h), st);
+  else
+    e = sc::launch_conv(cp, d.dtype, g.fast, conv_grid(h), st);
+  if (e != hipSuccess) return hip_fail(h, e, "chained conv launch");
+  if (h->emits()) {
+    e = launch_emit(h, st);
+    if (e != hipSuccess) return hip_fail(h, e, "emit launch");
+  }
+  h->list_valid = true;
   h->ref_pending = false;
   ++h->frames;
   if (z_t) *z_t = h->z();

@@ -29,6 +29,7 @@ SKIPCONV_SUPPORT_RF, SKIPCONV_SUPPORT_CENTRE = 0, 1
 SKIPCONV_GATE_INPUT_NORM, SKIPCONV_GATE_OUTPUT_NORM, SKIPCONV_GATE_LEARNED = 0, 1, 2
 SKIPCONV_ACT_NONE, SKIPCONV_ACT_IDENTITY, SKIPCONV_ACT_RELU = 0, 1, 2
 SKIPCONV_FLAG_KEEP_STATS, SKIPCONV_FLAG_FORCE_DENSE, SKIPCONV_FLAG_SPLIT_PIPELINE = 1, 2, 4
+SKIPCONV_FLAG_EMIT_RESIDUAL = 8
 
 
 class skipconv_desc(ctypes.Structure):
@@ -56,6 +57,7 @@ _SIGS = {
     "skipconv_workspace_size": (ctypes.c_int, [_D, ctypes.POINTER(ctypes.c_size_t)]),
     "skipconv_create": (ctypes.c_int, [_D, _P, _P, ctypes.c_size_t, _P, ctypes.POINTER(_P)]),
     "skipconv_step": (ctypes.c_int, [_P, _P, _P, ctypes.POINTER(_P)]),
+    "skipconv_step_chained": (ctypes.c_int, [_P, _P, _P, ctypes.POINTER(_P)]),
     "skipconv_reset": (ctypes.c_int, [_P]),
     "skipconv_set_eps": (ctypes.c_int, [_P, ctypes.c_float]),
     "skipconv_set_gate_weights": (ctypes.c_int, [_P, _P, ctypes.c_float, _P]),
@@ -143,6 +145,12 @@ def skipconv_create(d: skipconv_desc, weights_ptr: int, workspace_ptr: Optional[
 def skipconv_step(h: int, x_ptr: int, stream: int) -> int:
     z = ctypes.c_void_p()
     _check(lib().skipconv_step(h, x_ptr, stream, ctypes.byref(z)), h)
+    return z.value
+
+
+def skipconv_step_chained(h: int, up: int, stream: int) -> int:
+    z = ctypes.c_void_p()
+    _check(lib().skipconv_step_chained(h, up, stream, ctypes.byref(z)), h)
     return z.value
 
 
@@ -252,7 +260,7 @@ _GATE = {"input": SKIPCONV_GATE_INPUT_NORM, "output": SKIPCONV_GATE_OUTPUT_NORM,
 
 def make_desc(*, n, h, w, c_in, c_out, kernel, stride=1, pad=-1, groups=1, block=1, norm_p=2,
               support="rf", dtype="f32", act_out="none", eps=0.0, keep_stats=False,
-              force_dense=False, split=False, gate="input") -> skipconv_desc:
+              force_dense=False, split=False, gate="input", emit_residual=False) -> skipconv_desc:
     d = skipconv_desc_init()
     d.n, d.h, d.w, d.c_in, d.c_out = n, h, w, c_in, c_out
     d.kernel, d.stride, d.pad, d.groups, d.block = kernel, stride, pad, groups, block
@@ -260,7 +268,8 @@ def make_desc(*, n, h, w, c_in, c_out, kernel, stride=1, pad=-1, groups=1, block
     d.dtype = SKIPCONV_BF16 if dtype == "bf16" else SKIPCONV_F32
     d.act_out = _ACT[act_out]
     d.flags = ((SKIPCONV_FLAG_KEEP_STATS if keep_stats else 0) | (SKIPCONV_FLAG_FORCE_DENSE if force_dense else 0)
-               | (SKIPCONV_FLAG_SPLIT_PIPELINE if split else 0))
+               | (SKIPCONV_FLAG_SPLIT_PIPELINE if split else 0)
+               | (SKIPCONV_FLAG_EMIT_RESIDUAL if emit_residual else 0))
     d.eps = eps
     d.gate = _GATE[gate]
     return d
@@ -278,7 +287,8 @@ class SkipConv:
     def __init__(self, weight, *, n: int, h: int, w: int, stride: int = 1, pad: int = -1,
                  groups: int = 1, eps: float = 0.0, block: int = 1, norm_p: int = 2,
                  support: str = "rf", act_out: str = "none", keep_stats: bool = False,
-                 force_dense: bool = False, split: bool = False, gate: str = "input", stream=None):
+                 force_dense: bool = False, split: bool = False, gate: str = "input",
+                 emit_residual: bool = False, stream=None):
         import torch
 
         if not weight.is_cuda:
@@ -292,7 +302,7 @@ class SkipConv:
         self.desc = make_desc(n=n, h=h, w=w, c_in=cg * groups, c_out=c_out, kernel=k, stride=stride,
                               pad=pad, groups=groups, block=block, norm_p=norm_p, support=support,
                               dtype=self.dtype, act_out=act_out, eps=eps, keep_stats=keep_stats, gate=gate,
-                              force_dense=force_dense, split=split)
+                              force_dense=force_dense, split=split, emit_residual=emit_residual)
         self.h_out, self.w_out, self.hb, self.wb = skipconv_out_shape(self.desc)
         nbytes = skipconv_workspace_size(self.desc)
         self.device = weight.device
@@ -324,6 +334,18 @@ class SkipConv:
                 or x.device != self.device:
             raise ValueError(f"x must be a contiguous {self.tdtype} tensor of shape {self.shape_in} on {self.device}")
         zp = skipconv_step(self.handle, x.data_ptr(), self._stream())
+        if self._z is None:
+            self._z = self._view(zp, self.desc.n * self.h_out * self.w_out * self.desc.c_out,
+                                 self.torch.float32)
+        return self._z
+
+    def step_chained(self, upstream: "SkipConv"):
+        """One frame whose input is `upstream`'s activation output (upstream stepped first).
+
+        `upstream` must have been created with emit_residual=True; see
+        skipconv_step_chained for the contract.
+        """
+        zp = skipconv_step_chained(self.handle, upstream.handle, self._stream())
         if self._z is None:
             self._z = self._view(zp, self.desc.n * self.h_out * self.w_out * self.desc.c_out,
                                  self.torch.float32)

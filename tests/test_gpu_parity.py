@@ -545,3 +545,123 @@ def test_learned_gate_requires_weights_and_nan_turns_on():
     phi = np.full((16, 3, 3), -1.0, np.float32)  # strongly negative scores: off unless NaN
     run_single(frames, w, dtype="f32", eps=0.0, block=1, gate="learned", phi=phi, gate_bias=-1.0,
                tag="learned NaN")
+
+
+# ------------------------------------- sparse residual propagation (chained) --
+
+def run_chain_propagated(frames, weights, specs, *, dtype, act, epss, block, tag, resets=()):
+    """Layers 2.. step on the previous layer's emitted residual (skipconv_step_chained).
+
+    Checked per layer and frame against (a) the oracle fed the GPU's own layer
+    input (masks bit-exact, z within tolerance) and (b) the same stack stepped
+    with full frames through the split pipeline: masks, lists and z bit-exact.
+    """
+    n, h, w, _ = frames[0].shape
+    chained, plain, orcs = [], [], []
+    hh, ww = h, w
+    for i, (wt, sp) in enumerate(zip(weights, specs)):
+        last = i == len(weights) - 1
+        a = "none" if last else act
+        lay, orc = _layer_pair(wt, n=n, h=hh, w=ww, dtype=dtype, eps=epss[i], block=block,
+                               stride=sp.stride, groups=sp.groups, act_out=a, split=True)
+        lay.close()
+        ws = weight_storage(wt, dtype)
+        kw = dict(n=n, h=hh, w=ww, stride=sp.stride, groups=sp.groups, eps=epss[i], block=block,
+                  keep_stats=True, act_out=a, split=True)
+        chained.append(S.SkipConv(to_device(ws, dtype), emit_residual=not last, **kw))
+        plain.append(S.SkipConv(to_device(ws, dtype), **kw))
+        orcs.append(orc)
+        hh, ww = chained[-1].h_out, chained[-1].w_out
+    skipped = 0
+    for t, f in enumerate(frames):
+        for i in resets.get(t, ()) if isinstance(resets, dict) else ():
+            chained[i].reset()
+            plain[i].reset()
+            orcs[i].reset()
+        x_dev = to_device(syn.to_storage(f, dtype), dtype)
+        x_host = syn.to_storage(f, dtype)
+        for i in range(len(chained)):
+            say(f"[{tag}] frame {t} layer {i}")
+            if i == 0:
+                chained[0].step(x_dev)
+            else:
+                chained[i].step_chained(chained[i - 1])
+            plain[i].step(x_dev)
+            ref = orcs[i].step(x_host)
+            compare_frame(chained[i], ref, dtype, t=t, tag=f"{tag} L{i}", keep_stats=True)
+            torch.cuda.synchronize()
+            assert np.array_equal(chained[i].block_mask(), plain[i].block_mask()), f"{tag} L{i} t={t}"
+            assert np.array_equal(chained[i].active_list(), plain[i].active_list()), f"{tag} L{i} t={t}"
+            assert torch.equal(chained[i]._z, plain[i]._z), f"{tag} L{i} t={t}: z differs"
+            if i + 1 < len(chained):
+                ya, yb = chained[i].activation(), plain[i].activation()
+                torch.cuda.synchronize()
+                assert torch.equal(ya.view(torch.int16) if dtype == "bf16" else ya,
+                                   yb.view(torch.int16) if dtype == "bf16" else yb), f"{tag} L{i}: activation"
+                x_dev = yb
+                x_host = to_host_storage(yb, dtype)
+            if i > 0 and t > 0 and ref["count"] == 0:
+                skipped += 1
+    for lay in chained + plain:
+        lay.close()
+    return skipped
+
+
+def test_stack6_propagated_residuals():
+    wl = syn.workloads()["stack6"]
+    frames = list(wl.video(6))
+    sched = syn.eps_schedule(6) * 0.5
+    run_chain_propagated(frames, wl.weights(), wl.layers, dtype="bf16", act="relu", epss=list(sched), block=1,
+                         tag="stack6 chained", resets={4: (2,)})
+
+
+def test_mbconv192_propagated_residuals():
+    wl = syn.workloads()["mbconv192"]
+    frames = list(wl.video(8))
+    run_chain_propagated(frames, wl.weights(), wl.layers, dtype="bf16", act="identity", epss=[2.0, 1.5],
+                         block=8, tag="mbconv192 chained", resets={5: (0,)})
+
+
+@pytest.mark.parametrize("dtype,block", [("f32", 1), ("bf16", 4), ("bf16", 16)])
+def test_chain_two_layers_sparse_motion(dtype, block):
+    """A small moving patch: most gate tiles of the second layer see no upstream block and skip."""
+    rng = np.random.Generator(np.random.PCG64(97))
+    c0, c1, c2 = 16, 32, 32
+    w1 = rng.normal(0, 0.3, (c1, c0, 3, 3)).astype(np.float32)
+    w2 = rng.normal(0, 0.2, (c2, c1, 3, 3)).astype(np.float32)
+    x = rng.random((2, 64, 48, c0), dtype=np.float32)
+    frames = [x]
+    for t in range(5):
+        x = x.copy()
+        x[:, 10 + 3 * t:16 + 3 * t, 5 + 2 * t:12 + 2 * t] = rng.random((2, 6, 7, c0), dtype=np.float32)
+        frames.append(x)
+    Spec = type("Spec", (), {})
+    specs = []
+    for _ in range(2):
+        sp = Spec()
+        sp.stride, sp.groups = 1, 1
+        specs.append(sp)
+    run_chain_propagated(frames, [w1, w2], specs, dtype=dtype, act="relu", epss=[0.3, 0.3], block=block,
+                         tag=f"chain2 {dtype} b={block}", resets={3: (1,)})
+
+
+def test_chained_step_contract_errors():
+    rng = np.random.Generator(np.random.PCG64(98))
+    w = rng.normal(0, 0.3, (16, 16, 3, 3)).astype(np.float32)
+    wd = to_device(w, "f32")
+    up_plain = S.SkipConv(wd, n=1, h=16, w=16, act_out="relu")
+    up = S.SkipConv(wd, n=1, h=16, w=16, act_out="relu", emit_residual=True)
+    down = S.SkipConv(wd, n=1, h=16, w=16)
+    wrong = S.SkipConv(to_device(rng.normal(0, 0.3, (16, 16, 3, 3)).astype(np.float32), "f32"), n=1, h=8, w=16)
+    for upstream, code in ((up_plain, S.SKIPCONV_E_STATE), (up, S.SKIPCONV_E_STATE)):
+        with pytest.raises(S.SkipConvError) as ei:
+            down.step_chained(upstream)  # not emitting / not stepped yet
+        assert ei.value.code == code
+    up.step(to_device(rng.random((1, 16, 16, 16), dtype=np.float32), "f32"))
+    with pytest.raises(S.SkipConvError) as ei:
+        wrong.step_chained(up)
+    assert ei.value.code == S.SKIPCONV_E_INVALID_ARG
+    with pytest.raises(S.SkipConvError):
+        S.SkipConv(wd, n=1, h=16, w=16, emit_residual=True)  # no activation output to difference
+    for lay in (up_plain, up, down, wrong):
+        lay.close()
