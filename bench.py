@@ -396,6 +396,120 @@ def summarize_trace(db: str, out_md: str, command: str) -> None:
     print("\n".join(lines))
 
 
+# ----------------------------------------------------------------- stacks --
+
+def bench_stack(args):
+    """Six stacked 3x3 layers (3-32-64-64-128-128-128 channels, strides 1/2, ReLU,
+    per-site gates, 256 x 192 bf16 frames): one step = all six layers on one frame.
+
+    The layer thresholds are eps0 * a fixed per-layer schedule, eps0 bisected on
+    the GPU for a MAC-weighted density near --density. Two variants run the same
+    frames: 'full' (each layer reads its whole input frame, x_t and x_{t-1}) and
+    'chained' (layers 2..6 step on the previous layer's emitted residual).
+    """
+    import torch
+    from paper_2104_11487_amd import synthetic as syn
+    from paper_2104_11487_amd.skipconv import SkipConv
+
+    wl, clip = load_workload("stack6", args.frames)
+    frames_dev = upload(clip, wl.dtype)
+    wts = [weight_tensor(w, wl.dtype) for w in wl.weights()]
+    sched = syn.eps_schedule(len(wl.layers))
+
+    def build(eps0, chained):
+        lays, h, w = [], wl.h, wl.w
+        for i, sp in enumerate(wl.layers):
+            last = i == len(wl.layers) - 1
+            lay = SkipConv(wts[i], n=wl.n, h=h, w=w, stride=sp.stride, groups=sp.groups,
+                           eps=float(eps0 * sched[i]), block=wl.block, act_out="none" if last else "relu",
+                           emit_residual=chained and not last)
+            lays.append(lay)
+            h, w = lay.h_out, lay.w_out
+        return lays
+
+    def step(lays, x, chained):
+        lays[0].step(x)
+        for i in range(1, len(lays)):
+            if chained:
+                lays[i].step_chained(lays[i - 1])
+            else:
+                lays[i].step(lays[i - 1].activation())
+
+    def density(eps0):
+        lays = build(eps0, False)
+        act = dense = 0
+        for t, x in enumerate(frames_dev):
+            if t == 0:
+                for l in lays:
+                    l.reset()
+            step(lays, x, False)
+            if t > 0:
+                for l in lays:
+                    a, d = S_frame_macs(l)
+                    act += a
+                    dense += d
+        for l in lays:
+            l.close()
+        return act / max(dense, 1)
+
+    def S_frame_macs(l):
+        from paper_2104_11487_amd import skipconv as S
+        dense, active = S.skipconv_frame_macs(l.handle, l._stream())
+        return active, dense
+
+    lo, hi = 0.0, 8.0
+    for _ in range(14):
+        mid = 0.5 * (lo + hi)
+        if density(mid) > args.density:
+            lo = mid
+        else:
+            hi = mid
+    eps0 = 0.5 * (lo + hi)
+    d_mac = density(eps0)
+    log(f"[bench] stack6: eps0 {eps0:.4g}, MAC-weighted density {d_mac:.3f}")
+
+    nfr = len(frames_dev)
+    res = {}
+    for chained in (False, True):
+        lays = build(eps0, chained)
+        for _ in range(max(1, args.warmup // nfr)):
+            for t, x in enumerate(frames_dev):
+                if t == 0:
+                    for l in lays:
+                        l.reset()
+                step(lays, x, chained)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for j in range(args.steps):
+            if j % nfr == 0:
+                for l in lays:
+                    l.reset()
+            step(lays, frames_dev[j % nfr], chained)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        for l in lays:
+            l.close()
+        res["chained" if chained else "full"] = wall
+        log(f"[bench] stack6 {'chained' if chained else 'full'}: {args.steps / wall:.0f} frames/s, "
+            f"{1e6 * wall / args.steps:.1f} us/step")
+    # algorithmic bytes of the full-frame formulation: per layer 3|x| (x_t, x_{t-1}
+    # read, x_t kept) + 2 d |z| + activation writes; reported against the chained step
+    wall = res["chained"]
+    out = {
+        "metric": METRIC, "value": args.steps / wall, "unit": "frames/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": 1e3 * wall / args.steps, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic",
+        "config": {"workload": "stack6: six 3x3 layers 3-32-64-64-128-128-128, strides 1,2,1,2,1,1, ReLU, "
+                               f"256x192 frames, batch 1, {nfr}-frame clip (reset at frame 1), per-site gates, "
+                               "layers 2-6 chained on emitted residuals",
+                   "eps0": eps0, "mac_density": d_mac,
+                   "full_frames_per_s": args.steps / res["full"], "chained_frames_per_s": args.steps / wall,
+                   "speedup_chained": res["full"] / wall},
+        "roofline": None, "cpu_baseline": None, "sweep": [],
+    }
+    print(json.dumps(out), flush=True)
+
+
 # -------------------------------------------------------------------- main --
 
 def main():
@@ -403,7 +517,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=640)
     ap.add_argument("--warmup", type=int, default=64)
-    ap.add_argument("--workload", default="rect64", choices=["rect64", "blob128", "square16"])
+    ap.add_argument("--workload", default="rect64", choices=["rect64", "blob128", "square16", "stack6"])
     ap.add_argument("--block", type=int, default=None)
     ap.add_argument("--density", type=float, default=0.25)
     ap.add_argument("--frames", type=int, default=None)
@@ -439,6 +553,9 @@ def main():
 
     S.lib()  # fail loudly if the HIP library is missing
     torch.cuda.set_device(0)
+    if args.workload == "stack6":
+        bench_stack(args)
+        return
     wl, clip = load_workload(args.workload, args.frames)
     frames_dev = upload(clip, wl.dtype)
     w32 = wl.weights()[0]

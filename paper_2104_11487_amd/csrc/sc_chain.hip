@@ -18,23 +18,37 @@ namespace sc {
 namespace {
 
 constexpr int kEmitThreads = 256;
+constexpr int kEmitSites = 64;  // output sites (whole blocks) per workgroup, at least one block
 
+// Workgroup w takes blocks [w * bpw, (w + 1) * bpw) of the flattened block grid
+// (bpw = max(1, kEmitSites / b^2)); each thread walks (site, channel) elements.
 __global__ void __launch_bounds__(kEmitThreads)
-emit_kernel(const uint8_t* block_mask, uint8_t* prev_mask, const float* z, void* y, float* r32,
-            uint16_t* rb, int hb, int wb, int block, int h_out, int w_out, int c_out, int act, int dtype) {
-  const int blk = blockIdx.x;
-  const bool cur = block_mask[blk] != 0, was = prev_mask[blk] != 0;
-  if (!cur && !was) return;
-  const int img = blk / (hb * wb), rem = blk - img * hb * wb;
-  const int bi = rem / wb, bj = rem - bi * wb;
-  const int oy0 = bi * block, ox0 = bj * block;
-  const int bh = min(block, h_out - oy0), bw = min(block, w_out - ox0);
-  const int total = bh * bw * c_out;
-  for (int i = threadIdx.x; i < total; i += kEmitThreads) {
-    const int site = i / c_out, ch = i - site * c_out;
-    const int ly = site / bw, lx = site - ly * bw;
-    const size_t o = ((size_t)(img * h_out + oy0 + ly) * w_out + ox0 + lx) * c_out + ch;
-    if (!cur) {
+emit_kernel(const uint8_t* block_mask, uint8_t* prev_mask, int nb, int bpw, const float* z, void* y,
+            float* r32, uint16_t* rb, int hb, int wb, int block, int h_out, int w_out, int c_out, int act,
+            int dtype) {
+  __shared__ uint8_t state[kEmitSites];  // bit 0: updated now, bit 1: updated by the previous step
+  const int b0 = blockIdx.x * bpw, nblk = min(bpw, nb - b0);
+  int any = 0;
+  for (int i = threadIdx.x; i < nblk; i += kEmitThreads) {
+    const uint8_t st = (block_mask[b0 + i] ? 1 : 0) | (prev_mask[b0 + i] ? 2 : 0);
+    state[i] = st;
+    any |= st;
+  }
+  if (!__syncthreads_or(any)) return;
+  const int bsz = block * block;
+  const int total = nblk * bsz * c_out;
+  for (int e = threadIdx.x; e < total; e += kEmitThreads) {
+    const int bl = e / (bsz * c_out), rem0 = e - bl * bsz * c_out;
+    const uint8_t st = state[bl];
+    if (!st) continue;
+    const int site = rem0 / c_out, ch = rem0 - site * c_out;
+    const int blk = b0 + bl;
+    const int img = blk / (hb * wb), rem = blk - img * hb * wb;
+    const int bi = rem / wb, bj = rem - bi * wb;
+    const int oy = bi * block + site / block, ox = bj * block + site % block;
+    if (oy >= h_out || ox >= w_out) continue;  // ceil-mode edge block
+    const size_t o = ((size_t)(img * h_out + oy) * w_out + ox) * c_out + ch;
+    if (!(st & 1)) {
       r32[o] = 0.0f;
       if (dtype == 1) rb[o] = 0;
       continue;
@@ -56,7 +70,7 @@ emit_kernel(const uint8_t* block_mask, uint8_t* prev_mask, const float* z, void*
     r32[o] = r;
   }
   __syncthreads();
-  if (threadIdx.x == 0) prev_mask[blk] = cur ? 1 : 0;
+  for (int i = threadIdx.x; i < nblk; i += kEmitThreads) prev_mask[b0 + i] = state[i] & 1;
 }
 
 }  // namespace
@@ -65,8 +79,10 @@ hipError_t launch_emit(const uint8_t* block_mask, uint8_t* prev_mask, int nb, co
                        float* r32, uint16_t* rb, int n, int hb, int wb, int block, int h_out, int w_out,
                        int c_out, int act, int dtype, hipStream_t st) {
   (void)n;
-  hipLaunchKernelGGL(emit_kernel, dim3(nb), dim3(kEmitThreads), 0, st, block_mask, prev_mask, z, y, r32, rb,
-                     hb, wb, block, h_out, w_out, c_out, act, dtype);
+  const int bpw = max(1, kEmitSites / (block * block));
+  const int grid = (nb + bpw - 1) / bpw;
+  hipLaunchKernelGGL(emit_kernel, dim3(grid), dim3(kEmitThreads), 0, st, block_mask, prev_mask, nb, bpw, z, y,
+                     r32, rb, hb, wb, block, h_out, w_out, c_out, act, dtype);
   return hipGetLastError();
 }
 

@@ -111,6 +111,37 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
   const int tb_w = g.ts / g.block;
   const int npix = hh * hw;
 
+  if (g.up_mask) {
+    // chained input: the residual is zero outside the upstream layer's active
+    // blocks; a tile whose input region meets none of them has every gate off
+    // and stops here, before any load (norm gates only)
+    const int y0 = max(iy0, 0), y1 = min(iy0 + hh, g.h), x0 = max(ix0, 0), x1 = min(ix0 + hw, g.w);
+    const int by0 = y0 / g.up_block, by1 = (y1 - 1) / g.up_block;
+    const int bx0 = x0 / g.up_block, bx1 = (x1 - 1) / g.up_block;
+    const int nbx = bx1 - bx0 + 1, cnt = (by1 - by0 + 1) * nbx;
+    int any = 0;
+    for (int i = threadIdx.x; i < cnt; i += kThreads) {
+      const int by = by0 + i / nbx, bx = bx0 + i % nbx;
+      any |= g.up_mask[((size_t)n * g.up_hb + by) * g.up_wb + bx] != 0;
+    }
+    if (!__syncthreads_or(any)) {
+      if (g.keep_stats)
+        for (int q = threadIdx.x; q < oh * ow; q += kThreads) {
+          const int ly = q / ow, lx = q - ly * ow;
+          const size_t o = ((size_t)n * g.h_out + oy0 + ly) * g.w_out + ox0 + lx;
+          g.stat[o] = 0.0f;
+          g.site_mask[o] = 0;
+        }
+      const int nby = (oh + g.block - 1) / g.block, nbx2 = (ow + g.block - 1) / g.block;
+      const int bi0 = oy0 / g.block, bj0 = ox0 / g.block;
+      for (int i = threadIdx.x; i < nby * nbx2; i += kThreads) {
+        const int by = i / nbx2, bx = i - by * nbx2;
+        g.block_mask[((size_t)n * g.hb + bi0 + by) * g.wb + bj0 + bx] = 0;
+      }
+      return;
+    }
+  }
+
   // 1. weights: the waves past the first few issue the first chunk; the
   // barriers up to the product wait on LDS traffic only
   const int bw0 = min(kWaves - 1, 2);
@@ -171,13 +202,19 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
       const int hy = px[u] / hw, hx = px[u] - hy * hw;
       const int y = iy0 + hy, x = ix0 + hx;
       in[u] = px[u] >= 0 && y >= 0 && y < g.h && x >= 0 && x < g.w;
-      own[u] = in[u] && g.copy_in_halo && y >= own_y0 && y < own_y1 && x >= own_x0 && x < own_x1;
+      own[u] = in[u] && keep && g.copy_in_halo && y >= own_y0 && y < own_y1 && x >= own_x0 && x < own_x1;
       off[u] = in[u] ? ((size_t)(n * g.h + y) * g.w + x) * c + ch[u] * 8 : 0;
       vt[u] = uint4{0u, 0u, 0u, 0u};
       vp[u] = uint4{0u, 0u, 0u, 0u};
       if (in[u]) {
-        vt[u] = *reinterpret_cast<const uint4*>(xt + off[u]);
-        if (!g.reference) vp[u] = *reinterpret_cast<const uint4*>(xp + off[u]);
+        if (g.rin) {  // fp32 residual input: channels 0-3 in vt, 4-7 in vp
+          const float* rr = static_cast<const float*>(g.x_t) + off[u];
+          vt[u] = *reinterpret_cast<const uint4*>(rr);
+          vp[u] = *reinterpret_cast<const uint4*>(rr + 4);
+        } else {
+          vt[u] = *reinterpret_cast<const uint4*>(xt + off[u]);
+          if (!g.no_prev) vp[u] = *reinterpret_cast<const uint4*>(xp + off[u]);
+        }
       }
     }
 #pragma unroll
@@ -190,8 +227,15 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         // channels 2e (low half) and 2e + 1 (high half)
-        const float r0 = __fsub_rn(__uint_as_float(wt[e] << 16), __uint_as_float(wpv[e] << 16));
-        const float r1 = __fsub_rn(__uint_as_float(wt[e] & 0xffff0000u), __uint_as_float(wpv[e] & 0xffff0000u));
+        float r0, r1;
+        if (g.rin) {
+          const uint32_t* src = e < 2 ? wt : wpv;
+          r0 = __uint_as_float(src[(2 * e) & 3]);
+          r1 = __uint_as_float(src[(2 * e + 1) & 3]);
+        } else {
+          r0 = __fsub_rn(__uint_as_float(wt[e] << 16), __uint_as_float(wpv[e] << 16));
+          r1 = __fsub_rn(__uint_as_float(wt[e] & 0xffff0000u), __uint_as_float(wpv[e] & 0xffff0000u));
+        }
         sum = add_rn(sum, term(r0, g.norm_p));
         sum = add_rn(sum, term(r1, g.norm_p));
         outw[e] = pack_bf16(r0, r1);
@@ -203,7 +247,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
       if (own[u]) *reinterpret_cast<uint4*>(keep + off[u]) = vt[u];
     }
   }
-  if (!g.copy_in_halo) {
+  if (!g.copy_in_halo && keep) {
     const int ny = own_y1 - own_y0, nx = own_x1 - own_x0;
     const int per_row = nx * c;
     for (int i = threadIdx.x; i < ny * per_row; i += kThreads) {

@@ -45,6 +45,7 @@ struct GateParams {
   // region holds no upstream active block skip their loads; NULL = no skip
   const uint8_t* up_mask;
   int up_block, up_hb, up_wb;
+  int rin;                      // fused kernel: x_t is an fp32 residual (no x_{t-1})
 };
 
 // Sparse convolution over the active sites (dense groups = 1).

@@ -725,6 +725,28 @@ int skipconv_step_chained(skipconv_t h, skipconv_t up, void* stream, const float
   const skipconv_desc& d = h->d;
   const Geometry& g = h->g;
   const bool bf16 = d.dtype == SKIPCONV_BF16;
+  if (g.fused) {
+    // one-pass kernel on the fp32 residual (it rounds the operand itself)
+    sc::FusedParams fp = fused_params(h, up->r32(), false);
+    fp.g.x_prev = nullptr;
+    fp.g.x_keep = nullptr;
+    fp.g.no_prev = 1;
+    fp.g.rin = 1;
+    if (!g.learned) {
+      fp.g.up_mask = up->bmask();
+      fp.g.up_block = up->d.block;
+      fp.g.up_hb = up->g.hb;
+      fp.g.up_wb = up->g.wb;
+    }
+    hipError_t e = sc::launch_fused(fp, g.f_grid, st);
+    if (e == hipSuccess && h->emits()) e = launch_emit(h, st);
+    if (e != hipSuccess) return hip_fail(h, e, "chained fused launch");
+    h->list_valid = false;
+    h->ref_pending = false;
+    ++h->frames;
+    if (z_t) *z_t = h->z();
+    return SKIPCONV_OK;
+  }
   // gate on the upstream residual (fp32); no x_{t-1} slot is read or written
   sc::GateParams gp = gate_params(h, up->r32(), false);
   gp.x_prev = nullptr;

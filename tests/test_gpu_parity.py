@@ -549,7 +549,7 @@ def test_learned_gate_requires_weights_and_nan_turns_on():
 
 # ------------------------------------- sparse residual propagation (chained) --
 
-def run_chain_propagated(frames, weights, specs, *, dtype, act, epss, block, tag, resets=()):
+def run_chain_propagated(frames, weights, specs, *, dtype, act, epss, block, tag, resets=(), split=True):
     """Layers 2.. step on the previous layer's emitted residual (skipconv_step_chained).
 
     Checked per layer and frame against (a) the oracle fed the GPU's own layer
@@ -567,7 +567,7 @@ def run_chain_propagated(frames, weights, specs, *, dtype, act, epss, block, tag
         lay.close()
         ws = weight_storage(wt, dtype)
         kw = dict(n=n, h=hh, w=ww, stride=sp.stride, groups=sp.groups, eps=epss[i], block=block,
-                  keep_stats=True, act_out=a, split=True)
+                  keep_stats=True, act_out=a, split=split)
         chained.append(S.SkipConv(to_device(ws, dtype), emit_residual=not last, **kw))
         plain.append(S.SkipConv(to_device(ws, dtype), **kw))
         orcs.append(orc)
@@ -607,23 +607,26 @@ def run_chain_propagated(frames, weights, specs, *, dtype, act, epss, block, tag
     return skipped
 
 
-def test_stack6_propagated_residuals():
+@PIPE
+def test_stack6_propagated_residuals(split):
     wl = syn.workloads()["stack6"]
     frames = list(wl.video(6))
     sched = syn.eps_schedule(6) * 0.5
     run_chain_propagated(frames, wl.weights(), wl.layers, dtype="bf16", act="relu", epss=list(sched), block=1,
-                         tag="stack6 chained", resets={4: (2,)})
+                         tag=f"stack6 chained split={split}", resets={4: (2,)}, split=split)
 
 
-def test_mbconv192_propagated_residuals():
+@PIPE
+def test_mbconv192_propagated_residuals(split):
     wl = syn.workloads()["mbconv192"]
     frames = list(wl.video(8))
     run_chain_propagated(frames, wl.weights(), wl.layers, dtype="bf16", act="identity", epss=[2.0, 1.5],
-                         block=8, tag="mbconv192 chained", resets={5: (0,)})
+                         block=8, tag=f"mbconv192 chained split={split}", resets={5: (0,)}, split=split)
 
 
+@PIPE
 @pytest.mark.parametrize("dtype,block", [("f32", 1), ("bf16", 4), ("bf16", 16)])
-def test_chain_two_layers_sparse_motion(dtype, block):
+def test_chain_two_layers_sparse_motion(dtype, block, split):
     """A small moving patch: most gate tiles of the second layer see no upstream block and skip."""
     rng = np.random.Generator(np.random.PCG64(97))
     c0, c1, c2 = 16, 32, 32
@@ -642,7 +645,7 @@ def test_chain_two_layers_sparse_motion(dtype, block):
         sp.stride, sp.groups = 1, 1
         specs.append(sp)
     run_chain_propagated(frames, [w1, w2], specs, dtype=dtype, act="relu", epss=[0.3, 0.3], block=block,
-                         tag=f"chain2 {dtype} b={block}", resets={3: (1,)})
+                         tag=f"chain2 {dtype} b={block} split={split}", resets={3: (1,)}, split=split)
 
 
 def test_chained_step_contract_errors():
