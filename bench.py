@@ -469,11 +469,11 @@ def bench_stack(args):
     log(f"[bench] stack6: eps0 {eps0:.4g}, MAC-weighted density {d_mac:.3f}")
 
     nfr = len(frames_dev)
-    res = {}
-    for chained in (False, True):
+
+    def timed(frames, chained):
         lays = build(eps0, chained)
         for _ in range(max(1, args.warmup // nfr)):
-            for t, x in enumerate(frames_dev):
+            for t, x in enumerate(frames):
                 if t == 0:
                     for l in lays:
                         l.reset()
@@ -484,14 +484,30 @@ def bench_stack(args):
             if j % nfr == 0:
                 for l in lays:
                     l.reset()
-            step(lays, frames_dev[j % nfr], chained)
+            step(lays, frames[j % nfr], chained)
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
         for l in lays:
             l.close()
-        res["chained" if chained else "full"] = wall
+        return wall
+
+    res = {}
+    for chained in (False, True):
+        res["chained" if chained else "full"] = wall = timed(frames_dev, chained)
         log(f"[bench] stack6 {'chained' if chained else 'full'}: {args.steps / wall:.0f} frames/s, "
             f"{1e6 * wall / args.steps:.1f} us/step")
+    # the same stack and thresholds on the same rectangles over a noise-free
+    # static background: activity stays with the moving objects
+    clean = [syn.to_storage(f, wl.dtype) for f in
+             syn.RectVideo(wl.h, wl.w, wl.c, nfr, seed=401, batch=wl.n, noise_std=0.0)]
+    clean_dev = upload(clean, wl.dtype)
+    sweep = []
+    for chained in (False, True):
+        wall_c = timed(clean_dev, chained)
+        sweep.append({"label": f"clean background, {'chained' if chained else 'full'}",
+                      "frames_per_s": args.steps / wall_c, "ms_per_step": 1e3 * wall_c / args.steps})
+        log(f"[bench] stack6 clean background {'chained' if chained else 'full'}: {args.steps / wall_c:.0f} "
+            f"frames/s, {1e6 * wall_c / args.steps:.1f} us/step")
     # algorithmic bytes of the full-frame formulation: per layer 3|x| (x_t, x_{t-1}
     # read, x_t kept) + 2 d |z| + activation writes; reported against the chained step
     wall = res["chained"]
@@ -505,7 +521,7 @@ def bench_stack(args):
                    "eps0": eps0, "mac_density": d_mac,
                    "full_frames_per_s": args.steps / res["full"], "chained_frames_per_s": args.steps / wall,
                    "speedup_chained": res["full"] / wall},
-        "roofline": None, "cpu_baseline": None, "sweep": [],
+        "roofline": None, "cpu_baseline": None, "sweep": sweep,
     }
     print(json.dumps(out), flush=True)
 

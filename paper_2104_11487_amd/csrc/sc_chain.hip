@@ -36,38 +36,43 @@ emit_kernel(const uint8_t* block_mask, uint8_t* prev_mask, int nb, int bpw, cons
   }
   if (!__syncthreads_or(any)) return;
   const int bsz = block * block;
-  const int total = nblk * bsz * c_out;
+  // elements in groups of VEC consecutive channels (4 when c_out % 4 == 0)
+  const int vec = (c_out & 3) == 0 ? 4 : 1;
+  const int cg = c_out / vec;
+  const int total = nblk * bsz * cg;
   for (int e = threadIdx.x; e < total; e += kEmitThreads) {
-    const int bl = e / (bsz * c_out), rem0 = e - bl * bsz * c_out;
+    const int bl = e / (bsz * cg), rem0 = e - bl * bsz * cg;
     const uint8_t st = state[bl];
     if (!st) continue;
-    const int site = rem0 / c_out, ch = rem0 - site * c_out;
+    const int site = rem0 / cg, ch = (rem0 - site * cg) * vec;
     const int blk = b0 + bl;
     const int img = blk / (hb * wb), rem = blk - img * hb * wb;
     const int bi = rem / wb, bj = rem - bi * wb;
     const int oy = bi * block + site / block, ox = bj * block + site % block;
     if (oy >= h_out || ox >= w_out) continue;  // ceil-mode edge block
     const size_t o = ((size_t)(img * h_out + oy) * w_out + ox) * c_out + ch;
-    if (!(st & 1)) {
-      r32[o] = 0.0f;
-      if (dtype == 1) rb[o] = 0;
-      continue;
+    for (int v = 0; v < vec; ++v) {
+      if (!(st & 1)) {
+        r32[o + v] = 0.0f;
+        if (dtype == 1) rb[o + v] = 0;
+        continue;
+      }
+      float a = z[o + v];
+      if (act == 2) a = fmaxf(a, 0.0f);
+      float r;
+      if (dtype == 1) {
+        uint16_t* yb = static_cast<uint16_t*>(y);
+        const uint16_t yn = (uint16_t)f32_to_bf16(a);
+        r = __fsub_rn(bf16_to_f32(yn), bf16_to_f32(yb[o + v]));
+        yb[o + v] = yn;
+        rb[o + v] = (uint16_t)f32_to_bf16(r);
+      } else {
+        float* yf = static_cast<float*>(y);
+        r = __fsub_rn(a, yf[o + v]);
+        yf[o + v] = a;
+      }
+      r32[o + v] = r;
     }
-    float v = z[o];
-    if (act == 2) v = fmaxf(v, 0.0f);
-    float r;
-    if (dtype == 1) {
-      uint16_t* yb = static_cast<uint16_t*>(y);
-      const uint16_t yn = (uint16_t)f32_to_bf16(v);
-      r = __fsub_rn(bf16_to_f32(yn), bf16_to_f32(yb[o]));
-      yb[o] = yn;
-      rb[o] = (uint16_t)f32_to_bf16(r);
-    } else {
-      float* yf = static_cast<float*>(y);
-      r = __fsub_rn(v, yf[o]);
-      yf[o] = v;
-    }
-    r32[o] = r;
   }
   __syncthreads();
   for (int i = threadIdx.x; i < nblk; i += kEmitThreads) prev_mask[b0 + i] = state[i] & 1;

@@ -67,6 +67,41 @@ __device__ __forceinline__ void issue_b(const FusedParams& p, uint8_t* ldsb, int
     __builtin_amdgcn_global_load_lds(src + (size_t)u * 64, dst + u * 1024, 16, 0, 0);
 }
 
+// Residual emission, the part outside the epilogue: at the tile's blocks that
+// the previous step updated and this one does not, r = 0; then every block's
+// "updated by the previous step" flag becomes this step's. `cur` holds the
+// tile's block flags (NULL: none is active). All threads of the workgroup call it.
+__device__ void emit_clear(const FusedParams& p, int n, int oy0, int ox0, int oh, int ow, int tb_w,
+                           const uint32_t* cur, uint8_t* clr) {
+  const GateParams& g = p.g;
+  const int nby = (oh + g.block - 1) / g.block, nbx = (ow + g.block - 1) / g.block;
+  const int bi0 = oy0 / g.block, bj0 = ox0 / g.block;
+  int any = 0;
+  for (int i = threadIdx.x; i < nby * nbx; i += kThreads) {
+    const int by = i / nbx, bx = i - by * nbx;
+    const size_t gb = ((size_t)n * g.hb + bi0 + by) * g.wb + bj0 + bx;
+    const bool now = cur && cur[by * tb_w + bx] != 0u;
+    clr[i] = (p.prev_mask[gb] != 0 && !now) ? 1 : 0;
+    any |= clr[i];
+  }
+  if (__syncthreads_or(any)) {
+    const int c4 = p.c_out >> 2;
+    for (int e = threadIdx.x; e < oh * ow * c4; e += kThreads) {
+      const int site = e / c4, col = (e - site * c4) * 4;
+      const int ly = site / ow, lx = site - ly * ow;
+      if (!clr[(ly / g.block) * nbx + lx / g.block]) continue;
+      const size_t o = ((size_t)(n * g.h_out + oy0 + ly) * g.w_out + ox0 + lx) * p.c_out + col;
+      *reinterpret_cast<floatx4*>(p.r32 + o) = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+      *reinterpret_cast<uint2*>(p.rb + o) = uint2{0u, 0u};
+    }
+  }
+  for (int i = threadIdx.x; i < nby * nbx; i += kThreads) {
+    const int by = i / nbx, bx = i - by * nbx;
+    const size_t gb = ((size_t)n * g.hb + bi0 + by) * g.wb + bj0 + bx;
+    p.prev_mask[gb] = (cur && cur[by * tb_w + bx] != 0u) ? 1 : 0;
+  }
+}
+
 // Workgroup barrier that orders LDS accesses only: outstanding global loads
 // and stores (the weight copy, the z prefetch, the x_t copy) stay in flight.
 __device__ __forceinline__ void lds_barrier() {
@@ -86,6 +121,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
   __shared__ int rows_site[kMaxTileBlocks];
   __shared__ uint32_t wave_cnt[kWaves];
   __shared__ uint32_t tile_on;
+  __shared__ uint8_t emit_clr[kMaxTileBlocks];
 
   const GateParams& g = p.g;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -138,6 +174,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
         const int by = i / nbx2, bx = i - by * nbx2;
         g.block_mask[((size_t)n * g.hb + bi0 + by) * g.wb + bj0 + bx] = 0;
       }
+      if (p.emit) emit_clear(p, n, oy0, ox0, oh, ow, g.ts / g.block, nullptr, emit_clr);
       return;
     }
   }
@@ -164,6 +201,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
   int abase[WM], tapmul[WM], zsite[WM];
   uint32_t blk_of[WM];
   floatx4 zold[WM][WN];
+  uint2 yold[WM][WN];  // emitting layers: the activation output before this step
   if (kStatic) {
 #pragma unroll
     for (int i = 0; i < WM; ++i) {
@@ -300,6 +338,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
 
   if (!tile_on) {
     __builtin_amdgcn_s_waitcnt(0);  // no weight copy may still target this workgroup's LDS
+    if (p.emit) emit_clear(p, n, oy0, ox0, oh, ow, tb_w, blk_flag, emit_clr);
     return;
   }
   __syncthreads();  // the first weight chunk has landed in LDS
@@ -342,8 +381,12 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
       for (int j = 0; j < WN; ++j) {
         const int col = (wn * WN + j) * 16 + kq * 4;
         zold[i][j] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+        yold[i][j] = uint2{0u, 0u};
         if (zsite[i] >= 0 && !g.reference && col < p.c_out)
           zold[i][j] = *reinterpret_cast<const floatx4*>(p.z + (size_t)zsite[i] * p.c_out + col);
+        if (p.emit && zsite[i] >= 0 && col < p.c_out)
+          yold[i][j] = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(p.y) +
+                                                       (size_t)zsite[i] * p.c_out + col);
       }
   } else {
     // rows of blocks the gate left off are computed but not stored; the old z
@@ -355,8 +398,12 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
       for (int j = 0; j < WN; ++j) {
         const int col = (wn * WN + j) * 16 + kq * 4;
         zold[i][j] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+        yold[i][j] = uint2{0u, 0u};
         if (zsite[i] >= 0 && !g.reference && col < p.c_out)
           zold[i][j] = *reinterpret_cast<const floatx4*>(p.z + (size_t)zsite[i] * p.c_out + col);
+        if (p.emit && zsite[i] >= 0 && col < p.c_out)
+          yold[i][j] = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(p.y) +
+                                                       (size_t)zsite[i] * p.c_out + col);
       }
     }
   }
@@ -437,29 +484,41 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
     if (chunk + 1 < p.nchunks) __syncthreads();  // next chunk landed; this buffer free
   }
 
-  // 6. epilogue: z = z_{t-1} + U (assigned on a reference frame), activation output
-  if (!busy) return;
+  // 6. epilogue: z = z_{t-1} + U (assigned on a reference frame), activation
+  // output; emitting layers also write r = y_new - y_old for their successor
+  if (busy) {
 #pragma unroll
-  for (int i = 0; i < WM; ++i) {
-    if (zsite[i] < 0) continue;
+    for (int i = 0; i < WM; ++i) {
+      if (zsite[i] < 0) continue;
 #pragma unroll
-    for (int j = 0; j < WN; ++j) {
-      const int col = (wn * WN + j) * 16 + kq * 4;
-      if (col >= p.c_out) continue;
-      floatx4 nv;
+      for (int j = 0; j < WN; ++j) {
+        const int col = (wn * WN + j) * 16 + kq * 4;
+        if (col >= p.c_out) continue;
+        floatx4 nv;
 #pragma unroll
-      for (int v = 0; v < 4; ++v) nv[v] = g.reference ? acc[i][j][v] : zold[i][j][v] + acc[i][j][v];
-      const size_t o = (size_t)zsite[i] * p.c_out + col;
-      *reinterpret_cast<floatx4*>(p.z + o) = nv;
-      if (p.act) {
-        float av[4];
+        for (int v = 0; v < 4; ++v) nv[v] = g.reference ? acc[i][j][v] : zold[i][j][v] + acc[i][j][v];
+        const size_t o = (size_t)zsite[i] * p.c_out + col;
+        *reinterpret_cast<floatx4*>(p.z + o) = nv;
+        if (p.act) {
+          uint32_t yb[4];
 #pragma unroll
-        for (int v = 0; v < 4; ++v) av[v] = p.act == 2 ? fmaxf(nv[v], 0.0f) : nv[v];
-        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.y) + o) =
-            uint2{f32_to_bf16(av[0]) | (f32_to_bf16(av[1]) << 16), f32_to_bf16(av[2]) | (f32_to_bf16(av[3]) << 16)};
+          for (int v = 0; v < 4; ++v) yb[v] = f32_to_bf16(p.act == 2 ? fmaxf(nv[v], 0.0f) : nv[v]);
+          *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.y) + o) = uint2{yb[0] | (yb[1] << 16), yb[2] | (yb[3] << 16)};
+          if (p.emit) {
+            const uint32_t yo[4] = {yold[i][j].x & 0xffffu, yold[i][j].x >> 16, yold[i][j].y & 0xffffu,
+                                    yold[i][j].y >> 16};
+            floatx4 r;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) r[v] = __fsub_rn(bf16_to_f32(yb[v]), bf16_to_f32(yo[v]));
+            *reinterpret_cast<floatx4*>(p.r32 + o) = r;
+            *reinterpret_cast<uint2*>(p.rb + o) =
+                uint2{f32_to_bf16(r[0]) | (f32_to_bf16(r[1]) << 16), f32_to_bf16(r[2]) | (f32_to_bf16(r[3]) << 16)};
+          }
+        }
       }
     }
   }
+  if (p.emit) emit_clear(p, n, oy0, ox0, oh, ow, tb_w, blk_flag, emit_clr);
 }
 
 template <int WM, int WN, int GM>

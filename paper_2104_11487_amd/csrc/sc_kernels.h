@@ -91,6 +91,11 @@ struct FusedParams {
   int zero_pix;            // index of the all-zero pixel just past the halo
   int pstage;              // LDS floats per halo pixel of chunk sums: (c_in / 8) | 1
   int off_b, off_halo, off_a, off_part, lds_bytes;
+  // residual emission for a chained successor (act must be set): r = y_new - y_old
+  int emit;
+  float* r32;
+  uint16_t* rb;
+  uint8_t* prev_mask;      // blocks updated by the previous step
 };
 
 hipError_t launch_fused(const FusedParams& p, int grid, hipStream_t st);

@@ -390,7 +390,11 @@ sc::FusedParams fused_params(skipconv_layer* h, const void* x_t, bool ref) {
   fp.ntiles_n = g.ntn;
   fp.ksteps = g.ksteps;
   fp.csteps = d.c_in / 32;
-  fp.act = h->emits() ? 0 : d.act_out;  // an emitting layer writes y in the emit pass
+  fp.act = d.act_out;
+  fp.emit = h->emits() ? 1 : 0;  // the epilogue also writes the successor's residual
+  fp.r32 = h->r32();
+  fp.rb = h->rb();
+  fp.prev_mask = h->prev_mask();
   fp.kc = g.f_kc;
   fp.nchunks = g.f_nchunks;
   fp.nbuf = g.f_nbuf;
@@ -692,7 +696,7 @@ int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t
     if (e != hipSuccess) return hip_fail(h, e, "conv launch");
     h->list_valid = true;
   }
-  if (h->emits()) {
+  if (h->emits() && !g.fused) {  // the fused kernel emits in its epilogue
     e = launch_emit(h, st);
     if (e != hipSuccess) return hip_fail(h, e, "emit launch");
   }
@@ -738,8 +742,7 @@ int skipconv_step_chained(skipconv_t h, skipconv_t up, void* stream, const float
       fp.g.up_hb = up->g.hb;
       fp.g.up_wb = up->g.wb;
     }
-    hipError_t e = sc::launch_fused(fp, g.f_grid, st);
-    if (e == hipSuccess && h->emits()) e = launch_emit(h, st);
+    const hipError_t e = sc::launch_fused(fp, g.f_grid, st);
     if (e != hipSuccess) return hip_fail(h, e, "chained fused launch");
     h->list_valid = false;
     h->ref_pending = false;
