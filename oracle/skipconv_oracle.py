@@ -26,6 +26,10 @@ Processing", CVPR 2021):
   with one output channel and the layer's kernel size, stride and padding
   scores every output location; the gate rounds sigmoid(f), i.e. it is on
   exactly when f > 0. phi is a given parameter here (training is out of scope).
+* Sec. 3.3 (residuals between warped frames): with a warp T of the previous
+  frame, r_t = x_t - T(x_{t-1}) and z_t = T~(z_{t-1}) + w * r_t, T~ the same warp
+  on the output grid. Here T is a known global integer translation d (the
+  content moves by d pixels), so T~ is the translation by d / stride.
 * Sec. 3.2.2, "Structured Sparsity": max-pool the gate with kernel = stride = b,
   then nearest-neighbour upsample by b, giving b x b constant masks.
 * Sec. 4.2, "Runtime speed up": the sparse convolution is an im2col matrix
@@ -52,6 +56,14 @@ rest of the design notes):
   f[o] = sum of a over the in-frame taps of o in row-major order, plus the
   gate bias, all in float32 with one rounding per operation. The threshold
   eps is not used by this gate.
+* Translation-compensated step: T and T~ fill with zeros where the source lies
+  outside the frame; d must be a multiple of the stride. Convolution commutes
+  with the translation except at output rows (columns) where a tap reaches
+  content that the translation moved out of the frame, or whose source row
+  (column) lies outside the output grid ("exposed"); every block holding an
+  exposed site is recomputed from x_t (as on a reference frame, assigned), the
+  other blocks follow the gated recurrence on the translated state. With
+  eps = 0 this reproduces the dense convolution of every frame exactly.
 * Output-Norm gate: the weight norm is kept in the same power as the residual
   statistic (sum |w| for p = 1, sum w^2 for p = 2), summed in float64 over the
   weights in ascending flat OIHW order (|w| and w^2 of float32 or bf16 values
@@ -345,6 +357,42 @@ def conv_at_sites(rho: np.ndarray, weight: np.ndarray, stride: int, pad: int, gr
 
 
 # ----------------------------------------------------------------------------
+# Translation-compensated residual (Sec. 3.3, warp = integer translation)
+# ----------------------------------------------------------------------------
+
+
+def translate(x: np.ndarray, dy: int, dx: int) -> np.ndarray:
+    """T(x)[n, i, j] = x[n, i - dy, j - dx], zero where that lies outside the frame (NHWC or NHW)."""
+    out = np.zeros_like(x)
+    h, w = x.shape[1], x.shape[2]
+    ys, yd = slice(max(0, -dy), min(h, h - dy)), slice(max(0, dy), min(h, h + dy))
+    xs, xd = slice(max(0, -dx), min(w, w - dx)), slice(max(0, dx), min(w, w + dx))
+    out[:, yd, xd] = x[:, ys, xs]
+    return out
+
+
+def exposed_lines(n_out: int, n_in: int, k: int, stride: int, pad: int, d: int) -> np.ndarray:
+    """Output rows (or columns) where the translated recurrence is not exact (Sec. 3.3).
+
+    Line i is exposed when its source line i - d/stride lies outside the output
+    grid, or when one of its taps p = i*stride - pad + kh lies outside the frame
+    while p - d lies inside (content the translation pushed out of the frame).
+    """
+    do = d // stride
+    out = np.zeros(n_out, dtype=bool)
+    for i in range(n_out):
+        if not (0 <= i - do < n_out):
+            out[i] = True
+            continue
+        for kh in range(k):
+            p = i * stride - pad + kh
+            if (0 <= p - d < n_in) and not (0 <= p < n_in):
+                out[i] = True
+                break
+    return out
+
+
+# ----------------------------------------------------------------------------
 # The streaming layer
 # ----------------------------------------------------------------------------
 
@@ -404,11 +452,23 @@ class SkipConvOracle:
     def dense_macs(self) -> int:
         return self.n * self.h_out * self.w_out * self.c_out * (self.c_in // self.groups) * self.k * self.k
 
-    def step(self, x_t: np.ndarray) -> dict:
+    def step(self, x_t: np.ndarray, shift=(0, 0)) -> dict:
+        """One frame. shift = (dy, dx): the content moved by that many input pixels
+        since the previous frame (Sec. 3.3 with T a translation); multiples of the stride."""
         x32 = storage_to_f32(np.asarray(x_t), self.dtype)
         assert x32.shape == (self.n, self.h, self.w, self.c_in), x32.shape
         ref = self.reference_pending
+        dy, dx = int(shift[0]), int(shift[1])
+        shifted = (dy, dx) != (0, 0) and not ref
+        if shifted:
+            assert dy % self.stride == 0 and dx % self.stride == 0, "shift must be a multiple of the stride"
+            ex = (exposed_lines(self.h_out, self.h, self.k, self.stride, self.pad, dy)[:, None]
+                  | exposed_lines(self.w_out, self.w, self.k, self.stride, self.pad, dx)[None, :])
+            exposed = np.broadcast_to(ex, (self.n, self.h_out, self.w_out))
+            self.z = translate(self.z, dy // self.stride, dx // self.stride)
         prev = np.zeros_like(x32) if (ref or self.x_prev is None) else self.x_prev
+        if shifted:
+            prev = translate(prev, dy, dx)
         r = residual(x32, prev)
         if self.gate_kind == "learned":
             a = learned_pixel_taps(r, self.phi)
@@ -418,6 +478,8 @@ class SkipConvOracle:
             a = pixel_stat(r, self.norm_p)
             s = support_stat(a, self.k, self.stride, self.pad, self.h_out, self.w_out, self.support)
             g = gate(s, self.eps, self.norm_p, ref, self.wnorm)
+        if shifted:
+            g = g | exposed
         m_blk = block_pool(g, self.block)
         m = block_upsample(m_blk, self.block, self.h_out, self.w_out)
         lst = active_list(m_blk)
@@ -425,13 +487,22 @@ class SkipConvOracle:
             rho = x32.astype(np.float64) - prev.astype(np.float64)
         else:
             rho = operand(r, self.dtype)
-        sn, si, sj = np.nonzero(m)
+        # blocks holding an exposed site are recomputed from x_t (assigned)
+        xm = (block_upsample(block_pool(exposed, self.block), self.block, self.h_out, self.w_out)
+              if shifted else np.zeros_like(m))
+        sn, si, sj = np.nonzero(m & ~xm)
         if len(sn):
             u = conv_at_sites(rho, self.weight, self.stride, self.pad, self.groups, sn, si, sj)
             if ref:
                 self.z[sn, si, sj, :] = u
             else:
                 self.z[sn, si, sj, :] += u
+        sn, si, sj = np.nonzero(xm)
+        if len(sn):
+            rho_x = (x32.astype(np.float64) if self.exact_residual
+                     else operand(residual(x32, np.zeros_like(x32)), self.dtype))
+            self.z[sn, si, sj, :] = conv_at_sites(rho_x, self.weight, self.stride, self.pad, self.groups,
+                                                  sn, si, sj)
         self.x_prev = x32.copy()
         self.reference_pending = False
         self.frames += 1

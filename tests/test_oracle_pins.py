@@ -606,3 +606,97 @@ def test_learned_gate_nan_reference_and_strictness():
     y = np.array([[[0.0, -0.0, 1e-30, -1e-30, np.nan]]], np.float32)
     assert O.learned_gate(y, False).tolist() == [[[False, False, True, False, True]]]
     assert O.learned_gate(y, True).all()
+
+
+# ----------------------------------------------------------------------------
+# Translation-compensated residual (Sec. 3.3 with T an integer translation)
+# ----------------------------------------------------------------------------
+
+def test_exposed_lines_closed_form():
+    # H = 10, k = 3, pad 1, stride 1, content moved down by 2: rows 0-1 have no
+    # source row, row 9's bottom tap leaves the frame while its source is inside
+    assert np.flatnonzero(O.exposed_lines(10, 10, 3, 1, 1, 2)).tolist() == [0, 1, 9]
+    assert np.flatnonzero(O.exposed_lines(10, 10, 3, 1, 1, -2)).tolist() == [0, 8, 9]
+    assert not O.exposed_lines(10, 10, 3, 1, 1, 0).any()
+    # 1 x 1 kernel, no padding: only the rows without a source
+    assert np.flatnonzero(O.exposed_lines(8, 8, 1, 1, 0, 3)).tolist() == [0, 1, 2]
+
+
+@pytest.mark.parametrize("k,stride,d", [(3, 1, (2, -1)), (3, 2, (2, -4)), (5, 1, (-3, 2)), (1, 1, (1, 1))])
+def test_convolution_commutes_with_translation_off_the_exposed_lines(k, stride, d):
+    """w * T(x) == T~(w * x) exactly at every site that is not exposed (integer data)."""
+    rng = _rng(110 + k + stride)
+    n, h, wd, c, co = 2, 13, 11, 4, 3
+    pad = (k - 1) // 2
+    x = rng.integers(-5, 6, (n, h, wd, c)).astype(np.float64)
+    w = rng.integers(-3, 4, (co, c, k, k)).astype(np.float64)
+    a = torch_conv(O.translate(x, *d), w, stride, pad, 1)
+    b = O.translate(torch_conv(x, w, stride, pad, 1), d[0] // stride, d[1] // stride)
+    ho, wo = a.shape[1], a.shape[2]
+    ex = O.exposed_lines(ho, h, k, stride, pad, d[0])[:, None] | O.exposed_lines(wo, wd, k, stride, pad, d[1])[None, :]
+    assert np.array_equal(a[:, ~ex], b[:, ~ex])
+    assert ex.any() and (~ex).any()
+
+
+@pytest.mark.parametrize("dtype,stride", [("f32", 1), ("bf16", 1), ("f32", 2)])
+def test_translated_recurrence_eps0_is_dense_conv_integer_exact(dtype, stride):
+    """eps = 0 with translation compensation: every frame's z equals conv2d(x_t) exactly."""
+    rng = _rng(120 + stride)
+    n, h, wd, c, co, k = 1, 14, 12, 4, 5, 3
+    w = rng.integers(-2, 3, (co, c, k, k)).astype(np.float32)
+    lay = O.SkipConvOracle(w, n=n, h=h, w=wd, stride=stride, eps=0.0, block=2, dtype=dtype)
+    x = rng.integers(0, 8, (n, h, wd, c)).astype(np.float32)
+    shifts = [(0, 0), (2, 0), (0, -2), (-2, 2), (0, 0), (4, -2)]
+    for t, d in enumerate(shifts):
+        if t:
+            x = O.translate(x, *d)
+            fresh = rng.integers(0, 8, x.shape).astype(np.float32)
+            hole = O.translate(np.ones_like(x), *d) == 0        # entering content
+            x = np.where(hole, fresh, x)
+            x[:, 5, 3] += 1.0                                    # plus a local change
+        xs = O.f32_to_bf16_rne(x) if dtype == "bf16" else x
+        out = lay.step(xs, shift=d if t else (0, 0))
+        dense = torch_conv(x.astype(np.float64), w.astype(np.float64), stride, 1, 1)
+        assert np.array_equal(out["z"], dense), (dtype, stride, t)
+
+
+def test_translation_compensation_leaves_moved_static_content_off():
+    """A textured scene moving rigidly: compensated, only the entering strip and exposed
+    lines update; uncompensated, the whole textured frame fires."""
+    rng = _rng(130)
+    n, h, wd, c, co = 1, 24, 20, 8, 4
+    w = rng.normal(0, 0.3, (co, c, 3, 3)).astype(np.float32)
+    x = rng.random((n, h, wd, c), dtype=np.float32)
+    a = O.SkipConvOracle(w, n=n, h=h, w=wd, eps=1e-3, block=1)
+    b = O.SkipConvOracle(w, n=n, h=h, w=wd, eps=1e-3, block=1)
+    a.step(x)
+    b.step(x)
+    x1 = O.translate(x, 1, 2)
+    x1 = np.where(O.translate(np.ones_like(x), 1, 2) == 0, rng.random(x.shape, dtype=np.float32), x1)
+    ra, rb = a.step(x1, shift=(1, 2)), b.step(x1)
+    ex = O.exposed_lines(h, h, 3, 1, 1, 1)[:, None] | O.exposed_lines(wd, wd, 3, 1, 1, 2)[None, :]
+    # compensated: exactly the exposed sites and the sites whose support reaches
+    # the entering content (rows < 1, columns < 2 of the new frame)
+    hole = np.zeros((h, wd), bool)
+    hole[:1, :] = True
+    hole[:, :2] = True
+    near = np.zeros((h, wd), bool)
+    for i in range(h):
+        for j in range(wd):
+            near[i, j] = hole[max(0, i - 1):i + 2, max(0, j - 1):j + 2].any()
+    assert np.array_equal(ra["site_mask"][0], ex | near)
+    assert (ex | near).mean() < 0.5
+    assert rb["site_mask"].mean() > 0.9
+    dense = torch_conv(x1.astype(np.float64), w.astype(np.float64), 1, 1, 1)
+    assert np.abs(ra["z"] - dense).max() < 1e-5
+
+
+def test_zero_translation_is_the_plain_step():
+    rng = _rng(131)
+    w = rng.normal(0, 0.3, (4, 6, 3, 3)).astype(np.float32)
+    a = O.SkipConvOracle(w, n=1, h=9, w=10, eps=0.2, block=2)
+    b = O.SkipConvOracle(w, n=1, h=9, w=10, eps=0.2, block=2)
+    for t in range(4):
+        x = rng.random((1, 9, 10, 6), dtype=np.float32)
+        ra, rb = a.step(x, shift=(0, 0)), b.step(x)
+        assert np.array_equal(ra["z"], rb["z"]) and np.array_equal(ra["block_mask"], rb["block_mask"])
