@@ -91,12 +91,15 @@ enum { SKIPCONV_ACT_NONE = 0, SKIPCONV_ACT_IDENTITY = 1, SKIPCONV_ACT_RELU = 2 }
  * EMIT_RESIDUAL (needs an activation output): after every step, also hand a
  * chained successor its residual: r = fl32(y_new - y_old) at the blocks this
  * step updated (fp32, plus its bf16 rounding for bf16 layers) and r = 0 at
- * the blocks only the previous step updated; see skipconv_step_chained. */
+ * the blocks only the previous step updated; see skipconv_step_chained.
+ * TRANSLATE: allow skipconv_step_translated (a second z slot and two block
+ * lists in the workspace); not combinable with EMIT_RESIDUAL. */
 enum {
   SKIPCONV_FLAG_KEEP_STATS = 1u,
   SKIPCONV_FLAG_FORCE_DENSE = 2u,
   SKIPCONV_FLAG_SPLIT_PIPELINE = 4u,
-  SKIPCONV_FLAG_EMIT_RESIDUAL = 8u
+  SKIPCONV_FLAG_EMIT_RESIDUAL = 8u,
+  SKIPCONV_FLAG_TRANSLATE = 16u
 };
 
 typedef struct skipconv_desc {
@@ -162,6 +165,23 @@ int skipconv_create(const skipconv_desc* d, const void* weights, void* workspace
  * kernel (gather of residual patches, MFMA product over active sites only,
  * accumulate into z) on `stream`; no host synchronisation. */
 int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t);
+
+/* Process one frame whose content moved by (dy, dx) input pixels since the
+ * previous frame, a known global translation (Sec. 3.3 with the warp T an
+ * integer translation): r = x_t - T(x_{t-1}) and z = T~(z_{t-1}) + g (.) (w * r),
+ * where T(x)[y, x] = x[y - dy, x - dx] and T~ translates the output grid by
+ * (dy, dx) / stride, both zero where the source lies outside. Output rows
+ * (columns) where convolution and translation do not commute -- the source
+ * row is outside the grid, or a tap leaves the frame while its translated
+ * source is inside -- are "exposed": their sites are gated on, and every block
+ * holding one is recomputed from x_t and assigned. With eps = 0 every frame's
+ * z equals the dense convolution of x_t. dy and dx must be multiples of the
+ * stride with |dy| < h, |dx| < w; (0, 0) or a pending reference frame is a
+ * plain skipconv_step. The layer needs SKIPCONV_FLAG_TRANSLATE (E_STATE
+ * otherwise). Runs the split pipeline; z moves to the other of its two slots,
+ * so use the returned pointer. */
+int skipconv_step_translated(skipconv_t h, const void* x_t, int32_t dy, int32_t dx, void* stream,
+                             const float** z_t);
 
 /* Process one frame of a layer whose input is the activation output of the
  * layer `up` (sparse residual propagation between stacked layers, Sec. 3.1:

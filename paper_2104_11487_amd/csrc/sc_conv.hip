@@ -113,8 +113,9 @@ __device__ __forceinline__ bf16x8 gather_a_bf16(const ConvParams& p, const uint1
       const size_t off = ((size_t)(st.n * p.h + y) * p.w + x) * p.c + c0;
       float a[8], b[8];
       Elem<uint16_t>::load8(xt, off, a);
-      if (!p.no_prev) {
-        Elem<uint16_t>::load8(xp, off, b);
+      const long po = p.no_prev ? -1 : prev_off(p, st.n, y, x, c0);
+      if (po >= 0) {
+        Elem<uint16_t>::load8(xp, (size_t)po, b);
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[e] = __fsub_rn(a[e], b[e]);
       } else {
@@ -134,7 +135,8 @@ __device__ __forceinline__ bf16x8 gather_a_bf16(const ConvParams& p, const uint1
         if (y >= 0 && y < p.h && x >= 0 && x < p.w) {
           const size_t off = ((size_t)(st.n * p.h + y) * p.w + x) * p.c + ci;
           const float a = bf16_to_f32(xt[off]);
-          const float b = p.no_prev ? 0.0f : bf16_to_f32(xp[off]);
+          const long po = p.no_prev ? -1 : prev_off(p, st.n, y, x, ci);
+          const float b = po < 0 ? 0.0f : bf16_to_f32(xp[po]);
           v[e] = __fsub_rn(a, b);
         }
       }
@@ -300,7 +302,8 @@ conv_halo_kernel(ConvParams p, HaloParams hp) {
         if (in[u]) {
           const size_t off = ((size_t)(n * p.h + y) * p.w + x) * c + ch * 8;
           ra[u] = *reinterpret_cast<const uint4*>(xt + off);
-          if (!p.no_prev) rb[u] = *reinterpret_cast<const uint4*>(xp + off);
+          const long po = p.no_prev ? -1 : prev_off(p, n, y, x, ch * 8);
+          if (po >= 0) rb[u] = *reinterpret_cast<const uint4*>(xp + po);
         }
       }
 #pragma unroll
@@ -436,7 +439,8 @@ __global__ void __launch_bounds__(kConvThreads) conv_f32_kernel(ConvParams p) {
         const int y = iy + kh, x = ix + kw;
         if (y >= 0 && y < p.h && x >= 0 && x < p.w) {
           const size_t off = ((size_t)(st.n * p.h + y) * p.w + x) * p.c + ci;
-          a = p.no_prev ? xt[off] : __fsub_rn(xt[off], xp[off]);
+          const long po = p.no_prev ? -1 : prev_off(p, st.n, y, x, ci);
+          a = po < 0 ? xt[off] : __fsub_rn(xt[off], xp[po]);
         }
       }
       const float* wk = wp + (size_t)ks * NTN * 64 + lane;
@@ -494,20 +498,21 @@ __global__ void __launch_bounds__(kConvThreads) depthwise_kernel(ConvParams p) {
           if (x < 0 || x >= p.w) continue;
           const size_t off = ((size_t)(st.n * p.h + y) * p.w + x) * p.c + c0;
           float a[VEC], b[VEC];
+          const long po = p.no_prev ? -1 : prev_off(p, st.n, y, x, c0);
           if (VEC == 8) {
             Elem<T>::load8(xt, off, a);
-            if (!p.no_prev) Elem<T>::load8(xp, off, b);
+            if (po >= 0) Elem<T>::load8(xp, (size_t)po, b);
           } else if (VEC == 4) {
             Elem<T>::load4(xt, off, a);
-            if (!p.no_prev) Elem<T>::load4(xp, off, b);
+            if (po >= 0) Elem<T>::load4(xp, (size_t)po, b);
           } else {
             a[0] = Elem<T>::load1(xt, off);
-            if (!p.no_prev) b[0] = Elem<T>::load1(xp, off);
+            if (po >= 0) b[0] = Elem<T>::load1(xp, (size_t)po);
           }
           const float* wt = wp + (kh * p.k + kw) * p.c + c0;
 #pragma unroll
           for (int j = 0; j < VEC; ++j) {
-            float r = p.no_prev ? a[j] : __fsub_rn(a[j], b[j]);
+            float r = po < 0 ? a[j] : __fsub_rn(a[j], b[j]);
             if (bf16) r = bf16_to_f32(f32_to_bf16(r));
             acc[j] = __builtin_fmaf(wt[j], r, acc[j]);
           }

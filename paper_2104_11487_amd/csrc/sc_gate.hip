@@ -68,25 +68,27 @@ __device__ void halo_partials(const GateParams& p, int n, int iy0, int ix0, int 
       nel[u] = min(kChunk, c - ch * kChunk);
       off[u] = in[u] ? ((size_t)(n * p.h + y) * p.w + x) * c + ch * kChunk : 0;
       own[u] = in[u] && keep && p.copy_in_halo && y >= own_y0 && y < own_y1 && x >= own_x0 && x < own_x1;
+      // x_{t-1} under the step's translation (zero outside the frame)
+      const long po = (in[u] && !p.no_prev) ? prev_off(p, n, y, x, ch * kChunk) : -1;
       if (kPacked) {
         raw_t[kPacked ? u : 0] = uint4{0u, 0u, 0u, 0u};
         raw_p[kPacked ? u : 0] = uint4{0u, 0u, 0u, 0u};
         if (in[u]) {
           raw_t[kPacked ? u : 0] = *reinterpret_cast<const uint4*>(xt + off[u]);
-          if (!p.no_prev) raw_p[kPacked ? u : 0] = *reinterpret_cast<const uint4*>(xp + off[u]);
+          if (po >= 0) raw_p[kPacked ? u : 0] = *reinterpret_cast<const uint4*>(xp + po);
         }
       } else if (in[u]) {
         const int uu = kPacked ? 0 : u;
         if (VEC == kChunk) {
           load_vec<T, kChunk>(xt, off[u], vt[uu]);
-          if (!p.no_prev) load_vec<T, kChunk>(xp, off[u], vp[uu]);
+          if (po >= 0) load_vec<T, kChunk>(xp, (size_t)po, vp[uu]);
           else
             for (int j = 0; j < kChunk; ++j) vp[uu][j] = 0.0f;
         } else {
 #pragma unroll
           for (int j = 0; j < kChunk; ++j) {
             vt[uu][j] = j < nel[u] ? Elem<T>::load1(xt, off[u] + j) : 0.0f;
-            vp[uu][j] = (j < nel[u] && !p.no_prev) ? Elem<T>::load1(xp, off[u] + j) : 0.0f;
+            vp[uu][j] = (j < nel[u] && po >= 0) ? Elem<T>::load1(xp, (size_t)po + j) : 0.0f;
           }
         }
       }
@@ -151,21 +153,22 @@ __device__ void learned_halo(const GateParams& p, int n, int iy0, int ix0, int h
     for (int t = 0; t < K2; ++t) acc[t] = 0.0f;
     if (in) {
       const size_t base = ((size_t)(n * p.h + y) * p.w + x) * c;
+      const long pbase = p.no_prev ? -1 : prev_off(p, n, y, x, 0);  // translated x_{t-1}
       for (int c0 = 0; c0 < c; c0 += kChunk) {
         const int nel = min(kChunk, c - c0);
         float r[kChunk];
         if (VEC == kChunk) {
           float vt[kChunk], vp[kChunk];
           load_vec<T, kChunk>(xt, base + c0, vt);
-          if (!p.no_prev) load_vec<T, kChunk>(xp, base + c0, vp);
+          if (pbase >= 0) load_vec<T, kChunk>(xp, (size_t)pbase + c0, vp);
 #pragma unroll
-          for (int j = 0; j < kChunk; ++j) r[j] = p.no_prev ? vt[j] : __fsub_rn(vt[j], vp[j]);
+          for (int j = 0; j < kChunk; ++j) r[j] = pbase < 0 ? vt[j] : __fsub_rn(vt[j], vp[j]);
           if (own) copy_vec<T, kChunk>(keep, xt, base + c0);
         } else {
 #pragma unroll
           for (int j = 0; j < kChunk; ++j) {
             const float vt = j < nel ? Elem<T>::load1(xt, base + c0 + j) : 0.0f;
-            const float vp = (j < nel && !p.no_prev) ? Elem<T>::load1(xp, base + c0 + j) : 0.0f;
+            const float vp = (j < nel && pbase >= 0) ? Elem<T>::load1(xp, (size_t)pbase + c0 + j) : 0.0f;
             r[j] = __fsub_rn(vt, vp);
             if (own && j < nel) keep[base + c0 + j] = xt[base + c0 + j];
           }
@@ -311,7 +314,9 @@ __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
         }
       }
       sv = add_rn(sv, p.gate_bias);
-      const bool on = p.reference || p.force_dense || sv > 0.0f || (sv != sv);
+      const bool on = p.reference || p.force_dense || sv > 0.0f || (sv != sv) ||
+                      line_exposed(oy0 + ly, p.h_out, p.h, p.k, p.stride, p.pad, p.sy) ||
+                      line_exposed(ox0 + lx, p.w_out, p.w, p.k, p.stride, p.pad, p.sx);
       if (p.keep_stats) {
         const size_t o = ((size_t)n * p.h_out + oy0 + ly) * p.w_out + ox0 + lx;
         p.stat[o] = sv;
@@ -328,7 +333,9 @@ __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
     } else {
       sv = a_halo[(ly * s + p.pad) * hw + lx * s + p.pad];
     }
-    const bool on = p.reference || p.force_dense || ((double)sv * p.wnorm > p.thr) || (sv != sv);
+    const bool on = p.reference || p.force_dense || ((double)sv * p.wnorm > p.thr) || (sv != sv) ||
+                    line_exposed(oy0 + ly, p.h_out, p.h, p.k, p.stride, p.pad, p.sy) ||
+                    line_exposed(ox0 + lx, p.w_out, p.w, p.k, p.stride, p.pad, p.sx);
     if (p.keep_stats) {
       const size_t o = ((size_t)n * p.h_out + oy0 + ly) * p.w_out + ox0 + lx;
       p.stat[o] = sv;

@@ -46,6 +46,7 @@ struct GateParams {
   const uint8_t* up_mask;
   int up_block, up_hb, up_wb;
   int rin;                      // fused kernel: x_t is an fp32 residual (no x_{t-1})
+  int sy, sx;                   // translation of the content since x_{t-1} (split gate only)
 };
 
 // Sparse convolution over the active sites (dense groups = 1).
@@ -64,7 +65,33 @@ struct ConvParams {
   int reference;                // assign z instead of accumulating
   int no_prev;                  // x_{t-1} taken as 0 (reference frames; residual inputs)
   int act;                      // 0 none, 1 identity, 2 relu
+  int sy, sx;                   // translation of the content since x_{t-1} (input pixels; 0 = none)
 };
+
+// Element offset of x_{t-1} under the step's translation at input pixel
+// (n, y, x), channel ch: the translated previous frame holds x_{t-1}[y - sy,
+// x - sx], and zero where that lies outside the frame (returned as -1).
+template <typename P>
+__device__ __forceinline__ long prev_off(const P& p, int n, int y, int x, int ch) {
+  const int yp = y - p.sy, xq = x - p.sx;
+  if (yp < 0 || yp >= p.h || xq < 0 || xq >= p.w) return -1;
+  return ((long)(n * p.h + yp) * p.w + xq) * p.c + ch;
+}
+
+// Output line i (row or column) is "exposed" under a translation d of the
+// input (a multiple of the stride s) when its source line i - d/s is outside
+// the output grid, or when a tap p = i*s - pad + kh leaves the frame while
+// p - d lies inside it: convolution and translation do not commute there.
+__device__ __forceinline__ bool line_exposed(int i, int n_out, int n_in, int k, int s, int pad, int d) {
+  if (d == 0) return false;
+  const int src = i - d / s;
+  if (src < 0 || src >= n_out) return true;
+  for (int kh = 0; kh < k; ++kh) {
+    const int q = i * s - pad + kh;
+    if (q - d >= 0 && q - d < n_in && (q < 0 || q >= n_in)) return true;
+  }
+  return false;
+}
 
 // Block-halo variant of the dense bf16 convolution (see sc_conv.hip).
 struct HaloParams {
@@ -121,6 +148,15 @@ hipError_t launch_depthwise(const ConvParams& p, int dtype, int grid, hipStream_
 hipError_t launch_emit(const uint8_t* block_mask, uint8_t* prev_mask, int nb, const float* z, void* y,
                        float* r32, uint16_t* rb, int n, int hb, int wb, int block, int h_out, int w_out,
                        int c_out, int act, int dtype, hipStream_t st);
+
+// Translation-compensated steps (Sec. 3.3): the translated state, and the
+// active list split into translated-recurrence blocks and exposed blocks.
+hipError_t launch_translate_state(const float* z_src, float* z_dst, void* y, int n, int h_out, int w_out,
+                                  int c_out, int dyo, int dxo, int act, int dtype, hipStream_t st);
+hipError_t launch_split_list(const uint32_t* list, const uint32_t* counters, uint32_t* list_a,
+                             uint32_t* counters_a, uint32_t* list_b, uint32_t* counters_b, int hb, int wb,
+                             int block, int h_out, int w_out, int h, int w, int k, int stride, int pad, int sy,
+                             int sx, hipStream_t st);
 
 // One-time weight repacks (create time).
 hipError_t launch_pack_mfma(const void* w, void* out, int dtype, int c_out, int c_in, int k,

@@ -54,7 +54,7 @@ struct Geometry {
   int vec;              // gate load width (elements)
   size_t elem;
   size_t off_wpack, off_slot0, off_slot1, off_z, off_y, off_bmask, off_tflag, off_list, off_ctr,
-      off_stat, off_smask, off_phi, off_r32, off_rb, off_prev, total;
+      off_stat, off_smask, off_phi, off_r32, off_rb, off_prev, off_z2, off_list_a, off_list_b, total;
   int learned;          // learned gate: its kernel size (the layer's k), else 0
   bool phi_in_lds;      // learned gate: phi staged in LDS (else read through the caches)
   int phi_off;          // learned gate: LDS float offset of the staged phi
@@ -104,8 +104,10 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
     return fail(err, SKIPCONV_E_INVALID_ARG, "unknown act_out");
   if ((d->flags & SKIPCONV_FLAG_EMIT_RESIDUAL) && d->act_out == SKIPCONV_ACT_NONE)
     return fail(err, SKIPCONV_E_INVALID_ARG, "EMIT_RESIDUAL needs an activation output");
+  if ((d->flags & SKIPCONV_FLAG_EMIT_RESIDUAL) && (d->flags & SKIPCONV_FLAG_TRANSLATE))
+    return fail(err, SKIPCONV_E_UNSUPPORTED, "EMIT_RESIDUAL and TRANSLATE cannot be combined");
   if (d->flags & ~(uint32_t)(SKIPCONV_FLAG_KEEP_STATS | SKIPCONV_FLAG_FORCE_DENSE | SKIPCONV_FLAG_SPLIT_PIPELINE |
-                             SKIPCONV_FLAG_EMIT_RESIDUAL))
+                             SKIPCONV_FLAG_EMIT_RESIDUAL | SKIPCONV_FLAG_TRANSLATE))
     return fail(err, SKIPCONV_E_INVALID_ARG, "unknown flag bits");
   if (std::isnan(d->eps) || d->eps < 0.0f) return fail(err, SKIPCONV_E_INVALID_ARG, "eps must be >= 0");
   if (!depthwise && d->c_out > kMaxCout) return fail(err, SKIPCONV_E_UNSUPPORTED, "c_out > 256");
@@ -325,6 +327,14 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
     G.off_prev = off;
     off = align_up(off + (size_t)nb + 16);
   }
+  G.off_z2 = G.off_list_a = G.off_list_b = off;
+  if (d->flags & SKIPCONV_FLAG_TRANSLATE) {  // second z slot and the two block lists
+    off = align_up(off + G.z_bytes);
+    G.off_list_a = off;
+    off = align_up(off + (size_t)nb * 4);
+    G.off_list_b = off;
+    off = align_up(off + (size_t)nb * 4);
+  }
   G.total = off;
   return SKIPCONV_OK;
 }
@@ -352,7 +362,9 @@ struct skipconv_layer {
 
   void* wpack() { return ws + g.off_wpack; }
   void* slot(int i) { return ws + (i ? g.off_slot1 : g.off_slot0); }
-  float* z() { return reinterpret_cast<float*>(ws + g.off_z); }
+  int zslot = 0;             // translated steps alternate z between two slots
+  float* z() { return reinterpret_cast<float*>(ws + (zslot ? g.off_z2 : g.off_z)); }
+  float* z_other() { return reinterpret_cast<float*>(ws + (zslot ? g.off_z : g.off_z2)); }
   void* y() { return d.act_out ? (void*)(ws + g.off_y) : nullptr; }
   uint8_t* bmask() { return reinterpret_cast<uint8_t*>(ws + g.off_bmask); }
   uint8_t* tflags() { return reinterpret_cast<uint8_t*>(ws + g.off_tflag); }
@@ -705,6 +717,77 @@ int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t
     if (e != hipSuccess) return hip_fail(h, e, "event record");
     ++h->timing_done;
   }
+  h->cur ^= 1;
+  h->ref_pending = false;
+  ++h->frames;
+  if (z_t) *z_t = h->z();
+  return SKIPCONV_OK;
+}
+
+int skipconv_step_translated(skipconv_t h, const void* x_t, int32_t dy, int32_t dx, void* stream,
+                             const float** z_t) {
+  if (!h) return SKIPCONV_E_STATE;
+  if (!(h->d.flags & SKIPCONV_FLAG_TRANSLATE))
+    return fail(h->last_error, SKIPCONV_E_STATE, "the layer was created without SKIPCONV_FLAG_TRANSLATE");
+  const skipconv_desc& d = h->d;
+  if (dy % d.stride || dx % d.stride)
+    return fail(h->last_error, SKIPCONV_E_INVALID_ARG, "the translation must be a multiple of the stride");
+  if (dy <= -d.h || dy >= d.h || dx <= -d.w || dx >= d.w)
+    return fail(h->last_error, SKIPCONV_E_INVALID_ARG, "the translation must be smaller than the frame");
+  if ((dy == 0 && dx == 0) || h->ref_pending) return skipconv_step(h, x_t, stream, z_t);
+  if (!x_t) return fail(h->last_error, SKIPCONV_E_INVALID_ARG, "x_t is NULL");
+  if (reinterpret_cast<uintptr_t>(x_t) % 16)
+    return fail(h->last_error, SKIPCONV_E_INVALID_ARG, "x_t must be 16-byte aligned");
+  if (h->g.learned && !h->phi_set)
+    return fail(h->last_error, SKIPCONV_E_STATE, "learned gate: call skipconv_set_gate_weights first");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const Geometry& g = h->g;
+  // 1. z <- T~(z) into the other slot (activation output refreshed)
+  hipError_t e = sc::launch_translate_state(h->z(), h->z_other(), h->y(), d.n, g.h_out, g.w_out, d.c_out,
+                                            dy / d.stride, dx / d.stride, d.act_out, d.dtype, st);
+  if (e != hipSuccess) return hip_fail(h, e, "translate launch");
+  h->zslot ^= 1;
+  // 2. gate on r = x_t - T(x_{t-1}); exposed sites on
+  sc::GateParams gp = gate_params(h, x_t, false);
+  gp.sy = dy;
+  gp.sx = dx;
+  e = sc::launch_gate(gp, d.dtype, g.vec, g.gate_grid, g.gate_lds, st);
+  if (e == hipSuccess) e = launch_compaction(h, st);
+  // 3. active blocks: translated recurrence (list a) or recomputed from x_t (list b)
+  uint32_t* ctr = h->ctr();
+  uint32_t* list_a = reinterpret_cast<uint32_t*>(h->ws + g.off_list_a);
+  uint32_t* list_b = reinterpret_cast<uint32_t*>(h->ws + g.off_list_b);
+  if (e == hipSuccess)
+    e = sc::launch_split_list(h->list(), ctr, list_a, ctr + 2, list_b, ctr + 3, g.hb, g.wb, d.block, g.h_out,
+                              g.w_out, d.h, d.w, d.kernel, d.stride, g.pad, dy, dx, st);
+  if (e != hipSuccess) return hip_fail(h, e, "translated gate launch");
+  sc::ConvParams cp{};
+  cp.x_t = x_t;
+  cp.x_prev = h->slot(h->cur);
+  cp.wpack = h->wpack();
+  cp.z = h->z();
+  cp.y = h->y();
+  cp.n = d.n; cp.h = d.h; cp.w = d.w; cp.c = d.c_in; cp.c_out = d.c_out;
+  cp.h_out = g.h_out; cp.w_out = g.w_out; cp.k = d.kernel; cp.stride = d.stride; cp.pad = g.pad;
+  cp.block = d.block; cp.hb = g.hb; cp.wb = g.wb;
+  cp.ksteps = g.ksteps; cp.ntiles_n = g.ntn;
+  cp.act = d.act_out;
+  for (int pass = 0; pass < 2 && e == hipSuccess; ++pass) {
+    cp.list = pass ? list_b : list_a;
+    cp.counters = ctr + 2 + pass;
+    cp.reference = pass;  // exposed blocks: assigned from x_t
+    cp.no_prev = pass;
+    cp.sy = pass ? 0 : dy;
+    cp.sx = pass ? 0 : dx;
+    if (g.depthwise)
+      e = sc::launch_depthwise(cp, d.dtype, conv_grid(h), st);
+    else if (g.halo)
+      e = sc::launch_conv_halo(cp, g.hp, conv_grid(h), st);
+    else
+      e = sc::launch_conv(cp, d.dtype, g.fast, conv_grid(h), st);
+  }
+  if (e != hipSuccess) return hip_fail(h, e, "translated conv launch");
+  h->list_valid = true;
   h->cur ^= 1;
   h->ref_pending = false;
   ++h->frames;

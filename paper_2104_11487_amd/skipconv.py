@@ -30,6 +30,7 @@ SKIPCONV_GATE_INPUT_NORM, SKIPCONV_GATE_OUTPUT_NORM, SKIPCONV_GATE_LEARNED = 0, 
 SKIPCONV_ACT_NONE, SKIPCONV_ACT_IDENTITY, SKIPCONV_ACT_RELU = 0, 1, 2
 SKIPCONV_FLAG_KEEP_STATS, SKIPCONV_FLAG_FORCE_DENSE, SKIPCONV_FLAG_SPLIT_PIPELINE = 1, 2, 4
 SKIPCONV_FLAG_EMIT_RESIDUAL = 8
+SKIPCONV_FLAG_TRANSLATE = 16
 
 
 class skipconv_desc(ctypes.Structure):
@@ -58,6 +59,7 @@ _SIGS = {
     "skipconv_create": (ctypes.c_int, [_D, _P, _P, ctypes.c_size_t, _P, ctypes.POINTER(_P)]),
     "skipconv_step": (ctypes.c_int, [_P, _P, _P, ctypes.POINTER(_P)]),
     "skipconv_step_chained": (ctypes.c_int, [_P, _P, _P, ctypes.POINTER(_P)]),
+    "skipconv_step_translated": (ctypes.c_int, [_P, _P, ctypes.c_int32, ctypes.c_int32, _P, ctypes.POINTER(_P)]),
     "skipconv_reset": (ctypes.c_int, [_P]),
     "skipconv_set_eps": (ctypes.c_int, [_P, ctypes.c_float]),
     "skipconv_set_gate_weights": (ctypes.c_int, [_P, _P, ctypes.c_float, _P]),
@@ -151,6 +153,12 @@ def skipconv_step(h: int, x_ptr: int, stream: int) -> int:
 def skipconv_step_chained(h: int, up: int, stream: int) -> int:
     z = ctypes.c_void_p()
     _check(lib().skipconv_step_chained(h, up, stream, ctypes.byref(z)), h)
+    return z.value
+
+
+def skipconv_step_translated(h: int, x_ptr: int, dy: int, dx: int, stream: int) -> int:
+    z = ctypes.c_void_p()
+    _check(lib().skipconv_step_translated(h, x_ptr, dy, dx, stream, ctypes.byref(z)), h)
     return z.value
 
 
@@ -260,7 +268,8 @@ _GATE = {"input": SKIPCONV_GATE_INPUT_NORM, "output": SKIPCONV_GATE_OUTPUT_NORM,
 
 def make_desc(*, n, h, w, c_in, c_out, kernel, stride=1, pad=-1, groups=1, block=1, norm_p=2,
               support="rf", dtype="f32", act_out="none", eps=0.0, keep_stats=False,
-              force_dense=False, split=False, gate="input", emit_residual=False) -> skipconv_desc:
+              force_dense=False, split=False, gate="input", emit_residual=False,
+              translate=False) -> skipconv_desc:
     d = skipconv_desc_init()
     d.n, d.h, d.w, d.c_in, d.c_out = n, h, w, c_in, c_out
     d.kernel, d.stride, d.pad, d.groups, d.block = kernel, stride, pad, groups, block
@@ -269,7 +278,8 @@ def make_desc(*, n, h, w, c_in, c_out, kernel, stride=1, pad=-1, groups=1, block
     d.act_out = _ACT[act_out]
     d.flags = ((SKIPCONV_FLAG_KEEP_STATS if keep_stats else 0) | (SKIPCONV_FLAG_FORCE_DENSE if force_dense else 0)
                | (SKIPCONV_FLAG_SPLIT_PIPELINE if split else 0)
-               | (SKIPCONV_FLAG_EMIT_RESIDUAL if emit_residual else 0))
+               | (SKIPCONV_FLAG_EMIT_RESIDUAL if emit_residual else 0)
+               | (SKIPCONV_FLAG_TRANSLATE if translate else 0))
     d.eps = eps
     d.gate = _GATE[gate]
     return d
@@ -288,7 +298,7 @@ class SkipConv:
                  groups: int = 1, eps: float = 0.0, block: int = 1, norm_p: int = 2,
                  support: str = "rf", act_out: str = "none", keep_stats: bool = False,
                  force_dense: bool = False, split: bool = False, gate: str = "input",
-                 emit_residual: bool = False, stream=None):
+                 emit_residual: bool = False, translate: bool = False, stream=None):
         import torch
 
         if not weight.is_cuda:
@@ -302,7 +312,8 @@ class SkipConv:
         self.desc = make_desc(n=n, h=h, w=w, c_in=cg * groups, c_out=c_out, kernel=k, stride=stride,
                               pad=pad, groups=groups, block=block, norm_p=norm_p, support=support,
                               dtype=self.dtype, act_out=act_out, eps=eps, keep_stats=keep_stats, gate=gate,
-                              force_dense=force_dense, split=split, emit_residual=emit_residual)
+                              force_dense=force_dense, split=split, emit_residual=emit_residual,
+                              translate=translate)
         self.h_out, self.w_out, self.hb, self.wb = skipconv_out_shape(self.desc)
         nbytes = skipconv_workspace_size(self.desc)
         self.device = weight.device
@@ -312,6 +323,7 @@ class SkipConv:
         self.handle = skipconv_create(self.desc, self._weight.data_ptr(), self.workspace.data_ptr(),
                                       nbytes, self._stream())
         self._z = None
+        self._zp = None
         self._y = None
 
     def _stream(self) -> int:
@@ -333,11 +345,22 @@ class SkipConv:
         if tuple(x.shape) != self.shape_in or x.dtype != self.tdtype or not x.is_contiguous() \
                 or x.device != self.device:
             raise ValueError(f"x must be a contiguous {self.tdtype} tensor of shape {self.shape_in} on {self.device}")
-        zp = skipconv_step(self.handle, x.data_ptr(), self._stream())
-        if self._z is None:
+        return self._z_view(skipconv_step(self.handle, x.data_ptr(), self._stream()))
+
+    def _z_view(self, zp: int):
+        # the state pointer is fixed except across translated steps (two z slots)
+        if self._z is None or zp != self._zp:
             self._z = self._view(zp, self.desc.n * self.h_out * self.w_out * self.desc.c_out,
                                  self.torch.float32)
+            self._zp = zp
         return self._z
+
+    def step_translated(self, x, dy: int, dx: int):
+        """One frame whose content moved by (dy, dx) pixels since the previous one (Sec. 3.3)."""
+        if tuple(x.shape) != self.shape_in or x.dtype != self.tdtype or not x.is_contiguous() \
+                or x.device != self.device:
+            raise ValueError(f"x must be a contiguous {self.tdtype} tensor of shape {self.shape_in} on {self.device}")
+        return self._z_view(skipconv_step_translated(self.handle, x.data_ptr(), dy, dx, self._stream()))
 
     def step_chained(self, upstream: "SkipConv"):
         """One frame whose input is `upstream`'s activation output (upstream stepped first).
@@ -345,11 +368,7 @@ class SkipConv:
         `upstream` must have been created with emit_residual=True; see
         skipconv_step_chained for the contract.
         """
-        zp = skipconv_step_chained(self.handle, upstream.handle, self._stream())
-        if self._z is None:
-            self._z = self._view(zp, self.desc.n * self.h_out * self.w_out * self.desc.c_out,
-                                 self.torch.float32)
-        return self._z
+        return self._z_view(skipconv_step_chained(self.handle, upstream.handle, self._stream()))
 
     def activation(self):
         if self._y is None:

@@ -137,6 +137,7 @@ class RectVideo:
                 rs.append(_Rect(rh, rw, y, x, vy, vx, tex))
             rects.append(rs)
         self.shake_frames = []
+        self.shake_shift = {}  # frame -> (dy, dx): that frame's content moved by (dy, dx)
         for t in range(self.frames):
             out = np.empty((self.batch, self.h, self.w, self.c), np.float32)
             shake = None
@@ -146,6 +147,7 @@ class RectVideo:
                 if t > 0 and u < self.shake_prob:
                     shake = (int(d[0]), int(d[1]))
                     self.shake_frames.append(t)
+                    self.shake_shift[t] = shake
             for n in range(self.batch):
                 f = bgs[n] + rng.normal(0.0, self.noise_std,
                                         size=(self.h, self.w, self.c)).astype(np.float32)

@@ -43,7 +43,7 @@ def good(**kw):
     ("block", 0, S.SKIPCONV_E_INVALID_ARG), ("block", 65, S.SKIPCONV_E_INVALID_ARG),
     ("norm_p", 3, S.SKIPCONV_E_INVALID_ARG), ("support", 2, S.SKIPCONV_E_INVALID_ARG),
     ("dtype", 2, S.SKIPCONV_E_INVALID_ARG), ("act_out", 3, S.SKIPCONV_E_INVALID_ARG),
-    ("flags", 16, S.SKIPCONV_E_INVALID_ARG), ("flags", 8, S.SKIPCONV_E_INVALID_ARG),
+    ("flags", 32, S.SKIPCONV_E_INVALID_ARG), ("flags", 8, S.SKIPCONV_E_INVALID_ARG),
     ("eps", -1.0, S.SKIPCONV_E_INVALID_ARG),
     ("eps", float("nan"), S.SKIPCONV_E_INVALID_ARG), ("c_out", 272, S.SKIPCONV_E_UNSUPPORTED),
     ("gate", 7, S.SKIPCONV_E_INVALID_ARG), ("gate", -1, S.SKIPCONV_E_INVALID_ARG),
@@ -68,6 +68,8 @@ def test_valid_variants(lib):
     assert S.skipconv_validate(good(gate="output", norm_p=1, dtype="f32")) == 0
     assert S.skipconv_validate(good(gate="learned")) == 0
     assert S.skipconv_validate(good(act_out="relu", emit_residual=True)) == 0
+    assert S.skipconv_validate(good(translate=True)) == 0
+    assert S.skipconv_validate(good(act_out="relu", emit_residual=True, translate=True)) == S.SKIPCONV_E_UNSUPPORTED
     assert S.skipconv_validate(good(gate="learned", kernel=7, dtype="f32", c_in=256)) == 0
 
 
@@ -99,6 +101,7 @@ def test_workspace_size_covers_state(lib):
 def test_null_handles_and_status_strings(lib):
     assert lib.skipconv_step(None, None, None, None) == S.SKIPCONV_E_STATE
     assert lib.skipconv_step_chained(None, None, None, None) == S.SKIPCONV_E_STATE
+    assert lib.skipconv_step_translated(None, None, 0, 0, None, None) == S.SKIPCONV_E_STATE
     assert lib.skipconv_reset(None) == S.SKIPCONV_E_STATE
     assert lib.skipconv_destroy(None) == S.SKIPCONV_OK
     assert lib.skipconv_set_eps(None, ctypes.c_float(1.0)) == S.SKIPCONV_E_STATE

@@ -21,11 +21,12 @@ pytestmark = pytest.mark.gpu
 
 def _layer_pair(w_f32, *, n, h, w, dtype, eps, block, stride=1, pad=-1, groups=1, norm_p=2,
                 support="rf", keep_stats=True, act_out="none", force_dense=False, split=False,
-                gate="input", phi=None, gate_bias=0.0):
+                gate="input", phi=None, gate_bias=0.0, translate=False):
     ws = weight_storage(w_f32, dtype)
     layer = S.SkipConv(to_device(ws, dtype), n=n, h=h, w=w, stride=stride, pad=pad, groups=groups,
                        eps=eps, block=block, norm_p=norm_p, support=support, keep_stats=keep_stats,
-                       act_out=act_out, force_dense=force_dense, split=split, gate=gate)
+                       act_out=act_out, force_dense=force_dense, split=split, gate=gate,
+                       translate=translate)
     if gate == "learned":
         layer.set_gate_weights(torch.from_numpy(np.ascontiguousarray(phi, np.float32)).cuda(), gate_bias)
     orc = O.SkipConvOracle(ws, n=n, h=h, w=w, stride=stride, pad=None if pad == -1 else pad,
@@ -668,3 +669,104 @@ def test_chained_step_contract_errors():
         S.SkipConv(wd, n=1, h=16, w=16, emit_residual=True)  # no activation output to difference
     for lay in (up_plain, up, down, wrong):
         lay.close()
+
+
+# ------------------------------------- translation-compensated steps (Sec. 3.3) --
+
+def run_translated(frames, shifts, w_f32, *, dtype, eps, block, tag, exact_z=False, **kw):
+    n, h, w, _ = frames[0].shape
+    layer, orc = _layer_pair(w_f32, n=n, h=h, w=w, dtype=dtype, eps=eps, block=block, translate=True, **kw)
+    dens = []
+    for t, (f, d) in enumerate(zip(frames, shifts)):
+        xs = syn.to_storage(f, dtype)
+        say(f"[{tag}] frame {t} shift={d}")
+        layer.step_translated(to_device(xs, dtype), *d)
+        ref = orc.step(xs, shift=d)
+        compare_frame(layer, ref, dtype, t=t, tag=tag, keep_stats=True, exact_z=exact_z)
+        dens.append(ref["count"] / ref["block_mask"].size)
+    layer.close()
+    return dens
+
+
+def _translated_integer_video(rng, n, h, w, c, shifts, stride):
+    x = rng.integers(0, 8, (n, h, w, c)).astype(np.float32)
+    frames = [x]
+    for d in shifts[1:]:
+        x = O.translate(x, *d)
+        hole = O.translate(np.ones_like(x), *d) == 0
+        x = np.where(hole, rng.integers(0, 8, x.shape).astype(np.float32), x)
+        x[:, h // 2, w // 3] += 1.0
+        frames.append(x.astype(np.float32))
+    return frames
+
+
+@pytest.mark.parametrize("case", [
+    # dtype, block, k, stride, groups, c_in, c_out
+    ("f32", 1, 3, 1, 1, 8, 16),
+    ("bf16", 4, 3, 1, 1, 32, 64),     # halo conv
+    ("bf16", 8, 5, 1, 1, 16, 32),     # direct gather
+    ("f32", 2, 3, 2, 1, 8, 8),        # stride 2, even shifts
+    ("bf16", 1, 3, 1, 16, 16, 16),    # depthwise
+], ids=["f32b1", "bf16halo", "bf16k5", "f32s2", "bf16dw"])
+def test_translated_eps0_integer_is_dense_conv(case):
+    """eps = 0 over translated integer frames: z equals conv2d(x_t) bit for bit, masks match the oracle."""
+    dtype, block, k, stride, groups, c_in, c_out = case
+    rng = np.random.Generator(np.random.PCG64(140 + k + block))
+    s = stride
+    shifts = [(0, 0), (s, 0), (0, -2 * s), (-s, s), (0, 0), (2 * s, -s), (-3 * s, 2 * s)]
+    frames = _translated_integer_video(rng, 2, 26, 22, c_in, shifts, stride)
+    w = syn.integer_weights(c_out, c_in // groups, k, seed=141)
+    run_translated(frames, shifts, w, dtype=dtype, eps=0.0, block=block, stride=stride, groups=groups,
+                   pad=-1, tag=f"translated eps0 {case}", exact_z=True)
+
+
+@pytest.mark.parametrize("block", [1, 8])
+def test_translated_rect64_with_gate(block):
+    """The 128 x 96 x 64 layer on a video panning by a few pixels per frame, eps > 0."""
+    wl = syn.workloads()["rect64"]
+    base = list(wl.video(8))
+    shifts = [(0, 0), (1, 2), (1, 2), (0, -3), (2, 0), (0, 0), (-1, -1), (3, 1)]
+    frames, acc = [], (0, 0)
+    for f, d in zip(base, shifts):
+        acc = (acc[0] + d[0], acc[1] + d[1])
+        frames.append(O.translate(f, *acc))
+    stats = oracle_stats(base, (64, 64, 3, 3), dtype="bf16")
+    eps = eps_for_density(stats, block, 128, 96, 0.25)
+    dens = run_translated(frames, shifts, wl.weights()[0], dtype="bf16", eps=eps, block=block,
+                          tag=f"rect64 translated b={block}")
+    assert np.mean(dens[1:]) < 1.0
+
+
+def test_shake_frames_compensated():
+    """Camera-shake frames of the pointwise layer (1 x 1, 8 x 8 blocks): each frame is stepped with
+    its known shift relative to the previous one."""
+    wl = syn.workloads()["mbconv192"]
+    vid = syn.RectVideo(64, 64, 192, 16, seed=301, batch=1, shake_prob=0.3)
+    frames = list(vid)
+    assert vid.shake_frames, "no shake frame drawn"
+    prev = (0, 0)
+    shifts = []
+    for t in range(len(frames)):
+        cur = vid.shake_shift.get(t, (0, 0))
+        shifts.append((cur[0] - prev[0], cur[1] - prev[1]) if t else (0, 0))
+        prev = cur
+    run_translated(frames, shifts, wl.weights()[0], dtype="bf16", eps=2.0, block=8, tag="shake compensated")
+
+
+def test_translated_step_contract():
+    rng = np.random.Generator(np.random.PCG64(142))
+    w = to_device(rng.normal(0, 0.3, (8, 8, 3, 3)).astype(np.float32), "f32")
+    x = to_device(rng.random((1, 12, 12, 8), dtype=np.float32), "f32")
+    plain = S.SkipConv(w, n=1, h=12, w=12)
+    with pytest.raises(S.SkipConvError) as ei:
+        plain.step_translated(x, 1, 0)
+    assert ei.value.code == S.SKIPCONV_E_STATE
+    s2 = S.SkipConv(w, n=1, h=12, w=12, stride=2, translate=True)
+    s2.step(x)
+    with pytest.raises(S.SkipConvError) as ei:
+        s2.step_translated(x, 1, 0)   # not a multiple of the stride
+    assert ei.value.code == S.SKIPCONV_E_INVALID_ARG
+    with pytest.raises(S.SkipConvError):
+        s2.step_translated(x, 12, 0)  # as large as the frame
+    plain.close()
+    s2.close()
