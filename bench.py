@@ -255,6 +255,63 @@ def measure_point(make_layer, frames_dev, steps, warmup, geom, *, label, events=
     return res
 
 
+def translate_np(x, dy, dx):
+    """Frame content moved by (dy, dx) pixels, zero where nothing moved in (N, H, W, C)."""
+    out = np.zeros_like(x)
+    h, w = x.shape[1], x.shape[2]
+    out[:, max(0, dy):min(h, h + dy), max(0, dx):min(w, w + dx)] = \
+        x[:, max(0, -dy):min(h, h - dy), max(0, -dx):min(w, w - dx)]
+    return out
+
+
+def measure_translated(wt, layer_kw, clip, dtype, eps, block, steps):
+    """Clip frames with a (1, 1) pixel camera jitter on every other frame: steps with the
+    known translation (skipconv_step_translated) against plain steps on the same frames."""
+    import torch
+    from paper_2104_11487_amd.skipconv import SkipConv
+
+    nfr = len(clip)
+    jit = [(t % 2, t % 2) for t in range(nfr)]
+    frames = []
+    for t, x in enumerate(clip):
+        xs = x.view(np.uint16) if dtype == "bf16" else x
+        frames.append(translate_np(xs, *jit[t]))
+    dev = upload([f.view(np.uint16) if dtype == "bf16" else f for f in frames], dtype)
+    shifts = [(0, 0)] + [(jit[t][0] - jit[t - 1][0], jit[t][1] - jit[t - 1][1]) for t in range(1, nfr)]
+    out = []
+    for compensated in (True, False):
+        lay = SkipConv(wt, eps=eps, block=block, translate=True, **layer_kw)
+        sites = 0
+
+        def run(n, count=False):
+            nonlocal sites
+            for j in range(n):
+                t = j % nfr
+                if t == 0:
+                    lay.reset()
+                if compensated:
+                    lay.step_translated(dev[t], *shifts[t])
+                else:
+                    lay.step(dev[t])
+                if count:
+                    sites += lay.active_count()[1]
+
+        run(nfr, count=True)
+        run(nfr)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        run(steps)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        lay.close()
+        total = nfr * lay.h_out * lay.w_out * layer_kw["n"]
+        out.append({"label": f"camera jitter, {'translation-compensated' if compensated else 'plain'} steps",
+                    "frames_per_s": steps * layer_kw["n"] / wall, "ms_per_step": 1e3 * wall / steps,
+                    "density": sites / total})
+        log(f"[bench] {out[-1]['label']}: {out[-1]['frames_per_s']:.0f} frames/s, density {out[-1]['density']:.3f}")
+    return out
+
+
 def torch_dense_us(wt, shape, stride, steps=200):
     """torch conv2d (MIOpen) of the same shape, channels-last, for context only."""
     import torch
@@ -651,6 +708,10 @@ def main():
                           label=f"learned gate b={block} d={args.density}")
         r.update({"block": block, "target_density": args.density, "gate": "learned", "bias": bias})
         sweep.append(r)
+        # translation-compensated steps (Sec. 3.3): the clip with a one-pixel
+        # camera jitter on every other frame, stepped with the known shift vs. plainly
+        r1, r2 = measure_translated(wt, layer_kw, clip, wl.dtype, eps_head, block, sweep_steps)
+        sweep += [r1, r2]
         tus = torch_dense_us(wt, (wl.n, wl.h, wl.w, wl.c), spec.stride)
         sweep.append({"label": "torch conv2d (MIOpen), dense, same shape", "us_per_frame_batch": tus,
                       "dense_tflops": 2.0 * geom["sites"] * spec.c_out * kk / (tus * 1e-6) / 1e12})

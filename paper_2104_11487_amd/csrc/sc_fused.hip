@@ -112,8 +112,12 @@ __device__ __forceinline__ void lds_barrier() {
 
 // Wave layout of the product: GM waves along M (WM 16-row tiles each) by 2
 // along N (WN 16-column tiles each); waves past the first 2 * GM do no MFMA.
-template <int WM, int WN, int GM>
+// MODE bit 0: emit the successor's residual; bit 1: chained input (x_t is the
+// upstream layer's fp32 residual, tiles without upstream blocks exit early).
+template <int WM, int WN, int GM, int MODE>
 __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
+  constexpr bool EMIT = (MODE & 1) != 0;
+  constexpr bool CHAIN = (MODE & 2) != 0;
   constexpr int NTN = WN * 2;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   __shared__ uint32_t blk_flag[kMaxTileBlocks];
@@ -147,7 +151,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
   const int tb_w = g.ts / g.block;
   const int npix = hh * hw;
 
-  if (g.up_mask) {
+  if (CHAIN && g.up_mask) {
     // chained input: the residual is zero outside the upstream layer's active
     // blocks; a tile whose input region meets none of them has every gate off
     // and stops here, before any load (norm gates only)
@@ -174,7 +178,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
         const int by = i / nbx2, bx = i - by * nbx2;
         g.block_mask[((size_t)n * g.hb + bi0 + by) * g.wb + bj0 + bx] = 0;
       }
-      if (p.emit) emit_clear(p, n, oy0, ox0, oh, ow, g.ts / g.block, nullptr, emit_clr);
+      if (EMIT) emit_clear(p, n, oy0, ox0, oh, ow, g.ts / g.block, nullptr, emit_clr);
       return;
     }
   }
@@ -245,7 +249,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
       vt[u] = uint4{0u, 0u, 0u, 0u};
       vp[u] = uint4{0u, 0u, 0u, 0u};
       if (in[u]) {
-        if (g.rin) {  // fp32 residual input: channels 0-3 in vt, 4-7 in vp
+        if (CHAIN) {  // fp32 residual input: channels 0-3 in vt, 4-7 in vp
           const float* rr = static_cast<const float*>(g.x_t) + off[u];
           vt[u] = *reinterpret_cast<const uint4*>(rr);
           vp[u] = *reinterpret_cast<const uint4*>(rr + 4);
@@ -266,7 +270,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
       for (int e = 0; e < 4; ++e) {
         // channels 2e (low half) and 2e + 1 (high half)
         float r0, r1;
-        if (g.rin) {
+        if (CHAIN) {
           const uint32_t* src = e < 2 ? wt : wpv;
           r0 = __uint_as_float(src[(2 * e) & 3]);
           r1 = __uint_as_float(src[(2 * e + 1) & 3]);
@@ -338,7 +342,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
 
   if (!tile_on) {
     __builtin_amdgcn_s_waitcnt(0);  // no weight copy may still target this workgroup's LDS
-    if (p.emit) emit_clear(p, n, oy0, ox0, oh, ow, tb_w, blk_flag, emit_clr);
+    if (EMIT) emit_clear(p, n, oy0, ox0, oh, ow, tb_w, blk_flag, emit_clr);
     return;
   }
   __syncthreads();  // the first weight chunk has landed in LDS
@@ -384,7 +388,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
         yold[i][j] = uint2{0u, 0u};
         if (zsite[i] >= 0 && !g.reference && col < p.c_out)
           zold[i][j] = *reinterpret_cast<const floatx4*>(p.z + (size_t)zsite[i] * p.c_out + col);
-        if (p.emit && zsite[i] >= 0 && col < p.c_out)
+        if (EMIT && zsite[i] >= 0 && col < p.c_out)
           yold[i][j] = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(p.y) +
                                                        (size_t)zsite[i] * p.c_out + col);
       }
@@ -401,7 +405,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
         yold[i][j] = uint2{0u, 0u};
         if (zsite[i] >= 0 && !g.reference && col < p.c_out)
           zold[i][j] = *reinterpret_cast<const floatx4*>(p.z + (size_t)zsite[i] * p.c_out + col);
-        if (p.emit && zsite[i] >= 0 && col < p.c_out)
+        if (EMIT && zsite[i] >= 0 && col < p.c_out)
           yold[i][j] = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(p.y) +
                                                        (size_t)zsite[i] * p.c_out + col);
       }
@@ -504,7 +508,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
 #pragma unroll
           for (int v = 0; v < 4; ++v) yb[v] = f32_to_bf16(p.act == 2 ? fmaxf(nv[v], 0.0f) : nv[v]);
           *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.y) + o) = uint2{yb[0] | (yb[1] << 16), yb[2] | (yb[3] << 16)};
-          if (p.emit) {
+          if (EMIT) {
             const uint32_t yo[4] = {yold[i][j].x & 0xffffu, yold[i][j].x >> 16, yold[i][j].y & 0xffffu,
                                     yold[i][j].y >> 16};
             floatx4 r;
@@ -518,26 +522,42 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
       }
     }
   }
-  if (p.emit) emit_clear(p, n, oy0, ox0, oh, ow, tb_w, blk_flag, emit_clr);
+  if (EMIT) emit_clear(p, n, oy0, ox0, oh, ow, tb_w, blk_flag, emit_clr);
 }
 
 template <int WM, int WN, int GM>
 hipError_t launch_fused_t(const FusedParams& p, int grid, hipStream_t st) {
-  hipLaunchKernelGGL((fused_kernel<WM, WN, GM>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p);
+  switch ((p.emit ? 1 : 0) | (p.g.rin ? 2 : 0)) {
+    case 0: hipLaunchKernelGGL((fused_kernel<WM, WN, GM, 0>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+    case 1: hipLaunchKernelGGL((fused_kernel<WM, WN, GM, 1>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+    case 2: hipLaunchKernelGGL((fused_kernel<WM, WN, GM, 2>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+    default: hipLaunchKernelGGL((fused_kernel<WM, WN, GM, 3>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+  }
   return hipGetLastError();
 }
 
 // Allow the kernel its dynamic LDS (above the 64 KB default) and report how
 // many workgroups fit on one CU; done once, at create time.
-template <int WM, int WN, int GM>
-int prepare_fused_t(const FusedParams& p) {
-  const void* fn = reinterpret_cast<const void*>(fused_kernel<WM, WN, GM>);
+template <int WM, int WN, int GM, int MODE>
+int prepare_fused_e(const FusedParams& p) {
+  const void* fn = reinterpret_cast<const void*>(fused_kernel<WM, WN, GM, MODE>);
   if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, p.lds_bytes) != hipSuccess) return 0;
   int blocks = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, fused_kernel<WM, WN, GM>, kThreads, p.lds_bytes) !=
-      hipSuccess)
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, fused_kernel<WM, WN, GM, MODE>, kThreads,
+                                                   p.lds_bytes) != hipSuccess)
     return 0;
   return blocks;
+}
+
+// Every mode a layer may launch (plain or chained steps, with or without
+// emission) gets its LDS attribute; the occupancy reported is the plain one.
+template <int WM, int WN, int GM>
+int prepare_fused_t(const FusedParams& p) {
+  const int e = p.emit ? 1 : 0;
+  const int a = prepare_fused_e<WM, WN, GM, 0>(p);
+  const int b = prepare_fused_e<WM, WN, GM, 2>(p);
+  const int c = e ? std::min(prepare_fused_e<WM, WN, GM, 1>(p), prepare_fused_e<WM, WN, GM, 3>(p)) : a;
+  return std::min(std::min(a, b), c);
 }
 
 }  // namespace
