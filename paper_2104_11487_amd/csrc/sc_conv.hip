@@ -156,6 +156,7 @@ __global__ void __launch_bounds__(kConvThreads) conv_bf16_kernel(ConvParams p) {
   const int r16 = lane & 15, kq = lane >> 4;
   const int bb = p.block * p.block;
   const long total_rows = (long)p.counters[kCtrCount] * bb;
+  if (p.zero_ctr && blockIdx.x == 0 && threadIdx.x == 0) *p.zero_ctr = 0u;  // next step's work list
   const int ntiles = (int)((total_rows + kRowsPerTile - 1) / kRowsPerTile);
   const uint16_t* xt = static_cast<const uint16_t*>(p.x_t);
   const uint16_t* xp = static_cast<const uint16_t*>(p.x_prev);
@@ -228,6 +229,7 @@ conv_halo_kernel(ConvParams p, HaloParams hp) {
   const int lb = __ffs(b) - 1;
   const int tpb = hp.tiles_per_block;
   const int ntiles = (int)p.counters[kCtrCount] * tpb;
+  if (p.zero_ctr && blockIdx.x == 0 && threadIdx.x == 0) *p.zero_ctr = 0u;  // next step's work list
   const uint16_t* xt = static_cast<const uint16_t*>(p.x_t);
   const uint16_t* xp = static_cast<const uint16_t*>(p.x_prev);
   // packed weights through a buffer resource: lane offset in a VGPR, the
@@ -416,6 +418,7 @@ __global__ void __launch_bounds__(kConvThreads) conv_f32_kernel(ConvParams p) {
   const int r16 = lane & 15, kq = lane >> 4;
   const int bb = p.block * p.block;
   const long total_rows = (long)p.counters[kCtrCount] * bb;
+  if (p.zero_ctr && blockIdx.x == 0 && threadIdx.x == 0) *p.zero_ctr = 0u;  // next step's work list
   const int ntiles = (int)((total_rows + kRowsPerTile - 1) / kRowsPerTile);
   const float* xt = static_cast<const float*>(p.x_t);
   const float* xp = static_cast<const float*>(p.x_prev);
@@ -473,6 +476,7 @@ template <typename T, int VEC>
 __global__ void __launch_bounds__(kConvThreads) depthwise_kernel(ConvParams p) {
   const int bb = p.block * p.block;
   const long total_rows = (long)p.counters[kCtrCount] * bb;
+  if (p.zero_ctr && blockIdx.x == 0 && threadIdx.x == 0) *p.zero_ctr = 0u;  // next step's work list
   const int ntiles = (int)((total_rows + kRowsPerTile - 1) / kRowsPerTile);
   const T* xt = static_cast<const T*>(p.x_t);
   const T* xp = static_cast<const T*>(p.x_prev);

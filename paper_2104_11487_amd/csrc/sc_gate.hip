@@ -355,6 +355,29 @@ __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
     const int by = i / nblk_x, bx = i - by * nblk_x;
     p.block_mask[((size_t)n * p.hb + bi0 + by) * p.wb + bj0 + bx] = (uint8_t)blk_flag[by * tb_w + bx];
   }
+  if (p.wlist) {
+    // append the tile's active blocks to the (unordered) work list of the
+    // convolution: one thread per block (<= 256), wave ballots, one atomic
+    __shared__ uint32_t wave_cnt[kGateThreads / 64];
+    __shared__ uint32_t wl_base;
+    const int i = threadIdx.x, lane = i & 63, wv = i >> 6;
+    const int by = i / nblk_x, bx = i - by * nblk_x;
+    const bool act = i < nblk_y * nblk_x && blk_flag[by * tb_w + bx] != 0u;
+    const unsigned long long m = __ballot(act);
+    if (lane == 0) wave_cnt[wv] = (uint32_t)__popcll(m);
+    __syncthreads();
+    if (i == 0) {
+      uint32_t tot = 0;
+      for (int w = 0; w < kGateThreads / 64; ++w) tot += wave_cnt[w];
+      wl_base = tot ? atomicAdd(p.wctr, tot) : 0u;
+    }
+    __syncthreads();
+    if (act) {
+      uint32_t off = wl_base + (uint32_t)__popcll(m & ((1ull << lane) - 1ull));
+      for (int w = 0; w < wv; ++w) off += wave_cnt[w];
+      p.wlist[off] = (uint32_t)(((size_t)n * p.hb + bi0 + by) * p.wb + bj0 + bx);
+    }
+  }
 }
 
 // Ordered compaction (one workgroup of kScanThreads): each thread takes a

@@ -9,6 +9,7 @@ namespace sc {
 // counters[] slots in the workspace
 constexpr int kCtrCount = 0;  // active blocks of the last gate pass
 constexpr int kCtrSpare = 1;
+constexpr int kCtrWork = 4;   // kCtrWork + 0/1: counts of the two alternating work lists
 constexpr int kNumCounters = 16;
 
 constexpr int kMaxTileBlocks = 256;  // blocks per gate tile: (ts / b)^2 <= 256
@@ -47,6 +48,10 @@ struct GateParams {
   int up_block, up_hb, up_wb;
   int rin;                      // fused kernel: x_t is an fp32 residual (no x_{t-1})
   int sy, sx;                   // translation of the content since x_{t-1} (split gate only)
+  // unordered work list of the convolution (blocks appended per tile), its
+  // count (zero on entry); NULL when the ordered compaction builds the list
+  uint32_t* wlist;
+  uint32_t* wctr;
 };
 
 // Sparse convolution over the active sites (dense groups = 1).
@@ -66,6 +71,7 @@ struct ConvParams {
   int no_prev;                  // x_{t-1} taken as 0 (reference frames; residual inputs)
   int act;                      // 0 none, 1 identity, 2 relu
   int sy, sx;                   // translation of the content since x_{t-1} (input pixels; 0 = none)
+  uint32_t* zero_ctr;           // a work-list counter to clear for the next step (or NULL)
 };
 
 // Element offset of x_{t-1} under the step's translation at input pixel
@@ -157,6 +163,8 @@ hipError_t launch_split_list(const uint32_t* list, const uint32_t* counters, uin
                              uint32_t* counters_a, uint32_t* list_b, uint32_t* counters_b, int hb, int wb,
                              int block, int h_out, int w_out, int h, int w, int k, int stride, int pad, int sy,
                              int sx, hipStream_t st);
+
+hipError_t launch_fill_u32(uint32_t* p, int n, uint32_t v, hipStream_t st);
 
 // One-time weight repacks (create time).
 hipError_t launch_pack_mfma(const void* w, void* out, int dtype, int c_out, int c_in, int k,

@@ -54,7 +54,7 @@ struct Geometry {
   int vec;              // gate load width (elements)
   size_t elem;
   size_t off_wpack, off_slot0, off_slot1, off_z, off_y, off_bmask, off_tflag, off_list, off_ctr,
-      off_stat, off_smask, off_phi, off_r32, off_rb, off_prev, off_z2, off_list_a, off_list_b, total;
+      off_stat, off_smask, off_phi, off_r32, off_rb, off_prev, off_z2, off_list_a, off_list_b, off_wlist, total;
   int learned;          // learned gate: its kernel size (the layer's k), else 0
   bool phi_in_lds;      // learned gate: phi staged in LDS (else read through the caches)
   int phi_off;          // learned gate: LDS float offset of the staged phi
@@ -309,6 +309,7 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
   G.off_bmask = off; off = align_up(off + (size_t)nb + 16);  // zero padding to whole 16-byte words
   G.off_tflag = off; off = align_up(off + (size_t)G.gate_grid);
   G.off_list = off; off = align_up(off + (size_t)nb * 4);
+  G.off_wlist = off; off = align_up(off + (size_t)nb * 4);  // unordered work list of the split pipeline
   G.off_ctr = off; off = align_up(off + sc::kNumCounters * 4);
   G.off_stat = off;
   G.off_smask = off;
@@ -378,6 +379,12 @@ struct skipconv_layer {
   uint16_t* rb() { return reinterpret_cast<uint16_t*>(ws + g.off_rb); }
   uint8_t* prev_mask() { return reinterpret_cast<uint8_t*>(ws + g.off_prev); }
   bool phi_set = false;      // learned gate: skipconv_set_gate_weights was called
+  // split pipeline work list: the gate appends active blocks (unordered) and
+  // counts them in counter kCtrWork + wslot; the convolution clears the other
+  // counter for the next step. wclean: that counter is known to be zero.
+  int wslot = 0;
+  bool wclean[2] = {true, true};
+  uint32_t* wlist() { return reinterpret_cast<uint32_t*>(ws + g.off_wlist); }
   float gate_bias = 0.0f;
 };
 
@@ -505,6 +512,49 @@ hipError_t launch_compaction(skipconv_layer* h, hipStream_t st) {
   return sc::launch_compact(h->bmask(), g.nb, h->list(), h->ctr(), g.split_blocks ? h->tflags() : nullptr,
                             h->d.n, g.hb, g.wb, g.split_blocks ? h->d.block / g.ts : 0, g.tiles_y, g.tiles_x,
                             st);
+}
+
+// The list the split pipeline's convolution walks this step. Layers whose
+// blocks are larger than the gate tiles need the ordered compaction (block
+// flags are OR-ed over tiles first); every other layer takes the work list
+// the gate kernel appends to, with no compaction launch.
+struct StepList {
+  const uint32_t* list;
+  uint32_t* counters;  // counters[kCtrCount] = number of blocks in `list`
+  uint32_t* zero;      // counter the convolution clears for the next step
+};
+
+hipError_t begin_list(skipconv_layer* h, sc::GateParams& gp, hipStream_t st, StepList* out) {
+  if (h->g.split_blocks) {
+    *out = StepList{h->list(), h->ctr(), nullptr};
+    return hipSuccess;
+  }
+  const int slot = h->wslot;
+  uint32_t* c = h->ctr() + sc::kCtrWork + slot;
+  hipError_t e = hipSuccess;
+  if (!h->wclean[slot]) e = sc::launch_fill_u32(c, 1, 0u, st);
+  gp.wlist = h->wlist();
+  gp.wctr = c;
+  *out = StepList{h->wlist(), c, h->ctr() + sc::kCtrWork + (slot ^ 1)};
+  return e;
+}
+
+// After the gate: the ordered compaction when needed; called once per step.
+hipError_t gate_done(skipconv_layer* h, hipStream_t st) {
+  if (h->g.split_blocks) {
+    h->list_valid = true;
+    return launch_compaction(h, st);
+  }
+  h->list_valid = false;  // the ordered list is built on demand for introspection
+  return hipSuccess;
+}
+
+// After the convolution that cleared the other counter.
+void end_list(skipconv_layer* h) {
+  if (h->g.split_blocks) return;
+  h->wclean[h->wslot ^ 1] = true;
+  h->wclean[h->wslot] = false;
+  h->wslot ^= 1;
 }
 
 int conv_grid(const skipconv_layer* h) {
@@ -662,7 +712,7 @@ int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t
   const Geometry& g = h->g;
   const bool ref = h->ref_pending;
 
-  const sc::GateParams gp = gate_params(h, x_t, ref);
+  sc::GateParams gp = gate_params(h, x_t, ref);
 
   sc::ConvParams cp{};
   cp.x_t = x_t;
@@ -670,8 +720,6 @@ int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t
   cp.wpack = h->wpack();
   cp.z = h->z();
   cp.y = h->y();
-  cp.list = h->list();
-  cp.counters = h->ctr();
   cp.n = d.n; cp.h = d.h; cp.w = d.w; cp.c = d.c_in; cp.c_out = d.c_out;
   cp.h_out = g.h_out; cp.w_out = g.w_out; cp.k = d.kernel; cp.stride = d.stride; cp.pad = g.pad;
   cp.block = d.block; cp.hb = g.hb; cp.wb = g.wb;
@@ -693,10 +741,15 @@ int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t
     if (timing) e = hipEventRecord(h->ev[3 * h->timing_done + 1], st);
     h->list_valid = false;
   } else {
+    StepList sl{};
+    if (e == hipSuccess) e = begin_list(h, gp, st, &sl);
     if (e == hipSuccess) e = sc::launch_gate(gp, d.dtype, g.vec, g.gate_grid, g.gate_lds, st);
-    if (e == hipSuccess) e = launch_compaction(h, st);
+    if (e == hipSuccess) e = gate_done(h, st);
     if (e != hipSuccess) return hip_fail(h, e, "gate launch");
     if (timing) e = hipEventRecord(h->ev[3 * h->timing_done + 1], st);
+    cp.list = sl.list;
+    cp.counters = sl.counters;
+    cp.zero_ctr = sl.zero;
     if (e == hipSuccess) {
       if (g.depthwise)
         e = sc::launch_depthwise(cp, d.dtype, conv_grid(h), st);
@@ -706,7 +759,7 @@ int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t
         e = sc::launch_conv(cp, d.dtype, g.fast, conv_grid(h), st);
     }
     if (e != hipSuccess) return hip_fail(h, e, "conv launch");
-    h->list_valid = true;
+    end_list(h);
   }
   if (h->emits() && !g.fused) {  // the fused kernel emits in its epilogue
     e = launch_emit(h, st);
@@ -751,14 +804,16 @@ int skipconv_step_translated(skipconv_t h, const void* x_t, int32_t dy, int32_t 
   sc::GateParams gp = gate_params(h, x_t, false);
   gp.sy = dy;
   gp.sx = dx;
-  e = sc::launch_gate(gp, d.dtype, g.vec, g.gate_grid, g.gate_lds, st);
-  if (e == hipSuccess) e = launch_compaction(h, st);
+  StepList sl{};
+  e = begin_list(h, gp, st, &sl);
+  if (e == hipSuccess) e = sc::launch_gate(gp, d.dtype, g.vec, g.gate_grid, g.gate_lds, st);
+  if (e == hipSuccess) e = gate_done(h, st);
   // 3. active blocks: translated recurrence (list a) or recomputed from x_t (list b)
   uint32_t* ctr = h->ctr();
   uint32_t* list_a = reinterpret_cast<uint32_t*>(h->ws + g.off_list_a);
   uint32_t* list_b = reinterpret_cast<uint32_t*>(h->ws + g.off_list_b);
   if (e == hipSuccess)
-    e = sc::launch_split_list(h->list(), ctr, list_a, ctr + 2, list_b, ctr + 3, g.hb, g.wb, d.block, g.h_out,
+    e = sc::launch_split_list(sl.list, sl.counters, list_a, ctr + 2, list_b, ctr + 3, g.hb, g.wb, d.block, g.h_out,
                               g.w_out, d.h, d.w, d.kernel, d.stride, g.pad, dy, dx, st);
   if (e != hipSuccess) return hip_fail(h, e, "translated gate launch");
   sc::ConvParams cp{};
@@ -775,6 +830,7 @@ int skipconv_step_translated(skipconv_t h, const void* x_t, int32_t dy, int32_t 
   for (int pass = 0; pass < 2 && e == hipSuccess; ++pass) {
     cp.list = pass ? list_b : list_a;
     cp.counters = ctr + 2 + pass;
+    cp.zero_ctr = pass ? nullptr : sl.zero;
     cp.reference = pass;  // exposed blocks: assigned from x_t
     cp.no_prev = pass;
     cp.sy = pass ? 0 : dy;
@@ -787,7 +843,7 @@ int skipconv_step_translated(skipconv_t h, const void* x_t, int32_t dy, int32_t 
       e = sc::launch_conv(cp, d.dtype, g.fast, conv_grid(h), st);
   }
   if (e != hipSuccess) return hip_fail(h, e, "translated conv launch");
-  h->list_valid = true;
+  end_list(h);
   h->cur ^= 1;
   h->ref_pending = false;
   ++h->frames;
@@ -844,8 +900,10 @@ int skipconv_step_chained(skipconv_t h, skipconv_t up, void* stream, const float
     gp.up_hb = up->g.hb;
     gp.up_wb = up->g.wb;
   }
-  hipError_t e = sc::launch_gate(gp, SKIPCONV_F32, d.c_in % 8 == 0 ? 8 : 1, g.gate_grid, g.gate_lds, st);
-  if (e == hipSuccess) e = launch_compaction(h, st);
+  StepList sl{};
+  hipError_t e = begin_list(h, gp, st, &sl);
+  if (e == hipSuccess) e = sc::launch_gate(gp, SKIPCONV_F32, d.c_in % 8 == 0 ? 8 : 1, g.gate_grid, g.gate_lds, st);
+  if (e == hipSuccess) e = gate_done(h, st);
   if (e != hipSuccess) return hip_fail(h, e, "chained gate launch");
   // convolution of the residual operand (bf16-rounded for bf16 layers), accumulated into z
   sc::ConvParams cp{};
@@ -854,8 +912,9 @@ int skipconv_step_chained(skipconv_t h, skipconv_t up, void* stream, const float
   cp.wpack = h->wpack();
   cp.z = h->z();
   cp.y = h->y();
-  cp.list = h->list();
-  cp.counters = h->ctr();
+  cp.list = sl.list;
+  cp.counters = sl.counters;
+  cp.zero_ctr = sl.zero;
   cp.n = d.n; cp.h = d.h; cp.w = d.w; cp.c = d.c_in; cp.c_out = d.c_out;
   cp.h_out = g.h_out; cp.w_out = g.w_out; cp.k = d.kernel; cp.stride = d.stride; cp.pad = g.pad;
   cp.block = d.block; cp.hb = g.hb; cp.wb = g.wb;
@@ -874,7 +933,7 @@ int skipconv_step_chained(skipconv_t h, skipconv_t up, void* stream, const float
     e = launch_emit(h, st);
     if (e != hipSuccess) return hip_fail(h, e, "emit launch");
   }
-  h->list_valid = true;
+  end_list(h);
   h->ref_pending = false;
   ++h->frames;
   if (z_t) *z_t = h->z();

@@ -79,7 +79,18 @@ split_list_kernel(const uint32_t* list, const uint32_t* counters, uint32_t* list
   }
 }
 
+__global__ void fill_u32_kernel(uint32_t* p, int n, uint32_t v) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
 }  // namespace
+
+// A kernel rather than hipMemsetAsync, so that the step stays capturable in a graph.
+hipError_t launch_fill_u32(uint32_t* p, int n, uint32_t v, hipStream_t st) {
+  hipLaunchKernelGGL(fill_u32_kernel, dim3((n + 255) / 256), dim3(256), 0, st, p, n, v);
+  return hipGetLastError();
+}
 
 hipError_t launch_translate_state(const float* z_src, float* z_dst, void* y, int n, int h_out, int w_out,
                                   int c_out, int dyo, int dxo, int act, int dtype, hipStream_t st) {
