@@ -2,34 +2,38 @@
 // C_in % 32 == 0): one workgroup per TS x TS tile of output sites made of
 // whole gate blocks, doing every step of Eq. 3 for its tile in one launch:
 //
-//   1. weights: chunks of the packed weights are copied into LDS with
-//      asynchronous global_load_lds at kernel start, so the copy overlaps the
-//      halo and gate work (whose barriers wait on LDS traffic only);
-//   2. halo: every thread takes 8-channel chunks of the tile's halo pixels
+//   1. halo: every thread takes 8-channel chunks of the tile's halo pixels
 //      (16-byte loads of x_t and x_{t-1}, several in flight), forms
 //      r = x_t - x_{t-1} in fp32 (Eq. 2) and the chunk's statistic sum in the
 //      canonical order (channels ascending, one rounding per multiply and per
-//      add), parks the sum in LDS, writes rho = bf16_rne(r) to an LDS halo kept
-//      for the product, and copies owned pixels of x_t into the spare x_{t-1}
-//      slot; then one thread per pixel adds its chunk sums in ascending order;
-//   3. gate (Eq. 5): support sums over taps in row-major order, exact fp64
+//      add), writes rho = bf16_rne(r) to an LDS halo kept for the product, and
+//      copies owned pixels of x_t into the spare x_{t-1} slot; the chunk sums
+//      of a pixel are then added in ascending chunk order (across lanes, or
+//      through LDS);
+//   2. gate (Eq. 5): support sums over taps in row-major order, exact fp64
 //      threshold, block OR (Sec. 3.2.2); block flags go to global memory;
-//   4. product rows: for tiles of up to 8 x 8 sites the rows are all sites
-//      of the tile (one 16-row MFMA tile per wave) and the gate only decides
-//      which rows are stored; for larger tiles the active sites are compacted
-//      in row-major order (wave ballot + workgroup prefix) and become the
-//      rows; the old z of the stored rows is fetched before the product so
-//      its latency overlaps it;
-//   5. MFMA product over the rows (Sec. 4.2: im2col restricted to the
-//      non-sparse columns, never materialised: A fragments are read from the
-//      LDS halo at each row's pixel + tap offset; rows past the last one read
-//      a zero pixel);
-//   6. epilogue: z (+)= U at the active sites, activation output refreshed
-//      (the product is formed transposed, weights as the MFMA A operand, so a
-//      lane holds 4 consecutive output channels and z moves in 16-byte pieces).
+//      tiles with no active block stop here, so the hardware dispatcher
+//      balances the work;
+//   3. MFMA product (Sec. 4.2: im2col restricted to the non-sparse columns,
+//      never materialised: operand fragments are read from the LDS halo at
+//      each row's pixel + tap offset; rows past the last one read a zero
+//      pixel), formed transposed (weights as the MFMA A operand) so that a
+//      lane holds 4 consecutive output channels of one site;
+//   4. epilogue: z (+)= U at the active sites, activation output refreshed.
 //
-// Inactive tiles stop after step 3, so the hardware dispatcher balances the
-// work. The ordered global active list is not needed by this pipeline; it is
+// Two kernels share steps 1-2:
+//   * fused_rb_kernel (tiles of <= 8 x 8 sites): wave (ng, kp) owns two
+//     16-column tiles of the output and one part of the k-steps; its weight
+//     fragments go straight from global memory into registers (issued during
+//     the gate), so LDS carries only the residual operand; the k-partial sums
+//     meet in LDS and all waves finish the epilogue. The old z of every site
+//     is fetched with the halo, so no load waits between gate and product.
+//   * fused_kernel (16 x 16 tiles and shapes the first does not cover): the
+//     packed weights are copied into LDS with global_load_lds by two loader
+//     waves during the halo phase; 16 x 16 tiles compact their active sites
+//     (ballot + prefix) into the product rows.
+//
+// The ordered global active list is not needed by this pipeline; it is
 // produced on demand for introspection by the compaction kernel.
 #include "sc_device.h"
 #include "sc_kernels.h"
@@ -43,6 +47,8 @@ namespace {
 
 constexpr int kThreads = 512;
 constexpr int kWaves = kThreads / 64;
+constexpr int kLoadWaves = 2;  // fused_kernel: waves that copy the weights during the halo phase
+constexpr int kItems = 4;      // halo items per thread whose loads are in flight together
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float floatx2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -102,23 +108,573 @@ __device__ void emit_clear(const FusedParams& p, int n, int oy0, int ox0, int oh
   }
 }
 
+// Value of lane (this lane + J) of the same 16-lane row (DPP row_shl:J).
+template <int J>
+__device__ __forceinline__ float row_shl(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x100 + J, 0xf, 0xf, false));
+}
+
+template <int NC, int J>
+__device__ __forceinline__ float group_sum_from(float acc, float v) {
+  if constexpr (J < NC) {
+    return group_sum_from<NC, J + 1>(add_rn(acc, row_shl<J>(v)), v);
+  } else {
+    return acc;
+  }
+}
+
+// Ordered sum (from +0, ascending lanes) of the NC values held by lanes
+// l .. l + NC - 1 of one 16-lane row, valid in lane l (NC <= 16; the group
+// must not cross a row boundary). Lane-to-lane moves only, no LDS traffic.
+template <int NC>
+__device__ __forceinline__ float group_sum(float v) {
+  return group_sum_from<NC, 1>(add_rn(0.0f, v), v);
+}
+
 // Workgroup barrier that orders LDS accesses only: outstanding global loads
-// and stores (the weight copy, the z prefetch, the x_t copy) stay in flight.
+// and stores (register loads, the z prefetch, the x_t copy) stay in flight.
+// (A global_load_lds still in flight makes the compiler wait for it here.)
 __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
   __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-// Wave layout of the product: GM waves along M (WM 16-row tiles each) by 2
-// along N (WN 16-column tiles each); waves past the first 2 * GM do no MFMA.
-// MODE bit 0: emit the successor's residual; bit 1: chained input (x_t is the
-// upstream layer's fp32 residual, tiles without upstream blocks exit early).
+// Geometry of one tile of output sites and of its input halo. The halo has
+// the extent of a whole tile even for edge tiles (the extra pixels are out of
+// the frame or read by no site), so its layout is the same for every tile.
+struct Tile {
+  int n, oy0, ox0, oh, ow;          // image, first output row / column, tile extent
+  int iy0, ix0, hh, hw, npix;       // halo origin (input pixels) and extent
+  int own_y0, own_x0, own_y1, own_x1;  // input pixels whose x_t copy this tile writes
+  int tb_w;                         // blocks per tile row
+  float inv_ts, inv_blk, inv_hw;    // reciprocals for qdiv (computed on the host)
+};
+
+// The tile of this workgroup, from the table built at create time.
+__device__ __forceinline__ Tile make_tile(const FusedParams& p) {
+  const GateParams& g = p.g;
+  Tile T;
+  const uint32_t tc = p.tiles[blockIdx.x];
+  const int tx = (int)(tc & 1023u), ty = (int)((tc >> 10) & 1023u);
+  T.n = (int)(tc >> 20);
+  const int s = g.stride, k = g.k;
+  T.oy0 = ty * g.ts;
+  T.ox0 = tx * g.ts;
+  T.oh = min(g.ts, g.h_out - T.oy0);
+  T.ow = min(g.ts, g.w_out - T.ox0);
+  T.iy0 = T.oy0 * s - g.pad;
+  T.ix0 = T.ox0 * s - g.pad;
+  T.hh = (g.ts - 1) * s + k;
+  T.hw = T.hh;
+  T.npix = T.hh * T.hw;
+  T.own_y0 = T.oy0 * s;
+  T.own_x0 = T.ox0 * s;
+  T.own_y1 = (ty == g.tiles_y - 1) ? g.h : min(g.h, (T.oy0 + g.ts) * s);
+  T.own_x1 = (tx == g.tiles_x - 1) ? g.w : min(g.w, (T.ox0 + g.ts) * s);
+  T.tb_w = g.ts / g.block;
+  T.inv_ts = p.inv_ts;
+  T.inv_blk = p.inv_blk;
+  T.inv_hw = p.inv_hw;
+  return T;
+}
+
+__global__ void fused_tiles_kernel(uint32_t* table, int grid, int tiles_y, int tiles_x) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= grid) return;
+  const int tile = xcd_tile(b, grid);
+  const int per_img = tiles_y * tiles_x;
+  const int n = tile / per_img, rem = tile - n * per_img;
+  const int ty = rem / tiles_x, tx = rem - ty * tiles_x;
+  table[b] = (uint32_t)tx | ((uint32_t)ty << 10) | ((uint32_t)n << 20);
+}
+
+// Chained input: the residual is zero outside the upstream layer's active
+// blocks; a tile whose input region meets none of them has every gate off and
+// stops before any load (norm gates only). Returns true when the tile stops.
+template <bool EMIT>
+__device__ bool chain_skip(const FusedParams& p, const Tile& T, uint8_t* emit_clr) {
+  const GateParams& g = p.g;
+  const int thh = (T.oh - 1) * g.stride + g.k, thw = (T.ow - 1) * g.stride + g.k;  // the tile's own halo
+  const int y0 = max(T.iy0, 0), y1 = min(T.iy0 + thh, g.h), x0 = max(T.ix0, 0), x1 = min(T.ix0 + thw, g.w);
+  const int by0 = y0 / g.up_block, by1 = (y1 - 1) / g.up_block;
+  const int bx0 = x0 / g.up_block, bx1 = (x1 - 1) / g.up_block;
+  const int nbx = bx1 - bx0 + 1, cnt = (by1 - by0 + 1) * nbx;
+  int any = 0;
+  for (int i = threadIdx.x; i < cnt; i += kThreads) {
+    const int by = by0 + i / nbx, bx = bx0 + i % nbx;
+    any |= g.up_mask[((size_t)T.n * g.up_hb + by) * g.up_wb + bx] != 0;
+  }
+  if (__syncthreads_or(any)) return false;
+  if (g.keep_stats)
+    for (int q = threadIdx.x; q < T.oh * T.ow; q += kThreads) {
+      const int ly = q / T.ow, lx = q - ly * T.ow;
+      const size_t o = ((size_t)T.n * g.h_out + T.oy0 + ly) * g.w_out + T.ox0 + lx;
+      g.stat[o] = 0.0f;
+      g.site_mask[o] = 0;
+    }
+  const int nby = (T.oh + g.block - 1) / g.block, nbx2 = (T.ow + g.block - 1) / g.block;
+  const int bi0 = T.oy0 / g.block, bj0 = T.ox0 / g.block;
+  for (int i = threadIdx.x; i < nby * nbx2; i += kThreads) {
+    const int by = i / nbx2, bx = i - by * nbx2;
+    g.block_mask[((size_t)T.n * g.hb + bi0 + by) * g.wb + bj0 + bx] = 0;
+  }
+  if (EMIT) emit_clear(p, T.n, T.oy0, T.ox0, T.oh, T.ow, T.tb_w, nullptr, emit_clr);
+  return true;
+}
+
+// Split of a halo item index (pixel, 8-channel chunk).
+struct ChunkMap {
+  int nchk, total, lg;  // chunks per pixel, items in the halo, log2(nchk) or -1
+  float inv;            // 1 / nchk
+  bool lane_sum;        // a pixel's chunks sit in one aligned group of <= 16 lanes
+};
+
+__device__ __forceinline__ ChunkMap make_chunks(const FusedParams& p, const Tile& T) {
+  ChunkMap m;
+  m.nchk = p.g.c >> 3;
+  m.total = T.npix * m.nchk;
+  m.lg = (m.nchk & (m.nchk - 1)) == 0 ? __builtin_ctz(m.nchk) : -1;
+  m.inv = p.inv_chk;
+  m.lane_sum = m.nchk == 4 || m.nchk == 8 || m.nchk == 16;
+  return m;
+}
+
+// Per-thread walk over the halo items (pixel, 8-channel chunk). With
+// rw = hw * nchk items per halo row and rg = NTHR / rw >= 1 row groups, thread
+// t keeps one column item c = t % rw (pixel column c / nchk, chunk c % nchk)
+// and takes rows r0 + j * rg, r0 = t / rw, so item j costs one add (threads
+// t >= rg * rw take none); consecutive threads take consecutive chunks of a
+// row, so a wave's loads are contiguous and a pixel's chunks sit in one
+// aligned lane group. Rows longer than the thread count use the flat order
+// (item base + u * NTHR + t).
+struct HaloWalk {
+  bool twod;
+  int r0, rg, hx, ch, rows;   // 2-D walk; rows = items per thread (ceil(hh / rg))
+  bool xin, xown;             // column in the frame / in the owned range
+  long off0, ostep;           // frame element offset of item 0 (if in frame), step per item
+  int px0, pxstep;            // halo pixel of item 0, step per item
+};
+
+// TWOD: the caller guarantees rw <= NTHR (the 2-D walk is compiled alone).
+template <int NTHR, bool TWOD>
+__device__ __forceinline__ HaloWalk make_walk(const GateParams& g, const Tile& T, const ChunkMap& cm, int tid) {
+  HaloWalk W;
+  const int rw = T.hw * cm.nchk;
+  W.rg = NTHR / rw;
+  W.twod = TWOD || W.rg > 0;
+  if (!W.twod) return W;
+  const int c = tid - (tid / rw) * rw;  // division by a wave-uniform value, once per thread
+  W.r0 = tid / rw;
+  W.hx = cm.lg >= 0 ? c >> cm.lg : qdiv(c, cm.inv);
+  W.ch = c - W.hx * cm.nchk;
+  W.rows = W.r0 < W.rg ? (T.hh + W.rg - 1) / W.rg : 0;
+  const int x = T.ix0 + W.hx;
+  W.xin = x >= 0 && x < g.w;
+  W.xown = W.xin && g.x_keep != nullptr && g.copy_in_halo && x >= T.own_x0 && x < T.own_x1;
+  W.off0 = ((long)(T.n * g.h + T.iy0 + W.r0) * g.w + x) * g.c + W.ch * 8;
+  W.ostep = (long)W.rg * g.w * g.c;
+  W.px0 = W.r0 * T.hw + W.hx;
+  W.pxstep = W.rg * T.hw;
+  return W;
+}
+
+// One round of halo items: kItems items per thread (2-D walk: items
+// base + u of the thread's column; flat order: item base + u * NTHR + tid).
+struct HaloBatch {
+  uint4 vt[kItems], vp[kItems];
+  size_t off[kItems];
+  int px[kItems], ch[kItems];
+  bool in[kItems], own[kItems];
+};
+
+// Rounds of kItems items a workgroup's halo takes.
+template <int NTHR, bool TWOD>
+__device__ __forceinline__ int halo_rounds(const Tile& T, const ChunkMap& cm, const HaloWalk& W) {
+  const int per = (TWOD || W.twod) ? (T.hh + W.rg - 1) / W.rg : (cm.total + NTHR - 1) / NTHR;
+  return (per + kItems - 1) / kItems;
+}
+
+// Issue the loads of round `rd`. Addresses are clamped in bounds so that every
+// load is issued (the wait counts stay static); out-of-frame items are zeroed
+// when used.
+template <bool CHAIN, int NTHR, bool TWOD>
+__device__ __forceinline__ void halo_load(const GateParams& g, const Tile& T, const ChunkMap& cm,
+                                          const HaloWalk& W, int rd, int tid, HaloBatch& B) {
+  const uint16_t* xt = static_cast<const uint16_t*>(g.x_t);
+  const uint16_t* xp = static_cast<const uint16_t*>(g.no_prev ? g.x_t : g.x_prev);
+  const bool keep = g.x_keep != nullptr && g.copy_in_halo;
+#pragma unroll
+  for (int u = 0; u < kItems; ++u) {
+    if (TWOD || W.twod) {
+      const int j = rd * kItems + u;
+      const int hy = W.r0 + j * W.rg;
+      const int y = T.iy0 + hy;
+      const bool valid = j < W.rows && hy < T.hh;
+      B.px[u] = valid ? W.px0 + j * W.pxstep : -1;
+      B.ch[u] = W.ch;
+      B.in[u] = valid && W.xin && y >= 0 && y < g.h;
+      B.own[u] = B.in[u] && W.xown && y >= T.own_y0 && y < T.own_y1;
+      B.off[u] = B.in[u] ? (size_t)(W.off0 + j * W.ostep) : 0;
+    } else {
+      const int idx = rd * kItems * NTHR + u * NTHR + tid;
+      const int q = cm.lg >= 0 ? idx >> cm.lg : qdiv(idx, cm.inv);
+      B.px[u] = idx < cm.total ? q : -1;
+      B.ch[u] = idx - q * cm.nchk;
+      const int hy = qdiv(q, T.inv_hw), hx = q - hy * T.hw;
+      const int y = T.iy0 + hy, x = T.ix0 + hx;
+      B.in[u] = B.px[u] >= 0 && y >= 0 && y < g.h && x >= 0 && x < g.w;
+      B.own[u] = B.in[u] && keep && y >= T.own_y0 && y < T.own_y1 && x >= T.own_x0 && x < T.own_x1;
+      B.off[u] = B.in[u] ? (size_t)((T.n * g.h + y) * g.w + x) * g.c + B.ch[u] * 8 : 0;
+    }
+    if (CHAIN) {  // fp32 residual input: channels 0-3 in vt, 4-7 in vp
+      const float* rr = static_cast<const float*>(g.x_t) + B.off[u];
+      B.vt[u] = *reinterpret_cast<const uint4*>(rr);
+      B.vp[u] = *reinterpret_cast<const uint4*>(rr + 4);
+    } else {
+      B.vt[u] = *reinterpret_cast<const uint4*>(xt + B.off[u]);
+      B.vp[u] = *reinterpret_cast<const uint4*>(xp + B.off[u]);
+    }
+  }
+}
+
+// Use one round: r in fp32, the chunk's statistic sum in canonical order (one
+// rounding per multiply and per add) and rho = bf16_rne(r) into the LDS halo;
+// the pixel's chunk sums are added in ascending order by the group's first
+// lane through DPP row shifts (lane_sum), or parked in LDS for a later
+// combine. Then the owned pixels of x_t go to the spare x_{t-1} slot.
+// `wave` is the wave's index among the NTHR threads taking items.
+template <bool CHAIN, int NTHR, bool TWOD>
+__device__ __forceinline__ void halo_use(const FusedParams& p, const Tile& T, const ChunkMap& cm,
+                                         const HaloWalk& W, int rd, int wave, HaloBatch& B, uint8_t* halo,
+                                         float* a_halo, float* part) {
+  const GateParams& g = p.g;
+#pragma unroll
+  for (int u = 0; u < kItems; ++u) {
+    // wave-uniform: no item left for any lane of the wave
+    if ((TWOD || W.twod) ? (rd * kItems + u) * W.rg >= T.hh : (rd * kItems + u) * NTHR + wave * 64 >= cm.total)
+      break;
+    if (!B.in[u]) B.vt[u] = uint4{0u, 0u, 0u, 0u};
+    if (!B.in[u] || (!CHAIN && g.no_prev)) B.vp[u] = uint4{0u, 0u, 0u, 0u};
+    const uint32_t wt[4] = {B.vt[u].x, B.vt[u].y, B.vt[u].z, B.vt[u].w};
+    const uint32_t wpv[4] = {B.vp[u].x, B.vp[u].y, B.vp[u].z, B.vp[u].w};
+    uint32_t outw[4];
+    float sum = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      // channels 2e (low half) and 2e + 1 (high half)
+      float r0, r1;
+      if (CHAIN) {
+        const uint32_t* src = e < 2 ? wt : wpv;
+        r0 = __uint_as_float(src[(2 * e) & 3]);
+        r1 = __uint_as_float(src[(2 * e + 1) & 3]);
+      } else {
+        r0 = __fsub_rn(__uint_as_float(wt[e] << 16), __uint_as_float(wpv[e] << 16));
+        r1 = __fsub_rn(__uint_as_float(wt[e] & 0xffff0000u), __uint_as_float(wpv[e] & 0xffff0000u));
+      }
+      sum = add_rn(sum, term(r0, g.norm_p));
+      sum = add_rn(sum, term(r1, g.norm_p));
+      outw[e] = pack_bf16(r0, r1);
+    }
+    // out-of-frame pixels: zero operand and zero statistic (outw, sum are 0)
+    if (B.px[u] >= 0)
+      *reinterpret_cast<u32x4*>(halo + (size_t)B.px[u] * p.pstride + B.ch[u] * 16) =
+          u32x4{outw[0], outw[1], outw[2], outw[3]};
+    if (cm.lane_sum) {
+      float acc;
+      if (cm.nchk == 8) acc = group_sum<8>(sum);
+      else if (cm.nchk == 16) acc = group_sum<16>(sum);
+      else acc = group_sum<4>(sum);
+      if (B.px[u] >= 0 && B.ch[u] == 0) a_halo[B.px[u]] = acc;
+    } else if (B.px[u] >= 0) {
+      part[B.px[u] * p.pstage + B.ch[u]] = sum;
+    }
+  }
+  uint16_t* keep = static_cast<uint16_t*>(g.x_keep);
+#pragma unroll
+  for (int u = 0; u < kItems; ++u)
+    if (B.own[u]) *reinterpret_cast<uint4*>(keep + B.off[u]) = B.vt[u];
+}
+
+// Layers whose halos do not cover the pixels a tile owns (strides above the
+// kernel size) copy them element by element.
+__device__ __forceinline__ void copy_owned(const GateParams& g, const Tile& T) {
+  if (g.copy_in_halo || !g.x_keep) return;
+  const uint16_t* xt = static_cast<const uint16_t*>(g.x_t);
+  uint16_t* keep = static_cast<uint16_t*>(g.x_keep);
+  const int ny = T.own_y1 - T.own_y0, nx = T.own_x1 - T.own_x0;
+  const int per_row = nx * g.c;
+  for (int i = threadIdx.x; i < ny * per_row; i += kThreads) {
+    const int yy = i / per_row, e = i - yy * per_row;
+    const size_t o = ((size_t)(T.n * g.h + T.own_y0 + yy) * g.w + T.own_x0) * g.c + e;
+    keep[o] = xt[o];
+  }
+}
+
+// Pixel statistics complete (combining parked chunk sums if needed), then the
+// gate of every site of the tile (Eq. 5): support sum over in-frame taps in
+// row-major order, exact fp64 threshold (times the Output-Norm weight norm),
+// NaN on, block OR into blk_flag; block flags go to global memory. Ends after
+// a barrier with blk_flag and tile_on final. All threads call it.
+__device__ void gate_tile(const FusedParams& p, const Tile& T, const ChunkMap& cm, float* a_halo,
+                          const float* part, uint32_t* blk_flag, uint32_t* tile_on) {
+  const GateParams& g = p.g;
+  const int s = g.stride, k = g.k, hw = T.hw;
+  lds_barrier();
+  if (!cm.lane_sum) {
+    for (int q = threadIdx.x; q < T.npix; q += kThreads) {
+      float acc = 0.0f;
+      for (int j = 0; j < cm.nchk; ++j) acc = add_rn(acc, part[q * p.pstage + j]);
+      a_halo[q] = acc;
+    }
+    lds_barrier();
+  }
+  for (int q = threadIdx.x; q < g.ts * g.ts; q += kThreads) {
+    const int ly = qdiv(q, T.inv_ts), lx = q - ly * g.ts;
+    if (ly >= T.oh || lx >= T.ow) continue;
+    float sv;
+    if (g.support == 0 && k == 3) {
+      const float* base = a_halo + (ly * s) * hw + lx * s;
+      float v[9];
+#pragma unroll
+      for (int i = 0; i < 9; ++i) v[i] = base[(i / 3) * hw + i % 3];
+      sv = 0.0f;
+#pragma unroll
+      for (int i = 0; i < 9; ++i) sv = add_rn(sv, v[i]);
+    } else if (g.support == 0) {
+      sv = 0.0f;
+      const float* base = a_halo + (ly * s) * hw + lx * s;
+      for (int kh = 0; kh < k; ++kh)
+        for (int kw = 0; kw < k; ++kw) sv = add_rn(sv, base[kh * hw + kw]);
+    } else {
+      sv = a_halo[(ly * s + g.pad) * hw + lx * s + g.pad];
+    }
+    const bool on = g.reference || g.force_dense || ((double)sv * g.wnorm > g.thr) || (sv != sv);
+    if (g.keep_stats) {
+      const size_t o = ((size_t)T.n * g.h_out + T.oy0 + ly) * g.w_out + T.ox0 + lx;
+      g.stat[o] = sv;
+      g.site_mask[o] = on ? 1 : 0;
+    }
+    if (on) {
+      blk_flag[qdiv(ly, T.inv_blk) * T.tb_w + qdiv(lx, T.inv_blk)] = 1u;
+      *tile_on = 1u;
+    }
+  }
+  lds_barrier();
+  const int nby = (T.oh + g.block - 1) / g.block, nbx = (T.ow + g.block - 1) / g.block;
+  const int bi0 = T.oy0 / g.block, bj0 = T.ox0 / g.block;
+  for (int i = threadIdx.x; i < nby * nbx; i += kThreads) {
+    const int by = i / nbx, bx = i - by * nbx;
+    g.block_mask[((size_t)T.n * g.hb + bi0 + by) * g.wb + bj0 + bx] = (uint8_t)blk_flag[by * T.tb_w + bx];
+  }
+}
+
+// Epilogue of one output piece (4 consecutive channels of one site): z =
+// z_{t-1} + U (assigned on a reference frame), activation output; emitting
+// layers also write r = y_new - y_old for their successor.
+template <bool EMIT>
+__device__ __forceinline__ void store_piece(const FusedParams& p, size_t o, const floatx4& u, const floatx4& zold,
+                                            const uint2& yold) {
+  floatx4 nv;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) nv[v] = p.g.reference ? u[v] : zold[v] + u[v];
+  *reinterpret_cast<floatx4*>(p.z + o) = nv;
+  if (p.act) {
+    uint32_t yb[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) yb[v] = f32_to_bf16(p.act == 2 ? fmaxf(nv[v], 0.0f) : nv[v]);
+    *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.y) + o) = uint2{yb[0] | (yb[1] << 16), yb[2] | (yb[3] << 16)};
+    if (EMIT) {
+      const uint32_t yo[4] = {yold.x & 0xffffu, yold.x >> 16, yold.y & 0xffffu, yold.y >> 16};
+      floatx4 r;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) r[v] = __fsub_rn(bf16_to_f32(yb[v]), bf16_to_f32(yo[v]));
+      *reinterpret_cast<floatx4*>(p.r32 + o) = r;
+      *reinterpret_cast<uint2*>(p.rb + o) =
+          uint2{f32_to_bf16(r[0]) | (f32_to_bf16(r[1]) << 16), f32_to_bf16(r[2]) | (f32_to_bf16(r[3]) << 16)};
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Register-operand kernel for tiles of <= 8 x 8 sites (64 product rows, 4
+// M-tiles). Wave w = kp * NG + ng owns N-tiles 2ng, 2ng + 1 and k-steps
+// [kp * ksteps / KP, (kp + 1) * ksteps / KP) (at most KPS of them). Per tile
+// LDS carries the residual fragments (each read by the NG waves of a k-part)
+// and the KP partial sums; the weights come from global memory (L2) once.
+// MODE bit 0: emit the successor's residual; bit 1: chained input.
+template <int NG, int KPS, int MODE>
+__global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
+  constexpr bool EMIT = (MODE & 1) != 0;
+  constexpr bool CHAIN = (MODE & 2) != 0;
+  constexpr int NT = 2 * NG;        // 16-column tiles of the output
+  constexpr int KP = kWaves / NG;   // k-step parts
+  constexpr int EP = NT / 2;        // epilogue pieces per thread: 64 sites x 4 NT pieces / 512
+  constexpr int PROW = NT * 64 + 16;  // LDS bytes per site row of one partial (padded)
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  __shared__ uint32_t blk_flag[kMaxTileBlocks];
+  __shared__ uint32_t tile_on;
+  __shared__ uint8_t emit_clr[kMaxTileBlocks];
+
+  const GateParams& g = p.g;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, kq = lane >> 4;
+  const Tile T = make_tile(p);
+  if (CHAIN && g.up_mask && chain_skip<EMIT>(p, T, emit_clr)) return;
+  uint8_t* pbuf = lds + p.off_b;  // partial sums [kp][site][PROW]
+  uint8_t* halo = lds + p.off_halo;
+  float* a_halo = reinterpret_cast<float*>(lds + p.off_a);
+  float* part = reinterpret_cast<float*>(lds + p.off_part);
+  const ChunkMap cm = make_chunks(p, T);
+
+  // 1. halo loads of the first round, then the old z (and y) of this thread's
+  // epilogue pieces at every site of the tile (piece e = h * 512 + thread:
+  // site e / (4 NT), channels 4 (e % (4 NT)) ..), so that no load is left
+  // between the gate and the product
+  const HaloWalk hwk = make_walk<kThreads, true>(g, T, cm, threadIdx.x);
+  HaloBatch hb;
+  halo_load<CHAIN, kThreads, true>(g, T, cm, hwk, 0, threadIdx.x, hb);
+  int esite[EP], eloc[EP], ecol[EP];
+  floatx4 zold[EP];
+  uint2 yold[EP];
+#pragma unroll
+  for (int h = 0; h < EP; ++h) {
+    const int e = h * kThreads + threadIdx.x;
+    const int site = e / (4 * NT), col = (e - site * 4 * NT) * 4;
+    const int ly = qdiv(site, T.inv_ts), lx = site - ly * g.ts;
+    const bool ok = ly < T.oh && lx < T.ow && col < p.c_out;
+    const int gs = (T.n * g.h_out + T.oy0 + ly) * g.w_out + T.ox0 + lx;
+    esite[h] = ok ? gs : -1;
+    eloc[h] = ok ? qdiv(ly, T.inv_blk) * T.tb_w + qdiv(lx, T.inv_blk) : 0;
+    ecol[h] = col;
+    const size_t o = ok ? (size_t)gs * p.c_out + col : 0;
+    zold[h] = *reinterpret_cast<const floatx4*>(p.z + o);
+    yold[h] = uint2{0u, 0u};
+    if (EMIT) yold[h] = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(p.y) + o);
+  }
+
+  for (int i = threadIdx.x; i < kMaxTileBlocks; i += kThreads) blk_flag[i] = 0u;
+  if (threadIdx.x == 0) tile_on = 0u;
+  // the zero pixel read by product rows outside the tile and by padded k-steps
+  for (int i = threadIdx.x; i < (p.pstride >> 4); i += kThreads)
+    *reinterpret_cast<u32x4*>(halo + (size_t)p.zero_pix * p.pstride + i * 16) = u32x4{0u, 0u, 0u, 0u};
+  // product rows: the 64 sites of the tile in row-major order
+  int abase[4], tapmul[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = i * 16 + r16;
+    const int ly = qdiv(row, T.inv_ts), lx = row - ly * g.ts;
+    const bool ok = ly < T.oh && lx < T.ow;
+    abase[i] = (ok ? (ly * g.stride) * T.hw + lx * g.stride : p.zero_pix) * p.pstride + kq * 16;
+    tapmul[i] = ok ? p.pstride : 0;  // the zero pixel ignores the tap offset
+  }
+
+  // 2. halo use (and further rounds for large halos)
+  halo_use<CHAIN, kThreads, true>(p, T, cm, hwk, 0, wave, hb, halo, a_halo, part);
+  const int nrounds = halo_rounds<kThreads, true>(T, cm, hwk);
+  for (int rd = 1; rd < nrounds; ++rd) {
+    halo_load<CHAIN, kThreads, true>(g, T, cm, hwk, rd, threadIdx.x, hb);
+    halo_use<CHAIN, kThreads, true>(p, T, cm, hwk, rd, wave, hb, halo, a_halo, part);
+  }
+  copy_owned(g, T);
+
+  // 3. this wave's weight fragments, loaded into registers while the gate runs
+  const int ng = wave % NG, kp = wave / NG;
+  const bool mma = kp < KP;
+  const int ks_lo = kp * p.ksteps / KP;
+  const int nks = mma ? (kp + 1) * p.ksteps / KP - ks_lo : 0;
+  bf16x8 bw[KPS][2];
+  {
+    const bf16x8* src = static_cast<const bf16x8*>(p.wpack) + ((size_t)ks_lo * NT + ng * 2) * 64 + lane;
+#pragma unroll
+    for (int st = 0; st < KPS; ++st)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        bw[st][j] = bf16x8{};
+        if (st < nks) bw[st][j] = src[((size_t)st * NT + j) * 64];
+      }
+  }
+
+  // 4. gate
+  gate_tile(p, T, cm, a_halo, part, blk_flag, &tile_on);
+  if (!tile_on) {
+    if (EMIT) emit_clear(p, T.n, T.oy0, T.ox0, T.oh, T.ow, T.tb_w, blk_flag, emit_clr);
+    return;
+  }
+
+  // 5. product over this wave's k-steps; padded steps (st >= nks) read the
+  // zero pixel against zero weights and add nothing
+  floatx4 acc[4][2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+  if (mma) {
+    const int csteps = p.csteps, k = g.k, hw = T.hw;
+    const int zbase = p.zero_pix * p.pstride + kq * 16;
+    const int tap0 = ks_lo / csteps;
+    int cc = ks_lo - tap0 * csteps, kh = tap0 / k, kw = tap0 - (tap0 / k) * k;
+#pragma unroll
+    for (int st = 0; st < KPS; ++st) {
+      const int off = kh * hw + kw, coff = cc * 64;
+      const bool live = st < nks;
+      bf16x8 a[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        a[i] = *reinterpret_cast<const bf16x8*>(halo + (live ? abase[i] + off * tapmul[i] + coff : zbase));
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bw[st][j], a[i], acc[i][j], 0, 0, 0);
+      if (++cc == csteps) {
+        cc = 0;
+        if (++kw == k) {
+          kw = 0;
+          ++kh;
+        }
+      }
+    }
+    // partial sums of this k-part: lane (r16, kq) holds channels
+    // (2ng + j) * 16 + 4kq .. + 3 of site 16i + r16
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        *reinterpret_cast<floatx4*>(pbuf + (size_t)kp * 64 * PROW + (i * 16 + r16) * PROW +
+                                    ((ng * 2 + j) * 16 + kq * 4) * 4) = acc[i][j];
+  }
+  lds_barrier();
+
+  // 6. epilogue: the k-parts added in ascending order, at the active sites
+#pragma unroll
+  for (int h = 0; h < EP; ++h) {
+    if (esite[h] < 0 || blk_flag[eloc[h]] == 0u) continue;
+    const int e = h * kThreads + threadIdx.x;
+    const int site = e / (4 * NT);
+    const uint8_t* src = pbuf + site * PROW + ecol[h] * 4;
+    floatx4 u = *reinterpret_cast<const floatx4*>(src);
+#pragma unroll
+    for (int q = 1; q < KP; ++q) {
+      const floatx4 v = *reinterpret_cast<const floatx4*>(src + (size_t)q * 64 * PROW);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) u[c] = u[c] + v[c];
+    }
+    store_piece<EMIT>(p, (size_t)esite[h] * p.c_out + ecol[h], u, zold[h], yold[h]);
+  }
+  if (EMIT) emit_clear(p, T.n, T.oy0, T.ox0, T.oh, T.ow, T.tb_w, blk_flag, emit_clr);
+}
+
+// ---------------------------------------------------------------------------
+// LDS-operand kernel. Wave layout of the product: GM waves along M (WM
+// 16-row tiles each) by 2 along N (WN 16-column tiles each); waves past the
+// first 2 * GM do no MFMA. MODE as above.
 template <int WM, int WN, int GM, int MODE>
 __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
   constexpr bool EMIT = (MODE & 1) != 0;
   constexpr bool CHAIN = (MODE & 2) != 0;
   constexpr int NTN = WN * 2;
+  constexpr int kHaloThreads = kThreads - 64 * kLoadWaves;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   __shared__ uint32_t blk_flag[kMaxTileBlocks];
   __shared__ int rows_pix[kMaxTileBlocks];
@@ -130,63 +686,22 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
   const GateParams& g = p.g;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, kq = lane >> 4;
-  const int tile = xcd_tile(blockIdx.x, gridDim.x);
-  const int tiles_per_img = g.tiles_y * g.tiles_x;
-  const int n = tile / tiles_per_img;
-  const int trem = tile - n * tiles_per_img;
-  const int ty = trem / g.tiles_x;
-  const int tx = trem - ty * g.tiles_x;
-  const int oy0 = ty * g.ts, ox0 = tx * g.ts;
-  const int oh = min(g.ts, g.h_out - oy0), ow = min(g.ts, g.w_out - ox0);
-  const int s = g.stride, k = g.k, c = g.c;
-  const int iy0 = oy0 * s - g.pad, ix0 = ox0 * s - g.pad;
-  const int hh = (oh - 1) * s + k, hw = (ow - 1) * s + k;
-  const int own_y0 = oy0 * s, own_x0 = ox0 * s;
-  const int own_y1 = (ty == g.tiles_y - 1) ? g.h : min(g.h, (oy0 + g.ts) * s);
-  const int own_x1 = (tx == g.tiles_x - 1) ? g.w : min(g.w, (ox0 + g.ts) * s);
+  const Tile T = make_tile(p);
+  const int n = T.n, oy0 = T.oy0, ox0 = T.ox0, oh = T.oh, ow = T.ow, hw = T.hw;
+  const int s = g.stride, k = g.k;
+  if (CHAIN && g.up_mask && chain_skip<EMIT>(p, T, emit_clr)) return;
 
   uint8_t* ldsb = lds + p.off_b;
   uint8_t* halo = lds + p.off_halo;
   float* a_halo = reinterpret_cast<float*>(lds + p.off_a);
-  const int tb_w = g.ts / g.block;
-  const int npix = hh * hw;
+  float* part = reinterpret_cast<float*>(lds + p.off_part);
+  const ChunkMap cm = make_chunks(p, T);
 
-  if (CHAIN && g.up_mask) {
-    // chained input: the residual is zero outside the upstream layer's active
-    // blocks; a tile whose input region meets none of them has every gate off
-    // and stops here, before any load (norm gates only)
-    const int y0 = max(iy0, 0), y1 = min(iy0 + hh, g.h), x0 = max(ix0, 0), x1 = min(ix0 + hw, g.w);
-    const int by0 = y0 / g.up_block, by1 = (y1 - 1) / g.up_block;
-    const int bx0 = x0 / g.up_block, bx1 = (x1 - 1) / g.up_block;
-    const int nbx = bx1 - bx0 + 1, cnt = (by1 - by0 + 1) * nbx;
-    int any = 0;
-    for (int i = threadIdx.x; i < cnt; i += kThreads) {
-      const int by = by0 + i / nbx, bx = bx0 + i % nbx;
-      any |= g.up_mask[((size_t)n * g.up_hb + by) * g.up_wb + bx] != 0;
-    }
-    if (!__syncthreads_or(any)) {
-      if (g.keep_stats)
-        for (int q = threadIdx.x; q < oh * ow; q += kThreads) {
-          const int ly = q / ow, lx = q - ly * ow;
-          const size_t o = ((size_t)n * g.h_out + oy0 + ly) * g.w_out + ox0 + lx;
-          g.stat[o] = 0.0f;
-          g.site_mask[o] = 0;
-        }
-      const int nby = (oh + g.block - 1) / g.block, nbx2 = (ow + g.block - 1) / g.block;
-      const int bi0 = oy0 / g.block, bj0 = ox0 / g.block;
-      for (int i = threadIdx.x; i < nby * nbx2; i += kThreads) {
-        const int by = i / nbx2, bx = i - by * nbx2;
-        g.block_mask[((size_t)n * g.hb + bi0 + by) * g.wb + bj0 + bx] = 0;
-      }
-      if (EMIT) emit_clear(p, n, oy0, ox0, oh, ow, g.ts / g.block, nullptr, emit_clr);
-      return;
-    }
-  }
-
-  // 1. weights: the waves past the first few issue the first chunk; the
-  // barriers up to the product wait on LDS traffic only
-  const int bw0 = min(kWaves - 1, 2);
-  if (wave >= bw0) issue_b<NTN>(p, ldsb, 0, wave, lane, bw0);
+  // 1. weights: the last kLoadWaves waves issue the first chunk and take no
+  // halo work, so the halo loads of the other waves never queue behind the
+  // copy (vector memory counters retire in issue order within a wave)
+  const bool loader = wave >= kWaves - kLoadWaves;
+  if (loader) issue_b<NTN>(p, ldsb, 0, wave, lane, kWaves - kLoadWaves);
   for (int i = threadIdx.x; i < kMaxTileBlocks; i += kThreads) blk_flag[i] = 0u;
   if (threadIdx.x == 0) tile_on = 0u;
   // the zero pixel read by MFMA rows past the active count
@@ -197,9 +712,6 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
   // are all sites of the tile in row-major order, fixed before the gate, which
   // only decides which rows are stored. With larger tiles the rows are the
   // active sites, compacted after the gate (step 4).
-  // The product is computed transposed (weights as the MFMA A operand): a
-  // lane's accumulator holds 4 consecutive output channels of one row, so z
-  // moves in 16-byte pieces.
   constexpr bool kStatic = GM * WM * 16 == 64;
   const int wm = wave % GM, wn = wave / GM;
   int abase[WM], tapmul[WM], zsite[WM];
@@ -210,139 +722,32 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
 #pragma unroll
     for (int i = 0; i < WM; ++i) {
       const int row = (wm * WM + i) * 16 + r16;
-      const int ly = row / g.ts, lx = row - (row / g.ts) * g.ts;
+      const int ly = qdiv(row, T.inv_ts), lx = row - ly * g.ts;
       const bool ok = wn < 2 && ly < oh && lx < ow;
       abase[i] = (ok ? (ly * s) * hw + lx * s : p.zero_pix) * p.pstride + kq * 16;
       tapmul[i] = ok ? p.pstride : 0;  // the zero pixel ignores the tap offset
       zsite[i] = ok ? (n * g.h_out + oy0 + ly) * g.w_out + ox0 + lx : -1;
-      blk_of[i] = ok ? (ly / g.block) * tb_w + lx / g.block : 0u;
+      blk_of[i] = ok ? qdiv(ly, T.inv_blk) * T.tb_w + qdiv(lx, T.inv_blk) : 0u;
     }
   }
 
-  // 2. halo: one item = one 8-channel chunk of one halo pixel (consecutive
-  // items are consecutive chunks, so a wave's loads are contiguous); kItems
-  // items per thread have their loads in flight together. Each item forms r
-  // in fp32, its chunk sum in canonical order (channels ascending, one
-  // rounding per multiply and per add) and rho = bf16_rne(r) for the product.
-  const uint16_t* xt = static_cast<const uint16_t*>(g.x_t);
-  const uint16_t* xp = static_cast<const uint16_t*>(g.x_prev);
-  uint16_t* keep = static_cast<uint16_t*>(g.x_keep);
-  float* part = reinterpret_cast<float*>(lds + p.off_part);
-  const int nchk = c >> 3;  // 16-byte chunks per pixel
-  const int total = npix * nchk;
-  constexpr int kItems = 4;
-  for (int base = 0; base < total; base += kThreads * kItems) {
-    uint4 vt[kItems], vp[kItems];
-    size_t off[kItems];
-    int px[kItems], ch[kItems];
-    bool in[kItems], own[kItems];
-#pragma unroll
-    for (int u = 0; u < kItems; ++u) {
-      const int idx = base + u * kThreads + threadIdx.x;
-      px[u] = idx < total ? idx / nchk : -1;
-      ch[u] = idx - px[u] * nchk;
-      const int hy = px[u] / hw, hx = px[u] - hy * hw;
-      const int y = iy0 + hy, x = ix0 + hx;
-      in[u] = px[u] >= 0 && y >= 0 && y < g.h && x >= 0 && x < g.w;
-      own[u] = in[u] && keep && g.copy_in_halo && y >= own_y0 && y < own_y1 && x >= own_x0 && x < own_x1;
-      off[u] = in[u] ? ((size_t)(n * g.h + y) * g.w + x) * c + ch[u] * 8 : 0;
-      vt[u] = uint4{0u, 0u, 0u, 0u};
-      vp[u] = uint4{0u, 0u, 0u, 0u};
-      if (in[u]) {
-        if (CHAIN) {  // fp32 residual input: channels 0-3 in vt, 4-7 in vp
-          const float* rr = static_cast<const float*>(g.x_t) + off[u];
-          vt[u] = *reinterpret_cast<const uint4*>(rr);
-          vp[u] = *reinterpret_cast<const uint4*>(rr + 4);
-        } else {
-          vt[u] = *reinterpret_cast<const uint4*>(xt + off[u]);
-          if (!g.no_prev) vp[u] = *reinterpret_cast<const uint4*>(xp + off[u]);
-        }
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < kItems; ++u) {
-      if (px[u] < 0) continue;
-      const uint32_t wt[4] = {vt[u].x, vt[u].y, vt[u].z, vt[u].w};
-      const uint32_t wpv[4] = {vp[u].x, vp[u].y, vp[u].z, vp[u].w};
-      uint32_t outw[4];
-      float sum = 0.0f;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        // channels 2e (low half) and 2e + 1 (high half)
-        float r0, r1;
-        if (CHAIN) {
-          const uint32_t* src = e < 2 ? wt : wpv;
-          r0 = __uint_as_float(src[(2 * e) & 3]);
-          r1 = __uint_as_float(src[(2 * e + 1) & 3]);
-        } else {
-          r0 = __fsub_rn(__uint_as_float(wt[e] << 16), __uint_as_float(wpv[e] << 16));
-          r1 = __fsub_rn(__uint_as_float(wt[e] & 0xffff0000u), __uint_as_float(wpv[e] & 0xffff0000u));
-        }
-        sum = add_rn(sum, term(r0, g.norm_p));
-        sum = add_rn(sum, term(r1, g.norm_p));
-        outw[e] = pack_bf16(r0, r1);
-      }
-      // out-of-frame pixels: zero operand and zero statistic (outw, sum are 0)
-      *reinterpret_cast<u32x4*>(halo + (size_t)px[u] * p.pstride + ch[u] * 16) =
-          u32x4{outw[0], outw[1], outw[2], outw[3]};
-      part[px[u] * p.pstage + ch[u]] = sum;
-      if (own[u]) *reinterpret_cast<uint4*>(keep + off[u]) = vt[u];
+  // 2. halo, taken by the threads of the non-loader waves
+  if (!loader) {
+    const HaloWalk hwk = make_walk<kHaloThreads, false>(g, T, cm, threadIdx.x);
+    const int nrounds = halo_rounds<kHaloThreads, false>(T, cm, hwk);
+    for (int rd = 0; rd < nrounds; ++rd) {
+      HaloBatch hb;
+      halo_load<CHAIN, kHaloThreads, false>(g, T, cm, hwk, rd, threadIdx.x, hb);
+      halo_use<CHAIN, kHaloThreads, false>(p, T, cm, hwk, rd, wave, hb, halo, a_halo, part);
     }
   }
-  if (!g.copy_in_halo && keep) {
-    const int ny = own_y1 - own_y0, nx = own_x1 - own_x0;
-    const int per_row = nx * c;
-    for (int i = threadIdx.x; i < ny * per_row; i += kThreads) {
-      const int yy = i / per_row, e = i - yy * per_row;
-      const size_t o = ((size_t)(n * g.h + own_y0 + yy) * g.w + own_x0) * c + e;
-      keep[o] = xt[o];
-    }
-  }
-  lds_barrier();
-  // pixel statistic: the chunk sums of each pixel added in ascending chunk order
-  for (int q = threadIdx.x; q < npix; q += kThreads) {
-    float acc = 0.0f;
-    for (int j = 0; j < nchk; ++j) acc = add_rn(acc, part[q * p.pstage + j]);
-    a_halo[q] = acc;
-  }
-  lds_barrier();
+  copy_owned(g, T);
 
   // 3. gate
-  for (int q = threadIdx.x; q < oh * ow; q += kThreads) {
-    const int ly = q / ow, lx = q - ly * ow;
-    float sv;
-    if (g.support == 0) {
-      sv = 0.0f;
-      const float* base = a_halo + (ly * s) * hw + lx * s;
-      for (int kh = 0; kh < k; ++kh)
-        for (int kw = 0; kw < k; ++kw) sv = add_rn(sv, base[kh * hw + kw]);
-    } else {
-      sv = a_halo[(ly * s + g.pad) * hw + lx * s + g.pad];
-    }
-    const bool on = g.reference || g.force_dense || ((double)sv * g.wnorm > g.thr) || (sv != sv);
-    if (g.keep_stats) {
-      const size_t o = ((size_t)n * g.h_out + oy0 + ly) * g.w_out + ox0 + lx;
-      g.stat[o] = sv;
-      g.site_mask[o] = on ? 1 : 0;
-    }
-    if (on) {
-      blk_flag[(ly / g.block) * tb_w + lx / g.block] = 1u;
-      tile_on = 1u;
-    }
-  }
-  lds_barrier();
-  {
-    const int nby = (oh + g.block - 1) / g.block, nbx = (ow + g.block - 1) / g.block;
-    const int bi0 = oy0 / g.block, bj0 = ox0 / g.block;
-    for (int i = threadIdx.x; i < nby * nbx; i += kThreads) {
-      const int by = i / nbx, bx = i - by * nbx;
-      g.block_mask[((size_t)n * g.hb + bi0 + by) * g.wb + bj0 + bx] = (uint8_t)blk_flag[by * tb_w + bx];
-    }
-  }
-
+  gate_tile(p, T, cm, a_halo, part, blk_flag, &tile_on);
   if (!tile_on) {
     __builtin_amdgcn_s_waitcnt(0);  // no weight copy may still target this workgroup's LDS
-    if (EMIT) emit_clear(p, n, oy0, ox0, oh, ow, tb_w, blk_flag, emit_clr);
+    if (EMIT) emit_clear(p, n, oy0, ox0, oh, ow, T.tb_w, blk_flag, emit_clr);
     return;
   }
   __syncthreads();  // the first weight chunk has landed in LDS
@@ -353,8 +758,9 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
   if (!kStatic) {
     {
       const int q = threadIdx.x;
-      const int ly = q / ow, lx = q - (q / ow) * ow;
-      const bool act = q < oh * ow && blk_flag[(ly / g.block) * tb_w + lx / g.block] != 0u;
+      const int ly = qdiv(q, T.inv_ts), lx = q - ly * g.ts;
+      const bool act = q < g.ts * g.ts && ly < oh && lx < ow &&
+                       blk_flag[qdiv(ly, T.inv_blk) * T.tb_w + qdiv(lx, T.inv_blk)] != 0u;
       const unsigned long long m = __ballot(act);
       const uint32_t rank = __popcll(m & ((1ull << lane) - 1ull));
       if (lane == 0) wave_cnt[wave] = (uint32_t)__popcll(m);
@@ -378,39 +784,26 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
       zsite[i] = ok ? rows_site[row] : -1;
       blk_of[i] = 0u;
     }
-    // old z of the active rows, fetched now so that the load overlaps the product
+  } else {
+    // rows of blocks the gate left off are computed but not stored
 #pragma unroll
     for (int i = 0; i < WM; ++i)
-#pragma unroll
-      for (int j = 0; j < WN; ++j) {
-        const int col = (wn * WN + j) * 16 + kq * 4;
-        zold[i][j] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
-        yold[i][j] = uint2{0u, 0u};
-        if (zsite[i] >= 0 && !g.reference && col < p.c_out)
-          zold[i][j] = *reinterpret_cast<const floatx4*>(p.z + (size_t)zsite[i] * p.c_out + col);
-        if (EMIT && zsite[i] >= 0 && col < p.c_out)
-          yold[i][j] = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(p.y) +
-                                                       (size_t)zsite[i] * p.c_out + col);
-      }
-  } else {
-    // rows of blocks the gate left off are computed but not stored; the old z
-    // of the stored rows is fetched now so that the load overlaps the product
-#pragma unroll
-    for (int i = 0; i < WM; ++i) {
       if (zsite[i] >= 0 && blk_flag[blk_of[i]] == 0u) zsite[i] = -1;
-#pragma unroll
-      for (int j = 0; j < WN; ++j) {
-        const int col = (wn * WN + j) * 16 + kq * 4;
-        zold[i][j] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
-        yold[i][j] = uint2{0u, 0u};
-        if (zsite[i] >= 0 && !g.reference && col < p.c_out)
-          zold[i][j] = *reinterpret_cast<const floatx4*>(p.z + (size_t)zsite[i] * p.c_out + col);
-        if (EMIT && zsite[i] >= 0 && col < p.c_out)
-          yold[i][j] = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(p.y) +
-                                                       (size_t)zsite[i] * p.c_out + col);
-      }
-    }
   }
+  // old z of the stored rows, fetched now so that the load overlaps the product
+#pragma unroll
+  for (int i = 0; i < WM; ++i)
+#pragma unroll
+    for (int j = 0; j < WN; ++j) {
+      const int col = (wn * WN + j) * 16 + kq * 4;
+      zold[i][j] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+      yold[i][j] = uint2{0u, 0u};
+      if (zsite[i] >= 0 && !g.reference && col < p.c_out)
+        zold[i][j] = *reinterpret_cast<const floatx4*>(p.z + (size_t)zsite[i] * p.c_out + col);
+      if (EMIT && zsite[i] >= 0 && col < p.c_out)
+        yold[i][j] = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(p.y) +
+                                                     (size_t)zsite[i] * p.c_out + col);
+    }
   const bool busy = wn < 2 && (kStatic ? wm * WM * 16 < g.ts * g.ts : wm * WM * 16 < nrows);
 
   // 5. MFMA over the rows: wave (wm, wn) owns M-tiles wm*WM.. and N-tiles wn*WN..
@@ -488,8 +881,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
     if (chunk + 1 < p.nchunks) __syncthreads();  // next chunk landed; this buffer free
   }
 
-  // 6. epilogue: z = z_{t-1} + U (assigned on a reference frame), activation
-  // output; emitting layers also write r = y_new - y_old for their successor
+  // 6. epilogue
   if (busy) {
 #pragma unroll
     for (int i = 0; i < WM; ++i) {
@@ -498,32 +890,14 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
       for (int j = 0; j < WN; ++j) {
         const int col = (wn * WN + j) * 16 + kq * 4;
         if (col >= p.c_out) continue;
-        floatx4 nv;
-#pragma unroll
-        for (int v = 0; v < 4; ++v) nv[v] = g.reference ? acc[i][j][v] : zold[i][j][v] + acc[i][j][v];
-        const size_t o = (size_t)zsite[i] * p.c_out + col;
-        *reinterpret_cast<floatx4*>(p.z + o) = nv;
-        if (p.act) {
-          uint32_t yb[4];
-#pragma unroll
-          for (int v = 0; v < 4; ++v) yb[v] = f32_to_bf16(p.act == 2 ? fmaxf(nv[v], 0.0f) : nv[v]);
-          *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.y) + o) = uint2{yb[0] | (yb[1] << 16), yb[2] | (yb[3] << 16)};
-          if (EMIT) {
-            const uint32_t yo[4] = {yold[i][j].x & 0xffffu, yold[i][j].x >> 16, yold[i][j].y & 0xffffu,
-                                    yold[i][j].y >> 16};
-            floatx4 r;
-#pragma unroll
-            for (int v = 0; v < 4; ++v) r[v] = __fsub_rn(bf16_to_f32(yb[v]), bf16_to_f32(yo[v]));
-            *reinterpret_cast<floatx4*>(p.r32 + o) = r;
-            *reinterpret_cast<uint2*>(p.rb + o) =
-                uint2{f32_to_bf16(r[0]) | (f32_to_bf16(r[1]) << 16), f32_to_bf16(r[2]) | (f32_to_bf16(r[3]) << 16)};
-          }
-        }
+        store_piece<EMIT>(p, (size_t)zsite[i] * p.c_out + col, acc[i][j], zold[i][j], yold[i][j]);
       }
     }
   }
-  if (EMIT) emit_clear(p, n, oy0, ox0, oh, ow, tb_w, blk_flag, emit_clr);
+  if (EMIT) emit_clear(p, n, oy0, ox0, oh, ow, T.tb_w, blk_flag, emit_clr);
 }
+
+// ------------------------------------------------------------ launching --
 
 template <int WM, int WN, int GM>
 hipError_t launch_fused_t(const FusedParams& p, int grid, hipStream_t st) {
@@ -536,16 +910,25 @@ hipError_t launch_fused_t(const FusedParams& p, int grid, hipStream_t st) {
   return hipGetLastError();
 }
 
+template <int NG, int KPS>
+hipError_t launch_rb_t(const FusedParams& p, int grid, hipStream_t st) {
+  switch ((p.emit ? 1 : 0) | (p.g.rin ? 2 : 0)) {
+    case 0: hipLaunchKernelGGL((fused_rb_kernel<NG, KPS, 0>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+    case 1: hipLaunchKernelGGL((fused_rb_kernel<NG, KPS, 1>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+    case 2: hipLaunchKernelGGL((fused_rb_kernel<NG, KPS, 2>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+    default: hipLaunchKernelGGL((fused_rb_kernel<NG, KPS, 3>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+  }
+  return hipGetLastError();
+}
+
 // Allow the kernel its dynamic LDS (above the 64 KB default) and report how
 // many workgroups fit on one CU; done once, at create time.
-template <int WM, int WN, int GM, int MODE>
-int prepare_fused_e(const FusedParams& p) {
-  const void* fn = reinterpret_cast<const void*>(fused_kernel<WM, WN, GM, MODE>);
+template <typename K>
+int prepare_kernel(K kernel, const FusedParams& p) {
+  const void* fn = reinterpret_cast<const void*>(kernel);
   if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, p.lds_bytes) != hipSuccess) return 0;
   int blocks = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, fused_kernel<WM, WN, GM, MODE>, kThreads,
-                                                   p.lds_bytes) != hipSuccess)
-    return 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, kernel, kThreads, p.lds_bytes) != hipSuccess) return 0;
   return blocks;
 }
 
@@ -553,20 +936,62 @@ int prepare_fused_e(const FusedParams& p) {
 // emission) gets its LDS attribute; the occupancy reported is the plain one.
 template <int WM, int WN, int GM>
 int prepare_fused_t(const FusedParams& p) {
-  const int e = p.emit ? 1 : 0;
-  const int a = prepare_fused_e<WM, WN, GM, 0>(p);
-  const int b = prepare_fused_e<WM, WN, GM, 2>(p);
-  const int c = e ? std::min(prepare_fused_e<WM, WN, GM, 1>(p), prepare_fused_e<WM, WN, GM, 3>(p)) : a;
+  const int a = prepare_kernel(fused_kernel<WM, WN, GM, 0>, p);
+  const int b = prepare_kernel(fused_kernel<WM, WN, GM, 2>, p);
+  const int c = p.emit ? std::min(prepare_kernel(fused_kernel<WM, WN, GM, 1>, p),
+                                  prepare_kernel(fused_kernel<WM, WN, GM, 3>, p))
+                       : a;
+  return std::min(std::min(a, b), c);
+}
+
+template <int NG, int KPS>
+int prepare_rb_t(const FusedParams& p) {
+  const int a = prepare_kernel(fused_rb_kernel<NG, KPS, 0>, p);
+  const int b = prepare_kernel(fused_rb_kernel<NG, KPS, 2>, p);
+  const int c = p.emit ? std::min(prepare_kernel(fused_rb_kernel<NG, KPS, 1>, p),
+                                  prepare_kernel(fused_rb_kernel<NG, KPS, 3>, p))
+                       : a;
   return std::min(std::min(a, b), c);
 }
 
 }  // namespace
 
-// Instantiations: tiles of <= 8 x 8 sites use 4 x 2 waves of one M-tile
-// each (a 2 x 2 layout of 2 M-tiles per wave reads less LDS but measured
-// slower); 16 x 16 tiles use 4 x 2 waves of 4 M-tiles each. WN = N-tiles per
-// wave = ntiles_n / 2.
+hipError_t launch_fused_tiles(uint32_t* table, int grid, int tiles_y, int tiles_x, hipStream_t st) {
+  hipLaunchKernelGGL(fused_tiles_kernel, dim3((grid + 255) / 256), dim3(256), 0, st, table, grid, tiles_y, tiles_x);
+  return hipGetLastError();
+}
+
+// Register-operand instantiations (NG = ntiles_n / 2, KPS = k-steps per wave
+// rounded up to an instantiated value); 0 when none covers the layer.
+int fused_rb_kps(int ntiles_n, int ksteps, int halo_row_items) {
+  if (halo_row_items > kThreads) return 0;  // the kernel walks the halo in whole rows
+  static const int kNG[] = {1, 2, 4, 6};
+  static const int kKPS[4][2] = {{2, 3}, {3, 5}, {9, 9}, {6, 6}};
+  for (int i = 0; i < 4; ++i) {
+    if (ntiles_n != 2 * kNG[i]) continue;
+    const int kp = kWaves / kNG[i];
+    const int need = (ksteps + kp - 1) / kp;
+    for (int j = 0; j < 2; ++j)
+      if (need <= kKPS[i][j]) return kKPS[i][j];
+  }
+  return 0;
+}
+
+// LDS-operand instantiations: tiles of <= 8 x 8 sites use 4 x 2 waves of one
+// M-tile each; 16 x 16 tiles use 4 x 2 waves of 4 M-tiles each. WN = N-tiles
+// per wave = ntiles_n / 2.
 int prepare_fused(const FusedParams& p) {
+  if (p.rbk) {
+    switch (p.ntiles_n * 100 + p.rbk) {
+      case 202: return prepare_rb_t<1, 2>(p);
+      case 203: return prepare_rb_t<1, 3>(p);
+      case 403: return prepare_rb_t<2, 3>(p);
+      case 405: return prepare_rb_t<2, 5>(p);
+      case 809: return prepare_rb_t<4, 9>(p);
+      case 1206: return prepare_rb_t<6, 6>(p);
+      default: return 0;
+    }
+  }
   if (p.mw == 1) {
     switch (p.ntiles_n) {
       case 2: return prepare_fused_t<1, 1, 4>(p);
@@ -589,6 +1014,17 @@ int prepare_fused(const FusedParams& p) {
 }
 
 hipError_t launch_fused(const FusedParams& p, int grid, hipStream_t st) {
+  if (p.rbk) {
+    switch (p.ntiles_n * 100 + p.rbk) {
+      case 202: return launch_rb_t<1, 2>(p, grid, st);
+      case 203: return launch_rb_t<1, 3>(p, grid, st);
+      case 403: return launch_rb_t<2, 3>(p, grid, st);
+      case 405: return launch_rb_t<2, 5>(p, grid, st);
+      case 809: return launch_rb_t<4, 9>(p, grid, st);
+      case 1206: return launch_rb_t<6, 6>(p, grid, st);
+      default: return hipErrorInvalidValue;
+    }
+  }
   if (p.mw == 1) {
     switch (p.ntiles_n) {
       case 2: return launch_fused_t<1, 1, 4>(p, grid, st);

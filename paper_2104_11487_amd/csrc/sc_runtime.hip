@@ -50,11 +50,13 @@ struct Geometry {
   bool fused;           // single-pass kernel instead of gate + compaction + conv
   int f_ts, f_tiles_y, f_tiles_x, f_grid, f_copy_in_halo;
   int f_kc, f_nchunks, f_nbuf, f_mw, f_pstride, f_zero_pix, f_off_b, f_off_halo, f_off_a, f_lds;
+  int f_rb;             // register-operand fused kernel: its k-steps per wave (0: LDS operand)
   int f_pstage, f_off_part;
   int vec;              // gate load width (elements)
   size_t elem;
   size_t off_wpack, off_slot0, off_slot1, off_z, off_y, off_bmask, off_tflag, off_list, off_ctr,
-      off_stat, off_smask, off_phi, off_r32, off_rb, off_prev, off_z2, off_list_a, off_list_b, off_wlist, total;
+      off_stat, off_smask, off_phi, off_r32, off_rb, off_prev, off_z2, off_list_a, off_list_b, off_wlist,
+      off_ftiles, total;
   int learned;          // learned gate: its kernel size (the layer's k), else 0
   bool phi_in_lds;      // learned gate: phi staged in LDS (else read through the caches)
   int phi_off;          // learned gate: LDS float offset of the staged phi
@@ -268,7 +270,13 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
       const long whole = (long)G.ksteps * G.ntn * 1024;
       long b_bytes = whole;
       int kc = G.ksteps, nbuf = 1;
-      if (whole + halo_b + a_b + part_b > kFusedLdsLimit) {
+      // tiles of <= 8 x 8 sites: register-operand kernel when instantiated for
+      // the shape; LDS holds the partial sums of its k-parts instead of weights
+      const int rb = mw == 1 ? sc::fused_rb_kps(G.ntn, G.ksteps, hh * (d->c_in / 8)) : 0;
+      if (rb) {
+        const long kparts = 8 / (G.ntn / 2);
+        b_bytes = kparts * 64 * ((long)G.ntn * 64 + 16);
+      } else if (whole + halo_b + a_b + part_b > kFusedLdsLimit) {
         kc = std::max(1, 16 / G.ntn);
         nbuf = 2;
         b_bytes = (long)nbuf * kc * G.ntn * 1024;
@@ -277,6 +285,7 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
         G.fused = true;
         G.f_ts = ts;
         G.f_mw = mw;
+        G.f_rb = rb;
         G.f_kc = kc;
         G.f_nbuf = nbuf;
         G.f_nchunks = (G.ksteps + kc - 1) / kc;
@@ -291,6 +300,7 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
         G.f_tiles_y = (G.h_out + ts - 1) / ts;
         G.f_tiles_x = (G.w_out + ts - 1) / ts;
         G.f_grid = d->n * G.f_tiles_y * G.f_tiles_x;
+        if (G.f_tiles_x > 1024 || G.f_tiles_y > 1024 || d->n > 4096) G.fused = false;
         G.f_copy_in_halo = halo_covers_owned(d->h, G.h_out, ts, G.f_tiles_y, s, pad, k) &&
                            halo_covers_owned(d->w, G.w_out, ts, G.f_tiles_x, s, pad, k);
       }
@@ -311,6 +321,8 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
   G.off_list = off; off = align_up(off + (size_t)nb * 4);
   G.off_wlist = off; off = align_up(off + (size_t)nb * 4);  // unordered work list of the split pipeline
   G.off_ctr = off; off = align_up(off + sc::kNumCounters * 4);
+  G.off_ftiles = off;
+  if (G.fused) off = align_up(off + (size_t)G.f_grid * 4);  // tile table of the fused kernel
   G.off_stat = off;
   G.off_smask = off;
   if (d->flags & SKIPCONV_FLAG_KEEP_STATS) {
@@ -418,6 +430,12 @@ sc::FusedParams fused_params(skipconv_layer* h, const void* x_t, bool ref) {
   fp.nchunks = g.f_nchunks;
   fp.nbuf = g.f_nbuf;
   fp.mw = g.f_mw;
+  fp.rbk = g.f_rb;
+  fp.tiles = reinterpret_cast<const uint32_t*>(h->ws + g.off_ftiles);
+  fp.inv_ts = 1.0f / (float)g.f_ts;
+  fp.inv_blk = 1.0f / (float)d.block;
+  fp.inv_hw = 1.0f / (float)((g.f_ts - 1) * d.stride + d.kernel);
+  fp.inv_chk = 1.0f / (float)(d.c_in / 8);
   fp.pstride = g.f_pstride;
   fp.zero_pix = g.f_zero_pix;
   fp.off_b = g.f_off_b;
@@ -689,6 +707,9 @@ int skipconv_create(const skipconv_desc* d, const void* weights, void* workspace
       e = sc::launch_pack_mfma(weights, h->wpack(), d->dtype, d->c_out, d->c_in, d->kernel,
                                g.ksteps, g.ntn, st);
   }
+  if (e == hipSuccess && g.fused)
+    e = sc::launch_fused_tiles(reinterpret_cast<uint32_t*>(h->ws + g.off_ftiles), g.f_grid, g.f_tiles_y,
+                               g.f_tiles_x, st);
   if (e == hipSuccess && d->gate == SKIPCONV_GATE_OUTPUT_NORM) e = weight_norm(h, weights, st);
   if (e != hipSuccess) {
     snprintf(g_create_error, sizeof(g_create_error), "create: %s", hipGetErrorString(e));

@@ -51,6 +51,15 @@ __device__ __forceinline__ void copy_vec(T* dst, const T* src, size_t off) {
   }
 }
 
+// floor(n / d) for 0 <= n < 2^20 and d >= 1, given inv_d = 1 / d rounded to
+// fp32 (within 2.5 ulp): (n + 1/2) / d is at least 1 / (2d) away from an
+// integer, and the fp32 product lies within (n + 1/2) / d * 2^-21 < 1 / (2d)
+// of it, so truncation gives the exact quotient. A few VALU operations instead
+// of the long integer-division sequence.
+__device__ __forceinline__ int qdiv(int n, float inv_d) {
+  return (int)(((float)n + 0.5f) * inv_d);
+}
+
 // Workgroup b runs tile remap(b): XCD b % 8 (workgroups go to the XCDs
 // round-robin) receives a contiguous range of tiles, so neighbouring tiles
 // share their halo rows through one L2.
