@@ -499,9 +499,12 @@ __device__ __forceinline__ void store_piece(const FusedParams& p, size_t o, cons
 // ---------------------------------------------------------------------------
 // Register-operand kernel for tiles of <= 8 x 8 sites (64 product rows, 4
 // M-tiles). Wave w = kp * NG + ng owns N-tiles 2ng, 2ng + 1 and k-steps
-// [kp * ksteps / KP, (kp + 1) * ksteps / KP) (at most KPS of them). Per tile
-// LDS carries the residual fragments (each read by the NG waves of a k-part)
-// and the KP partial sums; the weights come from global memory (L2) once.
+// [kp * ksteps / KP, (kp + 1) * ksteps / KP): KPS or KPS - 1 of them (the
+// instantiation is chosen so). Per tile LDS carries the residual fragments
+// (each read by the NG waves of a k-part) and the KP partial sums; the
+// weights come from global memory (L2) once. Rows outside the tile read
+// pixel (tap) of the halo like row 0: their columns of the product are
+// discarded, and a site's outputs depend on its own column only.
 // MODE bit 0: emit the successor's residual; bit 1: chained input.
 template <int NG, int KPS, int MODE>
 __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
@@ -527,10 +530,25 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
   float* part = reinterpret_cast<float*>(lds + p.off_part);
   const ChunkMap cm = make_chunks(p, T);
 
-  // 1. halo loads of the first round, then the old z (and y) of this thread's
-  // epilogue pieces at every site of the tile (piece e = h * 512 + thread:
-  // site e / (4 NT), channels 4 (e % (4 NT)) ..), so that no load is left
-  // between the gate and the product
+  // 1. this wave's weight fragments (every load issued: a step past the
+  // wave's k-range rereads its first fragment and goes unused), the halo loads
+  // of the first round, then the old z (and y) of this thread's epilogue
+  // pieces at every site of the tile (piece e = h * 512 + thread: site
+  // e / (4 NT), channels 4 (e % (4 NT)) ..). All are in flight together, and
+  // no load is left between the gate and the product.
+  const int wv = __builtin_amdgcn_readfirstlane(wave);
+  const int ng = wv % NG, kp = wv / NG;
+  const bool mma = kp < KP;
+  const int ks_lo = mma ? kp * p.ksteps / KP : 0;
+  const int nks = mma ? (kp + 1) * p.ksteps / KP - ks_lo : 0;
+  bf16x8 bw[KPS][2];
+  {
+    const bf16x8* src = static_cast<const bf16x8*>(p.wpack) + ((size_t)ks_lo * NT + ng * 2) * 64 + lane;
+#pragma unroll
+    for (int st = 0; st < KPS; ++st)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) bw[st][j] = src[((size_t)(st < nks ? st : 0) * NT + j) * 64];
+  }
   const HaloWalk hwk = make_walk<kThreads, true>(g, T, cm, threadIdx.x);
   HaloBatch hb;
   halo_load<CHAIN, kThreads, true>(g, T, cm, hwk, 0, threadIdx.x, hb);
@@ -555,18 +573,14 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
 
   for (int i = threadIdx.x; i < kMaxTileBlocks; i += kThreads) blk_flag[i] = 0u;
   if (threadIdx.x == 0) tile_on = 0u;
-  // the zero pixel read by product rows outside the tile and by padded k-steps
-  for (int i = threadIdx.x; i < (p.pstride >> 4); i += kThreads)
-    *reinterpret_cast<u32x4*>(halo + (size_t)p.zero_pix * p.pstride + i * 16) = u32x4{0u, 0u, 0u, 0u};
   // product rows: the 64 sites of the tile in row-major order
-  int abase[4], tapmul[4];
+  int abase[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int row = i * 16 + r16;
     const int ly = qdiv(row, T.inv_ts), lx = row - ly * g.ts;
     const bool ok = ly < T.oh && lx < T.ow;
-    abase[i] = (ok ? (ly * g.stride) * T.hw + lx * g.stride : p.zero_pix) * p.pstride + kq * 16;
-    tapmul[i] = ok ? p.pstride : 0;  // the zero pixel ignores the tap offset
+    abase[i] = (ok ? (ly * g.stride) * T.hw + lx * g.stride : 0) * p.pstride + kq * 16;
   }
 
   // 2. halo use (and further rounds for large halos)
@@ -578,32 +592,16 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
   }
   copy_owned(g, T);
 
-  // 3. this wave's weight fragments, loaded into registers while the gate runs
-  const int ng = wave % NG, kp = wave / NG;
-  const bool mma = kp < KP;
-  const int ks_lo = kp * p.ksteps / KP;
-  const int nks = mma ? (kp + 1) * p.ksteps / KP - ks_lo : 0;
-  bf16x8 bw[KPS][2];
-  {
-    const bf16x8* src = static_cast<const bf16x8*>(p.wpack) + ((size_t)ks_lo * NT + ng * 2) * 64 + lane;
-#pragma unroll
-    for (int st = 0; st < KPS; ++st)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        bw[st][j] = bf16x8{};
-        if (st < nks) bw[st][j] = src[((size_t)st * NT + j) * 64];
-      }
-  }
-
-  // 4. gate
+  // 3. gate
   gate_tile(p, T, cm, a_halo, part, blk_flag, &tile_on);
   if (!tile_on) {
     if (EMIT) emit_clear(p, T.n, T.oy0, T.ox0, T.oh, T.ow, T.tb_w, blk_flag, emit_clr);
     return;
   }
 
-  // 5. product over this wave's k-steps; padded steps (st >= nks) read the
-  // zero pixel against zero weights and add nothing
+  // 4. product over this wave's k-steps: the first KPS - 1 always run, the
+  // last one when the wave has KPS (a wave-uniform branch); the tap and
+  // channel offset of a step is wave-uniform
   floatx4 acc[4][2];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -611,17 +609,15 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
     for (int j = 0; j < 2; ++j) acc[i][j] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
   if (mma) {
     const int csteps = p.csteps, k = g.k, hw = T.hw;
-    const int zbase = p.zero_pix * p.pstride + kq * 16;
     const int tap0 = ks_lo / csteps;
     int cc = ks_lo - tap0 * csteps, kh = tap0 / k, kw = tap0 - (tap0 / k) * k;
 #pragma unroll
     for (int st = 0; st < KPS; ++st) {
-      const int off = kh * hw + kw, coff = cc * 64;
-      const bool live = st < nks;
+      if (st == KPS - 1 && nks < KPS) break;
+      const int off = (kh * hw + kw) * p.pstride + cc * 64;
       bf16x8 a[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        a[i] = *reinterpret_cast<const bf16x8*>(halo + (live ? abase[i] + off * tapmul[i] + coff : zbase));
+      for (int i = 0; i < 4; ++i) a[i] = *reinterpret_cast<const bf16x8*>(halo + abase[i] + off);
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -646,7 +642,7 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
   }
   lds_barrier();
 
-  // 6. epilogue: the k-parts added in ascending order, at the active sites
+  // 5. epilogue: the k-parts added in ascending order, at the active sites
 #pragma unroll
   for (int h = 0; h < EP; ++h) {
     if (esite[h] < 0 || blk_flag[eloc[h]] == 0u) continue;
@@ -971,8 +967,8 @@ int fused_rb_kps(int ntiles_n, int ksteps, int halo_row_items) {
     if (ntiles_n != 2 * kNG[i]) continue;
     const int kp = kWaves / kNG[i];
     const int need = (ksteps + kp - 1) / kp;
-    for (int j = 0; j < 2; ++j)
-      if (need <= kKPS[i][j]) return kKPS[i][j];
+    for (int j = 0; j < 2; ++j)  // each wave takes KPS - 1 or KPS k-steps
+      if (need <= kKPS[i][j] && ksteps / kp >= kKPS[i][j] - 1) return kKPS[i][j];
   }
   return 0;
 }
