@@ -342,8 +342,7 @@ __device__ __forceinline__ void halo_load(const GateParams& g, const Tile& T, co
 // rounding per multiply and per add) and rho = bf16_rne(r) into the LDS halo;
 // the pixel's chunk sums are added in ascending order by the group's first
 // lane through DPP row shifts (lane_sum), or parked in LDS for a later
-// combine. Then the owned pixels of x_t go to the spare x_{t-1} slot.
-// `wave` is the wave's index among the NTHR threads taking items.
+// combine. `wave` is the wave's index among the NTHR threads taking items.
 template <bool CHAIN, int NTHR, bool TWOD>
 __device__ __forceinline__ void halo_use(const FusedParams& p, const Tile& T, const ChunkMap& cm,
                                          const HaloWalk& W, int rd, int wave, HaloBatch& B, uint8_t* halo,
@@ -390,10 +389,23 @@ __device__ __forceinline__ void halo_use(const FusedParams& p, const Tile& T, co
       part[B.px[u] * p.pstage + B.ch[u]] = sum;
     }
   }
+}
+
+// The owned pixels of a round's x_t go to the spare x_{t-1} slot.
+__device__ __forceinline__ void halo_keep(const GateParams& g, const HaloBatch& B) {
   uint16_t* keep = static_cast<uint16_t*>(g.x_keep);
 #pragma unroll
   for (int u = 0; u < kItems; ++u)
     if (B.own[u]) *reinterpret_cast<uint4*>(keep + B.off[u]) = B.vt[u];
+}
+
+// Marks a register value as needed here: the compiler completes its load
+// first. Used so that no load is still counted once stores are in flight
+// (loads and stores share one counter, and a wait on a load issued before a
+// store would otherwise wait for the store as well).
+template <typename V>
+__device__ __forceinline__ void settle(const V& v) {
+  asm volatile("" ::"v"(v));
 }
 
 // Layers whose halos do not cover the pixels a tile owns (strides above the
@@ -585,11 +597,20 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
 
   // 2. halo use (and further rounds for large halos)
   halo_use<CHAIN, kThreads, true>(p, T, cm, hwk, 0, wave, hb, halo, a_halo, part);
-  const int nrounds = halo_rounds<kThreads, true>(T, cm, hwk);
-  for (int rd = 1; rd < nrounds; ++rd) {
-    halo_load<CHAIN, kThreads, true>(g, T, cm, hwk, rd, threadIdx.x, hb);
-    halo_use<CHAIN, kThreads, true>(p, T, cm, hwk, rd, wave, hb, halo, a_halo, part);
+  // weights and old z arrived with (or just after) the halo: settle them
+  // before the x_t copy stores go out, so the product and the epilogue wait
+  // for nothing
+#pragma unroll
+  for (int st = 0; st < KPS; ++st) {
+    settle(bw[st][0]);
+    settle(bw[st][1]);
   }
+#pragma unroll
+  for (int h = 0; h < EP; ++h) {
+    settle(zold[h]);
+    if (EMIT) settle(yold[h]);
+  }
+  halo_keep(g, hb);  // the halo is one round (kItems rows per thread) for this kernel
   copy_owned(g, T);
 
   // 3. gate
@@ -735,6 +756,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
       HaloBatch hb;
       halo_load<CHAIN, kHaloThreads, false>(g, T, cm, hwk, rd, threadIdx.x, hb);
       halo_use<CHAIN, kHaloThreads, false>(p, T, cm, hwk, rd, wave, hb, halo, a_halo, part);
+      halo_keep(g, hb);
     }
   }
   copy_owned(g, T);
@@ -959,8 +981,10 @@ hipError_t launch_fused_tiles(uint32_t* table, int grid, int tiles_y, int tiles_
 
 // Register-operand instantiations (NG = ntiles_n / 2, KPS = k-steps per wave
 // rounded up to an instantiated value); 0 when none covers the layer.
-int fused_rb_kps(int ntiles_n, int ksteps, int halo_row_items) {
-  if (halo_row_items > kThreads) return 0;  // the kernel walks the halo in whole rows
+int fused_rb_kps(int ntiles_n, int ksteps, int halo_w, int chunks) {
+  // the kernel walks the halo in whole rows, in one round of kItems rows per thread
+  const int rw = halo_w * chunks;
+  if (rw > kThreads || (halo_w + kThreads / rw - 1) / (kThreads / rw) > kItems) return 0;
   static const int kNG[] = {1, 2, 4, 6};
   static const int kKPS[4][2] = {{2, 3}, {3, 5}, {9, 9}, {6, 6}};
   for (int i = 0; i < 4; ++i) {

@@ -140,9 +140,9 @@ int prepare_fused(const FusedParams& p);  // create time: LDS attribute; workgro
 // tx | ty << 10 | n << 20, in the XCD-aware order (tiles_x, tiles_y <= 1024).
 hipError_t launch_fused_tiles(uint32_t* table, int grid, int tiles_y, int tiles_x, hipStream_t st);
 // k-steps per wave of the register-operand fused kernel instantiated for this
-// shape (ntiles_n 16-column tiles, ksteps k-steps, halo_row_items = halo width
-// x c_in / 8), 0 if none covers it.
-int fused_rb_kps(int ntiles_n, int ksteps, int halo_row_items);
+// shape (ntiles_n 16-column tiles, ksteps k-steps, a square halo of halo_w
+// pixels a side, chunks = c_in / 8), 0 if none covers it.
+int fused_rb_kps(int ntiles_n, int ksteps, int halo_w, int chunks);
 
 hipError_t launch_gate(const GateParams& p, int dtype, int vec, int grid, size_t lds_bytes,
                        hipStream_t st);

@@ -272,7 +272,7 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
       int kc = G.ksteps, nbuf = 1;
       // tiles of <= 8 x 8 sites: register-operand kernel when instantiated for
       // the shape; LDS holds the partial sums of its k-parts instead of weights
-      const int rb = mw == 1 ? sc::fused_rb_kps(G.ntn, G.ksteps, hh * (d->c_in / 8)) : 0;
+      const int rb = mw == 1 ? sc::fused_rb_kps(G.ntn, G.ksteps, hh, d->c_in / 8) : 0;
       if (rb) {
         const long kparts = 8 / (G.ntn / 2);
         b_bytes = kparts * 64 * ((long)G.ntn * 64 + 16);
