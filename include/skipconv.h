@@ -227,9 +227,11 @@ int skipconv_activation(skipconv_t h, const void** y);
 /* Descriptor the handle was created with (eps as last set). Host only. */
 int skipconv_get_desc(skipconv_t h, skipconv_desc* d);
 
-/* Kernels one step launches: *fused = 1 for the single-pass kernel (gate,
- * local compaction and MFMA product in one launch), 0 for the gate +
- * compaction + convolution pipeline. Host only. */
+/* Kernels one step launches: *fused = 0 for the gate + compaction +
+ * convolution pipeline, 1 for the single-pass kernel (gate, local compaction
+ * and MFMA product in one launch) with the weights staged in LDS, 2 for the
+ * single-pass kernel whose waves hold their weight fragments in registers
+ * (tiles of <= 8 x 8 sites, shapes it is built for). Host only. */
 int skipconv_pipeline(skipconv_t h, int32_t* fused);
 
 /* ---- introspection (tests and benchmarks; each synchronises `stream`) ---- */

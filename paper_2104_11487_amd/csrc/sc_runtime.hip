@@ -1005,7 +1005,7 @@ int skipconv_activation(skipconv_t h, const void** y) {
 int skipconv_pipeline(skipconv_t h, int32_t* fused) {
   if (!h) return SKIPCONV_E_STATE;
   if (!fused) return SKIPCONV_E_INVALID_ARG;
-  *fused = h->g.fused ? 1 : 0;
+  *fused = h->g.fused ? (h->g.f_rb ? 2 : 1) : 0;
   return SKIPCONV_OK;
 }
 

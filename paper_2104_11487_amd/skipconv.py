@@ -383,6 +383,11 @@ class SkipConv:
     def fused(self) -> bool:
         return bool(skipconv_pipeline(self.handle))
 
+    @property
+    def fused_variant(self) -> int:
+        """0 split pipeline, 1 single-pass kernel with LDS weights, 2 with register weights."""
+        return skipconv_pipeline(self.handle)
+
     def set_eps(self, eps: float):
         skipconv_set_eps(self.handle, eps)
         self.desc.eps = eps

@@ -407,6 +407,51 @@ def test_pipeline_selection():
     assert not S.SkipConv(w16, n=1, h=32, w=32, block=8).fused
     w3 = to_device(weight_storage(syn.he_weights(64, 3, 3, seed=1), "bf16"), "bf16")
     assert not S.SkipConv(w3, n=1, h=32, w=32, block=1).fused
+    # 8 x 8 tiles take the variant whose waves hold their weight fragments in
+    # registers where it is built for the shape (64 -> 64, 3 x 3: K = 576);
+    # larger K and 16 x 16 tiles stage the weights in LDS
+    assert S.SkipConv(w, n=1, h=128, w=96, block=8).fused_variant == 2
+    assert S.SkipConv(w, n=1, h=128, w=96, block=1).fused_variant == 2
+    w128 = to_device(weight_storage(syn.he_weights(128, 128, 3, seed=1), "bf16"), "bf16")
+    assert S.SkipConv(w128, n=1, h=32, w=32, block=8).fused_variant == 1
+    assert S.SkipConv(w, n=1, h=64, w=64, block=16).fused_variant == 1
+
+
+# One shape per build of the single-pass kernel whose waves hold their weight
+# fragments in registers (variant 2), and shapes that stage the weights in LDS
+# (variant 1), on frames whose sizes leave edge tiles, with a reset mid-stream:
+# (n, h, w, c_in, c_out, k, stride, block, variant)
+FUSED_SHAPES = [
+    (1, 36, 44, 32, 32, 3, 1, 8, 2),
+    (1, 36, 44, 64, 32, 3, 1, 4, 2),
+    (1, 29, 37, 32, 64, 3, 1, 8, 2),
+    (2, 24, 40, 64, 64, 3, 1, 2, 2),
+    (1, 36, 28, 64, 128, 3, 1, 8, 2),
+    (1, 27, 21, 192, 192, 1, 1, 8, 2),
+    (1, 40, 34, 32, 64, 3, 2, 1, 2),
+    (1, 22, 26, 64, 64, 3, 1, 3, 2),
+    (1, 30, 26, 128, 128, 3, 1, 8, 1),
+    (1, 40, 36, 64, 64, 3, 1, 16, 1),
+]
+
+
+@pytest.mark.parametrize("case", FUSED_SHAPES, ids=[f"fused{i}" for i in range(len(FUSED_SHAPES))])
+def test_fused_variants(case):
+    n, h, w, ci, co, k, s, b, variant = case
+    rng = np.random.Generator(np.random.PCG64(2000 + sum(case)))
+    wt = rng.normal(0, (2.0 / (k * k * ci)) ** 0.5, (co, ci, k, k)).astype(np.float32)
+    probe = S.SkipConv(to_device(weight_storage(wt, "bf16"), "bf16"), n=n, h=h, w=w, stride=s, block=b)
+    assert probe.fused_variant == variant, (case, probe.fused_variant)
+    probe.close()
+    x = rng.random((n, h, w, ci), dtype=np.float32)
+    frames = [x]
+    for t in range(5):
+        x = x.copy()
+        y0, x0 = (5 * t) % max(1, h - 6), (7 * t) % max(1, w - 6)
+        x[:, y0:y0 + 6, x0:x0 + 6] = rng.random((n, min(6, h - y0), min(6, w - x0), ci), dtype=np.float32)
+        x += rng.normal(0, 0.002, x.shape).astype(np.float32)
+        frames.append(x)
+    run_single(frames, wt, dtype="bf16", eps=0.6, block=b, stride=s, tag=f"fused {case}", resets=(4,))
 
 
 # ------------------------------------------------------ Output-Norm gate --
