@@ -510,20 +510,22 @@ __device__ __forceinline__ void store_piece(const FusedParams& p, size_t o, cons
 
 // ---------------------------------------------------------------------------
 // Register-operand kernel for tiles of <= 8 x 8 sites (64 product rows, 4
-// M-tiles). Wave w = kp * NG + ng owns N-tiles 2ng, 2ng + 1 and k-steps
+// M-tiles, NT 16-column N-tiles). Wave w = (kp * MG + mg) * NG + ng owns
+// N-tiles ng * WN .. + WN - 1, M-tiles mg * MT .. + MT - 1 and k-steps
 // [kp * ksteps / KP, (kp + 1) * ksteps / KP): KPS or KPS - 1 of them (the
 // instantiation is chosen so). Per tile LDS carries the residual fragments
-// (each read by the NG waves of a k-part) and the KP partial sums; the
-// weights come from global memory (L2) once. Rows outside the tile read
-// pixel (tap) of the halo like row 0: their columns of the product are
+// (each read by the NG waves of a k-part and M-group) and the KP partial
+// sums; the weights come from global memory (L2) once. Rows outside the tile
+// read pixel (tap) of the halo like row 0: their columns of the product are
 // discarded, and a site's outputs depend on its own column only.
 // MODE bit 0: emit the successor's residual; bit 1: chained input.
-template <int NG, int KPS, int MODE>
+template <int NT, int WN, int MT, int KPS, int MODE>
 __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
   constexpr bool EMIT = (MODE & 1) != 0;
   constexpr bool CHAIN = (MODE & 2) != 0;
-  constexpr int NT = 2 * NG;        // 16-column tiles of the output
-  constexpr int KP = kWaves / NG;   // k-step parts
+  constexpr int NG = NT / WN;        // wave groups along N
+  constexpr int MG = 4 / MT;         // wave groups along M
+  constexpr int KP = kWaves / (NG * MG);  // k-step parts
   constexpr int EP = NT / 2;        // epilogue pieces per thread: 64 sites x 4 NT pieces / 512
   constexpr int PROW = NT * 64 + 16;  // LDS bytes per site row of one partial (padded)
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
@@ -549,17 +551,17 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
   // e / (4 NT), channels 4 (e % (4 NT)) ..). All are in flight together, and
   // no load is left between the gate and the product.
   const int wv = __builtin_amdgcn_readfirstlane(wave);
-  const int ng = wv % NG, kp = wv / NG;
+  const int ng = wv % NG, mg = (wv / NG) % MG, kp = wv / (NG * MG);
   const bool mma = kp < KP;
   const int ks_lo = mma ? kp * p.ksteps / KP : 0;
   const int nks = mma ? (kp + 1) * p.ksteps / KP - ks_lo : 0;
-  bf16x8 bw[KPS][2];
+  bf16x8 bw[KPS][WN];
   {
-    const bf16x8* src = static_cast<const bf16x8*>(p.wpack) + ((size_t)ks_lo * NT + ng * 2) * 64 + lane;
+    const bf16x8* src = static_cast<const bf16x8*>(p.wpack) + ((size_t)ks_lo * NT + ng * WN) * 64 + lane;
 #pragma unroll
     for (int st = 0; st < KPS; ++st)
 #pragma unroll
-      for (int j = 0; j < 2; ++j) bw[st][j] = src[((size_t)(st < nks ? st : 0) * NT + j) * 64];
+      for (int j = 0; j < WN; ++j) bw[st][j] = src[((size_t)(st < nks ? st : 0) * NT + j) * 64];
   }
   const HaloWalk hwk = make_walk<kThreads, true>(g, T, cm, threadIdx.x);
   HaloBatch hb;
@@ -585,14 +587,32 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
 
   for (int i = threadIdx.x; i < kMaxTileBlocks; i += kThreads) blk_flag[i] = 0u;
   if (threadIdx.x == 0) tile_on = 0u;
-  // product rows: the 64 sites of the tile in row-major order
-  int abase[4];
+  // product rows: M-tile i holds 16 sites of the tile. For 8 x 8 tiles they
+  // are two tile rows rd apart, rd chosen so that rd * (halo width) = 8
+  // (mod 16) when possible: a fragment read (16 lanes x 16 bytes, pixel stride
+  // an odd number of 16-byte units) then touches 16 distinct bank groups.
+  // Other tiles take the sites in row-major order.
+  int abase[MT], msite[MT];
+  {
+    const int hw = T.hw;
+    const int rd = (4 * hw) % 16 == 8 ? 4 : ((2 * hw) % 16 == 8 ? 2 : 1);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = i * 16 + r16;
-    const int ly = qdiv(row, T.inv_ts), lx = row - ly * g.ts;
-    const bool ok = ly < T.oh && lx < T.ow;
-    abase[i] = (ok ? (ly * g.stride) * T.hw + lx * g.stride : 0) * p.pstride + kq * 16;
+    for (int ii = 0; ii < MT; ++ii) {
+      const int i = mg * MT + ii;
+      int ly, lx;
+      if (g.ts == 8) {
+        const int y0 = rd == 4 ? i : (rd == 2 ? (i & 1) + 4 * (i >> 1) : 2 * i);
+        ly = y0 + (r16 >> 3) * rd;
+        lx = r16 & 7;
+      } else {
+        const int row = i * 16 + r16;
+        ly = qdiv(row, T.inv_ts);
+        lx = row - ly * g.ts;
+      }
+      msite[ii] = ly * g.ts + lx;
+      const bool ok = ly < T.oh && lx < T.ow;
+      abase[ii] = (ok ? (ly * g.stride) * hw + lx * g.stride : 0) * p.pstride + kq * 16;
+    }
   }
 
   // 2. halo use (and further rounds for large halos)
@@ -601,10 +621,9 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
   // before the x_t copy stores go out, so the product and the epilogue wait
   // for nothing
 #pragma unroll
-  for (int st = 0; st < KPS; ++st) {
-    settle(bw[st][0]);
-    settle(bw[st][1]);
-  }
+  for (int st = 0; st < KPS; ++st)
+#pragma unroll
+    for (int j = 0; j < WN; ++j) settle(bw[st][j]);
 #pragma unroll
   for (int h = 0; h < EP; ++h) {
     settle(zold[h]);
@@ -623,11 +642,11 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
   // 4. product over this wave's k-steps: the first KPS - 1 always run, the
   // last one when the wave has KPS (a wave-uniform branch); the tap and
   // channel offset of a step is wave-uniform
-  floatx4 acc[4][2];
+  floatx4 acc[MT][WN];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < MT; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+    for (int j = 0; j < WN; ++j) acc[i][j] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
   if (mma) {
     const int csteps = p.csteps, k = g.k, hw = T.hw;
     const int tap0 = ks_lo / csteps;
@@ -636,13 +655,13 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
     for (int st = 0; st < KPS; ++st) {
       if (st == KPS - 1 && nks < KPS) break;
       const int off = (kh * hw + kw) * p.pstride + cc * 64;
-      bf16x8 a[4];
+      bf16x8 a[MT];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = *reinterpret_cast<const bf16x8*>(halo + abase[i] + off);
+      for (int i = 0; i < MT; ++i) a[i] = *reinterpret_cast<const bf16x8*>(halo + abase[i] + off);
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < MT; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < WN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bw[st][j], a[i], acc[i][j], 0, 0, 0);
       if (++cc == csteps) {
         cc = 0;
@@ -653,13 +672,13 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
       }
     }
     // partial sums of this k-part: lane (r16, kq) holds channels
-    // (2ng + j) * 16 + 4kq .. + 3 of site 16i + r16
+    // (ng * WN + j) * 16 + 4kq .. + 3 of site msite[i]
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < MT; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-        *reinterpret_cast<floatx4*>(pbuf + (size_t)kp * 64 * PROW + (i * 16 + r16) * PROW +
-                                    ((ng * 2 + j) * 16 + kq * 4) * 4) = acc[i][j];
+      for (int j = 0; j < WN; ++j)
+        *reinterpret_cast<floatx4*>(pbuf + (size_t)kp * 64 * PROW + msite[i] * PROW +
+                                    ((ng * WN + j) * 16 + kq * 4) * 4) = acc[i][j];
   }
   lds_barrier();
 
@@ -928,13 +947,13 @@ hipError_t launch_fused_t(const FusedParams& p, int grid, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <int NG, int KPS>
+template <int NT, int WN, int MT, int KPS>
 hipError_t launch_rb_t(const FusedParams& p, int grid, hipStream_t st) {
   switch ((p.emit ? 1 : 0) | (p.g.rin ? 2 : 0)) {
-    case 0: hipLaunchKernelGGL((fused_rb_kernel<NG, KPS, 0>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
-    case 1: hipLaunchKernelGGL((fused_rb_kernel<NG, KPS, 1>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
-    case 2: hipLaunchKernelGGL((fused_rb_kernel<NG, KPS, 2>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
-    default: hipLaunchKernelGGL((fused_rb_kernel<NG, KPS, 3>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+    case 0: hipLaunchKernelGGL((fused_rb_kernel<NT, WN, MT, KPS, 0>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+    case 1: hipLaunchKernelGGL((fused_rb_kernel<NT, WN, MT, KPS, 1>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+    case 2: hipLaunchKernelGGL((fused_rb_kernel<NT, WN, MT, KPS, 2>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+    default: hipLaunchKernelGGL((fused_rb_kernel<NT, WN, MT, KPS, 3>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
   }
   return hipGetLastError();
 }
@@ -962,12 +981,12 @@ int prepare_fused_t(const FusedParams& p) {
   return std::min(std::min(a, b), c);
 }
 
-template <int NG, int KPS>
+template <int NT, int WN, int MT, int KPS>
 int prepare_rb_t(const FusedParams& p) {
-  const int a = prepare_kernel(fused_rb_kernel<NG, KPS, 0>, p);
-  const int b = prepare_kernel(fused_rb_kernel<NG, KPS, 2>, p);
-  const int c = p.emit ? std::min(prepare_kernel(fused_rb_kernel<NG, KPS, 1>, p),
-                                  prepare_kernel(fused_rb_kernel<NG, KPS, 3>, p))
+  const int a = prepare_kernel(fused_rb_kernel<NT, WN, MT, KPS, 0>, p);
+  const int b = prepare_kernel(fused_rb_kernel<NT, WN, MT, KPS, 2>, p);
+  const int c = p.emit ? std::min(prepare_kernel(fused_rb_kernel<NT, WN, MT, KPS, 1>, p),
+                                  prepare_kernel(fused_rb_kernel<NT, WN, MT, KPS, 3>, p))
                        : a;
   return std::min(std::min(a, b), c);
 }
@@ -979,22 +998,37 @@ hipError_t launch_fused_tiles(uint32_t* table, int grid, int tiles_y, int tiles_
   return hipGetLastError();
 }
 
-// Register-operand instantiations (NG = ntiles_n / 2, KPS = k-steps per wave
-// rounded up to an instantiated value); 0 when none covers the layer.
+// Register-operand builds: (16-column tiles, N-tiles per wave, M-tiles per
+// wave, k-steps per wave). Waves per k-part = (NT / WN) * (4 / MT); each wave
+// takes KPS or KPS - 1 k-steps. All waves hold every M-tile: with fewer, the
+// waves of one k-part would each load the same weight fragments (measured
+// slower for 64 -> 64 layers: the weight traffic from L2 doubles).
+namespace {
+struct RbBuild {
+  int nt, wn, mt, kps;
+};
+constexpr RbBuild kRbBuilds[] = {
+    {2, 2, 4, 2}, {2, 2, 4, 3}, {4, 2, 4, 3}, {4, 2, 4, 5}, {8, 2, 4, 9}, {12, 2, 4, 6},
+};
+}  // namespace
+
 int fused_rb_kps(int ntiles_n, int ksteps, int halo_w, int chunks) {
   // the kernel walks the halo in whole rows, in one round of kItems rows per thread
   const int rw = halo_w * chunks;
   if (rw > kThreads || (halo_w + kThreads / rw - 1) / (kThreads / rw) > kItems) return 0;
-  static const int kNG[] = {1, 2, 4, 6};
-  static const int kKPS[4][2] = {{2, 3}, {3, 5}, {9, 9}, {6, 6}};
-  for (int i = 0; i < 4; ++i) {
-    if (ntiles_n != 2 * kNG[i]) continue;
-    const int kp = kWaves / kNG[i];
-    const int need = (ksteps + kp - 1) / kp;
-    for (int j = 0; j < 2; ++j)  // each wave takes KPS - 1 or KPS k-steps
-      if (need <= kKPS[i][j] && ksteps / kp >= kKPS[i][j] - 1) return kKPS[i][j];
+  for (int i = 0; i < (int)(sizeof(kRbBuilds) / sizeof(kRbBuilds[0])); ++i) {
+    const RbBuild& b = kRbBuilds[i];
+    if (b.nt != ntiles_n) continue;
+    const int kp = kWaves / ((b.nt / b.wn) * (4 / b.mt));
+    if ((ksteps + kp - 1) / kp <= b.kps && ksteps / kp >= b.kps - 1) return i + 1;  // build index + 1
   }
   return 0;
+}
+
+// k-parts of the register-operand build `rb` (fused_rb_kps) for the LDS layout.
+int fused_rb_kparts(int rb) {
+  const RbBuild& b = kRbBuilds[rb - 1];
+  return kWaves / ((b.nt / b.wn) * (4 / b.mt));
 }
 
 // LDS-operand instantiations: tiles of <= 8 x 8 sites use 4 x 2 waves of one
@@ -1002,13 +1036,13 @@ int fused_rb_kps(int ntiles_n, int ksteps, int halo_w, int chunks) {
 // per wave = ntiles_n / 2.
 int prepare_fused(const FusedParams& p) {
   if (p.rbk) {
-    switch (p.ntiles_n * 100 + p.rbk) {
-      case 202: return prepare_rb_t<1, 2>(p);
-      case 203: return prepare_rb_t<1, 3>(p);
-      case 403: return prepare_rb_t<2, 3>(p);
-      case 405: return prepare_rb_t<2, 5>(p);
-      case 809: return prepare_rb_t<4, 9>(p);
-      case 1206: return prepare_rb_t<6, 6>(p);
+    switch (p.rbk) {
+      case 1: return prepare_rb_t<2, 2, 4, 2>(p);
+      case 2: return prepare_rb_t<2, 2, 4, 3>(p);
+      case 3: return prepare_rb_t<4, 2, 4, 3>(p);
+      case 4: return prepare_rb_t<4, 2, 4, 5>(p);
+      case 5: return prepare_rb_t<8, 2, 4, 9>(p);
+      case 6: return prepare_rb_t<12, 2, 4, 6>(p);
       default: return 0;
     }
   }
@@ -1035,13 +1069,13 @@ int prepare_fused(const FusedParams& p) {
 
 hipError_t launch_fused(const FusedParams& p, int grid, hipStream_t st) {
   if (p.rbk) {
-    switch (p.ntiles_n * 100 + p.rbk) {
-      case 202: return launch_rb_t<1, 2>(p, grid, st);
-      case 203: return launch_rb_t<1, 3>(p, grid, st);
-      case 403: return launch_rb_t<2, 3>(p, grid, st);
-      case 405: return launch_rb_t<2, 5>(p, grid, st);
-      case 809: return launch_rb_t<4, 9>(p, grid, st);
-      case 1206: return launch_rb_t<6, 6>(p, grid, st);
+    switch (p.rbk) {
+      case 1: return launch_rb_t<2, 2, 4, 2>(p, grid, st);
+      case 2: return launch_rb_t<2, 2, 4, 3>(p, grid, st);
+      case 3: return launch_rb_t<4, 2, 4, 3>(p, grid, st);
+      case 4: return launch_rb_t<4, 2, 4, 5>(p, grid, st);
+      case 5: return launch_rb_t<8, 2, 4, 9>(p, grid, st);
+      case 6: return launch_rb_t<12, 2, 4, 6>(p, grid, st);
       default: return hipErrorInvalidValue;
     }
   }

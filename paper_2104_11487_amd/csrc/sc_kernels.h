@@ -124,7 +124,7 @@ struct FusedParams {
   int zero_pix;            // index of the all-zero pixel just past the halo
   int pstage;              // LDS floats per halo pixel of chunk sums: (c_in / 8) | 1
   int off_b, off_halo, off_a, off_part, lds_bytes;  // off_b: weights, or partial sums (rb)
-  int rbk;                 // register-operand kernel: k-steps per wave it is instantiated for (0: LDS operand)
+  int rbk;                 // register-operand kernel: its build (fused_rb_kps), 0: LDS operand
   const uint32_t* tiles;   // per workgroup: its tile, tx | ty << 10 | n << 20 (XCD-aware order)
   float inv_ts, inv_blk, inv_hw, inv_chk;  // 1/ts, 1/block, 1/halo width, 1/(c_in / 8), rounded to fp32
   // residual emission for a chained successor (act must be set): r = y_new - y_old
@@ -139,10 +139,12 @@ int prepare_fused(const FusedParams& p);  // create time: LDS attribute; workgro
 // Tile table of the fused kernel: entry b = the tile workgroup b runs, packed
 // tx | ty << 10 | n << 20, in the XCD-aware order (tiles_x, tiles_y <= 1024).
 hipError_t launch_fused_tiles(uint32_t* table, int grid, int tiles_y, int tiles_x, hipStream_t st);
-// k-steps per wave of the register-operand fused kernel instantiated for this
-// shape (ntiles_n 16-column tiles, ksteps k-steps, a square halo of halo_w
-// pixels a side, chunks = c_in / 8), 0 if none covers it.
+// Build of the register-operand fused kernel for this shape (ntiles_n
+// 16-column tiles, ksteps k-steps, a square halo of halo_w pixels a side,
+// chunks = c_in / 8): its index + 1, or 0 if none covers it; and the number of
+// k-parts whose partial sums that build keeps in LDS.
 int fused_rb_kps(int ntiles_n, int ksteps, int halo_w, int chunks);
+int fused_rb_kparts(int rb);
 
 hipError_t launch_gate(const GateParams& p, int dtype, int vec, int grid, size_t lds_bytes,
                        hipStream_t st);

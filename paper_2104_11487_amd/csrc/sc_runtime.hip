@@ -50,7 +50,7 @@ struct Geometry {
   bool fused;           // single-pass kernel instead of gate + compaction + conv
   int f_ts, f_tiles_y, f_tiles_x, f_grid, f_copy_in_halo;
   int f_kc, f_nchunks, f_nbuf, f_mw, f_pstride, f_zero_pix, f_off_b, f_off_halo, f_off_a, f_lds;
-  int f_rb;             // register-operand fused kernel: its k-steps per wave (0: LDS operand)
+  int f_rb;             // register-operand fused kernel: its build (0: LDS operand)
   int f_pstage, f_off_part;
   int vec;              // gate load width (elements)
   size_t elem;
@@ -274,7 +274,7 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
       // the shape; LDS holds the partial sums of its k-parts instead of weights
       const int rb = mw == 1 ? sc::fused_rb_kps(G.ntn, G.ksteps, hh, d->c_in / 8) : 0;
       if (rb) {
-        const long kparts = 8 / (G.ntn / 2);
+        const long kparts = sc::fused_rb_kparts(rb);
         b_bytes = kparts * 64 * ((long)G.ntn * 64 + 16);
       } else if (whole + halo_b + a_b + part_b > kFusedLdsLimit) {
         kc = std::max(1, 16 / G.ntn);
