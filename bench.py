@@ -172,15 +172,16 @@ def clip_active(layer, frames_dev):
     return np.array(sites, np.int64), np.array(blocks, np.int64)
 
 
-def event_period(nfr: int) -> int:
+def event_period(nfr: int, steps: int) -> int:
     """Sampling period of the per-kernel events of the multi-kernel pipeline.
 
     Coprime with the clip length, so the sampled steps walk through every clip
-    position, and long enough (>= 17 steps) that the event records, each a
-    marker packet on the stream, add little to the timed wall clock.
+    position; as long as possible (up to 17 steps: the event records, marker
+    packets on the stream, then add little to the timed wall clock) while the
+    timed steps still give at least two samples of every clip position.
     """
-    for e in (17, 19, 23, 29, 31, 37):
-        if np.gcd(e, nfr) == 1:
+    for e in (17, 13, 11, 7, 5, 3, 2):
+        if np.gcd(e, nfr) == 1 and steps // e >= 2 * nfr:
             return e
     return 1
 
@@ -204,7 +205,7 @@ def measure_point(make_layer, frames_dev, steps, warmup, geom, *, label, events=
     if warmup:
         _, _, _, _, pos = run_steps(layer, frames_dev, warmup, pos)
     pos = (pos + nfr - 1) // nfr * nfr  # timed steps start at a clip boundary
-    every = event_period(nfr) if events and not fused else 0
+    every = event_period(nfr, steps) if events and not fused else 0
     blk = event_blocks(nfr) if events and fused else None
     wall, gate_ms, conv_ms, tpos, _ = run_steps(layer, frames_dev, steps, pos, every=every, block=blk)
     layer.close()
