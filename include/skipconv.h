@@ -93,13 +93,19 @@ enum { SKIPCONV_ACT_NONE = 0, SKIPCONV_ACT_IDENTITY = 1, SKIPCONV_ACT_RELU = 2 }
  * step updated (fp32, plus its bf16 rounding for bf16 layers) and r = 0 at
  * the blocks only the previous step updated; see skipconv_step_chained.
  * TRANSLATE: allow skipconv_step_translated (a second z slot and two block
- * lists in the workspace); not combinable with EMIT_RESIDUAL. */
+ * lists in the workspace); not combinable with EMIT_RESIDUAL.
+ * LARGE_GATE_TILES: the split pipeline's gate kernel takes tiles of 32 x 32
+ * output sites (instead of 16 x 16 or 8 x 8) when its chunk sums combine in
+ * lane groups (see skipconv_gate_tile) and such a tile holds at most 256
+ * blocks: fewer halo pixels read twice, four times fewer workgroups. A tuning
+ * knob; the results are the same. */
 enum {
   SKIPCONV_FLAG_KEEP_STATS = 1u,
   SKIPCONV_FLAG_FORCE_DENSE = 2u,
   SKIPCONV_FLAG_SPLIT_PIPELINE = 4u,
   SKIPCONV_FLAG_EMIT_RESIDUAL = 8u,
-  SKIPCONV_FLAG_TRANSLATE = 16u
+  SKIPCONV_FLAG_TRANSLATE = 16u,
+  SKIPCONV_FLAG_LARGE_GATE_TILES = 32u
 };
 
 typedef struct skipconv_desc {
@@ -233,6 +239,13 @@ int skipconv_get_desc(skipconv_t h, skipconv_desc* d);
  * single-pass kernel whose waves hold their weight fragments in registers
  * (tiles of <= 8 x 8 sites, shapes it is built for). Host only. */
 int skipconv_pipeline(skipconv_t h, int32_t* fused);
+
+/* Gate tiling of the split pipeline: *ts = output sites per side of one gate
+ * workgroup's tile (whole blocks, or a divisor of the block side), *lane_sum =
+ * 1 when a pixel's 8-channel chunk sums are added in registers by a group of
+ * 4, 8 or 16 lanes (norm gates with 32, 64 or 128 input channels), 0 when
+ * they are staged in LDS. Host only. */
+int skipconv_gate_tile(skipconv_t h, int32_t* ts, int32_t* lane_sum);
 
 /* ---- introspection (tests and benchmarks; each synchronises `stream`) ---- */
 

@@ -49,7 +49,6 @@ constexpr int kThreads = 512;
 constexpr int kWaves = kThreads / 64;
 constexpr int kLoadWaves = 2;  // fused_kernel: waves that copy the weights during the halo phase
 constexpr int kItems = 4;      // halo items per thread whose loads are in flight together
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float floatx2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
@@ -106,29 +105,6 @@ __device__ void emit_clear(const FusedParams& p, int n, int oy0, int ox0, int oh
     const size_t gb = ((size_t)n * g.hb + bi0 + by) * g.wb + bj0 + bx;
     p.prev_mask[gb] = (cur && cur[by * tb_w + bx] != 0u) ? 1 : 0;
   }
-}
-
-// Value of lane (this lane + J) of the same 16-lane row (DPP row_shl:J).
-template <int J>
-__device__ __forceinline__ float row_shl(float v) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x100 + J, 0xf, 0xf, false));
-}
-
-template <int NC, int J>
-__device__ __forceinline__ float group_sum_from(float acc, float v) {
-  if constexpr (J < NC) {
-    return group_sum_from<NC, J + 1>(add_rn(acc, row_shl<J>(v)), v);
-  } else {
-    return acc;
-  }
-}
-
-// Ordered sum (from +0, ascending lanes) of the NC values held by lanes
-// l .. l + NC - 1 of one 16-lane row, valid in lane l (NC <= 16; the group
-// must not cross a row boundary). Lane-to-lane moves only, no LDS traffic.
-template <int NC>
-__device__ __forceinline__ float group_sum(float v) {
-  return group_sum_from<NC, 1>(add_rn(0.0f, v), v);
 }
 
 // Workgroup barrier that orders LDS accesses only: outstanding global loads

@@ -17,8 +17,10 @@
 // One workgroup owns a TS x TS tile of output sites (whole blocks). One
 // thread takes one 8-channel chunk of one halo pixel at a time (a 16-byte
 // load of each frame for bf16; consecutive threads read consecutive chunks,
-// eight chunks in flight per thread), forms the chunk sum and parks it in LDS;
-// then one thread per halo pixel adds its chunk sums in order. Input pixels
+// eight chunks in flight per thread) and forms the chunk sum. With 4, 8 or 16
+// chunks per pixel the pixel's lanes add their chunk sums in order through
+// DPP lane shifts; otherwise the sums are parked in LDS and one thread per
+// halo pixel adds them in order. Input pixels
 // the tile owns are copied into the spare x_{t-1} slot on the way (ping-pong:
 // the slot being read is never written in the same step). Every workgroup
 // then writes its block flags. A second, one-workgroup kernel scans all
@@ -128,6 +130,105 @@ __device__ void halo_partials(const GateParams& p, int n, int iy0, int ix0, int 
   }
 }
 
+// Raw buffer resource over `bytes` bytes at `base`: a load at an offset at or
+// beyond `bytes` returns zeros and a store there is dropped, without a memory
+// access (range-checked buffer addressing of the CDNA ISA).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t frame_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+constexpr uint32_t kOutOfRange = 0x80000000u;  // byte offset past every frame resource
+// Cache policy of the x_{t-1} copy: non-temporal (streamed past the caches),
+// so that the frame being written does not evict the two frames the
+// convolution reads next.
+constexpr int kNonTemporal = 2;
+
+// Halo of a norm gate with NC = 4, 8 or 16 chunks per pixel (bf16 or fp32
+// frames). Items are taken in flat order (consecutive threads, consecutive
+// chunks), so a pixel's chunks sit in one aligned group of NC lanes: the
+// group's first lane adds the chunk sums in ascending order through DPP row
+// shifts and writes a[] of the pixel directly (no per-chunk staging in LDS, no
+// second pass). Loads and stores go through buffer resources over image n
+// (h * w * c * 4 < 2^31 bytes, checked by the host) with 32-bit byte offsets:
+// items outside the frame (or, for x_{t-1}, outside the translated frame)
+// load at an out-of-range offset and read zeros, and the x_t chunks of pixels
+// the tile does not own are stored out of range (dropped), so every item
+// issues the same loads and stores. A chunk is one 16-byte word per frame
+// (bf16) or two (fp32). The non-temporal copy to the spare x_{t-1} slot
+// follows the round's use.
+template <typename T, int NC>
+__device__ void halo_lane_sums(const GateParams& p, int n, int iy0, int ix0, int hh, int hw, int own_y0,
+                               int own_y1, int own_x0, int own_x1, float* a_halo) {
+  constexpr int kWords = sizeof(T) == 2 ? 1 : 2;  // 16-byte words per chunk and frame
+  constexpr int kItems = 8 / kWords;
+  constexpr int kLg = NC == 4 ? 2 : (NC == 8 ? 3 : 4);
+  const uint32_t img_bytes = (uint32_t)((size_t)p.h * p.w * p.c * sizeof(T));
+  const size_t img = (size_t)n * p.h * p.w * p.c;
+  const auto rt = frame_rsrc(static_cast<const T*>(p.x_t) + img, img_bytes);
+  const auto rp = frame_rsrc(static_cast<const T*>(p.no_prev ? p.x_t : p.x_prev) + img, img_bytes);
+  const bool keep_on = p.x_keep != nullptr && p.copy_in_halo;
+  const auto rk = frame_rsrc(keep_on ? static_cast<T*>(p.x_keep) + img : nullptr, keep_on ? img_bytes : 0u);
+  const int total = hh * hw * NC;
+  const float inv_hw = 1.0f / (float)hw;
+  const int wave0 = threadIdx.x & ~63;
+  for (int base = 0; base < total; base += kGateThreads * kItems) {
+    u32x4 vt[kItems][kWords], vp[kItems][kWords];
+    uint32_t koff[kItems];
+    // the thread index, opaque to loop-invariant code motion: the per-item
+    // terms below are recomputed each round rather than held in registers
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+#pragma unroll
+    for (int u = 0; u < kItems; ++u) {
+      const int idx = base + u * kGateThreads + tid;
+      const int q = idx >> kLg, ch = idx & (NC - 1);
+      const int hy = qdiv(q, inv_hw), hx = q - hy * hw;
+      const int y = iy0 + hy, x = ix0 + hx;
+      const bool in = idx < total && y >= 0 && y < p.h && x >= 0 && x < p.w;
+      const bool own = in && keep_on && y >= own_y0 && y < own_y1 && x >= own_x0 && x < own_x1;
+      const uint32_t off = (uint32_t)(((y * p.w + x) * p.c + ch * kChunk) * (int)sizeof(T));
+      // x_{t-1} under the step's translation (zero outside the frame)
+      const int yp = y - p.sy, xq = x - p.sx;
+      const bool pin = in && !p.no_prev && yp >= 0 && yp < p.h && xq >= 0 && xq < p.w;
+      const uint32_t po = (uint32_t)(((yp * p.w + xq) * p.c + ch * kChunk) * (int)sizeof(T));
+      koff[u] = own ? off : kOutOfRange;
+#pragma unroll
+      for (int wd = 0; wd < kWords; ++wd) {
+        vt[u][wd] = __builtin_amdgcn_raw_buffer_load_b128(rt, (in ? off : kOutOfRange) + 16 * wd, 0, 0);
+        vp[u][wd] = __builtin_amdgcn_raw_buffer_load_b128(rp, (pin ? po : kOutOfRange) + 16 * wd, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kItems; ++u) {
+      if (base + u * kGateThreads + wave0 >= total) break;  // wave-uniform
+      float sum = 0.0f;
+      if constexpr (kWords == 1) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {  // channels 2e (low half) and 2e + 1 (high half)
+          const uint32_t a = vt[u][0][e], b = vp[u][0][e];
+          const float r0 = __fsub_rn(__uint_as_float(a << 16), __uint_as_float(b << 16));
+          const float r1 = __fsub_rn(__uint_as_float(a & 0xffff0000u), __uint_as_float(b & 0xffff0000u));
+          sum = add_rn(sum, term(r0, p.norm_p));
+          sum = add_rn(sum, term(r1, p.norm_p));
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < kChunk; ++j) {  // channel j: word j / 4, component j % 4
+          const float r = __fsub_rn(__uint_as_float(vt[u][j >> 2][j & 3]), __uint_as_float(vp[u][j >> 2][j & 3]));
+          sum = add_rn(sum, term(r, p.norm_p));
+        }
+      }
+      const float acc = group_sum<NC>(sum);
+      const int idx = base + u * kGateThreads + threadIdx.x;
+      if (idx < total && (idx & (NC - 1)) == 0) a_halo[idx >> kLg] = acc;
+    }
+#pragma unroll
+    for (int u = 0; u < kItems; ++u)
+#pragma unroll
+      for (int wd = 0; wd < kWords; ++wd)
+        __builtin_amdgcn_raw_buffer_store_b128(vt[u][wd], rk, koff[u] + 16 * wd, 0, kNonTemporal);
+  }
+}
+
 // Learned gate (Eq. 8 at inference): one thread per halo pixel forms, for
 // every tap (kh, kw), a[q, tap] = sum_c phi[tap][c] * r[q, c] in the canonical
 // chunked order (8 channels ascending within a chunk from +0, chunk sums
@@ -195,7 +296,9 @@ __device__ void learned_halo(const GateParams& p, int n, int iy0, int ix0, int h
   }
 }
 
-template <typename T, int VEC, int KL>
+// KL: learned gate kernel size (0 = norm gate). NC > 0: bf16 norm gate with
+// NC chunks per pixel, chunk sums combined in lane groups (halo_lane_sums).
+template <typename T, int VEC, int KL, int NC>
 __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
   extern __shared__ float lds[];
   __shared__ uint32_t blk_flag[kMaxTileBlocks];
@@ -258,7 +361,9 @@ __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
     }
   }
 
-  if constexpr (KL == 0) {
+  if constexpr (NC > 0) {
+    halo_lane_sums<T, NC>(p, n, iy0, ix0, hh, hw, own_y0, own_y1, own_x0, own_x1, a_halo);
+  } else if constexpr (KL == 0) {
     halo_partials<T, VEC>(p, n, iy0, ix0, hh, hw, own_y0, own_y1, own_x0, own_x1, part);
     __syncthreads();
     for (int q = threadIdx.x; q < hh * hw; q += kGateThreads) {
@@ -458,12 +563,26 @@ __global__ void __launch_bounds__(kScanThreads) compact_kernel(uint8_t* block_ma
 
 template <typename T, int VEC>
 static hipError_t launch_gate_t(const GateParams& p, int grid, size_t lds_bytes, hipStream_t st) {
+  const int nchk = (p.c + kChunk - 1) / kChunk;
+  if (p.lane_sum) {
+    // the host sized the LDS without chunk-sum staging: only these shapes
+    if constexpr (VEC == kChunk) {
+      if (p.learned != 0 || !(nchk == 4 || nchk == 8 || nchk == 16) || (long)p.h * p.w * p.c * 4 >= (1L << 31))
+        return hipErrorInvalidValue;
+      if (nchk == 16) hipLaunchKernelGGL((gate_kernel<T, VEC, 0, 16>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p);
+      else if (nchk == 8) hipLaunchKernelGGL((gate_kernel<T, VEC, 0, 8>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p);
+      else hipLaunchKernelGGL((gate_kernel<T, VEC, 0, 4>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p);
+      return hipGetLastError();
+    } else {
+      return hipErrorInvalidValue;
+    }
+  }
   switch (p.learned) {
-    case 0: hipLaunchKernelGGL((gate_kernel<T, VEC, 0>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p); break;
-    case 1: hipLaunchKernelGGL((gate_kernel<T, VEC, 1>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p); break;
-    case 3: hipLaunchKernelGGL((gate_kernel<T, VEC, 3>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p); break;
-    case 5: hipLaunchKernelGGL((gate_kernel<T, VEC, 5>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p); break;
-    case 7: hipLaunchKernelGGL((gate_kernel<T, VEC, 7>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p); break;
+    case 0: hipLaunchKernelGGL((gate_kernel<T, VEC, 0, 0>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p); break;
+    case 1: hipLaunchKernelGGL((gate_kernel<T, VEC, 1, 0>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p); break;
+    case 3: hipLaunchKernelGGL((gate_kernel<T, VEC, 3, 0>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p); break;
+    case 5: hipLaunchKernelGGL((gate_kernel<T, VEC, 5, 0>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p); break;
+    case 7: hipLaunchKernelGGL((gate_kernel<T, VEC, 7, 0>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

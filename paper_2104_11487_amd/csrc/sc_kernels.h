@@ -24,6 +24,7 @@ struct GateParams {
   int ts, tiles_y, tiles_x;     // tile side (sites) and tile grid per image
   int halo_floats;              // LDS floats reserved for the a[] halo
   int stage_stride;             // LDS floats of chunk sums per halo pixel (>= ceil(c/8), odd)
+  int lane_sum;                 // 1: chunk sums combined in lane groups, no staging (c / 8 in {4, 8, 16})
   int rows_per_batch;           // unused (whole halo staged at once)
   int copy_in_halo;             // 1: every owned input pixel lies in its tile's halo
   int norm_p, support, reference, force_dense, keep_stats;

@@ -39,6 +39,7 @@ size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 struct Geometry {
   int pad, h_out, w_out, hb, wb, nb;
   int ts, tiles_y, tiles_x, gate_grid, split_blocks;
+  int lane_sum;  // gate chunk sums combined in lane groups (no LDS staging)
   int hh_max, hw_max, halo_floats, stage_stride, rows_per_batch;
   size_t gate_lds;
   int copy_in_halo;
@@ -109,7 +110,8 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
   if ((d->flags & SKIPCONV_FLAG_EMIT_RESIDUAL) && (d->flags & SKIPCONV_FLAG_TRANSLATE))
     return fail(err, SKIPCONV_E_UNSUPPORTED, "EMIT_RESIDUAL and TRANSLATE cannot be combined");
   if (d->flags & ~(uint32_t)(SKIPCONV_FLAG_KEEP_STATS | SKIPCONV_FLAG_FORCE_DENSE | SKIPCONV_FLAG_SPLIT_PIPELINE |
-                             SKIPCONV_FLAG_EMIT_RESIDUAL | SKIPCONV_FLAG_TRANSLATE))
+                             SKIPCONV_FLAG_EMIT_RESIDUAL | SKIPCONV_FLAG_TRANSLATE |
+                             SKIPCONV_FLAG_LARGE_GATE_TILES))
     return fail(err, SKIPCONV_E_INVALID_ARG, "unknown flag bits");
   if (std::isnan(d->eps) || d->eps < 0.0f) return fail(err, SKIPCONV_E_INVALID_ARG, "eps must be >= 0");
   if (!depthwise && d->c_out > kMaxCout) return fail(err, SKIPCONV_E_UNSUPPORTED, "c_out > 256");
@@ -142,6 +144,13 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
   const int nchk = (d->c_in + 7) / 8;
   G.stage_stride = nchk | 1;
   G.learned = d->gate == SKIPCONV_GATE_LEARNED ? k : 0;
+  // norm gates with 4, 8 or 16 chunks per pixel add a pixel's chunk sums in
+  // registers (lane groups), without per-chunk staging in LDS; the kernel
+  // addresses one image with 32-bit byte offsets (fp32 frames of chained
+  // steps included)
+  const bool lane_sum = !G.learned && d->c_in % 8 == 0 && (nchk == 4 || nchk == 8 || nchk == 16) &&
+                        (long)d->h * d->w * d->c_in * 4 < (1L << 31);
+  G.lane_sum = lane_sum ? 1 : 0;
   // learned gate: phi is staged in LDS unless that alone would not fit
   const long phi_floats = (long)k * k * d->c_in;
   G.phi_in_lds = G.learned && phi_floats * 4 <= (long)kLdsLimit / 2;
@@ -151,13 +160,20 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
     if (G.learned)  // per-pixel, per-tap gate terms (+ the staged phi)
       return ((eh * ew * k * k + 3) / 4 * 4 + (G.phi_in_lds ? phi_floats : 0)) * 4;
     const long halo = (eh * ew + 3) / 4 * 4;
-    return (halo + eh * ew * G.stage_stride) * 4;
+    return (halo + (lane_sum ? 0 : eh * ew * G.stage_stride)) * 4;
   };
   {
+    const int t32 = b <= 32 ? b * (32 / b) : b;
     const int t16 = b <= 16 ? b * (16 / b) : b;
     const int t8 = b <= 8 ? b * (8 / b) : b;
-    const long n16 = (long)d->n * ((G.h_out + t16 - 1) / t16) * ((G.w_out + t16 - 1) / t16);
-    G.ts = (n16 < 512 && b <= 8) ? t8 : t16;
+    auto tiles_for = [&](int t) { return (long)d->n * ((G.h_out + t - 1) / t) * ((G.w_out + t - 1) / t); };
+    G.ts = (tiles_for(t16) < 512 && b <= 8) ? t8 : t16;
+    // on request, 32 x 32 tiles when the chunk sums combine in registers: a
+    // smaller share of re-read halo, but four times fewer workgroups (on
+    // 4 x 512 x 512 x 128 frames 16 x 16 tiles are faster)
+    if ((d->flags & SKIPCONV_FLAG_LARGE_GATE_TILES) && lane_sum && b <= 32 &&
+        (t32 / b) * (t32 / b) <= sc::kMaxTileBlocks && gate_lds_for(t32) <= (long)kLdsLimit)
+      G.ts = t32;
     if (G.learned && b <= 8) G.ts = t8;  // the per-tap learned gate is VALU-heavy: more, smaller tiles
     if (gate_lds_for(G.ts) > (long)kLdsLimit && b <= 8) G.ts = t8;
     // blocks larger than a tile that fits: 16 x 16 (or 8 x 8) tiles, one flag
@@ -507,7 +523,7 @@ sc::GateParams gate_params(skipconv_layer* h, const void* x_t, bool ref) {
   gp.h_out = g.h_out; gp.w_out = g.w_out; gp.k = d.kernel; gp.stride = d.stride; gp.pad = g.pad;
   gp.block = d.block; gp.hb = g.hb; gp.wb = g.wb;
   gp.ts = g.ts; gp.tiles_y = g.tiles_y; gp.tiles_x = g.tiles_x;
-  gp.halo_floats = g.halo_floats; gp.stage_stride = g.stage_stride;
+  gp.halo_floats = g.halo_floats; gp.stage_stride = g.stage_stride; gp.lane_sum = g.lane_sum;
   gp.rows_per_batch = g.rows_per_batch; gp.copy_in_halo = g.copy_in_halo;
   gp.norm_p = d.norm_p; gp.support = d.support; gp.reference = ref ? 1 : 0; gp.no_prev = ref ? 1 : 0;
   gp.force_dense = (d.flags & SKIPCONV_FLAG_FORCE_DENSE) ? 1 : 0;
@@ -1006,6 +1022,14 @@ int skipconv_pipeline(skipconv_t h, int32_t* fused) {
   if (!h) return SKIPCONV_E_STATE;
   if (!fused) return SKIPCONV_E_INVALID_ARG;
   *fused = h->g.fused ? (h->g.f_rb ? 2 : 1) : 0;
+  return SKIPCONV_OK;
+}
+
+int skipconv_gate_tile(skipconv_t h, int32_t* ts, int32_t* lane_sum) {
+  if (!h) return SKIPCONV_E_STATE;
+  if (!ts || !lane_sum) return SKIPCONV_E_INVALID_ARG;
+  *ts = h->g.ts;
+  *lane_sum = h->g.lane_sum;
   return SKIPCONV_OK;
 }
 

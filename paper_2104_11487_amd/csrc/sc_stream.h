@@ -8,6 +8,8 @@
 
 namespace sc {
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
 constexpr int kUnroll = 4;  // staging chunks whose loads are issued together
 
 __device__ __forceinline__ float term(float r, int norm_p) {
@@ -58,6 +60,29 @@ __device__ __forceinline__ void copy_vec(T* dst, const T* src, size_t off) {
 // of the long integer-division sequence.
 __device__ __forceinline__ int qdiv(int n, float inv_d) {
   return (int)(((float)n + 0.5f) * inv_d);
+}
+
+// Value of lane (this lane + J) of the same 16-lane row (DPP row_shl:J).
+template <int J>
+__device__ __forceinline__ float row_shl(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x100 + J, 0xf, 0xf, false));
+}
+
+template <int NC, int J>
+__device__ __forceinline__ float group_sum_from(float acc, float v) {
+  if constexpr (J < NC) {
+    return group_sum_from<NC, J + 1>(add_rn(acc, row_shl<J>(v)), v);
+  } else {
+    return acc;
+  }
+}
+
+// Ordered sum (from +0, ascending lanes) of the NC values held by lanes
+// l .. l + NC - 1 of one 16-lane row, valid in lane l (NC <= 16; the group
+// must not cross a row boundary). Lane-to-lane moves only, no LDS traffic.
+template <int NC>
+__device__ __forceinline__ float group_sum(float v) {
+  return group_sum_from<NC, 1>(add_rn(0.0f, v), v);
 }
 
 // Workgroup b runs tile remap(b): XCD b % 8 (workgroups go to the XCDs

@@ -31,6 +31,7 @@ SKIPCONV_ACT_NONE, SKIPCONV_ACT_IDENTITY, SKIPCONV_ACT_RELU = 0, 1, 2
 SKIPCONV_FLAG_KEEP_STATS, SKIPCONV_FLAG_FORCE_DENSE, SKIPCONV_FLAG_SPLIT_PIPELINE = 1, 2, 4
 SKIPCONV_FLAG_EMIT_RESIDUAL = 8
 SKIPCONV_FLAG_TRANSLATE = 16
+SKIPCONV_FLAG_LARGE_GATE_TILES = 32
 
 
 class skipconv_desc(ctypes.Structure):
@@ -67,6 +68,7 @@ _SIGS = {
     "skipconv_activation": (ctypes.c_int, [_P, ctypes.POINTER(_P)]),
     "skipconv_get_desc": (ctypes.c_int, [_P, _D]),
     "skipconv_pipeline": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_int32)]),
+    "skipconv_gate_tile": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32)]),
     "skipconv_active_count": (ctypes.c_int, [_P, _P, ctypes.POINTER(ctypes.c_int64),
                                              ctypes.POINTER(ctypes.c_int64)]),
     "skipconv_copy_block_mask": (ctypes.c_int, [_P, _P, _P, ctypes.c_size_t]),
@@ -196,6 +198,12 @@ def skipconv_pipeline(h: int) -> int:
     return f.value
 
 
+def skipconv_gate_tile(h: int) -> Tuple[int, int]:
+    ts, ls = ctypes.c_int32(), ctypes.c_int32()
+    _check(lib().skipconv_gate_tile(h, ctypes.byref(ts), ctypes.byref(ls)), h)
+    return ts.value, ls.value
+
+
 def skipconv_active_count(h: int, stream: int) -> Tuple[int, int]:
     b, s = ctypes.c_int64(), ctypes.c_int64()
     _check(lib().skipconv_active_count(h, stream, ctypes.byref(b), ctypes.byref(s)), h)
@@ -269,7 +277,7 @@ _GATE = {"input": SKIPCONV_GATE_INPUT_NORM, "output": SKIPCONV_GATE_OUTPUT_NORM,
 def make_desc(*, n, h, w, c_in, c_out, kernel, stride=1, pad=-1, groups=1, block=1, norm_p=2,
               support="rf", dtype="f32", act_out="none", eps=0.0, keep_stats=False,
               force_dense=False, split=False, gate="input", emit_residual=False,
-              translate=False) -> skipconv_desc:
+              translate=False, large_gate_tiles=False) -> skipconv_desc:
     d = skipconv_desc_init()
     d.n, d.h, d.w, d.c_in, d.c_out = n, h, w, c_in, c_out
     d.kernel, d.stride, d.pad, d.groups, d.block = kernel, stride, pad, groups, block
@@ -279,7 +287,8 @@ def make_desc(*, n, h, w, c_in, c_out, kernel, stride=1, pad=-1, groups=1, block
     d.flags = ((SKIPCONV_FLAG_KEEP_STATS if keep_stats else 0) | (SKIPCONV_FLAG_FORCE_DENSE if force_dense else 0)
                | (SKIPCONV_FLAG_SPLIT_PIPELINE if split else 0)
                | (SKIPCONV_FLAG_EMIT_RESIDUAL if emit_residual else 0)
-               | (SKIPCONV_FLAG_TRANSLATE if translate else 0))
+               | (SKIPCONV_FLAG_TRANSLATE if translate else 0)
+               | (SKIPCONV_FLAG_LARGE_GATE_TILES if large_gate_tiles else 0))
     d.eps = eps
     d.gate = _GATE[gate]
     return d
@@ -298,7 +307,8 @@ class SkipConv:
                  groups: int = 1, eps: float = 0.0, block: int = 1, norm_p: int = 2,
                  support: str = "rf", act_out: str = "none", keep_stats: bool = False,
                  force_dense: bool = False, split: bool = False, gate: str = "input",
-                 emit_residual: bool = False, translate: bool = False, stream=None):
+                 emit_residual: bool = False, translate: bool = False, large_gate_tiles: bool = False,
+                 stream=None):
         import torch
 
         if not weight.is_cuda:
@@ -313,7 +323,7 @@ class SkipConv:
                               pad=pad, groups=groups, block=block, norm_p=norm_p, support=support,
                               dtype=self.dtype, act_out=act_out, eps=eps, keep_stats=keep_stats, gate=gate,
                               force_dense=force_dense, split=split, emit_residual=emit_residual,
-                              translate=translate)
+                              translate=translate, large_gate_tiles=large_gate_tiles)
         self.h_out, self.w_out, self.hb, self.wb = skipconv_out_shape(self.desc)
         nbytes = skipconv_workspace_size(self.desc)
         self.device = weight.device
@@ -387,6 +397,11 @@ class SkipConv:
     def fused_variant(self) -> int:
         """0 split pipeline, 1 single-pass kernel with LDS weights, 2 with register weights."""
         return skipconv_pipeline(self.handle)
+
+    @property
+    def gate_tile(self) -> Tuple[int, int]:
+        """(sites per side of a gate tile, 1 if chunk sums are combined in lane groups)."""
+        return skipconv_gate_tile(self.handle)
 
     def set_eps(self, eps: float):
         skipconv_set_eps(self.handle, eps)

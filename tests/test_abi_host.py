@@ -43,7 +43,7 @@ def good(**kw):
     ("block", 0, S.SKIPCONV_E_INVALID_ARG), ("block", 65, S.SKIPCONV_E_INVALID_ARG),
     ("norm_p", 3, S.SKIPCONV_E_INVALID_ARG), ("support", 2, S.SKIPCONV_E_INVALID_ARG),
     ("dtype", 2, S.SKIPCONV_E_INVALID_ARG), ("act_out", 3, S.SKIPCONV_E_INVALID_ARG),
-    ("flags", 32, S.SKIPCONV_E_INVALID_ARG), ("flags", 8, S.SKIPCONV_E_INVALID_ARG),
+    ("flags", 64, S.SKIPCONV_E_INVALID_ARG), ("flags", 8, S.SKIPCONV_E_INVALID_ARG),
     ("eps", -1.0, S.SKIPCONV_E_INVALID_ARG),
     ("eps", float("nan"), S.SKIPCONV_E_INVALID_ARG), ("c_out", 272, S.SKIPCONV_E_UNSUPPORTED),
     ("gate", 7, S.SKIPCONV_E_INVALID_ARG), ("gate", -1, S.SKIPCONV_E_INVALID_ARG),

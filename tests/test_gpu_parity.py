@@ -21,12 +21,12 @@ pytestmark = pytest.mark.gpu
 
 def _layer_pair(w_f32, *, n, h, w, dtype, eps, block, stride=1, pad=-1, groups=1, norm_p=2,
                 support="rf", keep_stats=True, act_out="none", force_dense=False, split=False,
-                gate="input", phi=None, gate_bias=0.0, translate=False):
+                gate="input", phi=None, gate_bias=0.0, translate=False, large_gate_tiles=False):
     ws = weight_storage(w_f32, dtype)
     layer = S.SkipConv(to_device(ws, dtype), n=n, h=h, w=w, stride=stride, pad=pad, groups=groups,
                        eps=eps, block=block, norm_p=norm_p, support=support, keep_stats=keep_stats,
                        act_out=act_out, force_dense=force_dense, split=split, gate=gate,
-                       translate=translate)
+                       translate=translate, large_gate_tiles=large_gate_tiles)
     if gate == "learned":
         layer.set_gate_weights(torch.from_numpy(np.ascontiguousarray(phi, np.float32)).cuda(), gate_bias)
     orc = O.SkipConvOracle(ws, n=n, h=h, w=w, stride=stride, pad=None if pad == -1 else pad,
@@ -56,7 +56,7 @@ def run_single(frames, w_f32, *, dtype, eps, block, tag, resets=(), exact_z=Fals
     return worst, dens
 
 
-def oracle_stats(frames, w_shape, *, dtype, stride=1, pad=None):
+def oracle_stats(frames, w_shape, *, dtype, stride=1, pad=None, norm_p=2):
     """Per-frame gate statistics of frames 2.. from the oracle (for eps calibration)."""
     k = w_shape[2]
     p = (k - 1) // 2 if pad is None else pad
@@ -65,7 +65,7 @@ def oracle_stats(frames, w_shape, *, dtype, stride=1, pad=None):
         x = O.storage_to_f32(syn.to_storage(f, dtype), dtype)
         if prev is not None:
             r = O.residual(x, prev)
-            a = O.pixel_stat(r, 2)
+            a = O.pixel_stat(r, norm_p)
             ho, wo = O.out_size(x.shape[1], k, stride, p), O.out_size(x.shape[2], k, stride, p)
             out.append(O.support_stat(a, k, stride, p, ho, wo))
         prev = x
@@ -415,6 +415,72 @@ def test_pipeline_selection():
     w128 = to_device(weight_storage(syn.he_weights(128, 128, 3, seed=1), "bf16"), "bf16")
     assert S.SkipConv(w128, n=1, h=32, w=32, block=8).fused_variant == 1
     assert S.SkipConv(w, n=1, h=64, w=64, block=16).fused_variant == 1
+    # split gate tiles: 16 x 16 sites on large frames, 8 x 8 on small ones, 32 x 32
+    # on request; 32, 64 and 128 channels add their chunk sums in lane groups,
+    # other channel counts stage them in LDS
+    assert S.SkipConv(w128, n=4, h=512, w=512, block=16).gate_tile == (16, 1)
+    assert S.SkipConv(w128, n=4, h=512, w=512, block=16, large_gate_tiles=True).gate_tile == (32, 1)
+    assert S.SkipConv(w, n=1, h=128, w=96, block=8, split=True).gate_tile == (8, 1)
+    assert S.SkipConv(w, n=1, h=128, w=96, block=8, split=True, large_gate_tiles=True).gate_tile == (32, 1)
+    w48 = to_device(weight_storage(syn.he_weights(64, 48, 3, seed=1), "bf16"), "bf16")
+    assert S.SkipConv(w48, n=4, h=512, w=512, block=16).gate_tile == (16, 0)
+
+
+# Gate tiles of 32 x 32 output sites with the chunk sums of a pixel combined
+# in lane groups (4, 8 or 16 lanes), forced on frames small enough for the
+# oracle; sizes leave edge tiles and a reset comes mid-stream:
+# (n, h, w, c_in, c_out, k, stride, block, dtype, norm_p, translated)
+LARGE_GATE = [
+    (2, 70, 45, 32, 16, 3, 1, 8, "bf16", 2, False),
+    (1, 67, 100, 64, 32, 3, 1, 16, "bf16", 2, False),
+    (1, 40, 70, 128, 16, 3, 1, 4, "bf16", 1, False),
+    (1, 50, 66, 32, 16, 3, 1, 2, "f32", 2, False),
+    (1, 90, 70, 32, 16, 3, 2, 8, "bf16", 2, False),
+    (1, 50, 50, 64, 16, 5, 1, 32, "bf16", 2, False),
+    (1, 45, 38, 128, 32, 1, 1, 8, "bf16", 2, False),
+    (2, 60, 52, 64, 16, 3, 1, 8, "bf16", 2, True),
+]
+
+
+@pytest.mark.parametrize("case", LARGE_GATE, ids=[f"gate32_{i}" for i in range(len(LARGE_GATE))])
+def test_large_gate_tiles(case):
+    """Split pipeline with 32 x 32-site gate tiles: statistic, masks and list bit-exact, z within
+    tolerance, including the x_{t-1} copy the tiles make (checked by the frames after it)."""
+    n, h, w, ci, co, k, s, b, dtype, p, translated = case
+    rng = np.random.Generator(np.random.PCG64(700 + ci + k + b))
+    vid = syn.RectVideo(h, w, ci, 6, seed=701 + ci, batch=n, n_rect=3, side_lo=6, side_hi=20)
+    base = list(vid)
+    shifts = [(0, 0), (s, -s), (0, 0), (-2 * s, s), (s, 0), (0, 2 * s)] if translated else [(0, 0)] * 6
+    frames, acc = [], (0, 0)
+    for f, d in zip(base, shifts):
+        acc = (acc[0] + d[0], acc[1] + d[1])
+        frames.append(O.translate(f, *acc) if translated else f)
+    wt = rng.normal(0, 0.2, (co, ci, k, k)).astype(np.float32)
+    pad = (k - 1) // 2
+    ho, wo = O.out_size(h, k, s, pad), O.out_size(w, k, s, pad)
+    stats = oracle_stats(base[:3], wt.shape, dtype=dtype, stride=s, norm_p=p)
+    eps = eps_for_density(stats, b, ho, wo, 0.4, norm_p=p)
+    tag = f"gate32 {case}"
+    layer, orc = _layer_pair(wt, n=n, h=h, w=w, dtype=dtype, eps=eps, block=b, stride=s, norm_p=p,
+                             split=True, translate=translated, large_gate_tiles=True)
+    assert layer.gate_tile == (32, 1), layer.gate_tile
+    dens = []
+    for t, (f, d) in enumerate(zip(frames, shifts)):
+        if t == 4:
+            layer.reset()
+            orc.reset()
+        xs = syn.to_storage(f, dtype)
+        say(f"[{tag}] frame {t} shift={d} eps={eps:.4g}")
+        if translated:
+            layer.step_translated(to_device(xs, dtype), *d)
+            ref = orc.step(xs, shift=d)
+        else:
+            layer.step(to_device(xs, dtype))
+            ref = orc.step(xs)
+        compare_frame(layer, ref, dtype, t=t, tag=tag, keep_stats=True)
+        dens.append(ref["count"] / ref["block_mask"].size)
+    layer.close()
+    assert 0.0 < np.mean(dens[1:4]) < 1.0
 
 
 # One shape per build of the single-pass kernel whose waves hold their weight
