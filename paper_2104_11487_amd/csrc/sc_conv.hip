@@ -25,6 +25,7 @@
 // thread per (site, 8 channels) sums the k x k taps with fp32 FMAs.
 #include "sc_device.h"
 #include "sc_kernels.h"
+#include "sc_stream.h"
 
 namespace sc {
 
@@ -33,7 +34,6 @@ namespace {
 constexpr int kConvThreads = 256;
 constexpr int kRowsPerTile = 64;
 
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float floatx2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
@@ -220,7 +220,7 @@ __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N) __attribute__((amdgpu_
 conv_halo_kernel(ConvParams p, HaloParams hp) {
   extern __shared__ __attribute__((aligned(16))) uint8_t halo[];
   constexpr int kThreads = 64 * WAVES_M * WAVES_N;
-  constexpr int kUnroll = WM >= 8 ? 4 : 8;         // halo loads in flight per thread
+  constexpr int kUnroll = 12;  // halo items (two 16-byte loads each) in flight per thread
   constexpr int kR = WN <= 2 ? 8 : (WN == 3 ? 6 : 4);  // B register ring (kR - 1 k-steps of lookahead), even
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave % WAVES_M, wn = wave / WAVES_M;
@@ -240,6 +240,8 @@ conv_halo_kernel(ConvParams p, HaloParams hp) {
   const int wn0 = __builtin_amdgcn_readfirstlane(wn) * WN;  // first 16-channel output tile
   const int chunks_per_px = c >> 3;
   const int csteps = c >> 5;  // k-steps per tap
+  const size_t ximg = (size_t)p.h * p.w * c;              // elements of one input image
+  const size_t zimg = (size_t)p.h_out * p.w_out * p.c_out;  // elements of one z image
   const int ksteps = p.ksteps;
   const int ntn = p.ntiles_n;
 
@@ -252,77 +254,121 @@ conv_halo_kernel(ConvParams p, HaloParams hp) {
     abase[i] = (ly * s * hp.hw + lx * s) * hp.pstride + kq * 16;
   }
 
-  for (TileWalk tw(ntiles); tw.t < tw.end; tw.t += tw.step) {
-    const int j0 = tw.t / tpb, band = tw.t - j0 * tpb;
-    const uint32_t blk = p.list[j0];
+  // Tiles walked in order; the active list is read through the scalar cache
+  // (written by an earlier kernel, read-only here), so decoding a tile waits
+  // on no vector memory operation.
+  typedef const __attribute__((address_space(4))) uint32_t const_u32;
+  const const_u32* list = (const const_u32*)p.list;
+  struct HTile {
+    int n, oy0, ox0, rows_ok, cols_ok, iy0, ix0;
+  };
+  auto decode = [&](int t) {
+    HTile T;
+    const int j0 = t / tpb, band = t - j0 * tpb;
+    const uint32_t blk = list[j0];
     const int per_img = p.hb * p.wb;
-    const int n = (int)(blk / per_img);
-    const int rem = (int)(blk - (uint32_t)n * per_img);
+    T.n = (int)(blk / per_img);
+    const int rem = (int)(blk - (uint32_t)T.n * per_img);
     const int bi = rem / p.wb, bj = rem - bi * p.wb;
-    const int oy0 = bi * b + band * hp.tr, ox0 = bj * b;
-    const int rows_ok = min(hp.tr, p.h_out - oy0), cols_ok = min(b, p.w_out - ox0);
-    const int iy0 = oy0 * s - p.pad, ix0 = ox0 * s - p.pad;
+    T.oy0 = bi * b + band * hp.tr;
+    T.ox0 = bj * b;
+    T.rows_ok = min(hp.tr, p.h_out - T.oy0);
+    T.cols_ok = min(b, p.w_out - T.ox0);
+    T.iy0 = T.oy0 * s - p.pad;
+    T.ix0 = T.ox0 * s - p.pad;
+    return T;
+  };
+  // z offset (bytes, within image T.n) of this lane's piece (M-tile i,
+  // column tile jn), or out of range outside the frame / past C_out
+  auto zoff = [&](const HTile& T, int i, int jn) {
+    int l16 = r16;  // opaque: recomputed per use rather than held per (i, jn)
+    asm volatile("" : "+v"(l16));
+    const int m = (wm * WM + i) * 16 + l16;
+    const int ly = m >> lb, lx = m & (b - 1);
+    const int col = (wn0 + jn) * 16 + kq * 4;
+    return (ly < T.rows_ok && lx < T.cols_ok && col < p.c_out)
+               ? (uint32_t)((((T.oy0 + ly) * p.w_out + T.ox0 + lx) * p.c_out + col) * 4)
+               : kOutOfRange;
+  };
+  auto zres = [&](const HTile& T) { return frame_rsrc(p.z + (size_t)T.n * zimg, (uint32_t)(zimg * 4)); };
+  // z_{t-1} of a tile in the transposed MFMA output layout (a lane holds 4
+  // consecutive output channels of one site: z moves in 16-byte pieces);
+  // zeros outside the frame and on a reference frame
+  // (none: every piece out of range, so the registers are always written)
+  auto load_z = [&](floatx4 (&dst)[WM][WN], const HTile& T, bool none) {
+    const auto zrs = zres(T);
+#pragma unroll
+    for (int i = 0; i < WM; ++i)
+#pragma unroll
+      for (int jn = 0; jn < WN; ++jn)
+        dst[i][jn] = __builtin_bit_cast(
+            floatx4,
+            __builtin_amdgcn_raw_buffer_load_b128(zrs, p.reference || none ? kOutOfRange : zoff(T, i, jn), 0, 0));
+  };
+  // one round of halo items: rho = bf16(x_t - x_{t-1}) into LDS. Buffer loads
+  // over image T.n with 32-bit offsets; items outside the frame (x_{t-1}:
+  // outside the translated frame, or none on a reference frame) read zeros at
+  // an out-of-range offset, so every lane issues the same loads.
+  const int total = hp.hh * hp.hw * chunks_per_px;
+  auto halo_round = [&](const HTile& T, int base) {
+    const auto xrs = frame_rsrc(xt + (size_t)T.n * ximg, (uint32_t)(ximg * 2));
+    const auto prs = frame_rsrc((p.no_prev ? xt : xp) + (size_t)T.n * ximg, (uint32_t)(ximg * 2));
+    u32x4 ra[kUnroll], rb[kUnroll];
+    // the thread index, opaque to loop-invariant code motion: the per-item
+    // terms are recomputed each round instead of occupying registers through
+    // the product loop
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int idx = base + u * kThreads + tid;
+      const int px = idx / chunks_per_px, ch = idx - px * chunks_per_px;
+      const int hy = px / hp.hw, hx = px - hy * hp.hw;
+      const int y = T.iy0 + hy, x = T.ix0 + hx;
+      const bool in = idx < total && y >= 0 && y < p.h && x >= 0 && x < p.w;
+      const int yp = y - p.sy, xq = x - p.sx;
+      const bool pin = in && !p.no_prev && yp >= 0 && yp < p.h && xq >= 0 && xq < p.w;
+      ra[u] = __builtin_amdgcn_raw_buffer_load_b128(
+          xrs, in ? (uint32_t)(((y * p.w + x) * c + ch * 8) * 2) : kOutOfRange, 0, 0);
+      rb[u] = __builtin_amdgcn_raw_buffer_load_b128(
+          prs, pin ? (uint32_t)(((yp * p.w + xq) * c + ch * 8) * 2) : kOutOfRange, 0, 0);
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int idx = base + u * kThreads + tid;
+      if (idx >= total) continue;
+      const int px = idx / chunks_per_px, ch = idx - px * chunks_per_px;
+      uint32_t q[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t wa = ra[u][e], wb = rb[u][e];
+        const float r0 = __fsub_rn(__uint_as_float(wa << 16), __uint_as_float(wb << 16));
+        const float r1 = __fsub_rn(__uint_as_float(wa & 0xffff0000u), __uint_as_float(wb & 0xffff0000u));
+        q[e] = pack_bf16(r0, r1);
+      }
+      *reinterpret_cast<u32x4*>(halo + px * hp.pstride + ch * 16) = u32x4{q[0], q[1], q[2], q[3]};
+    }
+  };
 
-    // ---- 1. accumulators = z_{t-1} at the tile's sites ----
-    // The product is computed transposed (weights as the MFMA A operand), so
-    // a lane's accumulator holds 4 consecutive output channels of one site:
-    // z moves in 16-byte pieces.
-    auto site = [&](int i) {  // output site of this lane in M-tile i, -1 outside the frame
-      const int m = (wm * WM + i) * 16 + r16;
-      const int ly = m >> lb, lx = m & (b - 1);
-      return (ly < rows_ok && lx < cols_ok) ? (n * p.h_out + oy0 + ly) * p.w_out + ox0 + lx : -1;
-    };
+  // Software pipeline over the workgroup's tiles: the z_{t-1} loads of the
+  // next tile are issued before the stores of the current one (sites of
+  // different tiles are disjoint), into registers that are not the stores'
+  // sources, so no wait on the stores precedes them; the halo loads of a
+  // tile then wait once for everything in flight.
+  TileWalk tw(ntiles);
+  if (tw.t >= tw.end) return;
+  HTile T = decode(tw.t);
+  floatx4 zn[WM][WN];
+  load_z(zn, T, false);
+  for (; tw.t < tw.end; tw.t += tw.step) {
+    // ---- 1. halo (the first round outside the loop: no loop-carried waits) ----
+    halo_round(T, 0);
+    for (int base = kThreads * kUnroll; base < total; base += kThreads * kUnroll) halo_round(T, base);
     floatx4 acc[WM][WN];
 #pragma unroll
-    for (int i = 0; i < WM; ++i) {
-      const int st = site(i);
+    for (int i = 0; i < WM; ++i)
 #pragma unroll
-      for (int jn = 0; jn < WN; ++jn) {
-        const int col = (wn0 + jn) * 16 + kq * 4;
-        acc[i][jn] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
-        if (st >= 0 && !p.reference && col < p.c_out)
-          acc[i][jn] = *reinterpret_cast<const floatx4*>(p.z + (size_t)st * p.c_out + col);
-      }
-    }
-
-    // ---- 2. halo: rho = bf16(x_t - x_{t-1}), zero outside the frame ----
-    const int total = hp.hh * hp.hw * chunks_per_px;
-    for (int base = 0; base < total; base += kThreads * kUnroll) {
-      uint4 ra[kUnroll], rb[kUnroll];
-      int dst[kUnroll];
-      bool in[kUnroll];
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const int idx = base + u * kThreads + threadIdx.x;
-        const int px = idx / chunks_per_px, ch = idx - px * chunks_per_px;
-        const int hy = px / hp.hw, hx = px - hy * hp.hw;
-        const int y = iy0 + hy, x = ix0 + hx;
-        in[u] = idx < total && y >= 0 && y < p.h && x >= 0 && x < p.w;
-        dst[u] = idx < total ? px * hp.pstride + ch * 16 : -1;
-        ra[u] = uint4{0u, 0u, 0u, 0u};
-        rb[u] = uint4{0u, 0u, 0u, 0u};
-        if (in[u]) {
-          const size_t off = ((size_t)(n * p.h + y) * p.w + x) * c + ch * 8;
-          ra[u] = *reinterpret_cast<const uint4*>(xt + off);
-          const long po = p.no_prev ? -1 : prev_off(p, n, y, x, ch * 8);
-          if (po >= 0) rb[u] = *reinterpret_cast<const uint4*>(xp + po);
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        if (dst[u] < 0) continue;
-        const uint32_t wa[4] = {ra[u].x, ra[u].y, ra[u].z, ra[u].w};
-        const uint32_t wb[4] = {rb[u].x, rb[u].y, rb[u].z, rb[u].w};
-        uint32_t q[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float r0 = __fsub_rn(__uint_as_float(wa[e] << 16), __uint_as_float(wb[e] << 16));
-          const float r1 = __fsub_rn(__uint_as_float(wa[e] & 0xffff0000u), __uint_as_float(wb[e] & 0xffff0000u));
-          q[e] = pack_bf16(r0, r1);
-        }
-        *reinterpret_cast<u32x4*>(halo + dst[u]) = u32x4{q[0], q[1], q[2], q[3]};
-      }
-    }
+      for (int jn = 0; jn < WN; ++jn) acc[i][jn] = zn[i][jn];
     __syncthreads();
 
     // ---- 3. MFMA over K = (kh, kw, ci) ----
@@ -383,30 +429,32 @@ conv_halo_kernel(ConvParams p, HaloParams hp) {
         read_a(aq[(r + 1) & 1]);
         mfmas(aq[r & 1], bq[r]);
       }
-    // all waves are done with the halo: the next tile may overwrite it (no
-    // stores are outstanding here, so this barrier waits on nothing in memory)
+    // all waves are done with the halo: the next tile may overwrite it
     __syncthreads();
 
-    // ---- 4. store z (+ activation output) ----
+    // ---- 3. next tile's z_{t-1}, then store this tile's z (+ activation) ----
+    const auto zrs = zres(T);
+    const bool more = tw.t + tw.step < tw.end;
+    const HTile Tn = more ? decode(tw.t + tw.step) : T;
+    load_z(zn, Tn, !more);
+    const auto yrs = frame_rsrc(p.act ? static_cast<uint16_t*>(p.y) + (size_t)T.n * zimg : nullptr,
+                                p.act ? (uint32_t)(zimg * 2) : 0u);
 #pragma unroll
-    for (int i = 0; i < WM; ++i) {
-      const int st = site(i);
-      if (st < 0) continue;
+    for (int i = 0; i < WM; ++i)
 #pragma unroll
       for (int jn = 0; jn < WN; ++jn) {
-        const int col = (wn0 + jn) * 16 + kq * 4;
-        if (col >= p.c_out) continue;
-        const size_t o = (size_t)st * p.c_out + col;
-        *reinterpret_cast<floatx4*>(p.z + o) = acc[i][jn];
+        const uint32_t o = zoff(T, i, jn);
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc[i][jn]), zrs, o, 0, 0);
         if (p.act) {
           const uint32_t lo = f32_to_bf16(activate(acc[i][jn][0], p.act)) |
                               (f32_to_bf16(activate(acc[i][jn][1], p.act)) << 16);
           const uint32_t hi = f32_to_bf16(activate(acc[i][jn][2], p.act)) |
                               (f32_to_bf16(activate(acc[i][jn][3], p.act)) << 16);
-          *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.y) + o) = uint2{lo, hi};
+          typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+          __builtin_amdgcn_raw_buffer_store_b64(u32x2{lo, hi}, yrs, o == kOutOfRange ? kOutOfRange : o / 2, 0, 0);
         }
       }
-    }
+    T = Tn;
   }
 }
 

@@ -130,13 +130,6 @@ __device__ void halo_partials(const GateParams& p, int n, int iy0, int ix0, int 
   }
 }
 
-// Raw buffer resource over `bytes` bytes at `base`: a load at an offset at or
-// beyond `bytes` returns zeros and a store there is dropped, without a memory
-// access (range-checked buffer addressing of the CDNA ISA).
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t frame_rsrc(const void* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
-}
-constexpr uint32_t kOutOfRange = 0x80000000u;  // byte offset past every frame resource
 // Cache policy of the x_{t-1} copy: non-temporal (streamed past the caches),
 // so that the frame being written does not evict the two frames the
 // convolution reads next.

@@ -234,8 +234,11 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
 
   // block-halo kernel: tile = tr rows x b columns of a block, chosen per wave layout
   G.halo = false;
+  // (one image of x and of z within 2^31 bytes: the kernel addresses them
+  // through buffer resources with 32-bit offsets)
   if (!depthwise && d->dtype == SKIPCONV_BF16 && d->c_in % 32 == 0 &&
-      d->c_out % 4 == 0 && (b == 4 || b == 8 || b == 16 || b == 32 || b == 64)) {
+      d->c_out % 4 == 0 && (b == 4 || b == 8 || b == 16 || b == 32 || b == 64) &&
+      (long)d->h * d->w * d->c_in * 2 < (1L << 31) && (long)G.h_out * G.w_out * d->c_out * 4 < (1L << 31)) {
     static const int ntns[] = {1, 2, 4, 8, 12, 16};
     int ni = 0;
     while (ntns[ni] != G.ntn) ++ni;

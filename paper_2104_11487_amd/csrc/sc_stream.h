@@ -85,6 +85,14 @@ __device__ __forceinline__ float group_sum(float v) {
   return group_sum_from<NC, 1>(add_rn(0.0f, v), v);
 }
 
+// Raw buffer resource over `bytes` bytes at `base`: a load at an offset at or
+// beyond `bytes` returns zeros and a store there is dropped, without a memory
+// access (range-checked buffer addressing of the CDNA ISA).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t frame_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+constexpr uint32_t kOutOfRange = 0x80000000u;  // byte offset past every frame resource
+
 // Workgroup b runs tile remap(b): XCD b % 8 (workgroups go to the XCDs
 // round-robin) receives a contiguous range of tiles, so neighbouring tiles
 // share their halo rows through one L2.
