@@ -107,14 +107,6 @@ __device__ void emit_clear(const FusedParams& p, int n, int oy0, int ox0, int oh
   }
 }
 
-// Workgroup barrier that orders LDS accesses only: outstanding global loads
-// and stores (register loads, the z prefetch, the x_t copy) stay in flight.
-// (A global_load_lds still in flight makes the compiler wait for it here.)
-__device__ __forceinline__ void lds_barrier() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
 
 // Geometry of one tile of output sites and of its input halo. The halo has
 // the extent of a whole tile even for edge tiles (the extra pixels are out of

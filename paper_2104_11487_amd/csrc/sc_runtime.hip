@@ -1036,6 +1036,13 @@ int skipconv_gate_tile(skipconv_t h, int32_t* ts, int32_t* lane_sum) {
   return SKIPCONV_OK;
 }
 
+int skipconv_conv_kernel(skipconv_t h, int32_t* kind) {
+  if (!h) return SKIPCONV_E_STATE;
+  if (!kind) return SKIPCONV_E_INVALID_ARG;
+  *kind = h->g.depthwise ? 2 : (h->g.halo ? 1 : 0);
+  return SKIPCONV_OK;
+}
+
 int skipconv_get_desc(skipconv_t h, skipconv_desc* d) {
   if (!h) return SKIPCONV_E_STATE;
   if (!d) return SKIPCONV_E_INVALID_ARG;

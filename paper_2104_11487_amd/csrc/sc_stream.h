@@ -85,6 +85,15 @@ __device__ __forceinline__ float group_sum(float v) {
   return group_sum_from<NC, 1>(add_rn(0.0f, v), v);
 }
 
+// Workgroup barrier that orders LDS accesses only: outstanding global loads
+// and stores stay in flight. (A global_load_lds still in flight makes the
+// compiler wait for it here.)
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // Raw buffer resource over `bytes` bytes at `base`: a load at an offset at or
 // beyond `bytes` returns zeros and a store there is dropped, without a memory
 // access (range-checked buffer addressing of the CDNA ISA).

@@ -69,6 +69,7 @@ _SIGS = {
     "skipconv_get_desc": (ctypes.c_int, [_P, _D]),
     "skipconv_pipeline": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_int32)]),
     "skipconv_gate_tile": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32)]),
+    "skipconv_conv_kernel": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_int32)]),
     "skipconv_active_count": (ctypes.c_int, [_P, _P, ctypes.POINTER(ctypes.c_int64),
                                              ctypes.POINTER(ctypes.c_int64)]),
     "skipconv_copy_block_mask": (ctypes.c_int, [_P, _P, _P, ctypes.c_size_t]),
@@ -202,6 +203,12 @@ def skipconv_gate_tile(h: int) -> Tuple[int, int]:
     ts, ls = ctypes.c_int32(), ctypes.c_int32()
     _check(lib().skipconv_gate_tile(h, ctypes.byref(ts), ctypes.byref(ls)), h)
     return ts.value, ls.value
+
+
+def skipconv_conv_kernel(h: int) -> int:
+    k = ctypes.c_int32()
+    _check(lib().skipconv_conv_kernel(h, ctypes.byref(k)), h)
+    return k.value
 
 
 def skipconv_active_count(h: int, stream: int) -> Tuple[int, int]:
@@ -402,6 +409,11 @@ class SkipConv:
     def gate_tile(self) -> Tuple[int, int]:
         """(sites per side of a gate tile, 1 if chunk sums are combined in lane groups)."""
         return skipconv_gate_tile(self.handle)
+
+    @property
+    def conv_kernel(self) -> int:
+        """Split-pipeline convolution kernel: 0 gather, 1 block halo, 2 depthwise."""
+        return skipconv_conv_kernel(self.handle)
 
     def set_eps(self, eps: float):
         skipconv_set_eps(self.handle, eps)

@@ -424,6 +424,13 @@ def test_pipeline_selection():
     assert S.SkipConv(w, n=1, h=128, w=96, block=8, split=True, large_gate_tiles=True).gate_tile == (32, 1)
     w48 = to_device(weight_storage(syn.he_weights(64, 48, 3, seed=1), "bf16"), "bf16")
     assert S.SkipConv(w48, n=4, h=512, w=512, block=16).gate_tile == (16, 0)
+    # split convolution kernels: block halo (bf16, C_in % 32 == 0, b in {4..64}),
+    # gather otherwise, depthwise for groups == C
+    assert S.SkipConv(w128, n=4, h=512, w=512, block=16).conv_kernel == 1
+    assert S.SkipConv(w, n=1, h=128, w=96, block=1, split=True).conv_kernel == 0
+    assert S.SkipConv(w48, n=1, h=32, w=32, block=8).conv_kernel == 0
+    wdw = to_device(weight_storage(syn.he_weights(64, 1, 3, seed=1), "bf16"), "bf16")
+    assert S.SkipConv(wdw, n=1, h=32, w=32, block=8, groups=64).conv_kernel == 2
 
 
 # Gate tiles of 32 x 32 output sites with the chunk sums of a pixel combined
@@ -481,6 +488,64 @@ def test_large_gate_tiles(case):
         dens.append(ref["count"] / ref["block_mask"].size)
     layer.close()
     assert 0.0 < np.mean(dens[1:4]) < 1.0
+
+
+# The block-halo convolution (tiles of rows of one active block, residual
+# halo in LDS) on frames with edge tiles: 64 and 128 output channels, 16 x 16
+# and 32 x 32 blocks, stride 2, 1 x 1, translated steps and a ReLU output:
+# (n, h, w, c_in, c_out, k, stride, block, translated)
+BLOCK_HALO = [
+    (2, 40, 44, 64, 64, 3, 1, 16, False),
+    (1, 36, 50, 128, 128, 3, 1, 16, False),
+    (1, 70, 66, 64, 128, 3, 1, 32, False),
+    (1, 40, 40, 32, 64, 3, 2, 16, False),
+    (1, 50, 48, 64, 64, 1, 1, 16, False),
+    (1, 48, 40, 64, 64, 3, 1, 16, True),
+]
+
+
+@pytest.mark.parametrize("case", BLOCK_HALO, ids=[f"halo{i}" for i in range(len(BLOCK_HALO))])
+def test_block_halo_conv(case):
+    """Split pipeline with the block-halo convolution: masks bit-exact, z within tolerance after
+    every frame (reset mid-stream), activation output = bf16(relu(z)) bit for bit."""
+    n, h, w, ci, co, k, s, b, translated = case
+    rng = np.random.Generator(np.random.PCG64(800 + ci + co + k + b))
+    vid = syn.RectVideo(h, w, ci, 7, seed=801 + ci, batch=n, n_rect=3, side_lo=5, side_hi=18)
+    base = list(vid)
+    shifts = [(0, 0), (s, 0), (0, -s), (0, 0), (-s, 2 * s), (s, s), (0, 0)] if translated else [(0, 0)] * 7
+    frames, acc = [], (0, 0)
+    for f, d in zip(base, shifts):
+        acc = (acc[0] + d[0], acc[1] + d[1])
+        frames.append(O.translate(f, *acc) if translated else f)
+    wt = rng.normal(0, 0.15, (co, ci, k, k)).astype(np.float32)
+    pad = (k - 1) // 2
+    ho, wo = O.out_size(h, k, s, pad), O.out_size(w, k, s, pad)
+    stats = oracle_stats(base[:3], wt.shape, dtype="bf16", stride=s)
+    eps = eps_for_density(stats, b, ho, wo, 0.4)
+    tag = f"block halo {case}"
+    layer, orc = _layer_pair(wt, n=n, h=h, w=w, dtype="bf16", eps=eps, block=b, stride=s, split=True,
+                             translate=translated, act_out="relu")
+    assert layer.conv_kernel == 1, layer.conv_kernel
+    for t, (f, d) in enumerate(zip(frames, shifts)):
+        if t == 5:
+            layer.reset()
+            orc.reset()
+        xs = syn.to_storage(f, "bf16")
+        say(f"[{tag}] frame {t} shift={d} eps={eps:.4g}")
+        if translated:
+            layer.step_translated(to_device(xs, "bf16"), *d)
+            ref = orc.step(xs, shift=d)
+        else:
+            layer.step(to_device(xs, "bf16"))
+            ref = orc.step(xs)
+        compare_frame(layer, ref, "bf16", t=t, tag=tag, keep_stats=True)
+        z = layer._z.cpu().numpy()
+        y = layer.activation()
+        torch.cuda.synchronize()
+        y_bits = y.view(torch.int16).cpu().numpy().view(np.uint16).reshape(z.shape)
+        assert np.array_equal(y_bits, O.f32_to_bf16_rne(np.maximum(z, 0.0).astype(np.float32))), \
+            f"{tag} t={t}: activation output"
+    layer.close()
 
 
 # One shape per build of the single-pass kernel whose waves hold their weight
