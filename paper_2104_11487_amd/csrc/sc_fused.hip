@@ -394,10 +394,10 @@ __device__ __forceinline__ void copy_owned(const GateParams& g, const Tile& T) {
 // Pixel statistics complete (combining parked chunk sums if needed), then the
 // gate of every site of the tile (Eq. 5): support sum over in-frame taps in
 // row-major order, exact fp64 threshold (times the Output-Norm weight norm),
-// NaN on, block OR into blk_flag; block flags go to global memory. Ends after
-// a barrier with blk_flag and tile_on final. All threads call it.
-__device__ void gate_tile(const FusedParams& p, const Tile& T, const ChunkMap& cm, float* a_halo,
-                          const float* part, uint32_t* blk_flag, uint32_t* tile_on) {
+// NaN on, block OR into blk_flag and tile_on (LDS). blk_flag and tile_on are
+// final only after the next barrier. All threads call it.
+__device__ void gate_sites(const FusedParams& p, const Tile& T, const ChunkMap& cm, float* a_halo,
+                           const float* part, uint32_t* blk_flag, uint32_t* tile_on) {
   const GateParams& g = p.g;
   const int s = g.stride, k = g.k, hw = T.hw;
   lds_barrier();
@@ -440,13 +440,27 @@ __device__ void gate_tile(const FusedParams& p, const Tile& T, const ChunkMap& c
       *tile_on = 1u;
     }
   }
-  lds_barrier();
+}
+
+// The tile's block flags to global memory (after the barrier that made
+// blk_flag final).
+__device__ void gate_flags(const FusedParams& p, const Tile& T, const uint32_t* blk_flag) {
+  const GateParams& g = p.g;
   const int nby = (T.oh + g.block - 1) / g.block, nbx = (T.ow + g.block - 1) / g.block;
   const int bi0 = T.oy0 / g.block, bj0 = T.ox0 / g.block;
   for (int i = threadIdx.x; i < nby * nbx; i += kThreads) {
     const int by = i / nbx, bx = i - by * nbx;
     g.block_mask[((size_t)T.n * g.hb + bi0 + by) * g.wb + bj0 + bx] = (uint8_t)blk_flag[by * T.tb_w + bx];
   }
+}
+
+// Gate of the tile; ends after a barrier with blk_flag and tile_on final and
+// the block flags stored. All threads call it.
+__device__ void gate_tile(const FusedParams& p, const Tile& T, const ChunkMap& cm, float* a_halo,
+                          const float* part, uint32_t* blk_flag, uint32_t* tile_on) {
+  gate_sites(p, T, cm, a_halo, part, blk_flag, tile_on);
+  lds_barrier();
+  gate_flags(p, T, blk_flag);
 }
 
 // Epilogue of one output piece (4 consecutive channels of one site): z =
@@ -600,14 +614,13 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
   halo_keep(g, hb);  // the halo is one round (kItems rows per thread) for this kernel
   copy_owned(g, T);
 
-  // 3. gate
-  gate_tile(p, T, cm, a_halo, part, blk_flag, &tile_on);
-  if (!tile_on) {
-    if (EMIT) emit_clear(p, T.n, T.oy0, T.ox0, T.oh, T.ow, T.tb_w, blk_flag, emit_clr);
-    return;
-  }
+  // 3. gate of every site, and 4. the product, with no barrier between them:
+  // the product is computed whether or not the gate turns any block of the
+  // tile on (it does not depend on the gate), so the gate's latency overlaps
+  // it instead of preceding it; a tile found off then stores nothing.
+  gate_sites(p, T, cm, a_halo, part, blk_flag, &tile_on);
 
-  // 4. product over this wave's k-steps: the first KPS - 1 always run, the
+  // product over this wave's k-steps: the first KPS - 1 always run, the
   // last one when the wave has KPS (a wave-uniform branch); the tap and
   // channel offset of a step is wave-uniform
   floatx4 acc[MT][WN];
@@ -649,6 +662,11 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
                                     ((ng * WN + j) * 16 + kq * 4) * 4) = acc[i][j];
   }
   lds_barrier();
+  gate_flags(p, T, blk_flag);
+  if (!tile_on) {
+    if (EMIT) emit_clear(p, T.n, T.oy0, T.ox0, T.oh, T.ow, T.tb_w, blk_flag, emit_clr);
+    return;
+  }
 
   // 5. epilogue: the k-parts added in ascending order, at the active sites
 #pragma unroll
