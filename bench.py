@@ -584,6 +584,166 @@ def bench_stack(args):
     print(json.dumps(out), flush=True)
 
 
+# ------------------------------------------------------- pointwise + dw --
+
+def bench_mbconv(args):
+    """Pointwise 1x1 192->192, then depthwise 3x3 (groups 192), 64 x 64 bf16 frames,
+    8 x 8 blocks, identity between (an MBConv-style pair); 10 % of the frames carry a
+    one-frame camera shake. One step = both layers on one frame. Per-layer thresholds
+    are calibrated for each target density on the GPU (layer 2 on layer 1's outputs).
+    Variants: 'full' (layer 2 steps on layer 1's activation output) and 'chained'
+    (layer 2 steps on layer 1's emitted residual); per-kernel times from the library's
+    events; shake frames: layer-1 density with and without the known-shift step."""
+    import torch
+    from paper_2104_11487_amd import skipconv as S
+    from paper_2104_11487_amd import synthetic as syn
+    from paper_2104_11487_amd.skipconv import SkipConv
+
+    wl, clip = load_workload("mbconv192", args.frames)
+    nfr = len(clip)
+    vid = syn.RectVideo(wl.h, wl.w, wl.c, nfr, seed=301, batch=wl.n, shake_prob=0.1)
+    for _ in vid:
+        pass
+    shake = set(vid.shake_frames)
+    frames_dev = upload(clip, wl.dtype)
+    w1, w2 = [weight_tensor(w, wl.dtype) for w in wl.weights()]
+    b = args.block or wl.block
+    kw1 = dict(n=wl.n, h=wl.h, w=wl.w, stride=1, groups=1)
+    kw2 = dict(n=wl.n, h=wl.h, w=wl.w, stride=1, groups=wl.c)
+    x_bytes = wl.n * wl.h * wl.w * wl.c * 2
+    sites = wl.n * wl.h * wl.w
+
+    def build(e1, e2, chained):
+        l1 = SkipConv(w1, eps=e1, block=b, act_out="identity", emit_residual=chained, **kw1)
+        l2 = SkipConv(w2, eps=e2, block=b, **kw2)
+        return l1, l2
+
+    def step(l1, l2, x, chained):
+        l1.step(x)
+        if chained:
+            l2.step_chained(l1)
+        else:
+            l2.step(l1.activation())
+
+    stats1 = gpu_stats(kw1, w1, frames_dev)
+
+    def calibrate(d):
+        e1 = eps_for_density(stats1, b, wl.h, wl.w, d)
+        l1 = SkipConv(w1, eps=e1, block=b, act_out="identity", **kw1)
+        ys = []
+        for x in frames_dev:
+            l1.step(x)
+            ys.append(l1.activation().clone().view(wl.n, wl.h, wl.w, wl.c))
+        l1.close()
+        e2 = eps_for_density(gpu_stats(kw2, w2, ys), b, wl.h, wl.w, d)
+        return e1, e2
+
+    def run(e1, e2, chained, steps, timing):
+        l1, l2 = build(e1, e2, chained)
+        for t in range(nfr):  # warm-up pass over the clip
+            if t == 0:
+                l1.reset()
+                l2.reset()
+            step(l1, l2, frames_dev[t], chained)
+        if timing:
+            S.skipconv_timing_begin(l1.handle, steps, 1)
+            S.skipconv_timing_begin(l2.handle, steps, 1)
+        act = [0, 0]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for j in range(steps):
+            if j % nfr == 0:
+                l1.reset()
+                l2.reset()
+            step(l1, l2, frames_dev[j % nfr], chained)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        res = {"frames_per_s": steps * wl.n / wall, "us_per_step": 1e6 * wall / steps}
+        if timing:
+            g1, c1, n1, _ = S.skipconv_timing_read(l1.handle, l1._stream(), steps)
+            g2, c2, n2, _ = S.skipconv_timing_read(l2.handle, l2._stream(), steps)
+            n1, n2 = max(n1, 1), max(n2, 1)
+            res.update({"pw_gate_us": 1e3 * g1 / n1, "pw_conv_us": 1e3 * c1 / n1,
+                        "dw_gate_us": 1e3 * g2 / n2, "dw_conv_us": 1e3 * c2 / n2, "timed_steps": [n1, n2]})
+            # active sites of both layers over one clip pass (same schedule)
+            for t in range(nfr):
+                if t == 0:
+                    l1.reset()
+                    l2.reset()
+                step(l1, l2, frames_dev[t], chained)
+                act[0] += l1.active_count()[1]
+                act[1] += l2.active_count()[1]
+            res["density_pw"] = act[0] / (sites * nfr)
+            res["density_dw"] = act[1] / (sites * nfr)
+            # depthwise convolution kernel: residual at the active sites (x_t and
+            # x_{t-1}) and z read-modify-written there, per launch
+            dw_bytes = act[1] / nfr * wl.c * (2 + 2 + 8)
+            res["dw_conv_bytes_per_launch"] = dw_bytes
+            res["dw_conv_gbs"] = dw_bytes / (res["dw_conv_us"] * 1e-6) / 1e9
+        l1.close()
+        l2.close()
+        return res
+
+    points = []
+    for d in (0.1, 0.25, 0.5):
+        e1, e2 = calibrate(d)
+        for chained in (False, True):
+            r = run(e1, e2, chained, args.steps, False)
+            r.update(run(e1, e2, chained, max(2 * nfr, 64), True) | {"frames_per_s": r["frames_per_s"],
+                                                                      "us_per_step": r["us_per_step"]})
+            r.update({"target_density": d, "eps": [e1, e2], "variant": "chained" if chained else "full"})
+            log(f"[bench] mbconv192 d={d} {r['variant']}: {r['frames_per_s']:.0f} frames/s, "
+                f"{r['us_per_step']:.1f} us/step; pw gate {r['pw_gate_us']:.1f} conv {r['pw_conv_us']:.1f}, "
+                f"dw gate {r['dw_gate_us']:.1f} conv {r['dw_conv_us']:.1f} us; density pw {r['density_pw']:.3f} "
+                f"dw {r['density_dw']:.3f}")
+            points.append(r)
+
+    # shake frames: layer-1 active sites per clip position, plain steps vs steps
+    # with the known shift (Sec. 3.3) at the 25 % threshold
+    e1, _ = calibrate(0.25)
+    shift = [(0, 0)] * nfr
+    prev = (0, 0)
+    for t in range(1, nfr):
+        cur = vid.shake_shift.get(t, (0, 0))
+        shift[t] = (cur[0] - prev[0], cur[1] - prev[1])
+        prev = cur
+    dens = {}
+    for comp in (False, True):
+        lay = SkipConv(w1, eps=e1, block=b, translate=True, **kw1)
+        per = []
+        for t in range(nfr):
+            if comp:
+                lay.step_translated(frames_dev[t], *shift[t])
+            else:
+                lay.step(frames_dev[t])
+            per.append(lay.active_count()[1] / sites)
+        lay.close()
+        sh = [per[t] for t in range(1, nfr) if shift[t] != (0, 0)]
+        ot = [per[t] for t in range(1, nfr) if shift[t] == (0, 0)]
+        dens["compensated" if comp else "plain"] = {"shake": float(np.mean(sh)) if sh else None,
+                                                    "other": float(np.mean(ot)) if ot else None}
+    log(f"[bench] mbconv192 shake frames {sorted(shake)}: layer-1 density {dens}")
+
+    head = next(p for p in points if p["target_density"] == args.density and p["variant"] == "chained") \
+        if any(p["target_density"] == args.density for p in points) else points[3]
+    a = head["dw_conv_gbs"]
+    out = {
+        "metric": METRIC, "value": head["frames_per_s"], "unit": "frames/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": nfr, "ms_per_step": head["us_per_step"] * 1e-3, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic",
+        "config": {"workload": "mbconv192: 1x1 conv 192->192 then depthwise 3x3 (groups 192), identity between, "
+                               f"64x64 frames, batch 1, {nfr}-frame clip (reset at frame 1), 8x8 blocks, "
+                               "10% camera-shake frames, layer 2 chained on layer 1's emitted residual",
+                   "target_density": head["target_density"], "eps": head["eps"],
+                   "shake_frames": sorted(shake), "shake_density_layer1": dens},
+        "roofline": {"kernel": "depthwise conv (VALU, active blocks)", "bound": "hbm", "achieved": a,
+                     "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": a / PEAK_HBM_GBS, "traffic": None,
+                     "bytes_per_launch": head["dw_conv_bytes_per_launch"], "us_per_launch": head["dw_conv_us"]},
+        "cpu_baseline": None, "sweep": points,
+    }
+    print(json.dumps(out), flush=True)
+
+
 # -------------------------------------------------------------------- main --
 
 def main():
@@ -591,7 +751,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=640)
     ap.add_argument("--warmup", type=int, default=64)
-    ap.add_argument("--workload", default="rect64", choices=["rect64", "blob128", "square16", "stack6"])
+    ap.add_argument("--workload", default="rect64",
+                    choices=["rect64", "blob128", "square16", "stack6", "mbconv192"])
     ap.add_argument("--block", type=int, default=None)
     ap.add_argument("--density", type=float, default=0.25)
     ap.add_argument("--frames", type=int, default=None)
@@ -629,6 +790,9 @@ def main():
     torch.cuda.set_device(0)
     if args.workload == "stack6":
         bench_stack(args)
+        return
+    if args.workload == "mbconv192":
+        bench_mbconv(args)
         return
     wl, clip = load_workload(args.workload, args.frames)
     frames_dev = upload(clip, wl.dtype)

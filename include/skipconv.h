@@ -250,7 +250,9 @@ int skipconv_gate_tile(skipconv_t h, int32_t* ts, int32_t* lane_sum);
 /* Convolution kernel of the split pipeline: *kind = 0 gather (tiles of 64
  * active sites, operands gathered from the frames), 1 block halo (tiles of
  * rows of one active block, the residual halo staged in LDS; bf16, C_in % 32
- * = 0, b in {4, 8, 16, 32, 64}), 2 depthwise. Host only. */
+ * = 0, b in {4, 8, 16, 32, 64}), 2 depthwise over the listed sites (fp32, or
+ * C % 8 != 0), 3 depthwise with the residual halo of tiles of an active block
+ * staged in LDS (bf16, C % 8 == 0). Host only. */
 int skipconv_conv_kernel(skipconv_t h, int32_t* kind);
 
 /* ---- introspection (tests and benchmarks; each synchronises `stream`) ---- */

@@ -581,6 +581,148 @@ __global__ void __launch_bounds__(kConvThreads) depthwise_kernel(ConvParams p) {
   }
 }
 
+// ------------------------------------------------ depthwise, bf16, halo ----
+//
+// Depthwise layers (groups = C, bf16, C % 8 == 0) over active blocks: a tile
+// is tr output rows x b columns of one active block (tr * b sites). Per tile:
+// the old z of this thread's outputs is loaded, then the residual halo
+// ((tr-1)s+k rows x (b-1)s+k columns x C) with every load of a round in
+// flight, rho = bf16(x_t - x_{t-1}) stored in LDS (zero outside the frame:
+// such taps add exactly nothing); each thread then forms 8 channels of one
+// site at a time, fp32 FMA over the k x k taps in row-major order with the
+// [tap][c] weights staged in LDS once per workgroup, and writes z (and the
+// activation). Consecutive threads take consecutive channel chunks, so z
+// moves in contiguous 32-byte pieces per thread and LDS reads are
+// conflict-free.
+constexpr int kDwThreads = 256;
+constexpr int kDwItems = 8;   // halo chunks in flight per thread
+constexpr int kDwOut = 8;     // output chunks per thread and pass
+
+__global__ void __launch_bounds__(kDwThreads) depthwise_halo_kernel(ConvParams p, HaloParams hp) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  uint8_t* halo = lds;
+  float* wl = reinterpret_cast<float*>(lds + hp.lds_bytes);  // [tap][c]
+  const int b = p.block, s = p.stride, k = p.k, c = p.c;
+  const int nchunk = c >> 3;
+  const int tpb = hp.tiles_per_block;
+  const int ntiles = (int)p.counters[kCtrCount] * tpb;
+  if (p.zero_ctr && blockIdx.x == 0 && threadIdx.x == 0) *p.zero_ctr = 0u;  // next step's work list
+  const uint16_t* xt = static_cast<const uint16_t*>(p.x_t);
+  const uint16_t* xp = static_cast<const uint16_t*>(p.x_prev);
+  const size_t ximg = (size_t)p.h * p.w * c;
+  const size_t zimg = (size_t)p.h_out * p.w_out * c;
+  const float* wp = static_cast<const float*>(p.wpack);
+  for (int i = threadIdx.x; i < k * k * c; i += kDwThreads) wl[i] = wp[i];
+  typedef const __attribute__((address_space(4))) uint32_t const_u32;
+  const const_u32* list = (const const_u32*)p.list;
+  const int total = hp.hh * hp.hw * nchunk;
+  const int nout = hp.tr * b * nchunk;
+
+  for (TileWalk tw(ntiles); tw.t < tw.end; tw.t += tw.step) {
+    const int j0 = tw.t / tpb, band = tw.t - j0 * tpb;
+    const uint32_t blk = list[j0];
+    const int per_img = p.hb * p.wb;
+    const int n = (int)(blk / per_img);
+    const int rem = (int)(blk - (uint32_t)n * per_img);
+    const int bi = rem / p.wb, bj = rem - bi * p.wb;
+    const int oy0 = bi * b + band * hp.tr, ox0 = bj * b;
+    const int rows_ok = min(min(hp.tr, b - band * hp.tr), p.h_out - oy0), cols_ok = min(b, p.w_out - ox0);
+    const int iy0 = oy0 * s - p.pad, ix0 = ox0 * s - p.pad;
+    const auto xrs = frame_rsrc(xt + (size_t)n * ximg, (uint32_t)(ximg * 2));
+    const auto prs = frame_rsrc((p.no_prev ? xt : xp) + (size_t)n * ximg, (uint32_t)(ximg * 2));
+    const auto zrs = frame_rsrc(p.z + (size_t)n * zimg, (uint32_t)(zimg * 4));
+
+    // halo rounds: rho = bf16(x_t - x_{t-1}) into LDS
+    for (int base = 0; base < total; base += kDwThreads * kDwItems) {
+      u32x4 ra[kDwItems], rb[kDwItems];
+#pragma unroll
+      for (int u = 0; u < kDwItems; ++u) {
+        const int idx = base + u * kDwThreads + threadIdx.x;
+        const int px = idx / nchunk, ch = idx - px * nchunk;
+        const int hy = px / hp.hw, hx = px - hy * hp.hw;
+        const int y = iy0 + hy, x = ix0 + hx;
+        const bool in = idx < total && y >= 0 && y < p.h && x >= 0 && x < p.w;
+        const int yp = y - p.sy, xq = x - p.sx;
+        const bool pin = in && !p.no_prev && yp >= 0 && yp < p.h && xq >= 0 && xq < p.w;
+        ra[u] = __builtin_amdgcn_raw_buffer_load_b128(
+            xrs, in ? (uint32_t)(((y * p.w + x) * c + ch * 8) * 2) : kOutOfRange, 0, 0);
+        rb[u] = __builtin_amdgcn_raw_buffer_load_b128(
+            prs, pin ? (uint32_t)(((yp * p.w + xq) * c + ch * 8) * 2) : kOutOfRange, 0, 0);
+      }
+#pragma unroll
+      for (int u = 0; u < kDwItems; ++u) {
+        const int idx = base + u * kDwThreads + threadIdx.x;
+        if (idx >= total) continue;
+        const int px = idx / nchunk, ch = idx - px * nchunk;
+        uint32_t q[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t wa = ra[u][e], wb = rb[u][e];
+          const float r0 = __fsub_rn(__uint_as_float(wa << 16), __uint_as_float(wb << 16));
+          const float r1 = __fsub_rn(__uint_as_float(wa & 0xffff0000u), __uint_as_float(wb & 0xffff0000u));
+          q[e] = pack_bf16(r0, r1);
+        }
+        *reinterpret_cast<u32x4*>(halo + px * hp.pstride + ch * 16) = u32x4{q[0], q[1], q[2], q[3]};
+      }
+    }
+    __syncthreads();
+
+    // outputs: kDwOut (site, chunk) items per thread and pass, old z loaded first
+    for (int base = 0; base < nout; base += kDwThreads * kDwOut) {
+      floatx4 zo[kDwOut][2];
+      uint32_t zoff[kDwOut];
+#pragma unroll
+      for (int u = 0; u < kDwOut; ++u) {
+        const int idx = base + u * kDwThreads + threadIdx.x;
+        const int site = idx / nchunk, ch = idx - site * nchunk;
+        const int ly = site / b, lx = site - ly * b;
+        const bool ok = idx < nout && ly < rows_ok && lx < cols_ok;
+        zoff[u] = ok ? (uint32_t)((((oy0 + ly) * p.w_out + ox0 + lx) * c + ch * 8) * 4) : kOutOfRange;
+#pragma unroll
+        for (int hlf = 0; hlf < 2; ++hlf)
+          zo[u][hlf] = __builtin_bit_cast(
+              floatx4, __builtin_amdgcn_raw_buffer_load_b128(
+                           zrs, p.reference || zoff[u] == kOutOfRange ? kOutOfRange : zoff[u] + 16 * hlf, 0, 0));
+      }
+#pragma unroll
+      for (int u = 0; u < kDwOut; ++u) {
+        const int idx = base + u * kDwThreads + threadIdx.x;
+        if (idx >= nout) continue;
+        const int site = idx / nchunk, ch = idx - site * nchunk;
+        const int ly = site / b, lx = site - ly * b;
+        float acc[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[j] = 0.0f;
+        for (int kh = 0; kh < k; ++kh)
+          for (int kw = 0; kw < k; ++kw) {
+            const u32x4 r = *reinterpret_cast<const u32x4*>(
+                halo + ((ly * s + kh) * hp.hw + lx * s + kw) * hp.pstride + ch * 16);
+            const float* wt = wl + (kh * k + kw) * c + ch * 8;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              acc[2 * e] = __builtin_fmaf(wt[2 * e], __uint_as_float(r[e] << 16), acc[2 * e]);
+              acc[2 * e + 1] = __builtin_fmaf(wt[2 * e + 1], __uint_as_float(r[e] & 0xffff0000u), acc[2 * e + 1]);
+            }
+          }
+        floatx4 nv[2];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) nv[j >> 2][j & 3] = p.reference ? acc[j] : zo[u][j >> 2][j & 3] + acc[j];
+#pragma unroll
+        for (int hlf = 0; hlf < 2; ++hlf)
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, nv[hlf]), zrs,
+                                                 zoff[u] == kOutOfRange ? kOutOfRange : zoff[u] + 16 * hlf, 0, 0);
+        if (p.act && zoff[u] != kOutOfRange) {
+          const size_t o = (size_t)n * zimg + zoff[u] / 4;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) store_y<uint16_t>(p.y, o + j, activate(nv[j >> 2][j & 3], p.act));
+        }
+      }
+    }
+    // all waves are done with the halo before the next tile overwrites it
+    __syncthreads();
+  }
+}
+
 // -------------------------------------------------------------- repack ----
 
 // B fragment layout of v_mfma_f32_16x16x32_bf16: for k-step ks and output tile
@@ -708,6 +850,23 @@ hipError_t launch_conv_halo(const ConvParams& p, const HaloParams& hp, int grid,
 #undef SC_X
     default: return hipErrorInvalidValue;
   }
+}
+
+hipError_t launch_depthwise_halo(const ConvParams& p, const HaloParams& hp, int grid, hipStream_t st) {
+  const int lds = hp.lds_bytes + p.k * p.k * p.c * 4;
+  hipLaunchKernelGGL(depthwise_halo_kernel, dim3(grid), dim3(kDwThreads), lds, st, p, hp);
+  return hipGetLastError();
+}
+
+int depthwise_halo_occupancy(const HaloParams& hp, int k, int c) {
+  const int lds = hp.lds_bytes + k * k * c * 4;
+  if (hipFuncSetAttribute(reinterpret_cast<const void*>(depthwise_halo_kernel),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess)
+    return 0;
+  int blocks = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, depthwise_halo_kernel, kDwThreads, lds) != hipSuccess)
+    return 0;
+  return blocks;
 }
 
 hipError_t launch_depthwise(const ConvParams& p, int dtype, int grid, hipStream_t st) {

@@ -160,6 +160,11 @@ hipError_t launch_conv(const ConvParams& p, int dtype, bool fast, int grid, hipS
 hipError_t launch_conv_halo(const ConvParams& p, const HaloParams& hp, int grid, hipStream_t st);
 int conv_halo_occupancy(const HaloParams& hp);  // resident workgroups per CU (0 on error)
 hipError_t launch_depthwise(const ConvParams& p, int dtype, int grid, hipStream_t st);
+// Depthwise over active blocks with the residual halo in LDS (bf16, C % 8 == 0):
+// hp.tr rows x block columns per tile, hp.lds_bytes of halo (+ the [tap][c]
+// fp32 weights, added by the launch).
+hipError_t launch_depthwise_halo(const ConvParams& p, const HaloParams& hp, int grid, hipStream_t st);
+int depthwise_halo_occupancy(const HaloParams& hp, int k, int c);  // resident workgroups per CU
 
 // Residual emission of a layer that feeds a chained layer: at the blocks the
 // step updated, y = dtype(act(z)) and r = y_new - y_old (fp32, and its bf16

@@ -48,6 +48,8 @@ struct Geometry {
   bool fast;
   bool halo;            // dense bf16 block-halo kernel (else the gather kernel)
   sc::HaloParams hp;
+  bool dw_halo;         // depthwise bf16: residual halo of tr x b sites in LDS
+  sc::HaloParams dwp;
   bool fused;           // single-pass kernel instead of gate + compaction + conv
   int f_ts, f_tiles_y, f_tiles_x, f_grid, f_copy_in_halo;
   int f_kc, f_nchunks, f_nbuf, f_mw, f_pstride, f_zero_pix, f_off_b, f_off_halo, f_off_a, f_lds;
@@ -231,6 +233,33 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
     G.wpack_bytes = (size_t)k * k * d->c_in * 4;
   }
   G.conv_max_tiles = (int)(((long)G.nb * b * b + 63) / 64);
+
+  // depthwise halo kernel: tiles of tr rows x b columns of an active block, tr
+  // the largest row count (halving from b) whose halo and [tap][c] weights
+  // fit in 64 KB of LDS; one image of x and z within 2^31 bytes
+  G.dw_halo = false;
+  if (depthwise && d->dtype == SKIPCONV_BF16 && d->c_in % 8 == 0 &&
+      (long)d->h * d->w * d->c_in * 2 < (1L << 31) && (long)G.h_out * G.w_out * d->c_in * 4 < (1L << 31)) {
+    sc::HaloParams& H = G.dwp;
+    H.config = 0;
+    H.pstride = 2 * d->c_in + 16;
+    H.hw = (b - 1) * s + k;
+    const long wbytes = (long)k * k * d->c_in * 4;
+    for (int tr = b; tr >= 1; tr = tr > 1 ? (tr + 1) / 2 : 0) {
+      const long hh = (long)(tr - 1) * s + k;
+      if (hh * H.hw * H.pstride + wbytes <= 64 * 1024) {
+        H.tr = tr;
+        H.hh = (int)hh;
+        H.tiles_per_block = (b + tr - 1) / tr;
+        H.lds_bytes = (int)(hh * H.hw * H.pstride);
+        H.threads = 256;
+        G.dw_halo = true;
+        G.conv_max_tiles = G.nb * H.tiles_per_block;
+        break;
+      }
+      if (tr == 1) break;
+    }
+  }
 
   // block-halo kernel: tile = tr rows x b columns of a block, chosen per wave layout
   G.halo = false;
@@ -689,6 +718,15 @@ int skipconv_create(const skipconv_desc* d, const void* weights, void* workspace
   // roofline. Threshold: four tiles per CU.
   if (h->g.fused && (h->g.f_grid > 4 * h->num_cu || sc::prepare_fused(fused_params(h, nullptr, true)) < 1))
     h->g.fused = false;
+  if (g.dw_halo) {
+    const int occ = sc::depthwise_halo_occupancy(g.dwp, d->kernel, d->c_in);
+    if (occ < 1) {
+      h->g.dw_halo = false;  // cannot hold the halo: per-site depthwise kernel
+      h->g.conv_max_tiles = (int)(((long)g.nb * d->block * d->block + 63) / 64);
+    } else {
+      h->conv_occ = std::min(8, occ);
+    }
+  }
   if (g.halo) {
     int max_lds = 0;
     if (hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, h->device) != hipSuccess ||
@@ -792,7 +830,7 @@ int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t
     cp.zero_ctr = sl.zero;
     if (e == hipSuccess) {
       if (g.depthwise)
-        e = sc::launch_depthwise(cp, d.dtype, conv_grid(h), st);
+        e = (g.dw_halo ? sc::launch_depthwise_halo(cp, g.dwp, conv_grid(h), st) : sc::launch_depthwise(cp, d.dtype, conv_grid(h), st));
       else if (g.halo)
         e = sc::launch_conv_halo(cp, g.hp, conv_grid(h), st);
       else
@@ -876,7 +914,7 @@ int skipconv_step_translated(skipconv_t h, const void* x_t, int32_t dy, int32_t 
     cp.sy = pass ? 0 : dy;
     cp.sx = pass ? 0 : dx;
     if (g.depthwise)
-      e = sc::launch_depthwise(cp, d.dtype, conv_grid(h), st);
+      e = (g.dw_halo ? sc::launch_depthwise_halo(cp, g.dwp, conv_grid(h), st) : sc::launch_depthwise(cp, d.dtype, conv_grid(h), st));
     else if (g.halo)
       e = sc::launch_conv_halo(cp, g.hp, conv_grid(h), st);
     else
@@ -963,7 +1001,7 @@ int skipconv_step_chained(skipconv_t h, skipconv_t up, void* stream, const float
   cp.no_prev = 1;
   cp.act = h->emits() ? 0 : d.act_out;
   if (g.depthwise)
-    e = sc::launch_depthwise(cp, d.dtype, conv_grid(h), st);
+    e = (g.dw_halo ? sc::launch_depthwise_halo(cp, g.dwp, conv_grid(h), st) : sc::launch_depthwise(cp, d.dtype, conv_grid(h), st));
   else if (g.halo)
     e = sc::launch_conv_halo(cp, g.hp, conv_grid(h), st);
   else
@@ -1039,7 +1077,7 @@ int skipconv_gate_tile(skipconv_t h, int32_t* ts, int32_t* lane_sum) {
 int skipconv_conv_kernel(skipconv_t h, int32_t* kind) {
   if (!h) return SKIPCONV_E_STATE;
   if (!kind) return SKIPCONV_E_INVALID_ARG;
-  *kind = h->g.depthwise ? 2 : (h->g.halo ? 1 : 0);
+  *kind = h->g.depthwise ? (h->g.dw_halo ? 3 : 2) : (h->g.halo ? 1 : 0);
   return SKIPCONV_OK;
 }
 

@@ -412,7 +412,7 @@ class SkipConv:
 
     @property
     def conv_kernel(self) -> int:
-        """Split-pipeline convolution kernel: 0 gather, 1 block halo, 2 depthwise."""
+        """Split-pipeline convolution kernel: 0 gather, 1 block halo, 2 depthwise per site, 3 depthwise halo."""
         return skipconv_conv_kernel(self.handle)
 
     def set_eps(self, eps: float):

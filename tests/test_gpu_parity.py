@@ -425,12 +425,16 @@ def test_pipeline_selection():
     w48 = to_device(weight_storage(syn.he_weights(64, 48, 3, seed=1), "bf16"), "bf16")
     assert S.SkipConv(w48, n=4, h=512, w=512, block=16).gate_tile == (16, 0)
     # split convolution kernels: block halo (bf16, C_in % 32 == 0, b in {4..64}),
-    # gather otherwise, depthwise for groups == C
+    # gather otherwise; depthwise (groups == C) with the halo in LDS for bf16
+    # and C % 8 == 0, per listed site otherwise
     assert S.SkipConv(w128, n=4, h=512, w=512, block=16).conv_kernel == 1
     assert S.SkipConv(w, n=1, h=128, w=96, block=1, split=True).conv_kernel == 0
     assert S.SkipConv(w48, n=1, h=32, w=32, block=8).conv_kernel == 0
     wdw = to_device(weight_storage(syn.he_weights(64, 1, 3, seed=1), "bf16"), "bf16")
-    assert S.SkipConv(wdw, n=1, h=32, w=32, block=8, groups=64).conv_kernel == 2
+    assert S.SkipConv(wdw, n=1, h=32, w=32, block=8, groups=64).conv_kernel == 3
+    assert S.SkipConv(wdw, n=1, h=32, w=32, block=1, groups=64).conv_kernel == 3
+    wdw32 = to_device(weight_storage(syn.he_weights(64, 1, 3, seed=1), "f32"), "f32")
+    assert S.SkipConv(wdw32, n=1, h=32, w=32, block=8, groups=64).conv_kernel == 2
 
 
 # Gate tiles of 32 x 32 output sites with the chunk sums of a pixel combined
@@ -526,6 +530,63 @@ def test_block_halo_conv(case):
     layer, orc = _layer_pair(wt, n=n, h=h, w=w, dtype="bf16", eps=eps, block=b, stride=s, split=True,
                              translate=translated, act_out="relu")
     assert layer.conv_kernel == 1, layer.conv_kernel
+    for t, (f, d) in enumerate(zip(frames, shifts)):
+        if t == 5:
+            layer.reset()
+            orc.reset()
+        xs = syn.to_storage(f, "bf16")
+        say(f"[{tag}] frame {t} shift={d} eps={eps:.4g}")
+        if translated:
+            layer.step_translated(to_device(xs, "bf16"), *d)
+            ref = orc.step(xs, shift=d)
+        else:
+            layer.step(to_device(xs, "bf16"))
+            ref = orc.step(xs)
+        compare_frame(layer, ref, "bf16", t=t, tag=tag, keep_stats=True)
+        z = layer._z.cpu().numpy()
+        y = layer.activation()
+        torch.cuda.synchronize()
+        y_bits = y.view(torch.int16).cpu().numpy().view(np.uint16).reshape(z.shape)
+        assert np.array_equal(y_bits, O.f32_to_bf16_rne(np.maximum(z, 0.0).astype(np.float32))), \
+            f"{tag} t={t}: activation output"
+    layer.close()
+
+
+# Depthwise layers (groups = C) with the residual halo staged in LDS: edge
+# tiles, 8 x 8, 4 x 4, 16 x 16 (tiles of 4 rows) and 3 x 3 blocks, stride 2,
+# 5 x 5, a translated run and a ReLU output:
+# (n, h, w, c, k, stride, block, translated)
+DW_HALO = [
+    (1, 37, 29, 192, 3, 1, 8, False),
+    (2, 40, 36, 64, 3, 2, 4, False),
+    (1, 45, 40, 192, 3, 1, 16, False),
+    (1, 33, 31, 32, 5, 1, 3, False),
+    (1, 30, 34, 64, 3, 1, 1, True),
+]
+
+
+@pytest.mark.parametrize("case", DW_HALO, ids=[f"dw{i}" for i in range(len(DW_HALO))])
+def test_depthwise_halo(case):
+    """Depthwise split pipeline with the LDS-halo kernel: masks bit-exact, z within tolerance after
+    every frame (reset mid-stream), activation output = bf16(relu(z)) bit for bit."""
+    n, h, w, c, k, s, b, translated = case
+    rng = np.random.Generator(np.random.PCG64(900 + c + k + b))
+    vid = syn.RectVideo(h, w, c, 7, seed=901 + c, batch=n, n_rect=3, side_lo=5, side_hi=14)
+    base = list(vid)
+    shifts = [(0, 0), (s, 0), (0, -s), (0, 0), (-s, 2 * s), (s, s), (0, 0)] if translated else [(0, 0)] * 7
+    frames, acc = [], (0, 0)
+    for f, d in zip(base, shifts):
+        acc = (acc[0] + d[0], acc[1] + d[1])
+        frames.append(O.translate(f, *acc) if translated else f)
+    wt = rng.normal(0, 0.3, (c, 1, k, k)).astype(np.float32)
+    pad = (k - 1) // 2
+    ho, wo = O.out_size(h, k, s, pad), O.out_size(w, k, s, pad)
+    stats = oracle_stats(base[:3], (c, c, k, k), dtype="bf16", stride=s)
+    eps = eps_for_density(stats, b, ho, wo, 0.4)
+    tag = f"depthwise halo {case}"
+    layer, orc = _layer_pair(wt, n=n, h=h, w=w, dtype="bf16", eps=eps, block=b, stride=s, groups=c,
+                             split=True, translate=translated, act_out="relu")
+    assert layer.conv_kernel == 3, layer.conv_kernel
     for t, (f, d) in enumerate(zip(frames, shifts)):
         if t == 5:
             layer.reset()
