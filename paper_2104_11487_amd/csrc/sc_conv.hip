@@ -595,7 +595,7 @@ __global__ void __launch_bounds__(kConvThreads) depthwise_kernel(ConvParams p) {
 // moves in contiguous 32-byte pieces per thread and LDS reads are
 // conflict-free.
 constexpr int kDwThreads = 256;
-constexpr int kDwItems = 8;   // halo chunks in flight per thread
+constexpr int kDwItems = 12;  // halo chunks in flight per thread (10 x 10 x 24 chunks: one round)
 constexpr int kDwOut = 8;     // output chunks per thread and pass
 
 __global__ void __launch_bounds__(kDwThreads) depthwise_halo_kernel(ConvParams p, HaloParams hp) {
@@ -611,8 +611,25 @@ __global__ void __launch_bounds__(kDwThreads) depthwise_halo_kernel(ConvParams p
   const uint16_t* xp = static_cast<const uint16_t*>(p.x_prev);
   const size_t ximg = (size_t)p.h * p.w * c;
   const size_t zimg = (size_t)p.h_out * p.w_out * c;
-  const float* wp = static_cast<const float*>(p.wpack);
-  for (int i = threadIdx.x; i < k * k * c; i += kDwThreads) wl[i] = wp[i];
+  {
+    // [tap][c] weights into LDS, 16 bytes per load, four loads in flight per thread
+    const float4* w4 = static_cast<const float4*>(p.wpack);
+    float4* l4 = reinterpret_cast<float4*>(wl);
+    const int nw4 = k * k * c / 4;
+    for (int base = 0; base < nw4; base += 4 * kDwThreads) {
+      float4 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = base + u * kDwThreads + threadIdx.x;
+        v[u] = w4[i < nw4 ? i : 0];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = base + u * kDwThreads + threadIdx.x;
+        if (i < nw4) l4[i] = v[u];
+      }
+    }
+  }
   typedef const __attribute__((address_space(4))) uint32_t const_u32;
   const const_u32* list = (const const_u32*)p.list;
   const int total = hp.hh * hp.hw * nchunk;
@@ -632,6 +649,63 @@ __global__ void __launch_bounds__(kDwThreads) depthwise_halo_kernel(ConvParams p
     const auto prs = frame_rsrc((p.no_prev ? xt : xp) + (size_t)n * ximg, (uint32_t)(ximg * 2));
     const auto zrs = frame_rsrc(p.z + (size_t)n * zimg, (uint32_t)(zimg * 4));
 
+    // old z of a pass of kDwOut (site, chunk) outputs per thread; out-of-range
+    // offsets for outputs outside the tile (and for every output on a reference frame)
+    floatx4 zo[kDwOut][2];
+    uint32_t zoff[kDwOut];
+    auto zload = [&](int base) {
+#pragma unroll
+      for (int u = 0; u < kDwOut; ++u) {
+        const int idx = base + u * kDwThreads + threadIdx.x;
+        const int site = idx / nchunk, ch = idx - site * nchunk;
+        const int ly = site / b, lx = site - ly * b;
+        const bool ok = idx < nout && ly < rows_ok && lx < cols_ok;
+        zoff[u] = ok ? (uint32_t)((((oy0 + ly) * p.w_out + ox0 + lx) * c + ch * 8) * 4) : kOutOfRange;
+#pragma unroll
+        for (int hlf = 0; hlf < 2; ++hlf)
+          zo[u][hlf] = __builtin_bit_cast(
+              floatx4, __builtin_amdgcn_raw_buffer_load_b128(
+                           zrs, p.reference || !ok ? kOutOfRange : zoff[u] + 16 * hlf, 0, 0));
+      }
+    };
+    auto outputs = [&](int base) {
+#pragma unroll
+      for (int u = 0; u < kDwOut; ++u) {
+        const int idx = base + u * kDwThreads + threadIdx.x;
+        if (idx >= nout) continue;
+        const int site = idx / nchunk, ch = idx - site * nchunk;
+        const int ly = site / b, lx = site - ly * b;
+        float acc[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[j] = 0.0f;
+        for (int kh = 0; kh < k; ++kh)
+          for (int kw = 0; kw < k; ++kw) {
+            const u32x4 r = *reinterpret_cast<const u32x4*>(
+                halo + ((ly * s + kh) * hp.hw + lx * s + kw) * hp.pstride + ch * 16);
+            const float* wt = wl + (kh * k + kw) * c + ch * 8;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              acc[2 * e] = __builtin_fmaf(wt[2 * e], __uint_as_float(r[e] << 16), acc[2 * e]);
+              acc[2 * e + 1] = __builtin_fmaf(wt[2 * e + 1], __uint_as_float(r[e] & 0xffff0000u), acc[2 * e + 1]);
+            }
+          }
+        floatx4 nv[2];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) nv[j >> 2][j & 3] = p.reference ? acc[j] : zo[u][j >> 2][j & 3] + acc[j];
+#pragma unroll
+        for (int hlf = 0; hlf < 2; ++hlf)
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, nv[hlf]), zrs,
+                                                 zoff[u] == kOutOfRange ? kOutOfRange : zoff[u] + 16 * hlf, 0, 0);
+        if (p.act && zoff[u] != kOutOfRange) {
+          const size_t o = (size_t)n * zimg + zoff[u] / 4;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) store_y<uint16_t>(p.y, o + j, activate(nv[j >> 2][j & 3], p.act));
+        }
+      }
+    };
+
+    // the first pass's old z is in flight with the halo loads
+    zload(0);
     // halo rounds: rho = bf16(x_t - x_{t-1}) into LDS
     for (int base = 0; base < total; base += kDwThreads * kDwItems) {
       u32x4 ra[kDwItems], rb[kDwItems];
@@ -666,57 +740,10 @@ __global__ void __launch_bounds__(kDwThreads) depthwise_halo_kernel(ConvParams p
       }
     }
     __syncthreads();
-
-    // outputs: kDwOut (site, chunk) items per thread and pass, old z loaded first
-    for (int base = 0; base < nout; base += kDwThreads * kDwOut) {
-      floatx4 zo[kDwOut][2];
-      uint32_t zoff[kDwOut];
-#pragma unroll
-      for (int u = 0; u < kDwOut; ++u) {
-        const int idx = base + u * kDwThreads + threadIdx.x;
-        const int site = idx / nchunk, ch = idx - site * nchunk;
-        const int ly = site / b, lx = site - ly * b;
-        const bool ok = idx < nout && ly < rows_ok && lx < cols_ok;
-        zoff[u] = ok ? (uint32_t)((((oy0 + ly) * p.w_out + ox0 + lx) * c + ch * 8) * 4) : kOutOfRange;
-#pragma unroll
-        for (int hlf = 0; hlf < 2; ++hlf)
-          zo[u][hlf] = __builtin_bit_cast(
-              floatx4, __builtin_amdgcn_raw_buffer_load_b128(
-                           zrs, p.reference || zoff[u] == kOutOfRange ? kOutOfRange : zoff[u] + 16 * hlf, 0, 0));
-      }
-#pragma unroll
-      for (int u = 0; u < kDwOut; ++u) {
-        const int idx = base + u * kDwThreads + threadIdx.x;
-        if (idx >= nout) continue;
-        const int site = idx / nchunk, ch = idx - site * nchunk;
-        const int ly = site / b, lx = site - ly * b;
-        float acc[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) acc[j] = 0.0f;
-        for (int kh = 0; kh < k; ++kh)
-          for (int kw = 0; kw < k; ++kw) {
-            const u32x4 r = *reinterpret_cast<const u32x4*>(
-                halo + ((ly * s + kh) * hp.hw + lx * s + kw) * hp.pstride + ch * 16);
-            const float* wt = wl + (kh * k + kw) * c + ch * 8;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              acc[2 * e] = __builtin_fmaf(wt[2 * e], __uint_as_float(r[e] << 16), acc[2 * e]);
-              acc[2 * e + 1] = __builtin_fmaf(wt[2 * e + 1], __uint_as_float(r[e] & 0xffff0000u), acc[2 * e + 1]);
-            }
-          }
-        floatx4 nv[2];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) nv[j >> 2][j & 3] = p.reference ? acc[j] : zo[u][j >> 2][j & 3] + acc[j];
-#pragma unroll
-        for (int hlf = 0; hlf < 2; ++hlf)
-          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, nv[hlf]), zrs,
-                                                 zoff[u] == kOutOfRange ? kOutOfRange : zoff[u] + 16 * hlf, 0, 0);
-        if (p.act && zoff[u] != kOutOfRange) {
-          const size_t o = (size_t)n * zimg + zoff[u] / 4;
-#pragma unroll
-          for (int j = 0; j < 8; ++j) store_y<uint16_t>(p.y, o + j, activate(nv[j >> 2][j & 3], p.act));
-        }
-      }
+    outputs(0);
+    for (int base = kDwThreads * kDwOut; base < nout; base += kDwThreads * kDwOut) {
+      zload(base);
+      outputs(base);
     }
     // all waves are done with the halo before the next tile overwrites it
     __syncthreads();
