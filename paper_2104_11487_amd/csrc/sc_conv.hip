@@ -159,37 +159,99 @@ __global__ void __launch_bounds__(kConvThreads) conv_bf16_kernel(ConvParams p) {
   if (p.zero_ctr && blockIdx.x == 0 && threadIdx.x == 0) *p.zero_ctr = 0u;  // next step's work list
   const int ntiles = (int)((total_rows + kRowsPerTile - 1) / kRowsPerTile);
   const uint16_t* xt = static_cast<const uint16_t*>(p.x_t);
-  const uint16_t* xp = static_cast<const uint16_t*>(p.x_prev);
+  const uint16_t* xp = static_cast<const uint16_t*>(p.no_prev ? p.x_t : p.x_prev);
   const bf16x8* wp = static_cast<const bf16x8*>(p.wpack);
+  // FAST (C % 32 == 0): the A fragment of a k-step is one 16-byte piece of
+  // each frame; the pieces and weight fragments of kChunkSteps k-steps are
+  // loaded together (clamped, unconditional loads masked after), so a chunk
+  // costs one memory round trip instead of one per k-step
+  constexpr int kChunkSteps = NTN <= 2 ? 8 : (NTN <= 4 ? 4 : 2);
 
   for (TileWalk tw(ntiles); tw.t < tw.end; tw.t += tw.step) {
     const long g = (long)tw.t * kRowsPerTile + wave * 16 + r16;
     const Site st = site_of_row(p, g, total_rows, bb);
     const int iy = st.oy * p.stride - p.pad, ix = st.ox * p.stride - p.pad;
+    // old z of the outputs this lane stores, loaded before the product
+    const int zrow_mine = st.ok ? (st.n * p.h_out + st.oy) * p.w_out + st.ox : -1;
+    int zrow[4];
+    float zold[4][NTN];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      zrow[v] = __shfl(zrow_mine, kq * 4 + v, 64);
+#pragma unroll
+      for (int i = 0; i < NTN; ++i) {
+        const int col = i * 16 + r16;
+        const bool ok = zrow[v] >= 0 && col < p.c_out && !p.reference;
+        zold[v][i] = p.z[ok ? (size_t)zrow[v] * p.c_out + col : 0];
+      }
+    }
     floatx4 acc[NTN];
 #pragma unroll
     for (int i = 0; i < NTN; ++i) acc[i] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
 
-    for (int ks = 0; ks < p.ksteps; ++ks) {
-      const bf16x8 a = gather_a_bf16<FAST>(p, xt, xp, st, iy, ix, ks, kq);
-      const bf16x8* wk = wp + (size_t)ks * NTN * 64 + lane;
+    if constexpr (FAST) {
+      const int cpt = p.c >> 5;  // k-steps per tap
+      for (int k0 = 0; k0 < p.ksteps; k0 += kChunkSteps) {
+        uint4 ra[kChunkSteps], rb[kChunkSteps];
+        bf16x8 wv[kChunkSteps][NTN];
+        bool in[kChunkSteps], pin[kChunkSteps];
 #pragma unroll
-      for (int i = 0; i < NTN; ++i)
-        acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, wk[i * 64], acc[i], 0, 0, 0);
+        for (int u = 0; u < kChunkSteps; ++u) {
+          const int ks = k0 + u;
+          const int tap = ks / cpt;
+          const int c0 = (ks - tap * cpt) * 32 + kq * 8;
+          const int kh = tap / p.k, kw = tap - kh * p.k;
+          const int y = iy + kh, x = ix + kw;
+          in[u] = st.ok && ks < p.ksteps && y >= 0 && y < p.h && x >= 0 && x < p.w;
+          const size_t off = in[u] ? ((size_t)(st.n * p.h + y) * p.w + x) * p.c + c0 : 0;
+          const long po = (in[u] && !p.no_prev) ? prev_off(p, st.n, y, x, c0) : -1;
+          pin[u] = po >= 0;
+          ra[u] = *reinterpret_cast<const uint4*>(xt + off);
+          rb[u] = *reinterpret_cast<const uint4*>(xp + (pin[u] ? (size_t)po : 0));
+          const bf16x8* wk = wp + (size_t)(ks < p.ksteps ? ks : 0) * NTN * 64 + lane;
+#pragma unroll
+          for (int i = 0; i < NTN; ++i) wv[u][i] = wk[i * 64];
+        }
+#pragma unroll
+        for (int u = 0; u < kChunkSteps; ++u) {
+          if (k0 + u >= p.ksteps) continue;  // wave-uniform (not a break: the loop stays unrolled)
+          const uint32_t wa[4] = {ra[u].x, ra[u].y, ra[u].z, ra[u].w};
+          const uint32_t wb[4] = {rb[u].x, rb[u].y, rb[u].z, rb[u].w};
+          u32x4 q;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float a0 = __uint_as_float(wa[e] << 16), a1 = __uint_as_float(wa[e] & 0xffff0000u);
+            const float b0 = pin[u] ? __uint_as_float(wb[e] << 16) : 0.0f;
+            const float b1 = pin[u] ? __uint_as_float(wb[e] & 0xffff0000u) : 0.0f;
+            const float r0 = in[u] ? __fsub_rn(a0, b0) : 0.0f, r1 = in[u] ? __fsub_rn(a1, b1) : 0.0f;
+            q[e] = f32_to_bf16(r0) | (f32_to_bf16(r1) << 16);
+          }
+          const bf16x8 a = __builtin_bit_cast(bf16x8, q);
+#pragma unroll
+          for (int i = 0; i < NTN; ++i)
+            acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, wv[u][i], acc[i], 0, 0, 0);
+        }
+      }
+    } else {
+      for (int ks = 0; ks < p.ksteps; ++ks) {
+        const bf16x8 a = gather_a_bf16<FAST>(p, xt, xp, st, iy, ix, ks, kq);
+        const bf16x8* wk = wp + (size_t)ks * NTN * 64 + lane;
+#pragma unroll
+        for (int i = 0; i < NTN; ++i)
+          acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, wk[i * 64], acc[i], 0, 0, 0);
+      }
     }
 
     // epilogue: lane holds D[4*(lane/16) + v][lane % 16] of each 16x16 tile
-    const int zrow_mine = st.ok ? (st.n * p.h_out + st.oy) * p.w_out + st.ox : -1;
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      const int zrow = __shfl(zrow_mine, kq * 4 + v, 64);
-      if (zrow < 0) continue;
+      if (zrow[v] < 0) continue;
 #pragma unroll
       for (int i = 0; i < NTN; ++i) {
         const int col = i * 16 + r16;
         if (col >= p.c_out) continue;
-        const size_t idx = (size_t)zrow * p.c_out + col;
-        const float nv = p.reference ? acc[i][v] : p.z[idx] + acc[i][v];
+        const size_t idx = (size_t)zrow[v] * p.c_out + col;
+        const float nv = p.reference ? acc[i][v] : zold[v][i] + acc[i][v];
         p.z[idx] = nv;
         if (p.act) store_y<uint16_t>(p.y, idx, activate(nv, p.act));
       }
@@ -462,6 +524,10 @@ conv_halo_kernel(ConvParams p, HaloParams hp) {
 
 template <int NTN>
 __global__ void __launch_bounds__(kConvThreads) conv_f32_kernel(ConvParams p) {
+  // k-steps whose operand (two frames) and weight loads are issued together:
+  // every load is unconditional (clamped to element 0 and masked after), so
+  // a chunk costs one memory round trip instead of one per k-step
+  constexpr int kChunkSteps = NTN <= 2 ? 16 : (NTN <= 4 ? 8 : 4);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, kq = lane >> 4;
   const int bb = p.block * p.block;
@@ -469,7 +535,7 @@ __global__ void __launch_bounds__(kConvThreads) conv_f32_kernel(ConvParams p) {
   if (p.zero_ctr && blockIdx.x == 0 && threadIdx.x == 0) *p.zero_ctr = 0u;  // next step's work list
   const int ntiles = (int)((total_rows + kRowsPerTile - 1) / kRowsPerTile);
   const float* xt = static_cast<const float*>(p.x_t);
-  const float* xp = static_cast<const float*>(p.x_prev);
+  const float* xp = static_cast<const float*>(p.no_prev ? p.x_t : p.x_prev);
   const float* wp = static_cast<const float*>(p.wpack);
   const int kk = p.k * p.k * p.c;
 
@@ -477,40 +543,64 @@ __global__ void __launch_bounds__(kConvThreads) conv_f32_kernel(ConvParams p) {
     const long g = (long)tw.t * kRowsPerTile + wave * 16 + r16;
     const Site st = site_of_row(p, g, total_rows, bb);
     const int iy = st.oy * p.stride - p.pad, ix = st.ox * p.stride - p.pad;
+    // old z of the outputs this lane stores (site of lane kq * 4 + v, column
+    // i * 16 + r16), loaded before the product
+    const int zrow_mine = st.ok ? (st.n * p.h_out + st.oy) * p.w_out + st.ox : -1;
+    int zrow[4];
+    float zold[4][NTN];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      zrow[v] = __shfl(zrow_mine, kq * 4 + v, 64);
+#pragma unroll
+      for (int i = 0; i < NTN; ++i) {
+        const int col = i * 16 + r16;
+        const bool ok = zrow[v] >= 0 && col < p.c_out && !p.reference;
+        zold[v][i] = p.z[ok ? (size_t)zrow[v] * p.c_out + col : 0];
+      }
+    }
     floatx4 acc[NTN];
 #pragma unroll
     for (int i = 0; i < NTN; ++i) acc[i] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
 
-    for (int ks = 0; ks < p.ksteps; ++ks) {
-      const int kidx = ks * 4 + kq;
-      float a = 0.0f;
-      if (st.ok && kidx < kk) {
+    for (int k0 = 0; k0 < p.ksteps; k0 += kChunkSteps) {
+      float av[kChunkSteps], pv[kChunkSteps], wv[kChunkSteps][NTN];
+      bool in[kChunkSteps], pin[kChunkSteps];
+#pragma unroll
+      for (int u = 0; u < kChunkSteps; ++u) {
+        const int ks = k0 + u;
+        const int kidx = ks * 4 + kq;
         const int tap = kidx / p.c, ci = kidx - tap * p.c;
         const int kh = tap / p.k, kw = tap - kh * p.k;
         const int y = iy + kh, x = ix + kw;
-        if (y >= 0 && y < p.h && x >= 0 && x < p.w) {
-          const size_t off = ((size_t)(st.n * p.h + y) * p.w + x) * p.c + ci;
-          const long po = p.no_prev ? -1 : prev_off(p, st.n, y, x, ci);
-          a = po < 0 ? xt[off] : __fsub_rn(xt[off], xp[po]);
+        in[u] = st.ok && ks < p.ksteps && kidx < kk && y >= 0 && y < p.h && x >= 0 && x < p.w;
+        const size_t off = in[u] ? ((size_t)(st.n * p.h + y) * p.w + x) * p.c + ci : 0;
+        const long po = (in[u] && !p.no_prev) ? prev_off(p, st.n, y, x, ci) : -1;
+        pin[u] = po >= 0;
+        av[u] = xt[off];
+        pv[u] = xp[pin[u] ? (size_t)po : 0];
+        const float* wk = wp + (size_t)(ks < p.ksteps ? ks : 0) * NTN * 64 + lane;
+#pragma unroll
+        for (int i = 0; i < NTN; ++i) wv[u][i] = wk[i * 64];
+      }
+#pragma unroll
+      for (int u = 0; u < kChunkSteps; ++u) {
+        if (k0 + u < p.ksteps) {  // wave-uniform (a guard, not a break: the loop stays unrolled)
+          const float a = !in[u] ? 0.0f : (pin[u] ? __fsub_rn(av[u], pv[u]) : av[u]);
+#pragma unroll
+          for (int i = 0; i < NTN; ++i) acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, wv[u][i], acc[i], 0, 0, 0);
         }
       }
-      const float* wk = wp + (size_t)ks * NTN * 64 + lane;
-#pragma unroll
-      for (int i = 0; i < NTN; ++i)
-        acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, wk[i * 64], acc[i], 0, 0, 0);
     }
 
-    const int zrow_mine = st.ok ? (st.n * p.h_out + st.oy) * p.w_out + st.ox : -1;
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      const int zrow = __shfl(zrow_mine, kq * 4 + v, 64);
-      if (zrow < 0) continue;
+      if (zrow[v] < 0) continue;
 #pragma unroll
       for (int i = 0; i < NTN; ++i) {
         const int col = i * 16 + r16;
         if (col >= p.c_out) continue;
-        const size_t idx = (size_t)zrow * p.c_out + col;
-        const float nv = p.reference ? acc[i][v] : p.z[idx] + acc[i][v];
+        const size_t idx = (size_t)zrow[v] * p.c_out + col;
+        const float nv = p.reference ? acc[i][v] : zold[v][i] + acc[i][v];
         p.z[idx] = nv;
         if (p.act) store_y<float>(p.y, idx, activate(nv, p.act));
       }
