@@ -237,7 +237,9 @@ int skipconv_get_desc(skipconv_t h, skipconv_desc* d);
  * convolution pipeline, 1 for the single-pass kernel (gate, local compaction
  * and MFMA product in one launch) with the weights staged in LDS, 2 for the
  * single-pass kernel whose waves hold their weight fragments in registers
- * (tiles of <= 8 x 8 sites, shapes it is built for). Host only. */
+ * (tiles of <= 8 x 8 sites, shapes it is built for), 3 for that kernel with
+ * the output channels of each tile split over 2, 4 or 8 workgroups (shapes
+ * built only for a share of the channels). Host only. */
 int skipconv_pipeline(skipconv_t h, int32_t* fused);
 
 /* Gate tiling of the split pipeline: *ts = output sites per side of one gate

@@ -119,11 +119,13 @@ struct Tile {
   float inv_ts, inv_blk, inv_hw;    // reciprocals for qdiv (computed on the host)
 };
 
-// The tile of this workgroup, from the table built at create time.
-__device__ __forceinline__ Tile make_tile(const FusedParams& p) {
+// The tile of this workgroup, from the table built at create time (with the
+// output channels split over nsplit workgroups, workgroups nsplit * i ..
+// nsplit * i + nsplit - 1 share tile i).
+__device__ __forceinline__ Tile make_tile(const FusedParams& p, int tile) {
   const GateParams& g = p.g;
   Tile T;
-  const uint32_t tc = p.tiles[blockIdx.x];
+  const uint32_t tc = p.tiles[tile];
   const int tx = (int)(tc & 1023u), ty = (int)((tc >> 10) & 1023u);
   T.n = (int)(tc >> 20);
   const int s = g.stride, k = g.k;
@@ -161,7 +163,7 @@ __global__ void fused_tiles_kernel(uint32_t* table, int grid, int tiles_y, int t
 // blocks; a tile whose input region meets none of them has every gate off and
 // stops before any load (norm gates only). Returns true when the tile stops.
 template <bool EMIT>
-__device__ bool chain_skip(const FusedParams& p, const Tile& T, uint8_t* emit_clr) {
+__device__ bool chain_skip(const FusedParams& p, const Tile& T, uint8_t* emit_clr, bool lead = true) {
   const GateParams& g = p.g;
   const int thh = (T.oh - 1) * g.stride + g.k, thw = (T.ow - 1) * g.stride + g.k;  // the tile's own halo
   const int y0 = max(T.iy0, 0), y1 = min(T.iy0 + thh, g.h), x0 = max(T.ix0, 0), x1 = min(T.ix0 + thw, g.w);
@@ -174,6 +176,7 @@ __device__ bool chain_skip(const FusedParams& p, const Tile& T, uint8_t* emit_cl
     any |= g.up_mask[((size_t)T.n * g.up_hb + by) * g.up_wb + bx] != 0;
   }
   if (__syncthreads_or(any)) return false;
+  if (!lead) return true;
   if (g.keep_stats)
     for (int q = threadIdx.x; q < T.oh * T.ow; q += kThreads) {
       const int ly = q / T.ow, lx = q - ly * T.ow;
@@ -397,7 +400,7 @@ __device__ __forceinline__ void copy_owned(const GateParams& g, const Tile& T) {
 // NaN on, block OR into blk_flag and tile_on (LDS). blk_flag and tile_on are
 // final only after the next barrier. All threads call it.
 __device__ void gate_sites(const FusedParams& p, const Tile& T, const ChunkMap& cm, float* a_halo,
-                           const float* part, uint32_t* blk_flag, uint32_t* tile_on) {
+                           const float* part, uint32_t* blk_flag, uint32_t* tile_on, bool lead = true) {
   const GateParams& g = p.g;
   const int s = g.stride, k = g.k, hw = T.hw;
   lds_barrier();
@@ -430,7 +433,7 @@ __device__ void gate_sites(const FusedParams& p, const Tile& T, const ChunkMap& 
       sv = a_halo[(ly * s + g.pad) * hw + lx * s + g.pad];
     }
     const bool on = g.reference || g.force_dense || ((double)sv * g.wnorm > g.thr) || (sv != sv);
-    if (g.keep_stats) {
+    if (g.keep_stats && lead) {
       const size_t o = ((size_t)T.n * g.h_out + T.oy0 + ly) * g.w_out + T.ox0 + lx;
       g.stat[o] = sv;
       g.site_mask[o] = on ? 1 : 0;
@@ -518,8 +521,15 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
   const GateParams& g = p.g;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, kq = lane >> 4;
-  const Tile T = make_tile(p);
-  if (CHAIN && g.up_mask && chain_skip<EMIT>(p, T, emit_clr)) return;
+  // output channels split over p.nsplit workgroups per tile: this one owns
+  // 16-column tiles n0 .. n0 + NT - 1; the lead (split 0) alone writes what
+  // every split would write alike (x_{t-1} copy, gate outputs, emitted-residual
+  // clears and the previous block flags it reads)
+  const int tile_i = p.nsplit > 1 ? (int)(blockIdx.x / p.nsplit) : (int)blockIdx.x;
+  const int n0 = ((int)blockIdx.x - tile_i * p.nsplit) * NT;
+  const bool lead = n0 == 0;
+  const Tile T = make_tile(p, tile_i);
+  if (CHAIN && g.up_mask && chain_skip<EMIT>(p, T, emit_clr, lead)) return;
   uint8_t* pbuf = lds + p.off_b;  // partial sums [kp][site][PROW]
   uint8_t* halo = lds + p.off_halo;
   float* a_halo = reinterpret_cast<float*>(lds + p.off_a);
@@ -539,11 +549,12 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
   const int nks = mma ? (kp + 1) * p.ksteps / KP - ks_lo : 0;
   bf16x8 bw[KPS][WN];
   {
-    const bf16x8* src = static_cast<const bf16x8*>(p.wpack) + ((size_t)ks_lo * NT + ng * WN) * 64 + lane;
+    const int ntn = p.ntiles_n;  // 16-column tiles of the packed weights
+    const bf16x8* src = static_cast<const bf16x8*>(p.wpack) + ((size_t)ks_lo * ntn + n0 + ng * WN) * 64 + lane;
 #pragma unroll
     for (int st = 0; st < KPS; ++st)
 #pragma unroll
-      for (int j = 0; j < WN; ++j) bw[st][j] = src[((size_t)(st < nks ? st : 0) * NT + j) * 64];
+      for (int j = 0; j < WN; ++j) bw[st][j] = src[((size_t)(st < nks ? st : 0) * ntn + j) * 64];
   }
   const HaloWalk hwk = make_walk<kThreads, true>(g, T, cm, threadIdx.x);
   HaloBatch hb;
@@ -554,14 +565,14 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
 #pragma unroll
   for (int h = 0; h < EP; ++h) {
     const int e = h * kThreads + threadIdx.x;
-    const int site = e / (4 * NT), col = (e - site * 4 * NT) * 4;
+    const int site = e / (4 * NT), col = (e - site * 4 * NT) * 4;  // column within this split
     const int ly = qdiv(site, T.inv_ts), lx = site - ly * g.ts;
-    const bool ok = ly < T.oh && lx < T.ow && col < p.c_out;
+    const bool ok = ly < T.oh && lx < T.ow && n0 * 16 + col < p.c_out;
     const int gs = (T.n * g.h_out + T.oy0 + ly) * g.w_out + T.ox0 + lx;
     esite[h] = ok ? gs : -1;
     eloc[h] = ok ? qdiv(ly, T.inv_blk) * T.tb_w + qdiv(lx, T.inv_blk) : 0;
     ecol[h] = col;
-    const size_t o = ok ? (size_t)gs * p.c_out + col : 0;
+    const size_t o = ok ? (size_t)gs * p.c_out + n0 * 16 + col : 0;
     zold[h] = *reinterpret_cast<const floatx4*>(p.z + o);
     yold[h] = uint2{0u, 0u};
     if (EMIT) yold[h] = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(p.y) + o);
@@ -611,14 +622,16 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
     settle(zold[h]);
     if (EMIT) settle(yold[h]);
   }
-  halo_keep(g, hb);  // the halo is one round (kItems rows per thread) for this kernel
-  copy_owned(g, T);
+  if (lead) {
+    halo_keep(g, hb);  // the halo is one round (kItems rows per thread) for this kernel
+    copy_owned(g, T);
+  }
 
   // 3. gate of every site, and 4. the product, with no barrier between them:
   // the product is computed whether or not the gate turns any block of the
   // tile on (it does not depend on the gate), so the gate's latency overlaps
   // it instead of preceding it; a tile found off then stores nothing.
-  gate_sites(p, T, cm, a_halo, part, blk_flag, &tile_on);
+  gate_sites(p, T, cm, a_halo, part, blk_flag, &tile_on, lead);
 
   // product over this wave's k-steps: the first KPS - 1 always run, the
   // last one when the wave has KPS (a wave-uniform branch); the tap and
@@ -662,9 +675,9 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
                                     ((ng * WN + j) * 16 + kq * 4) * 4) = acc[i][j];
   }
   lds_barrier();
-  gate_flags(p, T, blk_flag);
+  if (lead) gate_flags(p, T, blk_flag);
   if (!tile_on) {
-    if (EMIT) emit_clear(p, T.n, T.oy0, T.ox0, T.oh, T.ow, T.tb_w, blk_flag, emit_clr);
+    if (EMIT && lead) emit_clear(p, T.n, T.oy0, T.ox0, T.oh, T.ow, T.tb_w, blk_flag, emit_clr);
     return;
   }
 
@@ -682,9 +695,9 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
 #pragma unroll
       for (int c = 0; c < 4; ++c) u[c] = u[c] + v[c];
     }
-    store_piece<EMIT>(p, (size_t)esite[h] * p.c_out + ecol[h], u, zold[h], yold[h]);
+    store_piece<EMIT>(p, (size_t)esite[h] * p.c_out + n0 * 16 + ecol[h], u, zold[h], yold[h]);
   }
-  if (EMIT) emit_clear(p, T.n, T.oy0, T.ox0, T.oh, T.ow, T.tb_w, blk_flag, emit_clr);
+  if (EMIT && lead) emit_clear(p, T.n, T.oy0, T.ox0, T.oh, T.ow, T.tb_w, blk_flag, emit_clr);
 }
 
 // ---------------------------------------------------------------------------
@@ -708,7 +721,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
   const GateParams& g = p.g;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, kq = lane >> 4;
-  const Tile T = make_tile(p);
+  const Tile T = make_tile(p, blockIdx.x);
   const int n = T.n, oy0 = T.oy0, ox0 = T.ox0, oh = T.oh, ow = T.ow, hw = T.hw;
   const int s = g.stride, k = g.k;
   if (CHAIN && g.up_mask && chain_skip<EMIT>(p, T, emit_clr)) return;
@@ -995,6 +1008,7 @@ struct RbBuild {
 };
 constexpr RbBuild kRbBuilds[] = {
     {2, 2, 4, 2}, {2, 2, 4, 3}, {4, 2, 4, 3}, {4, 2, 4, 5}, {8, 2, 4, 9}, {12, 2, 4, 6},
+    {2, 2, 4, 5},  // a quarter of 128 output channels at K = 1152 (3 x 3, C_in = 128)
 };
 }  // namespace
 
@@ -1029,6 +1043,7 @@ int prepare_fused(const FusedParams& p) {
       case 4: return prepare_rb_t<4, 2, 4, 5>(p);
       case 5: return prepare_rb_t<8, 2, 4, 9>(p);
       case 6: return prepare_rb_t<12, 2, 4, 6>(p);
+      case 7: return prepare_rb_t<2, 2, 4, 5>(p);
       default: return 0;
     }
   }
@@ -1062,6 +1077,7 @@ hipError_t launch_fused(const FusedParams& p, int grid, hipStream_t st) {
       case 4: return launch_rb_t<4, 2, 4, 5>(p, grid, st);
       case 5: return launch_rb_t<8, 2, 4, 9>(p, grid, st);
       case 6: return launch_rb_t<12, 2, 4, 6>(p, grid, st);
+      case 7: return launch_rb_t<2, 2, 4, 5>(p, grid, st);
       default: return hipErrorInvalidValue;
     }
   }

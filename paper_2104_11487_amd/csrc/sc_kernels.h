@@ -126,6 +126,8 @@ struct FusedParams {
   int pstage;              // LDS floats per halo pixel of chunk sums: (c_in / 8) | 1
   int off_b, off_halo, off_a, off_part, lds_bytes;  // off_b: weights, or partial sums (rb)
   int rbk;                 // register-operand kernel: its build (fused_rb_kps), 0: LDS operand
+  int nsplit;              // register-operand kernel: workgroups per tile, each owning
+                           // ntiles_n / nsplit 16-column output tiles (1: no split)
   const uint32_t* tiles;   // per workgroup: its tile, tx | ty << 10 | n << 20 (XCD-aware order)
   float inv_ts, inv_blk, inv_hw, inv_chk;  // 1/ts, 1/block, 1/halo width, 1/(c_in / 8), rounded to fp32
   // residual emission for a chained successor (act must be set): r = y_new - y_old

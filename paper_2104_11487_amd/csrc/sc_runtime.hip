@@ -52,6 +52,7 @@ struct Geometry {
   sc::HaloParams dwp;
   bool fused;           // single-pass kernel instead of gate + compaction + conv
   int f_ts, f_tiles_y, f_tiles_x, f_grid, f_copy_in_halo;
+  int f_nsplit;         // workgroups per tile of the register-operand kernel (output channels split)
   int f_kc, f_nchunks, f_nbuf, f_mw, f_pstride, f_zero_pix, f_off_b, f_off_halo, f_off_a, f_lds;
   int f_rb;             // register-operand fused kernel: its build (0: LDS operand)
   int f_pstage, f_off_part;
@@ -320,10 +321,17 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
       int kc = G.ksteps, nbuf = 1;
       // tiles of <= 8 x 8 sites: register-operand kernel when instantiated for
       // the shape; LDS holds the partial sums of its k-parts instead of weights
-      const int rb = mw == 1 ? sc::fused_rb_kps(G.ntn, G.ksteps, hh, d->c_in / 8) : 0;
+      int rb = mw == 1 ? sc::fused_rb_kps(G.ntn, G.ksteps, hh, d->c_in / 8) : 0;
+      // no build for the whole width: the output channels split over 2, 4 or
+      // 8 workgroups per tile, each a build for its share (fewer k-steps per
+      // wave, so the weight fragments still fit in registers)
+      int nsplit = 1;
+      for (int sp = 2; mw == 1 && !rb && sp <= 8; sp *= 2)
+        if (G.ntn % sp == 0 && (rb = sc::fused_rb_kps(G.ntn / sp, G.ksteps, hh, d->c_in / 8)) != 0) nsplit = sp;
+      G.f_nsplit = nsplit;
       if (rb) {
         const long kparts = sc::fused_rb_kparts(rb);
-        b_bytes = kparts * 64 * ((long)G.ntn * 64 + 16);
+        b_bytes = kparts * 64 * ((long)(G.ntn / nsplit) * 64 + 16);
       } else if (whole + halo_b + a_b + part_b > kFusedLdsLimit) {
         kc = std::max(1, 16 / G.ntn);
         nbuf = 2;
@@ -479,6 +487,7 @@ sc::FusedParams fused_params(skipconv_layer* h, const void* x_t, bool ref) {
   fp.nbuf = g.f_nbuf;
   fp.mw = g.f_mw;
   fp.rbk = g.f_rb;
+  fp.nsplit = g.f_rb ? g.f_nsplit : 1;
   fp.tiles = reinterpret_cast<const uint32_t*>(h->ws + g.off_ftiles);
   fp.inv_ts = 1.0f / (float)g.f_ts;
   fp.inv_blk = 1.0f / (float)d.block;
@@ -716,7 +725,8 @@ int skipconv_create(const skipconv_desc* d, const void* weights, void* workspace
   // workgroup; it wins while the frame has few tiles (latency regime) and the
   // split pipeline wins on large frames, where each kernel streams at its own
   // roofline. Threshold: four tiles per CU.
-  if (h->g.fused && (h->g.f_grid > 4 * h->num_cu || sc::prepare_fused(fused_params(h, nullptr, true)) < 1))
+  if (h->g.fused && (h->g.f_grid * (h->g.f_rb ? h->g.f_nsplit : 1) > 4 * h->num_cu ||
+                     sc::prepare_fused(fused_params(h, nullptr, true)) < 1))
     h->g.fused = false;
   if (g.dw_halo) {
     const int occ = sc::depthwise_halo_occupancy(g.dwp, d->kernel, d->c_in);
@@ -814,7 +824,7 @@ int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t
   if (timing) e = hipEventRecord(h->ev[3 * h->timing_done], st);
   if (g.fused) {
     const sc::FusedParams fp = fused_params(h, x_t, ref);
-    if (e == hipSuccess) e = sc::launch_fused(fp, g.f_grid, st);
+    if (e == hipSuccess) e = sc::launch_fused(fp, g.f_grid * fp.nsplit, st);
     if (e != hipSuccess) return hip_fail(h, e, "fused launch");
     if (timing) e = hipEventRecord(h->ev[3 * h->timing_done + 1], st);
     h->list_valid = false;
@@ -959,7 +969,7 @@ int skipconv_step_chained(skipconv_t h, skipconv_t up, void* stream, const float
       fp.g.up_hb = up->g.hb;
       fp.g.up_wb = up->g.wb;
     }
-    const hipError_t e = sc::launch_fused(fp, g.f_grid, st);
+    const hipError_t e = sc::launch_fused(fp, g.f_grid * fp.nsplit, st);
     if (e != hipSuccess) return hip_fail(h, e, "chained fused launch");
     h->list_valid = false;
     h->ref_pending = false;
@@ -1062,7 +1072,7 @@ int skipconv_activation(skipconv_t h, const void** y) {
 int skipconv_pipeline(skipconv_t h, int32_t* fused) {
   if (!h) return SKIPCONV_E_STATE;
   if (!fused) return SKIPCONV_E_INVALID_ARG;
-  *fused = h->g.fused ? (h->g.f_rb ? 2 : 1) : 0;
+  *fused = h->g.fused ? (h->g.f_rb ? (h->g.f_nsplit > 1 ? 3 : 2) : 1) : 0;
   return SKIPCONV_OK;
 }
 

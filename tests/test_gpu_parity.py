@@ -413,7 +413,9 @@ def test_pipeline_selection():
     assert S.SkipConv(w, n=1, h=128, w=96, block=8).fused_variant == 2
     assert S.SkipConv(w, n=1, h=128, w=96, block=1).fused_variant == 2
     w128 = to_device(weight_storage(syn.he_weights(128, 128, 3, seed=1), "bf16"), "bf16")
-    assert S.SkipConv(w128, n=1, h=32, w=32, block=8).fused_variant == 1
+    # 128 -> 128 at K = 1152 has no whole-width register build: its output
+    # channels split over four workgroups per tile, each a register build
+    assert S.SkipConv(w128, n=1, h=32, w=32, block=8).fused_variant == 3
     assert S.SkipConv(w, n=1, h=64, w=64, block=16).fused_variant == 1
     # split gate tiles: 16 x 16 sites on large frames, 8 x 8 on small ones, 32 x 32
     # on request; 32, 64 and 128 channels add their chunk sums in lane groups,
@@ -610,8 +612,9 @@ def test_depthwise_halo(case):
 
 
 # One shape per build of the single-pass kernel whose waves hold their weight
-# fragments in registers (variant 2), and shapes that stage the weights in LDS
-# (variant 1), on frames whose sizes leave edge tiles, with a reset mid-stream:
+# fragments in registers (variant 2; variant 3: output channels split over
+# workgroups), and shapes that stage the weights in LDS (variant 1), on frames
+# whose sizes leave edge tiles, with a reset mid-stream:
 # (n, h, w, c_in, c_out, k, stride, block, variant)
 FUSED_SHAPES = [
     (1, 36, 44, 32, 32, 3, 1, 8, 2),
@@ -622,7 +625,8 @@ FUSED_SHAPES = [
     (1, 27, 21, 192, 192, 1, 1, 8, 2),
     (1, 40, 34, 32, 64, 3, 2, 1, 2),
     (1, 22, 26, 64, 64, 3, 1, 3, 2),
-    (1, 30, 26, 128, 128, 3, 1, 8, 1),
+    (1, 30, 26, 128, 128, 3, 1, 8, 3),
+    (2, 27, 21, 128, 128, 3, 1, 4, 3),
     (1, 40, 36, 64, 64, 3, 1, 16, 1),
 ]
 
