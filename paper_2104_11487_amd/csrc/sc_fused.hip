@@ -250,35 +250,36 @@ __device__ __forceinline__ HaloWalk make_walk(const GateParams& g, const Tile& T
   return W;
 }
 
-// One round of halo items: kItems items per thread (2-D walk: items
+// One round of halo items: KI items per thread (2-D walk: items
 // base + u of the thread's column; flat order: item base + u * NTHR + tid).
+template <int KI = kItems>
 struct HaloBatch {
-  uint4 vt[kItems], vp[kItems];
-  size_t off[kItems];
-  int px[kItems], ch[kItems];
-  bool in[kItems], own[kItems];
+  uint4 vt[KI], vp[KI];
+  size_t off[KI];
+  int px[KI], ch[KI];
+  bool in[KI], own[KI];
 };
 
-// Rounds of kItems items a workgroup's halo takes.
-template <int NTHR, bool TWOD>
+// Rounds of KI items a workgroup's halo takes.
+template <int NTHR, bool TWOD, int KI = kItems>
 __device__ __forceinline__ int halo_rounds(const Tile& T, const ChunkMap& cm, const HaloWalk& W) {
   const int per = (TWOD || W.twod) ? (T.hh + W.rg - 1) / W.rg : (cm.total + NTHR - 1) / NTHR;
-  return (per + kItems - 1) / kItems;
+  return (per + KI - 1) / KI;
 }
 
 // Issue the loads of round `rd`. Addresses are clamped in bounds so that every
 // load is issued (the wait counts stay static); out-of-frame items are zeroed
 // when used.
-template <bool CHAIN, int NTHR, bool TWOD>
+template <bool CHAIN, int NTHR, bool TWOD, int KI = kItems>
 __device__ __forceinline__ void halo_load(const GateParams& g, const Tile& T, const ChunkMap& cm,
-                                          const HaloWalk& W, int rd, int tid, HaloBatch& B) {
+                                          const HaloWalk& W, int rd, int tid, HaloBatch<KI>& B) {
   const uint16_t* xt = static_cast<const uint16_t*>(g.x_t);
   const uint16_t* xp = static_cast<const uint16_t*>(g.no_prev ? g.x_t : g.x_prev);
   const bool keep = g.x_keep != nullptr && g.copy_in_halo;
 #pragma unroll
-  for (int u = 0; u < kItems; ++u) {
+  for (int u = 0; u < KI; ++u) {
     if (TWOD || W.twod) {
-      const int j = rd * kItems + u;
+      const int j = rd * KI + u;
       const int hy = W.r0 + j * W.rg;
       const int y = T.iy0 + hy;
       const bool valid = j < W.rows && hy < T.hh;
@@ -288,7 +289,7 @@ __device__ __forceinline__ void halo_load(const GateParams& g, const Tile& T, co
       B.own[u] = B.in[u] && W.xown && y >= T.own_y0 && y < T.own_y1;
       B.off[u] = B.in[u] ? (size_t)(W.off0 + j * W.ostep) : 0;
     } else {
-      const int idx = rd * kItems * NTHR + u * NTHR + tid;
+      const int idx = rd * KI * NTHR + u * NTHR + tid;
       const int q = cm.lg >= 0 ? idx >> cm.lg : qdiv(idx, cm.inv);
       B.px[u] = idx < cm.total ? q : -1;
       B.ch[u] = idx - q * cm.nchk;
@@ -314,15 +315,15 @@ __device__ __forceinline__ void halo_load(const GateParams& g, const Tile& T, co
 // the pixel's chunk sums are added in ascending order by the group's first
 // lane through DPP row shifts (lane_sum), or parked in LDS for a later
 // combine. `wave` is the wave's index among the NTHR threads taking items.
-template <bool CHAIN, int NTHR, bool TWOD>
+template <bool CHAIN, int NTHR, bool TWOD, int KI = kItems>
 __device__ __forceinline__ void halo_use(const FusedParams& p, const Tile& T, const ChunkMap& cm,
-                                         const HaloWalk& W, int rd, int wave, HaloBatch& B, uint8_t* halo,
+                                         const HaloWalk& W, int rd, int wave, HaloBatch<KI>& B, uint8_t* halo,
                                          float* a_halo, float* part) {
   const GateParams& g = p.g;
 #pragma unroll
-  for (int u = 0; u < kItems; ++u) {
+  for (int u = 0; u < KI; ++u) {
     // wave-uniform: no item left for any lane of the wave
-    if ((TWOD || W.twod) ? (rd * kItems + u) * W.rg >= T.hh : (rd * kItems + u) * NTHR + wave * 64 >= cm.total)
+    if ((TWOD || W.twod) ? (rd * KI + u) * W.rg >= T.hh : (rd * KI + u) * NTHR + wave * 64 >= cm.total)
       break;
     if (!B.in[u]) B.vt[u] = uint4{0u, 0u, 0u, 0u};
     if (!B.in[u] || (!CHAIN && g.no_prev)) B.vp[u] = uint4{0u, 0u, 0u, 0u};
@@ -363,10 +364,11 @@ __device__ __forceinline__ void halo_use(const FusedParams& p, const Tile& T, co
 }
 
 // The owned pixels of a round's x_t go to the spare x_{t-1} slot.
-__device__ __forceinline__ void halo_keep(const GateParams& g, const HaloBatch& B) {
+template <int KI>
+__device__ __forceinline__ void halo_keep(const GateParams& g, const HaloBatch<KI>& B) {
   uint16_t* keep = static_cast<uint16_t*>(g.x_keep);
 #pragma unroll
-  for (int u = 0; u < kItems; ++u)
+  for (int u = 0; u < KI; ++u)
     if (B.own[u]) *reinterpret_cast<uint4*>(keep + B.off[u]) = B.vt[u];
 }
 
@@ -504,7 +506,7 @@ __device__ __forceinline__ void store_piece(const FusedParams& p, size_t o, cons
 // read pixel (tap) of the halo like row 0: their columns of the product are
 // discarded, and a site's outputs depend on its own column only.
 // MODE bit 0: emit the successor's residual; bit 1: chained input.
-template <int NT, int WN, int MT, int KPS, int MODE>
+template <int NT, int WN, int MT, int KPS, int KI, int MODE>
 __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
   constexpr bool EMIT = (MODE & 1) != 0;
   constexpr bool CHAIN = (MODE & 2) != 0;
@@ -557,8 +559,8 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
       for (int j = 0; j < WN; ++j) bw[st][j] = src[((size_t)(st < nks ? st : 0) * ntn + j) * 64];
   }
   const HaloWalk hwk = make_walk<kThreads, true>(g, T, cm, threadIdx.x);
-  HaloBatch hb;
-  halo_load<CHAIN, kThreads, true>(g, T, cm, hwk, 0, threadIdx.x, hb);
+  HaloBatch<KI> hb;
+  halo_load<CHAIN, kThreads, true, KI>(g, T, cm, hwk, 0, threadIdx.x, hb);
   int esite[EP], eloc[EP], ecol[EP];
   floatx4 zold[EP];
   uint2 yold[EP];
@@ -609,7 +611,7 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
   }
 
   // 2. halo use (and further rounds for large halos)
-  halo_use<CHAIN, kThreads, true>(p, T, cm, hwk, 0, wave, hb, halo, a_halo, part);
+  halo_use<CHAIN, kThreads, true, KI>(p, T, cm, hwk, 0, wave, hb, halo, a_halo, part);
   // weights and old z arrived with (or just after) the halo: settle them
   // before the x_t copy stores go out, so the product and the epilogue wait
   // for nothing
@@ -623,7 +625,7 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
     if (EMIT) settle(yold[h]);
   }
   if (lead) {
-    halo_keep(g, hb);  // the halo is one round (kItems rows per thread) for this kernel
+    halo_keep(g, hb);  // the halo is one round (KI rows per thread) for this kernel
     copy_owned(g, T);
   }
 
@@ -771,7 +773,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
     const HaloWalk hwk = make_walk<kHaloThreads, false>(g, T, cm, threadIdx.x);
     const int nrounds = halo_rounds<kHaloThreads, false>(T, cm, hwk);
     for (int rd = 0; rd < nrounds; ++rd) {
-      HaloBatch hb;
+      HaloBatch<> hb;
       halo_load<CHAIN, kHaloThreads, false>(g, T, cm, hwk, rd, threadIdx.x, hb);
       halo_use<CHAIN, kHaloThreads, false>(p, T, cm, hwk, rd, wave, hb, halo, a_halo, part);
       halo_keep(g, hb);
@@ -946,13 +948,13 @@ hipError_t launch_fused_t(const FusedParams& p, int grid, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <int NT, int WN, int MT, int KPS>
+template <int NT, int WN, int MT, int KPS, int KI>
 hipError_t launch_rb_t(const FusedParams& p, int grid, hipStream_t st) {
   switch ((p.emit ? 1 : 0) | (p.g.rin ? 2 : 0)) {
-    case 0: hipLaunchKernelGGL((fused_rb_kernel<NT, WN, MT, KPS, 0>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
-    case 1: hipLaunchKernelGGL((fused_rb_kernel<NT, WN, MT, KPS, 1>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
-    case 2: hipLaunchKernelGGL((fused_rb_kernel<NT, WN, MT, KPS, 2>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
-    default: hipLaunchKernelGGL((fused_rb_kernel<NT, WN, MT, KPS, 3>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+    case 0: hipLaunchKernelGGL((fused_rb_kernel<NT, WN, MT, KPS, KI, 0>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+    case 1: hipLaunchKernelGGL((fused_rb_kernel<NT, WN, MT, KPS, KI, 1>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+    case 2: hipLaunchKernelGGL((fused_rb_kernel<NT, WN, MT, KPS, KI, 2>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+    default: hipLaunchKernelGGL((fused_rb_kernel<NT, WN, MT, KPS, KI, 3>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
   }
   return hipGetLastError();
 }
@@ -980,12 +982,12 @@ int prepare_fused_t(const FusedParams& p) {
   return std::min(std::min(a, b), c);
 }
 
-template <int NT, int WN, int MT, int KPS>
+template <int NT, int WN, int MT, int KPS, int KI>
 int prepare_rb_t(const FusedParams& p) {
-  const int a = prepare_kernel(fused_rb_kernel<NT, WN, MT, KPS, 0>, p);
-  const int b = prepare_kernel(fused_rb_kernel<NT, WN, MT, KPS, 2>, p);
-  const int c = p.emit ? std::min(prepare_kernel(fused_rb_kernel<NT, WN, MT, KPS, 1>, p),
-                                  prepare_kernel(fused_rb_kernel<NT, WN, MT, KPS, 3>, p))
+  const int a = prepare_kernel(fused_rb_kernel<NT, WN, MT, KPS, KI, 0>, p);
+  const int b = prepare_kernel(fused_rb_kernel<NT, WN, MT, KPS, KI, 2>, p);
+  const int c = p.emit ? std::min(prepare_kernel(fused_rb_kernel<NT, WN, MT, KPS, KI, 1>, p),
+                                  prepare_kernel(fused_rb_kernel<NT, WN, MT, KPS, KI, 3>, p))
                        : a;
   return std::min(std::min(a, b), c);
 }
@@ -1004,21 +1006,23 @@ hipError_t launch_fused_tiles(uint32_t* table, int grid, int tiles_y, int tiles_
 // slower for 64 -> 64 layers: the weight traffic from L2 doubles).
 namespace {
 struct RbBuild {
-  int nt, wn, mt, kps;
+  int nt, wn, mt, kps, ki;  // ki: halo rows each thread loads (the halo is one round)
 };
 constexpr RbBuild kRbBuilds[] = {
-    {2, 2, 4, 2}, {2, 2, 4, 3}, {4, 2, 4, 3}, {4, 2, 4, 5}, {8, 2, 4, 9}, {12, 2, 4, 6},
-    {2, 2, 4, 5},  // a quarter of 128 output channels at K = 1152 (3 x 3, C_in = 128)
+    {2, 2, 4, 2, 4}, {2, 2, 4, 3, 4}, {4, 2, 4, 3, 4}, {4, 2, 4, 5, 4}, {8, 2, 4, 9, 4}, {12, 2, 4, 6, 4},
+    {2, 2, 4, 5, 4},  // a quarter of 128 output channels at K = 1152 (3 x 3, C_in = 128)
+    {8, 2, 4, 9, 6},  // stride 2, 64 -> 128: a 17 x 17 halo of 8 chunks a pixel
 };
 }  // namespace
 
 int fused_rb_kps(int ntiles_n, int ksteps, int halo_w, int chunks) {
-  // the kernel walks the halo in whole rows, in one round of kItems rows per thread
+  // the kernel walks the halo in whole rows, in one round of ki rows per thread
   const int rw = halo_w * chunks;
-  if (rw > kThreads || (halo_w + kThreads / rw - 1) / (kThreads / rw) > kItems) return 0;
+  if (rw > kThreads) return 0;
+  const int rows = (halo_w + kThreads / rw - 1) / (kThreads / rw);
   for (int i = 0; i < (int)(sizeof(kRbBuilds) / sizeof(kRbBuilds[0])); ++i) {
     const RbBuild& b = kRbBuilds[i];
-    if (b.nt != ntiles_n) continue;
+    if (b.nt != ntiles_n || rows > b.ki) continue;
     const int kp = kWaves / ((b.nt / b.wn) * (4 / b.mt));
     if ((ksteps + kp - 1) / kp <= b.kps && ksteps / kp >= b.kps - 1) return i + 1;  // build index + 1
   }
@@ -1037,13 +1041,14 @@ int fused_rb_kparts(int rb) {
 int prepare_fused(const FusedParams& p) {
   if (p.rbk) {
     switch (p.rbk) {
-      case 1: return prepare_rb_t<2, 2, 4, 2>(p);
-      case 2: return prepare_rb_t<2, 2, 4, 3>(p);
-      case 3: return prepare_rb_t<4, 2, 4, 3>(p);
-      case 4: return prepare_rb_t<4, 2, 4, 5>(p);
-      case 5: return prepare_rb_t<8, 2, 4, 9>(p);
-      case 6: return prepare_rb_t<12, 2, 4, 6>(p);
-      case 7: return prepare_rb_t<2, 2, 4, 5>(p);
+      case 1: return prepare_rb_t<2, 2, 4, 2, 4>(p);
+      case 2: return prepare_rb_t<2, 2, 4, 3, 4>(p);
+      case 3: return prepare_rb_t<4, 2, 4, 3, 4>(p);
+      case 4: return prepare_rb_t<4, 2, 4, 5, 4>(p);
+      case 5: return prepare_rb_t<8, 2, 4, 9, 4>(p);
+      case 6: return prepare_rb_t<12, 2, 4, 6, 4>(p);
+      case 7: return prepare_rb_t<2, 2, 4, 5, 4>(p);
+      case 8: return prepare_rb_t<8, 2, 4, 9, 6>(p);
       default: return 0;
     }
   }
@@ -1071,13 +1076,14 @@ int prepare_fused(const FusedParams& p) {
 hipError_t launch_fused(const FusedParams& p, int grid, hipStream_t st) {
   if (p.rbk) {
     switch (p.rbk) {
-      case 1: return launch_rb_t<2, 2, 4, 2>(p, grid, st);
-      case 2: return launch_rb_t<2, 2, 4, 3>(p, grid, st);
-      case 3: return launch_rb_t<4, 2, 4, 3>(p, grid, st);
-      case 4: return launch_rb_t<4, 2, 4, 5>(p, grid, st);
-      case 5: return launch_rb_t<8, 2, 4, 9>(p, grid, st);
-      case 6: return launch_rb_t<12, 2, 4, 6>(p, grid, st);
-      case 7: return launch_rb_t<2, 2, 4, 5>(p, grid, st);
+      case 1: return launch_rb_t<2, 2, 4, 2, 4>(p, grid, st);
+      case 2: return launch_rb_t<2, 2, 4, 3, 4>(p, grid, st);
+      case 3: return launch_rb_t<4, 2, 4, 3, 4>(p, grid, st);
+      case 4: return launch_rb_t<4, 2, 4, 5, 4>(p, grid, st);
+      case 5: return launch_rb_t<8, 2, 4, 9, 4>(p, grid, st);
+      case 6: return launch_rb_t<12, 2, 4, 6, 4>(p, grid, st);
+      case 7: return launch_rb_t<2, 2, 4, 5, 4>(p, grid, st);
+      case 8: return launch_rb_t<8, 2, 4, 9, 6>(p, grid, st);
       default: return hipErrorInvalidValue;
     }
   }

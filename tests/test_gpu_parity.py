@@ -625,6 +625,7 @@ FUSED_SHAPES = [
     (1, 27, 21, 192, 192, 1, 1, 8, 2),
     (1, 40, 34, 32, 64, 3, 2, 1, 2),
     (1, 22, 26, 64, 64, 3, 1, 3, 2),
+    (1, 36, 42, 64, 128, 3, 2, 8, 2),
     (1, 30, 26, 128, 128, 3, 1, 8, 3),
     (2, 27, 21, 128, 128, 3, 1, 4, 3),
     (1, 40, 36, 64, 64, 3, 1, 16, 1),
