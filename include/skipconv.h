@@ -245,8 +245,9 @@ int skipconv_pipeline(skipconv_t h, int32_t* fused);
 /* Gate tiling of the split pipeline: *ts = output sites per side of one gate
  * workgroup's tile (whole blocks, or a divisor of the block side), *lane_sum =
  * 1 when a pixel's 8-channel chunk sums are added in registers by a group of
- * 4, 8 or 16 lanes (norm gates with 32, 64 or 128 input channels), 0 when
- * they are staged in LDS. Host only. */
+ * 2, 4, 8 or 16 lanes (norm gates with 16, 32, 64 or 128 input channels) or a
+ * pixel's statistic is formed by one thread (fewer than 8 channels), 0 when
+ * the chunk sums are staged in LDS. Host only. */
 int skipconv_gate_tile(skipconv_t h, int32_t* ts, int32_t* lane_sum);
 
 /* Convolution kernel of the split pipeline: *kind = 0 gather (tiles of 64

@@ -135,7 +135,7 @@ __device__ void halo_partials(const GateParams& p, int n, int iy0, int ix0, int 
 // convolution reads next.
 constexpr int kNonTemporal = 2;
 
-// Halo of a norm gate with NC = 4, 8 or 16 chunks per pixel (bf16 or fp32
+// Halo of a norm gate with NC = 2, 4, 8 or 16 chunks per pixel (bf16 or fp32
 // frames). Items are taken in flat order (consecutive threads, consecutive
 // chunks), so a pixel's chunks sit in one aligned group of NC lanes: the
 // group's first lane adds the chunk sums in ascending order through DPP row
@@ -153,7 +153,7 @@ __device__ void halo_lane_sums(const GateParams& p, int n, int iy0, int ix0, int
                                int own_y1, int own_x0, int own_x1, float* a_halo) {
   constexpr int kWords = sizeof(T) == 2 ? 1 : 2;  // 16-byte words per chunk and frame
   constexpr int kItems = 8 / kWords;
-  constexpr int kLg = NC == 4 ? 2 : (NC == 8 ? 3 : 4);
+  constexpr int kLg = NC == 2 ? 1 : (NC == 4 ? 2 : (NC == 8 ? 3 : 4));
   const uint32_t img_bytes = (uint32_t)((size_t)p.h * p.w * p.c * sizeof(T));
   const size_t img = (size_t)n * p.h * p.w * p.c;
   const auto rt = frame_rsrc(static_cast<const T*>(p.x_t) + img, img_bytes);
@@ -219,6 +219,77 @@ __device__ void halo_lane_sums(const GateParams& p, int n, int iy0, int ix0, int
 #pragma unroll
       for (int wd = 0; wd < kWords; ++wd)
         __builtin_amdgcn_raw_buffer_store_b128(vt[u][wd], rk, koff[u] + 16 * wd, 0, kNonTemporal);
+  }
+}
+
+// Halo of a norm gate with fewer than 8 channels (one partial chunk per
+// pixel): one item per halo pixel, its c channels loaded element by element
+// through buffer resources (every load issued: channels past c and pixels
+// outside the frame read zeros at an out-of-range offset), the statistic
+// summed in channel order (the canonical single-chunk order) straight into
+// a[]; owned pixels copied element by element the same way (other items store
+// out of range).
+template <typename T>
+__device__ void halo_pixels(const GateParams& p, int n, int iy0, int ix0, int hh, int hw, int own_y0,
+                            int own_y1, int own_x0, int own_x1, float* a_halo) {
+  constexpr int kItems = 4;
+  constexpr int E = (int)sizeof(T);
+  const uint32_t img_bytes = (uint32_t)((size_t)p.h * p.w * p.c * E);
+  const size_t img = (size_t)n * p.h * p.w * p.c;
+  const auto rt = frame_rsrc(static_cast<const T*>(p.x_t) + img, img_bytes);
+  const auto rp = frame_rsrc(static_cast<const T*>(p.no_prev ? p.x_t : p.x_prev) + img, img_bytes);
+  const bool keep_on = p.x_keep != nullptr && p.copy_in_halo;
+  const auto rk = frame_rsrc(keep_on ? static_cast<T*>(p.x_keep) + img : nullptr, keep_on ? img_bytes : 0u);
+  const int total = hh * hw;
+  const float inv_hw = 1.0f / (float)hw;
+  for (int base = 0; base < total; base += kGateThreads * kItems) {
+    uint32_t vt[kItems][kChunk], vp[kItems][kChunk];
+    uint32_t off[kItems], po[kItems], ko[kItems];
+#pragma unroll
+    for (int u = 0; u < kItems; ++u) {
+      const int q = base + u * kGateThreads + threadIdx.x;
+      const int hy = qdiv(q, inv_hw), hx = q - hy * hw;
+      const int y = iy0 + hy, x = ix0 + hx;
+      const bool in = q < total && y >= 0 && y < p.h && x >= 0 && x < p.w;
+      const bool own = in && keep_on && y >= own_y0 && y < own_y1 && x >= own_x0 && x < own_x1;
+      const int yp = y - p.sy, xq = x - p.sx;
+      const bool pin = in && !p.no_prev && yp >= 0 && yp < p.h && xq >= 0 && xq < p.w;
+      off[u] = in ? (uint32_t)((y * p.w + x) * p.c * E) : kOutOfRange;
+      po[u] = pin ? (uint32_t)((yp * p.w + xq) * p.c * E) : kOutOfRange;
+      ko[u] = own ? off[u] : kOutOfRange;
+#pragma unroll
+      for (int j = 0; j < kChunk; ++j) {
+        const bool ch = j < p.c;
+        if constexpr (E == 2) {
+          vt[u][j] = __builtin_amdgcn_raw_buffer_load_b16(rt, ch ? off[u] + 2 * j : kOutOfRange, 0, 0);
+          vp[u][j] = __builtin_amdgcn_raw_buffer_load_b16(rp, ch ? po[u] + 2 * j : kOutOfRange, 0, 0);
+        } else {
+          vt[u][j] = __builtin_amdgcn_raw_buffer_load_b32(rt, ch ? off[u] + 4 * j : kOutOfRange, 0, 0);
+          vp[u][j] = __builtin_amdgcn_raw_buffer_load_b32(rp, ch ? po[u] + 4 * j : kOutOfRange, 0, 0);
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kItems; ++u) {
+      const int q = base + u * kGateThreads + threadIdx.x;
+      float sum = 0.0f;
+#pragma unroll
+      for (int j = 0; j < kChunk; ++j) {
+        if (j >= p.c) continue;
+        const float a = E == 2 ? __uint_as_float(vt[u][j] << 16) : __uint_as_float(vt[u][j]);
+        const float b = E == 2 ? __uint_as_float(vp[u][j] << 16) : __uint_as_float(vp[u][j]);
+        sum = add_rn(sum, term(__fsub_rn(a, b), p.norm_p));
+      }
+      if (q < total) a_halo[q] = sum;
+    }
+#pragma unroll
+    for (int u = 0; u < kItems; ++u)
+#pragma unroll
+      for (int j = 0; j < kChunk; ++j) {
+        const uint32_t o = (ko[u] == kOutOfRange || j >= p.c) ? kOutOfRange : ko[u] + E * j;
+        if constexpr (E == 2) __builtin_amdgcn_raw_buffer_store_b16((uint16_t)vt[u][j], rk, o, 0, 0);
+        else __builtin_amdgcn_raw_buffer_store_b32(vt[u][j], rk, o, 0, 0);
+      }
   }
 }
 
@@ -289,8 +360,9 @@ __device__ void learned_halo(const GateParams& p, int n, int iy0, int ix0, int h
   }
 }
 
-// KL: learned gate kernel size (0 = norm gate). NC > 0: bf16 norm gate with
-// NC chunks per pixel, chunk sums combined in lane groups (halo_lane_sums).
+// KL: learned gate kernel size (0 = norm gate). NC > 1: norm gate with NC
+// chunks per pixel, chunk sums combined in lane groups (halo_lane_sums); NC =
+// 1: norm gate with fewer than 8 channels, one item per pixel (halo_pixels).
 template <typename T, int VEC, int KL, int NC>
 __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
   extern __shared__ float lds[];
@@ -354,7 +426,9 @@ __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
     }
   }
 
-  if constexpr (NC > 0) {
+  if constexpr (NC == 1) {
+    halo_pixels<T>(p, n, iy0, ix0, hh, hw, own_y0, own_y1, own_x0, own_x1, a_halo);
+  } else if constexpr (NC > 0) {
     halo_lane_sums<T, NC>(p, n, iy0, ix0, hh, hw, own_y0, own_y1, own_x0, own_x1, a_halo);
   } else if constexpr (KL == 0) {
     halo_partials<T, VEC>(p, n, iy0, ix0, hh, hw, own_y0, own_y1, own_x0, own_x1, part);
@@ -559,16 +633,18 @@ static hipError_t launch_gate_t(const GateParams& p, int grid, size_t lds_bytes,
   const int nchk = (p.c + kChunk - 1) / kChunk;
   if (p.lane_sum) {
     // the host sized the LDS without chunk-sum staging: only these shapes
+    if (p.learned != 0 || (long)p.h * p.w * p.c * 4 >= (1L << 31)) return hipErrorInvalidValue;
     if constexpr (VEC == kChunk) {
-      if (p.learned != 0 || !(nchk == 4 || nchk == 8 || nchk == 16) || (long)p.h * p.w * p.c * 4 >= (1L << 31))
-        return hipErrorInvalidValue;
       if (nchk == 16) hipLaunchKernelGGL((gate_kernel<T, VEC, 0, 16>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p);
       else if (nchk == 8) hipLaunchKernelGGL((gate_kernel<T, VEC, 0, 8>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p);
-      else hipLaunchKernelGGL((gate_kernel<T, VEC, 0, 4>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p);
-      return hipGetLastError();
+      else if (nchk == 4) hipLaunchKernelGGL((gate_kernel<T, VEC, 0, 4>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p);
+      else if (nchk == 2) hipLaunchKernelGGL((gate_kernel<T, VEC, 0, 2>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p);
+      else return hipErrorInvalidValue;
     } else {
-      return hipErrorInvalidValue;
+      if (p.c >= kChunk) return hipErrorInvalidValue;
+      hipLaunchKernelGGL((gate_kernel<T, VEC, 0, 1>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p);
     }
+    return hipGetLastError();
   }
   switch (p.learned) {
     case 0: hipLaunchKernelGGL((gate_kernel<T, VEC, 0, 0>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p); break;

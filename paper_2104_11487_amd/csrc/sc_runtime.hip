@@ -147,12 +147,13 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
   const int nchk = (d->c_in + 7) / 8;
   G.stage_stride = nchk | 1;
   G.learned = d->gate == SKIPCONV_GATE_LEARNED ? k : 0;
-  // norm gates with 4, 8 or 16 chunks per pixel add a pixel's chunk sums in
-  // registers (lane groups), without per-chunk staging in LDS; the kernel
+  // norm gates with 2, 4, 8 or 16 chunks per pixel add a pixel's chunk sums
+  // in registers (lane groups), and those with fewer than 8 channels sum a
+  // pixel in one thread, without per-chunk staging in LDS; the kernel
   // addresses one image with 32-bit byte offsets (fp32 frames of chained
   // steps included)
-  const bool lane_sum = !G.learned && d->c_in % 8 == 0 && (nchk == 4 || nchk == 8 || nchk == 16) &&
-                        (long)d->h * d->w * d->c_in * 4 < (1L << 31);
+  const bool lane_sum = !G.learned && (long)d->h * d->w * d->c_in * 4 < (1L << 31) &&
+                        ((d->c_in % 8 == 0 && (nchk == 2 || nchk == 4 || nchk == 8 || nchk == 16)) || d->c_in < 8);
   G.lane_sum = lane_sum ? 1 : 0;
   // learned gate: phi is staged in LDS unless that alone would not fit
   const long phi_floats = (long)k * k * d->c_in;
