@@ -47,13 +47,13 @@ struct Site {
   bool ok;
 };
 
-__device__ __forceinline__ Site site_of_row(const ConvParams& p, long g, long total_rows,
+__device__ __forceinline__ Site site_of_row(const ConvParams& p, const WorkList& W, long g, long total_rows,
                                             int bb) {
   Site st{0, 0, 0, false};
   if (g < total_rows) {
     const int j = (int)(g / bb);
     const int within = (int)(g - (long)j * bb);
-    const uint32_t blk = p.list[j];
+    const uint32_t blk = p.list[work_pos(W, (uint32_t)j)];
     const int per_img = p.hb * p.wb;
     st.n = (int)(blk / per_img);
     const int rem = (int)(blk - (uint32_t)st.n * per_img);
@@ -155,8 +155,9 @@ __global__ void __launch_bounds__(kConvThreads) conv_bf16_kernel(ConvParams p) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, kq = lane >> 4;
   const int bb = p.block * p.block;
-  const long total_rows = (long)p.counters[kCtrCount] * bb;
-  if (p.zero_ctr && blockIdx.x == 0 && threadIdx.x == 0) *p.zero_ctr = 0u;  // next step's work list
+  const WorkList W = work_list(p.counters, p.seg_tiles, p.seg_cap);
+  const long total_rows = (long)W.total * bb;
+  if (p.zero_ctr && blockIdx.x == 0 && threadIdx.x < kSegs) p.zero_ctr[threadIdx.x * kSegStride] = 0u;  // next step's work list
   const int ntiles = (int)((total_rows + kRowsPerTile - 1) / kRowsPerTile);
   const uint16_t* xt = static_cast<const uint16_t*>(p.x_t);
   const uint16_t* xp = static_cast<const uint16_t*>(p.no_prev ? p.x_t : p.x_prev);
@@ -169,7 +170,7 @@ __global__ void __launch_bounds__(kConvThreads) conv_bf16_kernel(ConvParams p) {
 
   for (TileWalk tw(ntiles); tw.t < tw.end; tw.t += tw.step) {
     const long g = (long)tw.t * kRowsPerTile + wave * 16 + r16;
-    const Site st = site_of_row(p, g, total_rows, bb);
+    const Site st = site_of_row(p, W, g, total_rows, bb);
     const int iy = st.oy * p.stride - p.pad, ix = st.ox * p.stride - p.pad;
     // old z of the outputs this lane stores, loaded before the product
     const int zrow_mine = st.ok ? (st.n * p.h_out + st.oy) * p.w_out + st.ox : -1;
@@ -290,8 +291,9 @@ conv_halo_kernel(ConvParams p, HaloParams hp) {
   const int b = p.block, s = p.stride, k = p.k, c = p.c;
   const int lb = __ffs(b) - 1;
   const int tpb = hp.tiles_per_block;
-  const int ntiles = (int)p.counters[kCtrCount] * tpb;
-  if (p.zero_ctr && blockIdx.x == 0 && threadIdx.x == 0) *p.zero_ctr = 0u;  // next step's work list
+  const WorkList W = work_list(p.counters, p.seg_tiles, p.seg_cap);
+  const int ntiles = (int)W.total * tpb;
+  if (p.zero_ctr && blockIdx.x == 0 && threadIdx.x < kSegs) p.zero_ctr[threadIdx.x * kSegStride] = 0u;  // next step's work list
   const uint16_t* xt = static_cast<const uint16_t*>(p.x_t);
   const uint16_t* xp = static_cast<const uint16_t*>(p.x_prev);
   // packed weights through a buffer resource: lane offset in a VGPR, the
@@ -327,7 +329,7 @@ conv_halo_kernel(ConvParams p, HaloParams hp) {
   auto decode = [&](int t) {
     HTile T;
     const int j0 = t / tpb, band = t - j0 * tpb;
-    const uint32_t blk = list[j0];
+    const uint32_t blk = list[work_pos(W, (uint32_t)j0)];
     const int per_img = p.hb * p.wb;
     T.n = (int)(blk / per_img);
     const int rem = (int)(blk - (uint32_t)T.n * per_img);
@@ -531,8 +533,9 @@ __global__ void __launch_bounds__(kConvThreads) conv_f32_kernel(ConvParams p) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, kq = lane >> 4;
   const int bb = p.block * p.block;
-  const long total_rows = (long)p.counters[kCtrCount] * bb;
-  if (p.zero_ctr && blockIdx.x == 0 && threadIdx.x == 0) *p.zero_ctr = 0u;  // next step's work list
+  const WorkList W = work_list(p.counters, p.seg_tiles, p.seg_cap);
+  const long total_rows = (long)W.total * bb;
+  if (p.zero_ctr && blockIdx.x == 0 && threadIdx.x < kSegs) p.zero_ctr[threadIdx.x * kSegStride] = 0u;  // next step's work list
   const int ntiles = (int)((total_rows + kRowsPerTile - 1) / kRowsPerTile);
   const float* xt = static_cast<const float*>(p.x_t);
   const float* xp = static_cast<const float*>(p.no_prev ? p.x_t : p.x_prev);
@@ -541,7 +544,7 @@ __global__ void __launch_bounds__(kConvThreads) conv_f32_kernel(ConvParams p) {
 
   for (TileWalk tw(ntiles); tw.t < tw.end; tw.t += tw.step) {
     const long g = (long)tw.t * kRowsPerTile + wave * 16 + r16;
-    const Site st = site_of_row(p, g, total_rows, bb);
+    const Site st = site_of_row(p, W, g, total_rows, bb);
     const int iy = st.oy * p.stride - p.pad, ix = st.ox * p.stride - p.pad;
     // old z of the outputs this lane stores (site of lane kq * 4 + v, column
     // i * 16 + r16), loaded before the product
@@ -613,8 +616,9 @@ __global__ void __launch_bounds__(kConvThreads) conv_f32_kernel(ConvParams p) {
 template <typename T, int VEC>
 __global__ void __launch_bounds__(kConvThreads) depthwise_kernel(ConvParams p) {
   const int bb = p.block * p.block;
-  const long total_rows = (long)p.counters[kCtrCount] * bb;
-  if (p.zero_ctr && blockIdx.x == 0 && threadIdx.x == 0) *p.zero_ctr = 0u;  // next step's work list
+  const WorkList W = work_list(p.counters, p.seg_tiles, p.seg_cap);
+  const long total_rows = (long)W.total * bb;
+  if (p.zero_ctr && blockIdx.x == 0 && threadIdx.x < kSegs) p.zero_ctr[threadIdx.x * kSegStride] = 0u;  // next step's work list
   const int ntiles = (int)((total_rows + kRowsPerTile - 1) / kRowsPerTile);
   const T* xt = static_cast<const T*>(p.x_t);
   const T* xp = static_cast<const T*>(p.x_prev);
@@ -626,7 +630,7 @@ __global__ void __launch_bounds__(kConvThreads) depthwise_kernel(ConvParams p) {
     for (int item = threadIdx.x; item < kRowsPerTile * nchunk; item += kConvThreads) {
       const int row = item / nchunk;
       const int c0 = (item - row * nchunk) * VEC;
-      const Site st = site_of_row(p, (long)tw.t * kRowsPerTile + row, total_rows, bb);
+      const Site st = site_of_row(p, W, (long)tw.t * kRowsPerTile + row, total_rows, bb);
       if (!st.ok) continue;
       const int iy = st.oy * p.stride - p.pad, ix = st.ox * p.stride - p.pad;
       float acc[VEC];
@@ -695,8 +699,9 @@ __global__ void __launch_bounds__(kDwThreads) depthwise_halo_kernel(ConvParams p
   const int b = p.block, s = p.stride, k = p.k, c = p.c;
   const int nchunk = c >> 3;
   const int tpb = hp.tiles_per_block;
-  const int ntiles = (int)p.counters[kCtrCount] * tpb;
-  if (p.zero_ctr && blockIdx.x == 0 && threadIdx.x == 0) *p.zero_ctr = 0u;  // next step's work list
+  const WorkList W = work_list(p.counters, p.seg_tiles, p.seg_cap);
+  const int ntiles = (int)W.total * tpb;
+  if (p.zero_ctr && blockIdx.x == 0 && threadIdx.x < kSegs) p.zero_ctr[threadIdx.x * kSegStride] = 0u;  // next step's work list
   const uint16_t* xt = static_cast<const uint16_t*>(p.x_t);
   const uint16_t* xp = static_cast<const uint16_t*>(p.x_prev);
   const size_t ximg = (size_t)p.h * p.w * c;
@@ -727,7 +732,7 @@ __global__ void __launch_bounds__(kDwThreads) depthwise_halo_kernel(ConvParams p
 
   for (TileWalk tw(ntiles); tw.t < tw.end; tw.t += tw.step) {
     const int j0 = tw.t / tpb, band = tw.t - j0 * tpb;
-    const uint32_t blk = list[j0];
+    const uint32_t blk = list[work_pos(W, (uint32_t)j0)];
     const int per_img = p.hb * p.wb;
     const int n = (int)(blk / per_img);
     const int rem = (int)(blk - (uint32_t)n * per_img);

@@ -541,7 +541,11 @@ __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
     if (i == 0) {
       uint32_t tot = 0;
       for (int w = 0; w < kGateThreads / 64; ++w) tot += wave_cnt[w];
-      wl_base = tot ? atomicAdd(p.wctr, tot) : 0u;
+      // segment of this workgroup's XCD (xcd_tile hands XCD b % 8 a
+      // contiguous tile range starting at tile `first`)
+      const int x = blockIdx.x & 7, per = gridDim.x >> 3, rem = gridDim.x & 7;
+      const uint32_t first = (uint32_t)(x * per + min(x, rem));
+      wl_base = tot ? first * (uint32_t)p.seg_cap + atomicAdd(p.wctr + x * kSegStride, tot) : 0u;
     }
     __syncthreads();
     if (act) {

@@ -9,8 +9,13 @@ namespace sc {
 // counters[] slots in the workspace
 constexpr int kCtrCount = 0;  // active blocks of the last gate pass
 constexpr int kCtrSpare = 1;
-constexpr int kCtrWork = 4;   // kCtrWork + 0/1: counts of the two alternating work lists
 constexpr int kNumCounters = 16;
+// The gate appends active blocks to kSegs work-list segments, one per XCD's
+// contiguous range of gate tiles, each with its own counter kSegStride
+// uint32 apart (one 128-byte line each): appends to one counter serialise,
+// so spreading them over eight lines removes most of that wait.
+constexpr int kSegs = 8;
+constexpr int kSegStride = 32;
 
 constexpr int kMaxTileBlocks = 256;  // blocks per gate tile: (ts / b)^2 <= 256
 
@@ -52,7 +57,8 @@ struct GateParams {
   // unordered work list of the convolution (blocks appended per tile), its
   // count (zero on entry); NULL when the ordered compaction builds the list
   uint32_t* wlist;
-  uint32_t* wctr;
+  uint32_t* wctr;               // kSegs counters, kSegStride apart
+  int seg_cap;                  // work-list entries reserved per gate tile
 };
 
 // Sparse convolution over the active sites (dense groups = 1).
@@ -72,8 +78,52 @@ struct ConvParams {
   int no_prev;                  // x_{t-1} taken as 0 (reference frames; residual inputs)
   int act;                      // 0 none, 1 identity, 2 relu
   int sy, sx;                   // translation of the content since x_{t-1} (input pixels; 0 = none)
-  uint32_t* zero_ctr;           // a work-list counter to clear for the next step (or NULL)
+  uint32_t* zero_ctr;           // work-list counters (kSegs, kSegStride apart) to clear for the next step, or NULL
+  int seg_tiles, seg_cap;       // segmented work list: gate tiles and entries per tile; 0: plain list
 };
+
+// Work list of a convolution: a plain list with its count at
+// counters[kCtrCount], or the gate's kSegs segments, segment x holding the
+// blocks of gate tiles first(x) .. first(x + 1) - 1 (the XCD-contiguous tile
+// ranges of the gate launch) from entry first(x) * seg_cap on, its count at
+// counters[x * kSegStride]. Entries are the linear block indices.
+struct WorkList {
+  uint32_t total;
+  uint32_t pre[kSegs + 1];  // segmented: entries before segment x
+  uint32_t base[kSegs];     // segmented: first list entry of segment x
+  bool seg;
+};
+
+template <typename C>
+__device__ __forceinline__ WorkList work_list(const C* counters, int seg_tiles, int seg_cap) {
+  WorkList W;
+  W.seg = seg_tiles > 0;
+  if (!W.seg) {
+    W.total = counters[kCtrCount];
+    return W;
+  }
+  const int per = seg_tiles >> 3, rem = seg_tiles & 7;
+  uint32_t run = 0;
+#pragma unroll
+  for (int x = 0; x < kSegs; ++x) {
+    W.pre[x] = run;
+    W.base[x] = (uint32_t)((x * per + (x < rem ? x : rem)) * seg_cap);
+    run += counters[x * kSegStride];
+  }
+  W.pre[kSegs] = run;
+  W.total = run;
+  return W;
+}
+
+// List position of work item j (j < W.total).
+__device__ __forceinline__ uint32_t work_pos(const WorkList& W, uint32_t j) {
+  if (!W.seg) return j;
+  uint32_t pos = 0;
+#pragma unroll
+  for (int x = 0; x < kSegs; ++x)
+    if (j >= W.pre[x] && j < W.pre[x + 1]) pos = W.base[x] + (j - W.pre[x]);
+  return pos;
+}
 
 // Element offset of x_{t-1} under the step's translation at input pixel
 // (n, y, x), channel ch: the translated previous frame holds x_{t-1}[y - sy,
@@ -179,10 +229,10 @@ hipError_t launch_emit(const uint8_t* block_mask, uint8_t* prev_mask, int nb, co
 // active list split into translated-recurrence blocks and exposed blocks.
 hipError_t launch_translate_state(const float* z_src, float* z_dst, void* y, int n, int h_out, int w_out,
                                   int c_out, int dyo, int dxo, int act, int dtype, hipStream_t st);
-hipError_t launch_split_list(const uint32_t* list, const uint32_t* counters, uint32_t* list_a,
-                             uint32_t* counters_a, uint32_t* list_b, uint32_t* counters_b, int hb, int wb,
-                             int block, int h_out, int w_out, int h, int w, int k, int stride, int pad, int sy,
-                             int sx, hipStream_t st);
+hipError_t launch_split_list(const uint32_t* list, const uint32_t* counters, int seg_tiles, int seg_cap,
+                             uint32_t* list_a, uint32_t* counters_a, uint32_t* list_b, uint32_t* counters_b,
+                             int hb, int wb, int block, int h_out, int w_out, int h, int w, int k, int stride,
+                             int pad, int sy, int sx, hipStream_t st);
 
 hipError_t launch_fill_u32(uint32_t* p, int n, uint32_t v, hipStream_t st);
 

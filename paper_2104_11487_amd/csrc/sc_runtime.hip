@@ -39,6 +39,7 @@ size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 struct Geometry {
   int pad, h_out, w_out, hb, wb, nb;
   int ts, tiles_y, tiles_x, gate_grid, split_blocks;
+  int seg_cap;          // work-list entries per gate tile (blocks of a tile); 0: ordered compaction
   int lane_sum;  // gate chunk sums combined in lane groups (no LDS staging)
   int hh_max, hw_max, halo_floats, stage_stride, rows_per_batch;
   size_t gate_lds;
@@ -59,7 +60,7 @@ struct Geometry {
   int vec;              // gate load width (elements)
   size_t elem;
   size_t off_wpack, off_slot0, off_slot1, off_z, off_y, off_bmask, off_tflag, off_list, off_ctr,
-      off_stat, off_smask, off_phi, off_r32, off_rb, off_prev, off_z2, off_list_a, off_list_b, off_wlist,
+      off_stat, off_smask, off_phi, off_r32, off_rb, off_prev, off_z2, off_list_a, off_list_b, off_wlist, off_wctr,
       off_ftiles, total;
   int learned;          // learned gate: its kernel size (the layer's k), else 0
   bool phi_in_lds;      // learned gate: phi staged in LDS (else read through the caches)
@@ -376,8 +377,12 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
   G.off_bmask = off; off = align_up(off + (size_t)nb + 16);  // zero padding to whole 16-byte words
   G.off_tflag = off; off = align_up(off + (size_t)G.gate_grid);
   G.off_list = off; off = align_up(off + (size_t)nb * 4);
-  G.off_wlist = off; off = align_up(off + (size_t)nb * 4);  // unordered work list of the split pipeline
+  // unordered work list of the split pipeline: seg_cap entries per gate tile
+  // (its blocks), in kSegs segments with their counters in two alternating slots
+  G.seg_cap = G.split_blocks ? 0 : (G.ts / b) * (G.ts / b);
+  G.off_wlist = off; off = align_up(off + (size_t)std::max<long>(nb, (long)G.gate_grid * G.seg_cap) * 4);
   G.off_ctr = off; off = align_up(off + sc::kNumCounters * 4);
+  G.off_wctr = off; off = align_up(off + 2 * sc::kSegs * sc::kSegStride * 4);
   G.off_ftiles = off;
   if (G.fused) off = align_up(off + (size_t)G.f_grid * 4);  // tile table of the fused kernel
   G.off_stat = off;
@@ -449,11 +454,13 @@ struct skipconv_layer {
   uint8_t* prev_mask() { return reinterpret_cast<uint8_t*>(ws + g.off_prev); }
   bool phi_set = false;      // learned gate: skipconv_set_gate_weights was called
   // split pipeline work list: the gate appends active blocks (unordered) and
-  // counts them in counter kCtrWork + wslot; the convolution clears the other
-  // counter for the next step. wclean: that counter is known to be zero.
+  // counts them in the kSegs segment counters of slot wslot; the convolution
+  // clears the other slot's counters for the next step. wclean: a slot's
+  // counters are known to be zero.
   int wslot = 0;
   bool wclean[2] = {true, true};
   uint32_t* wlist() { return reinterpret_cast<uint32_t*>(ws + g.off_wlist); }
+  uint32_t* wctr() { return reinterpret_cast<uint32_t*>(ws + g.off_wctr); }
   float gate_bias = 0.0f;
 };
 
@@ -596,22 +603,25 @@ hipError_t launch_compaction(skipconv_layer* h, hipStream_t st) {
 // the gate kernel appends to, with no compaction launch.
 struct StepList {
   const uint32_t* list;
-  uint32_t* counters;  // counters[kCtrCount] = number of blocks in `list`
-  uint32_t* zero;      // counter the convolution clears for the next step
+  uint32_t* counters;  // counters[kCtrCount] = number of blocks in `list`, or kSegs segment counters
+  uint32_t* zero;      // counters the convolution clears for the next step
+  int seg_tiles, seg_cap;  // segmented work list (0: plain)
 };
 
 hipError_t begin_list(skipconv_layer* h, sc::GateParams& gp, hipStream_t st, StepList* out) {
   if (h->g.split_blocks) {
-    *out = StepList{h->list(), h->ctr(), nullptr};
+    *out = StepList{h->list(), h->ctr(), nullptr, 0, 0};
     return hipSuccess;
   }
   const int slot = h->wslot;
-  uint32_t* c = h->ctr() + sc::kCtrWork + slot;
+  constexpr int kSlot = sc::kSegs * sc::kSegStride;
+  uint32_t* c = h->wctr() + slot * kSlot;
   hipError_t e = hipSuccess;
-  if (!h->wclean[slot]) e = sc::launch_fill_u32(c, 1, 0u, st);
+  if (!h->wclean[slot]) e = sc::launch_fill_u32(c, kSlot, 0u, st);
   gp.wlist = h->wlist();
   gp.wctr = c;
-  *out = StepList{h->wlist(), c, h->ctr() + sc::kCtrWork + (slot ^ 1)};
+  gp.seg_cap = h->g.seg_cap;
+  *out = StepList{h->wlist(), c, h->wctr() + (slot ^ 1) * kSlot, h->g.gate_grid, h->g.seg_cap};
   return e;
 }
 
@@ -762,6 +772,7 @@ int skipconv_create(const skipconv_desc* d, const void* weights, void* workspace
     h->owns_ws = true;
   }
   e = hipMemsetAsync(h->ctr(), 0, sc::kNumCounters * 4, st);
+  if (e == hipSuccess) e = hipMemsetAsync(h->wctr(), 0, 2 * sc::kSegs * sc::kSegStride * 4, st);
   if (e == hipSuccess) e = hipMemsetAsync(h->bmask(), 0, g.off_list - g.off_bmask, st);
   if (e == hipSuccess) e = hipMemsetAsync(h->list(), 0, (size_t)g.nb * 4, st);
   if (e == hipSuccess && d->act_out != SKIPCONV_ACT_NONE)
@@ -839,6 +850,8 @@ int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t
     cp.list = sl.list;
     cp.counters = sl.counters;
     cp.zero_ctr = sl.zero;
+    cp.seg_tiles = sl.seg_tiles;
+    cp.seg_cap = sl.seg_cap;
     if (e == hipSuccess) {
       if (g.depthwise)
         e = (g.dw_halo ? sc::launch_depthwise_halo(cp, g.dwp, conv_grid(h), st) : sc::launch_depthwise(cp, d.dtype, conv_grid(h), st));
@@ -902,7 +915,8 @@ int skipconv_step_translated(skipconv_t h, const void* x_t, int32_t dy, int32_t 
   uint32_t* list_a = reinterpret_cast<uint32_t*>(h->ws + g.off_list_a);
   uint32_t* list_b = reinterpret_cast<uint32_t*>(h->ws + g.off_list_b);
   if (e == hipSuccess)
-    e = sc::launch_split_list(sl.list, sl.counters, list_a, ctr + 2, list_b, ctr + 3, g.hb, g.wb, d.block, g.h_out,
+    e = sc::launch_split_list(sl.list, sl.counters, sl.seg_tiles, sl.seg_cap, list_a, ctr + 2, list_b, ctr + 3, g.hb,
+                              g.wb, d.block, g.h_out,
                               g.w_out, d.h, d.w, d.kernel, d.stride, g.pad, dy, dx, st);
   if (e != hipSuccess) return hip_fail(h, e, "translated gate launch");
   sc::ConvParams cp{};
@@ -1004,6 +1018,8 @@ int skipconv_step_chained(skipconv_t h, skipconv_t up, void* stream, const float
   cp.list = sl.list;
   cp.counters = sl.counters;
   cp.zero_ctr = sl.zero;
+  cp.seg_tiles = sl.seg_tiles;
+  cp.seg_cap = sl.seg_cap;
   cp.n = d.n; cp.h = d.h; cp.w = d.w; cp.c = d.c_in; cp.c_out = d.c_out;
   cp.h_out = g.h_out; cp.w_out = g.w_out; cp.k = d.kernel; cp.stride = d.stride; cp.pad = g.pad;
   cp.block = d.block; cp.hb = g.hb; cp.wb = g.wb;

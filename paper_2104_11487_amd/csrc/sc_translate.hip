@@ -51,15 +51,16 @@ translate_state_kernel(const float* z_src, float* z_dst, void* y, int n, int h_o
 // One workgroup: list[0..count) -> list_a (translated recurrence) and list_b
 // (exposed blocks); counts at counters_a[kCtrCount], counters_b[kCtrCount].
 __global__ void __launch_bounds__(1024)
-split_list_kernel(const uint32_t* list, const uint32_t* counters, uint32_t* list_a, uint32_t* counters_a,
-                  uint32_t* list_b, uint32_t* counters_b, int hb, int wb, int block, int h_out, int w_out,
-                  int h, int w, int k, int stride, int pad, int sy, int sx) {
+split_list_kernel(const uint32_t* list, const uint32_t* counters, int seg_tiles, int seg_cap, uint32_t* list_a,
+                  uint32_t* counters_a, uint32_t* list_b, uint32_t* counters_b, int hb, int wb, int block,
+                  int h_out, int w_out, int h, int w, int k, int stride, int pad, int sy, int sx) {
   __shared__ uint32_t na, nb_;
   if (threadIdx.x == 0) na = nb_ = 0;
   __syncthreads();
-  const uint32_t count = counters[kCtrCount];
+  const WorkList W = work_list(counters, seg_tiles, seg_cap);
+  const uint32_t count = W.total;
   for (uint32_t i = threadIdx.x; i < count; i += blockDim.x) {
-    const uint32_t blk = list[i];
+    const uint32_t blk = list[work_pos(W, i)];
     const int rem = (int)(blk % (uint32_t)(hb * wb));
     const int bi = rem / wb, bj = rem - bi * wb;
     bool ex = false;
@@ -101,12 +102,12 @@ hipError_t launch_translate_state(const float* z_src, float* z_dst, void* y, int
   return hipGetLastError();
 }
 
-hipError_t launch_split_list(const uint32_t* list, const uint32_t* counters, uint32_t* list_a,
-                             uint32_t* counters_a, uint32_t* list_b, uint32_t* counters_b, int hb, int wb,
-                             int block, int h_out, int w_out, int h, int w, int k, int stride, int pad, int sy,
-                             int sx, hipStream_t st) {
-  hipLaunchKernelGGL(split_list_kernel, dim3(1), dim3(1024), 0, st, list, counters, list_a, counters_a, list_b,
-                     counters_b, hb, wb, block, h_out, w_out, h, w, k, stride, pad, sy, sx);
+hipError_t launch_split_list(const uint32_t* list, const uint32_t* counters, int seg_tiles, int seg_cap,
+                             uint32_t* list_a, uint32_t* counters_a, uint32_t* list_b, uint32_t* counters_b,
+                             int hb, int wb, int block, int h_out, int w_out, int h, int w, int k, int stride,
+                             int pad, int sy, int sx, hipStream_t st) {
+  hipLaunchKernelGGL(split_list_kernel, dim3(1), dim3(1024), 0, st, list, counters, seg_tiles, seg_cap, list_a,
+                     counters_a, list_b, counters_b, hb, wb, block, h_out, w_out, h, w, k, stride, pad, sy, sx);
   return hipGetLastError();
 }
 
