@@ -195,7 +195,7 @@ def event_blocks(nfr: int, length: int = 16):
     return 2 * nfr + length // 2, length
 
 
-def measure_point(make_layer, frames_dev, steps, warmup, geom, *, label, events=True):
+def measure_point(make_layer, frames_dev, steps, warmup, geom, *, label, events=True, retains=False):
     """Warm up, then time exactly `steps` steps; per-kernel times from HIP events on sampled steps."""
     layer = make_layer()
     fused = layer.fused
@@ -219,12 +219,14 @@ def measure_point(make_layer, frames_dev, steps, warmup, geom, *, label, events=
     conv_flop = 2.0 * sites[tpos].sum() * macs_per_site / nt
     xb, nb = geom["x_bytes"], geom["nb"]
     ref = (tpos == 0)
-    gate_bytes = (np.where(ref, 2 * xb, 3 * xb) + 2 * nb + 4 * blocks[tpos]).sum() / nt
-    # fused kernel: x_t, x_{t-1} read once, x_t copied, z read-modify-written at
-    # active sites (written only on a reference frame), weights, block flags
+    # x_t read (and copied unless the caller retains its frames), x_{t-1} read
+    # except on a reference frame
+    xio = np.where(ref, xb if retains else 2 * xb, 2 * xb if retains else 3 * xb)
+    gate_bytes = (xio + 2 * nb + 4 * blocks[tpos]).sum() / nt
+    # fused kernel: the same x traffic, z read-modify-written at active sites
+    # (written only on a reference frame), weights, block flags
     zb = 4.0 * geom["c_out"] * sites[tpos]
-    fused_bytes = (np.where(ref, 2 * xb, 3 * xb) + np.where(ref, zb, 2 * zb) + nb
-                   + geom["w_bytes"]).sum() / nt
+    fused_bytes = (xio + np.where(ref, zb, 2 * zb) + nb + geom["w_bytes"]).sum() / nt
     gate_us = 1e3 * gate_ms / nt if len(tpos) else None
     conv_us = 1e3 * conv_ms / nt if len(tpos) else None
     res = {
@@ -761,6 +763,8 @@ def main():
     ap.add_argument("--no-events", action="store_true", help="time without per-kernel events")
     ap.add_argument("--split", action="store_true",
                     help="force the gate + compaction + conv pipeline instead of the fused kernel")
+    ap.add_argument("--caller-retains", action="store_true",
+                    help="headline layer reads x_{t-1} from the previous frame's buffer (no copy)")
     ap.add_argument("--eps", type=float, default=None,
                     help="fixed gate threshold (skips calibration; used for counter runs)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -817,12 +821,14 @@ def main():
         torch.cuda.synchronize()
     stats = None if args.eps is not None else gpu_stats(layer_kw, wt, frames_dev)
 
-    def mk(b, eps, dense=False, split=args.split, gate="input"):
-        return lambda: SkipConv(wt, eps=eps, block=b, force_dense=dense, split=split, gate=gate, **layer_kw)
+    def mk(b, eps, dense=False, split=args.split, gate="input", retains=args.caller_retains):
+        return lambda: SkipConv(wt, eps=eps, block=b, force_dense=dense, split=split, gate=gate,
+                                caller_retains=retains, **layer_kw)
 
     eps_head = args.eps if args.eps is not None else eps_for_density(stats, block, h_out, w_out, args.density)
     head = measure_point(mk(block, eps_head), frames_dev, args.steps, args.warmup, geom,
-                         label=f"b={block} d={args.density}", events=not args.no_events)
+                         label=f"b={block} d={args.density}", events=not args.no_events,
+                         retains=args.caller_retains)
 
     sweep = []
     if not args.no_sweep and stats is not None:
@@ -841,6 +847,15 @@ def main():
         r = measure_point(mk(block, eps_head, split=not args.split), frames_dev, sweep_steps, len(clip), geom,
                           label=f"b={block} d={args.density} other pipeline")
         r.update({"block": block, "target_density": args.density})
+        sweep.append(r)
+        # the other x_{t-1} contract: read from the caller's previous frame
+        # (no copy written), or from the library's own copy
+        other = not args.caller_retains
+        r = measure_point(mk(block, eps_head, retains=other), frames_dev, sweep_steps, len(clip), geom,
+                          label=f"b={block} d={args.density} " + ("caller-retained frames" if other
+                                                                  else "library x_(t-1) copy"),
+                          retains=other)
+        r.update({"block": block, "target_density": args.density, "caller_retains": other})
         sweep.append(r)
         # Output-Norm gate (Eq. 7) at the same density: with p = 2 it compares
         # s * sum(w^2) with eps^2, so eps scales by the weight 2-norm
@@ -882,7 +897,11 @@ def main():
                       "dense_tflops": 2.0 * geom["sites"] * spec.c_out * kk / (tus * 1e-6) / 1e12})
         log(f"[bench] torch conv2d dense: {tus:.1f} us")
 
-    # roofline of the dominant kernel, from the events of the timed region
+    # roofline of the dominant kernel, from the events of the timed region;
+    # the committed counter summaries are of the library-copy contract
+    def traffic(kernel):
+        return None if args.caller_retains else profiled_traffic(args.workload, kernel)
+
     peak_mfma = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
     roof = None
     if head["gate_us"] is not None and head["pipeline"] == "fused":
@@ -892,26 +911,26 @@ def main():
             a = fb / (fus * 1e-6) / 1e9
             roof = {"kernel": "fused (residual, gate, local compaction, MFMA conv, z update)", "bound": "hbm",
                     "achieved": a, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": a / PEAK_HBM_GBS,
-                    "traffic": profiled_traffic(args.workload, "fused"), "bytes_per_launch": fb,
+                    "traffic": traffic("fused"), "bytes_per_launch": fb,
                     "flop_per_launch": ff, "us_per_launch": fus}
         else:
             a = ff / (fus * 1e-6) / 1e12
             roof = {"kernel": "fused (residual, gate, local compaction, MFMA conv, z update)", "bound": "mfma",
                     "achieved": a, "peak": peak_mfma, "unit": "TFLOP/s", "frac": a / peak_mfma,
-                    "traffic": profiled_traffic(args.workload, "fused"), "bytes_per_launch": fb,
+                    "traffic": traffic("fused"), "bytes_per_launch": fb,
                     "flop_per_launch": ff, "us_per_launch": fus}
     elif head["conv_us"] is not None:
         if head["conv_us"] >= head["gate_us"]:
             a = head["conv_active_tflops"]
             roof = {"kernel": "conv (sparse gather-MFMA)", "bound": "mfma", "achieved": a,
                     "peak": peak_mfma, "unit": "TFLOP/s", "frac": a / peak_mfma,
-                    "traffic": profiled_traffic(args.workload, "conv"),
+                    "traffic": traffic("conv"),
                     "flop_per_launch": head["conv_flop_per_launch"], "us_per_launch": head["conv_us"]}
         else:
             a = head["gate_gbs"]
             roof = {"kernel": "gate (residual, statistic, compaction)", "bound": "hbm", "achieved": a,
                     "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": a / PEAK_HBM_GBS,
-                    "traffic": profiled_traffic(args.workload, "gate"),
+                    "traffic": traffic("gate"),
                     "bytes_per_launch": head["gate_bytes_per_launch"], "us_per_launch": head["gate_us"]}
 
     cpu = None
@@ -939,7 +958,7 @@ def main():
             "eps": eps_head, "block": block, "density": head["density"],
             "density_steady": head["density_steady"],
             "active_tflops": head["active_tflops"], "dense_equiv_tflops": head["dense_equiv_tflops"],
-            "pipeline": head["pipeline"],
+            "pipeline": head["pipeline"], "caller_retains": bool(args.caller_retains),
             "kernel_us": head["gate_us"] if head["pipeline"] == "fused" else None,
             "gate_us": head["gate_us"] if head["pipeline"] == "split" else None,
             "conv_us": head["conv_us"] if head["pipeline"] == "split" else None,

@@ -98,14 +98,23 @@ enum { SKIPCONV_ACT_NONE = 0, SKIPCONV_ACT_IDENTITY = 1, SKIPCONV_ACT_RELU = 2 }
  * output sites (instead of 16 x 16 or 8 x 8) when its chunk sums combine in
  * lane groups (see skipconv_gate_tile) and such a tile holds at most 256
  * blocks: fewer halo pixels read twice, four times fewer workgroups. A tuning
- * knob; the results are the same. */
+ * knob; the results are the same.
+ * CALLER_RETAINS: x_{t-1} is read from the caller's own buffer, the x_t of the
+ * previous step, instead of a copy kept by the library (the state update of
+ * Eq. 2 then writes nothing): the gate stores no copy of x_t and the workspace
+ * holds no x_{t-1} slots (2 |x| less). The caller keeps each frame's buffer
+ * valid and unchanged until the next step's work on the stream is done, and
+ * passes a different buffer on every step after the first (E_INVALID_ARG for
+ * the same pointer twice in a row, which would read as a zero residual). The
+ * results are the same as without the flag. */
 enum {
   SKIPCONV_FLAG_KEEP_STATS = 1u,
   SKIPCONV_FLAG_FORCE_DENSE = 2u,
   SKIPCONV_FLAG_SPLIT_PIPELINE = 4u,
   SKIPCONV_FLAG_EMIT_RESIDUAL = 8u,
   SKIPCONV_FLAG_TRANSLATE = 16u,
-  SKIPCONV_FLAG_LARGE_GATE_TILES = 32u
+  SKIPCONV_FLAG_LARGE_GATE_TILES = 32u,
+  SKIPCONV_FLAG_CALLER_RETAINS = 64u
 };
 
 typedef struct skipconv_desc {
@@ -162,7 +171,8 @@ int skipconv_create(const skipconv_desc* d, const void* weights, void* workspace
 /* Process one frame (Eq. 3).
  *   x_t: device pointer, 16-byte aligned, N x H x W x C_in in the layer
  *        dtype; read by work enqueued on `stream`, so it must stay valid
- *        until that work is done.
+ *        until that work is done (until the next step's work is done with
+ *        SKIPCONV_FLAG_CALLER_RETAINS, whose next step reads it as x_{t-1}).
  *   *z_t: (may be NULL) set to the device pointer of the persistent state,
  *        N x H_out x W_out x C_out fp32, valid until the next step, reset or
  *        destroy on this handle. Copy it to keep it.

@@ -115,7 +115,7 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
     return fail(err, SKIPCONV_E_UNSUPPORTED, "EMIT_RESIDUAL and TRANSLATE cannot be combined");
   if (d->flags & ~(uint32_t)(SKIPCONV_FLAG_KEEP_STATS | SKIPCONV_FLAG_FORCE_DENSE | SKIPCONV_FLAG_SPLIT_PIPELINE |
                              SKIPCONV_FLAG_EMIT_RESIDUAL | SKIPCONV_FLAG_TRANSLATE |
-                             SKIPCONV_FLAG_LARGE_GATE_TILES))
+                             SKIPCONV_FLAG_LARGE_GATE_TILES | SKIPCONV_FLAG_CALLER_RETAINS))
     return fail(err, SKIPCONV_E_INVALID_ARG, "unknown flag bits");
   if (std::isnan(d->eps) || d->eps < 0.0f) return fail(err, SKIPCONV_E_INVALID_ARG, "eps must be >= 0");
   if (!depthwise && d->c_out > kMaxCout) return fail(err, SKIPCONV_E_UNSUPPORTED, "c_out > 256");
@@ -369,8 +369,10 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
   G.z_bytes = (size_t)sites * d->c_out * 4;
   size_t off = 0;
   G.off_wpack = off; off = align_up(off + G.wpack_bytes);
-  G.off_slot0 = off; off = align_up(off + G.x_bytes);
-  G.off_slot1 = off; off = align_up(off + G.x_bytes);
+  // the x_{t-1} ping-pong slots (none when the caller retains its frames)
+  const size_t slot_bytes = (d->flags & SKIPCONV_FLAG_CALLER_RETAINS) ? 0 : G.x_bytes;
+  G.off_slot0 = off; off = align_up(off + slot_bytes);
+  G.off_slot1 = off; off = align_up(off + slot_bytes);
   G.off_z = off; off = align_up(off + G.z_bytes);
   G.off_y = off;
   if (d->act_out != SKIPCONV_ACT_NONE) off = align_up(off + (size_t)sites * d->c_out * G.elem);
@@ -427,6 +429,7 @@ struct skipconv_layer {
   char* ws = nullptr;
   bool owns_ws = false;
   int cur = 0;               // slot holding x_{t-1}
+  const void* last_x = nullptr;  // CALLER_RETAINS: the previous step's x_t (NULL after create/reset)
   bool ref_pending = true;
   long long frames = 0;
   char last_error[256] = "";
@@ -437,6 +440,16 @@ struct skipconv_layer {
 
   void* wpack() { return ws + g.off_wpack; }
   void* slot(int i) { return ws + (i ? g.off_slot1 : g.off_slot0); }
+  bool retains() const { return (d.flags & SKIPCONV_FLAG_CALLER_RETAINS) != 0; }
+  // x_{t-1} as the kernels read it (x_t stands in on a reference frame, which
+  // reads no x_{t-1}), and where the gate copies x_t (NULL: no copy)
+  const void* prev_input(const void* x_t) { return retains() ? (last_x ? last_x : x_t) : slot(cur); }
+  void* keep_slot() { return retains() ? nullptr : slot(cur ^ 1); }
+  // the state update of Eq. 2 once the step's work is enqueued
+  void advance_input(const void* x_t) {
+    if (retains()) last_x = x_t;
+    else cur ^= 1;
+  }
   int zslot = 0;             // translated steps alternate z between two slots
   float* z() { return reinterpret_cast<float*>(ws + (zslot ? g.off_z2 : g.off_z)); }
   float* z_other() { return reinterpret_cast<float*>(ws + (zslot ? g.off_z : g.off_z2)); }
@@ -566,8 +579,8 @@ sc::GateParams gate_params(skipconv_layer* h, const void* x_t, bool ref) {
   const Geometry& g = h->g;
   sc::GateParams gp{};
   gp.x_t = x_t;
-  gp.x_prev = h->slot(h->cur);
-  gp.x_keep = h->slot(h->cur ^ 1);
+  gp.x_prev = h->prev_input(x_t);
+  gp.x_keep = h->keep_slot();
   gp.n = d.n; gp.h = d.h; gp.w = d.w; gp.c = d.c_in;
   gp.h_out = g.h_out; gp.w_out = g.w_out; gp.k = d.kernel; gp.stride = d.stride; gp.pad = g.pad;
   gp.block = d.block; gp.hb = g.hb; gp.wb = g.wb;
@@ -805,6 +818,8 @@ int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t
   if (!x_t) return fail(h->last_error, SKIPCONV_E_INVALID_ARG, "x_t is NULL");
   if (reinterpret_cast<uintptr_t>(x_t) % 16)
     return fail(h->last_error, SKIPCONV_E_INVALID_ARG, "x_t must be 16-byte aligned");
+  if (h->retains() && !h->ref_pending && x_t == h->last_x)
+    return fail(h->last_error, SKIPCONV_E_INVALID_ARG, "CALLER_RETAINS: x_t is the previous step's buffer");
   if (h->g.learned && !h->phi_set)
     return fail(h->last_error, SKIPCONV_E_STATE, "learned gate: call skipconv_set_gate_weights first");
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -816,7 +831,7 @@ int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t
 
   sc::ConvParams cp{};
   cp.x_t = x_t;
-  cp.x_prev = h->slot(h->cur);
+  cp.x_prev = h->prev_input(x_t);
   cp.wpack = h->wpack();
   cp.z = h->z();
   cp.y = h->y();
@@ -872,7 +887,7 @@ int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t
     if (e != hipSuccess) return hip_fail(h, e, "event record");
     ++h->timing_done;
   }
-  h->cur ^= 1;
+  h->advance_input(x_t);
   h->ref_pending = false;
   ++h->frames;
   if (z_t) *z_t = h->z();
@@ -893,6 +908,8 @@ int skipconv_step_translated(skipconv_t h, const void* x_t, int32_t dy, int32_t 
   if (!x_t) return fail(h->last_error, SKIPCONV_E_INVALID_ARG, "x_t is NULL");
   if (reinterpret_cast<uintptr_t>(x_t) % 16)
     return fail(h->last_error, SKIPCONV_E_INVALID_ARG, "x_t must be 16-byte aligned");
+  if (h->retains() && !h->ref_pending && x_t == h->last_x)
+    return fail(h->last_error, SKIPCONV_E_INVALID_ARG, "CALLER_RETAINS: x_t is the previous step's buffer");
   if (h->g.learned && !h->phi_set)
     return fail(h->last_error, SKIPCONV_E_STATE, "learned gate: call skipconv_set_gate_weights first");
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -921,7 +938,7 @@ int skipconv_step_translated(skipconv_t h, const void* x_t, int32_t dy, int32_t 
   if (e != hipSuccess) return hip_fail(h, e, "translated gate launch");
   sc::ConvParams cp{};
   cp.x_t = x_t;
-  cp.x_prev = h->slot(h->cur);
+  cp.x_prev = h->prev_input(x_t);
   cp.wpack = h->wpack();
   cp.z = h->z();
   cp.y = h->y();
@@ -947,7 +964,7 @@ int skipconv_step_translated(skipconv_t h, const void* x_t, int32_t dy, int32_t 
   }
   if (e != hipSuccess) return hip_fail(h, e, "translated conv launch");
   end_list(h);
-  h->cur ^= 1;
+  h->advance_input(x_t);
   h->ref_pending = false;
   ++h->frames;
   if (z_t) *z_t = h->z();
@@ -1048,6 +1065,7 @@ int skipconv_step_chained(skipconv_t h, skipconv_t up, void* stream, const float
 int skipconv_reset(skipconv_t h) {
   if (!h) return SKIPCONV_E_STATE;
   h->ref_pending = true;
+  h->last_x = nullptr;
   return SKIPCONV_OK;
 }
 

@@ -32,6 +32,7 @@ SKIPCONV_FLAG_KEEP_STATS, SKIPCONV_FLAG_FORCE_DENSE, SKIPCONV_FLAG_SPLIT_PIPELIN
 SKIPCONV_FLAG_EMIT_RESIDUAL = 8
 SKIPCONV_FLAG_TRANSLATE = 16
 SKIPCONV_FLAG_LARGE_GATE_TILES = 32
+SKIPCONV_FLAG_CALLER_RETAINS = 64
 
 
 class skipconv_desc(ctypes.Structure):
@@ -284,7 +285,7 @@ _GATE = {"input": SKIPCONV_GATE_INPUT_NORM, "output": SKIPCONV_GATE_OUTPUT_NORM,
 def make_desc(*, n, h, w, c_in, c_out, kernel, stride=1, pad=-1, groups=1, block=1, norm_p=2,
               support="rf", dtype="f32", act_out="none", eps=0.0, keep_stats=False,
               force_dense=False, split=False, gate="input", emit_residual=False,
-              translate=False, large_gate_tiles=False) -> skipconv_desc:
+              translate=False, large_gate_tiles=False, caller_retains=False) -> skipconv_desc:
     d = skipconv_desc_init()
     d.n, d.h, d.w, d.c_in, d.c_out = n, h, w, c_in, c_out
     d.kernel, d.stride, d.pad, d.groups, d.block = kernel, stride, pad, groups, block
@@ -295,7 +296,8 @@ def make_desc(*, n, h, w, c_in, c_out, kernel, stride=1, pad=-1, groups=1, block
                | (SKIPCONV_FLAG_SPLIT_PIPELINE if split else 0)
                | (SKIPCONV_FLAG_EMIT_RESIDUAL if emit_residual else 0)
                | (SKIPCONV_FLAG_TRANSLATE if translate else 0)
-               | (SKIPCONV_FLAG_LARGE_GATE_TILES if large_gate_tiles else 0))
+               | (SKIPCONV_FLAG_LARGE_GATE_TILES if large_gate_tiles else 0)
+               | (SKIPCONV_FLAG_CALLER_RETAINS if caller_retains else 0))
     d.eps = eps
     d.gate = _GATE[gate]
     return d
@@ -308,6 +310,11 @@ class SkipConv:
     step(x) takes an N x H x W x C_in tensor of the layer dtype and returns the
     persistent fp32 state z (N x H_out x W_out x C_out), a view that the next
     step overwrites.
+
+    caller_retains: the next step reads this step's x as x_{t-1} instead of a
+    copy in the workspace (no copy is written). The object keeps a reference
+    to the last frame so that its memory is not reused; the caller must not
+    modify it in place before the next step, and passes a new tensor each step.
     """
 
     def __init__(self, weight, *, n: int, h: int, w: int, stride: int = 1, pad: int = -1,
@@ -315,7 +322,7 @@ class SkipConv:
                  support: str = "rf", act_out: str = "none", keep_stats: bool = False,
                  force_dense: bool = False, split: bool = False, gate: str = "input",
                  emit_residual: bool = False, translate: bool = False, large_gate_tiles: bool = False,
-                 stream=None):
+                 caller_retains: bool = False, stream=None):
         import torch
 
         if not weight.is_cuda:
@@ -330,7 +337,8 @@ class SkipConv:
                               pad=pad, groups=groups, block=block, norm_p=norm_p, support=support,
                               dtype=self.dtype, act_out=act_out, eps=eps, keep_stats=keep_stats, gate=gate,
                               force_dense=force_dense, split=split, emit_residual=emit_residual,
-                              translate=translate, large_gate_tiles=large_gate_tiles)
+                              translate=translate, large_gate_tiles=large_gate_tiles,
+                              caller_retains=caller_retains)
         self.h_out, self.w_out, self.hb, self.wb = skipconv_out_shape(self.desc)
         nbytes = skipconv_workspace_size(self.desc)
         self.device = weight.device
@@ -342,6 +350,7 @@ class SkipConv:
         self._z = None
         self._zp = None
         self._y = None
+        self._prev_x = None  # caller_retains: the frame the next step reads as x_{t-1}
 
     def _stream(self) -> int:
         s = self.stream if self.stream is not None else self.torch.cuda.current_stream(self.device)
@@ -362,7 +371,13 @@ class SkipConv:
         if tuple(x.shape) != self.shape_in or x.dtype != self.tdtype or not x.is_contiguous() \
                 or x.device != self.device:
             raise ValueError(f"x must be a contiguous {self.tdtype} tensor of shape {self.shape_in} on {self.device}")
-        return self._z_view(skipconv_step(self.handle, x.data_ptr(), self._stream()))
+        z = self._z_view(skipconv_step(self.handle, x.data_ptr(), self._stream()))
+        self._retain(x)
+        return z
+
+    def _retain(self, x):
+        if self.desc.flags & SKIPCONV_FLAG_CALLER_RETAINS:
+            self._prev_x = x
 
     def _z_view(self, zp: int):
         # the state pointer is fixed except across translated steps (two z slots)
@@ -377,7 +392,9 @@ class SkipConv:
         if tuple(x.shape) != self.shape_in or x.dtype != self.tdtype or not x.is_contiguous() \
                 or x.device != self.device:
             raise ValueError(f"x must be a contiguous {self.tdtype} tensor of shape {self.shape_in} on {self.device}")
-        return self._z_view(skipconv_step_translated(self.handle, x.data_ptr(), dy, dx, self._stream()))
+        z = self._z_view(skipconv_step_translated(self.handle, x.data_ptr(), dy, dx, self._stream()))
+        self._retain(x)
+        return z
 
     def step_chained(self, upstream: "SkipConv"):
         """One frame whose input is `upstream`'s activation output (upstream stepped first).
@@ -395,6 +412,7 @@ class SkipConv:
 
     def reset(self):
         skipconv_reset(self.handle)
+        self._prev_x = None
 
     @property
     def fused(self) -> bool:

@@ -43,7 +43,7 @@ def good(**kw):
     ("block", 0, S.SKIPCONV_E_INVALID_ARG), ("block", 65, S.SKIPCONV_E_INVALID_ARG),
     ("norm_p", 3, S.SKIPCONV_E_INVALID_ARG), ("support", 2, S.SKIPCONV_E_INVALID_ARG),
     ("dtype", 2, S.SKIPCONV_E_INVALID_ARG), ("act_out", 3, S.SKIPCONV_E_INVALID_ARG),
-    ("flags", 64, S.SKIPCONV_E_INVALID_ARG), ("flags", 8, S.SKIPCONV_E_INVALID_ARG),
+    ("flags", 128, S.SKIPCONV_E_INVALID_ARG), ("flags", 8, S.SKIPCONV_E_INVALID_ARG),
     ("eps", -1.0, S.SKIPCONV_E_INVALID_ARG),
     ("eps", float("nan"), S.SKIPCONV_E_INVALID_ARG), ("c_out", 272, S.SKIPCONV_E_UNSUPPORTED),
     ("gate", 7, S.SKIPCONV_E_INVALID_ARG), ("gate", -1, S.SKIPCONV_E_INVALID_ARG),
@@ -96,6 +96,10 @@ def test_workspace_size_covers_state(lib):
     assert S.skipconv_workspace_size(d2) >= n + 128 * 96 * 64 * 2 + 128 * 96 * 5
     d3 = good(act_out="relu", emit_residual=True)  # + fp32 and bf16 residuals + previous block flags
     assert S.skipconv_workspace_size(d3) >= n + 128 * 96 * 64 * (2 + 4 + 2) + 16 * 12
+    # caller-retained frames: no x_{t-1} slots
+    d4 = good(caller_retains=True)
+    assert S.skipconv_validate(d4) == 0
+    assert n - S.skipconv_workspace_size(d4) == 2 * x
 
 
 def test_null_handles_and_status_strings(lib):

@@ -21,12 +21,14 @@ pytestmark = pytest.mark.gpu
 
 def _layer_pair(w_f32, *, n, h, w, dtype, eps, block, stride=1, pad=-1, groups=1, norm_p=2,
                 support="rf", keep_stats=True, act_out="none", force_dense=False, split=False,
-                gate="input", phi=None, gate_bias=0.0, translate=False, large_gate_tiles=False):
+                gate="input", phi=None, gate_bias=0.0, translate=False, large_gate_tiles=False,
+                caller_retains=False):
     ws = weight_storage(w_f32, dtype)
     layer = S.SkipConv(to_device(ws, dtype), n=n, h=h, w=w, stride=stride, pad=pad, groups=groups,
                        eps=eps, block=block, norm_p=norm_p, support=support, keep_stats=keep_stats,
                        act_out=act_out, force_dense=force_dense, split=split, gate=gate,
-                       translate=translate, large_gate_tiles=large_gate_tiles)
+                       translate=translate, large_gate_tiles=large_gate_tiles,
+                       caller_retains=caller_retains)
     if gate == "learned":
         layer.set_gate_weights(torch.from_numpy(np.ascontiguousarray(phi, np.float32)).cuda(), gate_bias)
     orc = O.SkipConvOracle(ws, n=n, h=h, w=w, stride=stride, pad=None if pad == -1 else pad,
@@ -493,6 +495,73 @@ def test_large_gate_tiles(case):
         compare_frame(layer, ref, dtype, t=t, tag=tag, keep_stats=True)
         dens.append(ref["count"] / ref["block_mask"].size)
     layer.close()
+    assert 0.0 < np.mean(dens[1:4]) < 1.0
+
+
+# Caller-retained frames (x_{t-1} read from the previous step's buffer, no
+# copy written): fused and split pipelines, fp32 and bf16, fewer than 8
+# channels, a 1 x 1 stride-2 layer (pixels outside every halo) and translated
+# steps. (n, h, w, c_in, c_out, k, stride, block, dtype, split, translated)
+RETAINS = [
+    (1, 40, 36, 64, 64, 3, 1, 8, "bf16", False, False),
+    (2, 33, 29, 64, 128, 3, 1, 4, "bf16", True, False),
+    (1, 24, 20, 3, 32, 3, 1, 1, "bf16", True, False),
+    (1, 32, 32, 16, 16, 3, 1, 1, "f32", False, False),
+    (1, 30, 30, 32, 64, 1, 2, 2, "bf16", False, False),
+    (1, 36, 40, 64, 64, 3, 2, 8, "bf16", True, True),
+]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("case", RETAINS)
+def test_caller_retains(case):
+    """CALLER_RETAINS: every frame matches the oracle (masks and list bit-exact, z within
+    tolerance) and the state equals, bit for bit, that of a layer keeping its own x_{t-1}
+    copy on the same frames; a reset in the middle; the same buffer twice is rejected."""
+    n, h, w, ci, co, k, s, b, dtype, split, translated = case
+    rng = np.random.Generator(np.random.PCG64(900 + ci + k + b))
+    base = list(syn.RectVideo(h, w, ci, 7, seed=901 + ci, batch=n, n_rect=3, side_lo=4, side_hi=14))
+    shifts = [(0, 0), (s, -s), (0, 0), (-2 * s, s), (0, 0), (s, 0), (0, 2 * s)] if translated else [(0, 0)] * 7
+    frames, acc = [], (0, 0)
+    for f, d in zip(base, shifts):
+        acc = (acc[0] + d[0], acc[1] + d[1])
+        frames.append(O.translate(f, *acc) if translated else f)
+    wt = rng.normal(0, 0.2, (co, ci, k, k)).astype(np.float32)
+    pad = (k - 1) // 2
+    ho, wo = O.out_size(h, k, s, pad), O.out_size(w, k, s, pad)
+    stats = oracle_stats(base[:3], wt.shape, dtype=dtype, stride=s)
+    eps = eps_for_density(stats, b, ho, wo, 0.4)
+    tag = f"retains {case}"
+    kw = dict(n=n, h=h, w=w, dtype=dtype, eps=eps, block=b, stride=s, split=split, translate=translated)
+    layer, orc = _layer_pair(wt, caller_retains=True, **kw)
+    own, _ = _layer_pair(wt, keep_stats=False, **kw)
+    assert layer.fused == own.fused and not (split and layer.fused)
+    assert layer.workspace.numel() < own.workspace.numel()
+    dens = []
+    for t, (f, d) in enumerate(zip(frames, shifts)):
+        if t == 4:
+            for m in (layer, own, orc):
+                m.reset()
+        xs = syn.to_storage(f, dtype)
+        x = to_device(xs, dtype)  # a new buffer every frame; the layer keeps the last one
+        say(f"[{tag}] frame {t} shift={d} eps={eps:.4g} fused={layer.fused}")
+        if translated:
+            layer.step_translated(x, *d)
+            own.step_translated(x.clone(), *d)
+            ref = orc.step(xs, shift=d)
+        else:
+            layer.step(x)
+            own.step(x.clone())
+            ref = orc.step(xs)
+        compare_frame(layer, ref, dtype, t=t, tag=tag, keep_stats=True)
+        torch.cuda.synchronize()
+        assert torch.equal(layer._z.view(torch.int32), own._z.view(torch.int32)), f"{tag} t={t}"
+        dens.append(ref["count"] / ref["block_mask"].size)
+    with pytest.raises(S.SkipConvError) as ei:
+        layer.step(layer._prev_x)
+    assert ei.value.code == S.SKIPCONV_E_INVALID_ARG
+    layer.close()
+    own.close()
     assert 0.0 < np.mean(dens[1:4]) < 1.0
 
 
