@@ -524,30 +524,40 @@ conv_halo_kernel(ConvParams p, HaloParams hp) {
 
 // ---------------------------------------------------------------- fp32 ----
 
+// Tiles of kConvF32Rows output sites; the waves of a workgroup split the
+// k-steps into contiguous parts. fp32 layers are the small frames, whose few
+// tiles left most of the chip idle while one wave per tile walked all of K.
+// The part sums meet in LDS, where wave 0 adds them in part order and updates
+// z. Tap and channel of a k index come from qdiv (exact for these sizes), not
+// from integer divisions.
 template <int NTN>
 __global__ void __launch_bounds__(kConvThreads) conv_f32_kernel(ConvParams p) {
   // k-steps whose operand (two frames) and weight loads are issued together:
   // every load is unconditional (clamped to element 0 and masked after), so
   // a chunk costs one memory round trip instead of one per k-step
   constexpr int kChunkSteps = NTN <= 2 ? 16 : (NTN <= 4 ? 8 : 4);
+  constexpr int kWaves = kConvThreads / 64;
+  __shared__ floatx4 part[kWaves - 1][NTN][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, kq = lane >> 4;
   const int bb = p.block * p.block;
   const WorkList W = work_list(p.counters, p.seg_tiles, p.seg_cap);
   const long total_rows = (long)W.total * bb;
   if (p.zero_ctr && blockIdx.x == 0 && threadIdx.x < kSegs) p.zero_ctr[threadIdx.x * kSegStride] = 0u;  // next step's work list
-  const int ntiles = (int)((total_rows + kRowsPerTile - 1) / kRowsPerTile);
+  const int ntiles = (int)((total_rows + kConvF32Rows - 1) / kConvF32Rows);
   const float* xt = static_cast<const float*>(p.x_t);
   const float* xp = static_cast<const float*>(p.no_prev ? p.x_t : p.x_prev);
   const float* wp = static_cast<const float*>(p.wpack);
   const int kk = p.k * p.k * p.c;
+  const int ks0 = wave * p.ksteps / kWaves, ks1 = (wave + 1) * p.ksteps / kWaves;  // this wave's k-part
+  const float inv_c = 1.0f / (float)p.c, inv_k = 1.0f / (float)p.k;
 
   for (TileWalk tw(ntiles); tw.t < tw.end; tw.t += tw.step) {
-    const long g = (long)tw.t * kRowsPerTile + wave * 16 + r16;
+    const long g = (long)tw.t * kConvF32Rows + r16;
     const Site st = site_of_row(p, W, g, total_rows, bb);
     const int iy = st.oy * p.stride - p.pad, ix = st.ox * p.stride - p.pad;
-    // old z of the outputs this lane stores (site of lane kq * 4 + v, column
-    // i * 16 + r16), loaded before the product
+    // old z of the outputs wave 0 stores (site of lane kq * 4 + v, column
+    // i * 16 + r16), loaded before the product (other waves read element 0)
     const int zrow_mine = st.ok ? (st.n * p.h_out + st.oy) * p.w_out + st.ox : -1;
     int zrow[4];
     float zold[4][NTN];
@@ -557,7 +567,7 @@ __global__ void __launch_bounds__(kConvThreads) conv_f32_kernel(ConvParams p) {
 #pragma unroll
       for (int i = 0; i < NTN; ++i) {
         const int col = i * 16 + r16;
-        const bool ok = zrow[v] >= 0 && col < p.c_out && !p.reference;
+        const bool ok = wave == 0 && zrow[v] >= 0 && col < p.c_out && !p.reference;
         zold[v][i] = p.z[ok ? (size_t)zrow[v] * p.c_out + col : 0];
       }
     }
@@ -565,29 +575,29 @@ __global__ void __launch_bounds__(kConvThreads) conv_f32_kernel(ConvParams p) {
 #pragma unroll
     for (int i = 0; i < NTN; ++i) acc[i] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
 
-    for (int k0 = 0; k0 < p.ksteps; k0 += kChunkSteps) {
+    for (int k0 = ks0; k0 < ks1; k0 += kChunkSteps) {
       float av[kChunkSteps], pv[kChunkSteps], wv[kChunkSteps][NTN];
       bool in[kChunkSteps], pin[kChunkSteps];
 #pragma unroll
       for (int u = 0; u < kChunkSteps; ++u) {
         const int ks = k0 + u;
         const int kidx = ks * 4 + kq;
-        const int tap = kidx / p.c, ci = kidx - tap * p.c;
-        const int kh = tap / p.k, kw = tap - kh * p.k;
+        const int tap = qdiv(kidx, inv_c), ci = kidx - tap * p.c;
+        const int kh = qdiv(tap, inv_k), kw = tap - kh * p.k;
         const int y = iy + kh, x = ix + kw;
-        in[u] = st.ok && ks < p.ksteps && kidx < kk && y >= 0 && y < p.h && x >= 0 && x < p.w;
+        in[u] = st.ok && ks < ks1 && kidx < kk && y >= 0 && y < p.h && x >= 0 && x < p.w;
         const size_t off = in[u] ? ((size_t)(st.n * p.h + y) * p.w + x) * p.c + ci : 0;
         const long po = (in[u] && !p.no_prev) ? prev_off(p, st.n, y, x, ci) : -1;
         pin[u] = po >= 0;
         av[u] = xt[off];
         pv[u] = xp[pin[u] ? (size_t)po : 0];
-        const float* wk = wp + (size_t)(ks < p.ksteps ? ks : 0) * NTN * 64 + lane;
+        const float* wk = wp + (size_t)(ks < ks1 ? ks : 0) * NTN * 64 + lane;
 #pragma unroll
         for (int i = 0; i < NTN; ++i) wv[u][i] = wk[i * 64];
       }
 #pragma unroll
       for (int u = 0; u < kChunkSteps; ++u) {
-        if (k0 + u < p.ksteps) {  // wave-uniform (a guard, not a break: the loop stays unrolled)
+        if (k0 + u < ks1) {  // wave-uniform (a guard, not a break: the loop stays unrolled)
           const float a = !in[u] ? 0.0f : (pin[u] ? __fsub_rn(av[u], pv[u]) : av[u]);
 #pragma unroll
           for (int i = 0; i < NTN; ++i) acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, wv[u][i], acc[i], 0, 0, 0);
@@ -595,19 +605,36 @@ __global__ void __launch_bounds__(kConvThreads) conv_f32_kernel(ConvParams p) {
       }
     }
 
+    if (wave > 0) {
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      if (zrow[v] < 0) continue;
+      for (int i = 0; i < NTN; ++i) part[wave - 1][i][lane] = acc[i];
+    }
+    __syncthreads();
+    if (wave == 0) {
 #pragma unroll
-      for (int i = 0; i < NTN; ++i) {
-        const int col = i * 16 + r16;
-        if (col >= p.c_out) continue;
-        const size_t idx = (size_t)zrow[v] * p.c_out + col;
-        const float nv = p.reference ? acc[i][v] : zold[v][i] + acc[i][v];
-        p.z[idx] = nv;
-        if (p.act) store_y<float>(p.y, idx, activate(nv, p.act));
+      for (int q = 0; q < kWaves - 1; ++q) {
+#pragma unroll
+        for (int i = 0; i < NTN; ++i) {
+          const floatx4 s4 = part[q][i][lane];
+#pragma unroll
+          for (int v = 0; v < 4; ++v) acc[i][v] = __fadd_rn(acc[i][v], s4[v]);
+        }
+      }
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        if (zrow[v] < 0) continue;
+#pragma unroll
+        for (int i = 0; i < NTN; ++i) {
+          const int col = i * 16 + r16;
+          if (col >= p.c_out) continue;
+          const size_t idx = (size_t)zrow[v] * p.c_out + col;
+          const float nv = p.reference ? acc[i][v] : zold[v][i] + acc[i][v];
+          p.z[idx] = nv;
+          if (p.act) store_y<float>(p.y, idx, activate(nv, p.act));
+        }
       }
     }
+    __syncthreads();  // part is rewritten by the next tile
   }
 }
 

@@ -17,6 +17,7 @@ constexpr int kNumCounters = 16;
 constexpr int kSegs = 8;
 constexpr int kSegStride = 32;
 
+constexpr int kConvF32Rows = 16;     // output sites per tile of the fp32 convolution
 constexpr int kMaxTileBlocks = 256;  // blocks per gate tile: (ts / b)^2 <= 256
 
 // Gate: residual, support statistic, threshold, block pooling, compaction.

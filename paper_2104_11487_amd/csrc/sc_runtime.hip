@@ -235,7 +235,8 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
   } else {
     G.wpack_bytes = (size_t)k * k * d->c_in * 4;
   }
-  G.conv_max_tiles = (int)(((long)G.nb * b * b + 63) / 64);
+  const int conv_rows = (!depthwise && d->dtype == SKIPCONV_F32) ? sc::kConvF32Rows : 64;
+  G.conv_max_tiles = (int)(((long)G.nb * b * b + conv_rows - 1) / conv_rows);
 
   // depthwise halo kernel: tiles of tr rows x b columns of an active block, tr
   // the largest row count (halving from b) whose halo and [tap][c] weights
