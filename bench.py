@@ -415,7 +415,7 @@ def summarize_pmc(fetch_db: str, write_db: str, out_json: str, *, workload: str,
     w_scale = copy_bytes / cw if cw > 0 else None
     kernels = {}
     for label, pred in (("gate", lambda k: "gate_kernel" in k), ("compact", lambda k: "compact_kernel" in k),
-                        ("fused", lambda k: "fused_kernel" in k or "fused_rb_kernel" in k),
+                        ("fused", lambda k: "fused_kernel" in k or "fused_rb_kernel" in k or "fused_dw_kernel" in k),
                         ("conv", lambda k: "conv_" in k and "_kernel" in k),
                         ("depthwise", lambda k: "depthwise_kernel" in k)):
         vf = [v for k, v in fetch if pred(k)]

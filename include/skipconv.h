@@ -249,7 +249,9 @@ int skipconv_get_desc(skipconv_t h, skipconv_desc* d);
  * single-pass kernel whose waves hold their weight fragments in registers
  * (tiles of <= 8 x 8 sites, shapes it is built for), 3 for that kernel with
  * the output channels of each tile split over 2, 4 or 8 workgroups (shapes
- * built only for a share of the channels). Host only. */
+ * built only for a share of the channels), 4 for the single-pass depthwise
+ * kernel (bf16, C % 8 == 0, blocks of <= 8: per-channel products over the
+ * taps, channels split over up to 8 workgroups per tile). Host only. */
 int skipconv_pipeline(skipconv_t h, int32_t* fused);
 
 /* Gate tiling of the split pipeline: *ts = output sites per side of one gate

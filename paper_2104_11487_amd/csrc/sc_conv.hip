@@ -96,60 +96,6 @@ __device__ __forceinline__ void store_y(void* y, size_t i, float v) {
 
 // ---------------------------------------------------------------- bf16 ----
 
-template <bool FAST>
-__device__ __forceinline__ bf16x8 gather_a_bf16(const ConvParams& p, const uint16_t* xt,
-                                                const uint16_t* xp, const Site& st, int iy, int ix,
-                                                int ks, int kq) {
-  float v[8];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) v[e] = 0.0f;
-  if (FAST) {
-    const int cpt = p.c >> 5;  // k-steps per tap
-    const int tap = ks / cpt;
-    const int c0 = (ks - tap * cpt) * 32 + kq * 8;
-    const int kh = tap / p.k, kw = tap - kh * p.k;
-    const int y = iy + kh, x = ix + kw;
-    if (st.ok && y >= 0 && y < p.h && x >= 0 && x < p.w) {
-      const size_t off = ((size_t)(st.n * p.h + y) * p.w + x) * p.c + c0;
-      float a[8], b[8];
-      Elem<uint16_t>::load8(xt, off, a);
-      const long po = p.no_prev ? -1 : prev_off(p, st.n, y, x, c0);
-      if (po >= 0) {
-        Elem<uint16_t>::load8(xp, (size_t)po, b);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = __fsub_rn(a[e], b[e]);
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = a[e];
-      }
-    }
-  } else {
-    const int kk = p.k * p.k * p.c;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int kidx = ks * 32 + kq * 8 + e;
-      if (kidx < kk && st.ok) {
-        const int tap = kidx / p.c, ci = kidx - tap * p.c;
-        const int kh = tap / p.k, kw = tap - kh * p.k;
-        const int y = iy + kh, x = ix + kw;
-        if (y >= 0 && y < p.h && x >= 0 && x < p.w) {
-          const size_t off = ((size_t)(st.n * p.h + y) * p.w + x) * p.c + ci;
-          const float a = bf16_to_f32(xt[off]);
-          const long po = p.no_prev ? -1 : prev_off(p, st.n, y, x, ci);
-          const float b = po < 0 ? 0.0f : bf16_to_f32(xp[po]);
-          v[e] = __fsub_rn(a, b);
-        }
-      }
-    }
-  }
-  u32x4 u;
-  u.x = f32_to_bf16(v[0]) | (f32_to_bf16(v[1]) << 16);
-  u.y = f32_to_bf16(v[2]) | (f32_to_bf16(v[3]) << 16);
-  u.z = f32_to_bf16(v[4]) | (f32_to_bf16(v[5]) << 16);
-  u.w = f32_to_bf16(v[6]) | (f32_to_bf16(v[7]) << 16);
-  return __builtin_bit_cast(bf16x8, u);
-}
-
 template <bool FAST, int NTN>
 __global__ void __launch_bounds__(kConvThreads) conv_bf16_kernel(ConvParams p) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -234,12 +180,57 @@ __global__ void __launch_bounds__(kConvThreads) conv_bf16_kernel(ConvParams p) {
         }
       }
     } else {
-      for (int ks = 0; ks < p.ksteps; ++ks) {
-        const bf16x8 a = gather_a_bf16<FAST>(p, xt, xp, st, iy, ix, ks, kq);
-        const bf16x8* wk = wp + (size_t)ks * NTN * 64 + lane;
+      // C % 32 != 0: the 8 k indices of a lane's A piece may fall on
+      // different taps, so each element is loaded on its own; the 16 element
+      // loads of every k-step of a chunk and its weight fragments go out
+      // together (clamped to element 0 and masked after, as above). Tap and
+      // channel come from qdiv (exact for these sizes).
+      constexpr int kSteps = NTN <= 4 ? 2 : 1;
+      const int kk = p.k * p.k * p.c;
+      const float inv_c = 1.0f / (float)p.c, inv_k = 1.0f / (float)p.k;
+      for (int k0 = 0; k0 < p.ksteps; k0 += kSteps) {
+        uint32_t ea[kSteps][8], eb[kSteps][8];
+        bool ein[kSteps][8], epin[kSteps][8];
+        bf16x8 wv[kSteps][NTN];
 #pragma unroll
-        for (int i = 0; i < NTN; ++i)
-          acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, wk[i * 64], acc[i], 0, 0, 0);
+        for (int u = 0; u < kSteps; ++u) {
+          const int ks = k0 + u;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int kidx = ks * 32 + kq * 8 + e;
+            const int tap = qdiv(kidx, inv_c), ci = kidx - tap * p.c;
+            const int kh = qdiv(tap, inv_k), kw = tap - kh * p.k;
+            const int y = iy + kh, x = ix + kw;
+            const bool in = st.ok && ks < p.ksteps && kidx < kk && y >= 0 && y < p.h && x >= 0 && x < p.w;
+            const size_t off = in ? ((size_t)(st.n * p.h + y) * p.w + x) * p.c + ci : 0;
+            const long po = (in && !p.no_prev) ? prev_off(p, st.n, y, x, ci) : -1;
+            ein[u][e] = in;
+            epin[u][e] = po >= 0;
+            ea[u][e] = xt[off];
+            eb[u][e] = xp[po >= 0 ? (size_t)po : 0];
+          }
+          const bf16x8* wk = wp + (size_t)(ks < p.ksteps ? ks : 0) * NTN * 64 + lane;
+#pragma unroll
+          for (int i = 0; i < NTN; ++i) wv[u][i] = wk[i * 64];
+        }
+#pragma unroll
+        for (int u = 0; u < kSteps; ++u) {
+          if (k0 + u >= p.ksteps) continue;  // wave-uniform (not a break: the loop stays unrolled)
+          float v[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float xa = __uint_as_float(ea[u][e] << 16);
+            const float xb = epin[u][e] ? __uint_as_float(eb[u][e] << 16) : 0.0f;
+            v[e] = ein[u][e] ? __fsub_rn(xa, xb) : 0.0f;
+          }
+          u32x4 q;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) q[e] = f32_to_bf16(v[2 * e]) | (f32_to_bf16(v[2 * e + 1]) << 16);
+          const bf16x8 a = __builtin_bit_cast(bf16x8, q);
+#pragma unroll
+          for (int i = 0; i < NTN; ++i)
+            acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, wv[u][i], acc[i], 0, 0, 0);
+        }
       }
     }
 

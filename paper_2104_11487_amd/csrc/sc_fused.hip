@@ -935,6 +935,136 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
   if (EMIT) emit_clear(p, n, oy0, ox0, oh, ow, T.tb_w, blk_flag, emit_clr);
 }
 
+// ---------------------------------------------------------------------------
+// Depthwise layers (groups = C_in = C_out, C % 8 == 0, tiles of <= 8 x 8
+// sites). Steps 1-2 are those above; the product has one input channel per
+// output channel (Eq. 3 with g = C), so it is VALU work, no MFMA: a thread
+// forms 4 channels of one site as fp32 FMAs over the taps in row-major order,
+// rho from the LDS halo and the [tap][c] weights staged in LDS. The channels
+// split over nsplit workgroups per tile (at most kDwSplitMax each, so a
+// thread holds at most kDwPieces pieces); every split loads the whole halo and
+// evaluates the gate, the lead alone writes what all would write alike. The
+// product runs before the gate's final barrier (it does not depend on it), and
+// a tile found off stores nothing. KI: halo rows per thread (one round).
+// MODE as above.
+template <int KI, int MODE>
+__global__ void __launch_bounds__(kThreads) fused_dw_kernel(FusedParams p) {
+  constexpr bool EMIT = (MODE & 1) != 0;
+  constexpr bool CHAIN = (MODE & 2) != 0;
+  constexpr int EP = kDwPieces;
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  __shared__ uint32_t blk_flag[kMaxTileBlocks];
+  __shared__ uint32_t tile_on;
+  __shared__ uint8_t emit_clr[kMaxTileBlocks];
+
+  const GateParams& g = p.g;
+  const int wave = threadIdx.x >> 6;
+  const int tile_i = p.nsplit > 1 ? (int)(blockIdx.x / p.nsplit) : (int)blockIdx.x;
+  const int cs = g.c / p.nsplit;  // channels of this split: c0 .. c0 + cs - 1
+  const int c0 = ((int)blockIdx.x - tile_i * p.nsplit) * cs;
+  const bool lead = c0 == 0;
+  const Tile T = make_tile(p, tile_i);
+  if (CHAIN && g.up_mask && chain_skip<EMIT>(p, T, emit_clr, lead)) return;
+  float* wl = reinterpret_cast<float*>(lds + p.off_b);  // [tap][cs]
+  uint8_t* halo = lds + p.off_halo;
+  float* a_halo = reinterpret_cast<float*>(lds + p.off_a);
+  float* part = reinterpret_cast<float*>(lds + p.off_part);
+  const ChunkMap cm = make_chunks(p, T);
+  const int q4 = cs >> 2;  // 4-channel pieces per site
+  const float inv_q4 = 1.0f / (float)q4;
+  const int kk = g.k * g.k;
+
+  // 1. this split's weights (float4 w of the k*k*cs/4: tap w / q4, channels
+  // c0 + 4 (w % q4) ..), the halo loads, and the old z (and y) of this
+  // thread's pieces (piece e = h * 512 + thread: site e / q4, channels
+  // c0 + 4 (e % q4) ..): all in flight together
+  float4 wreg[kDwWeightLoads];
+#pragma unroll
+  for (int j = 0; j < kDwWeightLoads; ++j) {
+    const int w4 = j * kThreads + threadIdx.x;
+    const int tap = qdiv(w4, inv_q4), j4 = w4 - tap * q4;
+    const bool ok = tap < kk;
+    wreg[j] = static_cast<const float4*>(p.wpack)[ok ? ((size_t)tap * g.c + c0) / 4 + j4 : 0];
+  }
+  const HaloWalk hwk = make_walk<kThreads, true>(g, T, cm, threadIdx.x);
+  HaloBatch<KI> hb;
+  halo_load<CHAIN, kThreads, true, KI>(g, T, cm, hwk, 0, threadIdx.x, hb);
+  int esite[EP], eloc[EP], ecol[EP], epix[EP];
+  floatx4 zold[EP];
+  uint2 yold[EP];
+#pragma unroll
+  for (int h = 0; h < EP; ++h) {
+    const int e = h * kThreads + threadIdx.x;
+    const int site = qdiv(e, inv_q4), j4 = e - site * q4;
+    const int ly = qdiv(site, T.inv_ts), lx = site - ly * g.ts;
+    const bool ok = site < g.ts * g.ts && ly < T.oh && lx < T.ow;
+    const int gs = (T.n * g.h_out + T.oy0 + ly) * g.w_out + T.ox0 + lx;
+    esite[h] = ok ? gs : -1;
+    eloc[h] = ok ? qdiv(ly, T.inv_blk) * T.tb_w + qdiv(lx, T.inv_blk) : 0;
+    ecol[h] = c0 + 4 * j4;
+    epix[h] = ok ? (ly * g.stride) * T.hw + lx * g.stride : 0;
+    const size_t o = ok ? (size_t)gs * p.c_out + ecol[h] : 0;
+    zold[h] = *reinterpret_cast<const floatx4*>(p.z + o);
+    yold[h] = uint2{0u, 0u};
+    if (EMIT) yold[h] = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(p.y) + o);
+  }
+  for (int i = threadIdx.x; i < kMaxTileBlocks; i += kThreads) blk_flag[i] = 0u;
+  if (threadIdx.x == 0) tile_on = 0u;
+
+  // 2. halo use; the weights to LDS; then (settled) the x_t copy
+  halo_use<CHAIN, kThreads, true, KI>(p, T, cm, hwk, 0, wave, hb, halo, a_halo, part);
+#pragma unroll
+  for (int j = 0; j < kDwWeightLoads; ++j) {
+    const int w4 = j * kThreads + threadIdx.x;
+    if (w4 < kk * q4) reinterpret_cast<float4*>(wl)[w4] = wreg[j];
+  }
+#pragma unroll
+  for (int h = 0; h < EP; ++h) {
+    settle(zold[h]);
+    if (EMIT) settle(yold[h]);
+  }
+  if (lead) {
+    halo_keep(g, hb);
+    copy_owned(g, T);
+  }
+
+  // 3. gate (its first barrier also makes the halo and the weights visible)
+  gate_sites(p, T, cm, a_halo, part, blk_flag, &tile_on, lead);
+
+  // 4. product of every piece of the tile, before the gate's outcome is known
+  floatx4 u[EP];
+#pragma unroll
+  for (int h = 0; h < EP; ++h) {
+    u[h] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+    if (esite[h] < 0) continue;
+    const uint8_t* px = halo + (size_t)epix[h] * p.pstride + ecol[h] * 2;
+    const float* wt = wl + (ecol[h] - c0);
+    for (int kh = 0; kh < g.k; ++kh)
+      for (int kw = 0; kw < g.k; ++kw) {
+        const uint2 r = *reinterpret_cast<const uint2*>(px + (kh * T.hw + kw) * p.pstride);
+        const float4 w = *reinterpret_cast<const float4*>(wt + (kh * g.k + kw) * cs);
+        u[h][0] = __builtin_fmaf(w.x, __uint_as_float(r.x << 16), u[h][0]);
+        u[h][1] = __builtin_fmaf(w.y, __uint_as_float(r.x & 0xffff0000u), u[h][1]);
+        u[h][2] = __builtin_fmaf(w.z, __uint_as_float(r.y << 16), u[h][2]);
+        u[h][3] = __builtin_fmaf(w.w, __uint_as_float(r.y & 0xffff0000u), u[h][3]);
+      }
+  }
+  lds_barrier();
+  if (lead) gate_flags(p, T, blk_flag);
+  if (!tile_on) {
+    if (EMIT && lead) emit_clear(p, T.n, T.oy0, T.ox0, T.oh, T.ow, T.tb_w, blk_flag, emit_clr);
+    return;
+  }
+
+  // 5. epilogue at the active sites
+#pragma unroll
+  for (int h = 0; h < EP; ++h) {
+    if (esite[h] < 0 || blk_flag[eloc[h]] == 0u) continue;
+    store_piece<EMIT>(p, (size_t)esite[h] * p.c_out + ecol[h], u[h], zold[h], yold[h]);
+  }
+  if (EMIT && lead) emit_clear(p, T.n, T.oy0, T.ox0, T.oh, T.ow, T.tb_w, blk_flag, emit_clr);
+}
+
 // ------------------------------------------------------------ launching --
 
 template <int WM, int WN, int GM>
@@ -944,6 +1074,17 @@ hipError_t launch_fused_t(const FusedParams& p, int grid, hipStream_t st) {
     case 1: hipLaunchKernelGGL((fused_kernel<WM, WN, GM, 1>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
     case 2: hipLaunchKernelGGL((fused_kernel<WM, WN, GM, 2>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
     default: hipLaunchKernelGGL((fused_kernel<WM, WN, GM, 3>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+  }
+  return hipGetLastError();
+}
+
+template <int KI>
+hipError_t launch_dw_t(const FusedParams& p, int grid, hipStream_t st) {
+  switch ((p.emit ? 1 : 0) | (p.g.rin ? 2 : 0)) {
+    case 0: hipLaunchKernelGGL((fused_dw_kernel<KI, 0>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+    case 1: hipLaunchKernelGGL((fused_dw_kernel<KI, 1>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+    case 2: hipLaunchKernelGGL((fused_dw_kernel<KI, 2>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+    default: hipLaunchKernelGGL((fused_dw_kernel<KI, 3>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
   }
   return hipGetLastError();
 }
@@ -978,6 +1119,16 @@ int prepare_fused_t(const FusedParams& p) {
   const int b = prepare_kernel(fused_kernel<WM, WN, GM, 2>, p);
   const int c = p.emit ? std::min(prepare_kernel(fused_kernel<WM, WN, GM, 1>, p),
                                   prepare_kernel(fused_kernel<WM, WN, GM, 3>, p))
+                       : a;
+  return std::min(std::min(a, b), c);
+}
+
+template <int KI>
+int prepare_dw_t(const FusedParams& p) {
+  const int a = prepare_kernel(fused_dw_kernel<KI, 0>, p);
+  const int b = prepare_kernel(fused_dw_kernel<KI, 2>, p);
+  const int c = p.emit ? std::min(prepare_kernel(fused_dw_kernel<KI, 1>, p),
+                                  prepare_kernel(fused_dw_kernel<KI, 3>, p))
                        : a;
   return std::min(std::min(a, b), c);
 }
@@ -1029,6 +1180,15 @@ int fused_rb_kps(int ntiles_n, int ksteps, int halo_w, int chunks) {
   return 0;
 }
 
+// Halo rows per thread (one round) the depthwise kernel is built for: 4 or 6
+// (the smallest that covers the shape), 0 if neither does.
+int fused_dw_ki(int halo_w, int chunks) {
+  const int rw = halo_w * chunks;
+  if (rw > kThreads) return 0;
+  const int rows = (halo_w + kThreads / rw - 1) / (kThreads / rw);
+  return rows <= 4 ? 4 : (rows <= 6 ? 6 : 0);
+}
+
 // k-parts of the register-operand build `rb` (fused_rb_kps) for the LDS layout.
 int fused_rb_kparts(int rb) {
   const RbBuild& b = kRbBuilds[rb - 1];
@@ -1039,6 +1199,7 @@ int fused_rb_kparts(int rb) {
 // M-tile each; 16 x 16 tiles use 4 x 2 waves of 4 M-tiles each. WN = N-tiles
 // per wave = ntiles_n / 2.
 int prepare_fused(const FusedParams& p) {
+  if (p.dw) return p.dw == 4 ? prepare_dw_t<4>(p) : (p.dw == 6 ? prepare_dw_t<6>(p) : 0);
   if (p.rbk) {
     switch (p.rbk) {
       case 1: return prepare_rb_t<2, 2, 4, 2, 4>(p);
@@ -1074,6 +1235,7 @@ int prepare_fused(const FusedParams& p) {
 }
 
 hipError_t launch_fused(const FusedParams& p, int grid, hipStream_t st) {
+  if (p.dw) return p.dw == 4 ? launch_dw_t<4>(p, grid, st) : (p.dw == 6 ? launch_dw_t<6>(p, grid, st) : hipErrorInvalidValue);
   if (p.rbk) {
     switch (p.rbk) {
       case 1: return launch_rb_t<2, 2, 4, 2, 4>(p, grid, st);

@@ -186,7 +186,15 @@ struct FusedParams {
   float* r32;
   uint16_t* rb;
   uint8_t* prev_mask;      // blocks updated by the previous step
+  int dw;                  // depthwise kernel: its halo rows per thread (fused_dw_ki), 0: dense
 };
+
+// Depthwise fused kernel: channels per workgroup (the split) at most
+// kDwSplitMax, so 64 sites x kDwSplitMax / 4 pieces take kDwPieces per thread
+// of 512; its weights, k*k*split/4 float4, take kDwWeightLoads loads per thread.
+constexpr int kDwSplitMax = 64;
+constexpr int kDwPieces = 2;
+constexpr int kDwWeightLoads = 2;
 
 hipError_t launch_fused(const FusedParams& p, int grid, hipStream_t st);
 int prepare_fused(const FusedParams& p);  // create time: LDS attribute; workgroups per CU (0 on error)
@@ -199,6 +207,10 @@ hipError_t launch_fused_tiles(uint32_t* table, int grid, int tiles_y, int tiles_
 // k-parts whose partial sums that build keeps in LDS.
 int fused_rb_kps(int ntiles_n, int ksteps, int halo_w, int chunks);
 int fused_rb_kparts(int rb);
+// Depthwise fused kernel: halo rows per thread of the build covering a square
+// halo of halo_w pixels a side with `chunks` 8-channel chunks a pixel (4 or 6),
+// or 0 if none does.
+int fused_dw_ki(int halo_w, int chunks);
 
 hipError_t launch_gate(const GateParams& p, int dtype, int vec, int grid, size_t lds_bytes,
                        hipStream_t st);

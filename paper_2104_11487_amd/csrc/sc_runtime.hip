@@ -56,6 +56,7 @@ struct Geometry {
   int f_nsplit;         // workgroups per tile of the register-operand kernel (output channels split)
   int f_kc, f_nchunks, f_nbuf, f_mw, f_pstride, f_zero_pix, f_off_b, f_off_halo, f_off_a, f_lds;
   int f_rb;             // register-operand fused kernel: its build (0: LDS operand)
+  int f_dw;             // depthwise fused kernel: its halo rows per thread (0: not depthwise)
   int f_pstage, f_off_part;
   int vec;              // gate load width (elements)
   size_t elem;
@@ -308,6 +309,7 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
   // fused single-pass kernel: dense bf16, C_in % 32 == 0, tiles of <= 16 x 16
   // sites, output tiles split over two wave groups (ntn >= 2)
   G.fused = false;
+  G.f_dw = 0;
   if (!depthwise && d->dtype == SKIPCONV_BF16 && d->c_in % 32 == 0 && d->c_out % 4 == 0 && b <= 16 &&
       G.ntn >= 2 && !G.learned && !(d->flags & SKIPCONV_FLAG_SPLIT_PIPELINE)) {
     const int ts = b <= 8 ? b * (8 / b) : b;
@@ -356,6 +358,49 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
         G.f_off_part = (int)(b_bytes + halo_b + a_b);
         G.f_pstage = pstage;
         G.f_lds = (int)(b_bytes + halo_b + a_b + part_b);
+        G.f_tiles_y = (G.h_out + ts - 1) / ts;
+        G.f_tiles_x = (G.w_out + ts - 1) / ts;
+        G.f_grid = d->n * G.f_tiles_y * G.f_tiles_x;
+        if (G.f_tiles_x > 1024 || G.f_tiles_y > 1024 || d->n > 4096) G.fused = false;
+        G.f_copy_in_halo = halo_covers_owned(d->h, G.h_out, ts, G.f_tiles_y, s, pad, k) &&
+                           halo_covers_owned(d->w, G.w_out, ts, G.f_tiles_x, s, pad, k);
+      }
+    }
+  }
+  // fused single-pass depthwise kernel: bf16, C % 8 == 0, tiles of <= 8 x 8
+  // sites; the channels split over 2, 4 or 8 workgroups per tile until each
+  // owns at most kDwSplitMax; the halo taken in one round
+  if (depthwise && d->dtype == SKIPCONV_BF16 && d->c_in % 8 == 0 && b <= 8 && !G.learned &&
+      !(d->flags & SKIPCONV_FLAG_SPLIT_PIPELINE)) {
+    const int ts = b * (8 / b);
+    const int hh = (ts - 1) * s + k;
+    const int nchk = d->c_in / 8;
+    int nsplit = 1;
+    while (d->c_in / nsplit > sc::kDwSplitMax && nsplit < 8 && nchk % (2 * nsplit) == 0) nsplit *= 2;
+    const int ki = sc::fused_dw_ki(hh, nchk);
+    if (d->c_in / nsplit <= sc::kDwSplitMax && ki) {
+      const long pstride = 2L * d->c_in + 16;
+      const long w_b = ((long)k * k * (d->c_in / nsplit) * 4 + 15) / 16 * 16;
+      const long halo_b = ((long)hh * hh + 1) * pstride;
+      const long a_b = ((long)hh * hh * 4 + 15) / 16 * 16;
+      const int pstage = nchk | 1;
+      const long part_b = ((long)hh * hh * pstage * 4 + 15) / 16 * 16;
+      if (w_b + halo_b + a_b + part_b <= kFusedLdsLimit) {
+        G.fused = true;
+        G.f_dw = ki;
+        G.f_nsplit = nsplit;
+        G.f_ts = ts;
+        G.f_mw = 1;
+        G.f_rb = 0;
+        G.f_kc = G.f_nchunks = G.f_nbuf = 0;
+        G.f_pstride = (int)pstride;
+        G.f_zero_pix = hh * hh;
+        G.f_off_b = 0;
+        G.f_off_halo = (int)w_b;
+        G.f_off_a = (int)(w_b + halo_b);
+        G.f_off_part = (int)(w_b + halo_b + a_b);
+        G.f_pstage = pstage;
+        G.f_lds = (int)(w_b + halo_b + a_b + part_b);
         G.f_tiles_y = (G.h_out + ts - 1) / ts;
         G.f_tiles_x = (G.w_out + ts - 1) / ts;
         G.f_grid = d->n * G.f_tiles_y * G.f_tiles_x;
@@ -509,7 +554,8 @@ sc::FusedParams fused_params(skipconv_layer* h, const void* x_t, bool ref) {
   fp.nbuf = g.f_nbuf;
   fp.mw = g.f_mw;
   fp.rbk = g.f_rb;
-  fp.nsplit = g.f_rb ? g.f_nsplit : 1;
+  fp.nsplit = (g.f_rb || g.f_dw) ? g.f_nsplit : 1;
+  fp.dw = g.f_dw;
   fp.tiles = reinterpret_cast<const uint32_t*>(h->ws + g.off_ftiles);
   fp.inv_ts = 1.0f / (float)g.f_ts;
   fp.inv_blk = 1.0f / (float)d.block;
@@ -750,7 +796,7 @@ int skipconv_create(const skipconv_desc* d, const void* weights, void* workspace
   // workgroup; it wins while the frame has few tiles (latency regime) and the
   // split pipeline wins on large frames, where each kernel streams at its own
   // roofline. Threshold: four tiles per CU.
-  if (h->g.fused && (h->g.f_grid * (h->g.f_rb ? h->g.f_nsplit : 1) > 4 * h->num_cu ||
+  if (h->g.fused && (h->g.f_grid * ((h->g.f_rb || h->g.f_dw) ? h->g.f_nsplit : 1) > 4 * h->num_cu ||
                      sc::prepare_fused(fused_params(h, nullptr, true)) < 1))
     h->g.fused = false;
   if (g.dw_halo) {
@@ -1108,7 +1154,7 @@ int skipconv_activation(skipconv_t h, const void** y) {
 int skipconv_pipeline(skipconv_t h, int32_t* fused) {
   if (!h) return SKIPCONV_E_STATE;
   if (!fused) return SKIPCONV_E_INVALID_ARG;
-  *fused = h->g.fused ? (h->g.f_rb ? (h->g.f_nsplit > 1 ? 3 : 2) : 1) : 0;
+  *fused = h->g.fused ? (h->g.f_dw ? 4 : (h->g.f_rb ? (h->g.f_nsplit > 1 ? 3 : 2) : 1)) : 0;
   return SKIPCONV_OK;
 }
 

@@ -421,7 +421,8 @@ class SkipConv:
     @property
     def fused_variant(self) -> int:
         """0 split pipeline, 1 single-pass kernel with LDS weights, 2 with register weights,
-        3 with register weights and the output channels split over workgroups."""
+        3 with register weights and the output channels split over workgroups, 4 single-pass
+        depthwise kernel."""
         return skipconv_pipeline(self.handle)
 
     @property

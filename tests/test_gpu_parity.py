@@ -437,6 +437,13 @@ def test_pipeline_selection():
     wdw = to_device(weight_storage(syn.he_weights(64, 1, 3, seed=1), "bf16"), "bf16")
     assert S.SkipConv(wdw, n=1, h=32, w=32, block=8, groups=64).conv_kernel == 3
     assert S.SkipConv(wdw, n=1, h=32, w=32, block=1, groups=64).conv_kernel == 3
+    # depthwise bf16 layers with C % 8 == 0 and blocks <= 8 take the single-pass
+    # depthwise kernel; 16 x 16 blocks and SPLIT_PIPELINE keep the split pipeline
+    assert S.SkipConv(wdw, n=1, h=32, w=32, block=8, groups=64).fused_variant == 4
+    assert S.SkipConv(wdw, n=1, h=32, w=32, block=16, groups=64).fused_variant == 0
+    assert S.SkipConv(wdw, n=1, h=32, w=32, block=8, groups=64, split=True).fused_variant == 0
+    wdw192 = to_device(weight_storage(syn.he_weights(192, 1, 3, seed=1), "bf16"), "bf16")
+    assert S.SkipConv(wdw192, n=1, h=64, w=64, block=8, groups=192).fused_variant == 4
     wdw32 = to_device(weight_storage(syn.he_weights(64, 1, 3, seed=1), "f32"), "f32")
     assert S.SkipConv(wdw32, n=1, h=32, w=32, block=8, groups=64).conv_kernel == 2
 
@@ -678,6 +685,70 @@ def test_depthwise_halo(case):
         assert np.array_equal(y_bits, O.f32_to_bf16_rne(np.maximum(z, 0.0).astype(np.float32))), \
             f"{tag} t={t}: activation output"
     layer.close()
+
+
+# The single-pass depthwise kernel (bf16, C % 8 == 0, blocks <= 8): channel
+# splits of 1, 2 and 4 workgroups per tile, one-round halos of 4 and 6 rows a
+# thread, 1 x 1, 5 x 5 and 7 x 7 taps, stride 2, 8 channels (chunk sums staged
+# in LDS), edge tiles, and translated steps (split pipeline) between fused
+# ones: (n, h, w, c, k, stride, block, translated)
+FUSED_DW = [
+    (1, 37, 29, 192, 3, 1, 8, False),
+    (2, 40, 36, 64, 3, 2, 4, False),
+    (1, 33, 31, 32, 5, 1, 2, False),
+    (1, 30, 34, 128, 3, 1, 1, False),
+    (1, 26, 22, 8, 3, 1, 8, False),
+    (1, 21, 19, 96, 7, 1, 8, False),
+    (1, 35, 27, 48, 1, 1, 8, False),
+    (1, 30, 34, 64, 3, 1, 4, True),
+]
+
+
+@pytest.mark.parametrize("case", FUSED_DW, ids=[f"fdw{i}" for i in range(len(FUSED_DW))])
+def test_fused_depthwise(case):
+    """Single-pass depthwise kernel: statistic, masks and list bit-exact, z within tolerance after
+    every frame (reset mid-stream), activation output = bf16(relu(z)) bit for bit."""
+    n, h, w, c, k, s, b, translated = case
+    rng = np.random.Generator(np.random.PCG64(950 + c + k + b))
+    vid = syn.RectVideo(h, w, c, 7, seed=951 + c, batch=n, n_rect=3, side_lo=5, side_hi=14)
+    base = list(vid)
+    shifts = [(0, 0), (s, 0), (0, -s), (0, 0), (-s, 2 * s), (s, s), (0, 0)] if translated else [(0, 0)] * 7
+    frames, acc = [], (0, 0)
+    for f, d in zip(base, shifts):
+        acc = (acc[0] + d[0], acc[1] + d[1])
+        frames.append(O.translate(f, *acc) if translated else f)
+    wt = rng.normal(0, 0.3, (c, 1, k, k)).astype(np.float32)
+    pad = (k - 1) // 2
+    ho, wo = O.out_size(h, k, s, pad), O.out_size(w, k, s, pad)
+    stats = oracle_stats(base[:3], (c, c, k, k), dtype="bf16", stride=s)
+    eps = eps_for_density(stats, b, ho, wo, 0.4)
+    tag = f"fused depthwise {case}"
+    layer, orc = _layer_pair(wt, n=n, h=h, w=w, dtype="bf16", eps=eps, block=b, stride=s, groups=c,
+                             translate=translated, act_out="relu")
+    assert layer.fused_variant == 4, layer.fused_variant
+    dens = []
+    for t, (f, d) in enumerate(zip(frames, shifts)):
+        if t == 5:
+            layer.reset()
+            orc.reset()
+        xs = syn.to_storage(f, "bf16")
+        say(f"[{tag}] frame {t} shift={d} eps={eps:.4g}")
+        if translated:
+            layer.step_translated(to_device(xs, "bf16"), *d)
+            ref = orc.step(xs, shift=d)
+        else:
+            layer.step(to_device(xs, "bf16"))
+            ref = orc.step(xs)
+        compare_frame(layer, ref, "bf16", t=t, tag=tag, keep_stats=True)
+        z = layer._z.cpu().numpy()
+        y = layer.activation()
+        torch.cuda.synchronize()
+        y_bits = y.view(torch.int16).cpu().numpy().view(np.uint16).reshape(z.shape)
+        assert np.array_equal(y_bits, O.f32_to_bf16_rne(np.maximum(z, 0.0).astype(np.float32))), \
+            f"{tag} t={t}: activation output"
+        dens.append(ref["count"] / ref["block_mask"].size)
+    layer.close()
+    assert 0.0 < np.mean(dens[1:4]) < 1.0
 
 
 # One shape per build of the single-pass kernel whose waves hold their weight
