@@ -251,7 +251,10 @@ int skipconv_get_desc(skipconv_t h, skipconv_desc* d);
  * the output channels of each tile split over 2, 4 or 8 workgroups (shapes
  * built only for a share of the channels), 4 for the single-pass depthwise
  * kernel (bf16, C % 8 == 0, blocks of <= 8: per-channel products over the
- * taps, channels split over up to 8 workgroups per tile). Host only. */
+ * taps, channels split over up to 8 workgroups per tile), 5 for the
+ * single-pass kernel for few input channels (fp32 C_in <= 16 or bf16
+ * C_in < 8, C_out <= 64, blocks of <= 8: element halo loads, MFMA product
+ * with the residual operand gathered per k index). Host only. */
 int skipconv_pipeline(skipconv_t h, int32_t* fused);
 
 /* Gate tiling of the split pipeline: *ts = output sites per side of one gate

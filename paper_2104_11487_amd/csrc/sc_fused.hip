@@ -35,6 +35,8 @@
 //
 // The ordered global active list is not needed by this pipeline; it is
 // produced on demand for introspection by the compaction kernel.
+#include <type_traits>
+
 #include "sc_device.h"
 #include "sc_kernels.h"
 #include "sc_stream.h"
@@ -97,7 +99,7 @@ __device__ void emit_clear(const FusedParams& p, int n, int oy0, int ox0, int oh
       if (!clr[(ly / g.block) * nbx + lx / g.block]) continue;
       const size_t o = ((size_t)(n * g.h_out + oy0 + ly) * g.w_out + ox0 + lx) * p.c_out + col;
       *reinterpret_cast<floatx4*>(p.r32 + o) = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
-      *reinterpret_cast<uint2*>(p.rb + o) = uint2{0u, 0u};
+      if (p.rb) *reinterpret_cast<uint2*>(p.rb + o) = uint2{0u, 0u};  // bf16 layers
     }
   }
   for (int i = threadIdx.x; i < nby * nbx; i += kThreads) {
@@ -1065,6 +1067,256 @@ __global__ void __launch_bounds__(kThreads) fused_dw_kernel(FusedParams p) {
   if (EMIT && lead) emit_clear(p, T.n, T.oy0, T.ox0, T.oh, T.ow, T.tb_w, blk_flag, emit_clr);
 }
 
+// ---------------------------------------------------------------------------
+// Layers with few input channels (fp32 with C_in <= 16, bf16 with C_in < 8):
+// the shapes whose pixels are narrower than the 8-channel chunks above. The
+// halo is loaded in elements, VEC at a time (x_t, x_{t-1} and the x_t copy),
+// and r = x_t - x_{t-1} goes to LDS in fp32; one thread per halo pixel forms
+// its canonical statistic (8-channel chunk sums, then their sum); the gate is
+// gate_sites. The
+// product is formed transposed, weights as the MFMA A operand straight from
+// the packed buffer (fetched with the halo, held in registers), the residual
+// operand (fp32, or its bf16 rounding) gathered from the LDS halo per k index:
+// wave w takes the 16 sites of group w % 4 and k-part w / 4 of all output
+// tiles; k-part 1 hands its sums to k-part 0 through LDS, which adds them and
+// runs the epilogue. Before the gate's last barrier, as above. MODE as above
+// (an emitting fp32 layer hands on r = y_new - y_old in fp32 only).
+// VEC consecutive elements of a frame as raw bits (what the x_{t-1} copy
+// writes back) and as fp32 values.
+template <typename T, int VEC>
+struct ElemVec {
+  static constexpr int kBytes = (int)sizeof(T) * VEC;
+  using Raw = typename std::conditional<
+      kBytes == 16, uint4,
+      typename std::conditional<kBytes == 8, uint2,
+                                typename std::conditional<kBytes == 4, uint32_t, uint16_t>::type>::type>::type;
+  __device__ __forceinline__ static Raw load(const T* p, size_t i) { return *reinterpret_cast<const Raw*>(p + i); }
+  __device__ __forceinline__ static void store(T* p, size_t i, Raw r) { *reinterpret_cast<Raw*>(p + i) = r; }
+  __device__ __forceinline__ static void to_f32(Raw r, float* v) {
+    if constexpr (sizeof(T) == 4 && VEC == 1) {
+      v[0] = __uint_as_float(r);
+    } else if constexpr (sizeof(T) == 4) {
+      v[0] = __uint_as_float(r.x); v[1] = __uint_as_float(r.y);
+      v[2] = __uint_as_float(r.z); v[3] = __uint_as_float(r.w);
+    } else if constexpr (VEC == 1) {
+      v[0] = __uint_as_float((uint32_t)r << 16);
+    } else {
+      v[0] = __uint_as_float(r.x << 16); v[1] = __uint_as_float(r.x & 0xffff0000u);
+      v[2] = __uint_as_float(r.y << 16); v[3] = __uint_as_float(r.y & 0xffff0000u);
+    }
+  }
+};
+
+template <typename T, int VEC, int NTN, int MODE>
+__global__ void __launch_bounds__(kThreads) fused_sc_kernel(FusedParams p) {
+  constexpr bool EMIT = (MODE & 1) != 0;
+  constexpr bool CHAIN = (MODE & 2) != 0;
+  constexpr bool BF = sizeof(T) == 2;
+  constexpr int KSTEP = BF ? 32 : 4;  // k indices per MFMA step
+  constexpr int KS = BF ? kScStepsBf16 : kScStepsF32;  // k-steps per wave, at most
+  using WFrag = typename std::conditional<BF, bf16x8, float>::type;
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  __shared__ uint32_t blk_flag[kMaxTileBlocks];
+  __shared__ uint32_t tile_on;
+  __shared__ uint8_t emit_clr[kMaxTileBlocks];
+
+  const GateParams& g = p.g;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, kq = lane >> 4;
+  const Tile TL = make_tile(p, blockIdx.x);
+  if (CHAIN && g.up_mask && chain_skip<EMIT>(p, TL, emit_clr)) return;
+  float* rh = reinterpret_cast<float*>(lds + p.off_halo);  // [pixel][c] fp32 residual
+  float* a_halo = reinterpret_cast<float*>(lds + p.off_a);
+  floatx4* part = reinterpret_cast<floatx4*>(lds + p.off_b);  // [group][n-tile][lane]
+  const int c = g.c, kk = g.k * g.k * c;
+  const int wv = __builtin_amdgcn_readfirstlane(wave);
+  const int sg = wv & 3, kp = wv >> 2;
+  const int ks_lo = kp * p.ksteps / 2, nks = (kp + 1) * p.ksteps / 2 - ks_lo;
+
+  // 1. this wave's weight fragments, the halo loads (rounds of kScItems per
+  // thread) and the old z (and y) of the pieces k-part 0 stores: lane
+  // (r16, kq) of group sg holds channels 16 i + 4 kq .. + 3 of site sg*16 + r16
+  WFrag aw[KS][NTN];
+#pragma unroll
+  for (int st = 0; st < KS; ++st)
+#pragma unroll
+    for (int i = 0; i < NTN; ++i)
+      aw[st][i] = static_cast<const WFrag*>(p.wpack)[((size_t)(st < nks ? ks_lo + st : 0) * NTN + i) * 64 + lane];
+  const int q = sg * 16 + r16;  // site of this lane's column of the product
+  const int qy = q >> 3, qx = q & 7;  // tiles are at most 8 x 8 sites, laid out 8 wide here
+  const bool qok = qy < TL.oh && qx < TL.ow && qy < g.ts && qx < g.ts;
+  const int gsite = (TL.n * g.h_out + TL.oy0 + qy) * g.w_out + TL.ox0 + qx;
+  using YOld = typename std::conditional<BF, uint2, floatx4>::type;  // 4 channels of y
+  floatx4 zold[NTN];
+  YOld yold[NTN];
+#pragma unroll
+  for (int i = 0; i < NTN; ++i) {
+    const int col = 16 * i + 4 * kq;
+    const bool ok = kp == 0 && qok && col < p.c_out;
+    const size_t o = ok ? (size_t)gsite * p.c_out + col : 0;
+    zold[i] = *reinterpret_cast<const floatx4*>(p.z + o);
+    yold[i] = YOld{};
+    if (EMIT) yold[i] = *reinterpret_cast<const YOld*>(static_cast<const T*>(p.y) + o);
+  }
+  for (int i = threadIdx.x; i < kMaxTileBlocks; i += kThreads) blk_flag[i] = 0u;
+  if (threadIdx.x == 0) tile_on = 0u;
+
+  const int cv = c / VEC;  // loads per pixel
+  const int items = TL.npix * cv;
+  const float inv_cv = 1.0f / (float)cv;
+  const bool keep = g.x_keep != nullptr && g.copy_in_halo;
+  using EV = ElemVec<T, VEC>;
+  for (int base = 0; base < items; base += kThreads * kScItems) {
+    typename EV::Raw rt[kScItems], rp[kScItems];
+    float vc[CHAIN ? kScItems : 1][VEC];
+    int ro[kScItems];
+    bool in[kScItems], own[kScItems];
+    size_t off[kScItems];
+#pragma unroll
+    for (int u = 0; u < kScItems; ++u) {
+      const int it = base + u * kThreads + threadIdx.x;
+      const int px = qdiv(it, inv_cv), v = it - px * cv;
+      const int hy = qdiv(px, TL.inv_hw), hx = px - hy * TL.hw;
+      const int y = TL.iy0 + hy, x = TL.ix0 + hx;
+      in[u] = it < items && y >= 0 && y < g.h && x >= 0 && x < g.w;
+      own[u] = in[u] && keep && y >= TL.own_y0 && y < TL.own_y1 && x >= TL.own_x0 && x < TL.own_x1;
+      ro[u] = it < items ? px * c + v * VEC : -1;
+      off[u] = in[u] ? ((size_t)(TL.n * g.h + y) * g.w + x) * c + v * VEC : 0;
+      if constexpr (CHAIN) {  // fp32 residual input
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) vc[u][j] = static_cast<const float*>(g.x_t)[off[u] + j];
+      } else {
+        rt[u] = EV::load(static_cast<const T*>(g.x_t), off[u]);
+        rp[u] = EV::load(static_cast<const T*>(g.no_prev ? g.x_t : g.x_prev), off[u]);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kScItems; ++u) {
+      if (ro[u] < 0) continue;
+      float a[VEC], b[VEC];
+      if constexpr (CHAIN) {
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) a[j] = vc[u][j];
+      } else {
+        EV::to_f32(rt[u], a);
+        EV::to_f32(rp[u], b);
+      }
+#pragma unroll
+      for (int j = 0; j < VEC; ++j)
+        rh[ro[u] + j] = !in[u] ? 0.0f : ((CHAIN || g.no_prev) ? a[j] : __fsub_rn(a[j], b[j]));
+      if (!CHAIN && own[u]) EV::store(static_cast<T*>(g.x_keep), off[u], rt[u]);
+    }
+  }
+  if (!CHAIN && !g.copy_in_halo && g.x_keep) {  // pixels outside every halo (strides above the kernel)
+    const int ny = TL.own_y1 - TL.own_y0, nx = TL.own_x1 - TL.own_x0;
+    for (int i = threadIdx.x; i < ny * nx * c; i += kThreads) {
+      const int yy = i / (nx * c), e = i - yy * nx * c;
+      const size_t o = ((size_t)(TL.n * g.h + TL.own_y0 + yy) * g.w + TL.own_x0) * c + e;
+      static_cast<T*>(g.x_keep)[o] = static_cast<const T*>(g.x_t)[o];
+    }
+  }
+  lds_barrier();
+  // pixel statistic in the canonical order: terms of each 8-channel chunk
+  // added from +0 in ascending order, then the chunk sums in ascending order
+  for (int px = threadIdx.x; px < TL.npix; px += kThreads) {
+    float acc = 0.0f;
+    for (int j0 = 0; j0 < c; j0 += kChunk) {
+      float part = 0.0f;
+      for (int j = j0; j < min(c, j0 + kChunk); ++j) part = add_rn(part, term(rh[px * c + j], g.norm_p));
+      acc = add_rn(acc, part);
+    }
+    a_halo[px] = acc;
+  }
+  // 2. gate (its first barrier makes a_halo visible; the chunk sums are
+  // already combined)
+  ChunkMap cm;
+  cm.nchk = 1;
+  cm.total = TL.npix;
+  cm.lg = 0;
+  cm.inv = 1.0f;
+  cm.lane_sum = true;
+  gate_sites(p, TL, cm, a_halo, nullptr, blk_flag, &tile_on);
+
+  // 3. product over this wave's k-steps (the gate's outcome not yet needed)
+  floatx4 acc[NTN];
+#pragma unroll
+  for (int i = 0; i < NTN; ++i) acc[i] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+  {
+    const int pix0 = (qok ? qy : 0) * g.stride * TL.hw + (qok ? qx : 0) * g.stride;
+    const float inv_c = 1.0f / (float)c, inv_k = 1.0f / (float)g.k;
+#pragma unroll
+    for (int st = 0; st < KS; ++st) {
+      if (st >= nks) continue;  // wave-uniform
+      const int ks = ks_lo + st;
+      float bv[BF ? 8 : 1];
+#pragma unroll
+      for (int e = 0; e < (BF ? 8 : 1); ++e) {
+        const int kidx = ks * KSTEP + (BF ? kq * 8 + e : kq);
+        const int tap = qdiv(kidx, inv_c), ci = kidx - tap * c;
+        const int kh = qdiv(tap, inv_k), kw = tap - kh * g.k;
+        const float r = rh[(kidx < kk ? pix0 + kh * TL.hw + kw : 0) * c + (kidx < kk ? ci : 0)];
+        bv[e] = kidx < kk ? r : 0.0f;
+      }
+      if constexpr (BF) {
+        u32x4 qv;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) qv[e] = pack_bf16(bv[2 * e], bv[2 * e + 1]);
+        const bf16x8 b = __builtin_bit_cast(bf16x8, qv);
+#pragma unroll
+        for (int i = 0; i < NTN; ++i) acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aw[st][i], b, acc[i], 0, 0, 0);
+      } else {
+#pragma unroll
+        for (int i = 0; i < NTN; ++i) acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(aw[st][i], bv[0], acc[i], 0, 0, 0);
+      }
+    }
+  }
+  if (kp == 1) {
+#pragma unroll
+    for (int i = 0; i < NTN; ++i) part[(sg * NTN + i) * 64 + lane] = acc[i];
+  }
+  lds_barrier();
+  gate_flags(p, TL, blk_flag);
+  if (!tile_on) {
+    if (EMIT) emit_clear(p, TL.n, TL.oy0, TL.ox0, TL.oh, TL.ow, TL.tb_w, blk_flag, emit_clr);
+    return;
+  }
+
+  // 4. epilogue (k-part 0): part sums in part order, z at the active sites
+  if (kp == 0 && qok && blk_flag[qdiv(qy, TL.inv_blk) * TL.tb_w + qdiv(qx, TL.inv_blk)] != 0u) {
+#pragma unroll
+    for (int i = 0; i < NTN; ++i) {
+      const int col = 16 * i + 4 * kq;
+      if (col >= p.c_out) continue;
+      const floatx4 v = part[(sg * NTN + i) * 64 + lane];
+      floatx4 u;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) u[j] = acc[i][j] + v[j];
+      const size_t o = (size_t)gsite * p.c_out + col;
+      if constexpr (BF) {
+        store_piece<EMIT>(p, o, u, zold[i], yold[i]);
+      } else {
+        floatx4 nv;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) nv[j] = g.reference ? u[j] : zold[i][j] + u[j];
+        *reinterpret_cast<floatx4*>(p.z + o) = nv;
+        if (p.act) {
+          floatx4 a;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) a[j] = p.act == 2 ? fmaxf(nv[j], 0.0f) : nv[j];
+          *reinterpret_cast<floatx4*>(static_cast<float*>(p.y) + o) = a;
+          if (EMIT) {
+            floatx4 r;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) r[j] = __fsub_rn(a[j], yold[i][j]);
+            *reinterpret_cast<floatx4*>(p.r32 + o) = r;
+          }
+        }
+      }
+    }
+  }
+  if (EMIT) emit_clear(p, TL.n, TL.oy0, TL.ox0, TL.oh, TL.ow, TL.tb_w, blk_flag, emit_clr);
+}
+
 // ------------------------------------------------------------ launching --
 
 template <int WM, int WN, int GM>
@@ -1076,6 +1328,27 @@ hipError_t launch_fused_t(const FusedParams& p, int grid, hipStream_t st) {
     default: hipLaunchKernelGGL((fused_kernel<WM, WN, GM, 3>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
   }
   return hipGetLastError();
+}
+
+template <typename T, int VEC, int NTN>
+hipError_t launch_sc_t(const FusedParams& p, int grid, hipStream_t st) {
+  switch ((p.emit ? 1 : 0) | (p.g.rin ? 2 : 0)) {
+    case 0: hipLaunchKernelGGL((fused_sc_kernel<T, VEC, NTN, 0>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+    case 2: hipLaunchKernelGGL((fused_sc_kernel<T, VEC, NTN, 2>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+    case 1: hipLaunchKernelGGL((fused_sc_kernel<T, VEC, NTN, 1>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+    default: hipLaunchKernelGGL((fused_sc_kernel<T, VEC, NTN, 3>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+  }
+  return hipGetLastError();
+}
+
+template <typename T, int VEC>
+hipError_t launch_sc_n(const FusedParams& p, int grid, hipStream_t st) {
+  switch (p.ntiles_n) {
+    case 1: return launch_sc_t<T, VEC, 1>(p, grid, st);
+    case 2: return launch_sc_t<T, VEC, 2>(p, grid, st);
+    case 4: return launch_sc_t<T, VEC, 4>(p, grid, st);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 template <int KI>
@@ -1121,6 +1394,26 @@ int prepare_fused_t(const FusedParams& p) {
                                   prepare_kernel(fused_kernel<WM, WN, GM, 3>, p))
                        : a;
   return std::min(std::min(a, b), c);
+}
+
+template <typename T, int VEC, int NTN>
+int prepare_sc_t(const FusedParams& p) {
+  const int a = prepare_kernel(fused_sc_kernel<T, VEC, NTN, 0>, p);
+  const int b = prepare_kernel(fused_sc_kernel<T, VEC, NTN, 2>, p);
+  const int c = p.emit ? std::min(prepare_kernel(fused_sc_kernel<T, VEC, NTN, 1>, p),
+                                  prepare_kernel(fused_sc_kernel<T, VEC, NTN, 3>, p))
+                       : a;
+  return std::min(std::min(a, b), c);
+}
+
+template <typename T, int VEC>
+int prepare_sc_n(const FusedParams& p) {
+  switch (p.ntiles_n) {
+    case 1: return prepare_sc_t<T, VEC, 1>(p);
+    case 2: return prepare_sc_t<T, VEC, 2>(p);
+    case 4: return prepare_sc_t<T, VEC, 4>(p);
+    default: return 0;
+  }
 }
 
 template <int KI>
@@ -1199,6 +1492,10 @@ int fused_rb_kparts(int rb) {
 // M-tile each; 16 x 16 tiles use 4 x 2 waves of 4 M-tiles each. WN = N-tiles
 // per wave = ntiles_n / 2.
 int prepare_fused(const FusedParams& p) {
+  if (p.sc == 1) return prepare_sc_n<float, 1>(p);
+  if (p.sc == 4) return prepare_sc_n<float, 4>(p);
+  if (p.sc == 2) return prepare_sc_n<uint16_t, 1>(p);
+  if (p.sc) return 0;
   if (p.dw) return p.dw == 4 ? prepare_dw_t<4>(p) : (p.dw == 6 ? prepare_dw_t<6>(p) : 0);
   if (p.rbk) {
     switch (p.rbk) {
@@ -1235,6 +1532,10 @@ int prepare_fused(const FusedParams& p) {
 }
 
 hipError_t launch_fused(const FusedParams& p, int grid, hipStream_t st) {
+  if (p.sc == 1) return launch_sc_n<float, 1>(p, grid, st);
+  if (p.sc == 4) return launch_sc_n<float, 4>(p, grid, st);
+  if (p.sc == 2) return launch_sc_n<uint16_t, 1>(p, grid, st);
+  if (p.sc) return hipErrorInvalidValue;
   if (p.dw) return p.dw == 4 ? launch_dw_t<4>(p, grid, st) : (p.dw == 6 ? launch_dw_t<6>(p, grid, st) : hipErrorInvalidValue);
   if (p.rbk) {
     switch (p.rbk) {

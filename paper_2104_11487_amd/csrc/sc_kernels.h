@@ -187,7 +187,14 @@ struct FusedParams {
   uint16_t* rb;
   uint8_t* prev_mask;      // blocks updated by the previous step
   int dw;                  // depthwise kernel: its halo rows per thread (fused_dw_ki), 0: dense
+  int sc;                  // few-channel kernel: 1 fp32 by elements, 4 fp32 by 4, 2 bf16; 0: none
 };
+
+// Few-channel fused kernel (fp32 C_in <= 16, bf16 C_in < 8): halo loads in
+// flight per thread per round, and k-steps per wave at most (two k-parts).
+constexpr int kScItems = 2;
+constexpr int kScStepsF32 = 24;
+constexpr int kScStepsBf16 = 6;
 
 // Depthwise fused kernel: channels per workgroup (the split) at most
 // kDwSplitMax, so 64 sites x kDwSplitMax / 4 pieces take kDwPieces per thread

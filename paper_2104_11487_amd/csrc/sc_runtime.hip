@@ -57,6 +57,7 @@ struct Geometry {
   int f_kc, f_nchunks, f_nbuf, f_mw, f_pstride, f_zero_pix, f_off_b, f_off_halo, f_off_a, f_lds;
   int f_rb;             // register-operand fused kernel: its build (0: LDS operand)
   int f_dw;             // depthwise fused kernel: its halo rows per thread (0: not depthwise)
+  int f_sc;             // few-channel fused kernel: 1 fp32 by elements, 4 fp32 by 4, 2 bf16 (0: none)
   int f_pstage, f_off_part;
   int vec;              // gate load width (elements)
   size_t elem;
@@ -310,6 +311,7 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
   // sites, output tiles split over two wave groups (ntn >= 2)
   G.fused = false;
   G.f_dw = 0;
+  G.f_sc = 0;
   if (!depthwise && d->dtype == SKIPCONV_BF16 && d->c_in % 32 == 0 && d->c_out % 4 == 0 && b <= 16 &&
       G.ntn >= 2 && !G.learned && !(d->flags & SKIPCONV_FLAG_SPLIT_PIPELINE)) {
     const int ts = b <= 8 ? b * (8 / b) : b;
@@ -365,6 +367,42 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
         G.f_copy_in_halo = halo_covers_owned(d->h, G.h_out, ts, G.f_tiles_y, s, pad, k) &&
                            halo_covers_owned(d->w, G.w_out, ts, G.f_tiles_x, s, pad, k);
       }
+    }
+  }
+  // fused single-pass kernel for few input channels (fp32 C_in <= 16, bf16
+  // C_in < 8): tiles of <= 8 x 8 sites, C_out <= 64, two k-parts of at most
+  // kScStepsF32 (kScStepsBf16) k-steps
+  const bool few = d->dtype == SKIPCONV_F32 ? d->c_in <= 16 : d->c_in < 8;
+  if (!depthwise && few && d->c_out % 4 == 0 && G.ntn >= 1 && G.ntn <= 4 && G.ntn != 3 && b <= 8 &&
+      !G.learned && !(d->flags & SKIPCONV_FLAG_SPLIT_PIPELINE) &&
+      (G.ksteps + 1) / 2 <= (d->dtype == SKIPCONV_F32 ? sc::kScStepsF32 : sc::kScStepsBf16)) {
+    const int ts = b * (8 / b);
+    const int hh = (ts - 1) * s + k;
+    const long rh_b = ((long)hh * hh * d->c_in * 4 + 15) / 16 * 16;
+    const long a_b = ((long)hh * hh * 4 + 15) / 16 * 16;
+    const long part_b = 4L * G.ntn * 64 * 16;
+    if (rh_b + a_b + part_b <= kFusedLdsLimit) {
+      G.fused = true;
+      G.f_sc = d->dtype == SKIPCONV_BF16 ? 2 : (d->c_in % 4 == 0 ? 4 : 1);
+      G.f_nsplit = 1;
+      G.f_ts = ts;
+      G.f_mw = 1;
+      G.f_rb = 0;
+      G.f_kc = G.f_nchunks = G.f_nbuf = 0;
+      G.f_pstride = 0;
+      G.f_zero_pix = hh * hh;
+      G.f_off_b = 0;
+      G.f_off_halo = (int)part_b;
+      G.f_off_a = (int)(part_b + rh_b);
+      G.f_off_part = G.f_off_a;
+      G.f_pstage = 1;
+      G.f_lds = (int)(part_b + rh_b + a_b);
+      G.f_tiles_y = (G.h_out + ts - 1) / ts;
+      G.f_tiles_x = (G.w_out + ts - 1) / ts;
+      G.f_grid = d->n * G.f_tiles_y * G.f_tiles_x;
+      if (G.f_tiles_x > 1024 || G.f_tiles_y > 1024 || d->n > 4096) G.fused = false;
+      G.f_copy_in_halo = halo_covers_owned(d->h, G.h_out, ts, G.f_tiles_y, s, pad, k) &&
+                         halo_covers_owned(d->w, G.w_out, ts, G.f_tiles_x, s, pad, k);
     }
   }
   // fused single-pass depthwise kernel: bf16, C % 8 == 0, tiles of <= 8 x 8
@@ -547,7 +585,7 @@ sc::FusedParams fused_params(skipconv_layer* h, const void* x_t, bool ref) {
   fp.act = d.act_out;
   fp.emit = h->emits() ? 1 : 0;  // the epilogue also writes the successor's residual
   fp.r32 = h->r32();
-  fp.rb = h->rb();
+  fp.rb = d.dtype == SKIPCONV_BF16 ? h->rb() : nullptr;  // the bf16 rounding of r: bf16 layers only
   fp.prev_mask = h->prev_mask();
   fp.kc = g.f_kc;
   fp.nchunks = g.f_nchunks;
@@ -556,6 +594,7 @@ sc::FusedParams fused_params(skipconv_layer* h, const void* x_t, bool ref) {
   fp.rbk = g.f_rb;
   fp.nsplit = (g.f_rb || g.f_dw) ? g.f_nsplit : 1;
   fp.dw = g.f_dw;
+  fp.sc = g.f_sc;
   fp.tiles = reinterpret_cast<const uint32_t*>(h->ws + g.off_ftiles);
   fp.inv_ts = 1.0f / (float)g.f_ts;
   fp.inv_blk = 1.0f / (float)d.block;
@@ -1154,7 +1193,7 @@ int skipconv_activation(skipconv_t h, const void** y) {
 int skipconv_pipeline(skipconv_t h, int32_t* fused) {
   if (!h) return SKIPCONV_E_STATE;
   if (!fused) return SKIPCONV_E_INVALID_ARG;
-  *fused = h->g.fused ? (h->g.f_dw ? 4 : (h->g.f_rb ? (h->g.f_nsplit > 1 ? 3 : 2) : 1)) : 0;
+  *fused = h->g.fused ? (h->g.f_sc ? 5 : (h->g.f_dw ? 4 : (h->g.f_rb ? (h->g.f_nsplit > 1 ? 3 : 2) : 1))) : 0;
   return SKIPCONV_OK;
 }
 

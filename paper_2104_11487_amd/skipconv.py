@@ -422,7 +422,7 @@ class SkipConv:
     def fused_variant(self) -> int:
         """0 split pipeline, 1 single-pass kernel with LDS weights, 2 with register weights,
         3 with register weights and the output channels split over workgroups, 4 single-pass
-        depthwise kernel."""
+        depthwise kernel, 5 single-pass kernel for few input channels."""
         return skipconv_pipeline(self.handle)
 
     @property

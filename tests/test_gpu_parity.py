@@ -407,8 +407,14 @@ def test_pipeline_selection():
     assert not S.SkipConv(w, n=4, h=512, w=512, block=16).fused
     w16 = to_device(weight_storage(syn.he_weights(16, 64, 3, seed=1), "bf16"), "bf16")
     assert not S.SkipConv(w16, n=1, h=32, w=32, block=8).fused
+    # few input channels (bf16 C_in < 8, fp32 C_in <= 16; C_out <= 64, blocks <= 8):
+    # the single-pass kernel with element halo loads
     w3 = to_device(weight_storage(syn.he_weights(64, 3, 3, seed=1), "bf16"), "bf16")
-    assert not S.SkipConv(w3, n=1, h=32, w=32, block=1).fused
+    assert S.SkipConv(w3, n=1, h=32, w=32, block=1).fused_variant == 5
+    assert S.SkipConv(w3, n=1, h=32, w=32, block=16).fused_variant == 0
+    wf16 = to_device(weight_storage(syn.he_weights(16, 16, 3, seed=1), "f32"), "f32")
+    assert S.SkipConv(wf16, n=1, h=32, w=32, block=1).fused_variant == 5
+    assert S.SkipConv(wf16, n=1, h=32, w=32, block=1, split=True).fused_variant == 0
     # 8 x 8 tiles take the variant whose waves hold their weight fragments in
     # registers where it is built for the shape (64 -> 64, 3 x 3: K = 576);
     # larger K and 16 x 16 tiles stage the weights in LDS
@@ -746,6 +752,75 @@ def test_fused_depthwise(case):
         y_bits = y.view(torch.int16).cpu().numpy().view(np.uint16).reshape(z.shape)
         assert np.array_equal(y_bits, O.f32_to_bf16_rne(np.maximum(z, 0.0).astype(np.float32))), \
             f"{tag} t={t}: activation output"
+        dens.append(ref["count"] / ref["block_mask"].size)
+    layer.close()
+    assert 0.0 < np.mean(dens[1:4]) < 1.0
+
+
+# The single-pass kernel for few input channels (fp32 C_in <= 16, bf16
+# C_in < 8): element-wise (C_in % 4 != 0) and 4-wide halo loads, 1 x 1 to
+# 7 x 7 taps, stride 2 (a 1 x 1 stride-2 layer copies pixels outside every
+# halo), 6 x 6 tiles (b = 3), 16 to 64 output channels (48: a masked output
+# tile), edge tiles, translated steps between fused ones:
+# (n, h, w, c_in, c_out, k, stride, block, dtype, translated)
+FUSED_FEW = [
+    (1, 37, 29, 3, 32, 3, 1, 1, "bf16", False),
+    (2, 30, 26, 5, 16, 5, 2, 2, "bf16", False),
+    (1, 33, 35, 7, 64, 3, 1, 4, "bf16", False),
+    (1, 30, 30, 4, 48, 1, 2, 2, "bf16", False),
+    (1, 28, 36, 12, 16, 3, 1, 1, "f32", False),
+    (1, 29, 31, 6, 32, 3, 2, 8, "f32", False),
+    (1, 40, 24, 1, 16, 7, 1, 3, "f32", False),
+    (1, 32, 28, 3, 16, 3, 1, 4, "bf16", True),
+]
+
+
+@pytest.mark.parametrize("case", FUSED_FEW, ids=[f"few{i}" for i in range(len(FUSED_FEW))])
+def test_fused_few_channels(case):
+    """Single-pass kernel for few input channels: statistic, masks and list bit-exact, z within
+    tolerance after every frame (reset mid-stream), activation output = relu(z) in the layer dtype."""
+    n, h, w, ci, co, k, s, b, dtype, translated = case
+    rng = np.random.Generator(np.random.PCG64(970 + ci + k + b))
+    vid = syn.RectVideo(h, w, ci, 7, seed=971 + ci, batch=n, n_rect=3, side_lo=5, side_hi=14)
+    base = list(vid)
+    shifts = [(0, 0), (s, 0), (0, -s), (0, 0), (-s, 2 * s), (s, s), (0, 0)] if translated else [(0, 0)] * 7
+    frames, acc = [], (0, 0)
+    for f, d in zip(base, shifts):
+        acc = (acc[0] + d[0], acc[1] + d[1])
+        frames.append(O.translate(f, *acc) if translated else f)
+    wt = rng.normal(0, 0.3, (co, ci, k, k)).astype(np.float32)
+    pad = (k - 1) // 2
+    ho, wo = O.out_size(h, k, s, pad), O.out_size(w, k, s, pad)
+    stats = oracle_stats(base[:3], wt.shape, dtype=dtype, stride=s)
+    eps = eps_for_density(stats, b, ho, wo, 0.4)
+    tag = f"few channels {case}"
+    layer, orc = _layer_pair(wt, n=n, h=h, w=w, dtype=dtype, eps=eps, block=b, stride=s,
+                             translate=translated, act_out="relu")
+    assert layer.fused_variant == 5, layer.fused_variant
+    dens = []
+    for t, (f, d) in enumerate(zip(frames, shifts)):
+        if t == 5:
+            layer.reset()
+            orc.reset()
+        xs = syn.to_storage(f, dtype)
+        say(f"[{tag}] frame {t} shift={d} eps={eps:.4g}")
+        if translated:
+            layer.step_translated(to_device(xs, dtype), *d)
+            ref = orc.step(xs, shift=d)
+        else:
+            layer.step(to_device(xs, dtype))
+            ref = orc.step(xs)
+        compare_frame(layer, ref, dtype, t=t, tag=tag, keep_stats=True)
+        z = layer._z.cpu().numpy()
+        y = layer.activation()
+        torch.cuda.synchronize()
+        relu = np.maximum(z, 0.0).astype(np.float32)
+        if dtype == "bf16":
+            y_bits = y.view(torch.int16).cpu().numpy().view(np.uint16).reshape(z.shape)
+            assert np.array_equal(y_bits, O.f32_to_bf16_rne(relu)), f"{tag} t={t}: activation output"
+        else:
+            assert np.array_equal(y.cpu().numpy().reshape(z.shape).view(np.uint32), relu.view(np.uint32)), \
+                f"{tag} t={t}: activation output"
         dens.append(ref["count"] / ref["block_mask"].size)
     layer.close()
     assert 0.0 < np.mean(dens[1:4]) < 1.0
