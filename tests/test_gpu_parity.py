@@ -844,6 +844,7 @@ FUSED_SHAPES = [
     (1, 30, 26, 128, 128, 3, 1, 8, 3),
     (2, 27, 21, 128, 128, 3, 1, 4, 3),
     (1, 40, 36, 64, 64, 3, 1, 16, 1),
+    (1, 40, 36, 128, 128, 3, 1, 16, 1),
 ]
 
 
