@@ -1456,6 +1456,7 @@ constexpr RbBuild kRbBuilds[] = {
     {2, 2, 4, 2, 4}, {2, 2, 4, 3, 4}, {4, 2, 4, 3, 4}, {4, 2, 4, 5, 4}, {8, 2, 4, 9, 4}, {12, 2, 4, 6, 4},
     {2, 2, 4, 5, 4},  // a quarter of 128 output channels at K = 1152 (3 x 3, C_in = 128)
     {8, 2, 4, 9, 6},  // stride 2, 64 -> 128: a 17 x 17 halo of 8 chunks a pixel
+    {6, 2, 4, 3, 4},  // half of 192 output channels at K = 192 (1 x 1, C_in = 192) on small frames
 };
 }  // namespace
 
@@ -1507,6 +1508,7 @@ int prepare_fused(const FusedParams& p) {
       case 6: return prepare_rb_t<12, 2, 4, 6, 4>(p);
       case 7: return prepare_rb_t<2, 2, 4, 5, 4>(p);
       case 8: return prepare_rb_t<8, 2, 4, 9, 6>(p);
+      case 9: return prepare_rb_t<6, 2, 4, 3, 4>(p);
       default: return 0;
     }
   }
@@ -1547,6 +1549,7 @@ hipError_t launch_fused(const FusedParams& p, int grid, hipStream_t st) {
       case 6: return launch_rb_t<12, 2, 4, 6, 4>(p, grid, st);
       case 7: return launch_rb_t<2, 2, 4, 5, 4>(p, grid, st);
       case 8: return launch_rb_t<8, 2, 4, 9, 6>(p, grid, st);
+      case 9: return launch_rb_t<6, 2, 4, 3, 4>(p, grid, st);
       default: return hipErrorInvalidValue;
     }
   }

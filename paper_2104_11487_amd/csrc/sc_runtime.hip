@@ -22,6 +22,7 @@ constexpr size_t kLdsLimit = 60 * 1024;  // dynamic; the gate kernel adds 2 KB s
 constexpr int kMaxCout = 256;
 constexpr long kHaloLdsLimit = 160 * 1024;  // LDS of one gfx950 CU
 constexpr long kFusedLdsLimit = 156 * 1024; // dynamic LDS of the fused kernel (+ ~3 KB static)
+constexpr long kCuGuess = 256;              // CUs assumed when a tiling is chosen before the device is queried
 
 // Does every tile's halo contain the input pixels the tile owns?
 int halo_covers_owned(int n_in, int n_out, int ts, int tiles, int s, int pad, int k) {
@@ -329,12 +330,22 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
       // tiles of <= 8 x 8 sites: register-operand kernel when instantiated for
       // the shape; LDS holds the partial sums of its k-parts instead of weights
       int rb = mw == 1 ? sc::fused_rb_kps(G.ntn, G.ksteps, hh, d->c_in / 8) : 0;
-      // no build for the whole width: the output channels split over 2, 4 or
-      // 8 workgroups per tile, each a build for its share (fewer k-steps per
-      // wave, so the weight fragments still fit in registers)
+      // no build for the whole width, or a wide layer (>= 192 output
+      // channels) with too few tiles to occupy half the CUs: the output
+      // channels split over 2, 4 or 8 workgroups per tile, each a build for
+      // its share (fewer k-steps per wave, so the weight fragments still fit
+      // in registers; fewer epilogue pieces per thread)
+      const long tiles = (long)d->n * ((G.h_out + ts - 1) / ts) * ((G.w_out + ts - 1) / ts);
+      const bool wide_few = G.ntn >= 12 && tiles * 2 < kCuGuess;
       int nsplit = 1;
-      for (int sp = 2; mw == 1 && !rb && sp <= 8; sp *= 2)
-        if (G.ntn % sp == 0 && (rb = sc::fused_rb_kps(G.ntn / sp, G.ksteps, hh, d->c_in / 8)) != 0) nsplit = sp;
+      for (int sp = 2; mw == 1 && (!rb || wide_few) && sp <= 8; sp *= 2) {
+        const int r = G.ntn % sp == 0 ? sc::fused_rb_kps(G.ntn / sp, G.ksteps, hh, d->c_in / 8) : 0;
+        if (r) {
+          rb = r;
+          nsplit = sp;
+          break;
+        }
+      }
       G.f_nsplit = nsplit;
       if (rb) {
         const long kparts = sc::fused_rb_kparts(rb);
