@@ -1457,6 +1457,7 @@ constexpr RbBuild kRbBuilds[] = {
     {2, 2, 4, 5, 4},  // a quarter of 128 output channels at K = 1152 (3 x 3, C_in = 128)
     {8, 2, 4, 9, 6},  // stride 2, 64 -> 128: a 17 x 17 halo of 8 chunks a pixel
     {6, 2, 4, 3, 4},  // half of 192 output channels at K = 192 (1 x 1, C_in = 192) on small frames
+    {4, 2, 4, 5, 6},  // half of 128 output channels, stride 2 (17 x 17 halo) on small frames
 };
 }  // namespace
 
@@ -1509,6 +1510,7 @@ int prepare_fused(const FusedParams& p) {
       case 7: return prepare_rb_t<2, 2, 4, 5, 4>(p);
       case 8: return prepare_rb_t<8, 2, 4, 9, 6>(p);
       case 9: return prepare_rb_t<6, 2, 4, 3, 4>(p);
+      case 10: return prepare_rb_t<4, 2, 4, 5, 6>(p);
       default: return 0;
     }
   }
@@ -1550,6 +1552,7 @@ hipError_t launch_fused(const FusedParams& p, int grid, hipStream_t st) {
       case 7: return launch_rb_t<2, 2, 4, 5, 4>(p, grid, st);
       case 8: return launch_rb_t<8, 2, 4, 9, 6>(p, grid, st);
       case 9: return launch_rb_t<6, 2, 4, 3, 4>(p, grid, st);
+      case 10: return launch_rb_t<4, 2, 4, 5, 6>(p, grid, st);
       default: return hipErrorInvalidValue;
     }
   }

@@ -330,13 +330,15 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
       // tiles of <= 8 x 8 sites: register-operand kernel when instantiated for
       // the shape; LDS holds the partial sums of its k-parts instead of weights
       int rb = mw == 1 ? sc::fused_rb_kps(G.ntn, G.ksteps, hh, d->c_in / 8) : 0;
-      // no build for the whole width, or a wide layer (>= 192 output
-      // channels) with too few tiles to occupy half the CUs: the output
+      // no build for the whole width, or a wide layer with few tiles (>= 192
+      // output channels and fewer tiles than half the CUs, or >= 128 and
+      // fewer than a quarter; narrower layers and more tiles measured slower
+      // split, e.g. 64 -> 64 on 192 tiles: 7.1 -> 10.5 us): the output
       // channels split over 2, 4 or 8 workgroups per tile, each a build for
       // its share (fewer k-steps per wave, so the weight fragments still fit
       // in registers; fewer epilogue pieces per thread)
       const long tiles = (long)d->n * ((G.h_out + ts - 1) / ts) * ((G.w_out + ts - 1) / ts);
-      const bool wide_few = G.ntn >= 12 && tiles * 2 < kCuGuess;
+      const bool wide_few = (G.ntn >= 12 && tiles * 2 < kCuGuess) || (G.ntn >= 8 && tiles * 4 < kCuGuess);
       int nsplit = 1;
       for (int sp = 2; mw == 1 && (!rb || wide_few) && sp <= 8; sp *= 2) {
         const int r = G.ntn % sp == 0 ? sc::fused_rb_kps(G.ntn / sp, G.ksteps, hh, d->c_in / 8) : 0;

@@ -836,12 +836,14 @@ FUSED_SHAPES = [
     (1, 36, 44, 64, 32, 3, 1, 4, 2),
     (1, 29, 37, 32, 64, 3, 1, 8, 2),
     (2, 24, 40, 64, 64, 3, 1, 2, 2),
-    (1, 36, 28, 64, 128, 3, 1, 8, 2),
+    (1, 36, 28, 64, 128, 3, 1, 8, 3),
+    (1, 72, 72, 64, 128, 3, 1, 8, 2),
     (1, 96, 96, 192, 192, 1, 1, 8, 2),
     (1, 27, 21, 192, 192, 1, 1, 8, 3),
     (1, 40, 34, 32, 64, 3, 2, 1, 2),
     (1, 22, 26, 64, 64, 3, 1, 3, 2),
-    (1, 36, 42, 64, 128, 3, 2, 8, 2),
+    (1, 36, 42, 64, 128, 3, 2, 8, 3),
+    (1, 136, 120, 64, 128, 3, 2, 8, 2),
     (1, 30, 26, 128, 128, 3, 1, 8, 3),
     (2, 27, 21, 128, 128, 3, 1, 4, 3),
     (1, 40, 36, 64, 64, 3, 1, 16, 1),
