@@ -1107,13 +1107,15 @@ struct ElemVec {
   }
 };
 
-template <typename T, int VEC, int NTN, int MODE>
+// KS: k-steps per wave at most (the weight fragments held in registers; a
+// one-step build for the smallest K keeps the kernel's registers low enough
+// for four workgroups per CU).
+template <typename T, int VEC, int NTN, int MODE, int KS>
 __global__ void __launch_bounds__(kThreads) fused_sc_kernel(FusedParams p) {
   constexpr bool EMIT = (MODE & 1) != 0;
   constexpr bool CHAIN = (MODE & 2) != 0;
   constexpr bool BF = sizeof(T) == 2;
   constexpr int KSTEP = BF ? 32 : 4;  // k indices per MFMA step
-  constexpr int KS = BF ? kScStepsBf16 : kScStepsF32;  // k-steps per wave, at most
   using WFrag = typename std::conditional<BF, bf16x8, float>::type;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   __shared__ uint32_t blk_flag[kMaxTileBlocks];
@@ -1330,23 +1332,31 @@ hipError_t launch_fused_t(const FusedParams& p, int grid, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <typename T, int VEC, int NTN>
+template <typename T, int VEC, int NTN, int KS>
 hipError_t launch_sc_t(const FusedParams& p, int grid, hipStream_t st) {
   switch ((p.emit ? 1 : 0) | (p.g.rin ? 2 : 0)) {
-    case 0: hipLaunchKernelGGL((fused_sc_kernel<T, VEC, NTN, 0>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
-    case 2: hipLaunchKernelGGL((fused_sc_kernel<T, VEC, NTN, 2>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
-    case 1: hipLaunchKernelGGL((fused_sc_kernel<T, VEC, NTN, 1>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
-    default: hipLaunchKernelGGL((fused_sc_kernel<T, VEC, NTN, 3>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+    case 0: hipLaunchKernelGGL((fused_sc_kernel<T, VEC, NTN, 0, KS>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+    case 2: hipLaunchKernelGGL((fused_sc_kernel<T, VEC, NTN, 2, KS>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+    case 1: hipLaunchKernelGGL((fused_sc_kernel<T, VEC, NTN, 1, KS>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+    default: hipLaunchKernelGGL((fused_sc_kernel<T, VEC, NTN, 3, KS>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
   }
   return hipGetLastError();
+}
+
+// k-steps per wave of the build: fp32 kScStepsF32; bf16 1 when the layer
+// has at most two k-steps, else kScStepsBf16
+template <typename T, int VEC, int NTN>
+hipError_t launch_sc_k(const FusedParams& p, int grid, hipStream_t st) {
+  if constexpr (sizeof(T) == 4) return launch_sc_t<T, VEC, NTN, kScStepsF32>(p, grid, st);
+  else return p.ksteps <= 2 ? launch_sc_t<T, VEC, NTN, 1>(p, grid, st) : launch_sc_t<T, VEC, NTN, kScStepsBf16>(p, grid, st);
 }
 
 template <typename T, int VEC>
 hipError_t launch_sc_n(const FusedParams& p, int grid, hipStream_t st) {
   switch (p.ntiles_n) {
-    case 1: return launch_sc_t<T, VEC, 1>(p, grid, st);
-    case 2: return launch_sc_t<T, VEC, 2>(p, grid, st);
-    case 4: return launch_sc_t<T, VEC, 4>(p, grid, st);
+    case 1: return launch_sc_k<T, VEC, 1>(p, grid, st);
+    case 2: return launch_sc_k<T, VEC, 2>(p, grid, st);
+    case 4: return launch_sc_k<T, VEC, 4>(p, grid, st);
     default: return hipErrorInvalidValue;
   }
 }
@@ -1396,22 +1406,28 @@ int prepare_fused_t(const FusedParams& p) {
   return std::min(std::min(a, b), c);
 }
 
-template <typename T, int VEC, int NTN>
+template <typename T, int VEC, int NTN, int KS>
 int prepare_sc_t(const FusedParams& p) {
-  const int a = prepare_kernel(fused_sc_kernel<T, VEC, NTN, 0>, p);
-  const int b = prepare_kernel(fused_sc_kernel<T, VEC, NTN, 2>, p);
-  const int c = p.emit ? std::min(prepare_kernel(fused_sc_kernel<T, VEC, NTN, 1>, p),
-                                  prepare_kernel(fused_sc_kernel<T, VEC, NTN, 3>, p))
+  const int a = prepare_kernel(fused_sc_kernel<T, VEC, NTN, 0, KS>, p);
+  const int b = prepare_kernel(fused_sc_kernel<T, VEC, NTN, 2, KS>, p);
+  const int c = p.emit ? std::min(prepare_kernel(fused_sc_kernel<T, VEC, NTN, 1, KS>, p),
+                                  prepare_kernel(fused_sc_kernel<T, VEC, NTN, 3, KS>, p))
                        : a;
   return std::min(std::min(a, b), c);
+}
+
+template <typename T, int VEC, int NTN>
+int prepare_sc_k(const FusedParams& p) {
+  if constexpr (sizeof(T) == 4) return prepare_sc_t<T, VEC, NTN, kScStepsF32>(p);
+  else return p.ksteps <= 2 ? prepare_sc_t<T, VEC, NTN, 1>(p) : prepare_sc_t<T, VEC, NTN, kScStepsBf16>(p);
 }
 
 template <typename T, int VEC>
 int prepare_sc_n(const FusedParams& p) {
   switch (p.ntiles_n) {
-    case 1: return prepare_sc_t<T, VEC, 1>(p);
-    case 2: return prepare_sc_t<T, VEC, 2>(p);
-    case 4: return prepare_sc_t<T, VEC, 4>(p);
+    case 1: return prepare_sc_k<T, VEC, 1>(p);
+    case 2: return prepare_sc_k<T, VEC, 2>(p);
+    case 4: return prepare_sc_k<T, VEC, 4>(p);
     default: return 0;
   }
 }
