@@ -513,8 +513,9 @@ def test_large_gate_tiles(case):
 
 # Caller-retained frames (x_{t-1} read from the previous step's buffer, no
 # copy written): fused and split pipelines, fp32 and bf16, fewer than 8
-# channels, a 1 x 1 stride-2 layer (pixels outside every halo) and translated
-# steps. (n, h, w, c_in, c_out, k, stride, block, dtype, split, translated)
+# channels (split, and the few-channel fused kernel), a 1 x 1 stride-2 layer
+# (pixels outside every halo) and translated steps.
+# (n, h, w, c_in, c_out, k, stride, block, dtype, split, translated)
 RETAINS = [
     (1, 40, 36, 64, 64, 3, 1, 8, "bf16", False, False),
     (2, 33, 29, 64, 128, 3, 1, 4, "bf16", True, False),
@@ -522,6 +523,8 @@ RETAINS = [
     (1, 32, 32, 16, 16, 3, 1, 1, "f32", False, False),
     (1, 30, 30, 32, 64, 1, 2, 2, "bf16", False, False),
     (1, 36, 40, 64, 64, 3, 2, 8, "bf16", True, True),
+    (1, 26, 30, 3, 32, 3, 1, 1, "bf16", False, False),
+    (1, 22, 26, 6, 16, 3, 2, 2, "f32", False, False),
 ]
 
 
