@@ -1,18 +1,24 @@
 """Benchmark of the streaming Skip-Conv layer on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload rect64|blob128|square16]
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+                    [--workload blob128|rect64|square16|stack6|mbconv192]
 
-One step = one call of skipconv_step on one batch (the whole hot path: gate
-kernel + sparse convolution kernel) over a frame of the synthetic clip; the
-clip repeats with a reset (dense reference frame) at its first frame. Inputs
-are resident in HBM before the timed region. Prints one JSON line.
+One step = one call of skipconv_step on one batch (the whole hot path) over a
+frame of the synthetic clip; the clip repeats with a reset (dense reference
+frame) at its first frame. Inputs are resident in HBM before the timed
+region. The timed region starts right after a reference frame, so K steps
+up to the clip length are steady-state frames; the reference frame is timed
+on its own. Prints one JSON line.
 
-Default workload (rect64): 3x3 conv 64 -> 64, bf16 operands with fp32
-accumulation, 128 x 96 frames, batch 1, a 32-frame clip of four moving
-textured rectangles over a static noise background; gate eps calibrated on
-the GPU's own gate statistics to ~25 % block density with 8 x 8 blocks.
-The sweep covers blocks {1, 4, 8} x densities {10, 25, 50 %} plus the same
-kernels forced dense and torch's conv2d (MIOpen) on the same shape.
+Default workload (blob128): 3x3 conv 128 -> 128, bf16 operands with fp32
+accumulation, four independent 512 x 512 streams (one step = one frame of
+each), a 64-frame clip of 16 moving Gaussian blobs over a static texture with
+a drifting illumination ramp, 16 x 16 gate blocks, eps calibrated on the
+GPU's own gate statistics to ~25 % block density. The sweep covers block
+densities 5 / 10 / 25 / 50 / 75 %, eps = 0 and the same kernels forced dense,
+each with the measured speed-up over forced dense printed beside the
+roofline-model speed-up, plus the caller-retained-frames contract, the other
+gate kinds and torch's conv2d (MIOpen) on the same shape for context.
 """
 from __future__ import annotations
 
@@ -204,12 +210,15 @@ def measure_point(make_layer, frames_dev, steps, warmup, geom, *, label, events=
     pos = nfr
     if warmup:
         _, _, _, _, pos = run_steps(layer, frames_dev, warmup, pos)
-    pos = (pos + nfr - 1) // nfr * nfr  # timed steps start at a clip boundary
+    # the timed steps start right after an untimed reference frame (clip position 0)
+    pos = (pos + nfr - 1) // nfr * nfr
+    _, _, _, _, pos = run_steps(layer, frames_dev, 1, pos)
     every = event_period(nfr, steps) if events and not fused else 0
     blk = event_blocks(nfr) if events and fused else None
     wall, gate_ms, conv_ms, tpos, _ = run_steps(layer, frames_dev, steps, pos, every=every, block=blk)
+    ref_us = reference_us(layer, frames_dev[0]) if events else None
     layer.close()
-    idx = np.arange(steps) % nfr
+    idx = (pos + np.arange(steps)) % nfr
     act_sites = sites[idx].astype(np.float64)
     macs_per_site = geom["c_out"] * geom["kk"]
     flops_active = 2.0 * act_sites.sum() * macs_per_site
@@ -248,6 +257,8 @@ def measure_point(make_layer, frames_dev, steps, warmup, geom, *, label, events=
         "conv_active_tflops": conv_flop / (conv_us * 1e-6) / 1e12 if conv_us else None,
         "gate_gbs": gate_bytes / (gate_us * 1e-6) / 1e9 if gate_us else None,
         "fused_bytes_per_launch": float(fused_bytes) if fused else None,
+        "reference_frame_us": ref_us,
+        "active_sites_per_launch": float(sites[tpos].mean()) if len(tpos) else None,
     }
     if fused:
         log(f"[bench] {label}: {res['frames_per_s']:.0f} frames/s, {res['ms_per_step'] * 1e3:.1f} us/step, "
@@ -256,6 +267,23 @@ def measure_point(make_layer, frames_dev, steps, warmup, geom, *, label, events=
         log(f"[bench] {label}: {res['frames_per_s']:.0f} frames/s, {res['ms_per_step'] * 1e3:.1f} us/step, "
             f"density {res['density']:.3f}, gate {gate_us or 0:.1f} us, conv {conv_us or 0:.1f} us")
     return res
+
+
+def reference_us(layer, frame, reps=3):
+    """Median duration of a reference frame (reset, then one dense step), HIP events on the launch stream."""
+    import torch
+
+    stream = layer.stream if layer.stream is not None else torch.cuda.current_stream()
+    out = []
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        layer.reset()
+        a.record(stream)
+        layer.step(frame)
+        b.record(stream)
+        torch.cuda.synchronize()
+        out.append(1e3 * a.elapsed_time(b))
+    return float(np.median(out))
 
 
 def translate_np(x, dy, dx):
@@ -336,32 +364,46 @@ def torch_dense_us(wt, shape, stride, steps=200):
 
 # ------------------------------------------------------------ CPU baseline --
 
-def cpu_baseline(wl, clip, w32, eps, block, budget_s=12.0):
-    """The CPU oracle as it stands, single-threaded BLAS, over a bounded sample of the clip."""
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(wl, w32, eps, block, streams=1, budget_s=12.0, threads=1):
+    """The CPU oracle as it stands, BLAS limited to `threads`, on a bounded sample of the
+    workload: the first `streams` stream(s) of the clip, the reference frame untimed, then
+    consecutive steady-state frames until `budget_s` has passed (at least two)."""
     from threadpoolctl import threadpool_limits
     from oracle import skipconv_oracle as O
+    from paper_2104_11487_amd import synthetic as syn
 
     lay_spec = wl.layers[0]
     wbits = w32 if wl.dtype == "f32" else O.f32_to_bf16_rne(w32)
-    done, t0 = 0, time.perf_counter()
-    with threadpool_limits(limits=1):
-        orc = O.SkipConvOracle(wbits, n=wl.n, h=wl.h, w=wl.w, stride=lay_spec.stride, eps=eps,
-                               block=block, dtype=wl.dtype)
-        while True:
-            pos = done % len(clip)
-            if pos == 0:
-                orc.reset()
-            orc.step(clip[pos])
+    n = min(streams, wl.n)
+    vid = wl.video(wl.frames)
+    with threadpool_limits(limits=threads):
+        orc = O.SkipConvOracle(wbits, n=n, h=wl.h, w=wl.w, stride=lay_spec.stride, eps=eps, block=block,
+                               dtype=wl.dtype)
+        orc.step(syn.to_storage(next(vid)[:n], wl.dtype))  # reference frame, untimed
+        done, el = 0, 0.0
+        for f in vid:
+            x = syn.to_storage(f[:n], wl.dtype)
+            t0 = time.perf_counter()
+            orc.step(x)
+            el += time.perf_counter() - t0
             done += 1
-            el = time.perf_counter() - t0
-            if el >= budget_s and done >= min(len(clip), 4):
+            if (el >= budget_s and done >= 2) or el >= 3 * budget_s:
                 break
-            if el >= 3 * budget_s:
-                break
-    el = time.perf_counter() - t0
-    return {"value": done * wl.n / el, "unit": "frames/s", "cores": 1, "kind": "oracle",
-            "sample": f"{done} consecutive steps of the same clip ({wl.name}, eps={eps:.4g}, b={block}, "
-                      f"reset every {len(clip)} frames), {el:.1f}s, numpy fp64 with BLAS limited to 1 thread"}
+    return {"value": done * n / el, "unit": "frames/s", "cores": threads, "kind": "oracle",
+            "sample": f"{done} consecutive steady-state frames (clip positions 1..{done}) of {n} of the "
+                      f"{wl.n} streams of {wl.name}, eps={eps:.4g}, b={block}, {el:.1f}s timed after an untimed "
+                      f"reference frame; numpy fp64, BLAS limited to {threads} thread(s)"}
 
 
 # ---------------------------------------------------------------- traffic --
@@ -751,9 +793,9 @@ def bench_mbconv(args):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=640)
-    ap.add_argument("--warmup", type=int, default=64)
-    ap.add_argument("--workload", default="rect64",
+    ap.add_argument("--steps", type=int, default=40)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--workload", default="blob128",
                     choices=["rect64", "blob128", "square16", "stack6", "mbconv192"])
     ap.add_argument("--block", type=int, default=None)
     ap.add_argument("--density", type=float, default=0.25)
@@ -761,6 +803,7 @@ def main():
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-events", action="store_true", help="time without per-kernel events")
+    ap.add_argument("--no-peaks", action="store_true", help="skip the measured copy / GEMM peaks")
     ap.add_argument("--split", action="store_true",
                     help="force the gate + compaction + conv pipeline instead of the fused kernel")
     ap.add_argument("--caller-retains", action="store_true",
@@ -809,16 +852,19 @@ def main():
     h_out, w_out = probe.h_out, probe.w_out
     probe.close()
     kk = spec.k * spec.k * spec.c_in // spec.groups
-    x_bytes = wl.n * wl.h * wl.w * wl.c * (2 if wl.dtype == "bf16" else 4)
+    esz = 2 if wl.dtype == "bf16" else 4
+    x_bytes = wl.n * wl.h * wl.w * wl.c * esz
     geom = {"n": wl.n, "sites": wl.n * h_out * w_out, "c_out": spec.c_out, "kk": kk, "x_bytes": x_bytes,
             "nb": wl.n * (-(-h_out // block)) * (-(-w_out // block)),
-            "w_bytes": kk * spec.c_out * (2 if wl.dtype == "bf16" else 4)}
+            "w_bytes": kk * spec.c_out * esz}
+    big = args.workload == "blob128"
 
     if args.copy_probe:
         src = torch.empty(args.copy_probe << 20, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
         dst.copy_(src)
         torch.cuda.synchronize()
+        del src, dst
     stats = None if args.eps is not None else gpu_stats(layer_kw, wt, frames_dev)
 
     def mk(b, eps, dense=False, split=args.split, gate="input", retains=args.caller_retains):
@@ -830,71 +876,110 @@ def main():
                          label=f"b={block} d={args.density}", events=not args.no_events,
                          retains=args.caller_retains)
 
+    # roofline model of one step (memory-bound at both ends of the sweep): the
+    # fixed bytes (x_t and x_{t-1} read, x_t kept unless the caller retains its
+    # frames, weights) plus the z read-modify-write at the active sites
+    z_bytes = geom["sites"] * spec.c_out * 4
+
+    def model_us(d, retains):
+        fixed = (2 if retains else 3) * x_bytes + geom["w_bytes"]
+        return 1e6 * (fixed + 2 * d * z_bytes) / (PEAK_HBM_GBS * 1e9)
+
+    dense_flop = 2.0 * geom["sites"] * spec.c_out * kk
+    peak_mfma = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
+    ideal_dense_us = 1e6 * max(dense_flop / (peak_mfma * 1e12), (2 * x_bytes + z_bytes + geom["w_bytes"])
+                               / (PEAK_HBM_GBS * 1e9))
+
     sweep = []
     if not args.no_sweep and stats is not None:
-        sweep_steps = max(len(clip) * 2, min(args.steps, 256))
-        for b in ([1, 4, 8] if args.workload != "blob128" else [16]):
-            for d in (0.1, 0.25, 0.5):
-                e = eps_for_density(stats, b, h_out, w_out, d)
-                g2 = dict(geom, nb=wl.n * (-(-h_out // b)) * (-(-w_out // b)))
-                r = measure_point(mk(b, e), frames_dev, sweep_steps, len(clip), g2, label=f"b={b} d={d}")
-                r.update({"block": b, "target_density": d, "eps": e})
-                sweep.append(r)
-        r = measure_point(mk(block, 0.0, dense=True), frames_dev, sweep_steps, len(clip), geom,
+        sweep_steps = min(args.steps, len(clip) - 1) if big else max(len(clip) * 2, min(args.steps, 256))
+        sweep_steps = max(sweep_steps, 8)
+        warm = 2 if big else len(clip)
+        blocks_sweep = [block] if big else [1, 4, 8]
+        dens_sweep = (0.05, 0.10, 0.25, 0.50, 0.75) if big else (0.10, 0.25, 0.50)
+        r = measure_point(mk(block, 0.0, dense=True), frames_dev, sweep_steps, warm, geom,
                           label=f"forced dense b={block}")
         r.update({"block": block, "target_density": 1.0, "forced_dense": True})
+        dense_ms = r["ms_per_step"]
         sweep.append(r)
-        r = measure_point(mk(block, eps_head, split=not args.split), frames_dev, sweep_steps, len(clip), geom,
-                          label=f"b={block} d={args.density} other pipeline")
-        r.update({"block": block, "target_density": args.density})
-        sweep.append(r)
-        # the other x_{t-1} contract: read from the caller's previous frame
-        # (no copy written), or from the library's own copy
-        other = not args.caller_retains
-        r = measure_point(mk(block, eps_head, retains=other), frames_dev, sweep_steps, len(clip), geom,
-                          label=f"b={block} d={args.density} " + ("caller-retained frames" if other
-                                                                  else "library x_(t-1) copy"),
-                          retains=other)
-        r.update({"block": block, "target_density": args.density, "caller_retains": other})
-        sweep.append(r)
+        for b in blocks_sweep:
+            for d in dens_sweep + ((0.0,) if big else ()):
+                e = eps_for_density(stats, b, h_out, w_out, d) if d > 0 else 0.0
+                g2 = dict(geom, nb=wl.n * (-(-h_out // b)) * (-(-w_out // b)))
+                lab = f"b={b} d={d}" if d > 0 else f"b={b} eps=0"
+                r = measure_point(mk(b, e), frames_dev, sweep_steps, warm, g2, label=lab)
+                r.update({"block": b, "target_density": d if d > 0 else 1.0, "eps": e})
+                if b == block:
+                    ds = r["density"]
+                    r["speedup_vs_forced_dense"] = dense_ms / r["ms_per_step"]
+                    r["model_speedup_vs_forced_dense"] = model_us(1.0, False) / model_us(ds, False)
+                    r["model_us_per_step"] = model_us(ds, False)
+                    r["model_speedup_vs_ideal_dense"] = ideal_dense_us / model_us(ds, False)
+                    log(f"[bench] {lab}: speed-up over forced dense {r['speedup_vs_forced_dense']:.2f}x "
+                        f"(roofline model {r['model_speedup_vs_forced_dense']:.2f}x at density {ds:.3f})")
+                sweep.append(r)
+                if big and d > 0:
+                    # the same point with caller-retained frames (no x_t copy)
+                    r2 = measure_point(mk(b, e, retains=True), frames_dev, sweep_steps, warm, g2,
+                                       label=f"{lab} caller-retained frames", retains=True)
+                    r2.update({"block": b, "target_density": d, "eps": e, "caller_retains": True,
+                               "speedup_vs_forced_dense": dense_ms / r2["ms_per_step"],
+                               "model_us_per_step": model_us(r2["density"], True),
+                               "model_speedup_vs_forced_dense": model_us(1.0, False) / model_us(r2["density"], True)})
+                    sweep.append(r2)
+        if not big:  # (the large workload runs the split pipeline either way)
+            r = measure_point(mk(block, eps_head, split=not args.split), frames_dev, sweep_steps, warm, geom,
+                              label=f"b={block} d={args.density} other pipeline")
+            r.update({"block": block, "target_density": args.density})
+            sweep.append(r)
+            other = not args.caller_retains
+            r = measure_point(mk(block, eps_head, retains=other), frames_dev, sweep_steps, warm, geom,
+                              label=f"b={block} d={args.density} " + ("caller-retained frames" if other
+                                                                      else "library x_(t-1) copy"),
+                              retains=other)
+            r.update({"block": block, "target_density": args.density, "caller_retains": other})
+            sweep.append(r)
         # Output-Norm gate (Eq. 7) at the same density: with p = 2 it compares
         # s * sum(w^2) with eps^2, so eps scales by the weight 2-norm
         wq = wt.float().cpu().numpy().astype(np.float64)
         e_out = eps_head * float(np.sqrt(np.sum(wq * wq)))
-        r = measure_point(mk(block, e_out, gate="output"), frames_dev, sweep_steps, len(clip), geom,
+        r = measure_point(mk(block, e_out, gate="output"), frames_dev, sweep_steps, warm, geom,
                           label=f"output-norm gate b={block} d={args.density}")
         r.update({"block": block, "target_density": args.density, "gate": "output-norm", "eps": e_out})
         sweep.append(r)
         # learned gate (Eq. 8 at inference; split pipeline): seeded random phi,
-        # bias from the GPU's own scores for the same block density
-        import torch
+        # bias from the GPU's own scores for the same block density (a 16-frame
+        # clip on the large workload)
+        short = frames_dev[:16] if big else frames_dev
         rng = np.random.Generator(np.random.PCG64(7))
         phi = torch.from_numpy(rng.normal(0, 0.05, (spec.c_in, spec.k, spec.k)).astype(np.float32)).cuda()
         probe = SkipConv(wt, eps=0.0, block=1, keep_stats=True, gate="learned", **layer_kw)
         probe.set_gate_weights(phi, 0.0)
         scores = []
-        for t, x in enumerate(frames_dev):
+        for t, x in enumerate(short):
             probe.step(x)
             if t > 0:
                 torch.cuda.synchronize()
                 scores.append(probe.stat())
         probe.close()
         bias = -block_quantile(scores, block, h_out, w_out, args.density)
+
         def mk_learned():
             lay = SkipConv(wt, eps=0.0, block=block, gate="learned", **layer_kw)
             lay.set_gate_weights(phi, bias)
             return lay
-        r = measure_point(mk_learned, frames_dev, sweep_steps, len(clip), geom,
-                          label=f"learned gate b={block} d={args.density}")
+        r = measure_point(mk_learned, short, min(sweep_steps, len(short) - 1) if big else sweep_steps,
+                          warm, geom, label=f"learned gate b={block} d={args.density}")
         r.update({"block": block, "target_density": args.density, "gate": "learned", "bias": bias})
         sweep.append(r)
         # translation-compensated steps (Sec. 3.3): the clip with a one-pixel
         # camera jitter on every other frame, stepped with the known shift vs. plainly
-        r1, r2 = measure_translated(wt, layer_kw, clip, wl.dtype, eps_head, block, sweep_steps)
+        r1, r2 = measure_translated(wt, layer_kw, clip[:16] if big else clip, wl.dtype, eps_head, block,
+                                    32 if big else sweep_steps)
         sweep += [r1, r2]
-        tus = torch_dense_us(wt, (wl.n, wl.h, wl.w, wl.c), spec.stride)
+        tus = torch_dense_us(wt, (wl.n, wl.h, wl.w, wl.c), spec.stride, steps=20 if big else 200)
         sweep.append({"label": "torch conv2d (MIOpen), dense, same shape", "us_per_frame_batch": tus,
-                      "dense_tflops": 2.0 * geom["sites"] * spec.c_out * kk / (tus * 1e-6) / 1e12})
+                      "dense_tflops": dense_flop / (tus * 1e-6) / 1e12})
         log(f"[bench] torch conv2d dense: {tus:.1f} us")
 
     # roofline of the dominant kernel, from the events of the timed region;
@@ -902,8 +987,8 @@ def main():
     def traffic(kernel):
         return None if args.caller_retains else profiled_traffic(args.workload, kernel)
 
-    peak_mfma = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
-    roof = None
+    meas = measured_peaks() if not args.no_peaks else None
+    roof, kernels = None, {}
     if head["gate_us"] is not None and head["pipeline"] == "fused":
         fb, ff, fus = head["fused_bytes_per_launch"], head["conv_flop_per_launch"], head["gate_us"]
         hbm_bound = fb / (PEAK_HBM_GBS * 1e9) >= ff / (peak_mfma * 1e12)
@@ -920,24 +1005,57 @@ def main():
                     "traffic": traffic("fused"), "bytes_per_launch": fb,
                     "flop_per_launch": ff, "us_per_launch": fus}
     elif head["conv_us"] is not None:
-        if head["conv_us"] >= head["gate_us"]:
-            a = head["conv_active_tflops"]
-            roof = {"kernel": "conv (sparse gather-MFMA)", "bound": "mfma", "achieved": a,
-                    "peak": peak_mfma, "unit": "TFLOP/s", "frac": a / peak_mfma,
-                    "traffic": traffic("conv"),
-                    "flop_per_launch": head["conv_flop_per_launch"], "us_per_launch": head["conv_us"]}
+        # convolution: algorithmic bytes = the residual operand at the active sites
+        # (x_t and x_{t-1}) + z read-modify-written there (written on a reference frame)
+        act_sites = head["active_sites_per_launch"]
+        conv_bytes = act_sites * (2 * spec.c_in * esz + 8 * spec.c_out) + geom["w_bytes"]
+        cf, cus = head["conv_flop_per_launch"], head["conv_us"]
+        gb, gus = head["gate_bytes_per_launch"], head["gate_us"]
+        kernels = {
+            "gate": {"us_per_launch": gus, "bytes_per_launch": gb, "gbs": gb / (gus * 1e-6) / 1e9,
+                     "frac_hbm": gb / (gus * 1e-6) / 1e9 / PEAK_HBM_GBS, "traffic": traffic("gate")},
+            "conv": {"us_per_launch": cus, "flop_per_launch": cf, "bytes_per_launch": conv_bytes,
+                     "tflops": cf / (cus * 1e-6) / 1e12, "frac_mfma": cf / (cus * 1e-6) / 1e12 / peak_mfma,
+                     "gbs": conv_bytes / (cus * 1e-6) / 1e9,
+                     "frac_hbm": conv_bytes / (cus * 1e-6) / 1e9 / PEAK_HBM_GBS,
+                     "arith_intensity": cf / conv_bytes, "traffic": traffic("conv")},
+        }
+        if meas:
+            kernels["gate"]["frac_measured_hbm"] = kernels["gate"]["gbs"] / meas["hbm_copy_gbs"]
+            kernels["conv"]["frac_measured_mfma"] = kernels["conv"]["tflops"] / meas["bf16_gemm_tflops"]
+            kernels["conv"]["frac_measured_hbm"] = kernels["conv"]["gbs"] / meas["hbm_copy_gbs"]
+        if cus >= gus:
+            k = kernels["conv"]
+            mfma_bound = cf / (peak_mfma * 1e12) >= conv_bytes / (PEAK_HBM_GBS * 1e9)
+            roof = {"kernel": "conv (sparse halo-gather MFMA over active blocks)",
+                    "bound": "mfma" if mfma_bound else "hbm",
+                    "achieved": k["tflops"] if mfma_bound else k["gbs"],
+                    "peak": peak_mfma if mfma_bound else PEAK_HBM_GBS,
+                    "unit": "TFLOP/s" if mfma_bound else "GB/s",
+                    "frac": k["frac_mfma"] if mfma_bound else k["frac_hbm"], "traffic": k["traffic"],
+                    "flop_per_launch": cf, "bytes_per_launch": conv_bytes, "us_per_launch": cus}
         else:
-            a = head["gate_gbs"]
-            roof = {"kernel": "gate (residual, statistic, compaction)", "bound": "hbm", "achieved": a,
-                    "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": a / PEAK_HBM_GBS,
-                    "traffic": traffic("gate"),
-                    "bytes_per_launch": head["gate_bytes_per_launch"], "us_per_launch": head["gate_us"]}
+            k = kernels["gate"]
+            roof = {"kernel": "gate (residual, statistic, threshold, blocks, work list, x_t copy)",
+                    "bound": "hbm", "achieved": k["gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                    "frac": k["frac_hbm"], "traffic": k["traffic"], "bytes_per_launch": gb,
+                    "us_per_launch": gus}
+    if roof is not None and meas:
+        roof["measured_peak"] = meas["hbm_copy_gbs"] if roof["unit"] == "GB/s" else meas["bf16_gemm_tflops"]
+        roof["frac_of_measured_peak"] = roof["achieved"] / roof["measured_peak"]
 
     cpu = None
     if not args.no_cpu:
-        cpu = cpu_baseline(wl, clip, w32, eps_head, block)
-        log(f"[bench] cpu oracle: {cpu['value']:.2f} frames/s")
+        e_cpu = eps_head
+        cpu = cpu_baseline(wl, w32, e_cpu, block, streams=1 if big else wl.n, threads=1)
+        log(f"[bench] cpu oracle, 1 core: {cpu['value']:.3f} frames/s")
+        ncores = len(os.sched_getaffinity(0))
+        allc = cpu_baseline(wl, w32, e_cpu, block, streams=1 if big else wl.n, threads=ncores)
+        log(f"[bench] cpu oracle, {ncores} cores: {allc['value']:.3f} frames/s")
+        cpu["all_cores"] = {"value": allc["value"], "cores": ncores, "sample": allc["sample"]}
+        cpu["cpu_model"] = cpu_model()
 
+    d_head = head["density"]
     out = {
         "metric": METRIC,
         "value": head["frames_per_s"],
@@ -953,21 +1071,62 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": f"{wl.name}: {spec.k}x{spec.k} conv {spec.c_in}->{spec.c_out} stride {spec.stride}, "
-                        f"{wl.h}x{wl.w} frames, batch {wl.n}, {len(clip)}-frame clip (reset at frame 1), "
-                        f"gate block {block}, eps for ~{args.density:.0%} density",
-            "eps": eps_head, "block": block, "density": head["density"],
+                        f"{wl.h}x{wl.w} frames, batch {wl.n} independent streams (one step = one frame of each), "
+                        f"{len(clip)}-frame clip (reset at frame 1), gate block {block}, "
+                        f"eps for ~{args.density:.0%} block density; steady-state steps after a reference frame",
+            "eps": eps_head, "block": block, "density": d_head,
             "density_steady": head["density_steady"],
             "active_tflops": head["active_tflops"], "dense_equiv_tflops": head["dense_equiv_tflops"],
             "pipeline": head["pipeline"], "caller_retains": bool(args.caller_retains),
             "kernel_us": head["gate_us"] if head["pipeline"] == "fused" else None,
             "gate_us": head["gate_us"] if head["pipeline"] == "split" else None,
             "conv_us": head["conv_us"] if head["pipeline"] == "split" else None,
+            "reference_frame_us": head["reference_frame_us"],
+            "model_us_per_step": model_us(d_head, args.caller_retains),
+            "model_frac": model_us(d_head, args.caller_retains) / (1e3 * head["ms_per_step"]),
+            "kernels": kernels or None,
+            "measured_peaks": meas,
         },
         "roofline": roof,
         "cpu_baseline": cpu,
         "sweep": sweep,
     }
     print(json.dumps(out), flush=True)
+
+
+def measured_peaks():
+    """Achievable peaks on this device, measured with torch next to the datasheet figures:
+    a 2 GiB device-to-device copy (bytes read + written per second) and a large bf16 GEMM
+    (hipBLASLt through torch.matmul)."""
+    import torch
+
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e-3 / reps
+
+    n = 2 << 30
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    t = timed(lambda: dst.copy_(src), 20)
+    copy_gbs = 2 * n / t / 1e9
+    del src, dst
+    m = 8192
+    a = torch.randn(m, m, device="cuda", dtype=torch.bfloat16)
+    bm = torch.randn(m, m, device="cuda", dtype=torch.bfloat16)
+    t = timed(lambda: torch.matmul(a, bm), 20)
+    gemm = 2.0 * m ** 3 / t / 1e12
+    del a, bm
+    log(f"[bench] measured peaks: device copy {copy_gbs:.0f} GB/s, bf16 GEMM {gemm:.0f} TFLOP/s")
+    return {"hbm_copy_gbs": copy_gbs, "bf16_gemm_tflops": gemm, "hbm_spec_gbs": PEAK_HBM_GBS,
+            "bf16_spec_tflops": PEAK_BF16_TFLOPS,
+            "how": "torch: 2 GiB device copy (read + write bytes), 8192^3 bf16 matmul"}
 
 
 if __name__ == "__main__":

@@ -157,7 +157,12 @@ int skipconv_out_shape(const skipconv_desc* d, int32_t* h_out, int32_t* w_out,
  * optional activation buffer, gate masks, active list, counters). Host only. */
 int skipconv_workspace_size(const skipconv_desc* d, size_t* bytes);
 
-/* Create a layer.
+/* Create a layer: the convolution of Eq. 1 (weights w, kernel k, stride,
+ * groups) run on residual frames (Eq. 3) behind the gate of Sec. 3.2.1
+ * (threshold eps, Eq. 5; Output-Norm variant Eq. 7) or Sec. 3.2.2 (learned
+ * gate, Eq. 8), with b x b block structure (Sec. 3.2.2, "Structured
+ * Sparsity"). The workspace argument is the bind-workspace call of the
+ * interface folded into create: every buffer the layer uses lives in it.
  *   weights:   device pointer, OIHW in d->dtype; copied and repacked on
  *              `stream` (the caller may free it once that work completes).
  *   workspace: device pointer of at least skipconv_workspace_size bytes,
@@ -176,10 +181,18 @@ int skipconv_create(const skipconv_desc* d, const void* weights, void* workspace
  *   *z_t: (may be NULL) set to the device pointer of the persistent state,
  *        N x H_out x W_out x C_out fp32, valid until the next step, reset or
  *        destroy on this handle. Copy it to keep it.
- * Enqueues the gate kernel (residual, support statistic, threshold, block
- * pooling, ordered compaction, x_{t-1} update) and the sparse convolution
- * kernel (gather of residual patches, MFMA product over active sites only,
- * accumulate into z) on `stream`; no host synchronisation. */
+ * Everything is enqueued on `stream`; no host synchronisation. The pipeline
+ * is chosen at create (skipconv_pipeline reports it):
+ *   fused: one kernel per frame; each workgroup takes one tile of output
+ *          sites through residual, statistic, threshold, block flags, x_{t-1}
+ *          update, product and z update. Tiles with no active block store
+ *          nothing; the product of a tile is formed before its gate is known
+ *          where that hides the gate's latency, so on those builds a tile's
+ *          MFMA work does not shrink with density, only its stores do.
+ *   split: the gate kernel (residual, statistic, threshold, block pooling,
+ *          x_{t-1} update, unordered work list of active blocks), then the
+ *          sparse convolution kernel, which walks only the listed blocks
+ *          (residual halo in LDS, MFMA product, z accumulate). */
 int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t);
 
 /* Process one frame whose content moved by (dy, dx) input pixels since the
@@ -285,6 +298,15 @@ int skipconv_copy_block_mask(skipconv_t h, void* stream, uint8_t* host, size_t b
  * n*HB*WB + bi*WB + bj. capacity in entries; *count receives the length. */
 int skipconv_copy_active_list(skipconv_t h, void* stream, uint32_t* host, size_t capacity,
                               int64_t* count);
+
+/* Host copy of the list of active blocks the last step's convolution walked
+ * (split pipeline): the gate kernel's work list, whose order is that of the
+ * appends (unordered; every active block once), or, for blocks larger than a
+ * gate tile, the ordered list the compaction wrote. capacity in entries;
+ * *count receives the length. E_UNSUPPORTED after a one-pass step (it keeps
+ * no list: its block flags, skipconv_copy_block_mask, are its own output). */
+int skipconv_copy_work_list(skipconv_t h, void* stream, uint32_t* host, size_t capacity,
+                            int64_t* count);
 
 /* Host copies of the last step's per-site gate bit (N x H_out x W_out bytes)
  * and gate statistic (fp32, same shape). E_STATE without KEEP_STATS. */

@@ -22,7 +22,7 @@ Processing", CVPR 2021):
   norm of the whole weight tensor (all four dimensions) before the comparison
   with eps. By Young's inequality (Eq. 6) that product bounds the norm of the
   skipped update at the site, so a skipped site's update has norm <= eps.
-* Sec. 3.2.1, Eq. 8 (Gumbel gate at inference): a light convolution f(r; phi)
+* Sec. 3.2.2, Eq. 8 (Gumbel gate at inference): a light convolution f(r; phi)
   with one output channel and the layer's kernel size, stride and padding
   scores every output location; the gate rounds sigmoid(f), i.e. it is on
   exactly when f > 0. phi is a given parameter here (training is out of scope).
@@ -80,9 +80,14 @@ rest of the design notes):
   treats x_{t-1} as zero, forces every site on and assigns z instead of adding.
 
 Parity pins: every function here is checked in ``tests/test_oracle_pins.py``
-against values the mathematics fixes (library conv2d / max_pool2d, exact
-integer arithmetic, exact rational arithmetic, brute-force loops, telescoping
-of Eq. 2, closed forms for an impulse residual). No function is unpinned.
+against values the mathematics fixes (library conv2d / max_pool2d /
+nearest interpolate / relu and casts, exact integer arithmetic, exact rational
+arithmetic, brute-force loops, telescoping of Eq. 2, closed forms for an
+impulse residual). Each function has a named pin: block_upsample equals the
+library's nearest interpolate and a per-site brute force; dense_conv equals the
+library conv2d in fp64 (exact on integers) and a brute force; activation_to_storage
+equals the library relu and casts; out_size / n_blocks equal the library's
+output shapes; translate equals a brute-force shift.
 """
 from __future__ import annotations
 
@@ -522,7 +527,10 @@ class SkipConvOracle:
 
 
 def activation_to_storage(z: np.ndarray, act: str, dtype: str) -> np.ndarray:
-    """Next layer's input from this layer's state: dtype(act(z)) (z is pre-activation, Eq. 1)."""
+    """Next layer's input from this layer's state: dtype(act(z)) (z is pre-activation, Eq. 1).
+
+    relu gives +0 for every non-positive value (-0 included) and passes NaN through.
+    """
     y = np.maximum(z, 0.0) if act == "relu" else z
     y32 = y.astype(np.float32)
     if dtype == "f32":

@@ -58,7 +58,7 @@ emit_kernel(const uint8_t* block_mask, uint8_t* prev_mask, int nb, int bpw, cons
         continue;
       }
       float a = z[o + v];
-      if (act == 2) a = fmaxf(a, 0.0f);
+      if (act == 2) a = relu_f32(a);
       float r;
       if (dtype == 1) {
         uint16_t* yb = static_cast<uint16_t*>(y);

@@ -87,7 +87,7 @@ struct TileWalk {
   }
 };
 
-__device__ __forceinline__ float activate(float v, int act) { return act == 2 ? fmaxf(v, 0.0f) : v; }
+__device__ __forceinline__ float activate(float v, int act) { return act == 2 ? relu_f32(v) : v; }
 
 template <typename T>
 __device__ __forceinline__ void store_y(void* y, size_t i, float v) {

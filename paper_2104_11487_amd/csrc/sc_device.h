@@ -65,6 +65,10 @@ template <> struct Elem<uint16_t> {
   }
 };
 
+// ReLU of the activation output: v for v > 0 and for NaN (a NaN state stays
+// visible to the next layer), +0 otherwise (also for -0).
+__device__ __forceinline__ float relu_f32(float v) { return (v > 0.0f || __builtin_isnan(v)) ? v : 0.0f; }
+
 // Exact IEEE single-precision operations with no contraction into FMA: the
 // gate statistic must round once per multiply and once per add.
 __device__ __forceinline__ float mul_rn(float a, float b) { return __fmul_rn(a, b); }

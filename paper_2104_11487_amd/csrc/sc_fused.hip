@@ -483,7 +483,7 @@ __device__ __forceinline__ void store_piece(const FusedParams& p, size_t o, cons
   if (p.act) {
     uint32_t yb[4];
 #pragma unroll
-    for (int v = 0; v < 4; ++v) yb[v] = f32_to_bf16(p.act == 2 ? fmaxf(nv[v], 0.0f) : nv[v]);
+    for (int v = 0; v < 4; ++v) yb[v] = f32_to_bf16(p.act == 2 ? relu_f32(nv[v]) : nv[v]);
     *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.y) + o) = uint2{yb[0] | (yb[1] << 16), yb[2] | (yb[3] << 16)};
     if (EMIT) {
       const uint32_t yo[4] = {yold.x & 0xffffu, yold.x >> 16, yold.y & 0xffffu, yold.y >> 16};
@@ -1304,7 +1304,7 @@ __global__ void __launch_bounds__(kThreads) fused_sc_kernel(FusedParams p) {
         if (p.act) {
           floatx4 a;
 #pragma unroll
-          for (int j = 0; j < 4; ++j) a[j] = p.act == 2 ? fmaxf(nv[j], 0.0f) : nv[j];
+          for (int j = 0; j < 4; ++j) a[j] = p.act == 2 ? relu_f32(nv[j]) : nv[j];
           *reinterpret_cast<floatx4*>(static_cast<float*>(p.y) + o) = a;
           if (EMIT) {
             floatx4 r;

@@ -1,12 +1,14 @@
-// Gate kernel of the Skip-Conv layer: residual, Input-Norm gate statistic,
-// threshold, block pooling and ordered compaction, fused in one launch.
+// Gate kernel of the Skip-Conv layer's split pipeline: residual, gate
+// statistic, threshold, block pooling and the convolution's work list, fused
+// in one launch.
 //
 //   Eq. 2     r = x_t - x_{t-1} (x_{t-1} = 0 on a reference frame, Sec. 3.1)
 //   Eq. 5     s[o] = norm of r over the kernel support of output o;
 //             g[o] = s[o] > eps^2 (p = 2) or s[o] > eps (p = 1), or s NaN
+//             (Eq. 7: s times the weight norm; Eq. 8: a learned score > 0)
 //   Sec 3.2.2 block mask M[B] = OR of g over the b x b block B (ceil mode)
-//   Sec 4.2   active list = ascending indices of active blocks (the
-//             "non-sparse columns" of the im2col product)
+//   Sec 4.2   work list = the active blocks (the "non-sparse columns" of the
+//             im2col product the convolution multiplies)
 //
 // Statistic arithmetic is canonical so that masks are reproducible bit for
 // bit: fp32 r; per pixel a[q] = chunk sums of 8 consecutive channels (terms
@@ -14,18 +16,25 @@
 // one rounding per multiply and per add, no FMA; s[o] = sum of a over the taps
 // (kh, kw) in row-major order, in fp32; the threshold comparison in fp64.
 //
-// One workgroup owns a TS x TS tile of output sites (whole blocks). One
-// thread takes one 8-channel chunk of one halo pixel at a time (a 16-byte
-// load of each frame for bf16; consecutive threads read consecutive chunks,
-// eight chunks in flight per thread) and forms the chunk sum. With 4, 8 or 16
-// chunks per pixel the pixel's lanes add their chunk sums in order through
-// DPP lane shifts; otherwise the sums are parked in LDS and one thread per
-// halo pixel adds them in order. Input pixels
-// the tile owns are copied into the spare x_{t-1} slot on the way (ping-pong:
-// the slot being read is never written in the same step). Every workgroup
-// then writes its block flags. A second, one-workgroup kernel scans all
-// block flags in index order and writes the active list and its length (a
-// kernel boundary, rather than a device-wide counter, orders the two).
+// One workgroup owns a TS x TS tile of output sites (whole blocks when
+// b <= 16). One thread takes one 8-channel chunk of one halo pixel at a time
+// (a 16-byte load of each frame for bf16; consecutive threads read
+// consecutive chunks, eight chunks in flight per thread) and forms the chunk
+// sum. With 4, 8 or 16 chunks per pixel the pixel's lanes add their chunk
+// sums in order through DPP lane shifts; otherwise the sums are parked in LDS
+// and one thread per halo pixel adds them in order. Input pixels the tile
+// owns are copied into the spare x_{t-1} slot on the way (ping-pong: the slot
+// being read is never written in the same step; no copy under caller-retained
+// frames). Every workgroup then writes its block flags and appends its active
+// blocks to the convolution's work list: a ballot and prefix count inside the
+// tile, then one atomic per tile on the counter of its segment (eight
+// segments, one per XCD's contiguous range of tiles, each counter on its own
+// 128-byte line). The list is therefore unordered; the convolution needs no
+// order. Blocks larger than a gate tile (b > 16) are the exception: the tiles
+// OR per-tile flags, and compact_kernel (one workgroup, a kernel boundary
+// after the gate) scans the flags in index order and writes the ordered list
+// and its length. The ordered list of every other layer is built on demand,
+// for introspection only.
 #include "sc_device.h"
 #include "sc_kernels.h"
 #include "sc_stream.h"

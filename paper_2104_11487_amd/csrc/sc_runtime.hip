@@ -569,6 +569,9 @@ struct skipconv_layer {
   // counters are known to be zero.
   int wslot = 0;
   bool wclean[2] = {true, true};
+  // the list the last step's convolution walked: 0 none (one-pass kernel),
+  // 1 the ordered list, 2 the segmented work list of slot work_slot
+  int work_kind = 0, work_slot = 0;
   uint32_t* wlist() { return reinterpret_cast<uint32_t*>(ws + g.off_wlist); }
   uint32_t* wctr() { return reinterpret_cast<uint32_t*>(ws + g.off_wctr); }
   float gate_bias = 0.0f;
@@ -723,9 +726,12 @@ struct StepList {
 hipError_t begin_list(skipconv_layer* h, sc::GateParams& gp, hipStream_t st, StepList* out) {
   if (h->g.split_blocks) {
     *out = StepList{h->list(), h->ctr(), nullptr, 0, 0};
+    h->work_kind = 1;
     return hipSuccess;
   }
   const int slot = h->wslot;
+  h->work_kind = 2;
+  h->work_slot = slot;
   constexpr int kSlot = sc::kSegs * sc::kSegStride;
   uint32_t* c = h->wctr() + slot * kSlot;
   hipError_t e = hipSuccess;
@@ -954,6 +960,7 @@ int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t
     if (e != hipSuccess) return hip_fail(h, e, "fused launch");
     if (timing) e = hipEventRecord(h->ev[3 * h->timing_done + 1], st);
     h->list_valid = false;
+    h->work_kind = 0;
   } else {
     StepList sl{};
     if (e == hipSuccess) e = begin_list(h, gp, st, &sl);
@@ -1297,6 +1304,45 @@ int skipconv_copy_active_list(skipconv_t h, void* stream, uint32_t* host, size_t
   if (capacity < cnt) return fail(h->last_error, SKIPCONV_E_SMALL_BUFFER, "list buffer too small");
   if (cnt == 0) return SKIPCONV_OK;
   return copy_back(h, stream, host, h->list(), (size_t)cnt * 4);
+}
+
+int skipconv_copy_work_list(skipconv_t h, void* stream, uint32_t* host, size_t capacity, int64_t* count) {
+  if (!h) return SKIPCONV_E_STATE;
+  if (!host || !count) return SKIPCONV_E_INVALID_ARG;
+  if (h->frames == 0) return fail(h->last_error, SKIPCONV_E_STATE, "no step yet");
+  if (h->work_kind == 0)
+    return fail(h->last_error, SKIPCONV_E_UNSUPPORTED, "one-pass kernel: no work list (its block flags are the block mask)");
+  if (h->work_kind == 1) {  // the ordered list the compaction wrote for the convolution
+    uint32_t cnt = 0;
+    int rc = copy_back(h, stream, &cnt, h->ctr() + sc::kCtrCount, 4);
+    if (rc) return rc;
+    *count = cnt;
+    if (capacity < cnt) return fail(h->last_error, SKIPCONV_E_SMALL_BUFFER, "list buffer too small");
+    return cnt ? copy_back(h, stream, host, h->list(), (size_t)cnt * 4) : SKIPCONV_OK;
+  }
+  // segment x of the work list starts at entry (first gate tile of x) * seg_cap
+  constexpr int kSlot = sc::kSegs * sc::kSegStride;
+  std::vector<uint32_t> ctr(kSlot);
+  int rc = copy_back(h, stream, ctr.data(), h->wctr() + h->work_slot * kSlot, kSlot * 4);
+  if (rc) return rc;
+  const int per = h->g.gate_grid / sc::kSegs, rem = h->g.gate_grid % sc::kSegs;
+  int64_t tot = 0;
+  for (int x = 0; x < sc::kSegs; ++x) tot += ctr[x * sc::kSegStride];
+  *count = tot;
+  if ((int64_t)capacity < tot) return fail(h->last_error, SKIPCONV_E_SMALL_BUFFER, "list buffer too small");
+  size_t at = 0;
+  for (int x = 0; x < sc::kSegs; ++x) {
+    const uint32_t n = ctr[x * sc::kSegStride];
+    const size_t base = (size_t)(x * per + std::min(x, rem)) * h->g.seg_cap;
+    if (n > (size_t)(x < sc::kSegs - 1 ? (x + 1) * per + std::min(x + 1, rem) : h->g.gate_grid) * h->g.seg_cap - base)
+      return fail(h->last_error, SKIPCONV_E_HIP, "work list segment overflows its range");
+    if (n) {
+      rc = copy_back(h, stream, host + at, h->wlist() + base, (size_t)n * 4);
+      if (rc) return rc;
+    }
+    at += n;
+  }
+  return SKIPCONV_OK;
 }
 
 int skipconv_copy_site_mask(skipconv_t h, void* stream, uint8_t* host, size_t bytes) {

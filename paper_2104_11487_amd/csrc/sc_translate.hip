@@ -38,7 +38,7 @@ translate_state_kernel(const float* z_src, float* z_dst, void* y, int n, int h_o
       const float zv = in ? z_src[so + v] : 0.0f;
       z_dst[o + v] = zv;
       if (act) {
-        const float a = act == 2 ? fmaxf(zv, 0.0f) : zv;
+        const float a = act == 2 ? relu_f32(zv) : zv;
         if (dtype == 1)
           static_cast<uint16_t*>(y)[o + v] = (uint16_t)f32_to_bf16(a);
         else

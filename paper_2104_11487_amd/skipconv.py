@@ -76,6 +76,8 @@ _SIGS = {
     "skipconv_copy_block_mask": (ctypes.c_int, [_P, _P, _P, ctypes.c_size_t]),
     "skipconv_copy_active_list": (ctypes.c_int, [_P, _P, _P, ctypes.c_size_t,
                                                  ctypes.POINTER(ctypes.c_int64)]),
+    "skipconv_copy_work_list": (ctypes.c_int, [_P, _P, _P, ctypes.c_size_t,
+                                                 ctypes.POINTER(ctypes.c_int64)]),
     "skipconv_copy_site_mask": (ctypes.c_int, [_P, _P, _P, ctypes.c_size_t]),
     "skipconv_copy_stat": (ctypes.c_int, [_P, _P, _P, ctypes.c_size_t]),
     "skipconv_frame_macs": (ctypes.c_int, [_P, _P, ctypes.POINTER(ctypes.c_uint64),
@@ -231,6 +233,13 @@ def skipconv_copy_active_list(h: int, stream: int, out) -> int:
     p, _ = _np_buf(out)
     cnt = ctypes.c_int64()
     _check(lib().skipconv_copy_active_list(h, stream, p, out.size, ctypes.byref(cnt)), h)
+    return cnt.value
+
+
+def skipconv_copy_work_list(h: int, stream: int, out) -> int:
+    p, _ = _np_buf(out)
+    cnt = ctypes.c_int64()
+    _check(lib().skipconv_copy_work_list(h, stream, p, out.size, ctypes.byref(cnt)), h)
     return cnt.value
 
 
@@ -461,6 +470,13 @@ class SkipConv:
         import numpy as np
         out = np.empty(self.desc.n * self.hb * self.wb, np.uint32)
         cnt = skipconv_copy_active_list(self.handle, self._stream(), out)
+        return out[:cnt].copy()
+
+    def work_list(self):
+        """Active blocks the last split-pipeline step's convolution walked, in append order."""
+        import numpy as np
+        out = np.empty(self.desc.n * self.hb * self.wb, np.uint32)
+        cnt = skipconv_copy_work_list(self.handle, self._stream(), out)
         return out[:cnt].copy()
 
     def site_mask(self):

@@ -56,6 +56,8 @@ def compare_frame(layer, ref: dict, dtype: str, *, t: int, tag: str, keep_stats:
     assert np.array_equal(bm.astype(bool), ref["block_mask"]), f"{tag} t={t}: block mask differs"
     lst = layer.active_list()
     assert np.array_equal(lst, ref["active"]), f"{tag} t={t}: active list differs"
+    if not layer.fused:
+        check_work_list(layer, ref["active"], tag=tag, t=t)
     blocks, sites = layer.active_count()
     assert blocks == ref["count"] and sites == ref["active_sites"], f"{tag} t={t}: counts differ"
     if keep_stats:
@@ -73,6 +75,14 @@ def compare_frame(layer, ref: dict, dtype: str, *, t: int, tag: str, keep_stats:
     e = rel_err(zg, ref["z"])
     assert e <= TOL[dtype], f"{tag} t={t}: z rel err {e:.3e} > {TOL[dtype]}"
     return e
+
+
+def check_work_list(layer, active, *, tag: str, t: int) -> None:
+    """The list the split pipeline's convolution walked (the gate's own appends, unordered):
+    every active block exactly once, nothing else."""
+    wl = layer.work_list()
+    assert len(np.unique(wl)) == len(wl), f"{tag} t={t}: work list holds a block twice"
+    assert np.array_equal(np.sort(wl), active), f"{tag} t={t}: work list is not the active set"
 
 
 def eps_for_density(stat_frames, block: int, h_out: int, w_out: int, target: float,

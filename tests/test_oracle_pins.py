@@ -542,7 +542,7 @@ def test_output_norm_gate_equals_input_norm_at_scaled_eps(p):
 
 
 # ----------------------------------------------------------------------------
-# Gumbel gate at inference (Sec. 3.2.1, Eq. 8)
+# Gumbel gate at inference (Sec. 3.2.2, Eq. 8)
 # ----------------------------------------------------------------------------
 
 @pytest.mark.parametrize("k,stride", [(1, 1), (3, 1), (3, 2), (5, 1)])
@@ -700,3 +700,98 @@ def test_zero_translation_is_the_plain_step():
         x = rng.random((1, 9, 10, 6), dtype=np.float32)
         ra, rb = a.step(x, shift=(0, 0)), b.step(x)
         assert np.array_equal(ra["z"], rb["z"]) and np.array_equal(ra["block_mask"], rb["block_mask"])
+
+
+# ----------------------------------------------------------------------------
+# Pins of the helpers used outside the recurrence: block upsample, dense
+# convolution, activation output, geometry and translation
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("b,h,w", [(1, 5, 7), (2, 13, 10), (3, 13, 10), (4, 16, 16), (8, 13, 10), (16, 9, 17)])
+def test_block_upsample_is_cropped_nearest_interpolate(b, h, w):
+    """Sec. 3.2.2: nearest-neighbour upsampling of the pooled gate by b, cropped to the output
+    grid; equal to the library routine and to site (i, j) reading block (i // b, j // b)."""
+    rng = _rng(70 + b)
+    m = rng.random((3, O.n_blocks(h, b), O.n_blocks(w, b))) < 0.4
+    up = O.block_upsample(m, b, h, w)
+    assert up.shape == (3, h, w) and up.dtype == bool
+    lib = F.interpolate(torch.from_numpy(m.astype(np.float32))[:, None], scale_factor=b, mode="nearest")
+    assert np.array_equal(up, lib[:, 0, :h, :w].numpy() > 0)
+    brute = np.array([[[m[n, i // b, j // b] for j in range(w)] for i in range(h)] for n in range(3)])
+    assert np.array_equal(up, brute)
+    # exact: pooling the upsampled mask gives the block mask back (no block grows)
+    assert np.array_equal(O.block_pool(up, b), m)
+
+
+@pytest.mark.parametrize("k,stride,pad,groups", [(1, 1, 0, 1), (3, 1, 1, 1), (3, 2, 1, 1), (3, 1, 0, 2),
+                                                 (5, 1, 2, 1), (3, 1, 1, 6), (3, 3, 2, 3)])
+def test_dense_conv_is_library_conv2d(k, stride, pad, groups):
+    """Eq. 1 at every output site: equal to the library conv2d in fp64 (and exact on integers)."""
+    rng = _rng(80 + k + stride + pad + groups)
+    c = 6
+    x = rng.normal(0, 1, (2, 11, 9, c))
+    w = rng.normal(0, 1, (12, c // groups, k, k))
+    z = O.dense_conv(x, w, stride, pad, groups)
+    np.testing.assert_allclose(z, torch_conv(x, w, stride, pad, groups), rtol=1e-12, atol=1e-12)
+    xi = rng.integers(-4, 5, x.shape).astype(np.float64)
+    wi = rng.integers(-3, 4, w.shape).astype(np.float64)
+    assert np.array_equal(O.dense_conv(xi, wi, stride, pad, groups), torch_conv(xi, wi, stride, pad, groups))
+
+
+def test_dense_conv_bruteforce_tiny():
+    rng = _rng(88)
+    x = rng.normal(0, 1, (1, 4, 5, 3))
+    w = rng.normal(0, 1, (2, 3, 3, 3))
+    z = O.dense_conv(x, w, 2, 1, 1)
+    sites = [(0, i, j) for i in range(z.shape[1]) for j in range(z.shape[2])]
+    ref = brute_update(x, w, 2, 1, 1, sites).reshape(z.shape)
+    np.testing.assert_allclose(z, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_activation_to_storage_is_relu_then_cast():
+    """The next layer's input dtype(act(z)): the library relu followed by the library casts
+    (fp64 -> fp32 -> bf16, round to nearest even), including signed zeros, NaN, ties and overflow.
+    Reading: relu returns +0 for every non-positive value, -0 included (the library keeps the
+    sign of a zero; adding +0 clears it), and passes NaN through."""
+    rng = _rng(90)
+    z = rng.normal(0, 10, 4096)
+    z[:12] = [0.0, -0.0, np.nan, -np.nan, np.inf, -np.inf, 3.0e38, -3.0e38, 1.0 + 2.0 ** -8,
+              1.0 + 3 * 2.0 ** -8, 1e-40, -1e-40]
+    zt = torch.from_numpy(z)
+    for act in ("relu", "identity"):
+        ref = (torch.relu(zt) + 0.0 if act == "relu" else zt).to(torch.float32)
+        got32 = O.activation_to_storage(z, act, "f32")
+        assert got32.dtype == np.float32
+        assert np.array_equal(got32.view(np.uint32)[~np.isnan(got32)],
+                              ref.numpy().view(np.uint32)[~np.isnan(got32)])
+        assert np.array_equal(np.isnan(got32), torch.isnan(ref).numpy())
+        bits = O.activation_to_storage(z, act, "bf16")
+        rb = ref.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+        fin = ~torch.isnan(ref).numpy()
+        assert np.array_equal(bits[fin], rb[fin])
+        assert np.all(np.isnan(O.bf16_bits_to_f32(bits[~fin])))
+    # relu keeps no negative value; identity keeps the sign
+    assert not np.any(O.bf16_bits_to_f32(O.activation_to_storage(z, "relu", "bf16")) < 0)
+    assert np.any(O.bf16_bits_to_f32(O.activation_to_storage(z, "identity", "bf16")) < 0)
+
+
+@pytest.mark.parametrize("n_in,k,stride,pad", [(7, 3, 1, 1), (7, 3, 2, 1), (8, 5, 3, 2), (1, 1, 1, 0), (9, 7, 2, 0)])
+def test_out_size_and_blocks_match_library(n_in, k, stride, pad):
+    z = F.conv2d(torch.zeros(1, 1, n_in, n_in + 1), torch.zeros(1, 1, k, k), stride=stride, padding=pad)
+    assert (O.out_size(n_in, k, stride, pad), O.out_size(n_in + 1, k, stride, pad)) == tuple(z.shape[2:])
+    for b in (1, 2, 3, 16):
+        pooled = F.max_pool2d(torch.zeros(1, 1, z.shape[2], z.shape[3]), b, b, ceil_mode=True)
+        assert (O.n_blocks(z.shape[2], b), O.n_blocks(z.shape[3], b)) == tuple(pooled.shape[2:])
+
+
+def test_translate_bruteforce():
+    rng = _rng(91)
+    x = rng.normal(0, 1, (2, 6, 7, 3))
+    for dy, dx in [(0, 0), (1, 0), (-2, 3), (5, -6), (6, 0), (0, -7)]:
+        t = O.translate(x, dy, dx)
+        ref = np.zeros_like(x)
+        for i in range(6):
+            for j in range(7):
+                if 0 <= i - dy < 6 and 0 <= j - dx < 7:
+                    ref[:, i, j] = x[:, i - dy, j - dx]
+        assert np.array_equal(t, ref)
