@@ -247,36 +247,36 @@ def test_stack6_relu_strided(split):
 
 # ------------------------------ stacks at calibrated densities, free-running --
 
-def _dense_chain_stats(frames, weights, specs, *, dtype, act, block):
-    """Gate statistics of frames 2.. of every layer on its own input, in the oracle's dense
-    chain (eps = 0 everywhere): the calibration source for per-layer thresholds."""
-    n, h, w, _ = frames[0].shape
-    orcs, hh, ww = [], h, w
-    for wt, sp in zip(weights, specs):
-        o = O.SkipConvOracle(weight_storage(wt, dtype), n=n, h=hh, w=ww, stride=sp.stride, groups=sp.groups,
-                             eps=0.0, block=block, dtype=dtype)
-        orcs.append(o)
-        hh, ww = o.h_out, o.w_out
-    stats = [[] for _ in orcs]
-    for t, f in enumerate(frames):
-        x = syn.to_storage(f, dtype)
-        for i, o in enumerate(orcs):
-            out = o.step(x)
-            if t > 0:
-                stats[i].append(out["stat"])
-            x = O.activation_to_storage(out["z"], act, dtype)
-    return stats, [(o.h_out, o.w_out) for o in orcs]
-
-
-_CHAIN_STATS = {}
+_CHAIN_EPS = {}
 
 
 def _calibrated_eps(frames, weights, specs, *, act, block, density, key):
-    """Per-layer thresholds for `density`; the dense-chain statistics are computed once per key."""
-    if key not in _CHAIN_STATS:
-        _CHAIN_STATS[key] = _dense_chain_stats(frames, weights, specs, dtype="bf16", act=act, block=block)
-    stats, shapes = _CHAIN_STATS[key]
-    return [eps_for_density(st, block, ho, wo, density) for st, (ho, wo) in zip(stats, shapes)]
+    """Per-layer thresholds for a block density near `density` on each layer's own input,
+    layer by layer in the oracle: a layer's threshold is the quantile of its gate statistic
+    over the calibration frames, and the oracle layer run at that threshold gives the next
+    layer's input (so an inner layer is calibrated on the sparse residuals it will see)."""
+    ck = (key, density)
+    if ck in _CHAIN_EPS:
+        return _CHAIN_EPS[ck]
+    xs = [syn.to_storage(f, "bf16") for f in frames]
+    n, h, w, _ = frames[0].shape
+    epss = []
+    for wt, sp in zip(weights, specs):
+        k = wt.shape[2]
+        pad = (k - 1) // 2
+        ho, wo = O.out_size(h, k, sp.stride, pad), O.out_size(w, k, sp.stride, pad)
+        stats = []
+        for t in range(1, len(xs)):
+            r = O.residual(O.bf16_bits_to_f32(xs[t]), O.bf16_bits_to_f32(xs[t - 1]))
+            stats.append(O.support_stat(O.pixel_stat(r, 2), k, sp.stride, pad, ho, wo))
+        e = eps_for_density(stats, block, ho, wo, density)
+        epss.append(e)
+        orc = O.SkipConvOracle(weight_storage(wt, "bf16"), n=n, h=h, w=w, stride=sp.stride, groups=sp.groups,
+                               eps=e, block=block, dtype="bf16")
+        xs = [O.activation_to_storage(orc.step(x)["z"], act, "bf16") for x in xs]
+        h, w = ho, wo
+    _CHAIN_EPS[ck] = epss
+    return epss
 
 
 def _mac_density(dens):
@@ -292,7 +292,7 @@ def test_mbconv192_calibrated_densities(density, split):
     frames = list(wl.video(10))
     ws = wl.weights()
     epss = _calibrated_eps(frames[:6], ws, wl.layers, act="identity", block=8, density=density,
-                          key="mbconv192")
+                           key="mbconv192")
     dens = []
     run_chain(frames, ws, wl.layers, dtype="bf16", act="identity", epss=epss, block=8,
               tag=f"mbconv192 d={density}", split=split, keep_stats=False, dens_out=dens)
@@ -318,9 +318,14 @@ def test_stack6_calibrated_densities(density, split):
 
 
 def test_stack6_free_running():
-    """The GPU stack steps on its own activations and the oracle stack on its own: a bf16 ulp of
-    difference in an inner layer's input can move a site across eps, so masks may differ at a few
-    sites; the count is reported and bounded, z stays within the tolerance."""
+    """The GPU stack steps on its own activations and the oracle stack on its own. A bf16 ulp of
+    difference in an inner layer's input can move a site across eps, so masks may differ at a
+    few sites; the count is reported and bounded. A site whose mask differed carries the skipped
+    (or extra) update in z from then on, and so does every later-layer site whose kernel support
+    reaches it: those sites are tracked ("tainted") and z must agree within the tolerance on
+    all the others."""
+    import torch.nn.functional as F
+
     wl = syn.workloads()["stack6"]
     frames = list(wl.video(10))
     ws = wl.weights()
@@ -335,6 +340,7 @@ def test_stack6_free_running():
         hh, ww = lay.h_out, lay.w_out
     diffs = np.zeros(len(layers), np.int64)
     sites = np.zeros(len(layers), np.int64)
+    taint = [np.zeros((1, l.h_out, l.w_out), bool) for l in layers]
     for t, f in enumerate(frames):
         x_dev = to_device(syn.to_storage(f, "bf16"), "bf16")
         x_host = syn.to_storage(f, "bf16")
@@ -343,21 +349,35 @@ def test_stack6_free_running():
             ref = orc.step(x_host)
             torch.cuda.synchronize()
             m = lay.block_mask().astype(bool)
-            d = int(np.sum(m ^ ref["block_mask"]))
+            dm = m ^ ref["block_mask"]
+            d = int(dm.sum())
             if i == 0:
                 assert d == 0, f"free stack t={t}: layer 1 sees the same input and must agree"
+            else:
+                # sites whose kernel support reaches a tainted input pixel
+                sp = wl.layers[i]
+                k = ws[i].shape[2]
+                up = torch.from_numpy(taint[i - 1].astype(np.float32))[:, None]
+                reach = F.max_pool2d(up, k, sp.stride, (k - 1) // 2)[:, 0].numpy() > 0
+                taint[i] |= reach
+            taint[i] |= dm
             diffs[i] += d
             sites[i] += m.size
-            e = rel_err(lay._z.cpu().numpy(), ref["z"])
-            say(f"[stack6 free] frame {t} layer {i}: {d} mask differences, z rel err {e:.2e}")
+            zg = lay._z.cpu().numpy()
+            keep = ~taint[i]
+            e = rel_err(zg[keep], ref["z"][keep])
+            say(f"[stack6 free] frame {t} layer {i}: {d} mask differences, {int(taint[i].sum())} tainted "
+                f"sites, z rel err {e:.2e} elsewhere (all sites {rel_err(zg, ref['z']):.2e})")
             assert e <= TOL["bf16"], f"free stack t={t} L{i}: z rel err {e:.2e}"
             if i + 1 < len(layers):
                 x_dev = lay.activation()
                 x_host = O.activation_to_storage(ref["z"], "relu", "bf16")
     for lay in layers:
         lay.close()
-    say(f"[stack6 free] mask differences per layer {diffs.tolist()} of {sites.tolist()} site-frames")
+    say(f"[stack6 free] mask differences per layer {diffs.tolist()} of {sites.tolist()} site-frames; "
+        f"tainted sites at the end {[int(x.sum()) for x in taint]}")
     assert np.all(diffs <= 0.01 * sites)
+    assert all(x.mean() <= 0.05 for x in taint)
 
 
 # ------------------------------------------- full size 4 x 512 x 512 x 128 --
