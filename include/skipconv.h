@@ -229,6 +229,33 @@ int skipconv_step_translated(skipconv_t h, const void* x_t, int32_t dy, int32_t 
  * its residual or has not stepped), E_HIP. */
 int skipconv_step_chained(skipconv_t h, skipconv_t up, void* stream, const float** z_t);
 
+/* One step for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation):
+ * the split-pipeline step of a layer with caller-retained frames, with no
+ * handle and no workspace. Allocates nothing: every buffer its kernels use
+ * beyond the arguments (work list and its counters, block flags, packed
+ * weights) sits in one fixed device array of 4 MiB inside the library, one
+ * per device, held until the process ends.
+ *   d:       descriptor as for skipconv_create; flags 0 or FORCE_DENSE only,
+ *            the Input-Norm gate, no activation output, and blocks no larger
+ *            than the gate tile (E_UNSUPPORTED otherwise). A layer whose
+ *            weights and work list need more than 4 MiB is rejected with
+ *            E_SMALL_BUFFER (skipconv_last_error(NULL) names both sizes).
+ *   weights: device pointer, OIHW in d->dtype, repacked into the array on
+ *            every call.
+ *   x_t:     device pointer, N x H x W x C_in, 16-byte aligned.
+ *   x_prev:  the previous frame (same layout), or NULL for a reference frame
+ *            (x_{t-1} taken as zero, every site on, z assigned).
+ *   z:       device pointer, N x H_out x W_out x C_out fp32, 16-byte aligned:
+ *            z_{t-1} on entry (not read on a reference frame), z_t on exit.
+ * Enqueued on `stream`; the results equal those of skipconv_step on a layer
+ * created with SKIPCONV_FLAG_SPLIT_PIPELINE | SKIPCONV_FLAG_CALLER_RETAINS.
+ * Every call on a device shares that device's array and leaves its contents
+ * behind: calls that overlap on one device (different streams, or threads)
+ * race and must be serialised by the caller. */
+int skipconv_step_static(const skipconv_desc* d, const void* weights, const void* x_t, const void* x_prev,
+                         float* z, void* stream);
+
 /* Make the next step a reference frame: x_{t-1} taken as zero, every site
  * active, z assigned instead of accumulated (Sec. 3.1, Table 4). */
 int skipconv_reset(skipconv_t h);

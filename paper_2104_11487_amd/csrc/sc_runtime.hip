@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -676,13 +677,9 @@ double threshold(const skipconv_desc& d) {
   return d.norm_p == 2 ? e * e : e;
 }
 
-sc::GateParams gate_params(skipconv_layer* h, const void* x_t, bool ref) {
-  const skipconv_desc& d = h->d;
-  const Geometry& g = h->g;
+// Gate parameters that follow from the descriptor and geometry alone (no buffers).
+sc::GateParams gate_geometry(const skipconv_desc& d, const Geometry& g, bool ref) {
   sc::GateParams gp{};
-  gp.x_t = x_t;
-  gp.x_prev = h->prev_input(x_t);
-  gp.x_keep = h->keep_slot();
   gp.n = d.n; gp.h = d.h; gp.w = d.w; gp.c = d.c_in;
   gp.h_out = g.h_out; gp.w_out = g.w_out; gp.k = d.kernel; gp.stride = d.stride; gp.pad = g.pad;
   gp.block = d.block; gp.hb = g.hb; gp.wb = g.wb;
@@ -693,16 +690,79 @@ sc::GateParams gate_params(skipconv_layer* h, const void* x_t, bool ref) {
   gp.force_dense = (d.flags & SKIPCONV_FLAG_FORCE_DENSE) ? 1 : 0;
   gp.keep_stats = (d.flags & SKIPCONV_FLAG_KEEP_STATS) ? 1 : 0;
   gp.thr = threshold(d);
-  gp.wnorm = h->wnorm;
+  gp.wnorm = 1.0;
   gp.learned = g.learned;
+  gp.phi_off = g.phi_in_lds ? g.phi_off : -1;
+  gp.split_blocks = g.split_blocks;
+  return gp;
+}
+
+sc::GateParams gate_params(skipconv_layer* h, const void* x_t, bool ref) {
+  sc::GateParams gp = gate_geometry(h->d, h->g, ref);
+  gp.x_t = x_t;
+  gp.x_prev = h->prev_input(x_t);
+  gp.x_keep = h->keep_slot();
+  gp.wnorm = h->wnorm;
   gp.phi = h->phi();
   gp.gate_bias = h->gate_bias;
-  gp.phi_off = g.phi_in_lds ? g.phi_off : -1;
   gp.block_mask = h->bmask(); gp.list = h->list(); gp.counters = h->ctr();
-  gp.tile_flags = h->tflags(); gp.split_blocks = g.split_blocks;
+  gp.tile_flags = h->tflags();
   gp.stat = h->stat(); gp.site_mask = h->smask();
-
   return gp;
+}
+
+// Convolution parameters that follow from the descriptor and geometry alone.
+sc::ConvParams conv_geometry(const skipconv_desc& d, const Geometry& g, bool ref) {
+  sc::ConvParams cp{};
+  cp.n = d.n; cp.h = d.h; cp.w = d.w; cp.c = d.c_in; cp.c_out = d.c_out;
+  cp.h_out = g.h_out; cp.w_out = g.w_out; cp.k = d.kernel; cp.stride = d.stride; cp.pad = g.pad;
+  cp.block = d.block; cp.hb = g.hb; cp.wb = g.wb;
+  cp.ksteps = g.ksteps; cp.ntiles_n = g.ntn;
+  cp.reference = ref ? 1 : 0;
+  cp.no_prev = ref ? 1 : 0;
+  cp.act = (d.flags & SKIPCONV_FLAG_EMIT_RESIDUAL) ? 0 : d.act_out;
+  return cp;
+}
+
+// The split pipeline's convolution kernel for this geometry.
+hipError_t launch_split_conv(const Geometry& g, const skipconv_desc& d, const sc::ConvParams& cp, int grid,
+                             hipStream_t st) {
+  if (g.depthwise)
+    return g.dw_halo ? sc::launch_depthwise_halo(cp, g.dwp, grid, st) : sc::launch_depthwise(cp, d.dtype, grid, st);
+  if (g.halo) return sc::launch_conv_halo(cp, g.hp, grid, st);
+  return sc::launch_conv(cp, d.dtype, g.fast, grid, st);
+}
+
+// Check that the split pipeline's convolution kernel fits the device (else
+// fall back to the per-site kernels) and return its resident workgroups per CU.
+int conv_setup(Geometry& g, const skipconv_desc* d, int device) {
+  int occ_out = 4;
+  if (g.dw_halo) {
+    const int occ = sc::depthwise_halo_occupancy(g.dwp, d->kernel, d->c_in);
+    if (occ < 1) {
+      g.dw_halo = false;  // cannot hold the halo: per-site depthwise kernel
+      g.conv_max_tiles = (int)(((long)g.nb * d->block * d->block + 63) / 64);
+    } else {
+      occ_out = std::min(8, occ);
+    }
+  }
+  if (g.halo) {
+    int max_lds = 0;
+    if (hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, device) != hipSuccess ||
+        max_lds < g.hp.lds_bytes) {
+      g.halo = false;  // this device cannot hold the halo: gather kernel
+      g.conv_max_tiles = (int)(((long)g.nb * d->block * d->block + 63) / 64);
+    } else {
+      occ_out = std::max(1, std::min(8, sc::conv_halo_occupancy(g.hp)));
+    }
+  }
+  return occ_out;
+}
+
+int conv_grid_of(const Geometry& g, int num_cu, int occ) {
+  int grid = std::min(g.conv_max_tiles, num_cu * occ);
+  if (grid >= 8) grid = (grid + 7) / 8 * 8;
+  return std::max(grid, 1);
 }
 
 hipError_t launch_compaction(skipconv_layer* h, hipStream_t st) {
@@ -761,11 +821,49 @@ void end_list(skipconv_layer* h) {
   h->wslot ^= 1;
 }
 
-int conv_grid(const skipconv_layer* h) {
-  int grid = std::min(h->g.conv_max_tiles, h->num_cu * h->conv_occ);
-  if (grid >= 8) grid = (grid + 7) / 8 * 8;
-  return std::max(grid, 1);
+int conv_grid(const skipconv_layer* h) { return conv_grid_of(h->g, h->num_cu, h->conv_occ); }
+
+// ---- scratch of skipconv_step_static ----
+// The work list, its counters, the block flags and the packed weights of a
+// step made by skipconv_step_static live in one file-scope device array of
+// fixed size. Each device holds its own copy, at its own address, until the
+// process ends; host code reaches it only through the address that
+// hipGetSymbolAddress returns on that device (the array's name is a host-side
+// stand-in, not a device address).
+constexpr size_t kStaticScratchBytes = (size_t)4 << 20;
+constexpr int kMaxStaticDevices = 64;
+static __device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
+std::mutex g_static_mu;
+void* g_static_ptr[kMaxStaticDevices];
+int g_static_cu[kMaxStaticDevices];
+
+// Once per device, with that device current: the scratch array's device
+// address and the device's CU count.
+int static_scratch(void** ptr, int* device, int* num_cu) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(g_create_error, SKIPCONV_E_HIP, "hipGetDevice failed");
+  if (dev < 0 || dev >= kMaxStaticDevices) return fail(g_create_error, SKIPCONV_E_UNSUPPORTED, "device index too large");
+  std::lock_guard<std::mutex> lock(g_static_mu);
+  if (!g_static_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      snprintf(g_create_error, sizeof(g_create_error), "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+      return SKIPCONV_E_HIP;
+    }
+    int cu = 0;
+    e = hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess || cu < 1) return fail(g_create_error, SKIPCONV_E_HIP, "CU count query failed");
+    g_static_cu[dev] = cu;
+    g_static_ptr[dev] = p;
+  }
+  *ptr = g_static_ptr[dev];
+  *device = dev;
+  *num_cu = g_static_cu[dev];
+  return SKIPCONV_OK;
 }
+
 
 void destroy_events(skipconv_layer* h) {
   for (hipEvent_t e : h->ev) (void)hipEventDestroy(e);
@@ -857,25 +955,7 @@ int skipconv_create(const skipconv_desc* d, const void* weights, void* workspace
   if (h->g.fused && (h->g.f_grid * ((h->g.f_rb || h->g.f_dw) ? h->g.f_nsplit : 1) > 4 * h->num_cu ||
                      sc::prepare_fused(fused_params(h, nullptr, true)) < 1))
     h->g.fused = false;
-  if (g.dw_halo) {
-    const int occ = sc::depthwise_halo_occupancy(g.dwp, d->kernel, d->c_in);
-    if (occ < 1) {
-      h->g.dw_halo = false;  // cannot hold the halo: per-site depthwise kernel
-      h->g.conv_max_tiles = (int)(((long)g.nb * d->block * d->block + 63) / 64);
-    } else {
-      h->conv_occ = std::min(8, occ);
-    }
-  }
-  if (g.halo) {
-    int max_lds = 0;
-    if (hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, h->device) != hipSuccess ||
-        max_lds < g.hp.lds_bytes) {
-      h->g.halo = false;  // this device cannot hold the halo: gather kernel
-      h->g.conv_max_tiles = (int)(((long)g.nb * d->block * d->block + 63) / 64);
-    } else {
-      h->conv_occ = std::max(1, std::min(8, sc::conv_halo_occupancy(g.hp)));
-    }
-  }
+  h->conv_occ = conv_setup(h->g, d, h->device);
   if (workspace) {
     h->ws = static_cast<char*>(workspace);
   } else {
@@ -973,14 +1053,7 @@ int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t
     cp.zero_ctr = sl.zero;
     cp.seg_tiles = sl.seg_tiles;
     cp.seg_cap = sl.seg_cap;
-    if (e == hipSuccess) {
-      if (g.depthwise)
-        e = (g.dw_halo ? sc::launch_depthwise_halo(cp, g.dwp, conv_grid(h), st) : sc::launch_depthwise(cp, d.dtype, conv_grid(h), st));
-      else if (g.halo)
-        e = sc::launch_conv_halo(cp, g.hp, conv_grid(h), st);
-      else
-        e = sc::launch_conv(cp, d.dtype, g.fast, conv_grid(h), st);
-    }
+    if (e == hipSuccess) e = launch_split_conv(g, d, cp, conv_grid(h), st);
     if (e != hipSuccess) return hip_fail(h, e, "conv launch");
     end_list(h);
   }
@@ -1061,12 +1134,7 @@ int skipconv_step_translated(skipconv_t h, const void* x_t, int32_t dy, int32_t 
     cp.no_prev = pass;
     cp.sy = pass ? 0 : dy;
     cp.sx = pass ? 0 : dx;
-    if (g.depthwise)
-      e = (g.dw_halo ? sc::launch_depthwise_halo(cp, g.dwp, conv_grid(h), st) : sc::launch_depthwise(cp, d.dtype, conv_grid(h), st));
-    else if (g.halo)
-      e = sc::launch_conv_halo(cp, g.hp, conv_grid(h), st);
-    else
-      e = sc::launch_conv(cp, d.dtype, g.fast, conv_grid(h), st);
+    e = launch_split_conv(g, d, cp, conv_grid(h), st);
   }
   if (e != hipSuccess) return hip_fail(h, e, "translated conv launch");
   end_list(h);
@@ -1150,12 +1218,7 @@ int skipconv_step_chained(skipconv_t h, skipconv_t up, void* stream, const float
   cp.reference = 0;
   cp.no_prev = 1;
   cp.act = h->emits() ? 0 : d.act_out;
-  if (g.depthwise)
-    e = (g.dw_halo ? sc::launch_depthwise_halo(cp, g.dwp, conv_grid(h), st) : sc::launch_depthwise(cp, d.dtype, conv_grid(h), st));
-  else if (g.halo)
-    e = sc::launch_conv_halo(cp, g.hp, conv_grid(h), st);
-  else
-    e = sc::launch_conv(cp, d.dtype, g.fast, conv_grid(h), st);
+  e = launch_split_conv(g, d, cp, conv_grid(h), st);
   if (e != hipSuccess) return hip_fail(h, e, "chained conv launch");
   if (h->emits()) {
     e = launch_emit(h, st);
@@ -1430,6 +1493,82 @@ int skipconv_timing_read(skipconv_t h, void* stream, double* ms, int* frames_tim
     if (step_index) step_index[i] = h->ev_step[i];
   }
   if (frames_timed) *frames_timed = h->timing_done;
+  return SKIPCONV_OK;
+}
+
+int skipconv_step_static(const skipconv_desc* d, const void* weights, const void* x_t, const void* x_prev,
+                         float* z, void* stream) {
+  if (!d || !weights || !x_t || !z) return fail(g_create_error, SKIPCONV_E_INVALID_ARG, "NULL argument");
+  if (reinterpret_cast<uintptr_t>(x_t) % 16 || reinterpret_cast<uintptr_t>(x_prev) % 16 ||
+      reinterpret_cast<uintptr_t>(z) % 16)
+    return fail(g_create_error, SKIPCONV_E_INVALID_ARG, "x_t, x_prev and z must be 16-byte aligned");
+  if (x_prev == x_t) return fail(g_create_error, SKIPCONV_E_INVALID_ARG, "x_prev is x_t");
+  if (d->flags & ~(uint32_t)SKIPCONV_FLAG_FORCE_DENSE)
+    return fail(g_create_error, SKIPCONV_E_UNSUPPORTED, "skipconv_step_static takes no flags but FORCE_DENSE");
+  if (d->gate != SKIPCONV_GATE_INPUT_NORM)
+    return fail(g_create_error, SKIPCONV_E_UNSUPPORTED, "skipconv_step_static takes the Input-Norm gate only");
+  if (d->act_out != SKIPCONV_ACT_NONE)
+    return fail(g_create_error, SKIPCONV_E_UNSUPPORTED, "skipconv_step_static has no activation output");
+  skipconv_desc dd = *d;
+  dd.flags |= SKIPCONV_FLAG_SPLIT_PIPELINE | SKIPCONV_FLAG_CALLER_RETAINS;
+  Geometry g;
+  int rc = derive(&dd, &g, g_create_error);
+  if (rc) return rc;
+  if (g.split_blocks)
+    return fail(g_create_error, SKIPCONV_E_UNSUPPORTED, "skipconv_step_static: blocks larger than the gate tile");
+  // scratch layout: work-list counters, packed weights, block flags, work list
+  const size_t off_wpack = align_up((size_t)sc::kSegs * sc::kSegStride * 4);
+  const size_t off_bmask = align_up(off_wpack + g.wpack_bytes);
+  const size_t off_wlist = align_up(off_bmask + (size_t)g.nb + 16);
+  const size_t need = off_wlist + (size_t)std::max<long>(g.nb, (long)g.gate_grid * g.seg_cap) * 4;
+  if (need > kStaticScratchBytes) {
+    snprintf(g_create_error, sizeof(g_create_error),
+             "skipconv_step_static: the layer needs %zu bytes of scratch, the static scratch holds %zu", need,
+             kStaticScratchBytes);
+    return SKIPCONV_E_SMALL_BUFFER;
+  }
+  void* base = nullptr;
+  int dev = 0, num_cu = 0;
+  rc = static_scratch(&base, &dev, &num_cu);
+  if (rc) return rc;
+  const int occ = conv_setup(g, &dd, dev);
+  char* sb = static_cast<char*>(base);
+  uint32_t* ctr = reinterpret_cast<uint32_t*>(sb);
+  void* wpack = sb + off_wpack;
+  uint8_t* bmask = reinterpret_cast<uint8_t*>(sb + off_bmask);
+  uint32_t* wlist = reinterpret_cast<uint32_t*>(sb + off_wlist);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const bool ref = x_prev == nullptr;
+
+  // the previous call's counters are not zero: clear them with a kernel
+  hipError_t e = sc::launch_fill_u32(ctr, sc::kSegs * sc::kSegStride, 0u, st);
+  if (e == hipSuccess)
+    e = g.depthwise ? sc::launch_pack_depthwise(weights, static_cast<float*>(wpack), dd.dtype, dd.c_in, dd.kernel, st)
+                    : sc::launch_pack_mfma(weights, wpack, dd.dtype, dd.c_out, dd.c_in, dd.kernel, g.ksteps, g.ntn, st);
+  sc::GateParams gp = gate_geometry(dd, g, ref);
+  gp.x_t = x_t;
+  gp.x_prev = ref ? x_t : x_prev;
+  gp.x_keep = nullptr;
+  gp.block_mask = bmask;
+  gp.counters = ctr;
+  gp.wlist = wlist;
+  gp.wctr = ctr;
+  gp.seg_cap = g.seg_cap;
+  if (e == hipSuccess) e = sc::launch_gate(gp, dd.dtype, g.vec, g.gate_grid, g.gate_lds, st);
+  sc::ConvParams cp = conv_geometry(dd, g, ref);
+  cp.x_t = x_t;
+  cp.x_prev = ref ? x_t : x_prev;
+  cp.wpack = wpack;
+  cp.z = z;
+  cp.list = wlist;
+  cp.counters = ctr;
+  cp.seg_tiles = g.gate_grid;
+  cp.seg_cap = g.seg_cap;
+  if (e == hipSuccess) e = launch_split_conv(g, dd, cp, conv_grid_of(g, num_cu, occ), st);
+  if (e != hipSuccess) {
+    snprintf(g_create_error, sizeof(g_create_error), "skipconv_step_static: %s", hipGetErrorString(e));
+    return SKIPCONV_E_HIP;
+  }
   return SKIPCONV_OK;
 }
 

@@ -62,6 +62,7 @@ _SIGS = {
     "skipconv_step": (ctypes.c_int, [_P, _P, _P, ctypes.POINTER(_P)]),
     "skipconv_step_chained": (ctypes.c_int, [_P, _P, _P, ctypes.POINTER(_P)]),
     "skipconv_step_translated": (ctypes.c_int, [_P, _P, ctypes.c_int32, ctypes.c_int32, _P, ctypes.POINTER(_P)]),
+    "skipconv_step_static": (ctypes.c_int, [_D, _P, _P, _P, _P, _P]),
     "skipconv_reset": (ctypes.c_int, [_P]),
     "skipconv_set_eps": (ctypes.c_int, [_P, ctypes.c_float]),
     "skipconv_set_gate_weights": (ctypes.c_int, [_P, _P, ctypes.c_float, _P]),
@@ -154,6 +155,11 @@ def skipconv_step(h: int, x_ptr: int, stream: int) -> int:
     z = ctypes.c_void_p()
     _check(lib().skipconv_step(h, x_ptr, stream, ctypes.byref(z)), h)
     return z.value
+
+
+def skipconv_step_static(d: skipconv_desc, weights_ptr: int, x_ptr: int, x_prev_ptr: Optional[int],
+                         z_ptr: int, stream: int) -> None:
+    _check(lib().skipconv_step_static(ctypes.byref(d), weights_ptr, x_ptr, x_prev_ptr, z_ptr, stream))
 
 
 def skipconv_step_chained(h: int, up: int, stream: int) -> int:
