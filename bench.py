@@ -498,6 +498,24 @@ def summarize_trace(db: str, out_md: str, command: str) -> None:
     print("\n".join(lines))
 
 
+def summarize_counters(db: str, out_md: str, command: str) -> None:
+    """Markdown table of the per-dispatch average of every counter in a rocprofv3 --pmc database, per kernel."""
+    import sqlite3
+
+    con = sqlite3.connect(db)
+    rows = con.execute("select kernel_name, counter_name, count(*), avg(value) from counters_collection "
+                       "group by kernel_name, counter_name order by kernel_name, counter_name").fetchall()
+    con.close()
+    lines = [f"# rocprofv3 counters: {os.path.basename(db)}", "", "Command:", "", "```", command, "```", "",
+             "| kernel | counter | dispatches | average per dispatch |", "|---|---|---:|---:|"]
+    for name, counter, n, avg in rows:
+        short = name.replace("(anonymous namespace)::", "").split("(sc::")[0].split("(unsigned")[0]
+        lines.append(f"| `{short[:90]}` | {counter} | {n} | {avg:.6g} |")
+    with open(out_md, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 # ----------------------------------------------------------------- stacks --
 
 def bench_stack(args):
@@ -816,9 +834,14 @@ def main():
                     help="write a markdown summary of a rocprofv3 --kernel-trace database")
     ap.add_argument("--summarize-pmc", nargs=3, metavar=("FETCH_DB", "WRITE_DB", "OUT_JSON"),
                     help="turn the databases of two rocprofv3 --pmc runs into a traffic summary")
+    ap.add_argument("--summarize-counters", nargs=3, metavar=("PMC_DB", "OUT_MD", "COMMAND"),
+                    help="write a markdown summary of any rocprofv3 --pmc database")
     args = ap.parse_args()
     if args.summarize_trace:
         summarize_trace(*args.summarize_trace)
+        return
+    if args.summarize_counters:
+        summarize_counters(*args.summarize_counters)
         return
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc, workload=args.workload, copy_mib=args.copy_probe)

@@ -24,6 +24,7 @@
 // Depthwise layers (groups = C): no contraction to speak of, so no MFMA; one
 // thread per (site, 8 channels) sums the k x k taps with fp32 FMAs.
 #include "sc_device.h"
+#include "sc_halo_conv.h"
 #include "sc_kernels.h"
 #include "sc_stream.h"
 
@@ -34,13 +35,6 @@ namespace {
 constexpr int kConvThreads = 256;
 constexpr int kRowsPerTile = 64;
 
-typedef float floatx2 __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-
-// bf16 round-to-nearest-even of two floats, packed (v_cvt_pk_bf16_f32).
-__device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2{a, b}, bf16x2));
-}
 
 struct Site {
   int n, oy, ox;
@@ -87,7 +81,6 @@ struct TileWalk {
   }
 };
 
-__device__ __forceinline__ float activate(float v, int act) { return act == 2 ? relu_f32(v) : v; }
 
 template <typename T>
 __device__ __forceinline__ void store_y(void* y, size_t i, float v) {
@@ -254,261 +247,64 @@ __global__ void __launch_bounds__(kConvThreads) conv_bf16_kernel(ConvParams p) {
 // ------------------------------------------------------- bf16, halo ----
 //
 // Block tiles (b in {4, 8, 16, 32, 64}, C_in % 32 == 0): a tile is `tr` output
-// rows x b columns of one active block. Per tile:
-//   1. the accumulators start from z_{t-1} of the tile's sites (0 on a
-//      reference frame), loaded straight into the MFMA output layout, so the
-//      read half of the z update overlaps the halo load;
-//   2. the input halo ((tr-1)s+k rows x (b-1)s+k columns x C_in) is loaded with
-//      16-byte loads, eight per thread in flight, turned into
-//      rho = bf16(x_t - x_{t-1}) and stored in LDS with a pixel stride of
-//      2*C_in + 16 bytes (16 consecutive pixels read 16 bytes each on distinct
-//      banks);
-//   3. MFMA A fragments are read straight from the halo (row m of the tile at
-//      tap (kh, kw) is halo pixel (ly*s + kh, lx*s + kw): no im2col copy); B
-//      fragments come from the packed weights (L1/L2) one k-step ahead of use;
-//   4. the accumulators are stored back to z (and the activation output).
-// Waves are laid out WAVES_M x WAVES_N; each owns WM x WN 16x16 output tiles.
+// rows x b columns of one active block, convolved by HaloConv (sc_halo_conv.h).
+// A persistent grid walks the tiles of the listed blocks; with PZ the next
+// tile's z_{t-1} is issued before this tile's stores (sites of different tiles
+// are disjoint), into registers that are not the stores' sources, so no wait
+// on the stores precedes them; the halo loads of a tile then wait once for
+// everything in flight. Without PZ a tile's z_{t-1} is loaded with its halo.
+// OCC: waves per SIMD the register budget aims for.
 
-template <int WAVES_M, int WAVES_N, int WM, int WN>
-__global__ void __launch_bounds__(64 * WAVES_M * WAVES_N) __attribute__((amdgpu_waves_per_eu(2)))
+template <int WAVES_M, int WAVES_N, int WM, int WN, int KR = 0, bool PZ = true, int OCC = 2, int KU = 12,
+          int ADB = 2>
+__global__ void __launch_bounds__(64 * WAVES_M * WAVES_N) __attribute__((amdgpu_waves_per_eu(OCC)))
 conv_halo_kernel(ConvParams p, HaloParams hp) {
   extern __shared__ __attribute__((aligned(16))) uint8_t halo[];
-  constexpr int kThreads = 64 * WAVES_M * WAVES_N;
-  constexpr int kUnroll = 12;  // halo items (two 16-byte loads each) in flight per thread
-  constexpr int kR = WN <= 2 ? 8 : (WN == 3 ? 6 : 4);  // B register ring (kR - 1 k-steps of lookahead), even
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave % WAVES_M, wn = wave / WAVES_M;
-  const int r16 = lane & 15, kq = lane >> 4;
-  const int b = p.block, s = p.stride, k = p.k, c = p.c;
-  const int lb = __ffs(b) - 1;
+  typedef HaloConv<WAVES_M, WAVES_N, WM, WN, KR, KU, ADB> HC;
   const int tpb = hp.tiles_per_block;
   const WorkList W = work_list(p.counters, p.seg_tiles, p.seg_cap);
   const int ntiles = (int)W.total * tpb;
   if (p.zero_ctr && blockIdx.x == 0 && threadIdx.x < kSegs) p.zero_ctr[threadIdx.x * kSegStride] = 0u;  // next step's work list
-  const uint16_t* xt = static_cast<const uint16_t*>(p.x_t);
-  const uint16_t* xp = static_cast<const uint16_t*>(p.x_prev);
-  // packed weights through a buffer resource: lane offset in a VGPR, the
-  // (k-step, column tile) offset in an SGPR
-  const __amdgpu_buffer_rsrc_t wrs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p.wpack), 0, p.ksteps * p.ntiles_n * 1024, 0x00020000);
-  const int boff = lane * 16;
-  const int wn0 = __builtin_amdgcn_readfirstlane(wn) * WN;  // first 16-channel output tile
-  const int chunks_per_px = c >> 3;
-  const int csteps = c >> 5;  // k-steps per tap
-  const size_t ximg = (size_t)p.h * p.w * c;              // elements of one input image
-  const size_t zimg = (size_t)p.h_out * p.w_out * p.c_out;  // elements of one z image
-  const int ksteps = p.ksteps;
-  const int ntn = p.ntiles_n;
-
-  // halo byte offset of this lane's A row in each of its M-tiles, before the tap
-  int abase[WM];
-#pragma unroll
-  for (int i = 0; i < WM; ++i) {
-    const int m = (wm * WM + i) * 16 + r16;
-    const int ly = m >> lb, lx = m & (b - 1);
-    abase[i] = (ly * s * hp.hw + lx * s) * hp.pstride + kq * 16;
-  }
+  const HC H(p, hp, halo);
 
   // Tiles walked in order; the active list is read through the scalar cache
   // (written by an earlier kernel, read-only here), so decoding a tile waits
   // on no vector memory operation.
   typedef const __attribute__((address_space(4))) uint32_t const_u32;
   const const_u32* list = (const const_u32*)p.list;
-  struct HTile {
-    int n, oy0, ox0, rows_ok, cols_ok, iy0, ix0;
-  };
   auto decode = [&](int t) {
-    HTile T;
     const int j0 = t / tpb, band = t - j0 * tpb;
     const uint32_t blk = list[work_pos(W, (uint32_t)j0)];
     const int per_img = p.hb * p.wb;
-    T.n = (int)(blk / per_img);
-    const int rem = (int)(blk - (uint32_t)T.n * per_img);
+    const int n = (int)(blk / per_img);
+    const int rem = (int)(blk - (uint32_t)n * per_img);
     const int bi = rem / p.wb, bj = rem - bi * p.wb;
-    T.oy0 = bi * b + band * hp.tr;
-    T.ox0 = bj * b;
-    T.rows_ok = min(hp.tr, p.h_out - T.oy0);
-    T.cols_ok = min(b, p.w_out - T.ox0);
-    T.iy0 = T.oy0 * s - p.pad;
-    T.ix0 = T.ox0 * s - p.pad;
-    return T;
-  };
-  // z offset (bytes, within image T.n) of this lane's piece (M-tile i,
-  // column tile jn), or out of range outside the frame / past C_out
-  auto zoff = [&](const HTile& T, int i, int jn) {
-    int l16 = r16;  // opaque: recomputed per use rather than held per (i, jn)
-    asm volatile("" : "+v"(l16));
-    const int m = (wm * WM + i) * 16 + l16;
-    const int ly = m >> lb, lx = m & (b - 1);
-    const int col = (wn0 + jn) * 16 + kq * 4;
-    return (ly < T.rows_ok && lx < T.cols_ok && col < p.c_out)
-               ? (uint32_t)((((T.oy0 + ly) * p.w_out + T.ox0 + lx) * p.c_out + col) * 4)
-               : kOutOfRange;
-  };
-  auto zres = [&](const HTile& T) { return frame_rsrc(p.z + (size_t)T.n * zimg, (uint32_t)(zimg * 4)); };
-  // z_{t-1} of a tile in the transposed MFMA output layout (a lane holds 4
-  // consecutive output channels of one site: z moves in 16-byte pieces);
-  // zeros outside the frame and on a reference frame
-  // (none: every piece out of range, so the registers are always written)
-  auto load_z = [&](floatx4 (&dst)[WM][WN], const HTile& T, bool none) {
-    const auto zrs = zres(T);
-#pragma unroll
-    for (int i = 0; i < WM; ++i)
-#pragma unroll
-      for (int jn = 0; jn < WN; ++jn)
-        dst[i][jn] = __builtin_bit_cast(
-            floatx4,
-            __builtin_amdgcn_raw_buffer_load_b128(zrs, p.reference || none ? kOutOfRange : zoff(T, i, jn), 0, 0));
-  };
-  // one round of halo items: rho = bf16(x_t - x_{t-1}) into LDS. Buffer loads
-  // over image T.n with 32-bit offsets; items outside the frame (x_{t-1}:
-  // outside the translated frame, or none on a reference frame) read zeros at
-  // an out-of-range offset, so every lane issues the same loads.
-  const int total = hp.hh * hp.hw * chunks_per_px;
-  auto halo_round = [&](const HTile& T, int base) {
-    const auto xrs = frame_rsrc(xt + (size_t)T.n * ximg, (uint32_t)(ximg * 2));
-    const auto prs = frame_rsrc((p.no_prev ? xt : xp) + (size_t)T.n * ximg, (uint32_t)(ximg * 2));
-    u32x4 ra[kUnroll], rb[kUnroll];
-    // the thread index, opaque to loop-invariant code motion: the per-item
-    // terms are recomputed each round instead of occupying registers through
-    // the product loop
-    int tid = threadIdx.x;
-    asm volatile("" : "+v"(tid));
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int idx = base + u * kThreads + tid;
-      const int px = idx / chunks_per_px, ch = idx - px * chunks_per_px;
-      const int hy = px / hp.hw, hx = px - hy * hp.hw;
-      const int y = T.iy0 + hy, x = T.ix0 + hx;
-      const bool in = idx < total && y >= 0 && y < p.h && x >= 0 && x < p.w;
-      const int yp = y - p.sy, xq = x - p.sx;
-      const bool pin = in && !p.no_prev && yp >= 0 && yp < p.h && xq >= 0 && xq < p.w;
-      ra[u] = __builtin_amdgcn_raw_buffer_load_b128(
-          xrs, in ? (uint32_t)(((y * p.w + x) * c + ch * 8) * 2) : kOutOfRange, 0, 0);
-      rb[u] = __builtin_amdgcn_raw_buffer_load_b128(
-          prs, pin ? (uint32_t)(((yp * p.w + xq) * c + ch * 8) * 2) : kOutOfRange, 0, 0);
-    }
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int idx = base + u * kThreads + tid;
-      if (idx >= total) continue;
-      const int px = idx / chunks_per_px, ch = idx - px * chunks_per_px;
-      uint32_t q[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint32_t wa = ra[u][e], wb = rb[u][e];
-        const float r0 = __fsub_rn(__uint_as_float(wa << 16), __uint_as_float(wb << 16));
-        const float r1 = __fsub_rn(__uint_as_float(wa & 0xffff0000u), __uint_as_float(wb & 0xffff0000u));
-        q[e] = pack_bf16(r0, r1);
-      }
-      *reinterpret_cast<u32x4*>(halo + px * hp.pstride + ch * 16) = u32x4{q[0], q[1], q[2], q[3]};
-    }
+    return H.tile(n, bi * p.block + band * hp.tr, bj * p.block);
   };
 
-  // Software pipeline over the workgroup's tiles: the z_{t-1} loads of the
-  // next tile are issued before the stores of the current one (sites of
-  // different tiles are disjoint), into registers that are not the stores'
-  // sources, so no wait on the stores precedes them; the halo loads of a
-  // tile then wait once for everything in flight.
   TileWalk tw(ntiles);
   if (tw.t >= tw.end) return;
-  HTile T = decode(tw.t);
-  floatx4 zn[WM][WN];
-  load_z(zn, T, false);
+  HaloTile T = decode(tw.t);
+  typename HC::Acc zn;
+  if constexpr (PZ) H.load_z(zn, T, false);
   for (; tw.t < tw.end; tw.t += tw.step) {
-    // ---- 1. halo (the first round outside the loop: no loop-carried waits) ----
-    halo_round(T, 0);
-    for (int base = kThreads * kUnroll; base < total; base += kThreads * kUnroll) halo_round(T, base);
-    floatx4 acc[WM][WN];
-#pragma unroll
-    for (int i = 0; i < WM; ++i)
-#pragma unroll
-      for (int jn = 0; jn < WN; ++jn) acc[i][jn] = zn[i][jn];
-    __syncthreads();
-
-    // ---- 3. MFMA over K = (kh, kw, ci) ----
-    // B fragments are loaded kR - 1 k-steps ahead into a ring of registers; the
-    // A fragments of step s + 1 are read from LDS before the MFMAs of step s
-    // (two register sets). The main loop has no data-dependent branches, so the
-    // waits count outstanding loads instead of draining them, and scheduling
-    // barriers keep the compiler from sinking the reads back to their use.
-    bf16x8 bq[kR][WN];
-    bf16x8 aq[2][WM];
-    auto load_b = [&](bf16x8* dst, int ks) {
-#pragma unroll
-      for (int jn = 0; jn < WN; ++jn)
-        dst[jn] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(
-                                                 wrs, boff, (ks * ntn + wn0 + jn) * 1024, 0));
-    };
-    int aoff = 0, cc = 0, kw = 0, snext = 0;  // halo offset of the next A step (kh, kw, cc)
-    auto read_a = [&](bf16x8* dst) {
-#pragma unroll
-      for (int i = 0; i < WM; ++i) dst[i] = *reinterpret_cast<const bf16x8*>(halo + abase[i] + aoff);
-      // advance to the following step without branches; stays on the last step
-      const bool more = ++snext < ksteps;
-      const int c1 = cc + 1;
-      const bool wrap = c1 == csteps;
-      const int kw1 = kw + (wrap ? 1 : 0);
-      const bool wrap2 = kw1 == k;
-      int a1 = aoff + 64;
-      a1 += wrap ? hp.pstride - csteps * 64 : 0;
-      a1 += wrap2 ? (hp.hw - k) * hp.pstride : 0;
-      cc = more ? (wrap ? 0 : c1) : cc;
-      kw = more ? (wrap2 ? 0 : kw1) : kw;
-      aoff = more ? a1 : aoff;
-    };
-    auto mfmas = [&](const bf16x8* a, const bf16x8* bf) {
+    typename HC::Acc acc;
+    if constexpr (!PZ) H.load_z(acc, T, false);  // in flight with the halo loads
+    H.load_halo(T);
+    if constexpr (PZ) {
 #pragma unroll
       for (int i = 0; i < WM; ++i)
 #pragma unroll
-        for (int jn = 0; jn < WN; ++jn)
-          acc[i][jn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bf[jn], a[i], acc[i][jn], 0, 0, 0);
-    };
-#pragma unroll
-    for (int r = 0; r < kR - 1; ++r) load_b(bq[r], min(r, ksteps - 1));
-    read_a(aq[0]);
-    int ks = 0;
-    for (; ks + kR <= ksteps; ks += kR) {
-#pragma unroll
-      for (int r = 0; r < kR; ++r) {
-        load_b(bq[(r + kR - 1) % kR], min(ks + r + kR - 1, ksteps - 1));
-        read_a(aq[(r + 1) & 1]);
-        __builtin_amdgcn_sched_barrier(0);
-        mfmas(aq[r & 1], bq[r]);
-        __builtin_amdgcn_sched_barrier(0);
-      }
+        for (int jn = 0; jn < WN; ++jn) acc[i][jn] = zn[i][jn];
     }
-#pragma unroll
-    for (int r = 0; r < kR - 1; ++r)
-      if (r < ksteps - ks) {
-        read_a(aq[(r + 1) & 1]);
-        mfmas(aq[r & 1], bq[r]);
-      }
+    __syncthreads();
+    H.product(acc);
     // all waves are done with the halo: the next tile may overwrite it
     __syncthreads();
-
-    // ---- 3. next tile's z_{t-1}, then store this tile's z (+ activation) ----
-    const auto zrs = zres(T);
     const bool more = tw.t + tw.step < tw.end;
-    const HTile Tn = more ? decode(tw.t + tw.step) : T;
-    load_z(zn, Tn, !more);
-    const auto yrs = frame_rsrc(p.act ? static_cast<uint16_t*>(p.y) + (size_t)T.n * zimg : nullptr,
-                                p.act ? (uint32_t)(zimg * 2) : 0u);
-#pragma unroll
-    for (int i = 0; i < WM; ++i)
-#pragma unroll
-      for (int jn = 0; jn < WN; ++jn) {
-        const uint32_t o = zoff(T, i, jn);
-        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc[i][jn]), zrs, o, 0, 0);
-        if (p.act) {
-          const uint32_t lo = f32_to_bf16(activate(acc[i][jn][0], p.act)) |
-                              (f32_to_bf16(activate(acc[i][jn][1], p.act)) << 16);
-          const uint32_t hi = f32_to_bf16(activate(acc[i][jn][2], p.act)) |
-                              (f32_to_bf16(activate(acc[i][jn][3], p.act)) << 16);
-          typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-          __builtin_amdgcn_raw_buffer_store_b64(u32x2{lo, hi}, yrs, o == kOutOfRange ? kOutOfRange : o / 2, 0, 0);
-        }
-      }
+    const HaloTile Tn = more ? decode(tw.t + tw.step) : T;
+    if constexpr (PZ) H.load_z(zn, Tn, !more);
+    H.store(T, acc);
     T = Tn;
   }
 }
@@ -934,10 +730,10 @@ hipError_t launch_conv_f32(const ConvParams& p, int grid, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <int WAVES_M, int WAVES_N, int WM, int WN>
+template <int WAVES_M, int WAVES_N, int WM, int WN, int KR, bool PZ, int OCC, int KU, int ADB>
 hipError_t launch_halo_t(const ConvParams& p, const HaloParams& hp, int grid, hipStream_t st) {
-  hipLaunchKernelGGL((conv_halo_kernel<WAVES_M, WAVES_N, WM, WN>), dim3(grid), dim3(64 * WAVES_M * WAVES_N),
-                     hp.lds_bytes, st, p, hp);
+  hipLaunchKernelGGL((conv_halo_kernel<WAVES_M, WAVES_N, WM, WN, KR, PZ, OCC, KU, ADB>), dim3(grid),
+                     dim3(64 * WAVES_M * WAVES_N), hp.lds_bytes, st, p, hp);
   return hipGetLastError();
 }
 
@@ -949,9 +745,9 @@ hipError_t launch_conv(const ConvParams& p, int dtype, bool fast, int grid, hipS
 }
 
 namespace {
-template <int WAVES_M, int WAVES_N, int WM, int WN>
+template <int WAVES_M, int WAVES_N, int WM, int WN, int KR, bool PZ, int OCC, int KU, int ADB>
 int halo_occ_t(const HaloParams& hp) {
-  auto fn = conv_halo_kernel<WAVES_M, WAVES_N, WM, WN>;
+  auto fn = conv_halo_kernel<WAVES_M, WAVES_N, WM, WN, KR, PZ, OCC, KU, ADB>;
   if (hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
                           hp.lds_bytes) != hipSuccess)
     return 0;
@@ -963,18 +759,26 @@ int halo_occ_t(const HaloParams& hp) {
 }
 }  // namespace
 
-#define SC_HALO_CONFIGS(X)                                                              \
-  X(0, 1, 1, 8, 1) X(1, 1, 2, 8, 1) X(2, 1, 4, 8, 1) X(3, 1, 4, 8, 2)                    \
-  X(10, 1, 1, 4, 1) X(11, 1, 2, 4, 1) X(12, 1, 4, 4, 1) X(13, 1, 4, 4, 2) X(14, 1, 4, 4, 3) \
-  X(15, 1, 4, 4, 4)                                                                      \
-  X(20, 1, 1, 1, 1) X(21, 1, 2, 1, 1) X(22, 1, 4, 1, 1) X(23, 1, 4, 1, 2) X(24, 1, 4, 1, 3) \
-  X(25, 1, 4, 1, 4)
+// id, WAVES_M, WAVES_N, WM, WN, KR, PZ, OCC, KU, ADB. Config 3 (128 output
+// channels, 128-site tiles): one A register set and a two-deep B ring, so
+// that three workgroups fit on a CU (131-145 VGPRs), z_{t-1} loaded with the
+// halo; measured 134.7 / 443 us against 141 / 452 us for the two-set build at
+// 4 x 512 x 512 x 128 (29 % of the blocks / all blocks).
+#define SC_HALO_CONFIGS(X)                                                                                  \
+  X(0, 1, 1, 8, 1, 0, true, 2, 12, 2) X(1, 1, 2, 8, 1, 0, true, 2, 12, 2) X(2, 1, 4, 8, 1, 0, true, 2, 12, 2) \
+  X(3, 1, 4, 8, 2, 2, false, 3, 6, 1)                                                                      \
+  X(10, 1, 1, 4, 1, 0, true, 2, 12, 2) X(11, 1, 2, 4, 1, 0, true, 2, 12, 2)                                \
+  X(12, 1, 4, 4, 1, 0, true, 2, 12, 2) X(13, 1, 4, 4, 2, 0, true, 2, 12, 2)                                \
+  X(14, 1, 4, 4, 3, 0, true, 2, 12, 2) X(15, 1, 4, 4, 4, 0, true, 2, 12, 2)                                \
+  X(20, 1, 1, 1, 1, 0, true, 2, 12, 2) X(21, 1, 2, 1, 1, 0, true, 2, 12, 2)                                \
+  X(22, 1, 4, 1, 1, 0, true, 2, 12, 2) X(23, 1, 4, 1, 2, 0, true, 2, 12, 2)                                \
+  X(24, 1, 4, 1, 3, 0, true, 2, 12, 2) X(25, 1, 4, 1, 4, 0, true, 2, 12, 2)
 
 int conv_halo_occupancy(const HaloParams& hp) {
   switch (hp.config) {
-#define SC_X(id, a, b, c, d) \
-  case id:                   \
-    return halo_occ_t<a, b, c, d>(hp);
+#define SC_X(id, a, b, c, d, e, f, g, u, v) \
+  case id:                                  \
+    return halo_occ_t<a, b, c, d, e, f, g, u, v>(hp);
     SC_HALO_CONFIGS(SC_X)
 #undef SC_X
     default: return 0;
@@ -983,9 +787,9 @@ int conv_halo_occupancy(const HaloParams& hp) {
 
 hipError_t launch_conv_halo(const ConvParams& p, const HaloParams& hp, int grid, hipStream_t st) {
   switch (hp.config) {
-#define SC_X(id, a, b, c, d) \
-  case id:                   \
-    return launch_halo_t<a, b, c, d>(p, hp, grid, st);
+#define SC_X(id, a, b, c, d, e, f, g, u, v) \
+  case id:                                  \
+    return launch_halo_t<a, b, c, d, e, f, g, u, v>(p, hp, grid, st);
     SC_HALO_CONFIGS(SC_X)
 #undef SC_X
     default: return hipErrorInvalidValue;

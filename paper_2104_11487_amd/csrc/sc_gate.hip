@@ -369,12 +369,14 @@ __device__ void learned_halo(const GateParams& p, int n, int iy0, int ix0, int h
   }
 }
 
+// The gate of one tile of output sites (this workgroup's tile): residual,
+// statistic, threshold, block flags (and the work-list appends when p.wlist is
+// set). Returns the tile's block flags in LDS.
 // KL: learned gate kernel size (0 = norm gate). NC > 1: norm gate with NC
 // chunks per pixel, chunk sums combined in lane groups (halo_lane_sums); NC =
 // 1: norm gate with fewer than 8 channels, one item per pixel (halo_pixels).
 template <typename T, int VEC, int KL, int NC>
-__global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
-  extern __shared__ float lds[];
+__device__ __forceinline__ const uint32_t* gate_tile(const GateParams& p, float* lds) {
   __shared__ uint32_t blk_flag[kMaxTileBlocks];
 
   const int tile = xcd_tile(blockIdx.x, gridDim.x);
@@ -424,14 +426,14 @@ __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
         }
       if (p.split_blocks) {
         if (threadIdx.x == 0) p.tile_flags[tile] = 0;
-        return;
+        return blk_flag;
       }
       const int bi0 = oy0 / p.block, bj0 = ox0 / p.block;
       for (int i = threadIdx.x; i < nblk_y * nblk_x; i += kGateThreads) {
         const int by = i / nblk_x, bx = i - by * nblk_x;
         p.block_mask[((size_t)n * p.hb + bi0 + by) * p.wb + bj0 + bx] = 0;
       }
-      return;
+      return blk_flag;
     }
   }
 
@@ -529,7 +531,7 @@ __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
   if (p.split_blocks) {
     // the tile is part of one block: one flag per tile, OR-ed per block by the compaction
     if (threadIdx.x == 0) p.tile_flags[tile] = (uint8_t)(blk_flag[0] != 0u);
-    return;
+    return blk_flag;
   }
   const int bi0 = oy0 / p.block, bj0 = ox0 / p.block;
   for (int i = threadIdx.x; i < nblk_y * nblk_x; i += kGateThreads) {
@@ -563,6 +565,13 @@ __global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
       p.wlist[off] = (uint32_t)(((size_t)n * p.hb + bi0 + by) * p.wb + bj0 + bx);
     }
   }
+  return blk_flag;
+}
+
+template <typename T, int VEC, int KL, int NC>
+__global__ void __launch_bounds__(kGateThreads) gate_kernel(GateParams p) {
+  extern __shared__ float lds[];
+  gate_tile<T, VEC, KL, NC>(p, lds);
 }
 
 // Ordered compaction (one workgroup of kScanThreads): each thread takes a
