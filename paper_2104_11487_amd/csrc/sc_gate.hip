@@ -302,6 +302,94 @@ __device__ void halo_pixels(const GateParams& p, int n, int iy0, int ix0, int hh
   }
 }
 
+// Learned gate (Eq. 8 at inference) with NC = 2, 4, 8 or 16 chunks per pixel:
+// the items of halo_lane_sums (one 8-channel chunk of one halo pixel per lane,
+// consecutive lanes holding consecutive chunks of a pixel, kItems items with
+// their loads in flight together), each forming the K2 per-tap chunk terms
+// sum_j phi[tap][c0 + j] * r[c0 + j] in ascending order from +0; the pixel's
+// lane group then adds each tap's chunk terms in ascending chunk order (DPP
+// row shifts), the canonical order, and its first lane writes a[q, tap].
+// Owned pixels are copied to the spare x_{t-1} slot on the way.
+template <typename T, int NC, int KL>
+__device__ void learned_lane_sums(const GateParams& p, int n, int iy0, int ix0, int hh, int hw, int own_y0,
+                                  int own_y1, int own_x0, int own_x1, float* a2, const float* phi) {
+  constexpr int K2 = KL * KL;
+  constexpr int kWords = sizeof(T) == 2 ? 1 : 2;  // 16-byte words per chunk and frame
+  constexpr int kItems = 4 / kWords;
+  constexpr int kLg = NC == 2 ? 1 : (NC == 4 ? 2 : (NC == 8 ? 3 : 4));
+  const uint32_t img_bytes = (uint32_t)((size_t)p.h * p.w * p.c * sizeof(T));
+  const size_t img = (size_t)n * p.h * p.w * p.c;
+  const auto rt = frame_rsrc(static_cast<const T*>(p.x_t) + img, img_bytes);
+  const auto rp = frame_rsrc(static_cast<const T*>(p.no_prev ? p.x_t : p.x_prev) + img, img_bytes);
+  const bool keep_on = p.x_keep != nullptr && p.copy_in_halo;
+  const auto rk = frame_rsrc(keep_on ? static_cast<T*>(p.x_keep) + img : nullptr, keep_on ? img_bytes : 0u);
+  const int total = hh * hw * NC;
+  const float inv_hw = 1.0f / (float)hw;
+  const int wave0 = threadIdx.x & ~63;
+  // a thread's chunk is the same for every item (NC divides the item stride)
+  const int ch = threadIdx.x & (NC - 1);
+  const float* ph = phi + ch * kChunk;
+  for (int base = 0; base < total; base += kGateThreads * kItems) {
+    u32x4 vt[kItems][kWords], vp[kItems][kWords];
+    uint32_t koff[kItems];
+#pragma unroll
+    for (int u = 0; u < kItems; ++u) {
+      const int idx = base + u * kGateThreads + threadIdx.x;
+      const int q = idx >> kLg;
+      const int hy = qdiv(q, inv_hw), hx = q - hy * hw;
+      const int y = iy0 + hy, x = ix0 + hx;
+      const bool in = idx < total && y >= 0 && y < p.h && x >= 0 && x < p.w;
+      const bool own = in && keep_on && y >= own_y0 && y < own_y1 && x >= own_x0 && x < own_x1;
+      const uint32_t off = (uint32_t)(((y * p.w + x) * p.c + ch * kChunk) * (int)sizeof(T));
+      // x_{t-1} under the step's translation (zero outside the frame)
+      const int yp = y - p.sy, xq = x - p.sx;
+      const bool pin = in && !p.no_prev && yp >= 0 && yp < p.h && xq >= 0 && xq < p.w;
+      const uint32_t po = (uint32_t)(((yp * p.w + xq) * p.c + ch * kChunk) * (int)sizeof(T));
+      koff[u] = own ? off : kOutOfRange;
+#pragma unroll
+      for (int wd = 0; wd < kWords; ++wd) {
+        vt[u][wd] = __builtin_amdgcn_raw_buffer_load_b128(rt, (in ? off : kOutOfRange) + 16 * wd, 0, 0);
+        vp[u][wd] = __builtin_amdgcn_raw_buffer_load_b128(rp, (pin ? po : kOutOfRange) + 16 * wd, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kItems; ++u) {
+      if (base + u * kGateThreads + wave0 >= total) break;  // wave-uniform
+      float r[kChunk];
+      if constexpr (kWords == 1) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {  // channels 2e (low half) and 2e + 1 (high half)
+          const uint32_t a = vt[u][0][e], b = vp[u][0][e];
+          r[2 * e] = __fsub_rn(__uint_as_float(a << 16), __uint_as_float(b << 16));
+          r[2 * e + 1] = __fsub_rn(__uint_as_float(a & 0xffff0000u), __uint_as_float(b & 0xffff0000u));
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < kChunk; ++j)
+          r[j] = __fsub_rn(__uint_as_float(vt[u][j >> 2][j & 3]), __uint_as_float(vp[u][j >> 2][j & 3]));
+      }
+      const int idx = base + u * kGateThreads + threadIdx.x;
+      const int q = idx >> kLg;
+#pragma unroll
+      for (int t = 0; t < K2; ++t) {
+        const float4 f0 = *reinterpret_cast<const float4*>(ph + t * p.c);
+        const float4 f1 = *reinterpret_cast<const float4*>(ph + t * p.c + 4);
+        const float f[kChunk] = {f0.x, f0.y, f0.z, f0.w, f1.x, f1.y, f1.z, f1.w};
+        float part = 0.0f;
+#pragma unroll
+        for (int j = 0; j < kChunk; ++j) part = add_rn(part, mul_rn(f[j], r[j]));
+        const float acc = group_sum<NC>(part);
+        if (idx < total && ch == 0) a2[q * K2 + t] = acc;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kItems; ++u)
+#pragma unroll
+      for (int wd = 0; wd < kWords; ++wd)
+        __builtin_amdgcn_raw_buffer_store_b128(vt[u][wd], rk, koff[u] + 16 * wd, 0, kNonTemporal);
+  }
+}
+
 // Learned gate (Eq. 8 at inference): one thread per halo pixel forms, for
 // every tap (kh, kw), a[q, tap] = sum_c phi[tap][c] * r[q, c] in the canonical
 // chunked order (8 channels ascending within a chunk from +0, chunk sums
@@ -437,9 +525,9 @@ __device__ __forceinline__ const uint32_t* gate_tile(const GateParams& p, float*
     }
   }
 
-  if constexpr (NC == 1) {
+  if constexpr (NC == 1 && KL == 0) {
     halo_pixels<T>(p, n, iy0, ix0, hh, hw, own_y0, own_y1, own_x0, own_x1, a_halo);
-  } else if constexpr (NC > 0) {
+  } else if constexpr (NC > 0 && KL == 0) {
     halo_lane_sums<T, NC>(p, n, iy0, ix0, hh, hw, own_y0, own_y1, own_x0, own_x1, a_halo);
   } else if constexpr (KL == 0) {
     halo_partials<T, VEC>(p, n, iy0, ix0, hh, hw, own_y0, own_y1, own_x0, own_x1, part);
@@ -463,7 +551,10 @@ __device__ __forceinline__ const uint32_t* gate_tile(const GateParams& p, float*
       __syncthreads();
       phi = staged;
     }
-    learned_halo<T, VEC, KL>(p, n, iy0, ix0, hh, hw, own_y0, own_y1, own_x0, own_x1, lds, phi);
+    if constexpr (NC > 1)
+      learned_lane_sums<T, NC, KL>(p, n, iy0, ix0, hh, hw, own_y0, own_y1, own_x0, own_x1, lds, phi);
+    else
+      learned_halo<T, VEC, KL>(p, n, iy0, ix0, hh, hw, own_y0, own_y1, own_x0, own_x1, lds, phi);
   }
 
   if (!p.copy_in_halo && p.x_keep) {
@@ -653,6 +744,28 @@ __global__ void __launch_bounds__(kScanThreads) compact_kernel(uint8_t* block_ma
 template <typename T, int VEC>
 static hipError_t launch_gate_t(const GateParams& p, int grid, size_t lds_bytes, hipStream_t st) {
   const int nchk = (p.c + kChunk - 1) / kChunk;
+  if (p.lane_sum && p.learned) {
+    // learned gate over lane groups (c = 16, 32, 64 or 128, c % 8 == 0)
+    if constexpr (VEC == kChunk) {
+      if ((long)p.h * p.w * p.c * 4 >= (1L << 31)) return hipErrorInvalidValue;
+#define SC_LG(nc)                                                                                                \
+  switch (p.learned) {                                                                                           \
+    case 1: hipLaunchKernelGGL((gate_kernel<T, VEC, 1, nc>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p); break; \
+    case 3: hipLaunchKernelGGL((gate_kernel<T, VEC, 3, nc>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p); break; \
+    case 5: hipLaunchKernelGGL((gate_kernel<T, VEC, 5, nc>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p); break; \
+    case 7: hipLaunchKernelGGL((gate_kernel<T, VEC, 7, nc>), dim3(grid), dim3(kGateThreads), lds_bytes, st, p); break; \
+    default: return hipErrorInvalidValue;                                                                        \
+  }
+      if (nchk == 16) { SC_LG(16) }
+      else if (nchk == 8) { SC_LG(8) }
+      else if (nchk == 4) { SC_LG(4) }
+      else if (nchk == 2) { SC_LG(2) }
+      else return hipErrorInvalidValue;
+#undef SC_LG
+      return hipGetLastError();
+    }
+    return hipErrorInvalidValue;
+  }
   if (p.lane_sum) {
     // the host sized the LDS without chunk-sum staging: only these shapes
     if (p.learned != 0 || (long)p.h * p.w * p.c * 4 >= (1L << 31)) return hipErrorInvalidValue;

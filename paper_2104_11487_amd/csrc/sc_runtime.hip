@@ -159,7 +159,11 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
   // steps included)
   const bool lane_sum = !G.learned && (long)d->h * d->w * d->c_in * 4 < (1L << 31) &&
                         ((d->c_in % 8 == 0 && (nchk == 2 || nchk == 4 || nchk == 8 || nchk == 16)) || d->c_in < 8);
-  G.lane_sum = lane_sum ? 1 : 0;
+  // the learned gate takes the same lane groups (per-tap chunk terms) when
+  // the channels come in 2, 4, 8 or 16 whole chunks
+  const bool learned_lanes = G.learned && (long)d->h * d->w * d->c_in * 4 < (1L << 31) && d->c_in % 8 == 0 &&
+                             (nchk == 2 || nchk == 4 || nchk == 8 || nchk == 16);
+  G.lane_sum = (lane_sum || learned_lanes) ? 1 : 0;
   // learned gate: phi is staged in LDS unless that alone would not fit
   const long phi_floats = (long)k * k * d->c_in;
   G.phi_in_lds = G.learned && phi_floats * 4 <= (long)kLdsLimit / 2;
