@@ -646,6 +646,98 @@ def bench_stack(args):
     print(json.dumps(out), flush=True)
 
 
+# ------------------------------------------- two large layers, chained --
+
+def bench_blob_pair(args):
+    """Two stacked 3x3 128 -> 128 bf16 layers with ReLU between on the 4 x 512 x 512
+    blob clip, 16 x 16 blocks, each layer's threshold for ~--density block density on
+    its own input. 'full': layer 2 steps on layer 1's activation (x_t and x_{t-1} over
+    the whole frame); 'chained': layer 2 steps on the residual layer 1 emits at the
+    blocks it updated (Sec. 3.1: residuals at intermediate feature maps), its gate
+    skipping tiles with no upstream block."""
+    import torch
+    from paper_2104_11487_amd import skipconv as S
+    from paper_2104_11487_amd import synthetic as syn
+    from paper_2104_11487_amd.skipconv import SkipConv
+
+    wl, clip = load_workload("blob128", args.frames)
+    frames_dev = upload(clip, wl.dtype)
+    nfr = len(frames_dev)
+    w1 = weight_tensor(wl.weights()[0], wl.dtype)
+    w2 = weight_tensor(syn.he_weights(128, 128, 3, seed=519), wl.dtype)
+    kw = dict(n=wl.n, h=wl.h, w=wl.w, stride=1, groups=1)
+    b = wl.block
+    e1 = eps_for_density(gpu_stats(kw, w1, frames_dev), b, wl.h, wl.w, args.density)
+    # layer 2's statistics on layer 1's activations at e1
+    l1 = SkipConv(w1, eps=e1, block=b, act_out="relu", **kw)
+    probe = SkipConv(w2, eps=0.0, block=1, keep_stats=True, **kw)
+    stats2 = []
+    for t, x in enumerate(frames_dev):
+        l1.step(x)
+        probe.step(l1.activation())
+        if t > 0:
+            torch.cuda.synchronize()
+            stats2.append(probe.stat())
+    l1.close()
+    probe.close()
+    e2 = eps_for_density(stats2, b, wl.h, wl.w, args.density)
+    log(f"[bench] blob pair: eps {e1:.4g} / {e2:.4g}")
+
+    def run(chained, steps, count=False):
+        a = SkipConv(w1, eps=e1, block=b, act_out="relu", emit_residual=chained, **kw)
+        c = SkipConv(w2, eps=e2, block=b, **kw)
+        dens = [0, 0]
+
+        def one(j, counted):
+            t = j % nfr
+            if t == 0:
+                a.reset()
+                c.reset()
+            a.step(frames_dev[t])
+            if chained:
+                c.step_chained(a)
+            else:
+                c.step(a.activation())
+            if counted:
+                dens[0] += a.active_count()[1]
+                dens[1] += c.active_count()[1]
+
+        for j in range(nfr + 1):  # warm-up: one clip and the next reference frame
+            one(j, False)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for j in range(1, steps + 1):  # steady-state frames after the reference
+            one(j, count)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        a.close()
+        c.close()
+        return wall, dens
+
+    res = {}
+    for chained in (False, True):
+        wall, _ = run(chained, args.steps)
+        res["chained" if chained else "full"] = wall
+        log(f"[bench] blob pair {'chained' if chained else 'full'}: {args.steps * wl.n / wall:.0f} frames/s, "
+            f"{1e6 * wall / args.steps:.1f} us/step")
+    _, dens = run(False, nfr - 1, count=True)
+    sites = wl.n * wl.h * wl.w * (nfr - 1)
+    out = {
+        "metric": METRIC, "value": args.steps * wl.n / res["chained"], "unit": "frames/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": nfr + 1, "ms_per_step": 1e3 * res["chained"] / args.steps,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic",
+        "config": {"workload": "blob pair: two 3x3 conv 128->128 layers with ReLU between on 4 x 512 x 512 "
+                               f"frames, {nfr}-frame blob clip (reset at frame 1), 16x16 blocks, layer 2 chained on "
+                               "layer 1's emitted residual; steady-state steps",
+                   "eps": [e1, e2], "density": [dens[0] / sites, dens[1] / sites],
+                   "full_frames_per_s": args.steps * wl.n / res["full"],
+                   "chained_frames_per_s": args.steps * wl.n / res["chained"],
+                   "speedup_chained": res["full"] / res["chained"]},
+        "roofline": None, "cpu_baseline": None, "sweep": [],
+    }
+    print(json.dumps(out), flush=True)
+
+
 # ------------------------------------------------------- pointwise + dw --
 
 def bench_mbconv(args):
@@ -814,7 +906,7 @@ def main():
     ap.add_argument("--steps", type=int, default=40)
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--workload", default="blob128",
-                    choices=["rect64", "blob128", "square16", "stack6", "mbconv192"])
+                    choices=["rect64", "blob128", "square16", "stack6", "mbconv192", "blobpair"])
     ap.add_argument("--block", type=int, default=None)
     ap.add_argument("--density", type=float, default=0.25)
     ap.add_argument("--frames", type=int, default=None)
@@ -863,6 +955,9 @@ def main():
         return
     if args.workload == "mbconv192":
         bench_mbconv(args)
+        return
+    if args.workload == "blobpair":
+        bench_blob_pair(args)
         return
     wl, clip = load_workload(args.workload, args.frames)
     frames_dev = upload(clip, wl.dtype)

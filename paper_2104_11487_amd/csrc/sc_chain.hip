@@ -36,8 +36,9 @@ emit_kernel(const uint8_t* block_mask, uint8_t* prev_mask, int nb, int bpw, cons
   }
   if (!__syncthreads_or(any)) return;
   const int bsz = block * block;
-  // elements in groups of VEC consecutive channels (4 when c_out % 4 == 0)
-  const int vec = (c_out & 3) == 0 ? 4 : 1;
+  // elements in groups of VEC consecutive channels: 8 (16-byte y / rb and
+  // 32-byte z / r32 accesses) when c_out % 8 == 0, else 1
+  const int vec = (c_out & 7) == 0 ? 8 : 1;
   const int cg = c_out / vec;
   const int total = nblk * bsz * cg;
   for (int e = threadIdx.x; e < total; e += kEmitThreads) {
@@ -51,28 +52,64 @@ emit_kernel(const uint8_t* block_mask, uint8_t* prev_mask, int nb, int bpw, cons
     const int oy = bi * block + site / block, ox = bj * block + site % block;
     if (oy >= h_out || ox >= w_out) continue;  // ceil-mode edge block
     const size_t o = ((size_t)(img * h_out + oy) * w_out + ox) * c_out + ch;
-    for (int v = 0; v < vec; ++v) {
+    if (vec == 8) {
       if (!(st & 1)) {
-        r32[o + v] = 0.0f;
-        if (dtype == 1) rb[o + v] = 0;
+        *reinterpret_cast<float4*>(r32 + o) = float4{0.f, 0.f, 0.f, 0.f};
+        *reinterpret_cast<float4*>(r32 + o + 4) = float4{0.f, 0.f, 0.f, 0.f};
+        if (dtype == 1) *reinterpret_cast<uint4*>(rb + o) = uint4{0u, 0u, 0u, 0u};
         continue;
       }
-      float a = z[o + v];
-      if (act == 2) a = relu_f32(a);
-      float r;
+      const float4 z0 = *reinterpret_cast<const float4*>(z + o), z1 = *reinterpret_cast<const float4*>(z + o + 4);
+      float a[8] = {z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w};
+      if (act == 2)
+        for (int v = 0; v < 8; ++v) a[v] = relu_f32(a[v]);
+      float r[8];
       if (dtype == 1) {
         uint16_t* yb = static_cast<uint16_t*>(y);
-        const uint16_t yn = (uint16_t)f32_to_bf16(a);
-        r = __fsub_rn(bf16_to_f32(yn), bf16_to_f32(yb[o + v]));
-        yb[o + v] = yn;
-        rb[o + v] = (uint16_t)f32_to_bf16(r);
+        const uint4 yo = *reinterpret_cast<const uint4*>(yb + o);
+        const uint32_t wo[4] = {yo.x, yo.y, yo.z, yo.w};
+        uint32_t wn[4], wr[4];
+        for (int v = 0; v < 4; ++v) {
+          const uint32_t n0 = f32_to_bf16(a[2 * v]), n1 = f32_to_bf16(a[2 * v + 1]);
+          r[2 * v] = __fsub_rn(bf16_to_f32(n0), bf16_to_f32(wo[v] & 0xffffu));
+          r[2 * v + 1] = __fsub_rn(bf16_to_f32(n1), bf16_to_f32(wo[v] >> 16));
+          wn[v] = n0 | (n1 << 16);
+          wr[v] = f32_to_bf16(r[2 * v]) | (f32_to_bf16(r[2 * v + 1]) << 16);
+        }
+        *reinterpret_cast<uint4*>(yb + o) = uint4{wn[0], wn[1], wn[2], wn[3]};
+        *reinterpret_cast<uint4*>(rb + o) = uint4{wr[0], wr[1], wr[2], wr[3]};
       } else {
         float* yf = static_cast<float*>(y);
-        r = __fsub_rn(a, yf[o + v]);
-        yf[o + v] = a;
+        const float4 y0 = *reinterpret_cast<const float4*>(yf + o), y1 = *reinterpret_cast<const float4*>(yf + o + 4);
+        const float yo[8] = {y0.x, y0.y, y0.z, y0.w, y1.x, y1.y, y1.z, y1.w};
+        for (int v = 0; v < 8; ++v) r[v] = __fsub_rn(a[v], yo[v]);
+        *reinterpret_cast<float4*>(yf + o) = float4{a[0], a[1], a[2], a[3]};
+        *reinterpret_cast<float4*>(yf + o + 4) = float4{a[4], a[5], a[6], a[7]};
       }
-      r32[o + v] = r;
+      *reinterpret_cast<float4*>(r32 + o) = float4{r[0], r[1], r[2], r[3]};
+      *reinterpret_cast<float4*>(r32 + o + 4) = float4{r[4], r[5], r[6], r[7]};
+      continue;
     }
+    if (!(st & 1)) {
+      r32[o] = 0.0f;
+      if (dtype == 1) rb[o] = 0;
+      continue;
+    }
+    float a = z[o];
+    if (act == 2) a = relu_f32(a);
+    float r;
+    if (dtype == 1) {
+      uint16_t* yb = static_cast<uint16_t*>(y);
+      const uint16_t yn = (uint16_t)f32_to_bf16(a);
+      r = __fsub_rn(bf16_to_f32(yn), bf16_to_f32(yb[o]));
+      yb[o] = yn;
+      rb[o] = (uint16_t)f32_to_bf16(r);
+    } else {
+      float* yf = static_cast<float*>(y);
+      r = __fsub_rn(a, yf[o]);
+      yf[o] = a;
+    }
+    r32[o] = r;
   }
   __syncthreads();
   for (int i = threadIdx.x; i < nblk; i += kEmitThreads) prev_mask[b0 + i] = state[i] & 1;

@@ -472,10 +472,11 @@ __device__ void gate_tile(const FusedParams& p, const Tile& T, const ChunkMap& c
 
 // Epilogue of one output piece (4 consecutive channels of one site): z =
 // z_{t-1} + U (assigned on a reference frame), activation output; emitting
-// layers also write r = y_new - y_old for their successor.
+// layers also write r = y_new - y_old for their successor, y_old =
+// dtype(act(z_{t-1})) (the activation output always equals dtype(act(z)), so
+// the old z already loaded for the update gives it).
 template <bool EMIT>
-__device__ __forceinline__ void store_piece(const FusedParams& p, size_t o, const floatx4& u, const floatx4& zold,
-                                            const uint2& yold) {
+__device__ __forceinline__ void store_piece(const FusedParams& p, size_t o, const floatx4& u, const floatx4& zold) {
   floatx4 nv;
 #pragma unroll
   for (int v = 0; v < 4; ++v) nv[v] = p.g.reference ? u[v] : zold[v] + u[v];
@@ -486,7 +487,9 @@ __device__ __forceinline__ void store_piece(const FusedParams& p, size_t o, cons
     for (int v = 0; v < 4; ++v) yb[v] = f32_to_bf16(p.act == 2 ? relu_f32(nv[v]) : nv[v]);
     *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.y) + o) = uint2{yb[0] | (yb[1] << 16), yb[2] | (yb[3] << 16)};
     if (EMIT) {
-      const uint32_t yo[4] = {yold.x & 0xffffu, yold.x >> 16, yold.y & 0xffffu, yold.y >> 16};
+      uint32_t yo[4];
+#pragma unroll
+      for (int v = 0; v < 4; ++v) yo[v] = f32_to_bf16(p.act == 2 ? relu_f32(zold[v]) : zold[v]);
       floatx4 r;
 #pragma unroll
       for (int v = 0; v < 4; ++v) r[v] = __fsub_rn(bf16_to_f32(yb[v]), bf16_to_f32(yo[v]));
@@ -565,7 +568,6 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
   halo_load<CHAIN, kThreads, true, KI>(g, T, cm, hwk, 0, threadIdx.x, hb);
   int esite[EP], eloc[EP], ecol[EP];
   floatx4 zold[EP];
-  uint2 yold[EP];
 #pragma unroll
   for (int h = 0; h < EP; ++h) {
     const int e = h * kThreads + threadIdx.x;
@@ -578,8 +580,6 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
     ecol[h] = col;
     const size_t o = ok ? (size_t)gs * p.c_out + n0 * 16 + col : 0;
     zold[h] = *reinterpret_cast<const floatx4*>(p.z + o);
-    yold[h] = uint2{0u, 0u};
-    if (EMIT) yold[h] = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(p.y) + o);
   }
 
   for (int i = threadIdx.x; i < kMaxTileBlocks; i += kThreads) blk_flag[i] = 0u;
@@ -622,10 +622,7 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
 #pragma unroll
     for (int j = 0; j < WN; ++j) settle(bw[st][j]);
 #pragma unroll
-  for (int h = 0; h < EP; ++h) {
-    settle(zold[h]);
-    if (EMIT) settle(yold[h]);
-  }
+  for (int h = 0; h < EP; ++h) settle(zold[h]);
   if (lead) {
     halo_keep(g, hb);  // the halo is one round (KI rows per thread) for this kernel
     copy_owned(g, T);
@@ -699,7 +696,7 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
 #pragma unroll
       for (int c = 0; c < 4; ++c) u[c] = u[c] + v[c];
     }
-    store_piece<EMIT>(p, (size_t)esite[h] * p.c_out + n0 * 16 + ecol[h], u, zold[h], yold[h]);
+    store_piece<EMIT>(p, (size_t)esite[h] * p.c_out + n0 * 16 + ecol[h], u, zold[h]);
   }
   if (EMIT && lead) emit_clear(p, T.n, T.oy0, T.ox0, T.oh, T.ow, T.tb_w, blk_flag, emit_clr);
 }
@@ -756,7 +753,6 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
   int abase[WM], tapmul[WM], zsite[WM];
   uint32_t blk_of[WM];
   floatx4 zold[WM][WN];
-  uint2 yold[WM][WN];  // emitting layers: the activation output before this step
   if (kStatic) {
 #pragma unroll
     for (int i = 0; i < WM; ++i) {
@@ -837,12 +833,9 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
     for (int j = 0; j < WN; ++j) {
       const int col = (wn * WN + j) * 16 + kq * 4;
       zold[i][j] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
-      yold[i][j] = uint2{0u, 0u};
-      if (zsite[i] >= 0 && !g.reference && col < p.c_out)
+      // (emitting layers also on a reference frame: z_{t-1} gives y_{t-1})
+      if (zsite[i] >= 0 && (!g.reference || EMIT) && col < p.c_out)
         zold[i][j] = *reinterpret_cast<const floatx4*>(p.z + (size_t)zsite[i] * p.c_out + col);
-      if (EMIT && zsite[i] >= 0 && col < p.c_out)
-        yold[i][j] = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(p.y) +
-                                                     (size_t)zsite[i] * p.c_out + col);
     }
   const bool busy = wn < 2 && (kStatic ? wm * WM * 16 < g.ts * g.ts : wm * WM * 16 < nrows);
 
@@ -930,7 +923,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedParams p) {
       for (int j = 0; j < WN; ++j) {
         const int col = (wn * WN + j) * 16 + kq * 4;
         if (col >= p.c_out) continue;
-        store_piece<EMIT>(p, (size_t)zsite[i] * p.c_out + col, acc[i][j], zold[i][j], yold[i][j]);
+        store_piece<EMIT>(p, (size_t)zsite[i] * p.c_out + col, acc[i][j], zold[i][j]);
       }
     }
   }
@@ -993,7 +986,6 @@ __global__ void __launch_bounds__(kThreads) fused_dw_kernel(FusedParams p) {
   halo_load<CHAIN, kThreads, true, KI>(g, T, cm, hwk, 0, threadIdx.x, hb);
   int esite[EP], eloc[EP], ecol[EP], epix[EP];
   floatx4 zold[EP];
-  uint2 yold[EP];
 #pragma unroll
   for (int h = 0; h < EP; ++h) {
     const int e = h * kThreads + threadIdx.x;
@@ -1007,8 +999,6 @@ __global__ void __launch_bounds__(kThreads) fused_dw_kernel(FusedParams p) {
     epix[h] = ok ? (ly * g.stride) * T.hw + lx * g.stride : 0;
     const size_t o = ok ? (size_t)gs * p.c_out + ecol[h] : 0;
     zold[h] = *reinterpret_cast<const floatx4*>(p.z + o);
-    yold[h] = uint2{0u, 0u};
-    if (EMIT) yold[h] = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(p.y) + o);
   }
   for (int i = threadIdx.x; i < kMaxTileBlocks; i += kThreads) blk_flag[i] = 0u;
   if (threadIdx.x == 0) tile_on = 0u;
@@ -1021,10 +1011,7 @@ __global__ void __launch_bounds__(kThreads) fused_dw_kernel(FusedParams p) {
     if (w4 < kk * q4) reinterpret_cast<float4*>(wl)[w4] = wreg[j];
   }
 #pragma unroll
-  for (int h = 0; h < EP; ++h) {
-    settle(zold[h]);
-    if (EMIT) settle(yold[h]);
-  }
+  for (int h = 0; h < EP; ++h) settle(zold[h]);
   if (lead) {
     halo_keep(g, hb);
     copy_owned(g, T);
@@ -1062,7 +1049,7 @@ __global__ void __launch_bounds__(kThreads) fused_dw_kernel(FusedParams p) {
 #pragma unroll
   for (int h = 0; h < EP; ++h) {
     if (esite[h] < 0 || blk_flag[eloc[h]] == 0u) continue;
-    store_piece<EMIT>(p, (size_t)esite[h] * p.c_out + ecol[h], u[h], zold[h], yold[h]);
+    store_piece<EMIT>(p, (size_t)esite[h] * p.c_out + ecol[h], u[h], zold[h]);
   }
   if (EMIT && lead) emit_clear(p, T.n, T.oy0, T.ox0, T.oh, T.ow, T.tb_w, blk_flag, emit_clr);
 }
@@ -1148,17 +1135,13 @@ __global__ void __launch_bounds__(kThreads) fused_sc_kernel(FusedParams p) {
   const int qy = q >> 3, qx = q & 7;  // tiles are at most 8 x 8 sites, laid out 8 wide here
   const bool qok = qy < TL.oh && qx < TL.ow && qy < g.ts && qx < g.ts;
   const int gsite = (TL.n * g.h_out + TL.oy0 + qy) * g.w_out + TL.ox0 + qx;
-  using YOld = typename std::conditional<BF, uint2, floatx4>::type;  // 4 channels of y
   floatx4 zold[NTN];
-  YOld yold[NTN];
 #pragma unroll
   for (int i = 0; i < NTN; ++i) {
     const int col = 16 * i + 4 * kq;
     const bool ok = kp == 0 && qok && col < p.c_out;
     const size_t o = ok ? (size_t)gsite * p.c_out + col : 0;
     zold[i] = *reinterpret_cast<const floatx4*>(p.z + o);
-    yold[i] = YOld{};
-    if (EMIT) yold[i] = *reinterpret_cast<const YOld*>(static_cast<const T*>(p.y) + o);
   }
   for (int i = threadIdx.x; i < kMaxTileBlocks; i += kThreads) blk_flag[i] = 0u;
   if (threadIdx.x == 0) tile_on = 0u;
@@ -1295,7 +1278,7 @@ __global__ void __launch_bounds__(kThreads) fused_sc_kernel(FusedParams p) {
       for (int j = 0; j < 4; ++j) u[j] = acc[i][j] + v[j];
       const size_t o = (size_t)gsite * p.c_out + col;
       if constexpr (BF) {
-        store_piece<EMIT>(p, o, u, zold[i], yold[i]);
+        store_piece<EMIT>(p, o, u, zold[i]);
       } else {
         floatx4 nv;
 #pragma unroll
@@ -1309,7 +1292,8 @@ __global__ void __launch_bounds__(kThreads) fused_sc_kernel(FusedParams p) {
           if (EMIT) {
             floatx4 r;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) r[j] = __fsub_rn(a[j], yold[i][j]);
+            for (int j = 0; j < 4; ++j)
+              r[j] = __fsub_rn(a[j], p.act == 2 ? relu_f32(zold[i][j]) : zold[i][j]);
             *reinterpret_cast<floatx4*>(p.r32 + o) = r;
           }
         }

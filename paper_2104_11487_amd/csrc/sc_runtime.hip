@@ -980,6 +980,9 @@ int skipconv_create(const skipconv_desc* d, const void* weights, void* workspace
   if (e == hipSuccess && d->act_out != SKIPCONV_ACT_NONE)
     e = hipMemsetAsync(h->y(), 0, (size_t)d->n * g.h_out * g.w_out * d->c_out * g.elem, st);
   if (e == hipSuccess && h->emits()) e = hipMemsetAsync(h->r32(), 0, g.total - g.off_r32, st);
+  // z starts at 0, so the activation output (0) is dtype(act(z)) from the start:
+  // emitting kernels take the previous activation from the old z
+  if (e == hipSuccess && h->emits()) e = hipMemsetAsync(h->z(), 0, g.z_bytes, st);
   if (e == hipSuccess) {
     if (g.depthwise)
       e = sc::launch_pack_depthwise(weights, static_cast<float*>(h->wpack()), d->dtype, d->c_in,
