@@ -1065,7 +1065,7 @@ def main():
                           label=f"output-norm gate b={block} d={args.density}")
         r.update({"block": block, "target_density": args.density, "gate": "output-norm", "eps": e_out})
         sweep.append(r)
-        # learned gate (Eq. 8 at inference; split pipeline): seeded random phi,
+        # learned gate (Eq. 8 at inference; the layer's own pipeline): seeded random phi,
         # bias from the GPU's own scores for the same block density (a 16-frame
         # clip on the large workload)
         short = frames_dev[:16] if big else frames_dev

@@ -257,9 +257,9 @@ __device__ __forceinline__ HaloWalk make_walk(const GateParams& g, const Tile& T
 template <int KI = kItems>
 struct HaloBatch {
   uint4 vt[KI], vp[KI];
-  size_t off[KI];
+  size_t off[KI], offp[KI];  // offp: translated steps, the x_{t-1} element offset
   int px[KI], ch[KI];
-  bool in[KI], own[KI];
+  bool in[KI], own[KI], pin[KI];  // pin: translated steps, x_{t-1} source in the frame
 };
 
 // Rounds of KI items a workgroup's halo takes.
@@ -272,9 +272,12 @@ __device__ __forceinline__ int halo_rounds(const Tile& T, const ChunkMap& cm, co
 // Issue the loads of round `rd`. Addresses are clamped in bounds so that every
 // load is issued (the wait counts stay static); out-of-frame items are zeroed
 // when used.
-template <bool CHAIN, int NTHR, bool TWOD, int KI = kItems>
+// TRANS (translated steps, 2-D walk): x_{t-1} is read at the pixel shifted
+// back by (g.sy, g.sx), zero where that lies outside the frame.
+template <bool CHAIN, int NTHR, bool TWOD, int KI = kItems, bool TRANS = false>
 __device__ __forceinline__ void halo_load(const GateParams& g, const Tile& T, const ChunkMap& cm,
                                           const HaloWalk& W, int rd, int tid, HaloBatch<KI>& B) {
+  static_assert(!TRANS || (TWOD && !CHAIN), "translated steps take the 2-D walk on full frames");
   const uint16_t* xt = static_cast<const uint16_t*>(g.x_t);
   const uint16_t* xp = static_cast<const uint16_t*>(g.no_prev ? g.x_t : g.x_prev);
   const bool keep = g.x_keep != nullptr && g.copy_in_halo;
@@ -290,6 +293,11 @@ __device__ __forceinline__ void halo_load(const GateParams& g, const Tile& T, co
       B.in[u] = valid && W.xin && y >= 0 && y < g.h;
       B.own[u] = B.in[u] && W.xown && y >= T.own_y0 && y < T.own_y1;
       B.off[u] = B.in[u] ? (size_t)(W.off0 + j * W.ostep) : 0;
+      if constexpr (TRANS) {
+        const int yq = y - g.sy, xq = T.ix0 + W.hx - g.sx;
+        B.pin[u] = B.in[u] && yq >= 0 && yq < g.h && xq >= 0 && xq < g.w;
+        B.offp[u] = B.pin[u] ? (size_t)((long)B.off[u] - ((long)g.sy * g.w + g.sx) * g.c) : 0;
+      }
     } else {
       const int idx = rd * KI * NTHR + u * NTHR + tid;
       const int q = cm.lg >= 0 ? idx >> cm.lg : qdiv(idx, cm.inv);
@@ -307,8 +315,37 @@ __device__ __forceinline__ void halo_load(const GateParams& g, const Tile& T, co
       B.vp[u] = *reinterpret_cast<const uint4*>(rr + 4);
     } else {
       B.vt[u] = *reinterpret_cast<const uint4*>(xt + B.off[u]);
-      B.vp[u] = *reinterpret_cast<const uint4*>(xp + B.off[u]);
+      B.vp[u] = *reinterpret_cast<const uint4*>(xp + (TRANS ? B.offp[u] : B.off[u]));
     }
+  }
+}
+
+// Learned gate terms of one halo item (a pixel's 8-channel chunk, r in fp32):
+// for every tap t, the chunk's term sum_j phi[t][8 ch + j] * r[j] (ascending
+// from +0, one rounding per multiply and per add), then the pixel's chunk terms
+// in ascending chunk order from +0 (lane group of NC), stored by the group's
+// first lane (dst: its pixel's k^2 terms, null elsewhere). ph = phi + 8 ch,
+// phi [tap][c] in LDS. 3 x 3 kernels take an unrolled loop: the nine chains
+// are independent, so their LDS reads and group sums overlap. (Reading a
+// tap's phi once for all of a thread's items, or skipping per wave the tap
+// rows that no pixel of the wave serves, measured slower.)
+template <int NC>
+__device__ __forceinline__ void learned_taps(const float* ph, int c, int k, const float (&r)[8], float* dst) {
+  auto tap = [&](int t) {
+    const float4 f0 = *reinterpret_cast<const float4*>(ph + t * c);
+    const float4 f1 = *reinterpret_cast<const float4*>(ph + t * c + 4);
+    const float f[8] = {f0.x, f0.y, f0.z, f0.w, f1.x, f1.y, f1.z, f1.w};
+    float pt = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) pt = add_rn(pt, mul_rn(f[j], r[j]));
+    const float acc = group_sum<NC>(pt);
+    if (dst) dst[t] = acc;
+  };
+  if (k == 3) {
+#pragma unroll
+    for (int t = 0; t < 9; ++t) tap(t);
+  } else {
+    for (int t = 0; t < k * k; ++t) tap(t);
   }
 }
 
@@ -317,10 +354,15 @@ __device__ __forceinline__ void halo_load(const GateParams& g, const Tile& T, co
 // the pixel's chunk sums are added in ascending order by the group's first
 // lane through DPP row shifts (lane_sum), or parked in LDS for a later
 // combine. `wave` is the wave's index among the NTHR threads taking items.
-template <bool CHAIN, int NTHR, bool TWOD, int KI = kItems>
+// LEARNED (Eq. 8, lane_sum shapes): instead of the norm statistic, every tap
+// t of the pixel gets a[q][t] = sum_c phi[t][c] * r[q][c] in the canonical
+// chunked order (8 channels ascending from +0, chunk sums ascending from +0),
+// into a_halo[q * k^2 + t]; `part` then holds phi [tap][c] (fp32, staged).
+template <bool CHAIN, int NTHR, bool TWOD, int KI = kItems, bool LEARNED = false, bool TRANS = false>
 __device__ __forceinline__ void halo_use(const FusedParams& p, const Tile& T, const ChunkMap& cm,
                                          const HaloWalk& W, int rd, int wave, HaloBatch<KI>& B, uint8_t* halo,
                                          float* a_halo, float* part) {
+  static_assert(!LEARNED || TWOD, "the learned gate takes the 2-D halo walk");
   const GateParams& g = p.g;
 #pragma unroll
   for (int u = 0; u < KI; ++u) {
@@ -328,10 +370,11 @@ __device__ __forceinline__ void halo_use(const FusedParams& p, const Tile& T, co
     if ((TWOD || W.twod) ? (rd * KI + u) * W.rg >= T.hh : (rd * KI + u) * NTHR + wave * 64 >= cm.total)
       break;
     if (!B.in[u]) B.vt[u] = uint4{0u, 0u, 0u, 0u};
-    if (!B.in[u] || (!CHAIN && g.no_prev)) B.vp[u] = uint4{0u, 0u, 0u, 0u};
+    if (!B.in[u] || (!CHAIN && g.no_prev) || (TRANS && !B.pin[u])) B.vp[u] = uint4{0u, 0u, 0u, 0u};
     const uint32_t wt[4] = {B.vt[u].x, B.vt[u].y, B.vt[u].z, B.vt[u].w};
     const uint32_t wpv[4] = {B.vp[u].x, B.vp[u].y, B.vp[u].z, B.vp[u].w};
     uint32_t outw[4];
+    float r[8];
     float sum = 0.0f;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -345,22 +388,34 @@ __device__ __forceinline__ void halo_use(const FusedParams& p, const Tile& T, co
         r0 = __fsub_rn(__uint_as_float(wt[e] << 16), __uint_as_float(wpv[e] << 16));
         r1 = __fsub_rn(__uint_as_float(wt[e] & 0xffff0000u), __uint_as_float(wpv[e] & 0xffff0000u));
       }
-      sum = add_rn(sum, term(r0, g.norm_p));
-      sum = add_rn(sum, term(r1, g.norm_p));
+      r[2 * e] = r0;
+      r[2 * e + 1] = r1;
+      if constexpr (!LEARNED) {
+        sum = add_rn(sum, term(r0, g.norm_p));
+        sum = add_rn(sum, term(r1, g.norm_p));
+      }
       outw[e] = pack_bf16(r0, r1);
     }
     // out-of-frame pixels: zero operand and zero statistic (outw, sum are 0)
     if (B.px[u] >= 0)
       *reinterpret_cast<u32x4*>(halo + (size_t)B.px[u] * p.pstride + B.ch[u] * 16) =
           u32x4{outw[0], outw[1], outw[2], outw[3]};
-    if (cm.lane_sum) {
-      float acc;
-      if (cm.nchk == 8) acc = group_sum<8>(sum);
-      else if (cm.nchk == 16) acc = group_sum<16>(sum);
-      else acc = group_sum<4>(sum);
-      if (B.px[u] >= 0 && B.ch[u] == 0) a_halo[B.px[u]] = acc;
-    } else if (B.px[u] >= 0) {
-      part[B.px[u] * p.pstage + B.ch[u]] = sum;
+    if constexpr (LEARNED) {
+      const float* ph = part + B.ch[u] * 8;
+      float* dst = (B.px[u] >= 0 && B.ch[u] == 0) ? a_halo + B.px[u] * g.k * g.k : nullptr;
+      if (cm.nchk == 8) learned_taps<8>(ph, g.c, g.k, r, dst);
+      else if (cm.nchk == 16) learned_taps<16>(ph, g.c, g.k, r, dst);
+      else learned_taps<4>(ph, g.c, g.k, r, dst);
+    } else {
+      if (cm.lane_sum) {
+        float acc;
+        if (cm.nchk == 8) acc = group_sum<8>(sum);
+        else if (cm.nchk == 16) acc = group_sum<16>(sum);
+        else acc = group_sum<4>(sum);
+        if (B.px[u] >= 0 && B.ch[u] == 0) a_halo[B.px[u]] = acc;
+      } else if (B.px[u] >= 0) {
+        part[B.px[u] * p.pstage + B.ch[u]] = sum;
+      }
     }
   }
 }
@@ -449,6 +504,101 @@ __device__ void gate_sites(const FusedParams& p, const Tile& T, const ChunkMap& 
   }
 }
 
+// gate_sites for the register-operand kernel's learned-gate and translated
+// modes: LEARNED, the Eq. 8 score (the in-frame per-tap terms in row-major
+// order, then the bias; on above zero); TRANS, exposed sites on (Sec. 3.3),
+// their blocks marked in blk_exp and tile_exp. (Folding these modes into
+// gate_sites changed how the compiler inlined it into the other kernels, and
+// some of those then took a scratch frame.)
+template <bool LEARNED, bool TRANS>
+__device__ __forceinline__ void gate_sites_t(const FusedParams& p, const Tile& T, const ChunkMap& cm, float* a_halo,
+                           const float* part, uint32_t* blk_flag, uint32_t* tile_on, bool lead = true,
+                           uint32_t* blk_exp = nullptr, uint32_t* tile_exp = nullptr) {
+  const GateParams& g = p.g;
+  const int s = g.stride, k = g.k, hw = T.hw;
+  lds_barrier();
+  if (!cm.lane_sum) {
+    for (int q = threadIdx.x; q < T.npix; q += kThreads) {
+      float acc = 0.0f;
+      for (int j = 0; j < cm.nchk; ++j) acc = add_rn(acc, part[q * p.pstage + j]);
+      a_halo[q] = acc;
+    }
+    lds_barrier();
+  }
+  for (int q = threadIdx.x; q < g.ts * g.ts; q += kThreads) {
+    const int ly = qdiv(q, T.inv_ts), lx = q - ly * g.ts;
+    if (ly >= T.oh || lx >= T.ow) continue;
+    float sv;
+    if (LEARNED && k == 3) {
+      // Eq. 8 score: the in-frame taps' terms in row-major order, then the
+      // bias. An out-of-frame tap adds +0 instead of being skipped: the sum
+      // starts at +0 and so is never -0, and x + (+0) = x for every other x.
+      // The nine reads are issued together.
+      const float* base = a_halo + ((ly * s) * hw + lx * s) * 9;
+      const int y0 = T.iy0 + ly * s, x0 = T.ix0 + lx * s;
+      float v[9];
+#pragma unroll
+      for (int i = 0; i < 9; ++i) {
+        const int kh = i / 3, kw = i % 3;
+        const bool in = y0 + kh >= 0 && y0 + kh < g.h && x0 + kw >= 0 && x0 + kw < g.w;
+        const float a = base[(kh * hw + kw) * 9 + i];
+        v[i] = in ? a : 0.0f;
+      }
+      sv = 0.0f;
+#pragma unroll
+      for (int i = 0; i < 9; ++i) sv = add_rn(sv, v[i]);
+      sv = add_rn(sv, g.gate_bias);
+    } else if (LEARNED) {
+      // as above, any kernel size: in-frame taps only
+      const int k2 = k * k;
+      sv = 0.0f;
+      for (int kh = 0; kh < k; ++kh) {
+        const int hy = ly * s + kh, y = T.iy0 + hy;
+        if (y < 0 || y >= g.h) continue;
+        for (int kw = 0; kw < k; ++kw) {
+          const int hx = lx * s + kw, x = T.ix0 + hx;
+          if (x < 0 || x >= g.w) continue;
+          sv = add_rn(sv, a_halo[(hy * hw + hx) * k2 + kh * k + kw]);
+        }
+      }
+      sv = add_rn(sv, g.gate_bias);
+    } else if (g.support == 0 && k == 3) {
+      const float* base = a_halo + (ly * s) * hw + lx * s;
+      float v[9];
+#pragma unroll
+      for (int i = 0; i < 9; ++i) v[i] = base[(i / 3) * hw + i % 3];
+      sv = 0.0f;
+#pragma unroll
+      for (int i = 0; i < 9; ++i) sv = add_rn(sv, v[i]);
+    } else if (g.support == 0) {
+      sv = 0.0f;
+      const float* base = a_halo + (ly * s) * hw + lx * s;
+      for (int kh = 0; kh < k; ++kh)
+        for (int kw = 0; kw < k; ++kw) sv = add_rn(sv, base[kh * hw + kw]);
+    } else {
+      sv = a_halo[(ly * s + g.pad) * hw + lx * s + g.pad];
+    }
+    // translated steps: exposed sites on (their blocks are recomputed from x_t)
+    const bool ex = TRANS && (line_exposed(T.oy0 + ly, g.h_out, g.h, k, s, g.pad, g.sy) ||
+                              line_exposed(T.ox0 + lx, g.w_out, g.w, k, s, g.pad, g.sx));
+    const bool on = g.reference || g.force_dense || (LEARNED ? sv > 0.0f : (double)sv * g.wnorm > g.thr) ||
+                    (sv != sv) || ex;
+    if (TRANS && ex) {
+      blk_exp[qdiv(ly, T.inv_blk) * T.tb_w + qdiv(lx, T.inv_blk)] = 1u;
+      *tile_exp = 1u;
+    }
+    if (g.keep_stats && lead) {
+      const size_t o = ((size_t)T.n * g.h_out + T.oy0 + ly) * g.w_out + T.ox0 + lx;
+      g.stat[o] = sv;
+      g.site_mask[o] = on ? 1 : 0;
+    }
+    if (on) {
+      blk_flag[qdiv(ly, T.inv_blk) * T.tb_w + qdiv(lx, T.inv_blk)] = 1u;
+      *tile_on = 1u;
+    }
+  }
+}
+
 // The tile's block flags to global memory (after the barrier that made
 // blk_flag final).
 __device__ void gate_flags(const FusedParams& p, const Tile& T, const uint32_t* blk_flag) {
@@ -475,11 +625,12 @@ __device__ void gate_tile(const FusedParams& p, const Tile& T, const ChunkMap& c
 // layers also write r = y_new - y_old for their successor, y_old =
 // dtype(act(z_{t-1})) (the activation output always equals dtype(act(z)), so
 // the old z already loaded for the update gives it).
-template <bool EMIT>
+// ASSIGN: z = U (blocks recomputed from x_t on translated steps).
+template <bool EMIT, bool ASSIGN = false>
 __device__ __forceinline__ void store_piece(const FusedParams& p, size_t o, const floatx4& u, const floatx4& zold) {
   floatx4 nv;
 #pragma unroll
-  for (int v = 0; v < 4; ++v) nv[v] = p.g.reference ? u[v] : zold[v] + u[v];
+  for (int v = 0; v < 4; ++v) nv[v] = (ASSIGN || p.g.reference) ? u[v] : zold[v] + u[v];
   *reinterpret_cast<floatx4*>(p.z + o) = nv;
   if (p.act) {
     uint32_t yb[4];
@@ -500,6 +651,18 @@ __device__ __forceinline__ void store_piece(const FusedParams& p, size_t o, cons
   }
 }
 
+// Translated steps: a site whose block is off keeps the translated z_{t-1}
+// (written to the new slot, with its activation output).
+__device__ __forceinline__ void store_copy(const FusedParams& p, size_t o, const floatx4& zold) {
+  *reinterpret_cast<floatx4*>(p.z + o) = zold;
+  if (p.act) {
+    uint32_t yb[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) yb[v] = f32_to_bf16(p.act == 2 ? relu_f32(zold[v]) : zold[v]);
+    *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.y) + o) = uint2{yb[0] | (yb[1] << 16), yb[2] | (yb[3] << 16)};
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Register-operand kernel for tiles of <= 8 x 8 sites (64 product rows, 4
 // M-tiles, NT 16-column N-tiles). Wave w = (kp * MG + mg) * NG + ng owns
@@ -510,11 +673,19 @@ __device__ __forceinline__ void store_piece(const FusedParams& p, size_t o, cons
 // sums; the weights come from global memory (L2) once. Rows outside the tile
 // read pixel (tap) of the halo like row 0: their columns of the product are
 // discarded, and a site's outputs depend on its own column only.
-// MODE bit 0: emit the successor's residual; bit 1: chained input.
+// MODE bit 0: emit the successor's residual; bit 1: chained input; bit 2:
+// learned gate (Eq. 8; phi staged in the chunk-sum region of LDS, the per-tap
+// terms in the statistic region); bit 3: translated step (Sec. 3.3: x_{t-1}
+// and z_{t-1} read shifted, every site written to the new z slot, and the
+// blocks holding an exposed site recomputed from x_t in a second product over
+// the same weights, with the halo rewritten to bf16(x_t)).
 template <int NT, int WN, int MT, int KPS, int KI, int MODE>
 __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
   constexpr bool EMIT = (MODE & 1) != 0;
   constexpr bool CHAIN = (MODE & 2) != 0;
+  constexpr bool LEARNED = (MODE & 4) != 0;
+  constexpr bool TRANS = (MODE & 8) != 0;
+  static_assert(!TRANS || !(EMIT || CHAIN), "translated steps neither emit nor chain");
   constexpr int NG = NT / WN;        // wave groups along N
   constexpr int MG = 4 / MT;         // wave groups along M
   constexpr int KP = kWaves / (NG * MG);  // k-step parts
@@ -524,6 +695,8 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
   __shared__ uint32_t blk_flag[kMaxTileBlocks];
   __shared__ uint32_t tile_on;
   __shared__ uint8_t emit_clr[kMaxTileBlocks];
+  __shared__ uint32_t blk_exp[TRANS ? kMaxTileBlocks : 1];  // translated steps: blocks with an exposed site
+  __shared__ uint32_t tile_exp;
 
   const GateParams& g = p.g;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -542,6 +715,17 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
   float* a_halo = reinterpret_cast<float*>(lds + p.off_a);
   float* part = reinterpret_cast<float*>(lds + p.off_part);
   const ChunkMap cm = make_chunks(p, T);
+  // learned gate: phi [tap][c] (k^2 c / 4 float4, at most kFusedPhiLoads per
+  // thread), loaded before anything else so that its LDS copy waits for it alone
+  float4 phv[LEARNED ? kFusedPhiLoads : 1];
+  if constexpr (LEARNED) {
+    const int nf4 = g.k * g.k * g.c / 4;
+#pragma unroll
+    for (int i = 0; i < kFusedPhiLoads; ++i) {
+      const int j = i * kThreads + threadIdx.x;
+      phv[i] = reinterpret_cast<const float4*>(g.phi)[j < nf4 ? j : 0];
+    }
+  }
 
   // 1. this wave's weight fragments (every load issued: a step past the
   // wave's k-range rereads its first fragment and goes unused), the halo loads
@@ -565,9 +749,10 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
   }
   const HaloWalk hwk = make_walk<kThreads, true>(g, T, cm, threadIdx.x);
   HaloBatch<KI> hb;
-  halo_load<CHAIN, kThreads, true, KI>(g, T, cm, hwk, 0, threadIdx.x, hb);
+  halo_load<CHAIN, kThreads, true, KI, TRANS>(g, T, cm, hwk, 0, threadIdx.x, hb);
   int esite[EP], eloc[EP], ecol[EP];
   floatx4 zold[EP];
+  bool zin[EP];  // translated steps: the source site lies in the grid (else z_{t-1} = 0 there)
 #pragma unroll
   for (int h = 0; h < EP; ++h) {
     const int e = h * kThreads + threadIdx.x;
@@ -578,12 +763,23 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
     esite[h] = ok ? gs : -1;
     eloc[h] = ok ? qdiv(ly, T.inv_blk) * T.tb_w + qdiv(lx, T.inv_blk) : 0;
     ecol[h] = col;
-    const size_t o = ok ? (size_t)gs * p.c_out + n0 * 16 + col : 0;
-    zold[h] = *reinterpret_cast<const floatx4*>(p.z + o);
+    if constexpr (TRANS) {
+      const int sy = T.oy0 + ly - g.sy / g.stride, sx = T.ox0 + lx - g.sx / g.stride;
+      zin[h] = ok && sy >= 0 && sy < g.h_out && sx >= 0 && sx < g.w_out;
+      const size_t os = zin[h] ? ((size_t)(T.n * g.h_out + sy) * g.w_out + sx) * p.c_out + n0 * 16 + col : 0;
+      zold[h] = *reinterpret_cast<const floatx4*>(p.zsrc + os);
+    } else {
+      const size_t o = ok ? (size_t)gs * p.c_out + n0 * 16 + col : 0;
+      zold[h] = *reinterpret_cast<const floatx4*>(p.z + o);
+    }
   }
 
   for (int i = threadIdx.x; i < kMaxTileBlocks; i += kThreads) blk_flag[i] = 0u;
   if (threadIdx.x == 0) tile_on = 0u;
+  if constexpr (TRANS) {
+    for (int i = threadIdx.x; i < kMaxTileBlocks; i += kThreads) blk_exp[i] = 0u;
+    if (threadIdx.x == 0) tile_exp = 0u;
+  }
   // product rows: M-tile i holds 16 sites of the tile. For 8 x 8 tiles they
   // are two tile rows rd apart, rd chosen so that rd * (halo width) = 8
   // (mod 16) when possible: a fragment read (16 lanes x 16 bytes, pixel stride
@@ -612,8 +808,18 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
     }
   }
 
+  if constexpr (LEARNED) {
+    const int nf4 = g.k * g.k * g.c / 4;
+#pragma unroll
+    for (int i = 0; i < kFusedPhiLoads; ++i) {
+      const int j = i * kThreads + threadIdx.x;
+      if (j < nf4) reinterpret_cast<float4*>(part)[j] = phv[i];
+    }
+    lds_barrier();
+  }
+
   // 2. halo use (and further rounds for large halos)
-  halo_use<CHAIN, kThreads, true, KI>(p, T, cm, hwk, 0, wave, hb, halo, a_halo, part);
+  halo_use<CHAIN, kThreads, true, KI, LEARNED, TRANS>(p, T, cm, hwk, 0, wave, hb, halo, a_halo, part);
   // weights and old z arrived with (or just after) the halo: settle them
   // before the x_t copy stores go out, so the product and the epilogue wait
   // for nothing
@@ -632,11 +838,15 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
   // the product is computed whether or not the gate turns any block of the
   // tile on (it does not depend on the gate), so the gate's latency overlaps
   // it instead of preceding it; a tile found off then stores nothing.
-  gate_sites(p, T, cm, a_halo, part, blk_flag, &tile_on, lead);
+  if constexpr (LEARNED || TRANS)
+    gate_sites_t<LEARNED, TRANS>(p, T, cm, a_halo, part, blk_flag, &tile_on, lead, blk_exp, &tile_exp);
+  else
+    gate_sites(p, T, cm, a_halo, part, blk_flag, &tile_on, lead);
 
   // product over this wave's k-steps: the first KPS - 1 always run, the
   // last one when the wave has KPS (a wave-uniform branch); the tap and
   // channel offset of a step is wave-uniform
+  auto product = [&]() {
   floatx4 acc[MT][WN];
 #pragma unroll
   for (int i = 0; i < MT; ++i)
@@ -675,19 +885,20 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
         *reinterpret_cast<floatx4*>(pbuf + (size_t)kp * 64 * PROW + msite[i] * PROW +
                                     ((ng * WN + j) * 16 + kq * 4) * 4) = acc[i][j];
   }
+  };
+  product();
   lds_barrier();
   if (lead) gate_flags(p, T, blk_flag);
-  if (!tile_on) {
+  if (!TRANS && !tile_on) {
     if (EMIT && lead) emit_clear(p, T.n, T.oy0, T.ox0, T.oh, T.ow, T.tb_w, blk_flag, emit_clr);
     return;
   }
 
   // 5. epilogue: the k-parts added in ascending order, at the active sites
-#pragma unroll
-  for (int h = 0; h < EP; ++h) {
-    if (esite[h] < 0 || blk_flag[eloc[h]] == 0u) continue;
-    const int e = h * kThreads + threadIdx.x;
-    const int site = e / (4 * NT);
+  // (translated steps: the blocks off keep the translated z_{t-1}; those with
+  // an exposed site wait for the second product)
+  auto sum_parts = [&](int h) {
+    const int site = (h * kThreads + (int)threadIdx.x) / (4 * NT);
     const uint8_t* src = pbuf + site * PROW + ecol[h] * 4;
     floatx4 u = *reinterpret_cast<const floatx4*>(src);
 #pragma unroll
@@ -696,9 +907,44 @@ __global__ void __launch_bounds__(kThreads) fused_rb_kernel(FusedParams p) {
 #pragma unroll
       for (int c = 0; c < 4; ++c) u[c] = u[c] + v[c];
     }
-    store_piece<EMIT>(p, (size_t)esite[h] * p.c_out + n0 * 16 + ecol[h], u, zold[h]);
+    return u;
+  };
+#pragma unroll
+  for (int h = 0; h < EP; ++h) {
+    if (esite[h] < 0) continue;
+    const size_t o = (size_t)esite[h] * p.c_out + n0 * 16 + ecol[h];
+    if constexpr (TRANS) {
+      if (!zin[h]) zold[h] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+      if (blk_exp[eloc[h]] != 0u) continue;
+      if (blk_flag[eloc[h]] == 0u) {
+        store_copy(p, o, zold[h]);
+        continue;
+      }
+    } else if (blk_flag[eloc[h]] == 0u) {
+      continue;
+    }
+    store_piece<EMIT>(p, o, sum_parts(h), zold[h]);
   }
   if (EMIT && lead) emit_clear(p, T.n, T.oy0, T.ox0, T.oh, T.ow, T.tb_w, blk_flag, emit_clr);
+  if constexpr (TRANS) {
+    if (!tile_exp) return;  // block-uniform (LDS, final since the barrier above)
+    // 6. blocks holding an exposed site: z = W * bf16(x_t) (assigned). The
+    // halo takes the x_t words (zero outside the frame) once every wave has
+    // read the partial sums of the first product.
+    lds_barrier();
+#pragma unroll
+    for (int u = 0; u < KI; ++u)
+      if (hb.px[u] >= 0)
+        *reinterpret_cast<uint4*>(halo + (size_t)hb.px[u] * p.pstride + hb.ch[u] * 16) = hb.vt[u];
+    lds_barrier();
+    product();
+    lds_barrier();
+#pragma unroll
+    for (int h = 0; h < EP; ++h) {
+      if (esite[h] < 0 || blk_exp[eloc[h]] == 0u) continue;
+      store_piece<false, true>(p, (size_t)esite[h] * p.c_out + n0 * 16 + ecol[h], sum_parts(h), zold[h]);
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1358,12 +1604,21 @@ hipError_t launch_dw_t(const FusedParams& p, int grid, hipStream_t st) {
 
 template <int NT, int WN, int MT, int KPS, int KI>
 hipError_t launch_rb_t(const FusedParams& p, int grid, hipStream_t st) {
-  switch ((p.emit ? 1 : 0) | (p.g.rin ? 2 : 0)) {
-    case 0: hipLaunchKernelGGL((fused_rb_kernel<NT, WN, MT, KPS, KI, 0>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
-    case 1: hipLaunchKernelGGL((fused_rb_kernel<NT, WN, MT, KPS, KI, 1>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
-    case 2: hipLaunchKernelGGL((fused_rb_kernel<NT, WN, MT, KPS, KI, 2>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
-    default: hipLaunchKernelGGL((fused_rb_kernel<NT, WN, MT, KPS, KI, 3>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p); break;
+#define SC_RB(m) hipLaunchKernelGGL((fused_rb_kernel<NT, WN, MT, KPS, KI, m>), dim3(grid), dim3(kThreads), p.lds_bytes, st, p)
+  switch ((p.emit ? 1 : 0) | (p.g.rin ? 2 : 0) | (p.g.learned ? 4 : 0) | (p.zsrc ? 8 : 0)) {
+    case 0: SC_RB(0); break;
+    case 1: SC_RB(1); break;
+    case 2: SC_RB(2); break;
+    case 3: SC_RB(3); break;
+    case 4: SC_RB(4); break;
+    case 5: SC_RB(5); break;
+    case 6: SC_RB(6); break;
+    case 7: SC_RB(7); break;
+    case 8: SC_RB(8); break;
+    case 12: SC_RB(12); break;
+    default: return hipErrorInvalidValue;
   }
+#undef SC_RB
   return hipGetLastError();
 }
 
@@ -1426,14 +1681,23 @@ int prepare_dw_t(const FusedParams& p) {
   return std::min(std::min(a, b), c);
 }
 
-template <int NT, int WN, int MT, int KPS, int KI>
-int prepare_rb_t(const FusedParams& p) {
-  const int a = prepare_kernel(fused_rb_kernel<NT, WN, MT, KPS, KI, 0>, p);
-  const int b = prepare_kernel(fused_rb_kernel<NT, WN, MT, KPS, KI, 2>, p);
-  const int c = p.emit ? std::min(prepare_kernel(fused_rb_kernel<NT, WN, MT, KPS, KI, 1>, p),
-                                  prepare_kernel(fused_rb_kernel<NT, WN, MT, KPS, KI, 3>, p))
+template <int NT, int WN, int MT, int KPS, int KI, int L>
+int prepare_rb_m(const FusedParams& p) {
+  const int a = prepare_kernel(fused_rb_kernel<NT, WN, MT, KPS, KI, L>, p);
+  const int b = prepare_kernel(fused_rb_kernel<NT, WN, MT, KPS, KI, L | 2>, p);
+  const int c = p.emit ? std::min(prepare_kernel(fused_rb_kernel<NT, WN, MT, KPS, KI, L | 1>, p),
+                                  prepare_kernel(fused_rb_kernel<NT, WN, MT, KPS, KI, L | 3>, p))
                        : a;
   return std::min(std::min(a, b), c);
+}
+
+template <int NT, int WN, int MT, int KPS, int KI>
+int prepare_rb_t(const FusedParams& p) {
+  int occ = p.g.learned ? prepare_rb_m<NT, WN, MT, KPS, KI, 4>(p) : prepare_rb_m<NT, WN, MT, KPS, KI, 0>(p);
+  if (p.trans_ok)
+    occ = std::min(occ, p.g.learned ? prepare_kernel(fused_rb_kernel<NT, WN, MT, KPS, KI, 12>, p)
+                                    : prepare_kernel(fused_rb_kernel<NT, WN, MT, KPS, KI, 8>, p));
+  return occ;
 }
 
 }  // namespace

@@ -188,7 +188,16 @@ struct FusedParams {
   uint8_t* prev_mask;      // blocks updated by the previous step
   int dw;                  // depthwise kernel: its halo rows per thread (fused_dw_ki), 0: dense
   int sc;                  // few-channel kernel: 1 fp32 by elements, 4 fp32 by 4, 2 bf16; 0: none
+  // translated step (Sec. 3.3): z_{t-1} in the other slot, read at the site
+  // shifted back by (g.sy, g.sx) / stride (zero outside the grid); z is then
+  // written at every site. Null on other steps.
+  const float* zsrc;
+  int trans_ok;            // the layer may take translated steps (create: prepare that mode)
 };
+
+// Learned gate in the register-operand fused kernel: phi (k^2 * C_in fp32)
+// takes at most this many float4 loads per thread (512 threads).
+constexpr int kFusedPhiLoads = 2;
 
 // Few-channel fused kernel (fp32 C_in <= 16, bf16 C_in < 8): halo loads in
 // flight per thread per round, and k-steps per wave at most (two k-parts).

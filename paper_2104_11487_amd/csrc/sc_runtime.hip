@@ -318,17 +318,24 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
   G.fused = false;
   G.f_dw = 0;
   G.f_sc = 0;
+  // the learned gate runs in the register-operand build when a pixel's chunks
+  // form one lane group (C_in 32, 64 or 128) and phi fits its staging loads
+  const bool learned_fused = !G.learned || ((d->c_in == 32 || d->c_in == 64 || d->c_in == 128) &&
+                                            (long)k * k * d->c_in <= (long)sc::kFusedPhiLoads * 512 * 4);
   if (!depthwise && d->dtype == SKIPCONV_BF16 && d->c_in % 32 == 0 && d->c_out % 4 == 0 && b <= 16 &&
-      G.ntn >= 2 && !G.learned && !(d->flags & SKIPCONV_FLAG_SPLIT_PIPELINE)) {
+      G.ntn >= 2 && learned_fused && !(d->flags & SKIPCONV_FLAG_SPLIT_PIPELINE)) {
     const int ts = b <= 8 ? b * (8 / b) : b;
     const int mw = ts <= 8 ? 1 : 4;
     if (!(mw == 4 && G.ntn > 8)) {
       const int hh = (ts - 1) * s + k;
       const long pstride = 2L * d->c_in + 16;
       const long halo_b = ((long)hh * hh + 1) * pstride;  // + the zero pixel
-      const long a_b = ((long)hh * hh * 4 + 15) / 16 * 16;
+      // pixel statistics (learned gate: per-tap terms) and parked chunk sums
+      // (learned gate: the staged phi)
+      const long a_b = ((long)hh * hh * (G.learned ? k * k : 1) * 4 + 15) / 16 * 16;
       const int pstage = (d->c_in / 8) | 1;
-      const long part_b = ((long)hh * hh * pstage * 4 + 15) / 16 * 16;
+      const long part_b = std::max(((long)hh * hh * pstage * 4 + 15) / 16 * 16,
+                                   G.learned ? (long)k * k * d->c_in * 4 : 0L);
       const long whole = (long)G.ksteps * G.ntn * 1024;
       long b_bytes = whole;
       int kc = G.ksteps, nbuf = 1;
@@ -357,6 +364,8 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
       if (rb) {
         const long kparts = sc::fused_rb_kparts(rb);
         b_bytes = kparts * 64 * ((long)(G.ntn / nsplit) * 64 + 16);
+      } else if (G.learned) {
+        b_bytes = kFusedLdsLimit + 1;  // the learned gate has the register-operand build only
       } else if (whole + halo_b + a_b + part_b > kFusedLdsLimit) {
         kc = std::max(1, 16 / G.ntn);
         nbuf = 2;
@@ -616,6 +625,7 @@ sc::FusedParams fused_params(skipconv_layer* h, const void* x_t, bool ref) {
   fp.nsplit = (g.f_rb || g.f_dw) ? g.f_nsplit : 1;
   fp.dw = g.f_dw;
   fp.sc = g.f_sc;
+  fp.trans_ok = (d.flags & SKIPCONV_FLAG_TRANSLATE) ? 1 : 0;
   fp.tiles = reinterpret_cast<const uint32_t*>(h->ws + g.off_ftiles);
   fp.inv_ts = 1.0f / (float)g.f_ts;
   fp.inv_blk = 1.0f / (float)d.block;
@@ -1100,6 +1110,26 @@ int skipconv_step_translated(skipconv_t h, const void* x_t, int32_t dy, int32_t 
     return fail(h->last_error, SKIPCONV_E_STATE, "learned gate: call skipconv_set_gate_weights first");
   hipStream_t st = static_cast<hipStream_t>(stream);
   const Geometry& g = h->g;
+  if (g.fused && g.f_rb) {
+    // one pass of the register-operand kernel: x_{t-1} and z_{t-1} read
+    // shifted, every site written to the other z slot, blocks holding an
+    // exposed site recomputed from x_t
+    sc::FusedParams fp = fused_params(h, x_t, false);
+    fp.z = h->z_other();
+    fp.zsrc = h->z();
+    fp.g.sy = dy;
+    fp.g.sx = dx;
+    const hipError_t e = sc::launch_fused(fp, g.f_grid * fp.nsplit, st);
+    if (e != hipSuccess) return hip_fail(h, e, "translated fused launch");
+    h->zslot ^= 1;
+    h->list_valid = false;
+    h->work_kind = 0;
+    h->advance_input(x_t);
+    h->ref_pending = false;
+    ++h->frames;
+    if (z_t) *z_t = h->z();
+    return SKIPCONV_OK;
+  }
   // 1. z <- T~(z) into the other slot (activation output refreshed)
   hipError_t e = sc::launch_translate_state(h->z(), h->z_other(), h->y(), d.n, g.h_out, g.w_out, d.c_out,
                                             dy / d.stride, dx / d.stride, d.act_out, d.dtype, st);

@@ -38,10 +38,12 @@ def _layer_pair(w_f32, *, n, h, w, dtype, eps, block, stride=1, pad=-1, groups=1
 
 
 def run_single(frames, w_f32, *, dtype, eps, block, tag, resets=(), exact_z=False,
-               keep_stats=True, **kw):
+               keep_stats=True, expect_fused=None, **kw):
     n, h, w, _ = frames[0].shape
     layer, orc = _layer_pair(w_f32, n=n, h=h, w=w, dtype=dtype, eps=eps, block=block,
                              keep_stats=keep_stats, **kw)
+    if expect_fused is not None:
+        assert layer.fused == expect_fused, (tag, layer.fused)
     worst, dens = 0.0, []
     for t, f in enumerate(frames):
         if t in resets:
@@ -1195,8 +1197,9 @@ def _learned_bias(frames, phi, dtype, k, stride, site_density):
     return float(np.float32(-np.quantile(np.concatenate(vals), 1.0 - site_density)))
 
 
+@pytest.mark.parametrize("split", [False, True], ids=["fused", "split"])
 @pytest.mark.parametrize("block", [1, 8])
-def test_learned_gate_rect64(block):
+def test_learned_gate_rect64(block, split):
     wl = syn.workloads()["rect64"]
     frames = list(wl.video(10))
     rng = np.random.Generator(np.random.PCG64(95))
@@ -1204,8 +1207,28 @@ def test_learned_gate_rect64(block):
     # per-site score quantile; with 8 x 8 blocks a much smaller site fraction leaves blocks off
     bias = _learned_bias(frames, phi, "bf16", 3, 1, 0.25 if block == 1 else 0.003)
     worst, dens = run_single(frames, wl.weights()[0], dtype="bf16", eps=0.0, block=block, gate="learned",
-                             phi=phi, gate_bias=bias, tag=f"rect64 learned gate b={block}", resets=(6,))
+                             phi=phi, gate_bias=bias, tag=f"rect64 learned gate b={block} split={split}",
+                             resets=(6,), split=split, expect_fused=not split)
     assert 0.0 < np.mean(dens[1:]) < 1.0
+
+
+@pytest.mark.parametrize("case", [
+    # c_in, c_out, k, stride, block, frame h, w, batch
+    (32, 64, 3, 1, 8, 37, 29, 2),     # ragged tiles, 4 chunks a pixel
+    (128, 128, 3, 1, 4, 24, 40, 1),   # 16 chunks a pixel, output channels split over 4 workgroups
+    (64, 128, 3, 2, 4, 33, 35, 1),    # stride 2 (a 17 x 17 halo), split over 2 workgroups
+], ids=["c32ragged", "c128", "s2"])
+def test_learned_gate_fused_geometries(case):
+    """The learned gate in the single-pass kernel (per-tap chunk terms in its
+    halo phase) against the oracle, on shapes that take it."""
+    c_in, c_out, k, stride, block, h, w, n = case
+    rng = np.random.Generator(np.random.PCG64(190 + c_in + k))
+    wt = rng.normal(0, 0.1, (c_out, c_in, k, k)).astype(np.float32)
+    phi = rng.normal(0, 0.2, (c_in, k, k)).astype(np.float32)
+    frames = list(syn.RectVideo(h, w, c_in, 7, seed=191 + c_in, batch=n, side_lo=3, side_hi=8))
+    bias = _learned_bias(frames, phi, "bf16", k, stride, 0.2)
+    run_single(frames, wt, dtype="bf16", eps=0.0, block=block, stride=stride, gate="learned", phi=phi,
+               gate_bias=bias, tag=f"learned fused {case}", resets=(4,), expect_fused=True)
 
 
 @pytest.mark.parametrize("case", [
@@ -1261,27 +1284,40 @@ def test_learned_gate_requires_weights_and_nan_turns_on():
 
 # ------------------------------------- sparse residual propagation (chained) --
 
-def run_chain_propagated(frames, weights, specs, *, dtype, act, epss, block, tag, resets=(), split=True):
+def run_chain_propagated(frames, weights, specs, *, dtype, act, epss, block, tag, resets=(), split=True,
+                         learned=None, expect_fused=None):
     """Layers 2.. step on the previous layer's emitted residual (skipconv_step_chained).
 
     Checked per layer and frame against (a) the oracle fed the GPU's own layer
     input (masks bit-exact, z within tolerance) and (b) the same stack stepped
-    with full frames through the split pipeline: masks, lists and z bit-exact.
+    with full frames: masks, lists and z bit-exact. learned: {layer: (phi,
+    bias)} for layers with the learned gate (Eq. 8). expect_fused: the
+    pipeline every layer must take.
     """
     n, h, w, _ = frames[0].shape
+    learned = learned or {}
     chained, plain, orcs = [], [], []
     hh, ww = h, w
     for i, (wt, sp) in enumerate(zip(weights, specs)):
         last = i == len(weights) - 1
         a = "none" if last else act
+        gk = {}
+        if i in learned:
+            gk = dict(gate="learned", phi=learned[i][0], gate_bias=learned[i][1])
         lay, orc = _layer_pair(wt, n=n, h=hh, w=ww, dtype=dtype, eps=epss[i], block=block,
-                               stride=sp.stride, groups=sp.groups, act_out=a, split=True)
+                               stride=sp.stride, groups=sp.groups, act_out=a, split=True, **gk)
         lay.close()
         ws = weight_storage(wt, dtype)
         kw = dict(n=n, h=hh, w=ww, stride=sp.stride, groups=sp.groups, eps=epss[i], block=block,
-                  keep_stats=True, act_out=a, split=split)
+                  keep_stats=True, act_out=a, split=split, gate=gk.get("gate", "input"))
         chained.append(S.SkipConv(to_device(ws, dtype), emit_residual=not last, **kw))
         plain.append(S.SkipConv(to_device(ws, dtype), **kw))
+        for lay in (chained[-1], plain[-1]):
+            if gk:
+                lay.set_gate_weights(torch.from_numpy(np.ascontiguousarray(gk["phi"], np.float32)).cuda(),
+                                     gk["gate_bias"])
+            if expect_fused is not None:
+                assert lay.fused == expect_fused, (tag, i, lay.fused)
         orcs.append(orc)
         hh, ww = chained[-1].h_out, chained[-1].w_out
     skipped = 0
@@ -1360,6 +1396,31 @@ def test_chain_two_layers_sparse_motion(dtype, block, split):
                          tag=f"chain2 {dtype} b={block} split={split}", resets={3: (1,)}, split=split)
 
 
+@PIPE
+def test_chain_learned_gate_layers(split):
+    """Both layers with the learned gate (Eq. 8), the second stepped on the
+    first's emitted residual: a zero residual leaves the score at the bias, so
+    no tile may be skipped for lack of upstream blocks."""
+    rng = np.random.Generator(np.random.PCG64(99))
+    c0, c1, c2 = 32, 64, 64
+    w1 = rng.normal(0, 0.15, (c1, c0, 3, 3)).astype(np.float32)
+    w2 = rng.normal(0, 0.1, (c2, c1, 3, 3)).astype(np.float32)
+    frames = list(syn.RectVideo(40, 56, c0, 6, seed=199, batch=2, side_lo=4, side_hi=10))
+    phi1 = rng.normal(0, 0.2, (c0, 3, 3)).astype(np.float32)
+    phi2 = rng.normal(0, 0.1, (c1, 3, 3)).astype(np.float32)
+    bias1 = _learned_bias(frames, phi1, "bf16", 3, 1, 0.3)
+    Spec = type("Spec", (), {})
+    specs = []
+    for _ in range(2):
+        sp = Spec()
+        sp.stride, sp.groups = 1, 1
+        specs.append(sp)
+    # second layer: a small positive bias keeps the sites with a zero residual on
+    run_chain_propagated(frames, [w1, w2], specs, dtype="bf16", act="relu", epss=[0.0, 0.0], block=8,
+                         tag=f"chain learned split={split}", resets={4: (1,)}, split=split,
+                         learned={0: (phi1, bias1), 1: (phi2, np.float32(0.02))}, expect_fused=not split)
+
+
 def test_chained_step_contract_errors():
     rng = np.random.Generator(np.random.PCG64(98))
     w = rng.normal(0, 0.3, (16, 16, 3, 3)).astype(np.float32)
@@ -1384,9 +1445,11 @@ def test_chained_step_contract_errors():
 
 # ------------------------------------- translation-compensated steps (Sec. 3.3) --
 
-def run_translated(frames, shifts, w_f32, *, dtype, eps, block, tag, exact_z=False, **kw):
+def run_translated(frames, shifts, w_f32, *, dtype, eps, block, tag, exact_z=False, expect_fused=None, **kw):
     n, h, w, _ = frames[0].shape
     layer, orc = _layer_pair(w_f32, n=n, h=h, w=w, dtype=dtype, eps=eps, block=block, translate=True, **kw)
+    if expect_fused is not None:
+        assert layer.fused == expect_fused, (tag, layer.fused)
     dens = []
     for t, (f, d) in enumerate(zip(frames, shifts)):
         xs = syn.to_storage(f, dtype)
@@ -1412,40 +1475,62 @@ def _translated_integer_video(rng, n, h, w, c, shifts, stride):
 
 
 @pytest.mark.parametrize("case", [
-    # dtype, block, k, stride, groups, c_in, c_out
-    ("f32", 1, 3, 1, 1, 8, 16),
-    ("bf16", 4, 3, 1, 1, 32, 64),     # halo conv
-    ("bf16", 8, 5, 1, 1, 16, 32),     # direct gather
-    ("f32", 2, 3, 2, 1, 8, 8),        # stride 2, even shifts
-    ("bf16", 1, 3, 1, 16, 16, 16),    # depthwise
-], ids=["f32b1", "bf16halo", "bf16k5", "f32s2", "bf16dw"])
+    # dtype, block, k, stride, groups, c_in, c_out, split pipeline
+    ("f32", 1, 3, 1, 1, 8, 16, True),
+    ("bf16", 4, 3, 1, 1, 32, 64, True),     # halo conv
+    ("bf16", 4, 3, 1, 1, 32, 64, False),    # single-pass kernel (second product for exposed blocks)
+    ("bf16", 8, 3, 2, 1, 64, 128, False),   # single-pass, stride 2, even shifts
+    ("bf16", 8, 5, 1, 1, 16, 32, True),     # direct gather
+    ("f32", 2, 3, 2, 1, 8, 8, True),        # stride 2, even shifts
+    ("bf16", 1, 3, 1, 16, 16, 16, True),    # depthwise
+], ids=["f32b1", "bf16halo", "bf16fused", "bf16fuseds2", "bf16k5", "f32s2", "bf16dw"])
 def test_translated_eps0_integer_is_dense_conv(case):
     """eps = 0 over translated integer frames: z equals conv2d(x_t) bit for bit, masks match the oracle."""
-    dtype, block, k, stride, groups, c_in, c_out = case
+    dtype, block, k, stride, groups, c_in, c_out, split = case
     rng = np.random.Generator(np.random.PCG64(140 + k + block))
     s = stride
     shifts = [(0, 0), (s, 0), (0, -2 * s), (-s, s), (0, 0), (2 * s, -s), (-3 * s, 2 * s)]
     frames = _translated_integer_video(rng, 2, 26, 22, c_in, shifts, stride)
     w = syn.integer_weights(c_out, c_in // groups, k, seed=141)
     run_translated(frames, shifts, w, dtype=dtype, eps=0.0, block=block, stride=stride, groups=groups,
-                   pad=-1, tag=f"translated eps0 {case}", exact_z=True)
+                   pad=-1, tag=f"translated eps0 {case}", exact_z=True, split=split,
+                   expect_fused=False if split else True)
 
 
-@pytest.mark.parametrize("block", [1, 8])
-def test_translated_rect64_with_gate(block):
-    """The 128 x 96 x 64 layer on a video panning by a few pixels per frame, eps > 0."""
+def _panning_rect64(n_frames):
     wl = syn.workloads()["rect64"]
-    base = list(wl.video(8))
-    shifts = [(0, 0), (1, 2), (1, 2), (0, -3), (2, 0), (0, 0), (-1, -1), (3, 1)]
+    base = list(wl.video(n_frames))
+    shifts = [(0, 0), (1, 2), (1, 2), (0, -3), (2, 0), (0, 0), (-1, -1), (3, 1)][:n_frames]
     frames, acc = [], (0, 0)
     for f, d in zip(base, shifts):
         acc = (acc[0] + d[0], acc[1] + d[1])
         frames.append(O.translate(f, *acc))
+    return wl, base, frames, shifts
+
+
+@PIPE
+@pytest.mark.parametrize("block", [1, 8])
+def test_translated_rect64_with_gate(block, split):
+    """The 128 x 96 x 64 layer on a video panning by a few pixels per frame, eps > 0."""
+    wl, base, frames, shifts = _panning_rect64(8)
     stats = oracle_stats(base, (64, 64, 3, 3), dtype="bf16")
     eps = eps_for_density(stats, block, 128, 96, 0.25)
     dens = run_translated(frames, shifts, wl.weights()[0], dtype="bf16", eps=eps, block=block,
-                          tag=f"rect64 translated b={block}")
+                          tag=f"rect64 translated b={block} split={split}", split=split, expect_fused=not split)
     assert np.mean(dens[1:]) < 1.0
+
+
+@PIPE
+def test_translated_rect64_learned_gate(split):
+    """Translated steps with the learned gate (Eq. 8 on r = x_t - T(x_{t-1}), exposed sites on)."""
+    wl, base, frames, shifts = _panning_rect64(8)
+    rng = np.random.Generator(np.random.PCG64(142))
+    phi = rng.normal(0, 0.05, (64, 3, 3)).astype(np.float32)
+    bias = _learned_bias(base, phi, "bf16", 3, 1, 0.004)
+    dens = run_translated(frames, shifts, wl.weights()[0], dtype="bf16", eps=0.0, block=8, gate="learned",
+                          phi=phi, gate_bias=bias, tag=f"rect64 translated learned split={split}", split=split,
+                          expect_fused=not split)
+    assert 0.0 < np.mean(dens[1:]) < 1.0
 
 
 def test_shake_frames_compensated():
