@@ -327,10 +327,14 @@ __device__ __forceinline__ void halo_load(const GateParams& g, const Tile& T, co
 // first lane (dst: its pixel's k^2 terms, null elsewhere). ph = phi + 8 ch,
 // phi [tap][c] in LDS. 3 x 3 kernels take an unrolled loop: the nine chains
 // are independent, so their LDS reads and group sums overlap. (Reading a
-// tap's phi once for all of a thread's items, or skipping per wave the tap
-// rows that no pixel of the wave serves, measured slower.)
+// tap's phi once for all of a thread's items measured no faster.) A wave
+// skips a row kh of three taps when none of its pixels (halo row hy) serves
+// it: a site's score reads tap (kh, kw) of halo row ly * stride + kh only, so
+// hy - kh must lie in [0, span], span = (oh - 1) * stride (the halo's border
+// rows need one or two of the three rows).
 template <int NC>
-__device__ __forceinline__ void learned_taps(const float* ph, int c, int k, const float (&r)[8], float* dst) {
+__device__ __forceinline__ void learned_taps(const float* ph, int c, int k, const float (&r)[8], float* dst,
+                                             int hy, int span) {
   auto tap = [&](int t) {
     const float4 f0 = *reinterpret_cast<const float4*>(ph + t * c);
     const float4 f1 = *reinterpret_cast<const float4*>(ph + t * c + 4);
@@ -343,7 +347,11 @@ __device__ __forceinline__ void learned_taps(const float* ph, int c, int k, cons
   };
   if (k == 3) {
 #pragma unroll
-    for (int t = 0; t < 9; ++t) tap(t);
+    for (int kh = 0; kh < 3; ++kh) {
+      if (__ballot(dst != nullptr && hy >= kh && hy - kh <= span) == 0ull) continue;  // wave-uniform
+#pragma unroll
+      for (int kw = 0; kw < 3; ++kw) tap(kh * 3 + kw);
+    }
   } else {
     for (int t = 0; t < k * k; ++t) tap(t);
   }
@@ -403,9 +411,10 @@ __device__ __forceinline__ void halo_use(const FusedParams& p, const Tile& T, co
     if constexpr (LEARNED) {
       const float* ph = part + B.ch[u] * 8;
       float* dst = (B.px[u] >= 0 && B.ch[u] == 0) ? a_halo + B.px[u] * g.k * g.k : nullptr;
-      if (cm.nchk == 8) learned_taps<8>(ph, g.c, g.k, r, dst);
-      else if (cm.nchk == 16) learned_taps<16>(ph, g.c, g.k, r, dst);
-      else learned_taps<4>(ph, g.c, g.k, r, dst);
+      const int hy = W.r0 + (rd * KI + u) * W.rg, span = (T.oh - 1) * g.stride;
+      if (cm.nchk == 8) learned_taps<8>(ph, g.c, g.k, r, dst, hy, span);
+      else if (cm.nchk == 16) learned_taps<16>(ph, g.c, g.k, r, dst, hy, span);
+      else learned_taps<4>(ph, g.c, g.k, r, dst, hy, span);
     } else {
       if (cm.lane_sum) {
         float acc;
