@@ -73,7 +73,9 @@ enum { SKIPCONV_SUPPORT_RF = 0, SKIPCONV_SUPPORT_CENTRE = 1 };
  *                phi[c, tap] * r[q, c] over chunks of 8 channels (ascending
  *                within a chunk, chunk sums ascending), all fp32 without FMA;
  *                phi and bias come from skipconv_set_gate_weights; eps and
- *                norm_p are not used. Split pipeline only.
+ *                norm_p are not used. Runs on the split pipeline, and in the
+ *                single-pass register-operand kernel for bf16 layers with
+ *                c_in 32, 64 or 128 and k*k*c_in <= 4096.
  * A NaN statistic turns the gate on in all three; a reference frame is dense. */
 enum { SKIPCONV_GATE_INPUT_NORM = 0, SKIPCONV_GATE_OUTPUT_NORM = 1, SKIPCONV_GATE_LEARNED = 2 };
 
@@ -207,8 +209,10 @@ int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t
  * z equals the dense convolution of x_t. dy and dx must be multiples of the
  * stride with |dy| < h, |dx| < w; (0, 0) or a pending reference frame is a
  * plain skipconv_step. The layer needs SKIPCONV_FLAG_TRANSLATE (E_STATE
- * otherwise). Runs the split pipeline; z moves to the other of its two slots,
- * so use the returned pointer. */
+ * otherwise). Layers on the single-pass register-operand kernel take the
+ * translated step in that kernel (the exposed blocks in a second product over
+ * the same weights); the others run the split pipeline. z moves to the other
+ * of its two slots, so use the returned pointer. */
 int skipconv_step_translated(skipconv_t h, const void* x_t, int32_t dy, int32_t dx, void* stream,
                              const float** z_t);
 

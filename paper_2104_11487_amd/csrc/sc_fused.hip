@@ -21,17 +21,23 @@
 //      lane holds 4 consecutive output channels of one site;
 //   4. epilogue: z (+)= U at the active sites, activation output refreshed.
 //
-// Two kernels share steps 1-2:
+// Kernels sharing steps 1-2:
 //   * fused_rb_kernel (tiles of <= 8 x 8 sites): wave (ng, kp) owns two
 //     16-column tiles of the output and one part of the k-steps; its weight
 //     fragments go straight from global memory into registers (issued during
 //     the gate), so LDS carries only the residual operand; the k-partial sums
 //     meet in LDS and all waves finish the epilogue. The old z of every site
 //     is fetched with the halo, so no load waits between gate and product.
+//     It also runs the learned gate (Eq. 8: per-tap chunk terms in the halo
+//     phase) and translated steps (Sec. 3.3: shifted x_{t-1} and z_{t-1}
+//     reads, exposed blocks recomputed from x_t in a second product).
 //   * fused_kernel (16 x 16 tiles and shapes the first does not cover): the
 //     packed weights are copied into LDS with global_load_lds by two loader
 //     waves during the halo phase; 16 x 16 tiles compact their active sites
 //     (ballot + prefix) into the product rows.
+//   * fused_dw_kernel (depthwise) and fused_sc_kernel (fewer than 8 bf16 or
+//     at most 16 fp32 input channels): the product on the VALU, or with the
+//     weights as the MFMA A operand.
 //
 // The ordered global active list is not needed by this pipeline; it is
 // produced on demand for introspection by the compaction kernel.
