@@ -6,7 +6,9 @@ import numpy as np
 
 from oracle import skipconv_oracle as O
 
-TOL = {"f32": 1e-4, "bf16": 2e-2}  # normwise relative bound on z after every frame
+TOL = {"f32": 1e-4, "bf16": 2e-2}  # normwise relative bound on z after every frame (the contract)
+ORDER_TOL = 1e-4   # normwise, both dtypes: accumulation order only (measured <= 1.8e-6)
+ELEM_TOL = 1e-2    # per element, relative to |z| + 1e-3 max|z| (measured <= 4.4e-4)
 
 
 def say(msg: str) -> None:
@@ -74,7 +76,24 @@ def compare_frame(layer, ref: dict, dtype: str, *, t: int, tag: str, keep_stats:
         return 0.0
     e = rel_err(zg, ref["z"])
     assert e <= TOL[dtype], f"{tag} t={t}: z rel err {e:.3e} > {TOL[dtype]}"
+    # tighter than the contract: both sides apply the same operand rounding,
+    # so what remains is the fp32 accumulation order of one frame's K <= 1152
+    # products (K * 2^-24 < 1e-4 normwise) carried over the frames
+    assert e <= ORDER_TOL, f"{tag} t={t}: z rel err {e:.3e} > {ORDER_TOL} (accumulation-order bound)"
+    pe = elementwise_err(zg, ref["z"])
+    assert pe <= ELEM_TOL, f"{tag} t={t}: per-element z error {pe:.3e} > {ELEM_TOL}"
     return e
+
+
+def elementwise_err(z_gpu: np.ndarray, z_ref: np.ndarray) -> float:
+    """max |z_gpu - z_ref| / (|z_ref| + 1e-3 max |z_ref|) over finite entries: an
+    update missing at a few sites shows here even when the normwise error is small."""
+    fin = ~np.isnan(z_ref)
+    if not fin.any():
+        return 0.0
+    scale = max(float(np.max(np.abs(z_ref[fin]))), 1e-30)
+    d = np.abs(z_gpu[fin].astype(np.float64) - z_ref[fin])
+    return float(np.max(d / (np.abs(z_ref[fin]) + 1e-3 * scale)))
 
 
 def check_work_list(layer, active, *, tag: str, t: int) -> None:
