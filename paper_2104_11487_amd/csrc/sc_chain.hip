@@ -19,6 +19,7 @@ namespace {
 
 constexpr int kEmitThreads = 256;
 constexpr int kEmitSites = 64;  // output sites (whole blocks) per workgroup, at least one block
+constexpr int kEmitUnroll = 4;  // 8-channel groups a thread has in flight (bf16 layers)
 
 // Workgroup w takes blocks [w * bpw, (w + 1) * bpw) of the flattened block grid
 // (bpw = max(1, kEmitSites / b^2)); each thread walks (site, channel) elements.
@@ -41,6 +42,71 @@ emit_kernel(const uint8_t* block_mask, uint8_t* prev_mask, int nb, int bpw, cons
   const int vec = (c_out & 7) == 0 ? 8 : 1;
   const int cg = c_out / vec;
   const int total = nblk * bsz * cg;
+  if (vec == 8 && dtype == 1) {
+    // bf16 layers: kEmitUnroll groups per thread in flight (their z and y
+    // loads issued together), then computed and stored
+    constexpr int U = kEmitUnroll;
+    uint16_t* yb = static_cast<uint16_t*>(y);
+    for (int e0 = threadIdx.x; e0 < total; e0 += kEmitThreads * U) {
+      size_t o[U];
+      uint8_t stu[U];
+      float4 z0[U], z1[U];
+      uint4 yo[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int e = e0 + u * kEmitThreads;
+        stu[u] = 0;
+        o[u] = 0;
+        if (e < total) {
+          const int bl = e / (bsz * cg), rem0 = e - bl * bsz * cg;
+          const int site = rem0 / cg, ch = (rem0 - site * cg) * 8;
+          const int blk = b0 + bl;
+          const int img = blk / (hb * wb), rem = blk - img * hb * wb;
+          const int bi = rem / wb, bj = rem - bi * wb;
+          const int oy = bi * block + site / block, ox = bj * block + site % block;
+          if (oy < h_out && ox < w_out) {  // ceil-mode edge block
+            stu[u] = state[bl];
+            o[u] = ((size_t)(img * h_out + oy) * w_out + ox) * c_out + ch;
+          }
+        }
+        if (stu[u] & 1) {
+          z0[u] = *reinterpret_cast<const float4*>(z + o[u]);
+          z1[u] = *reinterpret_cast<const float4*>(z + o[u] + 4);
+          yo[u] = *reinterpret_cast<const uint4*>(yb + o[u]);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (!stu[u]) continue;
+        if (!(stu[u] & 1)) {
+          *reinterpret_cast<float4*>(r32 + o[u]) = float4{0.f, 0.f, 0.f, 0.f};
+          *reinterpret_cast<float4*>(r32 + o[u] + 4) = float4{0.f, 0.f, 0.f, 0.f};
+          *reinterpret_cast<uint4*>(rb + o[u]) = uint4{0u, 0u, 0u, 0u};
+          continue;
+        }
+        float a[8] = {z0[u].x, z0[u].y, z0[u].z, z0[u].w, z1[u].x, z1[u].y, z1[u].z, z1[u].w};
+        if (act == 2)
+          for (int v = 0; v < 8; ++v) a[v] = relu_f32(a[v]);
+        const uint32_t wo[4] = {yo[u].x, yo[u].y, yo[u].z, yo[u].w};
+        float r[8];
+        uint32_t wn[4], wr[4];
+        for (int v = 0; v < 4; ++v) {
+          const uint32_t n0 = f32_to_bf16(a[2 * v]), n1 = f32_to_bf16(a[2 * v + 1]);
+          r[2 * v] = __fsub_rn(bf16_to_f32(n0), bf16_to_f32(wo[v] & 0xffffu));
+          r[2 * v + 1] = __fsub_rn(bf16_to_f32(n1), bf16_to_f32(wo[v] >> 16));
+          wn[v] = n0 | (n1 << 16);
+          wr[v] = f32_to_bf16(r[2 * v]) | (f32_to_bf16(r[2 * v + 1]) << 16);
+        }
+        *reinterpret_cast<uint4*>(yb + o[u]) = uint4{wn[0], wn[1], wn[2], wn[3]};
+        *reinterpret_cast<uint4*>(rb + o[u]) = uint4{wr[0], wr[1], wr[2], wr[3]};
+        *reinterpret_cast<float4*>(r32 + o[u]) = float4{r[0], r[1], r[2], r[3]};
+        *reinterpret_cast<float4*>(r32 + o[u] + 4) = float4{r[4], r[5], r[6], r[7]};
+      }
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < nblk; i += kEmitThreads) prev_mask[b0 + i] = state[i] & 1;
+    return;
+  }
   for (int e = threadIdx.x; e < total; e += kEmitThreads) {
     const int bl = e / (bsz * cg), rem0 = e - bl * bsz * cg;
     const uint8_t st = state[bl];

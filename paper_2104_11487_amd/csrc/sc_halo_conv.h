@@ -1,8 +1,7 @@
 // Block-halo MFMA convolution of one tile of output sites (Eq. 3 over the
-// active sites, as the im2col product of Sec. 4.2 restricted to one block),
-// shared by the split pipeline's convolution kernel (which walks the work
-// list) and the gate-conv kernel (which convolves the block its gate has just
-// found active). bf16 operands, fp32 accumulation, C_in % 32 == 0.
+// active sites, as the im2col product of Sec. 4.2 restricted to one block):
+// the per-tile work of the split pipeline's convolution kernel, which walks
+// the work list. bf16 operands, fp32 accumulation, C_in % 32 == 0.
 //
 // A tile is `tr` output rows x b columns of one block. Per tile:
 //   1. the accumulators start from z_{t-1} of the tile's sites (0 on a
