@@ -26,7 +26,7 @@ constexpr int kEmitUnroll = 4;  // 8-channel groups a thread has in flight (bf16
 __global__ void __launch_bounds__(kEmitThreads)
 emit_kernel(const uint8_t* block_mask, uint8_t* prev_mask, int nb, int bpw, const float* z, void* y,
             float* r32, uint16_t* rb, int hb, int wb, int block, int h_out, int w_out, int c_out, int act,
-            int dtype) {
+            int dtype, int clear_only) {
   __shared__ uint8_t state[kEmitSites];  // bit 0: updated now, bit 1: updated by the previous step
   const int b0 = blockIdx.x * bpw, nblk = min(bpw, nb - b0);
   int any = 0;
@@ -65,7 +65,8 @@ emit_kernel(const uint8_t* block_mask, uint8_t* prev_mask, int nb, int bpw, cons
           const int bi = rem / wb, bj = rem - bi * wb;
           const int oy = bi * block + site / block, ox = bj * block + site % block;
           if (oy < h_out && ox < w_out) {  // ceil-mode edge block
-            stu[u] = state[bl];
+            // clear_only: the convolution already emitted at the updated blocks
+            stu[u] = (clear_only && (state[bl] & 1)) ? 0 : state[bl];
             o[u] = ((size_t)(img * h_out + oy) * w_out + ox) * c_out + ch;
           }
         }
@@ -109,7 +110,7 @@ emit_kernel(const uint8_t* block_mask, uint8_t* prev_mask, int nb, int bpw, cons
   }
   for (int e = threadIdx.x; e < total; e += kEmitThreads) {
     const int bl = e / (bsz * cg), rem0 = e - bl * bsz * cg;
-    const uint8_t st = state[bl];
+    const uint8_t st = (clear_only && (state[bl] & 1)) ? 0 : state[bl];
     if (!st) continue;
     const int site = rem0 / cg, ch = (rem0 - site * cg) * vec;
     const int blk = b0 + bl;
@@ -185,12 +186,12 @@ emit_kernel(const uint8_t* block_mask, uint8_t* prev_mask, int nb, int bpw, cons
 
 hipError_t launch_emit(const uint8_t* block_mask, uint8_t* prev_mask, int nb, const float* z, void* y,
                        float* r32, uint16_t* rb, int n, int hb, int wb, int block, int h_out, int w_out,
-                       int c_out, int act, int dtype, hipStream_t st) {
+                       int c_out, int act, int dtype, int clear_only, hipStream_t st) {
   (void)n;
   const int bpw = max(1, kEmitSites / (block * block));
   const int grid = (nb + bpw - 1) / bpw;
   hipLaunchKernelGGL(emit_kernel, dim3(grid), dim3(kEmitThreads), 0, st, block_mask, prev_mask, nb, bpw, z, y,
-                     r32, rb, hb, wb, block, h_out, w_out, c_out, act, dtype);
+                     r32, rb, hb, wb, block, h_out, w_out, c_out, act, dtype, clear_only);
   return hipGetLastError();
 }
 

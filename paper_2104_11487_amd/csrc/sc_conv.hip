@@ -255,9 +255,11 @@ __global__ void __launch_bounds__(kConvThreads) conv_bf16_kernel(ConvParams p) {
 // everything in flight. Without PZ a tile's z_{t-1} is loaded with its halo.
 // OCC: waves per SIMD the register budget aims for.
 
+// EMIT: the epilogue also writes y_new and the successor's residual; y_old is
+// loaded with z_{t-1}.
 template <int WAVES_M, int WAVES_N, int WM, int WN, int KR = 0, bool PZ = true, int OCC = 2, int KU = 12,
-          int ADB = 2>
-__global__ void __launch_bounds__(64 * WAVES_M * WAVES_N) __attribute__((amdgpu_waves_per_eu(OCC)))
+          int ADB = 2, bool EMIT = false>
+__global__ void __launch_bounds__(64 * WAVES_M * WAVES_N) __attribute__((amdgpu_waves_per_eu(EMIT && OCC > 2 ? 2 : OCC)))
 conv_halo_kernel(ConvParams p, HaloParams hp) {
   extern __shared__ __attribute__((aligned(16))) uint8_t halo[];
   typedef HaloConv<WAVES_M, WAVES_N, WM, WN, KR, KU, ADB> HC;
@@ -286,16 +288,23 @@ conv_halo_kernel(ConvParams p, HaloParams hp) {
   if (tw.t >= tw.end) return;
   HaloTile T = decode(tw.t);
   typename HC::Acc zn;
+  typename HC::Yv yn;  // emission: y_old of the next tile (PZ)
   if constexpr (PZ) H.load_z(zn, T, false);
+  if constexpr (PZ && EMIT) H.load_y(yn, T, false);
   for (; tw.t < tw.end; tw.t += tw.step) {
     typename HC::Acc acc;
+    typename HC::Yv yo;
     if constexpr (!PZ) H.load_z(acc, T, false);  // in flight with the halo loads
+    if constexpr (!PZ && EMIT) H.load_y(yo, T, false);
     H.load_halo(T);
     if constexpr (PZ) {
 #pragma unroll
       for (int i = 0; i < WM; ++i)
 #pragma unroll
-        for (int jn = 0; jn < WN; ++jn) acc[i][jn] = zn[i][jn];
+        for (int jn = 0; jn < WN; ++jn) {
+          acc[i][jn] = zn[i][jn];
+          if constexpr (EMIT) yo[i][jn] = yn[i][jn];
+        }
     }
     __syncthreads();
     H.product(acc);
@@ -304,7 +313,9 @@ conv_halo_kernel(ConvParams p, HaloParams hp) {
     const bool more = tw.t + tw.step < tw.end;
     const HaloTile Tn = more ? decode(tw.t + tw.step) : T;
     if constexpr (PZ) H.load_z(zn, Tn, !more);
-    H.store(T, acc);
+    if constexpr (PZ && EMIT) H.load_y(yn, Tn, !more);
+    if constexpr (EMIT) H.store_emit(T, acc, yo);
+    else H.store(T, acc);
     T = Tn;
   }
 }
@@ -732,8 +743,12 @@ hipError_t launch_conv_f32(const ConvParams& p, int grid, hipStream_t st) {
 
 template <int WAVES_M, int WAVES_N, int WM, int WN, int KR, bool PZ, int OCC, int KU, int ADB>
 hipError_t launch_halo_t(const ConvParams& p, const HaloParams& hp, int grid, hipStream_t st) {
-  hipLaunchKernelGGL((conv_halo_kernel<WAVES_M, WAVES_N, WM, WN, KR, PZ, OCC, KU, ADB>), dim3(grid),
-                     dim3(64 * WAVES_M * WAVES_N), hp.lds_bytes, st, p, hp);
+  if (hp.emit)
+    hipLaunchKernelGGL((conv_halo_kernel<WAVES_M, WAVES_N, WM, WN, KR, PZ, OCC, KU, ADB, true>), dim3(grid),
+                       dim3(64 * WAVES_M * WAVES_N), hp.lds_bytes, st, p, hp);
+  else
+    hipLaunchKernelGGL((conv_halo_kernel<WAVES_M, WAVES_N, WM, WN, KR, PZ, OCC, KU, ADB>), dim3(grid),
+                       dim3(64 * WAVES_M * WAVES_N), hp.lds_bytes, st, p, hp);
   return hipGetLastError();
 }
 
@@ -747,7 +762,8 @@ hipError_t launch_conv(const ConvParams& p, int dtype, bool fast, int grid, hipS
 namespace {
 template <int WAVES_M, int WAVES_N, int WM, int WN, int KR, bool PZ, int OCC, int KU, int ADB>
 int halo_occ_t(const HaloParams& hp) {
-  auto fn = conv_halo_kernel<WAVES_M, WAVES_N, WM, WN, KR, PZ, OCC, KU, ADB>;
+  auto fn = hp.emit ? conv_halo_kernel<WAVES_M, WAVES_N, WM, WN, KR, PZ, OCC, KU, ADB, true>
+                    : conv_halo_kernel<WAVES_M, WAVES_N, WM, WN, KR, PZ, OCC, KU, ADB>;
   if (hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
                           hp.lds_bytes) != hipSuccess)
     return 0;

@@ -264,6 +264,55 @@ struct HaloConv {
       }
   }
 
+  // the activation output y_old = dtype(act(z_{t-1})) of the tile's sites in
+  // the same layout, 4 bf16 per piece (residual emission); zeros outside
+  typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
+  typedef u32x2v Yv[WM][WN];
+  __device__ __amdgpu_buffer_rsrc_t yres(const HaloTile& T) const {
+    return frame_rsrc(static_cast<uint16_t*>(p.y) + (size_t)T.n * zimg, (uint32_t)(zimg * 2));
+  }
+  __device__ void load_y(Yv& dst, const HaloTile& T, bool none) const {
+    const auto yrs = yres(T);
+#pragma unroll
+    for (int i = 0; i < WM; ++i)
+#pragma unroll
+      for (int jn = 0; jn < WN; ++jn) {
+        const uint32_t o = zoff(T, i, jn);
+        dst[i][jn] = __builtin_bit_cast(
+            u32x2v, __builtin_amdgcn_raw_buffer_load_b64(yrs, none || o == kOutOfRange ? kOutOfRange : o / 2, 0, 0));
+      }
+  }
+
+  // z, y_new = dtype(act(z)) and the successor's residual r = fl32(y_new -
+  // y_old) in fp32 and rounded to bf16, at the tile's sites
+  __device__ void store_emit(const HaloTile& T, const Acc& acc, const Yv& yo) const {
+    const auto zrs = zres(T);
+    const auto yrs = yres(T);
+    const auto rrs = frame_rsrc(p.r32 + (size_t)T.n * zimg, (uint32_t)(zimg * 4));
+    const auto brs = frame_rsrc(p.rb + (size_t)T.n * zimg, (uint32_t)(zimg * 2));
+#pragma unroll
+    for (int i = 0; i < WM; ++i)
+#pragma unroll
+      for (int jn = 0; jn < WN; ++jn) {
+        const uint32_t o = zoff(T, i, jn);
+        const uint32_t oh = o == kOutOfRange ? kOutOfRange : o / 2;
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc[i][jn]), zrs, o, 0, 0);
+        uint32_t yn[4];
+        floatx4 r;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          yn[v] = f32_to_bf16(activate(acc[i][jn][v], p.act));
+          const uint32_t ob = (v < 2 ? yo[i][jn].x : yo[i][jn].y) >> (16 * (v & 1));
+          r[v] = __fsub_rn(bf16_to_f32(yn[v]), bf16_to_f32(ob & 0xffffu));
+        }
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2v{yn[0] | (yn[1] << 16), yn[2] | (yn[3] << 16)}, yrs, oh, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, r), rrs, o, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b64(
+            u32x2v{f32_to_bf16(r[0]) | (f32_to_bf16(r[1]) << 16), f32_to_bf16(r[2]) | (f32_to_bf16(r[3]) << 16)}, brs,
+            oh, 0, 0);
+      }
+  }
+
   // z (and the activation output) of the tile's sites
   __device__ void store(const HaloTile& T, const Acc& acc) const {
     const auto zrs = zres(T);

@@ -81,6 +81,10 @@ struct ConvParams {
   int sy, sx;                   // translation of the content since x_{t-1} (input pixels; 0 = none)
   uint32_t* zero_ctr;           // work-list counters (kSegs, kSegStride apart) to clear for the next step, or NULL
   int seg_tiles, seg_cap;       // segmented work list: gate tiles and entries per tile; 0: plain list
+  // residual emission in the block-halo kernel's epilogue (HaloParams::emit):
+  // r = fl32(y_new - y_old) and its bf16 rounding at every site it updates
+  float* r32;
+  uint16_t* rb;
 };
 
 // Work list of a convolution: a plain list with its count at
@@ -160,6 +164,7 @@ struct HaloParams {
   int pstride;           // LDS bytes per halo pixel: 2*c_in + 16
   int lds_bytes;         // hh * hw * pstride
   int threads;           // workgroup size
+  int emit;              // the epilogue also writes the successor's residual (bf16, C_out % 8 == 0)
 };
 
 // Fused single-pass step for dense bf16 layers (see sc_fused.hip). `g` carries
@@ -252,7 +257,7 @@ int depthwise_halo_occupancy(const HaloParams& hp, int k, int c);  // resident w
 // rounding for bf16 layers); at blocks updated by the previous step only, r = 0.
 hipError_t launch_emit(const uint8_t* block_mask, uint8_t* prev_mask, int nb, const float* z, void* y,
                        float* r32, uint16_t* rb, int n, int hb, int wb, int block, int h_out, int w_out,
-                       int c_out, int act, int dtype, hipStream_t st);
+                       int c_out, int act, int dtype, int clear_only, hipStream_t st);
 
 // Translation-compensated steps (Sec. 3.3): the translated state, and the
 // active list split into translated-recurrence blocks and exposed blocks.

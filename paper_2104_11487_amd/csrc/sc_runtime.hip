@@ -301,6 +301,9 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
       H.config = 20 + ni;
     }
     H.threads = 64 * (G.ntn == 1 ? 1 : (G.ntn == 2 ? 2 : 4));
+    // emitting layers: the epilogue writes the successor's residual (16-byte
+    // r32 pieces of 4 channels, whole 8-channel groups for the clears)
+    H.emit = (d->flags & SKIPCONV_FLAG_EMIT_RESIDUAL) && d->c_out % 8 == 0 ? 1 : 0;
     H.tiles_per_block = b / H.tr;
     H.hh = (H.tr - 1) * s + k;
     H.hw = (b - 1) * s + k;
@@ -674,11 +677,18 @@ hipError_t weight_norm(skipconv_layer* h, const void* weights, hipStream_t st) {
   return hipSuccess;
 }
 
+// The split pipeline's convolution writes the emitted residual itself (the
+// block-halo kernel's emitting build) instead of the emission kernel.
+bool conv_emits(const Geometry& g) { return g.halo && !g.depthwise && g.hp.emit; }
+
+// After a split-pipeline step of an emitting layer: the residual at the blocks
+// it updated (unless its block-halo convolution emitted them in its
+// epilogue) and zeros at the blocks only the previous step updated.
 hipError_t launch_emit(skipconv_layer* h, hipStream_t st) {
   const Geometry& g = h->g;
   return sc::launch_emit(h->bmask(), h->prev_mask(), g.nb, h->z(), h->y(), h->r32(), h->rb(), h->d.n, g.hb,
                          g.wb, h->d.block, g.h_out, g.w_out, h->d.c_out, h->d.act_out,
-                         h->d.dtype == SKIPCONV_BF16 ? 1 : 0, st);
+                         h->d.dtype == SKIPCONV_BF16 ? 1 : 0, conv_emits(g) ? 1 : 0, st);
 }
 
 int hip_fail(skipconv_t h, hipError_t e, const char* what) {
@@ -734,7 +744,7 @@ sc::ConvParams conv_geometry(const skipconv_desc& d, const Geometry& g, bool ref
   cp.ksteps = g.ksteps; cp.ntiles_n = g.ntn;
   cp.reference = ref ? 1 : 0;
   cp.no_prev = ref ? 1 : 0;
-  cp.act = (d.flags & SKIPCONV_FLAG_EMIT_RESIDUAL) ? 0 : d.act_out;
+  cp.act = ((d.flags & SKIPCONV_FLAG_EMIT_RESIDUAL) && !conv_emits(g)) ? 0 : d.act_out;
   return cp;
 }
 
@@ -1043,7 +1053,9 @@ int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t
   cp.ksteps = g.ksteps; cp.ntiles_n = g.ntn;
   cp.reference = ref ? 1 : 0;
   cp.no_prev = ref ? 1 : 0;
-  cp.act = h->emits() ? 0 : d.act_out;
+  cp.act = (h->emits() && !conv_emits(g)) ? 0 : d.act_out;
+  cp.r32 = h->r32();
+  cp.rb = h->rb();
 
   const bool timing = h->timing_done < h->timing_frames && h->timing_seen % h->timing_every == 0;
   if (h->timing_frames) ++h->timing_seen;
@@ -1254,7 +1266,9 @@ int skipconv_step_chained(skipconv_t h, skipconv_t up, void* stream, const float
   cp.ksteps = g.ksteps; cp.ntiles_n = g.ntn;
   cp.reference = 0;
   cp.no_prev = 1;
-  cp.act = h->emits() ? 0 : d.act_out;
+  cp.act = (h->emits() && !conv_emits(g)) ? 0 : d.act_out;
+  cp.r32 = h->r32();
+  cp.rb = h->rb();
   e = launch_split_conv(g, d, cp, conv_grid(h), st);
   if (e != hipSuccess) return hip_fail(h, e, "chained conv launch");
   if (h->emits()) {
