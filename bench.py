@@ -441,6 +441,9 @@ def summarize_pmc(fetch_db: str, write_db: str, out_json: str, *, workload: str,
     """
     import sqlite3
 
+    if copy_mib <= 0:
+        raise SystemExit("--summarize-pmc needs --copy-probe MIB: the size of the copy the counted run made")
+
     def rows(db, counter):
         con = sqlite3.connect(db)
         out = con.execute("select kernel_name, value from counters_collection where counter_name = ?",
