@@ -979,6 +979,15 @@ int skipconv_create(const skipconv_desc* d, const void* weights, void* workspace
   if (h->g.fused && (h->g.f_grid * ((h->g.f_rb || h->g.f_dw) ? h->g.f_nsplit : 1) > 4 * h->num_cu ||
                      sc::prepare_fused(fused_params(h, nullptr, true)) < 1))
     h->g.fused = false;
+  // 16 x 16 tiles with the weights staged in LDS restage the whole weight
+  // tensor per tile: they beat the split pipeline only for narrow layers on
+  // few tiles (measured, 3 x 3 and 1 x 1, n = 1: 32 -> 32 up to ~3 tiles per
+  // CU, 64 -> 64 up to one; 128 input or output channels lose at every size,
+  // e.g. one 512 x 512 128 -> 128 frame 147 us against 78.5 us split).
+  if (h->g.fused && !h->g.f_rb && !h->g.f_dw && !h->g.f_sc && h->g.f_mw == 4) {
+    const long cap = (long)(d->c_in * d->c_out <= 32 * 32 ? 3 : 1) * h->num_cu;
+    if (d->c_in > 64 || d->c_out > 64 || h->g.f_grid > cap) h->g.fused = false;
+  }
   h->conv_occ = conv_setup(h->g, d, h->device);
   if (workspace) {
     h->ws = static_cast<char*>(workspace);

@@ -674,6 +674,16 @@ def test_pipeline_selection():
     # channels split over four workgroups per tile, each a register build
     assert S.SkipConv(w128, n=1, h=32, w=32, block=8).fused_variant == 3
     assert S.SkipConv(w, n=1, h=64, w=64, block=16).fused_variant == 1
+    # 16 x 16 tiles stage the weights in LDS per tile: only narrow layers on
+    # few tiles keep the single-pass kernel (64 channels: one tile per CU,
+    # 32 -> 32: three), 128 input or output channels take the split pipeline
+    assert S.SkipConv(w, n=1, h=240, w=240, block=16).fused_variant == 1
+    assert S.SkipConv(w, n=1, h=384, w=384, block=16).fused_variant == 0
+    w32 = to_device(weight_storage(syn.he_weights(32, 32, 3, seed=1), "bf16"), "bf16")
+    assert S.SkipConv(w32, n=1, h=384, w=384, block=16).fused_variant == 1
+    assert S.SkipConv(w32, n=1, h=512, w=512, block=16).fused_variant == 0
+    assert S.SkipConv(w128, n=1, h=64, w=64, block=16).fused_variant == 0
+    assert S.SkipConv(w128, n=1, h=512, w=512, block=16).fused_variant == 0
     # split gate tiles: 16 x 16 sites on large frames, 8 x 8 on small ones, 32 x 32
     # on request; 32, 64 and 128 channels add their chunk sums in lane groups,
     # other channel counts stage them in LDS
@@ -1099,7 +1109,8 @@ FUSED_SHAPES = [
     (1, 30, 26, 128, 128, 3, 1, 8, 3),
     (2, 27, 21, 128, 128, 3, 1, 4, 3),
     (1, 40, 36, 64, 64, 3, 1, 16, 1),
-    (1, 40, 36, 128, 128, 3, 1, 16, 1),
+    (1, 40, 36, 32, 64, 3, 1, 16, 1),
+    (1, 40, 36, 128, 128, 3, 1, 16, 0),  # LDS-staged 128-channel weights: split pipeline
 ]
 
 
