@@ -45,7 +45,6 @@ namespace sc {
 
 namespace {
 
-constexpr int kGateThreads = 256;
 // Per-chunk partial sums of the tile's halo: one item = one chunk of kChunk
 // channels of one halo pixel (consecutive items = consecutive chunks, so the
 // loads of a wave are contiguous). kItems items per thread have their loads in
@@ -306,14 +305,22 @@ __device__ void halo_pixels(const GateParams& p, int n, int iy0, int ix0, int hh
 // the items of halo_lane_sums (one 8-channel chunk of one halo pixel per lane,
 // consecutive lanes holding consecutive chunks of a pixel, kItems items with
 // their loads in flight together), each forming the K2 per-tap chunk terms
-// sum_j phi[tap][c0 + j] * r[c0 + j] in ascending order from +0; the pixel's
-// lane group then adds each tap's chunk terms in ascending chunk order (DPP
-// row shifts), the canonical order, and its first lane writes a[q, tap].
-// Owned pixels are copied to the spare x_{t-1} slot on the way.
+// sum_j phi[tap][c0 + j] * r[c0 + j] in ascending order from +0. The terms of
+// up to kLearnTapGroup taps go to the wave's exchange area in LDS, [pixel]
+// [tap][chunk]; lane l of a pixel's group then reads the NC terms of tap
+// l (l + NC, ...) and adds them in ascending chunk order from +0, the
+// canonical order, and writes a[q, tap]. Every lane reduces a different tap,
+// where a lane-shift chain per tap would run in all NC lanes for one result.
+// For kernels of up to 3 x 3 a lane holds its phi chunk of every tap in
+// registers, so the tap loop's only LDS traffic is the exchange (reading phi
+// from LDS per tap as well took the blob-sized gate from 0.29 to 0.75 ms).
+// Owned pixels are copied to the spare x_{t-1} slot on the way. phi: staged
+// in LDS, or in memory (each call site inlines its own copy).
 template <typename T, int NC, int KL>
-__device__ void learned_lane_sums(const GateParams& p, int n, int iy0, int ix0, int hh, int hw, int own_y0,
-                                  int own_y1, int own_x0, int own_x1, float* a2, const float* phi) {
+__device__ __forceinline__ void learned_lane_sums(const GateParams& p, int n, int iy0, int ix0, int hh, int hw, int own_y0,
+                                  int own_y1, int own_x0, int own_x1, float* a2, const float* phi, float* xch) {
   constexpr int K2 = KL * KL;
+  constexpr int TG = K2 < kLearnTapGroup ? K2 : kLearnTapGroup;
   constexpr int kWords = sizeof(T) == 2 ? 1 : 2;  // 16-byte words per chunk and frame
   constexpr int kItems = 4 / kWords;
   constexpr int kLg = NC == 2 ? 1 : (NC == 4 ? 2 : (NC == 8 ? 3 : 4));
@@ -329,6 +336,21 @@ __device__ void learned_lane_sums(const GateParams& p, int n, int iy0, int ix0, 
   // a thread's chunk is the same for every item (NC divides the item stride)
   const int ch = threadIdx.x & (NC - 1);
   const float* ph = phi + ch * kChunk;
+  // this lane's pixel group in the wave's exchange area: TG taps x NC chunks
+  float* xg = xch + wave0 * TG + ((threadIdx.x & 63) >> kLg) * (TG * NC);
+  // kernels of up to 3 x 3: this lane's phi chunk of every tap in registers
+  // (loaded once), so that the tap loop reads LDS only for the exchange
+  constexpr bool kRegPhi = K2 <= 9;
+  float fr[kRegPhi ? K2 : 1][kChunk];
+  if constexpr (kRegPhi) {
+#pragma unroll
+    for (int t = 0; t < K2; ++t) {
+      const float4 f0 = *reinterpret_cast<const float4*>(ph + t * p.c);
+      const float4 f1 = *reinterpret_cast<const float4*>(ph + t * p.c + 4);
+      fr[t][0] = f0.x; fr[t][1] = f0.y; fr[t][2] = f0.z; fr[t][3] = f0.w;
+      fr[t][4] = f1.x; fr[t][5] = f1.y; fr[t][6] = f1.z; fr[t][7] = f1.w;
+    }
+  }
   for (int base = 0; base < total; base += kGateThreads * kItems) {
     u32x4 vt[kItems][kWords], vp[kItems][kWords];
     uint32_t koff[kItems];
@@ -370,16 +392,60 @@ __device__ void learned_lane_sums(const GateParams& p, int n, int iy0, int ix0, 
       }
       const int idx = base + u * kGateThreads + threadIdx.x;
       const int q = idx >> kLg;
+      const bool pix_ok = idx < total;  // (total is a multiple of NC: the whole group agrees)
 #pragma unroll
-      for (int t = 0; t < K2; ++t) {
-        const float4 f0 = *reinterpret_cast<const float4*>(ph + t * p.c);
-        const float4 f1 = *reinterpret_cast<const float4*>(ph + t * p.c + 4);
-        const float f[kChunk] = {f0.x, f0.y, f0.z, f0.w, f1.x, f1.y, f1.z, f1.w};
-        float part = 0.0f;
+      for (int t0 = 0; t0 < K2; t0 += TG) {
+        const int tg = K2 - t0 < TG ? K2 - t0 : TG;
 #pragma unroll
-        for (int j = 0; j < kChunk; ++j) part = add_rn(part, mul_rn(f[j], r[j]));
-        const float acc = group_sum<NC>(part);
-        if (idx < total && ch == 0) a2[q * K2 + t] = acc;
+        for (int tl = 0; tl < TG; ++tl) {
+          if (tl < tg) {
+            float f[kChunk];
+            if constexpr (kRegPhi) {
+#pragma unroll
+              for (int j = 0; j < kChunk; ++j) f[j] = fr[kRegPhi ? t0 + tl : 0][j];
+            } else {
+              const float4 f0 = *reinterpret_cast<const float4*>(ph + (t0 + tl) * p.c);
+              const float4 f1 = *reinterpret_cast<const float4*>(ph + (t0 + tl) * p.c + 4);
+              f[0] = f0.x; f[1] = f0.y; f[2] = f0.z; f[3] = f0.w;
+              f[4] = f1.x; f[5] = f1.y; f[6] = f1.z; f[7] = f1.w;
+            }
+            float part = 0.0f;
+#pragma unroll
+            for (int j = 0; j < kChunk; ++j) part = add_rn(part, mul_rn(f[j], r[j]));
+            xg[tl * NC + ch] = part;
+          }
+        }
+        // the group's terms are written by lanes of this wave: LDS serves a
+        // wave's accesses in order, so only the compiler must keep them so
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront", "local");
+#pragma unroll
+        for (int rr = 0; rr < TG; rr += NC) {
+          const int tl = rr + ch;
+          if (tl < tg) {
+            float v[NC];
+            if constexpr (NC % 4 == 0) {
+#pragma unroll
+              for (int i4 = 0; i4 < NC; i4 += 4) {
+                const float4 w4 = *reinterpret_cast<const float4*>(xg + tl * NC + i4);
+                v[i4] = w4.x;
+                v[i4 + 1] = w4.y;
+                v[i4 + 2] = w4.z;
+                v[i4 + 3] = w4.w;
+              }
+            } else {
+              const float2 w2 = *reinterpret_cast<const float2*>(xg + tl * NC);
+              v[0] = w2.x;
+              v[1] = w2.y;
+            }
+            float acc = add_rn(0.0f, v[0]);
+#pragma unroll
+            for (int i = 1; i < NC; ++i) acc = add_rn(acc, v[i]);
+            if (pix_ok) a2[q * K2 + t0 + tl] = acc;
+          }
+        }
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront", "local");
       }
     }
 #pragma unroll
@@ -551,9 +617,14 @@ __device__ __forceinline__ const uint32_t* gate_tile(const GateParams& p, float*
       __syncthreads();
       phi = staged;
     }
-    if constexpr (NC > 1)
-      learned_lane_sums<T, NC, KL>(p, n, iy0, ix0, hh, hw, own_y0, own_y1, own_x0, own_x1, lds, phi);
-    else
+    if constexpr (NC > 1) {
+      if (p.phi_off >= 0)
+        learned_lane_sums<T, NC, KL>(p, n, iy0, ix0, hh, hw, own_y0, own_y1, own_x0, own_x1, lds,
+                                     lds + p.phi_off, lds + p.tr_off);
+      else
+        learned_lane_sums<T, NC, KL>(p, n, iy0, ix0, hh, hw, own_y0, own_y1, own_x0, own_x1, lds, p.phi,
+                                     lds + p.tr_off);
+    } else
       learned_halo<T, VEC, KL>(p, n, iy0, ix0, hh, hw, own_y0, own_y1, own_x0, own_x1, lds, phi);
   }
 

@@ -49,6 +49,7 @@ struct GateParams {
   const float* phi;
   float gate_bias;
   int phi_off;                  // LDS float offset of the staged phi, or -1: read phi from memory
+  int tr_off;                   // learned gate over lane groups: LDS float offset of the per-wave tap-term exchange
   // chained input (x_t is the upstream layer's residual): tiles whose input
   // region holds no upstream active block skip their loads; NULL = no skip
   const uint8_t* up_mask;
@@ -92,6 +93,10 @@ struct ConvParams {
 // blocks of gate tiles first(x) .. first(x + 1) - 1 (the XCD-contiguous tile
 // ranges of the gate launch) from entry first(x) * seg_cap on, its count at
 // counters[x * kSegStride]. Entries are the linear block indices.
+constexpr int kGateThreads = 256;  // threads of a gate workgroup
+// learned gate over lane groups: taps whose chunk terms are exchanged at once
+constexpr int kLearnTapGroup = 9;
+
 struct WorkList {
   uint32_t total;
   uint32_t pre[kSegs + 1];  // segmented: entries before segment x

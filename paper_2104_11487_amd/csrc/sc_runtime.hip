@@ -69,6 +69,7 @@ struct Geometry {
   int learned;          // learned gate: its kernel size (the layer's k), else 0
   bool phi_in_lds;      // learned gate: phi staged in LDS (else read through the caches)
   int phi_off;          // learned gate: LDS float offset of the staged phi
+  int tr_off;           // learned gate over lane groups: LDS float offset of the tap-term exchange
   size_t wpack_bytes, x_bytes, z_bytes;
   int conv_max_tiles;
 };
@@ -170,8 +171,9 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
   auto gate_lds_for = [&](int ts) {
     const long eh = (long)(std::min(ts, G.h_out) - 1) * s + k;  // largest halo actually used
     const long ew = (long)(std::min(ts, G.w_out) - 1) * s + k;
-    if (G.learned)  // per-pixel, per-tap gate terms (+ the staged phi)
-      return ((eh * ew * k * k + 3) / 4 * 4 + (G.phi_in_lds ? phi_floats : 0)) * 4;
+    if (G.learned)  // per-pixel, per-tap gate terms (+ the staged phi, + the lane groups' tap-term exchange)
+      return ((eh * ew * k * k + 3) / 4 * 4 + (G.phi_in_lds ? (phi_floats + 3) / 4 * 4 : 0) +
+              (learned_lanes ? (long)sc::kGateThreads * std::min(k * k, sc::kLearnTapGroup) : 0)) * 4;
     const long halo = (eh * ew + 3) / 4 * 4;
     return (halo + (lane_sum ? 0 : eh * ew * G.stage_stride)) * 4;
   };
@@ -208,6 +210,7 @@ int derive(const skipconv_desc* d, Geometry* g, char* err) {
   G.hw_max = (std::min(G.ts, G.w_out) - 1) * s + k;
   G.halo_floats = (G.hh_max * G.hw_max + 3) / 4 * 4;
   G.phi_off = (G.hh_max * G.hw_max * k * k + 3) / 4 * 4;
+  G.tr_off = G.phi_off + (G.phi_in_lds ? (int)((phi_floats + 3) / 4 * 4) : 0);
   G.rows_per_batch = G.hh_max;
   G.gate_lds = gate_lds_for(G.ts);
   if (G.gate_lds > kLdsLimit)
@@ -717,6 +720,7 @@ sc::GateParams gate_geometry(const skipconv_desc& d, const Geometry& g, bool ref
   gp.wnorm = 1.0;
   gp.learned = g.learned;
   gp.phi_off = g.phi_in_lds ? g.phi_off : -1;
+  gp.tr_off = g.tr_off;
   gp.split_blocks = g.split_blocks;
   return gp;
 }
