@@ -18,32 +18,49 @@ namespace {
 
 constexpr int kTrThreads = 256;
 
+// One thread per VEC consecutive channels of one site (VEC = 4: 16-byte
+// loads and stores), one grid row per output row (blockIdx.y = image row):
+// 32-bit index arithmetic, one division per thread.
+template <int VEC>
 __global__ void __launch_bounds__(kTrThreads)
-translate_state_kernel(const float* z_src, float* z_dst, void* y, int n, int h_out, int w_out, int c_out,
+translate_state_kernel(const float* z_src, float* z_dst, void* y, int row0, int h_out, int w_out, int c_out,
                        int dyo, int dxo, int act, int dtype) {
-  const int vec = (c_out & 3) == 0 ? 4 : 1;
-  const int cg = c_out / vec;
-  const long total = (long)n * h_out * w_out * cg;
-  for (long e = (long)blockIdx.x * kTrThreads + threadIdx.x; e < total; e += (long)gridDim.x * kTrThreads) {
-    const long site = e / cg;
-    const int ch = (int)(e - site * cg) * vec;
-    const int img = (int)(site / ((long)h_out * w_out));
-    const int rem = (int)(site - (long)img * h_out * w_out);
-    const int oy = rem / w_out, ox = rem - oy * w_out;
-    const int sy = oy - dyo, sx = ox - dxo;
-    const bool in = sy >= 0 && sy < h_out && sx >= 0 && sx < w_out;
-    const size_t o = (size_t)site * c_out + ch;
-    const size_t so = (((size_t)img * h_out + sy) * w_out + sx) * c_out + ch;
-    for (int v = 0; v < vec; ++v) {
-      const float zv = in ? z_src[so + v] : 0.0f;
-      z_dst[o + v] = zv;
-      if (act) {
-        const float a = act == 2 ? relu_f32(zv) : zv;
-        if (dtype == 1)
-          static_cast<uint16_t*>(y)[o + v] = (uint16_t)f32_to_bf16(a);
-        else
-          static_cast<float*>(y)[o + v] = a;
+  const int cg = c_out / VEC;
+  const int e = blockIdx.x * kTrThreads + threadIdx.x;
+  if (e >= w_out * cg) return;
+  const int row = row0 + (int)blockIdx.y;  // image * h_out + oy
+  const int img = row / h_out, oy = row - img * h_out;
+  const int ox = e / cg, ch = (e - ox * cg) * VEC;
+  const int sy = oy - dyo, sx = ox - dxo;
+  const bool in = sy >= 0 && sy < h_out && sx >= 0 && sx < w_out;
+  const size_t o = ((size_t)row * w_out + ox) * c_out + ch;
+  const size_t so = (((size_t)img * h_out + sy) * w_out + sx) * c_out + ch;
+  float zv[VEC];
+  if constexpr (VEC == 4) {
+    const float4 v = in ? *reinterpret_cast<const float4*>(z_src + so) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    zv[0] = v.x; zv[1] = v.y; zv[2] = v.z; zv[3] = v.w;
+    *reinterpret_cast<float4*>(z_dst + o) = v;
+  } else {
+    zv[0] = in ? z_src[so] : 0.0f;
+    z_dst[o] = zv[0];
+  }
+  if (act) {
+    float a[VEC];
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) a[v] = act == 2 ? relu_f32(zv[v]) : zv[v];
+    if (dtype == 1) {
+      uint16_t* yb = static_cast<uint16_t*>(y) + o;
+      if constexpr (VEC == 4) {
+        const uint2 pk = make_uint2((uint32_t)f32_to_bf16(a[0]) | ((uint32_t)f32_to_bf16(a[1]) << 16),
+                                    (uint32_t)f32_to_bf16(a[2]) | ((uint32_t)f32_to_bf16(a[3]) << 16));
+        *reinterpret_cast<uint2*>(yb) = pk;
+      } else {
+        yb[0] = (uint16_t)f32_to_bf16(a[0]);
       }
+    } else {
+      float* yf = static_cast<float*>(y) + o;
+      if constexpr (VEC == 4) *reinterpret_cast<float4*>(yf) = make_float4(a[0], a[1], a[2], a[3]);
+      else yf[0] = a[0];
     }
   }
 }
@@ -95,11 +112,24 @@ hipError_t launch_fill_u32(uint32_t* p, int n, uint32_t v, hipStream_t st) {
 
 hipError_t launch_translate_state(const float* z_src, float* z_dst, void* y, int n, int h_out, int w_out,
                                   int c_out, int dyo, int dxo, int act, int dtype, hipStream_t st) {
-  const long total = (long)n * h_out * w_out * (c_out % 4 == 0 ? c_out / 4 : c_out);
-  const int grid = (int)std::min<long>((total + kTrThreads - 1) / kTrThreads, 4096);
-  hipLaunchKernelGGL(translate_state_kernel, dim3(grid), dim3(kTrThreads), 0, st, z_src, z_dst, y, n, h_out, w_out,
-                     c_out, dyo, dxo, act, dtype);
-  return hipGetLastError();
+  const bool v4 = c_out % 4 == 0;
+  const long per_row = (long)w_out * (v4 ? c_out / 4 : c_out);
+  const long rows = (long)n * h_out;
+  if (per_row >= (1L << 30) || rows >= (1L << 31)) return hipErrorInvalidValue;
+  constexpr long kRowsPerLaunch = 65535;  // grid.y limit
+  for (long r0 = 0; r0 < rows; r0 += kRowsPerLaunch) {
+    const dim3 grid((unsigned)((per_row + kTrThreads - 1) / kTrThreads),
+                    (unsigned)std::min<long>(rows - r0, kRowsPerLaunch));
+    if (v4)
+      hipLaunchKernelGGL(translate_state_kernel<4>, grid, dim3(kTrThreads), 0, st, z_src, z_dst, y, (int)r0, h_out,
+                         w_out, c_out, dyo, dxo, act, dtype);
+    else
+      hipLaunchKernelGGL(translate_state_kernel<1>, grid, dim3(kTrThreads), 0, st, z_src, z_dst, y, (int)r0, h_out,
+                         w_out, c_out, dyo, dxo, act, dtype);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_split_list(const uint32_t* list, const uint32_t* counters, int seg_tiles, int seg_cap,
