@@ -67,12 +67,32 @@ translate_state_kernel(const float* z_src, float* z_dst, void* y, int row0, int 
 
 // One workgroup: list[0..count) -> list_a (translated recurrence) and list_b
 // (exposed blocks); counts at counters_a[kCtrCount], counters_b[kCtrCount].
+// A block is exposed when one of its output rows or columns is: the flags of
+// every block row and block column are formed first (each line tested once),
+// so a listed block costs two LDS reads.
+constexpr int kSplitMaxLines = 4096;
 __global__ void __launch_bounds__(1024)
 split_list_kernel(const uint32_t* list, const uint32_t* counters, int seg_tiles, int seg_cap, uint32_t* list_a,
                   uint32_t* counters_a, uint32_t* list_b, uint32_t* counters_b, int hb, int wb, int block,
                   int h_out, int w_out, int h, int w, int k, int stride, int pad, int sy, int sx) {
   __shared__ uint32_t na, nb_;
+  __shared__ uint8_t row_ex[kSplitMaxLines], col_ex[kSplitMaxLines];
   if (threadIdx.x == 0) na = nb_ = 0;
+  const bool tables = hb <= kSplitMaxLines && wb <= kSplitMaxLines;
+  if (tables) {
+    for (int bi = threadIdx.x; bi < hb; bi += blockDim.x) {
+      bool ex = false;
+      for (int r = bi * block; r < min((bi + 1) * block, h_out) && !ex; ++r)
+        ex = line_exposed(r, h_out, h, k, stride, pad, sy);
+      row_ex[bi] = ex ? 1 : 0;
+    }
+    for (int bj = threadIdx.x; bj < wb; bj += blockDim.x) {
+      bool ex = false;
+      for (int c = bj * block; c < min((bj + 1) * block, w_out) && !ex; ++c)
+        ex = line_exposed(c, w_out, w, k, stride, pad, sx);
+      col_ex[bj] = ex ? 1 : 0;
+    }
+  }
   __syncthreads();
   const WorkList W = work_list(counters, seg_tiles, seg_cap);
   const uint32_t count = W.total;
@@ -81,10 +101,14 @@ split_list_kernel(const uint32_t* list, const uint32_t* counters, int seg_tiles,
     const int rem = (int)(blk % (uint32_t)(hb * wb));
     const int bi = rem / wb, bj = rem - bi * wb;
     bool ex = false;
-    for (int r = bi * block; r < min((bi + 1) * block, h_out) && !ex; ++r)
-      ex = line_exposed(r, h_out, h, k, stride, pad, sy);
-    for (int c = bj * block; c < min((bj + 1) * block, w_out) && !ex; ++c)
-      ex = line_exposed(c, w_out, w, k, stride, pad, sx);
+    if (tables) {
+      ex = row_ex[bi] != 0 || col_ex[bj] != 0;
+    } else {
+      for (int r = bi * block; r < min((bi + 1) * block, h_out) && !ex; ++r)
+        ex = line_exposed(r, h_out, h, k, stride, pad, sy);
+      for (int c = bj * block; c < min((bj + 1) * block, w_out) && !ex; ++c)
+        ex = line_exposed(c, w_out, w, k, stride, pad, sx);
+    }
     if (ex)
       list_b[atomicAdd(&nb_, 1u)] = blk;
     else
