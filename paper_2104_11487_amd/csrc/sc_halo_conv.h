@@ -120,15 +120,32 @@ struct HaloConv {
   // z_{t-1} of a tile in the transposed MFMA output layout; zeros outside the
   // frame and on a reference frame (none: every piece out of range, so the
   // registers are always written)
+  // (translated steps: from zsrc at the site shifted back by (zdy, zdx))
   __device__ void load_z(Acc& dst, const HaloTile& T, bool none) const {
-    const auto zrs = zres(T);
+    const auto zrs = p.zsrc ? frame_rsrc(p.zsrc + (size_t)T.n * zimg, (uint32_t)(zimg * 4)) : zres(T);
 #pragma unroll
     for (int i = 0; i < WM; ++i)
 #pragma unroll
       for (int jn = 0; jn < WN; ++jn)
         dst[i][jn] = __builtin_bit_cast(
-            floatx4,
-            __builtin_amdgcn_raw_buffer_load_b128(zrs, p.reference || none ? kOutOfRange : zoff(T, i, jn), 0, 0));
+            floatx4, __builtin_amdgcn_raw_buffer_load_b128(
+                         zrs, p.reference || none ? kOutOfRange : (p.zsrc ? zoff_src(T, i, jn) : zoff(T, i, jn)),
+                         0, 0));
+  }
+
+  // byte offset in zsrc of z_{t-1} for this lane's piece under the step's
+  // translation, or out of range where the shifted site leaves the frame
+  __device__ uint32_t zoff_src(const HaloTile& T, int i, int jn) const {
+    int l16 = r16;
+    asm volatile("" : "+v"(l16));
+    const int m = (wm * WM + i) * 16 + l16;
+    const int ly = m >> lb, lx = m & (p.block - 1);
+    const int col = (wn0 + jn) * 16 + kq * 4;
+    const int sy = T.oy0 + ly - p.zdy, sx = T.ox0 + lx - p.zdx;
+    return (ly < T.rows_ok && lx < T.cols_ok && col < p.c_out && sy >= 0 && sy < p.h_out && sx >= 0 &&
+            sx < p.w_out)
+               ? (uint32_t)(((sy * p.w_out + sx) * p.c_out + col) * 4)
+               : kOutOfRange;
   }
 
   // one round of halo items: rho = bf16(x_t - x_{t-1}) into LDS

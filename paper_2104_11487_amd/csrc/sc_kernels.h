@@ -86,6 +86,11 @@ struct ConvParams {
   // r = fl32(y_new - y_old) and its bf16 rounding at every site it updates
   float* r32;
   uint16_t* rb;
+  // translated steps (block-halo convolution): z_{t-1} is read from zsrc at
+  // the output site shifted back by (zdy, zdx), zero outside the frame, and
+  // the sum written to z; NULL = read z itself
+  const float* zsrc;
+  int zdy, zdx;
 };
 
 // Work list of a convolution: a plain list with its count at
@@ -267,7 +272,8 @@ hipError_t launch_emit(const uint8_t* block_mask, uint8_t* prev_mask, int nb, co
 // Translation-compensated steps (Sec. 3.3): the translated state, and the
 // active list split into translated-recurrence blocks and exposed blocks.
 hipError_t launch_translate_state(const float* z_src, float* z_dst, void* y, int n, int h_out, int w_out,
-                                  int c_out, int dyo, int dxo, int act, int dtype, hipStream_t st);
+                                  int c_out, int dyo, int dxo, int act, int dtype, const uint8_t* skip_mask,
+                                  int block, int hb, int wb, hipStream_t st);
 hipError_t launch_split_list(const uint32_t* list, const uint32_t* counters, int seg_tiles, int seg_cap,
                              uint32_t* list_a, uint32_t* counters_a, uint32_t* list_b, uint32_t* counters_b,
                              int hb, int wb, int block, int h_out, int w_out, int h, int w, int k, int stride,

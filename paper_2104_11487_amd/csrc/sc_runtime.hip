@@ -1155,9 +1155,15 @@ int skipconv_step_translated(skipconv_t h, const void* x_t, int32_t dy, int32_t 
     if (z_t) *z_t = h->z();
     return SKIPCONV_OK;
   }
-  // 1. z <- T~(z) into the other slot (activation output refreshed)
-  hipError_t e = sc::launch_translate_state(h->z(), h->z_other(), h->y(), d.n, g.h_out, g.w_out, d.c_out,
-                                            dy / d.stride, dx / d.stride, d.act_out, d.dtype, st);
+  // 1. z <- T~(z) into the other slot (activation output refreshed). The
+  // block-halo convolution reads z_{t-1} from the old slot at the shifted site
+  // itself, so there the shift runs after the gate and skips active blocks.
+  const float* z_old = h->z();
+  const bool zshift = g.halo && !g.depthwise;
+  hipError_t e = hipSuccess;
+  if (!zshift)
+    e = sc::launch_translate_state(z_old, h->z_other(), h->y(), d.n, g.h_out, g.w_out, d.c_out, dy / d.stride,
+                                   dx / d.stride, d.act_out, d.dtype, nullptr, d.block, g.hb, g.wb, st);
   if (e != hipSuccess) return hip_fail(h, e, "translate launch");
   h->zslot ^= 1;
   // 2. gate on r = x_t - T(x_{t-1}); exposed sites on
@@ -1168,6 +1174,9 @@ int skipconv_step_translated(skipconv_t h, const void* x_t, int32_t dy, int32_t 
   e = begin_list(h, gp, st, &sl);
   if (e == hipSuccess) e = sc::launch_gate(gp, d.dtype, g.vec, g.gate_grid, g.gate_lds, st);
   if (e == hipSuccess) e = gate_done(h, st);
+  if (e == hipSuccess && zshift)
+    e = sc::launch_translate_state(z_old, h->z(), h->y(), d.n, g.h_out, g.w_out, d.c_out, dy / d.stride,
+                                   dx / d.stride, d.act_out, d.dtype, h->bmask(), d.block, g.hb, g.wb, st);
   // 3. active blocks: translated recurrence (list a) or recomputed from x_t (list b)
   uint32_t* ctr = h->ctr();
   uint32_t* list_a = reinterpret_cast<uint32_t*>(h->ws + g.off_list_a);
@@ -1196,6 +1205,9 @@ int skipconv_step_translated(skipconv_t h, const void* x_t, int32_t dy, int32_t 
     cp.no_prev = pass;
     cp.sy = pass ? 0 : dy;
     cp.sx = pass ? 0 : dx;
+    cp.zsrc = (zshift && !pass) ? z_old : nullptr;
+    cp.zdy = dy / d.stride;
+    cp.zdx = dx / d.stride;
     e = launch_split_conv(g, d, cp, conv_grid(h), st);
   }
   if (e != hipSuccess) return hip_fail(h, e, "translated conv launch");

@@ -5,7 +5,9 @@
 // (line_exposed); blocks holding an exposed site are recomputed from x_t.
 //
 //   translate_state_kernel  z_dst[o] = z_src[o - d_out] (0 outside), and the
-//                           activation output refreshed from it;
+//                           activation output refreshed from it (optionally
+//                           only outside the step's active blocks, which the
+//                           block-halo convolution writes itself);
 //   split_list_kernel       the step's ordered active list split into the
 //                           blocks that follow the translated recurrence and
 //                           the exposed blocks recomputed from x_t.
@@ -24,13 +26,15 @@ constexpr int kTrThreads = 256;
 template <int VEC>
 __global__ void __launch_bounds__(kTrThreads)
 translate_state_kernel(const float* z_src, float* z_dst, void* y, int row0, int h_out, int w_out, int c_out,
-                       int dyo, int dxo, int act, int dtype) {
+                       int dyo, int dxo, int act, int dtype, const uint8_t* skip_mask, int block, int hb, int wb) {
   const int cg = c_out / VEC;
   const int e = blockIdx.x * kTrThreads + threadIdx.x;
   if (e >= w_out * cg) return;
   const int row = row0 + (int)blockIdx.y;  // image * h_out + oy
   const int img = row / h_out, oy = row - img * h_out;
   const int ox = e / cg, ch = (e - ox * cg) * VEC;
+  // sites of active blocks are written by the step's convolution
+  if (skip_mask && skip_mask[((size_t)img * hb + oy / block) * wb + ox / block]) return;
   const int sy = oy - dyo, sx = ox - dxo;
   const bool in = sy >= 0 && sy < h_out && sx >= 0 && sx < w_out;
   const size_t o = ((size_t)row * w_out + ox) * c_out + ch;
@@ -135,7 +139,8 @@ hipError_t launch_fill_u32(uint32_t* p, int n, uint32_t v, hipStream_t st) {
 }
 
 hipError_t launch_translate_state(const float* z_src, float* z_dst, void* y, int n, int h_out, int w_out,
-                                  int c_out, int dyo, int dxo, int act, int dtype, hipStream_t st) {
+                                  int c_out, int dyo, int dxo, int act, int dtype, const uint8_t* skip_mask,
+                                  int block, int hb, int wb, hipStream_t st) {
   const bool v4 = c_out % 4 == 0;
   const long per_row = (long)w_out * (v4 ? c_out / 4 : c_out);
   const long rows = (long)n * h_out;
@@ -146,10 +151,10 @@ hipError_t launch_translate_state(const float* z_src, float* z_dst, void* y, int
                     (unsigned)std::min<long>(rows - r0, kRowsPerLaunch));
     if (v4)
       hipLaunchKernelGGL(translate_state_kernel<4>, grid, dim3(kTrThreads), 0, st, z_src, z_dst, y, (int)r0, h_out,
-                         w_out, c_out, dyo, dxo, act, dtype);
+                         w_out, c_out, dyo, dxo, act, dtype, skip_mask, block, hb, wb);
     else
       hipLaunchKernelGGL(translate_state_kernel<1>, grid, dim3(kTrThreads), 0, st, z_src, z_dst, y, (int)r0, h_out,
-                         w_out, c_out, dyo, dxo, act, dtype);
+                         w_out, c_out, dyo, dxo, act, dtype, skip_mask, block, hb, wb);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
