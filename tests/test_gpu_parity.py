@@ -1508,6 +1508,43 @@ def test_translated_eps0_integer_is_dense_conv(case):
                    expect_fused=False if split else True)
 
 
+@pytest.mark.parametrize("stride", [1, 2])
+def test_translated_halo_masked_shift(stride):
+    """Split pipeline, block-halo convolution, translated steps on frames with
+    interior blocks: active blocks read z_{t-1} from the old slot at the shifted
+    site, the state shift covers only the other blocks. eps = 0 on integer
+    frames: z equals conv2d(x_t) bit for bit, masks match the oracle."""
+    rng = np.random.Generator(np.random.PCG64(150 + stride))
+    s = stride
+    shifts = [(0, 0), (s, 0), (0, -2 * s), (-s, s), (0, 0), (2 * s, -s), (-3 * s, 2 * s)]
+    frames = _translated_integer_video(rng, 2, 64, 72, 32, shifts, stride)
+    w = syn.integer_weights(64, 32, 3, seed=151)
+    layer = S.SkipConv(to_device(weight_storage(w, "bf16"), "bf16"), n=2, h=64, w=72, stride=stride, block=8,
+                       split=True, translate=True)
+    assert layer.conv_kernel == 1, layer.conv_kernel  # block halo
+    layer.close()
+    tag = f"translated halo s={stride}"
+    layer, orc = _layer_pair(w, n=2, h=64, w=72, dtype="bf16", eps=0.0, block=8, stride=stride, split=True,
+                             translate=True, act_out="relu")
+    dens = []
+    for t, (f, d) in enumerate(zip(frames, shifts)):
+        xs = syn.to_storage(f, "bf16")
+        say(f"[{tag}] frame {t} shift={d}")
+        z = layer.step_translated(to_device(xs, "bf16"), *d)
+        ref = orc.step(xs, shift=d)
+        compare_frame(layer, ref, "bf16", t=t, tag=tag, keep_stats=True, exact_z=True)
+        # the activation output: refreshed by the shift outside the active
+        # blocks, written by the convolution inside them
+        torch.cuda.synchronize()
+        z_np = z.cpu().numpy()
+        y = layer.activation().view(torch.int16).cpu().numpy().view(np.uint16).reshape(z_np.shape)
+        exp = O.f32_to_bf16_rne(np.maximum(z_np, 0.0).astype(np.float32))
+        assert np.array_equal(y, exp), f"{tag} t={t}: activation differs"
+        dens.append(ref["count"] / ref["block_mask"].size)
+    layer.close()
+    assert 0.0 < np.mean(dens[1:]) < 1.0  # some blocks off: the masked shift has work
+
+
 def _panning_rect64(n_frames):
     wl = syn.workloads()["rect64"]
     base = list(wl.video(n_frames))
