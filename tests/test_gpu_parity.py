@@ -1268,6 +1268,29 @@ def test_learned_gate_geometries(case):
                phi=phi, gate_bias=bias, tag=f"learned {case}", resets=(3,))
 
 
+@pytest.mark.parametrize("case", [
+    # c_in, c_out, k, dtype, block, site density: the split pipeline's lane-group learned gate
+    (128, 64, 3, "bf16", 8, 0.02),  # 16 chunks a pixel: one tap per lane, phi in registers
+    (32, 32, 5, "bf16", 4, 0.1),    # 25 taps in groups of 9, phi read from LDS
+    (16, 16, 7, "f32", 1, 0.3),     # 2 chunks a pixel, 49 taps: five reader rounds per group
+], ids=["c128k3", "c32k5", "f32c16k7"])
+def test_learned_gate_lane_groups_split(case):
+    """Learned gate (Eq. 8) on the split pipeline's lane groups: each lane's
+    per-tap chunk terms go through the exchange and are summed in the
+    canonical chunk order by one lane per tap; masks, lists and statistics
+    bit-exact against the oracle, z within tolerance."""
+    c_in, c_out, k, dtype, block, site_density = case
+    rng = np.random.Generator(np.random.PCG64(160 + c_in + k))
+    wt = rng.normal(0, 0.1, (c_out, c_in, k, k)).astype(np.float32)
+    phi = rng.normal(0, 0.2, (c_in, k, k)).astype(np.float32)
+    frames = list(syn.RectVideo(40, 36, c_in, 6, seed=161 + c_in, batch=2, side_lo=3, side_hi=9))
+    bias = _learned_bias(frames, phi, dtype, k, 1, site_density)
+    worst, dens = run_single(frames, wt, dtype=dtype, eps=0.0, block=block, gate="learned", phi=phi,
+                             gate_bias=bias, tag=f"learned lanes split {case}", resets=(4,), split=True,
+                             expect_fused=False)
+    assert 0.0 < np.mean(dens[1:]) < 1.0
+
+
 def test_learned_gate_requires_weights_and_nan_turns_on():
     wl = syn.workloads()["square16"]
     w = wl.weights()[0]
