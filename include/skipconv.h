@@ -194,7 +194,11 @@ int skipconv_create(const skipconv_desc* d, const void* weights, void* workspace
  *   split: the gate kernel (residual, statistic, threshold, block pooling,
  *          x_{t-1} update, unordered work list of active blocks), then the
  *          sparse convolution kernel, which walks only the listed blocks
- *          (residual halo in LDS, MFMA product, z accumulate). */
+ *          (residual halo in LDS, MFMA product, z accumulate).
+ * fused is chosen for shapes it is built for whose frames have at most four
+ * tiles per compute unit (the variant with weights staged in LDS only for
+ * layers of <= 64 input and output channels on at most one tile per compute
+ * unit, three for 32 -> 32); SKIPCONV_FLAG_SPLIT_PIPELINE forces split. */
 int skipconv_step(skipconv_t h, const void* x_t, void* stream, const float** z_t);
 
 /* Process one frame whose content moved by (dy, dx) input pixels since the
