@@ -1517,7 +1517,8 @@ def _translated_integer_video(rng, n, h, w, c, shifts, stride):
     ("bf16", 8, 5, 1, 1, 16, 32, True),     # direct gather
     ("f32", 2, 3, 2, 1, 8, 8, True),        # stride 2, even shifts
     ("bf16", 1, 3, 1, 16, 16, 16, True),    # depthwise
-], ids=["f32b1", "bf16halo", "bf16fused", "bf16fuseds2", "bf16k5", "f32s2", "bf16dw"])
+    ("f32", 2, 3, 1, 1, 8, 6, True),        # C_out % 4 != 0: the state shift moves single channels
+], ids=["f32b1", "bf16halo", "bf16fused", "bf16fuseds2", "bf16k5", "f32s2", "bf16dw", "f32cout6"])
 def test_translated_eps0_integer_is_dense_conv(case):
     """eps = 0 over translated integer frames: z equals conv2d(x_t) bit for bit, masks match the oracle."""
     dtype, block, k, stride, groups, c_in, c_out, split = case
